@@ -1,0 +1,275 @@
+"""Checkpoint planners and the memory accounting of a static plan.
+
+TEST INFRASTRUCTURE ONLY (see the package header).
+
+Notation.  The chain has n units; unit i maps x_i to x_{i+1}.  For each unit
+the caller gives ``layer_bytes[i]`` -- the bytes the unit holds while its
+segment is re-run (its saved internals plus its output; Alg. 3's
+"size-of-output" at unit granularity) -- and ``cut_bytes[i]`` -- the bytes of
+x_{i+1}, kept when the chain is cut after unit i, or 0 when x_{i+1} is not a
+candidate split point (Alg. 3's set C).  The last unit is never a candidate:
+its output feeds the loss directly (Alg. 1).
+
+A cut c means: store x_{c+1} (Alg. 3 sets m(v) = 0 on that node) and start a
+new segment at unit c+1.  Segments are half-open [begin, end) as in Alg. 1.
+
+Modes:
+* NONE      -- one segment, forward activations kept (no recomputation).
+* SQRT      -- section 4.3, Eq. 1: k = ceil(sqrt(n)) equal segments (stride s,
+               cuts at s-1, 2s-1, ... below n-1); an explicit stride may be
+               given in ``budget``.  A target that is not a candidate moves to
+               the next candidate.
+* GREEDY    -- Alg. 3: walk the units in order accumulating temp; at a
+               candidate where temp > B, cut, add the cut's bytes to x, raise y
+               to temp and reset temp to 0.  x and y are returned exactly as
+               Alg. 3 computes them (y only sees segments that end at a cut).
+* RECURSIVE -- section 4.4 with k = 1 (Eq. 2-3): a segment of length L > 1 is
+               split at a + floor(L/2); its first half's boundary is stored,
+               and each half is handled the same way; a single unit is
+               re-forwarded once.
+* USER      -- an explicit cut list (the user-set mirror attribute of
+               section 4.5).
+
+Flag KEEP_LAST: the last segment keeps the activations of the first forward
+instead of recomputing them (the literal Alg. 1 re-runs every segment, so
+without the flag a one-level plan costs exactly n extra unit forwards).  NONE
+always keeps them.
+
+Accounting (exact bytes of the executor's static layout; the paper reports the
+exact feature-map cost of a static plan, excluding parameters and temporary
+operator workspace, section 5.1):
+* CKPT  -- stored boundaries.  One-level: sum of b_{c+1} over cuts.
+           Recursive: the largest total of simultaneously stored split points.
+* ARENA -- the largest of (a) every forward-sweep unit's transient need
+           (input if it lives in the arena) + internals + (output if it is not
+           stored), and (b) every re-run segment's sum of internals + outputs.
+* GRAD  -- two gradient slots of max_{1<=i<=n} b_i and one scratch of max q_i.
+* PEAK  -- CKPT + ARENA + GRAD.
+
+Parity: pinned by brute force over all cut sets for n <= 16, Alg. 3
+invariants, and the closed forms of Eq. 1 and Eq. 3 (tests/test_oracle_planner.py).
+"""
+from __future__ import annotations
+
+import math
+import struct
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4
+FLAG_KEEP_LAST = 1
+MAGIC = b"CKPL"
+VERSION = 1
+
+
+class PlanError(ValueError):
+    pass
+
+
+class Unsupported(PlanError):
+    pass
+
+
+@dataclass
+class Plan:
+    mode: int
+    n: int
+    cuts: List[int] = field(default_factory=list)
+    x: int = 0
+    y: int = 0
+    extra_forwards: int = 0
+    keep_last: bool = False
+
+    def segments(self):
+        """Half-open [begin, end) segments of a one-level plan."""
+        out, b = [], 0
+        for c in self.cuts:
+            out.append((b, c + 1))
+            b = c + 1
+        out.append((b, self.n))
+        return out
+
+    def serialize(self) -> bytes:
+        body = struct.pack("<4sIIIII", MAGIC, VERSION, self.mode, 1 if self.keep_last else 0,
+                           self.n, len(self.cuts))
+        body += struct.pack(f"<{len(self.cuts)}i", *self.cuts)
+        body += struct.pack("<QQQ", self.x, self.y, self.extra_forwards)
+        return body
+
+
+def ceil_isqrt(n: int) -> int:
+    r = math.isqrt(n)
+    return r if r * r == n else r + 1
+
+
+def xy_of_cuts(layer_bytes: Sequence[int], cut_bytes: Sequence[int], cuts: Sequence[int]):
+    """Alg. 3's outputs for a given cut set: x = kept bytes, y = the largest
+    segment total among segments that end at a cut."""
+    x = sum(cut_bytes[c] for c in cuts)
+    y, b = 0, 0
+    for c in cuts:
+        y = max(y, sum(layer_bytes[b:c + 1]))
+        b = c + 1
+    return x, y
+
+
+def greedy_alg3(layer_bytes, cut_bytes, B):
+    """Alg. 3, step by step."""
+    temp = x = y = 0
+    cuts = []
+    for i in range(len(layer_bytes)):
+        temp += layer_bytes[i]
+        if cut_bytes[i] > 0 and temp > B:
+            x += cut_bytes[i]
+            y = max(y, temp)
+            cuts.append(i)
+            temp = 0
+    return cuts, x, y
+
+
+def sqrt_cuts(n, cut_bytes, stride):
+    cuts = []
+    j = 1
+    while True:
+        t = j * stride - 1
+        if t >= n - 1:
+            break
+        c = t
+        while c < n - 1 and cut_bytes[c] == 0:
+            c += 1
+        if c < n - 1 and (not cuts or c > cuts[-1]):
+            cuts.append(c)
+        j += 1
+    return cuts
+
+
+def recursive_extra(n: int) -> int:
+    """Unit forwards done after the first full forward, by the recursion below."""
+    def R(a, b):
+        if b - a == 1:
+            return 1
+        m = a + (b - a) // 2
+        return (m - a) + R(m, b) + R(a, m)
+    if n == 1:
+        return R(0, 1)
+    m = n // 2
+    return R(m, n) + R(0, m)
+
+
+def plan(n: int, layer_bytes: Sequence[int], cut_bytes: Sequence[int], budget: int, mode: int,
+         user_cuts: Optional[Sequence[int]] = None, flags: int = 0) -> Plan:
+    if n <= 0 or len(layer_bytes) != n or len(cut_bytes) != n:
+        raise PlanError("n must be positive and both size arrays must have n entries")
+    if any(v < 0 for v in layer_bytes) or any(v < 0 for v in cut_bytes):
+        raise PlanError("sizes are unsigned")
+    if cut_bytes[n - 1] != 0:
+        raise PlanError("the last unit cannot be a cut")
+    keep_last = bool(flags & FLAG_KEEP_LAST)
+    if mode == NONE:
+        return Plan(NONE, n, [], 0, 0, 0, True)
+    if mode == SQRT:
+        stride = budget if budget > 0 else ceil_isqrt(n)
+        cuts = sqrt_cuts(n, cut_bytes, stride)
+    elif mode == GREEDY:
+        cuts, x, y = greedy_alg3(layer_bytes, cut_bytes, budget)
+    elif mode == USER:
+        cuts = list(user_cuts or [])
+        for k, c in enumerate(cuts):
+            if c < 0 or c >= n - 1 or cut_bytes[c] == 0 or (k and c <= cuts[k - 1]):
+                raise PlanError("user cuts must be ascending candidates below n-1")
+    elif mode == RECURSIVE:
+        if any(cut_bytes[i] == 0 for i in range(n - 1)):
+            raise Unsupported("the recursive schedule needs every boundary to be a candidate")
+        return Plan(RECURSIVE, n, [], 0, 0, recursive_extra(n), False)
+    else:
+        raise PlanError(f"unknown mode {mode}")
+    x, y = xy_of_cuts(layer_bytes, cut_bytes, cuts)
+    p = Plan(mode, n, cuts, x, y, 0, keep_last)
+    if keep_last:
+        p.extra_forwards = cuts[-1] + 1 if cuts else 0
+    else:
+        p.extra_forwards = n
+    return p
+
+
+# --------------------------------------------------------------------------
+# accounting
+# --------------------------------------------------------------------------
+
+@dataclass
+class Accounting:
+    ckpt: int
+    arena: int
+    grad: int
+
+    @property
+    def peak(self) -> int:
+        return self.ckpt + self.arena + self.grad
+
+
+def _sweep_needs(b, a, lo, hi, stored):
+    """Transient arena need of each unit of a forward sweep over [lo, hi) whose
+    first input is external; ``stored`` is the set of units whose output is kept
+    outside the arena."""
+    needs = []
+    for i in range(lo, hi):
+        in_arena = i > lo and (i - 1) not in stored
+        out_arena = i not in stored
+        needs.append((b[i] if in_arena else 0) + a[i] + (b[i + 1] if out_arena else 0))
+    return needs
+
+
+def grad_bytes(b, q):
+    n = len(q)
+    return 2 * max(b[1:n + 1]) + max(q)
+
+
+def account(p: Plan, b: Sequence[int], a: Sequence[int], q: Sequence[int]) -> Accounting:
+    """b has n+1 entries (x_0..x_n), a and q have n entries."""
+    n = p.n
+    assert len(b) == n + 1 and len(a) == n and len(q) == n
+    G = grad_bytes(b, q)
+    if p.mode == RECURSIVE:
+        arena = 0
+        stack: List[int] = []
+        ckpt_max = 0
+
+        def R(lo, hi):
+            nonlocal arena, ckpt_max
+            if hi - lo == 1:
+                arena = max(arena, a[lo] + b[lo + 1])
+                return
+            m = lo + (hi - lo) // 2
+            arena = max(arena, *_sweep_needs(b, a, lo, m, {m - 1}))
+            stack.append(b[m])
+            ckpt_max = max(ckpt_max, sum(stack))
+            R(m, hi)
+            stack.pop()
+            R(lo, m)
+
+        if n == 1:
+            arena = max(arena, *_sweep_needs(b, a, 0, 1, set()))
+            R(0, 1)
+        else:
+            m = n // 2
+            arena = max(arena, *_sweep_needs(b, a, 0, n, {m - 1}))
+            stack.append(b[m])
+            ckpt_max = max(ckpt_max, sum(stack))
+            R(m, n)
+            stack.pop()
+            R(0, m)
+        return Accounting(ckpt_max, arena, G)
+    cuts = set(p.cuts)
+    segs = p.segments()
+    fwd_hi = segs[-1][0] if p.keep_last else n
+    arena = 0
+    if fwd_hi > 0:
+        arena = max(_sweep_needs(b, a, 0, fwd_hi, cuts))
+    for (lo, hi) in segs:
+        arena = max(arena, sum(a[i] + b[i + 1] for i in range(lo, hi)))
+    ckpt = sum(b[c + 1] for c in p.cuts)
+    return Accounting(ckpt, arena, G)
+
+
+def unit_forwards(p: Plan) -> int:
+    return p.n + p.extra_forwards

@@ -1,0 +1,232 @@
+/*
+ * ckpt.h -- C ABI of libckpt: the checkpointed (sublinear-memory) training
+ * step of Chen, Xu, Zhang and Guestrin, "Training Deep Nets with Sublinear
+ * Memory Cost", on AMD Instinct MI355X (gfx950).
+ *
+ * The paper's problem (section 4.1): train an n-unit chain while keeping only
+ * some intermediate results and recomputing the others during back-propagation.
+ * Two calls carry it:
+ *   plan_checkpoints(n, per-unit sizes, budget)  -> which boundaries to keep
+ *   train_step(net, batch, plan)                 -> loss, every gradient, peak
+ *                                                   activation bytes
+ *
+ * Conventions
+ *   - Every function returning int returns CKPT_OK (0) or a negative CKPT_E_*
+ *     code; ckpt_last_error() then describes the failure (thread-local string,
+ *     valid until the next call on the same thread).
+ *   - Arguments are validated before anything is launched on the GPU: a call
+ *     that returns an error other than CKPT_E_HIP has enqueued no work.
+ *   - "device" pointers are GPU memory (hipMalloc or torch tensors) that the
+ *     caller owns; "host" pointers are ordinary CPU memory.  The library never
+ *     allocates or frees device memory: the caller passes one workspace.
+ *   - Unit i of the chain maps x_i to x_{i+1}; a cut at c keeps x_{c+1}.
+ *   - Plans and nets are library-owned opaque objects, freed with plan_free /
+ *     net_destroy.  They are immutable after creation and may be shared
+ *     between threads; calls that use the same workspace must not overlap.
+ */
+#ifndef CKPT_H
+#define CKPT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ------------------------------------------------------ */
+#define CKPT_OK              0
+#define CKPT_E_INVALID     (-1)  /* bad argument (null pointer, size, cut list) */
+#define CKPT_E_WORKSPACE   (-2)  /* workspace smaller than net_workspace_bytes  */
+#define CKPT_E_MISMATCH    (-3)  /* plan built for a different unit count        */
+#define CKPT_E_HIP         (-4)  /* a HIP runtime call failed (message has text) */
+#define CKPT_E_UNSUPPORTED (-5)  /* valid request this build does not handle     */
+
+/* ---- plan modes (section 4) --------------------------------------------- */
+#define CKPT_NONE      0  /* one segment, activations of the first forward kept     */
+#define CKPT_SQRT      1  /* section 4.3, Eq. 1: ceil(sqrt n) equal segments         */
+#define CKPT_GREEDY    2  /* Alg. 3: budget-driven greedy segmentation               */
+#define CKPT_RECURSIVE 3  /* section 4.4, Eq. 2-3 with k = 1: O(log n) boundaries    */
+#define CKPT_USER      4  /* explicit cut list: the user-set mirror attribute (4.5)  */
+
+/* plan flags */
+#define CKPT_FLAG_KEEP_LAST 1 /* one-level plans: reuse the last segment's first-
+                                 forward activations instead of re-running it   */
+
+typedef struct ckpt_plan ckpt_plan;
+typedef struct ckpt_net ckpt_net;
+
+/*
+ * plan_checkpoints -- choose the boundaries to keep (section 4.3, Alg. 3,
+ * section 4.4).
+ *   n_layers     number of units n (> 0).
+ *   layer_bytes  host [n]: bytes unit i holds while its segment is re-run
+ *                (saved internals + output; Alg. 3's size-of-output).
+ *   cut_bytes    host [n]: bytes of x_{i+1} when kept; 0 marks a boundary that
+ *                is not a candidate split point (Alg. 3's set C).  The last
+ *                entry must be 0: the chain's output feeds the loss (Alg. 1).
+ *   budget       GREEDY: Alg. 3's per-segment budget B (bytes).  SQRT: the
+ *                stride (units per segment) if > 0, else ceil(sqrt n).
+ *                Ignored by the other modes.
+ *   mode         CKPT_NONE .. CKPT_USER.
+ *   user_cuts    host [n_user_cuts], CKPT_USER only: strictly ascending
+ *                candidate positions below n-1.
+ *   flags        0 or CKPT_FLAG_KEEP_LAST.
+ *   out          receives the new plan (free with plan_free).
+ * Errors: CKPT_E_INVALID for n <= 0, null pointers, cut_bytes[n-1] != 0, an
+ *   unknown mode, or a user cut list that is unsorted, repeated, out of range
+ *   or on a non-candidate; CKPT_E_UNSUPPORTED for RECURSIVE on a chain with a
+ *   non-candidate boundary.
+ */
+int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
+                     uint64_t budget, int32_t mode, const int32_t *user_cuts,
+                     int32_t n_user_cuts, int32_t flags, ckpt_plan **out);
+
+/*
+ * plan_info -- summary of a plan.  Any output pointer may be null.
+ *   mode, n_layers, n_cuts   as planned (RECURSIVE reports 0 cuts: its split
+ *                            tree is implicit, midpoint splits of every range)
+ *   x, y                     Alg. 3's outputs for the plan's cut set: kept
+ *                            boundary bytes, and the largest segment total
+ *                            among segments ending at a cut (0 for RECURSIVE)
+ *   extra_unit_forwards      unit forwards beyond the first pass: n for a
+ *                            literal one-level plan (one extra forward pass,
+ *                            section 4.3), fewer with KEEP_LAST, 0 for NONE,
+ *                            the recursion's count for RECURSIVE.
+ */
+int plan_info(const ckpt_plan *plan, int32_t *mode, int32_t *n_layers, int32_t *n_cuts,
+              uint64_t *x, uint64_t *y, uint64_t *extra_unit_forwards);
+
+/* plan_cuts -- copy the ascending cut list into host cuts[cap]; *n_cuts gets
+ * the full count (the copy is truncated to cap). */
+int plan_cuts(const ckpt_plan *plan, int32_t *cuts, int32_t cap, int32_t *n_cuts);
+
+/*
+ * plan_serialize -- canonical little-endian bytes of the plan:
+ *   "CKPL" u32 version=1, u32 mode, u32 keep_last, u32 n, u32 n_cuts,
+ *   i32 cuts[n_cuts], u64 x, u64 y, u64 extra_unit_forwards.
+ * buf (host, cap bytes) may be null to query *len.  CKPT_E_INVALID if cap is
+ * too small for a non-null buf.
+ */
+int plan_serialize(const ckpt_plan *plan, uint8_t *buf, uint64_t cap, uint64_t *len);
+
+void plan_free(ckpt_plan *plan);
+
+/* ---- networks --------------------------------------------------------- */
+#define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
+#define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */
+
+typedef struct ckpt_net_desc {
+  int32_t kind;          /* CKPT_NET_*                                             */
+  int32_t batch;         /* samples per step                                       */
+  int32_t depth;         /* MLP: blocks.  RESNET_BASIC: basic blocks per stage    */
+  int32_t width;         /* MLP: width.   RESNET_BASIC: first-stage channels      */
+  int32_t image;         /* RESNET_BASIC: input side (square images, 3 channels)  */
+  int32_t n_classes;     /* RESNET_BASIC: classifier outputs                       */
+  int32_t reserved[10];  /* must be zero                                           */
+} ckpt_net_desc;
+
+/*
+ * net_create -- build the unit chain described by desc (host only).
+ *   MLP:          n = depth units; parameters per unit W [width, width]
+ *                 (x W, row-major [in, out]) then b [width]; input x0 f32
+ *                 [batch, width]; target f32 [batch, width]; loss = mean
+ *                 squared error over all elements.
+ *   RESNET_BASIC: n = 1 + 3*depth units: stem conv3x3 3->width + BN + ReLU,
+ *                 then basic blocks (conv3x3-BN-ReLU-conv3x3-BN, identity or
+ *                 option-A shortcut, ReLU) of width, 2 width, 4 width channels
+ *                 with stride-2 transitions; head = global average pool, FC
+ *                 [4 width, n_classes] + bias, softmax cross-entropy averaged
+ *                 over the batch.  Conv weights [Cout,3,3,Cin]; input f32 NHWC
+ *                 [batch, image, image, 3]; target int32 [batch].
+ * Errors: CKPT_E_INVALID for a null pointer, an unknown kind or a
+ *   non-positive or inconsistent size.
+ */
+int net_create(const ckpt_net_desc *desc, ckpt_net **out);
+void net_destroy(ckpt_net *net);
+
+/* net_units -- number of units n in the chain. */
+int net_units(const ckpt_net *net, int32_t *n);
+
+/*
+ * net_unit_sizes -- the static layout's byte tables (host arrays, any may be
+ * null): b[n+1] boundary x_i bytes, a[n] saved internals, q[n] gradient
+ * scratch.  Every tensor is rounded up to 256 bytes.
+ */
+int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q);
+
+/* net_layer_sizes -- plan_checkpoints inputs: layer_bytes[i] = a_i + b_{i+1},
+ * cut_bytes[i] = b_{i+1} (0 for the last unit).  Host arrays of n entries. */
+int net_layer_sizes(const ckpt_net *net, uint64_t *layer_bytes, uint64_t *cut_bytes);
+
+/*
+ * Parameters and gradients live in two caller-owned device buffers of
+ * net_param_bytes bytes each, f32, tensor k at byte offset *offset with
+ * *numel elements (256-byte aligned, in chain order, head last).  The name is
+ * "u<i>.<tensor>" or "head.<tensor>" (copied into host name[cap], NUL-ended).
+ */
+int net_param_bytes(const ckpt_net *net, uint64_t *bytes);
+int net_param_count(const ckpt_net *net, int32_t *count);
+int net_param_info(const ckpt_net *net, int32_t k, char *name, int32_t cap, uint64_t *offset,
+                   uint64_t *numel);
+
+/*
+ * plan_accounting -- exact feature-map bytes of the plan on this net (the
+ * cost a static allocation gives, section 5.1; parameters and operator
+ * workspace excluded): kept boundaries (ckpt), the re-run arena (arena) and
+ * the gradient buffers (grad); peak = ckpt + arena + grad.  Any output may be
+ * null.  CKPT_E_MISMATCH if the plan's n differs from the net's.
+ */
+int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt, uint64_t *arena,
+                    uint64_t *grad, uint64_t *peak);
+
+/* net_workspace_bytes -- size of the single device workspace train_step needs
+ * for this plan: peak plus operator workspace (loss partials, reduction
+ * partials, head buffers), each region 256-byte aligned. */
+int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *bytes);
+
+typedef struct ckpt_batch {
+  const void *input;   /* device: MLP f32 [batch,width]; RESNET_BASIC f32 NHWC images */
+  const void *target;  /* device: MLP f32 [batch,width]; RESNET_BASIC int32 [batch]   */
+} ckpt_batch;
+
+typedef struct ckpt_step_stats {
+  uint64_t unit_forwards;   /* unit forward passes run (n + extra)                */
+  uint64_t unit_backwards;  /* unit backward passes run (n)                       */
+  uint64_t kernel_launches; /* kernels enqueued by this step                      */
+  uint64_t ckpt_bytes, arena_bytes, grad_bytes; /* plan_accounting of this step   */
+} ckpt_step_stats;
+
+/*
+ * train_step -- one checkpointed training step (Alg. 1 for one-level plans,
+ * the section 4.4 recursion for RECURSIVE): forward keeping only the plan's
+ * boundaries, the loss head, then for each segment in reverse order its
+ * forward re-run from the kept boundary followed by its backward.
+ *   params     device f32, net_param_bytes (read only)
+ *   grads      device f32, net_param_bytes: every gradient is overwritten
+ *   batch      device input/target pointers (read only)
+ *   workspace  device, >= net_workspace_bytes(net, plan) bytes, 256-aligned;
+ *              contents on entry are ignored
+ *   stream     hipStream_t to enqueue on (null = the default stream)
+ *   loss_dev   nullable device f32 scalar receiving the loss (asynchronous)
+ *   loss_host  nullable host float: if given, the stream is synchronised and
+ *              the loss copied here
+ *   peak       nullable host: the plan's peak activation bytes
+ *   stats      nullable host: counters of this step
+ * The gradients are bit-identical for every plan of the same net: every
+ * kernel reduces in a fixed order and recomputation reproduces the first
+ * forward exactly (section 5.1: the same weight gradient).
+ * Errors: CKPT_E_INVALID (null net/params/grads/batch/plan/workspace, or an
+ *   unaligned workspace), CKPT_E_MISMATCH, CKPT_E_WORKSPACE, CKPT_E_HIP.
+ */
+int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+               const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
+               float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
+
+/* ckpt_last_error -- message of the last failed call on this thread ("" if
+ * none). */
+const char *ckpt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CKPT_H */

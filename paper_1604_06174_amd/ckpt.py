@@ -1,0 +1,245 @@
+"""Thin ctypes binding of libckpt (include/ckpt.h).
+
+Argument marshalling only: every step of the training path runs in the
+library's HIP kernels.  Device buffers are passed as torch tensors (their
+``data_ptr()``) or raw integer addresses; the library never allocates device
+memory.  Importing this module fails loudly when libckpt.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libckpt.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1604_06174_amd.build`")
+
+_lib = C.CDLL(LIB_PATH)
+
+OK, E_INVALID, E_WORKSPACE, E_MISMATCH, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4
+FLAG_KEEP_LAST = 1
+NET_MLP, NET_RESNET_BASIC = 1, 2
+
+_u64p = C.POINTER(C.c_uint64)
+_i32p = C.POINTER(C.c_int32)
+
+
+class NetDesc(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("batch", C.c_int32), ("depth", C.c_int32),
+                ("width", C.c_int32), ("image", C.c_int32), ("n_classes", C.c_int32),
+                ("reserved", C.c_int32 * 10)]
+
+
+class Batch(C.Structure):
+    _fields_ = [("input", C.c_void_p), ("target", C.c_void_p)]
+
+
+class StepStats(C.Structure):
+    _fields_ = [("unit_forwards", C.c_uint64), ("unit_backwards", C.c_uint64),
+                ("kernel_launches", C.c_uint64), ("ckpt_bytes", C.c_uint64),
+                ("arena_bytes", C.c_uint64), ("grad_bytes", C.c_uint64)]
+
+    def as_dict(self):
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_sig("ckpt_last_error", C.c_char_p, [])
+_sig("plan_checkpoints", C.c_int, [C.c_int32, _u64p, _u64p, C.c_uint64, C.c_int32, _i32p,
+                                   C.c_int32, C.c_int32, C.POINTER(C.c_void_p)])
+_sig("plan_info", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, _u64p, _u64p, _u64p])
+_sig("plan_cuts", C.c_int, [C.c_void_p, _i32p, C.c_int32, _i32p])
+_sig("plan_serialize", C.c_int, [C.c_void_p, C.POINTER(C.c_uint8), C.c_uint64, _u64p])
+_sig("plan_free", None, [C.c_void_p])
+_sig("net_create", C.c_int, [C.POINTER(NetDesc), C.POINTER(C.c_void_p)])
+_sig("net_destroy", None, [C.c_void_p])
+_sig("net_units", C.c_int, [C.c_void_p, _i32p])
+_sig("net_unit_sizes", C.c_int, [C.c_void_p, _u64p, _u64p, _u64p])
+_sig("net_layer_sizes", C.c_int, [C.c_void_p, _u64p, _u64p])
+_sig("net_param_bytes", C.c_int, [C.c_void_p, _u64p])
+_sig("net_param_count", C.c_int, [C.c_void_p, _i32p])
+_sig("net_param_info", C.c_int, [C.c_void_p, C.c_int32, C.c_char_p, C.c_int32, _u64p, _u64p])
+_sig("plan_accounting", C.c_int, [C.c_void_p, C.c_void_p, _u64p, _u64p, _u64p, _u64p])
+_sig("net_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
+_sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
+                             C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
+                             C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
+
+EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
+            "plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
+            "net_layer_sizes", "net_param_bytes", "net_param_count", "net_param_info",
+            "plan_accounting", "net_workspace_bytes", "train_step"]
+
+
+class CkptError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise CkptError(rc, _lib.ckpt_last_error().decode())
+
+
+def _u64arr(vals: Sequence[int]):
+    return (C.c_uint64 * max(1, len(vals)))(*[int(v) for v in vals])
+
+
+def _addr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+# ---------------------------------------------------------------- plans --
+class Plan:
+    """Owner of a library plan object."""
+
+    def __init__(self, handle: int):
+        self._h = C.c_void_p(handle)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self) -> Dict[str, int]:
+        mode, n, nc = C.c_int32(), C.c_int32(), C.c_int32()
+        x, y, ex = C.c_uint64(), C.c_uint64(), C.c_uint64()
+        _check(_lib.plan_info(self._h, C.byref(mode), C.byref(n), C.byref(nc), C.byref(x),
+                              C.byref(y), C.byref(ex)))
+        return dict(mode=mode.value, n=n.value, n_cuts=nc.value, x=x.value, y=y.value,
+                    extra_unit_forwards=ex.value)
+
+    def cuts(self) -> List[int]:
+        nc = C.c_int32()
+        _check(_lib.plan_cuts(self._h, None, 0, C.byref(nc)))
+        buf = (C.c_int32 * max(1, nc.value))()
+        _check(_lib.plan_cuts(self._h, buf, nc.value, C.byref(nc)))
+        return list(buf[:nc.value])
+
+    def serialize(self) -> bytes:
+        ln = C.c_uint64()
+        _check(_lib.plan_serialize(self._h, None, 0, C.byref(ln)))
+        buf = (C.c_uint8 * ln.value)()
+        _check(_lib.plan_serialize(self._h, buf, ln.value, C.byref(ln)))
+        return bytes(buf)
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _lib.plan_free(self._h)
+            self._h = None
+
+
+def plan_checkpoints(layer_bytes: Sequence[int], cut_bytes: Sequence[int], budget: int, mode: int,
+                     user_cuts: Optional[Sequence[int]] = None, flags: int = 0,
+                     n_layers: Optional[int] = None) -> Plan:
+    n = len(layer_bytes) if n_layers is None else n_layers
+    uc = list(user_cuts or [])
+    ucarr = (C.c_int32 * max(1, len(uc)))(*uc)
+    h = C.c_void_p()
+    _check(_lib.plan_checkpoints(n, _u64arr(layer_bytes), _u64arr(cut_bytes), int(budget), mode,
+                                 ucarr if user_cuts is not None else None, len(uc), flags,
+                                 C.byref(h)))
+    return Plan(h.value)
+
+
+# ----------------------------------------------------------------- nets --
+class Net:
+    """Owner of a library net object (host descriptor)."""
+
+    def __init__(self, kind: int, batch: int, depth: int, width: int, image: int = 0,
+                 n_classes: int = 0):
+        d = NetDesc(kind, batch, depth, width, image, n_classes)
+        h = C.c_void_p()
+        _check(_lib.net_create(C.byref(d), C.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def n(self) -> int:
+        v = C.c_int32()
+        _check(_lib.net_units(self._h, C.byref(v)))
+        return v.value
+
+    def unit_sizes(self) -> Tuple[List[int], List[int], List[int]]:
+        n = self.n
+        b, a, q = (C.c_uint64 * (n + 1))(), (C.c_uint64 * n)(), (C.c_uint64 * n)()
+        _check(_lib.net_unit_sizes(self._h, b, a, q))
+        return list(b), list(a), list(q)
+
+    def layer_sizes(self) -> Tuple[List[int], List[int]]:
+        n = self.n
+        lb, cb = (C.c_uint64 * n)(), (C.c_uint64 * n)()
+        _check(_lib.net_layer_sizes(self._h, lb, cb))
+        return list(lb), list(cb)
+
+    def param_bytes(self) -> int:
+        v = C.c_uint64()
+        _check(_lib.net_param_bytes(self._h, C.byref(v)))
+        return v.value
+
+    def param_layout(self) -> List[Tuple[str, int, int]]:
+        cnt = C.c_int32()
+        _check(_lib.net_param_count(self._h, C.byref(cnt)))
+        out = []
+        name = C.create_string_buffer(128)
+        off, numel = C.c_uint64(), C.c_uint64()
+        for k in range(cnt.value):
+            _check(_lib.net_param_info(self._h, k, name, 128, C.byref(off), C.byref(numel)))
+            out.append((name.value.decode(), off.value, numel.value))
+        return out
+
+    def accounting(self, plan: Plan) -> Dict[str, int]:
+        ck, ar, gr, pk = C.c_uint64(), C.c_uint64(), C.c_uint64(), C.c_uint64()
+        _check(_lib.plan_accounting(self._h, plan.handle, C.byref(ck), C.byref(ar), C.byref(gr),
+                                    C.byref(pk)))
+        return dict(ckpt=ck.value, arena=ar.value, grad=gr.value, peak=pk.value)
+
+    def workspace_bytes(self, plan: Plan) -> int:
+        v = C.c_uint64()
+        _check(_lib.net_workspace_bytes(self._h, plan.handle, C.byref(v)))
+        return v.value
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _lib.net_destroy(self._h)
+            self._h = None
+
+
+def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,
+               n_classes: int = 0) -> Net:
+    return Net(kind, batch, depth, width, image, n_classes)
+
+
+def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,
+               workspace_bytes: int, stream=None, loss_dev=None, want_loss: bool = True):
+    """Run one step; returns (loss or None, peak bytes, stats dict)."""
+    b = Batch(_addr(batch_input), _addr(batch_target))
+    loss = C.c_float()
+    peak = C.c_uint64()
+    st = StepStats()
+    s = None
+    if stream is not None:
+        s = stream if isinstance(stream, int) else int(stream.cuda_stream)
+    ld = _addr(loss_dev)
+    _check(_lib.train_step(net.handle, _addr(params), _addr(grads), C.byref(b), plan.handle,
+                           _addr(workspace), int(workspace_bytes), s,
+                           C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
+                           C.byref(loss) if want_loss else None, C.byref(peak), C.byref(st)))
+    return (loss.value if want_loss else None), peak.value, st.as_dict()

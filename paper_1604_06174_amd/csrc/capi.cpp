@@ -1,0 +1,236 @@
+// extern "C" boundary of libckpt: argument validation, error codes and the
+// thread-local error message.  Nothing here launches work before every
+// argument has been checked.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <memory>
+
+#include "net.h"
+
+struct ckpt_plan {
+  ckpt::Plan p;
+};
+struct ckpt_net {
+  std::unique_ptr<ckpt::Net> net;
+};
+
+namespace ckpt {
+uint64_t workspace_bytes(const Net &net, const Accounting &acc);
+void run_train_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
+                    const Plan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
+                    float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
+}  // namespace ckpt
+
+namespace {
+thread_local std::string g_err;
+
+template <class F>
+int guarded(F &&f) {
+  try {
+    f();
+    g_err.clear();
+    return CKPT_OK;
+  } catch (const ckpt::Error &e) {
+    g_err = e.msg;
+    return e.code;
+  } catch (const std::bad_alloc &) {
+    g_err = "host allocation failed";
+    return CKPT_E_INVALID;
+  } catch (const std::exception &e) {
+    g_err = e.what();
+    return CKPT_E_INVALID;
+  }
+}
+
+void need(const void *p, const char *what) {
+  if (!p) ckpt::fail(CKPT_E_INVALID, std::string(what) + ": null pointer");
+}
+}  // namespace
+
+extern "C" {
+
+const char *ckpt_last_error(void) { return g_err.c_str(); }
+
+int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
+                     uint64_t budget, int32_t mode, const int32_t *user_cuts, int32_t n_user_cuts,
+                     int32_t flags, ckpt_plan **out) {
+  return guarded([&] {
+    need(out, "plan_checkpoints(out)");
+    *out = nullptr;
+    auto p = std::make_unique<ckpt_plan>();
+    p->p = ckpt::make_plan(n_layers, layer_bytes, cut_bytes, budget, mode, user_cuts,
+                           n_user_cuts, flags);
+    *out = p.release();
+  });
+}
+
+int plan_info(const ckpt_plan *plan, int32_t *mode, int32_t *n_layers, int32_t *n_cuts,
+              uint64_t *x, uint64_t *y, uint64_t *extra) {
+  return guarded([&] {
+    need(plan, "plan_info");
+    if (mode) *mode = plan->p.mode;
+    if (n_layers) *n_layers = plan->p.n;
+    if (n_cuts) *n_cuts = int32_t(plan->p.cuts.size());
+    if (x) *x = plan->p.x;
+    if (y) *y = plan->p.y;
+    if (extra) *extra = plan->p.extra;
+  });
+}
+
+int plan_cuts(const ckpt_plan *plan, int32_t *cuts, int32_t cap, int32_t *n_cuts) {
+  return guarded([&] {
+    need(plan, "plan_cuts");
+    const auto &c = plan->p.cuts;
+    if (n_cuts) *n_cuts = int32_t(c.size());
+    if (cuts && cap > 0) std::memcpy(cuts, c.data(), sizeof(int32_t) * std::min<size_t>(size_t(cap), c.size()));
+  });
+}
+
+int plan_serialize(const ckpt_plan *plan, uint8_t *buf, uint64_t cap, uint64_t *len) {
+  return guarded([&] {
+    need(plan, "plan_serialize");
+    auto v = ckpt::serialize(plan->p);
+    if (len) *len = v.size();
+    if (buf) {
+      if (cap < v.size()) ckpt::fail(CKPT_E_INVALID, "plan_serialize: buffer too small");
+      std::memcpy(buf, v.data(), v.size());
+    }
+  });
+}
+
+void plan_free(ckpt_plan *plan) { delete plan; }
+
+int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
+  return guarded([&] {
+    need(desc, "net_create(desc)");
+    need(out, "net_create(out)");
+    *out = nullptr;
+    for (int32_t r : desc->reserved)
+      if (r != 0) ckpt::fail(CKPT_E_INVALID, "net_create: reserved fields must be zero");
+    auto h = std::make_unique<ckpt_net>();
+    switch (desc->kind) {
+      case CKPT_NET_MLP: h->net = ckpt::make_mlp_net(*desc); break;
+      case CKPT_NET_RESNET_BASIC: h->net = ckpt::make_resnet_basic_net(*desc); break;
+      default: ckpt::fail(CKPT_E_INVALID, "net_create: unknown network kind");
+    }
+    *out = h.release();
+  });
+}
+
+void net_destroy(ckpt_net *net) { delete net; }
+
+int net_units(const ckpt_net *net, int32_t *n) {
+  return guarded([&] {
+    need(net, "net_units");
+    need(n, "net_units(n)");
+    *n = net->net->n;
+  });
+}
+
+int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q) {
+  return guarded([&] {
+    need(net, "net_unit_sizes");
+    const auto &N = *net->net;
+    if (b) std::memcpy(b, N.b.data(), N.b.size() * 8);
+    if (a) std::memcpy(a, N.a.data(), N.a.size() * 8);
+    if (q) std::memcpy(q, N.q.data(), N.q.size() * 8);
+  });
+}
+
+int net_layer_sizes(const ckpt_net *net, uint64_t *layer_bytes, uint64_t *cut_bytes) {
+  return guarded([&] {
+    need(net, "net_layer_sizes");
+    const auto &N = *net->net;
+    for (int32_t i = 0; i < N.n; ++i) {
+      if (layer_bytes) layer_bytes[i] = N.a[size_t(i)] + N.b[size_t(i) + 1];
+      if (cut_bytes) cut_bytes[i] = (i + 1 < N.n) ? N.b[size_t(i) + 1] : 0;
+    }
+  });
+}
+
+int net_param_bytes(const ckpt_net *net, uint64_t *bytes) {
+  return guarded([&] {
+    need(net, "net_param_bytes");
+    need(bytes, "net_param_bytes(bytes)");
+    *bytes = net->net->param_bytes;
+  });
+}
+
+int net_param_count(const ckpt_net *net, int32_t *count) {
+  return guarded([&] {
+    need(net, "net_param_count");
+    need(count, "net_param_count(count)");
+    *count = int32_t(net->net->params.size());
+  });
+}
+
+int net_param_info(const ckpt_net *net, int32_t k, char *name, int32_t cap, uint64_t *offset,
+                   uint64_t *numel) {
+  return guarded([&] {
+    need(net, "net_param_info");
+    const auto &ps = net->net->params;
+    if (k < 0 || size_t(k) >= ps.size()) ckpt::fail(CKPT_E_INVALID, "net_param_info: bad index");
+    const auto &t = ps[size_t(k)];
+    if (name && cap > 0) {
+      size_t nlen = std::min(size_t(cap - 1), t.name.size());
+      std::memcpy(name, t.name.data(), nlen);
+      name[nlen] = 0;
+    }
+    if (offset) *offset = t.off;
+    if (numel) *numel = t.numel;
+  });
+}
+
+int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt_b, uint64_t *arena,
+                    uint64_t *grad, uint64_t *peak) {
+  return guarded([&] {
+    need(net, "plan_accounting(net)");
+    need(plan, "plan_accounting(plan)");
+    if (plan->p.n != net->net->n)
+      ckpt::fail(CKPT_E_MISMATCH, "plan_accounting: plan n differs from the net's unit count");
+    auto acc = ckpt::account(plan->p, net->net->b, net->net->a, net->net->q);
+    if (ckpt_b) *ckpt_b = acc.ckpt;
+    if (arena) *arena = acc.arena;
+    if (grad) *grad = acc.grad;
+    if (peak) *peak = acc.peak();
+  });
+}
+
+int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *bytes) {
+  return guarded([&] {
+    need(net, "net_workspace_bytes(net)");
+    need(plan, "net_workspace_bytes(plan)");
+    need(bytes, "net_workspace_bytes(bytes)");
+    if (plan->p.n != net->net->n)
+      ckpt::fail(CKPT_E_MISMATCH, "net_workspace_bytes: plan n differs from the net's unit count");
+    auto acc = ckpt::account(plan->p, net->net->b, net->net->a, net->net->q);
+    *bytes = ckpt::workspace_bytes(*net->net, acc);
+  });
+}
+
+int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+               const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
+               float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats) {
+  return guarded([&] {
+    need(net, "train_step(net)");
+    need(params, "train_step(params)");
+    need(grads, "train_step(grads)");
+    need(batch, "train_step(batch)");
+    need(batch->input, "train_step(batch.input)");
+    need(batch->target, "train_step(batch.target)");
+    need(plan, "train_step(plan)");
+    need(workspace, "train_step(workspace)");
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+      ckpt::fail(CKPT_E_INVALID, "train_step: workspace must be 256-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
+      ckpt::fail(CKPT_E_INVALID, "train_step: params and grads must be 256-byte aligned");
+    if (plan->p.n != net->net->n)
+      ckpt::fail(CKPT_E_MISMATCH, "train_step: plan n differs from the net's unit count");
+    ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
+                         *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
+                         static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// Internal declarations shared by the libckpt sources.
+#pragma once
+
+#include <cstdint>
+#include <exception>
+#include <string>
+#include <vector>
+
+#include "../../include/ckpt.h"
+
+namespace ckpt {
+
+inline uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+// An error carried to the C boundary as (code, message).
+struct Error : std::exception {
+  int code;
+  std::string msg;
+  Error(int c, std::string m) : code(c), msg(std::move(m)) {}
+  const char *what() const noexcept override { return msg.c_str(); }
+};
+
+[[noreturn]] inline void fail(int code, const std::string &msg) { throw Error(code, msg); }
+
+// ---------------------------------------------------------------- plans --
+struct Plan {
+  int32_t mode = CKPT_NONE;
+  int32_t n = 0;
+  bool keep_last = false;
+  std::vector<int32_t> cuts;   // ascending; cut c keeps x_{c+1}
+  uint64_t x = 0, y = 0, extra = 0;
+
+  // half-open segments [lo, hi) of a one-level plan
+  std::vector<std::pair<int32_t, int32_t>> segments() const {
+    std::vector<std::pair<int32_t, int32_t>> s;
+    int32_t lo = 0;
+    for (int32_t c : cuts) {
+      s.emplace_back(lo, c + 1);
+      lo = c + 1;
+    }
+    s.emplace_back(lo, n);
+    return s;
+  }
+};
+
+struct Accounting {
+  uint64_t ckpt = 0, arena = 0, grad = 0;
+  uint64_t peak() const { return ckpt + arena + grad; }
+};
+
+Plan make_plan(int32_t n, const uint64_t *layer_bytes, const uint64_t *cut_bytes, uint64_t budget,
+               int32_t mode, const int32_t *user_cuts, int32_t n_user_cuts, int32_t flags);
+std::vector<uint8_t> serialize(const Plan &p);
+// b: n+1 entries, a and q: n entries
+Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
+                   const std::vector<uint64_t> &q);
+uint64_t recursive_extra(int32_t n);
+
+}  // namespace ckpt

@@ -1,0 +1,79 @@
+// Residual-MLP chain: unit i computes y = x + relu(x W_i + b_i) on [batch, width]
+// fp32 (the fully connected operator of the paper's Fig. 1, made residual so
+// that a deep chain stays trainable); head = mean squared error.
+//
+// Static layout per unit: boundary b = [B, D] f32; saved internals a = the
+// pre-activation z [B, D]; gradient scratch q = the masked gradient dr [B, D].
+#include "kernels.h"
+#include "net.h"
+
+namespace ckpt {
+namespace {
+
+class MlpNet : public Net {
+ public:
+  int B, D;
+  std::vector<int> wi, bi;
+
+  explicit MlpNet(const ckpt_net_desc &d) {
+    desc = d;
+    n = d.depth;
+    B = d.batch;
+    D = d.width;
+    const uint64_t t = align256(uint64_t(B) * D * 4);
+    b.assign(size_t(n) + 1, t);
+    a.assign(size_t(n), t);
+    q.assign(size_t(n), t);
+    for (int i = 0; i < n; ++i) {
+      wi.push_back(add_param("u" + std::to_string(i) + ".W", uint64_t(D) * D));
+      bi.push_back(add_param("u" + std::to_string(i) + ".b", uint64_t(D)));
+    }
+    ks_bytes = 256;  // loss scalar
+  }
+
+  void fwd(int32_t i, const void *x, void *y, void *saved, StepCtx &c) override {
+    gemm_f32(c.s, B, D, D, static_cast<const float *>(x), D, false, P(c, wi[i]), D, false,
+             static_cast<float *>(y), D, GEMM_EPI_MLPFWD, nullptr, 0, P(c, bi[i]),
+             static_cast<float *>(saved), D);
+    c.launches += 1;
+  }
+
+  void bwd(int32_t i, const void *g, void *dx, const void *x, const void *, const void *saved,
+           void *q, StepCtx &c) override {
+    const float *gf = static_cast<const float *>(g);
+    float *dr = static_cast<float *>(q);
+    mlp_relu_bwd(c.s, B, D, gf, static_cast<const float *>(saved), dr, G(c, bi[i]));
+    // dW = x^T dr : [D_in, D_out] = [D, B] x [B, D]
+    gemm_f32(c.s, D, D, B, static_cast<const float *>(x), D, true, dr, D, false, G(c, wi[i]), D,
+             GEMM_EPI_STORE);
+    c.launches += 2;
+    if (dx) {  // dx = g + dr W^T
+      gemm_f32(c.s, B, D, D, dr, D, false, P(c, wi[i]), D, true, static_cast<float *>(dx), D,
+               GEMM_EPI_ADD, gf, D);
+      c.launches += 1;
+    }
+  }
+
+  void head(const void *xn, void *g, StepCtx &c) override {
+    mse_head(c.s, int64_t(B) * D, static_cast<const float *>(xn),
+             static_cast<const float *>(c.target), static_cast<float *>(g),
+             reinterpret_cast<float *>(c.ks));
+    c.launches += 1;
+  }
+
+  const float *loss_ptr(const StepCtx &c) const override {
+    return reinterpret_cast<const float *>(c.ks);
+  }
+};
+
+}  // namespace
+
+std::unique_ptr<Net> make_mlp_net(const ckpt_net_desc &d) {
+  if (d.depth <= 0 || d.width <= 0 || d.batch <= 0)
+    fail(CKPT_E_INVALID, "net_create: MLP needs positive depth, width and batch");
+  if (int64_t(d.batch) * d.width > (int64_t(1) << 31))
+    fail(CKPT_E_INVALID, "net_create: MLP tensor too large");
+  return std::make_unique<MlpNet>(d);
+}
+
+}  // namespace ckpt

@@ -1,0 +1,162 @@
+"""C-ABI checks that need no GPU: the library loads and exports every symbol
+the header declares; the C++ planner and accounting agree with the oracle
+(byte-identical serialisation, identical PEAK), fuzzed; error paths return the
+documented codes before anything is launched."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import planner as PL
+from oracle import sizes as SZ
+
+K = pytest.importorskip("paper_1604_06174_amd.ckpt")
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "ckpt.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(?:int|void|const char \*)\s*\**\s*([a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert "train_step" in names and "plan_checkpoints" in names
+    for nm in names:
+        assert hasattr(K._lib, nm), nm
+    assert sorted(K.EXPORTED) == names
+
+
+def _lib_plan(n, lb, cb, budget, mode, user=None, flags=0):
+    return K.plan_checkpoints(lb, cb, budget, mode, user, flags, n_layers=n)
+
+
+def _compare(n, lb, cb, budget, mode, user=None, flags=0):
+    op = PL.plan(n, lb, cb, budget, mode, user, flags)
+    lp = _lib_plan(n, lb, cb, budget, mode, user, flags)
+    assert lp.serialize() == op.serialize()
+    assert lp.cuts() == op.cuts
+    return op, lp
+
+
+def test_planner_fuzz_matches_oracle():
+    rng = np.random.default_rng(7)
+    for trial in range(400):
+        n = int(rng.integers(1, 300)) if trial % 10 else int(rng.integers(1000, 20000))
+        lb = [int(v) for v in rng.integers(0, 1 << 20, n)]
+        cand = rng.random(n) < (1.0 if trial % 3 == 0 else 0.8)
+        cb = [int(v) if c else 0 for v, c in zip(rng.integers(1, 1 << 18, n), cand)]
+        cb[-1] = 0
+        total = sum(lb)
+        for mode, budget in [(PL.SQRT, 0), (PL.SQRT, int(rng.integers(1, 40))),
+                             (PL.GREEDY, 0), (PL.GREEDY, int(rng.integers(0, total + 2))),
+                             (PL.GREEDY, total), (PL.NONE, 0)]:
+            for flags in (0, PL.FLAG_KEEP_LAST):
+                _compare(n, lb, cb, budget, mode, flags=flags)
+        if all(c > 0 for c in cb[:-1]):
+            _compare(n, lb, cb, 0, PL.RECURSIVE)
+        cands = [i for i in range(n - 1) if cb[i] > 0]
+        if cands:
+            k = int(rng.integers(0, min(len(cands), 20) + 1))
+            user = sorted(rng.choice(cands, k, replace=False).tolist())
+            _compare(n, lb, cb, 0, PL.USER, user)
+
+
+def test_planner_edge_cases():
+    _compare(1, [5], [0], 0, PL.SQRT)
+    _compare(1, [5], [0], 0, PL.GREEDY)
+    _compare(1, [5], [0], 0, PL.RECURSIVE)
+    _compare(2, [5, 5], [0, 0], 0, PL.GREEDY)          # no candidates
+    _compare(2, [0, 0], [3, 0], 0, PL.GREEDY)          # zero-size units never exceed B = 0
+    _compare(7, [1] * 7, [1] * 6 + [0], 10 ** 12, PL.SQRT)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((0, [], [], 0, PL.SQRT), K.E_INVALID),
+    ((3, [1, 1, 1], [1, 1, 1], 0, PL.SQRT), K.E_INVALID),
+    ((4, [1] * 4, [1, 1, 1, 0], 0, PL.USER, [1, 0]), K.E_INVALID),
+    ((4, [1] * 4, [1, 1, 1, 0], 0, PL.USER, [1, 1]), K.E_INVALID),
+    ((4, [1] * 4, [1, 1, 1, 0], 0, PL.USER, [3]), K.E_INVALID),
+    ((4, [1] * 4, [1, 0, 1, 0], 0, PL.USER, [1]), K.E_INVALID),
+    ((4, [1] * 4, [1, 0, 1, 0], 0, PL.RECURSIVE), K.E_UNSUPPORTED),
+    ((4, [1] * 4, [1, 1, 1, 0], 0, 77), K.E_INVALID),
+])
+def test_planner_errors(args, code):
+    with pytest.raises(K.CkptError) as ei:
+        _lib_plan(*args)
+    assert ei.value.code == code
+
+
+WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
+                 dict(kind="mlp", depth=1024, width=1024, batch=256),
+                 dict(kind="mlp", depth=7, width=40, batch=3)]
+
+
+@pytest.mark.parametrize("cfg", WORKLOADS_CPU)
+def test_net_tables_and_accounting_match_oracle(cfg):
+    from paper_1604_06174_amd.workload import net_for
+    net = net_for(cfg)
+    st = synth.structure(cfg)
+    b, a, q = net.unit_sizes()
+    assert (b, a, q) == tuple(SZ.tables(st))
+    lb, cb = net.layer_sizes()
+    assert (lb, cb) == SZ.layer_and_cut_bytes(st)
+    n = st.n
+    modes = [(PL.NONE, 0, 0), (PL.SQRT, 0, 0), (PL.SQRT, 8, PL.FLAG_KEEP_LAST),
+             (PL.GREEDY, sum(lb) // 10, 0), (PL.RECURSIVE, 0, 0)]
+    for mode, budget, flags in modes:
+        lp = _lib_plan(n, lb, cb, budget, mode, flags=flags)
+        op = PL.plan(n, lb, cb, budget, mode, flags=flags)
+        acc = net.accounting(lp)
+        oacc = PL.account(op, b, a, q)
+        assert (acc["ckpt"], acc["arena"], acc["grad"], acc["peak"]) == \
+            (oacc.ckpt, oacc.arena, oacc.grad, oacc.peak)
+        assert net.workspace_bytes(lp) >= acc["peak"]
+
+
+def test_param_layout_names_match_structure():
+    from paper_1604_06174_amd.workload import net_for
+    cfg = dict(kind="mlp", depth=5, width=40, batch=3)
+    net = net_for(cfg)
+    names = [nm for nm, _, _ in net.param_layout()]
+    assert names == [nm for nm, _, _ in synth.structure(cfg).param_list()]
+    offs = [off for _, off, _ in net.param_layout()]
+    assert all(o % 256 == 0 for o in offs)
+
+
+def test_net_create_errors():
+    with pytest.raises(K.CkptError) as ei:
+        K.net_create(99, 1, 1, 1)
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError):
+        K.net_create(K.NET_MLP, 0, 4, 4)
+
+
+def test_train_step_rejects_before_launch():
+    """Every rejected call returns before any HIP work: fake device addresses
+    are never dereferenced."""
+    net = K.net_create(K.NET_MLP, 4, 6, 8)
+    lb, cb = net.layer_sizes()
+    plan = K.plan_checkpoints(lb, cb, 0, K.SQRT)
+    other = K.plan_checkpoints([1] * 5, [1] * 4 + [0], 0, K.SQRT)
+    fake = 1 << 20
+    need = net.workspace_bytes(plan)
+    with pytest.raises(K.CkptError) as ei:
+        K.train_step(net, fake, fake, fake, fake, plan, fake, need - 256)
+    assert ei.value.code == K.E_WORKSPACE
+    with pytest.raises(K.CkptError) as ei:
+        K.train_step(net, fake, fake, fake, fake, other, fake, need)
+    assert ei.value.code == K.E_MISMATCH
+    with pytest.raises(K.CkptError) as ei:
+        K.train_step(net, fake, fake, fake, fake, plan, fake + 16, need)
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError) as ei:
+        K.train_step(net, 0, fake, fake, fake, plan, fake, need)
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError) as ei:
+        K.train_step(net, fake, fake, 0, fake, plan, fake, need)
+    assert ei.value.code == K.E_INVALID

@@ -1,0 +1,354 @@
+// Batch normalisation (training mode, per-channel statistics over N*H*W),
+// its backward, and the global-average-pool + FC + softmax cross-entropy head.
+// NHWC fp32 tensors; channel counts are multiples of 4 so every thread moves
+// one float4 of channels.  Channel sums are accumulated in float64 and
+// reduced in a fixed order (per-workgroup partials, then a tree), so the
+// results are bit-reproducible and insensitive to cancellation in
+// E[x^2] - E[x]^2.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace ckpt {
+namespace {
+
+constexpr float BN_EPS = 1e-5f;
+
+// ---- partial sums for the backward: sum(ds), sum(ds * xhat) per channel ----
+template <bool MASKED>
+__global__ __launch_bounds__(256) void k_bn_bwd_partials(int P, int J, int PB, const float *__restrict__ G,
+                                                         const float *__restrict__ Ym,
+                                                         const float *__restrict__ Cv,
+                                                         const float *__restrict__ st,
+                                                         double *__restrict__ part) {
+  __shared__ double red[2][256][4];
+  const int CQ = J / 4, PL = 256 / CQ;
+  const int cq = threadIdx.x % CQ, pl = threadIdx.x / CQ;
+  const int c0 = cq * 4;
+  const int p0 = blockIdx.x * PB, p1 = min(P, p0 + PB);
+  float mean[4], rstd[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    mean[k] = st[c0 + k];
+    rstd[k] = st[J + c0 + k];
+  }
+  double s1[4] = {0, 0, 0, 0}, s2[4] = {0, 0, 0, 0};
+  if (pl < PL) {
+    for (int p = p0 + pl; p < p1; p += PL) {
+      const size_t o = size_t(p) * J + c0;
+      const float4 g = *reinterpret_cast<const float4 *>(G + o);
+      const float4 c = *reinterpret_cast<const float4 *>(Cv + o);
+      float gv[4] = {g.x, g.y, g.z, g.w}, cv[4] = {c.x, c.y, c.z, c.w};
+      if (MASKED) {
+        const float4 y = *reinterpret_cast<const float4 *>(Ym + o);
+        float yv[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) gv[k] = yv[k] > 0.f ? gv[k] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float xh = (cv[k] - mean[k]) * rstd[k];
+        s1[k] += double(gv[k]);
+        s2[k] += double(gv[k]) * double(xh);
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    red[0][threadIdx.x][k] = s1[k];
+    red[1][threadIdx.x][k] = s2[k];
+  }
+  __syncthreads();
+  // tree over pixel lanes (threads with the same cq are tid = cq + CQ*pl)
+  for (int w = PL / 2; w > 0; w >>= 1) {
+    if (pl < w) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        red[0][threadIdx.x][k] += red[0][threadIdx.x + w * CQ][k];
+        red[1][threadIdx.x][k] += red[1][threadIdx.x + w * CQ][k];
+      }
+    }
+    __syncthreads();
+  }
+  if (pl == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      part[(size_t(blockIdx.x) * 2 + 0) * J + c0 + k] = red[0][threadIdx.x][k];
+      part[(size_t(blockIdx.x) * 2 + 1) * J + c0 + k] = red[1][threadIdx.x][k];
+    }
+  }
+}
+
+// One workgroup per channel: sum the per-workgroup partials in a fixed order.
+//   FWD: partials are (sum v, sum v^2) -> out0 = mean, out1 = rstd
+//   BWD: partials are (sum ds, sum ds*xhat) -> out0 = mean(ds),
+//        out1 = mean(ds*xhat); dgamma = sum ds*xhat, dbeta = sum ds
+template <bool FWD>
+__global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ part, int nb, int J,
+                                                     double m, float *__restrict__ out,
+                                                     float *__restrict__ dgamma,
+                                                     float *__restrict__ dbeta) {
+  __shared__ double r0[256], r1[256];
+  const int j = blockIdx.x;
+  double a = 0, b = 0;
+  for (int k = threadIdx.x; k < nb; k += 256) {
+    a += part[(size_t(k) * 2 + 0) * J + j];
+    b += part[(size_t(k) * 2 + 1) * J + j];
+  }
+  r0[threadIdx.x] = a;
+  r1[threadIdx.x] = b;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      r0[threadIdx.x] += r0[threadIdx.x + w];
+      r1[threadIdx.x] += r1[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    if (FWD) {
+      const double mean = r0[0] / m;
+      double var = r1[0] / m - mean * mean;
+      if (var < 0) var = 0;
+      out[j] = float(mean);
+      out[J + j] = float(1.0 / sqrt(var + double(BN_EPS)));
+    } else {
+      out[j] = float(r0[0] / m);
+      out[J + j] = float(r1[0] / m);
+      dbeta[j] = float(r0[0]);
+      dgamma[j] = float(r1[0]);
+    }
+  }
+}
+
+// y = [relu]( gamma (c - mean) rstd + beta [+ shortcut] )
+template <int RES>
+__global__ __launch_bounds__(256) void k_bn_apply(int64_t P, int J, const float *__restrict__ Cv,
+                                                  const float *__restrict__ st,
+                                                  const float *__restrict__ gamma,
+                                                  const float *__restrict__ beta,
+                                                  const float *__restrict__ X, int H, int W, int Cx,
+                                                  float *__restrict__ Y) {
+  const int CQ = J / 4;
+  const int64_t total = P * CQ;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c0 = int(e % CQ) * 4;
+    const int64_t p = e / CQ;
+    const float4 c = *reinterpret_cast<const float4 *>(Cv + p * J + c0);
+    float cv[4] = {c.x, c.y, c.z, c.w}, o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = gamma[c0 + k] * ((cv[k] - st[c0 + k]) * st[J + c0 + k]) + beta[c0 + k];
+    if (RES == BN_RES_ID) {
+      const float4 x = *reinterpret_cast<const float4 *>(X + p * J + c0);
+      o[0] += x.x; o[1] += x.y; o[2] += x.z; o[3] += x.w;
+    } else if (RES == BN_RES_A) {
+      // option A: x[n, 2h, 2w, c] for c < Cx, zero for the appended channels
+      const int64_t w = p % W, h = (p / W) % H, n = p / (int64_t(W) * H);
+      const int64_t xo = ((n * 2 * H + 2 * h) * 2 * W + 2 * w) * Cx;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (c0 + k < Cx) o[k] += X[xo + c0 + k];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = fmaxf(o[k], 0.f);
+    *reinterpret_cast<float4 *>(Y + p * J + c0) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// dc = gamma rstd (ds - mean(ds) - xhat mean(ds xhat)),  ds = [mask] g
+template <bool MASKED>
+__global__ __launch_bounds__(256) void k_bn_bwd_apply(int64_t P, int J, const float *__restrict__ G,
+                                                      const float *__restrict__ Ym,
+                                                      const float *__restrict__ Cv,
+                                                      const float *__restrict__ st,
+                                                      const float *__restrict__ gamma,
+                                                      const float *__restrict__ sums,
+                                                      float *__restrict__ D) {
+  const int CQ = J / 4;
+  const int64_t total = P * CQ;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c0 = int(e % CQ) * 4;
+    const int64_t o = (e / CQ) * J + c0;
+    const float4 g = *reinterpret_cast<const float4 *>(G + o);
+    const float4 c = *reinterpret_cast<const float4 *>(Cv + o);
+    float gv[4] = {g.x, g.y, g.z, g.w}, cv[4] = {c.x, c.y, c.z, c.w}, r[4];
+    if (MASKED) {
+      const float4 y = *reinterpret_cast<const float4 *>(Ym + o);
+      float yv[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) gv[k] = yv[k] > 0.f ? gv[k] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int ch = c0 + k;
+      const float rs = st[J + ch];
+      const float xh = (cv[k] - st[ch]) * rs;
+      r[k] = gamma[ch] * rs * (gv[k] - sums[ch] - xh * sums[J + ch]);
+    }
+    *reinterpret_cast<float4 *>(D + o) = make_float4(r[0], r[1], r[2], r[3]);
+  }
+}
+
+// ---- head: global average pool -> FC -> softmax cross-entropy ----
+// One workgroup per sample.
+__global__ __launch_bounds__(256) void k_head_sample(int N, int HW, int C, int K,
+                                                     const float *__restrict__ X,
+                                                     const float *__restrict__ Wf,
+                                                     const float *__restrict__ bf,
+                                                     const int *__restrict__ labels,
+                                                     float *__restrict__ pooled,
+                                                     float *__restrict__ dlog,
+                                                     float *__restrict__ lossn,
+                                                     float *__restrict__ G) {
+  extern __shared__ float sh[];
+  float *pl = sh;           // [C]
+  float *lg = sh + C;       // [K]
+  float *red = sh + C + K;  // [256]
+  const int n = blockIdx.x, t = threadIdx.x;
+  const float inv = 1.0f / float(HW);
+  for (int c = t; c < C; c += 256) {
+    float s = 0.f;
+    for (int p = 0; p < HW; ++p) s += X[(size_t(n) * HW + p) * C + c];
+    pl[c] = s * inv;
+    pooled[size_t(n) * C + c] = s * inv;
+  }
+  __syncthreads();
+  for (int k = t; k < K; k += 256) {
+    float s = bf[k];
+    for (int c = 0; c < C; ++c) s += pl[c] * Wf[size_t(c) * K + k];
+    lg[k] = s;
+  }
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int k = t; k < K; k += 256) mx = fmaxf(mx, lg[k]);
+  red[t] = mx;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float se = 0.f;
+  for (int k = t; k < K; k += 256) se += expf(lg[k] - mx);
+  red[t] = se;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] += red[t + w];
+    __syncthreads();
+  }
+  se = red[0];
+  // a label outside [0, K) yields a NaN loss for the sample and no one-hot term
+  const int lab = labels[n];
+  const bool lab_ok = lab >= 0 && lab < K;
+  if (t == 0) lossn[n] = lab_ok ? (logf(se) + mx) - lg[lab] : NAN;
+  __syncthreads();
+  const float invN = 1.0f / float(N);
+  for (int k = t; k < K; k += 256) {
+    const float p = expf(lg[k] - mx) / se;
+    const float d = (p - (k == lab ? 1.f : 0.f)) * invN;
+    dlog[size_t(n) * K + k] = d;
+    lg[k] = d;
+  }
+  __syncthreads();
+  for (int c = t; c < C; c += 256) {
+    float s = 0.f;
+    for (int k = 0; k < K; ++k) s += lg[k] * Wf[size_t(c) * K + k];
+    s *= inv;
+    for (int p = 0; p < HW; ++p) G[(size_t(n) * HW + p) * C + c] = s;
+  }
+}
+
+// dW[c][k] = sum_n pooled[n][c] dlog[n][k]; db[k] = sum_n dlog[n][k];
+// loss = sum_n lossn[n] / N  (n in order)
+__global__ __launch_bounds__(256) void k_head_params(int N, int C, int K,
+                                                     const float *__restrict__ pooled,
+                                                     const float *__restrict__ dlog,
+                                                     const float *__restrict__ lossn,
+                                                     float *__restrict__ dW, float *__restrict__ db,
+                                                     float *__restrict__ loss) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e < C * K) {
+    const int c = e / K, k = e % K;
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) s += pooled[size_t(n) * C + c] * dlog[size_t(n) * K + k];
+    dW[e] = s;
+  } else if (e < C * K + K) {
+    const int k = e - C * K;
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) s += dlog[size_t(n) * K + k];
+    db[k] = s;
+  } else if (e == C * K + K) {
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) s += lossn[n];
+    loss[0] = s / float(N);
+  }
+}
+
+inline int ew_grid(int64_t work) {
+  int64_t g = (work + 255) / 256;
+  return int(g < 8192 ? (g < 1 ? 1 : g) : 8192);
+}
+
+}  // namespace
+
+int bn_partial_blocks(int64_t P, int J) {
+  const int PL = 256 / (J / 4);
+  int64_t pb = (P + 511) / 512;
+  pb = (pb + PL - 1) / PL * PL;
+  if (pb < PL) pb = PL;
+  return int((P + pb - 1) / pb);
+}
+
+static int64_t bn_pb(int64_t P, int J) {
+  const int nb = bn_partial_blocks(P, J);
+  return (P + nb - 1) / nb;
+}
+
+void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st) {
+  hipLaunchKernelGGL((k_bn_finalize<true>), dim3(J), dim3(256), 0, s, part, nb, J, double(m), st,
+                     nullptr, nullptr);
+}
+
+void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const float *st,
+              const float *gamma, const float *beta, const float *X, int H, int W, int Cx, float *Y) {
+  const int g = ew_grid(P * (J / 4));
+  if (res == BN_RES_NONE)
+    hipLaunchKernelGGL((k_bn_apply<BN_RES_NONE>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
+  else if (res == BN_RES_ID)
+    hipLaunchKernelGGL((k_bn_apply<BN_RES_ID>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
+  else
+    hipLaunchKernelGGL((k_bn_apply<BN_RES_A>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
+}
+
+void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Ym, const float *Cv,
+                 const float *st, const float *gamma, double *part, float *sums, float *dgamma,
+                 float *dbeta, float *D) {
+  const int nb = bn_partial_blocks(P, J);
+  const int pb = int(bn_pb(P, J));
+  if (Ym)
+    hipLaunchKernelGGL((k_bn_bwd_partials<true>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, Ym, Cv, st, part);
+  else
+    hipLaunchKernelGGL((k_bn_bwd_partials<false>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, Ym, Cv, st, part);
+  hipLaunchKernelGGL((k_bn_finalize<false>), dim3(J), dim3(256), 0, s, part, nb, J, double(P), sums,
+                     dgamma, dbeta);
+  const int g = ew_grid(P * (J / 4));
+  if (Ym)
+    hipLaunchKernelGGL((k_bn_bwd_apply<true>), dim3(g), dim3(256), 0, s, P, J, G, Ym, Cv, st, gamma, sums, D);
+  else
+    hipLaunchKernelGGL((k_bn_bwd_apply<false>), dim3(g), dim3(256), 0, s, P, J, G, Ym, Cv, st, gamma, sums, D);
+}
+
+void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X, const float *Wf,
+                     const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
+                     float *G, float *dW, float *db, float *loss) {
+  const size_t lds = size_t(C + K + 256) * 4;
+  hipLaunchKernelGGL(k_head_sample, dim3(N), dim3(256), lds, s, N, HW, C, K, X, Wf, bf, labels,
+                     pooled, dlog, lossn, G);
+  const int tot = C * K + K + 1;
+  hipLaunchKernelGGL(k_head_params, dim3((tot + 255) / 256), dim3(256), 0, s, N, C, K, pooled,
+                     dlog, lossn, dW, db, loss);
+}
+
+}  // namespace ckpt

@@ -1,0 +1,453 @@
+// 3x3 convolutions (pad 1) as implicit GEMMs on fp32 MFMA (v_mfma_f32_16x16x4f32),
+// NHWC activations, weights [Cout, 3, 3, Cin].
+//
+// Forward / data-gradient kernel (k_conv3x3):
+//   out[n, h, w, j] = sum_{tap, c} in(n, h, w, tap, c) * B(tap, c, j)
+// One workgroup = R consecutive output rows of one image x BN output channels.
+// The input rows it needs (a halo, zero outside the image) are staged once in
+// LDS; the 3x3 taps are then read from LDS, so every input element is fetched
+// from memory once per workgroup.  Weights for one tap are staged per tap with
+// double buffering.
+//   FWD:   in = x[n, h*S + kh - 1, w*S + kw - 1, c],  B = W[j, kh, kw, c]
+//   DGRAD: the output gradient is up-sampled by the stride U (zeros between
+//          samples) and correlated with the flipped kernel:
+//          in = dy_up[n, h + 1 - kh, w + 1 - kw, c], B = W[c, kh, kw, j]
+// Epilogues: STATS (store, plus per-workgroup float64 sums of v and v^2 per
+// channel for batch-norm statistics), MASK (store acc * [m > 0]), SC1 / SC2
+// (add the shortcut's gradient g * [y > 0]: identity, or the option-A
+// subsample-and-zero-pad shortcut of a stride-2 block).
+//
+// Weight-gradient kernel (k_conv3x3_wgrad): per workgroup (same row tiling as
+// the forward) a partial dW[j, kh, kw, c] = sum over its pixels of
+// dy[p, j] * x(p, tap, c); a second kernel sums the partials over workgroups
+// in a fixed order.  No atomics anywhere: results are bit-reproducible.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace ckpt {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+struct ConvArgs {
+  const float *X;   // kernel input  [N, Hx, Wx, C]
+  const float *Wt;  // weights [Cout, 3, 3, Cin]
+  float *Y;         // kernel output [N, H, W, J]
+  int N, H, W;      // output dims
+  int Hx, Wx;       // input dims
+  int C, J;         // reduction / output channels
+  int R, rblk;      // output rows per workgroup, workgroups per image
+  const float *E0, *E1;  // epilogue operands (MASK: E0; SC: E0 = g, E1 = y)
+  int Eh, Ew, Ec;        // SC2: dims of g and y
+  double *stats;         // STATS: [gridDim.x][2][J]
+};
+
+__device__ __forceinline__ int cpad4(int c) { return (c + 3) & ~3; }
+
+template <int PSW, int NSUB, int MODE, int S, int EPI>
+__global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
+  constexpr int BN = 16 * NSUB;
+  extern __shared__ __align__(16) float smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, q = lane >> 4;
+  const int blk = blockIdx.x;
+  const int n = blk / a.rblk, r0 = (blk % a.rblk) * a.R;
+  const int j0 = blockIdx.y * BN;
+  const int Cp = cpad4(a.C), Cs = Cp + 4;
+  const int HR = MODE == CONV_FWD ? (a.R - 1) * S + 3 : a.R + 2;
+  const int HC = MODE == CONV_FWD ? (a.W - 1) * S + 3 : a.W + 2;
+  float *halo = smem;
+  float *Bs = smem + HR * HC * Cs;
+
+  // ---- halo fill: halo[(hr*HC + hc)*Cs + c] ----
+  {
+    const int cq = Cp / 4;
+    const int total = HR * HC * cq;
+    for (int e = tid; e < total; e += 256) {
+      const int c4 = (e % cq) * 4;
+      const int hc = (e / cq) % HC;
+      const int hr = e / (cq * HC);
+      int ir, ic;
+      bool ok;
+      if (MODE == CONV_FWD) {
+        ir = r0 * S - 1 + hr;
+        ic = hc - 1;
+        ok = ir >= 0 && ir < a.Hx && ic >= 0 && ic < a.Wx;
+      } else {  // up-sampled output gradient
+        const int ur = r0 - 1 + hr, uc = hc - 1;
+        ok = ur >= 0 && uc >= 0 && (ur % S) == 0 && (uc % S) == 0;
+        ir = ur / S;
+        ic = uc / S;
+        ok = ok && ir < a.Hx && ic < a.Wx;
+      }
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (ok) {
+        const float *src = a.X + ((size_t(n) * a.Hx + ir) * a.Wx + ic) * a.C + c4;
+        if ((a.C & 3) == 0) {
+          float4 t = *reinterpret_cast<const float4 *>(src);
+          v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = (c4 + k < a.C) ? src[k] : 0.f;
+        }
+      }
+      *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
+
+  // ---- weights of one tap: Bs[buf][c*BN + jj] ----
+  auto wval = [&](int tap, int c, int jj) -> float {
+    const int j = j0 + jj;
+    if (c >= a.C || j >= a.J) return 0.f;
+    if (MODE == CONV_FWD) return a.Wt[(size_t(j) * 9 + tap) * a.C + c];
+    return a.Wt[(size_t(c) * 9 + tap) * a.J + j];
+  };
+  const int bel = Cp * BN;  // elements per tap
+  constexpr int BREG = 8;   // supports Cp * BN <= 2048
+  float breg[BREG];
+  auto bload = [&](int tap) {
+#pragma unroll
+    for (int k = 0; k < BREG; ++k) {
+      const int e = tid + k * 256;
+      breg[k] = (e < bel) ? wval(tap, e / BN, e % BN) : 0.f;
+    }
+  };
+  auto bstore = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < BREG; ++k) {
+      const int e = tid + k * 256;
+      if (e < bel) Bs[buf * bel + e] = breg[k];
+    }
+  };
+  bload(0);
+  bstore(0);
+  __syncthreads();
+
+  // ---- pixel of each A-fragment row this lane supplies ----
+  const int npix = a.R * a.W;
+  int pr[PSW], pc[PSW];
+#pragma unroll
+  for (int s = 0; s < PSW; ++s) {
+    int p = (wave * PSW + s) * 16 + i16;
+    if (p >= npix) p = npix - 1;  // clamped rows are computed but never stored
+    pr[s] = p / a.W;
+    pc[s] = p % a.W;
+  }
+
+  floatx4 acc[PSW][NSUB];
+#pragma unroll
+  for (int s = 0; s < PSW; ++s)
+#pragma unroll
+    for (int t = 0; t < NSUB; ++t) acc[s][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int tap = 0; tap < 9; ++tap) {
+    const int kh = tap / 3, kw = tap % 3, buf = tap & 1;
+    if (tap + 1 < 9) bload(tap + 1);
+    int base[PSW];
+#pragma unroll
+    for (int s = 0; s < PSW; ++s) {
+      const int hr = MODE == CONV_FWD ? pr[s] * S + kh : pr[s] + 2 - kh;
+      const int hc = MODE == CONV_FWD ? pc[s] * S + kw : pc[s] + 2 - kw;
+      base[s] = (hr * HC + hc) * Cs + q;
+    }
+    const float *Bt = Bs + buf * bel + q * BN + i16;
+    for (int c = 0; c < Cp; c += 4) {
+      float av[PSW], bv[NSUB];
+#pragma unroll
+      for (int s = 0; s < PSW; ++s) av[s] = halo[base[s] + c];
+#pragma unroll
+      for (int t = 0; t < NSUB; ++t) bv[t] = Bt[c * BN + t * 16];
+#pragma unroll
+      for (int s = 0; s < PSW; ++s)
+#pragma unroll
+        for (int t = 0; t < NSUB; ++t)
+          acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s], bv[t], acc[s][t], 0, 0, 0);
+    }
+    if (tap + 1 < 9) bstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue ----
+  double s1[NSUB], s2[NSUB];
+#pragma unroll
+  for (int t = 0; t < NSUB; ++t) s1[t] = s2[t] = 0.0;
+#pragma unroll
+  for (int s = 0; s < PSW; ++s) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int p = (wave * PSW + s) * 16 + 4 * q + r;
+      const int rr = p / a.W, cc = p % a.W;
+      const int h = r0 + rr;
+      const bool pv = p < npix && h < a.H;
+#pragma unroll
+      for (int t = 0; t < NSUB; ++t) {
+        const int j = j0 + t * 16 + i16;
+        if (!pv || j >= a.J) continue;
+        const size_t o = ((size_t(n) * a.H + h) * a.W + cc) * a.J + j;
+        float v = acc[s][t][r];
+        if (EPI == CONV_EPI_STATS) {
+          s1[t] += double(v);
+          s2[t] += double(v) * double(v);
+        } else if (EPI == CONV_EPI_MASK) {
+          v = a.E0[o] > 0.f ? v : 0.f;
+        } else if (EPI == CONV_EPI_SC1) {
+          v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
+        } else if (EPI == CONV_EPI_SC2) {
+          if (((h | cc) & 1) == 0) {
+            const size_t o2 = ((size_t(n) * a.Eh + (h >> 1)) * a.Ew + (cc >> 1)) * a.Ec + j;
+            v += a.E1[o2] > 0.f ? a.E0[o2] : 0.f;
+          }
+        }
+        a.Y[o] = v;
+      }
+    }
+  }
+  if (EPI == CONV_EPI_STATS) {
+    // per-channel sums over the workgroup: lanes (q) then waves, fixed order
+    double *red = reinterpret_cast<double *>(smem);  // halo is no longer read
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NSUB; ++t) {
+      red[((wave * 4 + q) * 2 + 0) * BN + t * 16 + i16] = s1[t];
+      red[((wave * 4 + q) * 2 + 1) * BN + t * 16 + i16] = s2[t];
+    }
+    __syncthreads();
+    if (tid < 2 * BN) {
+      const int which = tid / BN, jj = tid % BN;
+      double acc2 = 0.0;
+      for (int k = 0; k < 16; ++k) acc2 += red[(k * 2 + which) * BN + jj];
+      if (j0 + jj < a.J) a.stats[(size_t(blk) * 2 + which) * a.J + j0 + jj] = acc2;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- wgrad --
+struct WgArgs {
+  const float *X;   // conv input [N, Hx, Wx, C]
+  const float *DY;  // conv output gradient [N, H, W, J]
+  float *part;      // [gridDim.x][J][9][C]
+  int N, H, W, Hx, Wx, C, J, R, rblk, S;
+};
+
+template <int GB>
+__global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
+  extern __shared__ __align__(16) float smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, q = lane >> 4;
+  const int blk = blockIdx.x;
+  const int n = blk / a.rblk, r0 = (blk % a.rblk) * a.R;
+  const int S = a.S;
+  const int Cp = cpad4(a.C), Cs = Cp + 4;
+  const int HR = (a.R - 1) * S + 3, HC = (a.W - 1) * S + 3;
+  const int npix = a.R * a.W;
+  const int npix4 = (npix + 3) & ~3;
+  const int Js = ((a.J + 15) & ~15) + 4;
+  float *halo = smem;
+  float *dys = smem + HR * HC * Cs;  // [npix4][Js]
+
+  {
+    const int cq = Cp / 4;
+    for (int e = tid; e < HR * HC * cq; e += 256) {
+      const int c4 = (e % cq) * 4, hc = (e / cq) % HC, hr = e / (cq * HC);
+      const int ir = r0 * S - 1 + hr, ic = hc - 1;
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (ir >= 0 && ir < a.Hx && ic >= 0 && ic < a.Wx) {
+        const float *src = a.X + ((size_t(n) * a.Hx + ir) * a.Wx + ic) * a.C + c4;
+        if ((a.C & 3) == 0) {
+          float4 t = *reinterpret_cast<const float4 *>(src);
+          v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = (c4 + k < a.C) ? src[k] : 0.f;
+        }
+      }
+      *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    for (int e = tid; e < npix4 * Js; e += 256) {
+      const int p = e / Js, j = e % Js;
+      const int h = r0 + p / a.W, w = p % a.W;
+      float v = 0.f;
+      if (p < npix && h < a.H && j < a.J) v = a.DY[((size_t(n) * a.H + h) * a.W + w) * a.J + j];
+      dys[e] = v;
+    }
+  }
+  __syncthreads();
+
+  const int jsub = (a.J + 15) / 16, csub = (Cp + 15) / 16;
+  const int ngroups = jsub * 9 * csub;  // group = (j subtile, tap, c subtile)
+  for (int g0 = wave; g0 < ngroups; g0 += 4 * GB) {
+    floatx4 acc[GB];
+    int gj[GB], gt[GB], gc[GB];
+#pragma unroll
+    for (int k = 0; k < GB; ++k) {
+      acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+      int g = g0 + 4 * k;
+      if (g >= ngroups) g = ngroups - 1;  // computed, not stored
+      gj[k] = g / (9 * csub);
+      gt[k] = (g / csub) % 9;
+      gc[k] = g % csub;
+    }
+    for (int p0 = 0; p0 < npix4; p0 += 4) {
+      const int p = p0 + q;
+      const int pp = p < npix ? p : npix - 1;  // its dy row is zero
+      const int rr = pp / a.W, cc = pp % a.W;
+#pragma unroll
+      for (int k = 0; k < GB; ++k) {
+        const float av = dys[p * Js + gj[k] * 16 + i16];
+        const int kh = gt[k] / 3, kw = gt[k] % 3;
+        const int c = gc[k] * 16 + i16;
+        const float bv = c < Cp ? halo[((rr * S + kh) * HC + (cc * S + kw)) * Cs + c] : 0.f;
+        acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[k], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < GB; ++k) {
+      const int g = g0 + 4 * k;
+      if (g >= ngroups) continue;
+      const int c = gc[k] * 16 + i16;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = gj[k] * 16 + 4 * q + r;
+        if (j < a.J && c < a.C)
+          a.part[((size_t(blk) * a.J + j) * 9 + gt[k]) * a.C + c] = acc[k][r];
+      }
+    }
+  }
+}
+
+// out[e] = sum over b of part[b][e], b in a fixed order: 16 slices of b,
+// then the slices in order.
+__global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ part, int nb,
+                                                      int E, float *__restrict__ out) {
+  __shared__ float red[16][16];
+  const int ex = threadIdx.x & 15, sl = threadIdx.x >> 4;
+  const int e = blockIdx.x * 16 + ex;
+  float s = 0.f;
+  if (e < E)
+    for (int b = sl; b < nb; b += 16) s += part[size_t(b) * E + e];
+  red[sl][ex] = s;
+  __syncthreads();
+  if (sl == 0 && e < E) {
+    float t = 0.f;
+    for (int k = 0; k < 16; ++k) t += red[k][ex];
+    out[e] = t;
+  }
+}
+
+struct Tile {
+  int R, rblk, psw;
+};
+
+constexpr size_t kMaxLds = 64 * 1024;
+
+size_t conv_lds(int mode, int S, int R, int W, int C, int J) {
+  const int Cp = (C + 3) & ~3, Cs = Cp + 4;
+  const int HR = mode == CONV_FWD ? (R - 1) * S + 3 : R + 2;
+  const int HC = mode == CONV_FWD ? (W - 1) * S + 3 : W + 2;
+  const int BN = J > 16 ? 32 : 16;
+  size_t halo = size_t(HR) * HC * Cs * 4;
+  size_t red = size_t(16) * 2 * BN * 8;
+  return (halo > red ? halo : red) + size_t(2) * Cp * BN * 4;
+}
+
+size_t wgrad_lds(int S, int R, int W, int C, int J) {
+  const int Cp = (C + 3) & ~3, Cs = Cp + 4;
+  const int HR = (R - 1) * S + 3, HC = (W - 1) * S + 3;
+  const int npix4 = (R * W + 3) & ~3;
+  const int Js = ((J + 15) & ~15) + 4;
+  return (size_t(HR) * HC * Cs + size_t(npix4) * Js) * 4;
+}
+
+// Whole output rows, at most 128 output pixels (8 MFMA row tiles) per
+// workgroup, shrunk until the LDS footprint fits.
+template <class Lds>
+Tile tile_for(int H, int W, Lds lds) {
+  int R = 128 / W;
+  if (R < 1) R = 1;
+  if (R > H) R = H;
+  while (R > 1 && lds(R) > kMaxLds) --R;
+  const int npix = R * W;
+  const int psw = (npix + 63) / 64;  // 16-pixel tiles per wavefront
+  return {R, (H + R - 1) / R, psw};
+}
+
+Tile conv_tile(int mode, int S, int H, int W, int C, int J) {
+  return tile_for(H, W, [&](int R) { return conv_lds(mode, S, R, W, C, J); });
+}
+
+Tile wgrad_tile(int S, int H, int W, int C, int J) {
+  return tile_for(H, W, [&](int R) { return wgrad_lds(S, R, W, C, J); });
+}
+
+template <int PSW, int NSUB, int MODE, int S>
+void launch_conv(const ConvArgs &a, int epi, size_t lds, dim3 grid, hipStream_t st) {
+  switch (epi) {
+    case CONV_EPI_STATS: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STATS>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_MASK: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASK>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_SC1: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC1>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_SC2: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC2>), grid, dim3(256), lds, st, a); break;
+    default: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STORE>), grid, dim3(256), lds, st, a); break;
+  }
+}
+
+template <int PSW, int NSUB>
+void launch_mode(const ConvArgs &a, int mode, int S, int epi, size_t lds, dim3 grid, hipStream_t st) {
+  if (mode == CONV_FWD) {
+    if (S == 1) launch_conv<PSW, NSUB, CONV_FWD, 1>(a, epi, lds, grid, st);
+    else launch_conv<PSW, NSUB, CONV_FWD, 2>(a, epi, lds, grid, st);
+  } else {
+    if (S == 1) launch_conv<PSW, NSUB, CONV_DGRAD, 1>(a, epi, lds, grid, st);
+    else launch_conv<PSW, NSUB, CONV_DGRAD, 2>(a, epi, lds, grid, st);
+  }
+}
+
+}  // namespace
+
+int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J) {
+  return N * conv_tile(mode, S, H, W, C, J).rblk;
+}
+
+int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J) {
+  return N * wgrad_tile(S, H, W, C, J).rblk;
+}
+
+bool conv3x3_supported(int mode, int S, int H, int W, int C, int J) {
+  const int BN = J > 16 ? 32 : 16;
+  if (((C + 3) & ~3) * BN > 2048) return false;  // per-tap weight staging
+  if (W > 128) return false;                      // <= 2 row tiles per wavefront
+  if (conv_lds(mode, S, conv_tile(mode, S, H, W, C, J).R, W, C, J) > kMaxLds) return false;
+  if (mode == CONV_FWD && wgrad_lds(S, wgrad_tile(S, H, W, C, J).R, W, C, J) > kMaxLds)
+    return false;
+  return true;
+}
+
+void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
+             int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1,
+             int Eh, int Ew, int Ec, double *stats) {
+  Tile t = conv_tile(mode, S, H, W, C, J);
+  const int NSUB = J > 16 ? 2 : 1;
+  ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats};
+  dim3 grid(N * t.rblk, (J + 16 * NSUB - 1) / (16 * NSUB));
+  const size_t lds = conv_lds(mode, S, t.R, W, C, J);
+  if (t.psw == 1) {
+    if (NSUB == 1) launch_mode<1, 1>(a, mode, S, epi, lds, grid, st);
+    else launch_mode<1, 2>(a, mode, S, epi, lds, grid, st);
+  } else {
+    if (NSUB == 1) launch_mode<2, 1>(a, mode, S, epi, lds, grid, st);
+    else launch_mode<2, 2>(a, mode, S, epi, lds, grid, st);
+  }
+}
+
+void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float *part, float *dW,
+                   int N, int H, int W, int Hx, int Wx, int C, int J) {
+  Tile t = wgrad_tile(S, H, W, C, J);
+  WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, t.R, t.rblk, S};
+  const int nb = N * t.rblk;
+  hipLaunchKernelGGL((k_conv3x3_wgrad<4>), dim3(nb), dim3(256), wgrad_lds(S, t.R, W, C, J), st, a);
+  const int E = J * 9 * C;
+  hipLaunchKernelGGL(k_sum_partials, dim3((E + 15) / 16), dim3(256), 0, st, part, nb, E, dW);
+}
+
+}  // namespace ckpt

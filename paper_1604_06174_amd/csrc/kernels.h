@@ -26,4 +26,40 @@ void mse_head(hipStream_t s, int64_t count, const float *y, const float *t, floa
 // Copy one f32 scalar (device to device) -- used to publish the loss.
 void copy_scalar(hipStream_t s, const float *src, float *dst);
 
+// ---- 3x3 convolutions (conv.hip) ----
+enum { CONV_FWD = 0, CONV_DGRAD = 1 };
+enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 = 3, CONV_EPI_SC2 = 4 };
+
+// Y[N,H,W,J] = conv of X[N,Hx,Wx,C] (FWD: stride S; DGRAD: gradient of a
+// stride-S forward conv, X = dy).  Epilogue operands: MASK E0 = mask tensor
+// shaped like Y; SC1 E0 = g, E1 = y shaped like Y; SC2 E0 = g, E1 = y of dims
+// [N, Eh, Ew, Ec].  STATS writes [blocks][2][J] float64 channel sums.
+void conv3x3(hipStream_t s, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
+             int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0 = nullptr,
+             const float *E1 = nullptr, int Eh = 0, int Ew = 0, int Ec = 0,
+             double *stats = nullptr);
+int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J);
+int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J);
+bool conv3x3_supported(int mode, int S, int H, int W, int C, int J);
+// dW[J,3,3,C] of a stride-S forward conv with input X[N,Hx,Wx,C] and output
+// gradient DY[N,H,W,J]; part holds conv3x3_wgrad_blocks * J*9*C floats.
+void conv3x3_wgrad(hipStream_t s, int S, const float *X, const float *DY, float *part, float *dW,
+                   int N, int H, int W, int Hx, int Wx, int C, int J);
+
+// ---- batch norm and the classifier head (bn.hip) ----
+enum { BN_RES_NONE = 0, BN_RES_ID = 1, BN_RES_A = 2 };
+int bn_partial_blocks(int64_t P, int J);
+// st[0..J) = mean, st[J..2J) = rstd from conv STATS partials over m values.
+void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st);
+// Y = relu(gamma (C - mean) rstd + beta [+ shortcut(X)]) over P pixels x J.
+void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const float *st,
+              const float *gamma, const float *beta, const float *X, int H, int W, int Cx, float *Y);
+// ds = Ym ? g [Ym > 0] : g; writes dgamma, dbeta and D = dL/dC.
+void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Ym, const float *Cv,
+                 const float *st, const float *gamma, double *part, float *sums, float *dgamma,
+                 float *dbeta, float *D);
+void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X, const float *Wf,
+                     const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
+                     float *G, float *dW, float *db, float *loss);
+
 }  // namespace ckpt

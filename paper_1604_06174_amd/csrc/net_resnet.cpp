@@ -1,8 +1,244 @@
-// CIFAR-shaped residual CNN (placeholder until its kernels land).
+// CIFAR-shaped residual CNN chain (fp32, NHWC).
+//   unit 0      stem: conv3x3 3 -> C0, BN, ReLU
+//   units 1..   basic blocks: conv3x3(stride s) - BN - ReLU - conv3x3 - BN,
+//               + shortcut (identity, or option A: subsample by 2 and append
+//               zero channels), ReLU; three stages of C0, 2 C0, 4 C0 channels,
+//               the first block of stages 2 and 3 has stride 2
+//   head        global average pool, FC, softmax cross-entropy over the batch
+// This is the convolution / batch-norm / activation pipeline of the paper's
+// section 4.2 arranged as a residual network (section 5.2).
+//
+// Static layout per unit (T = one [N, Ho, Ho, Cout] f32 tensor, SB = a BN
+// mean/rstd pair of Cout floats each, both rounded up to 256 bytes):
+//   stem   a = c | st            q = dc
+//   block  a = c1 | r1 | c2 | st1 | st2     q = two T buffers
+// The boundary b_i is the unit's input tensor (b_0 = the image batch).
+#include <algorithm>
+
+#include "kernels.h"
 #include "net.h"
 
 namespace ckpt {
-std::unique_ptr<Net> make_resnet_basic_net(const ckpt_net_desc &) {
-  fail(CKPT_E_UNSUPPORTED, "net_create: RESNET_BASIC is not built yet");
+namespace {
+
+struct Blk {
+  int cin, cout, stride, hin, hout;
+  int w1, g1, b1, w2, g2, b2;  // parameter indices (stem: w1, g1, b1)
+};
+
+class ResNetBasic : public Net {
+ public:
+  int N, S, C0, K, nb;
+  std::vector<Blk> u;
+  int hw, hb;  // head parameter indices
+  // operator workspace offsets (bytes)
+  uint64_t ks_loss = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0, ks_pooled = 0, ks_dlog = 0,
+           ks_lossn = 0;
+
+  explicit ResNetBasic(const ckpt_net_desc &d) {
+    desc = d;
+    N = d.batch;
+    S = d.image;
+    C0 = d.width;
+    K = d.n_classes;
+    nb = d.depth;
+    auto T = [&](int h, int c) { return align256(uint64_t(N) * h * h * c * 4); };
+    b.push_back(align256(uint64_t(N) * S * S * 3 * 4));
+    {
+      Blk s{3, C0, 1, S, S, 0, 0, 0, -1, -1, -1};
+      s.w1 = add_param("u0.W", uint64_t(C0) * 9 * 3);
+      s.g1 = add_param("u0.gamma", C0);
+      s.b1 = add_param("u0.beta", C0);
+      u.push_back(s);
+      a.push_back(T(S, C0) + align256(8ull * C0));
+      q.push_back(T(S, C0));
+      b.push_back(T(S, C0));
+    }
+    int cin = C0, side = S;
+    for (int st = 0; st < 3; ++st) {
+      const int cout = C0 << st;
+      for (int j = 0; j < nb; ++j) {
+        const int stride = (st > 0 && j == 0) ? 2 : 1;
+        const int i = int(u.size());
+        const std::string p = "u" + std::to_string(i) + ".";
+        Blk k{cin, cout, stride, side, side / stride, 0, 0, 0, 0, 0, 0};
+        k.w1 = add_param(p + "W1", uint64_t(cout) * 9 * cin);
+        k.g1 = add_param(p + "gamma1", cout);
+        k.b1 = add_param(p + "beta1", cout);
+        k.w2 = add_param(p + "W2", uint64_t(cout) * 9 * cout);
+        k.g2 = add_param(p + "gamma2", cout);
+        k.b2 = add_param(p + "beta2", cout);
+        u.push_back(k);
+        const uint64_t t = T(k.hout, cout);
+        a.push_back(3 * t + 2 * align256(8ull * cout));
+        q.push_back(2 * t);
+        b.push_back(t);
+        cin = cout;
+        side = k.hout;
+      }
+    }
+    hw = add_param("head.W", uint64_t(cin) * K);
+    hb = add_param("head.b", uint64_t(K));
+    n = int32_t(u.size());
+
+    // operator workspace: the largest partial-sum buffers any unit needs
+    uint64_t bnpart = 0, wpart = 0;
+    for (const Blk &k : u) {
+      const int64_t np = int64_t(N) * k.hout * k.hout;
+      const int conv_in[2] = {k.cin, k.cout};
+      const int conv_s[2] = {k.stride, 1};
+      for (int c = 0; c < (k.w2 >= 0 ? 2 : 1); ++c) {
+        bnpart = std::max<uint64_t>(
+            bnpart, uint64_t(conv3x3_blocks(CONV_FWD, conv_s[c], N, k.hout, k.hout, conv_in[c], k.cout)) *
+                        2 * k.cout * 8);
+        wpart = std::max<uint64_t>(
+            wpart, uint64_t(conv3x3_wgrad_blocks(conv_s[c], N, k.hout, k.hout, conv_in[c], k.cout)) *
+                       k.cout * 9 * conv_in[c] * 4);
+      }
+      bnpart = std::max<uint64_t>(bnpart, uint64_t(bn_partial_blocks(np, k.cout)) * 2 * k.cout * 8);
+    }
+    const int CL = u.back().cout;
+    uint64_t off = 0;
+    auto take = [&](uint64_t bytes) {
+      uint64_t o = off;
+      off += align256(bytes);
+      return o;
+    };
+    ks_loss = take(4);
+    ks_bnpart = take(bnpart);
+    ks_sums = take(8ull * (C0 << 2));
+    ks_wpart = take(wpart);
+    ks_pooled = take(4ull * N * CL);
+    ks_dlog = take(4ull * N * K);
+    ks_lossn = take(4ull * N);
+    ks_bytes = off;
+  }
+
+  double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
+  float *ksf(StepCtx &c, uint64_t off) const { return reinterpret_cast<float *>(c.ks + off); }
+
+  void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
+    const Blk &k = u[size_t(i)];
+    const float *x = static_cast<const float *>(xv);
+    float *y = static_cast<float *>(yv);
+    char *sv = static_cast<char *>(saved);
+    const uint64_t t = align256(uint64_t(N) * k.hout * k.hout * k.cout * 4);
+    const int64_t np = int64_t(N) * k.hout * k.hout;
+    if (k.w2 < 0) {  // stem
+      float *cv = reinterpret_cast<float *>(sv);
+      float *st = reinterpret_cast<float *>(sv + t);
+      conv3x3(c.s, CONV_FWD, 1, CONV_EPI_STATS, x, P(c, k.w1), cv, N, S, S, S, S, 3, C0, nullptr,
+              nullptr, 0, 0, 0, bnpart(c));
+      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st);
+      bn_apply(c.s, BN_RES_NONE, np, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, y);
+      c.launches += 3;
+      return;
+    }
+    float *c1 = reinterpret_cast<float *>(sv);
+    float *r1 = reinterpret_cast<float *>(sv + t);
+    float *c2 = reinterpret_cast<float *>(sv + 2 * t);
+    const uint64_t sb = align256(8ull * k.cout);
+    float *st1 = reinterpret_cast<float *>(sv + 3 * t);
+    float *st2 = reinterpret_cast<float *>(sv + 3 * t + sb);
+    const int ho = k.hout;
+    conv3x3(c.s, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, N, ho, ho, k.hin, k.hin,
+            k.cin, k.cout, nullptr, nullptr, 0, 0, 0, bnpart(c));
+    bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
+                    k.cout, np, st1);
+    bn_apply(c.s, BN_RES_NONE, np, k.cout, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, r1);
+    conv3x3(c.s, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, N, ho, ho, ho, ho, k.cout, k.cout,
+            nullptr, nullptr, 0, 0, 0, bnpart(c));
+    bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
+                    np, st2);
+    bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),
+             P(c, k.b2), x, ho, ho, k.cin, y);
+    c.launches += 6;
+  }
+
+  void bwd(int32_t i, const void *gv, void *dxv, const void *xv, const void *yv, const void *saved,
+           void *qv, StepCtx &c) override {
+    const Blk &k = u[size_t(i)];
+    const float *g = static_cast<const float *>(gv);
+    const float *x = static_cast<const float *>(xv);
+    const float *y = static_cast<const float *>(yv);
+    const char *sv = static_cast<const char *>(saved);
+    const uint64_t t = align256(uint64_t(N) * k.hout * k.hout * k.cout * 4);
+    const int64_t np = int64_t(N) * k.hout * k.hout;
+    float *sums = ksf(c, ks_sums);
+    float *wpart = ksf(c, ks_wpart);
+    if (k.w2 < 0) {  // stem: no input gradient
+      const float *cv = reinterpret_cast<const float *>(sv);
+      const float *st = reinterpret_cast<const float *>(sv + t);
+      float *dc = static_cast<float *>(qv);
+      bn_backward(c.s, np, C0, g, y, cv, st, P(c, k.g1), bnpart(c), sums, G(c, k.g1), G(c, k.b1), dc);
+      conv3x3_wgrad(c.s, 1, x, dc, wpart, G(c, k.w1), N, S, S, S, S, 3, C0);
+      c.launches += 5;
+      return;
+    }
+    const float *c1 = reinterpret_cast<const float *>(sv);
+    const float *r1 = reinterpret_cast<const float *>(sv + t);
+    const float *c2 = reinterpret_cast<const float *>(sv + 2 * t);
+    const uint64_t sb = align256(8ull * k.cout);
+    const float *st1 = reinterpret_cast<const float *>(sv + 3 * t);
+    const float *st2 = reinterpret_cast<const float *>(sv + 3 * t + sb);
+    float *Pb = static_cast<float *>(qv);
+    float *Qb = reinterpret_cast<float *>(static_cast<char *>(qv) + t);
+    const int ho = k.hout;
+    // second BN (its input gradient is g masked by the block's final ReLU)
+    bn_backward(c.s, np, k.cout, g, y, c2, st2, P(c, k.g2), bnpart(c), sums, G(c, k.g2), G(c, k.b2), Qb);
+    // conv2: data gradient masked by the first ReLU, and weight gradient
+    conv3x3(c.s, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, N, ho, ho, ho, ho, k.cout, k.cout,
+            r1);
+    conv3x3_wgrad(c.s, 1, r1, Qb, wpart, G(c, k.w2), N, ho, ho, ho, ho, k.cout, k.cout);
+    // first BN
+    bn_backward(c.s, np, k.cout, Pb, nullptr, c1, st1, P(c, k.g1), bnpart(c), sums, G(c, k.g1),
+                G(c, k.b1), Qb);
+    c.launches += 9;
+    if (dxv) {  // conv1 data gradient plus the shortcut's gradient
+      conv3x3(c.s, CONV_DGRAD, k.stride, k.stride == 1 ? CONV_EPI_SC1 : CONV_EPI_SC2, Qb, P(c, k.w1),
+              static_cast<float *>(dxv), N, k.hin, k.hin, ho, ho, k.cout, k.cin, g, y, ho, ho, k.cout);
+      c.launches += 1;
+    }
+    conv3x3_wgrad(c.s, k.stride, x, Qb, wpart, G(c, k.w1), N, ho, ho, k.hin, k.hin, k.cin, k.cout);
+    c.launches += 2;
+  }
+
+  void head(const void *xn, void *g, StepCtx &c) override {
+    const Blk &k = u.back();
+    pool_fc_ce_head(c.s, N, k.hout * k.hout, k.cout, K, static_cast<const float *>(xn), P(c, hw),
+                    P(c, hb), static_cast<const int *>(c.target), ksf(c, ks_pooled),
+                    ksf(c, ks_dlog), ksf(c, ks_lossn), static_cast<float *>(g), G(c, hw),
+                    G(c, hb), ksf(c, ks_loss));
+    c.launches += 2;
+  }
+
+  const float *loss_ptr(const StepCtx &c) const override {
+    return reinterpret_cast<const float *>(c.ks + ks_loss);
+  }
+};
+
+bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+}  // namespace
+
+std::unique_ptr<Net> make_resnet_basic_net(const ckpt_net_desc &d) {
+  if (d.batch <= 0 || d.depth <= 0 || d.width <= 0 || d.image <= 0 || d.n_classes <= 0)
+    fail(CKPT_E_INVALID, "net_create: RESNET_BASIC needs positive batch, depth, width, image, classes");
+  if (d.width % 4 != 0 || !pow2(d.width / 4) || (d.width << 2) > 1024)
+    fail(CKPT_E_UNSUPPORTED, "net_create: RESNET_BASIC width must be 4 * 2^k and at most 256");
+  if (d.image % 4 != 0)
+    fail(CKPT_E_INVALID, "net_create: RESNET_BASIC image side must be a multiple of 4");
+  if (int64_t(d.batch) * d.image * d.image * (d.width << 2) > (int64_t(1) << 31))
+    fail(CKPT_E_INVALID, "net_create: RESNET_BASIC tensors too large");
+  for (int st = 0; st < 3; ++st) {
+    const int cout = d.width << st, side = d.image >> st;
+    const int cin = st == 0 ? d.width : cout / 2;
+    if (!conv3x3_supported(CONV_FWD, st == 0 ? 1 : 2, side, side, cin, cout) ||
+        !conv3x3_supported(CONV_FWD, 1, side, side, cout, cout) ||
+        !conv3x3_supported(CONV_DGRAD, st == 0 ? 1 : 2, side << (st ? 1 : 0), side << (st ? 1 : 0), cout, cin))
+      fail(CKPT_E_UNSUPPORTED, "net_create: RESNET_BASIC shape outside the conv kernels' tiling");
+  }
+  return std::make_unique<ResNetBasic>(d);
 }
+
 }  // namespace ckpt

@@ -93,7 +93,10 @@ def test_planner_errors(args, code):
 
 WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
                  dict(kind="mlp", depth=1024, width=1024, batch=256),
-                 dict(kind="mlp", depth=7, width=40, batch=3)]
+                 dict(kind="mlp", depth=7, width=40, batch=3),
+                 dict(kind="resnet_basic", blocks_per_stage=18, base=16, batch=128, image=32,
+                      classes=10),
+                 dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=3, image=12, classes=5)]
 
 
 @pytest.mark.parametrize("cfg", WORKLOADS_CPU)
@@ -118,9 +121,11 @@ def test_net_tables_and_accounting_match_oracle(cfg):
         assert net.workspace_bytes(lp) >= acc["peak"]
 
 
-def test_param_layout_names_match_structure():
+@pytest.mark.parametrize("cfg", [dict(kind="mlp", depth=5, width=40, batch=3),
+                                 dict(kind="resnet_basic", blocks_per_stage=3, base=8, batch=2,
+                                      image=16, classes=7)])
+def test_param_layout_names_match_structure(cfg):
     from paper_1604_06174_amd.workload import net_for
-    cfg = dict(kind="mlp", depth=5, width=40, batch=3)
     net = net_for(cfg)
     names = [nm for nm, _, _ in net.param_layout()]
     assert names == [nm for nm, _, _ in synth.structure(cfg).param_list()]

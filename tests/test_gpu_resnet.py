@@ -1,0 +1,77 @@
+"""GPU parity of the CIFAR-shaped residual CNN checkpointed step.
+
+Small networks (several tiles, ragged spatial tails) are compared with the
+float64 oracle at the strict bar, max |gpu - oracle| / max |oracle| <= 1e-4 per
+tensor, for every plan mode; each case first checks that it is well posed at
+float32 (the oracle's own float32 run is within 2e-5 of its float64 run, i.e.
+no ReLU decision sits inside the float32 rounding band).  Every plan must
+give the same gradient bytes as the no-checkpoint run, the oracle's peak bytes
+and unit-forward count.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import nets, planner as PL, sizes as SZ, units as U
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _err(g, o):
+    g = np.asarray(g, np.float64).reshape(-1)
+    o = np.asarray(o, np.float64).reshape(-1)
+    return float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-30))
+
+
+def _oracle(d, prec=U.F64):
+    chain = nets.Chain(d["structure"], d["params"], prec)
+    return nets.full_storage_step(chain, d["input"], d["target"])
+
+
+CASES = {
+    "tiny": dict(kind="resnet_basic", blocks_per_stage=1, base=4, batch=2, image=8, classes=5, seed=61),
+    "ragged": dict(kind="resnet_basic", blocks_per_stage=2, base=8, batch=3, image=12, classes=7, seed=62),
+    "cifar_channels": dict(kind="resnet_basic", blocks_per_stage=2, base=16, batch=4, image=32,
+                           classes=10, seed=63),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_resnet_step_parity_all_modes(case):
+    import torch
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = CASES[case]
+    print(f"[resnet parity] case={case} cfg={cfg}", flush=True)
+    d = synth.make(cfg)
+    loss_o, grads_o = _oracle(d)
+    _, grads_32 = _oracle(d, U.Prec(np.float32))
+    cond = max(_err(grads_32[k], grads_o[k]) for k in grads_o)
+    assert cond < 2e-5, f"case not well posed at float32 ({cond:.2e})"
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    st = d["structure"]
+    b, a, q = SZ.tables(st)
+    lb, cb = SZ.layer_and_cut_bytes(st)
+    n = st.n
+    modes = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
+             ("sqrt_keep", PL.SQRT, 0, None, PL.FLAG_KEEP_LAST),
+             ("greedy", PL.GREEDY, sum(lb) // 4, None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
+             ("user", PL.USER, 0, [0, n - 2], 0)]
+    ref = None
+    for name, mode, budget, user, flags in modes:
+        plan = step.plan(mode, budget, user, flags)
+        step.grads.fill_(float("nan"))
+        loss, peak, stats = step.run(plan)
+        torch.cuda.synchronize()
+        op = PL.plan(n, lb, cb, budget, mode, user, flags)
+        assert peak == PL.account(op, b, a, q).peak, name
+        assert stats["unit_forwards"] == PL.unit_forwards(op), name
+        assert abs(loss - loss_o) <= TOL * abs(loss_o), (name, loss, loss_o)
+        g = step.grads_host()
+        worst = max((_err(g[k], v), k) for k, v in grads_o.items())
+        assert worst[0] <= TOL, (name, worst)
+        gb = step.grads_bytes()
+        if ref is None:
+            ref = gb
+        assert gb == ref, f"{name}: gradients differ from the no-checkpoint run"

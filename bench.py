@@ -1,0 +1,187 @@
+#!/usr/bin/env python3
+"""Benchmark of the checkpointed training step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload cifar110]
+
+Default workload: the CIFAR-shaped 110-layer residual CNN (stem + 3 x 18 basic
+blocks, batch 128, fp32) with the sqrt(n) schedule (section 4.3).  A step is
+one whole checkpointed train step: forward keeping only segment boundaries,
+loss head, and for every segment in reverse its forward re-run followed by its
+backward, producing every gradient.  Inputs are seeded synthetic tensors
+already resident in HBM.
+
+Printed (one JSON line): samples/s of the checkpointed step, its peak
+activation bytes (exact, from the static layout), the recompute overhead
+(step time / the same kernels without checkpointing), the dominant kernel's
+roofline position from HIP events recorded around its launches in a second
+timed pass, and the CPU oracle's checkpointed step on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "checkpointed train-step samples/s + peak activation GB + recompute overhead ×"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+HBM_GBS = 8000.0
+
+
+def _plan_args(cfg, net):
+    from paper_1604_06174_amd import ckpt as K
+    lb, _ = net.layer_sizes()
+    mode = cfg.get("plan", "sqrt")
+    if mode == "sqrt":
+        return K.SQRT, int(cfg.get("stride", 0)), "sqrt"
+    if mode == "greedy":
+        return K.GREEDY, int(sum(lb) * cfg.get("budget_frac", 0.1)), "greedy"
+    if mode == "recursive":
+        return K.RECURSIVE, 0, "recursive"
+    raise ValueError(mode)
+
+
+def _cpu_baseline(cfg, sample_batch):
+    """The oracle's own checkpointed executor (Alg. 1 with the same plan) on a
+    smaller batch of the same network; samples/s = sample batch / wall time."""
+    import numpy as np
+    import synth
+    from oracle import nets, planner as PL, schedule as SCH, sizes as SZ
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()
+                       if t.get("internal_api") in ("openblas", "mkl", "blis")] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    c = dict(cfg)
+    c["batch"] = sample_batch
+    d = synth.make(c)
+    chain = nets.Chain(d["structure"], d["params"])
+    lb, cb = SZ.layer_and_cut_bytes(d["structure"])
+    n = d["structure"].n
+    mode = {"sqrt": PL.SQRT, "greedy": PL.GREEDY, "recursive": PL.RECURSIVE}[cfg.get("plan", "sqrt")]
+    budget = int(cfg.get("stride", 0)) if mode == PL.SQRT else int(sum(lb) * cfg.get("budget_frac", 0.1))
+    t0 = time.perf_counter()
+    if mode == PL.RECURSIVE:
+        SCH.recursive_step(chain, d["input"], d["target"])
+    else:
+        SCH.segment_step(chain, d["input"], d["target"], PL.plan(n, lb, cb, budget, mode))
+    dt = time.perf_counter() - t0
+    return {"value": sample_batch / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one float64 NumPy checkpointed step (same plan) of the same network on "
+                      f"{sample_batch} of its {cfg['batch']} samples; {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="cifar110")
+    ap.add_argument("--cpu-sample", type=int, default=128, help="batch of the CPU oracle sample (0: skip)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the checkpointed step is "
+                                   "measured per device; multi-GPU sharding is not built",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    from paper_1604_06174_amd import ckpt as K
+    from paper_1604_06174_amd.workload import GpuStep
+
+    cfg = dict(synth.WORKLOADS[args.workload])
+    d = synth.make(cfg)
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    mode, budget, mode_name = _plan_args(cfg, step.net)
+    plan = step.plan(mode, budget)
+    none = step.plan(K.NONE)
+    acc = step.net.accounting(plan)
+    acc_none = step.net.accounting(none)
+    step.workspace(none)  # the larger workspace serves both plans
+    s = torch.cuda.current_stream()
+
+    def run(p, k):
+        st = None
+        for _ in range(k):
+            _, _, st = step.run(p, stream=s, want_loss=False)
+        return st
+
+    stats = run(plan, args.warmup)
+    run(none, args.warmup)
+    torch.cuda.synchronize()
+
+    def timed(p):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s)
+        run(p, args.steps)
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    ms = timed(plan)
+    ms_none = timed(none)
+    loss = float(step.loss_dev.item())
+
+    # second timed pass: HIP events around every launch of the dominant kernel
+    step.net.timing_enable(True)
+    run(plan, args.steps)
+    torch.cuda.synchronize()
+    kt = step.net.timing_read()
+    step.net.timing_enable(False)
+
+    dtype = cfg.get("dtype", "f32")
+    achieved = kt["flops"] / (kt["ms"] / 1e3) / 1e12 if kt["ms"] > 0 else 0.0
+    peak = PEAK_TFLOPS[dtype]
+    roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "kernel": kt["kernel"], "launches": kt["launches"],
+            "avg_launch_us": round(kt["ms"] * 1e3 / max(kt["launches"], 1), 3),
+            "flops_per_launch": kt["flops"] / max(kt["launches"], 1),
+            "hbm_gbs_algorithmic": round(kt["bytes"] / (kt["ms"] / 1e3) / 1e9, 1) if kt["ms"] > 0 else 0}
+
+    cpu = None
+    if args.cpu_sample > 0:
+        cpu = _cpu_baseline(cfg, min(args.cpu_sample, cfg["batch"]))
+
+    batch = cfg["batch"]
+    out = {
+        "metric": METRIC,
+        "value": round(batch / (ms / 1e3), 3),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": args.workload, "kind": cfg["kind"], "batch": batch,
+                   "units": step.net.n, "plan": mode_name,
+                   "stride_or_budget": budget, "cuts": len(plan.cuts())},
+        "peak_activation_gb": round(acc["peak"] / 1e9, 6),
+        "peak_activation_gb_no_ckpt": round(acc_none["peak"] / 1e9, 6),
+        "recompute_overhead_x": round(ms / ms_none, 4),
+        "ms_per_step_no_ckpt": round(ms_none, 4),
+        "unit_forwards_per_step": stats["unit_forwards"],
+        "kernel_launches_per_step": stats["kernel_launches"],
+        "loss": loss,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -222,6 +222,21 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
                const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
 
+/*
+ * Kernel timing for benchmarks.  net_timing_enable(net, 1) makes every later
+ * train_step bracket each launch of the net's dominant kernel family (the
+ * conv3x3 forward / data-gradient kernel of RESNET_BASIC, the GEMM of MLP)
+ * with a pair of HIP events on the step's stream, and resets the totals;
+ * 0 turns it off.  net_timing_read synchronises on the recorded events and
+ * returns, since the last enable: the launches timed, their summed duration
+ * (ms), their summed algorithmic flops and bytes (each operand read once, each
+ * result written once), and the family's kernel-name prefix (host name[cap]).
+ * The events add a little time to each step: time throughput separately.
+ */
+int net_timing_enable(ckpt_net *net, int32_t enable);
+int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops, double *bytes,
+                    char *name, int32_t cap);
+
 /* ckpt_last_error -- message of the last failed call on this thread ("" if
  * none). */
 const char *ckpt_last_error(void);

@@ -71,6 +71,9 @@ _sig("net_param_count", C.c_int, [C.c_void_p, _i32p])
 _sig("net_param_info", C.c_int, [C.c_void_p, C.c_int32, C.c_char_p, C.c_int32, _u64p, _u64p])
 _sig("plan_accounting", C.c_int, [C.c_void_p, C.c_void_p, _u64p, _u64p, _u64p, _u64p])
 _sig("net_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
+_sig("net_timing_enable", C.c_int, [C.c_void_p, C.c_int32])
+_sig("net_timing_read", C.c_int, [C.c_void_p, _u64p, C.POINTER(C.c_double), C.POINTER(C.c_double),
+                                  C.POINTER(C.c_double), C.c_char_p, C.c_int32])
 _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
                              C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
                              C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
@@ -78,7 +81,8 @@ _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch
 EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
             "plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_param_bytes", "net_param_count", "net_param_info",
-            "plan_accounting", "net_workspace_bytes", "train_step"]
+            "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
+            "train_step"]
 
 
 class CkptError(RuntimeError):
@@ -215,6 +219,18 @@ class Net:
         v = C.c_uint64()
         _check(_lib.net_workspace_bytes(self._h, plan.handle, C.byref(v)))
         return v.value
+
+    def timing_enable(self, on: bool = True):
+        _check(_lib.net_timing_enable(self._h, 1 if on else 0))
+
+    def timing_read(self) -> Dict:
+        n = C.c_uint64()
+        ms, fl, by = C.c_double(), C.c_double(), C.c_double()
+        name = C.create_string_buffer(64)
+        _check(_lib.net_timing_read(self._h, C.byref(n), C.byref(ms), C.byref(fl), C.byref(by),
+                                    name, 64))
+        return dict(launches=n.value, ms=ms.value, flops=fl.value, bytes=by.value,
+                    kernel=name.value.decode())
 
     def __del__(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -233,4 +233,32 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
   });
 }
 
+int net_timing_enable(ckpt_net *net, int32_t enable) {
+  return guarded([&] {
+    need(net, "net_timing_enable");
+    auto &t = net->net->timer;
+    t.reset();
+    t.enabled = enable != 0;
+  });
+}
+
+int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops, double *bytes,
+                    char *name, int32_t cap) {
+  return guarded([&] {
+    need(net, "net_timing_read");
+    auto &t = net->net->timer;
+    t.harvest();
+    if (launches) *launches = t.launches;
+    if (ms) *ms = t.ms;
+    if (flops) *flops = t.flops;
+    if (bytes) *bytes = t.bytes;
+    if (name && cap > 0) {
+      const std::string &f = net->net->timed_family;
+      size_t k = std::min(size_t(cap - 1), f.size());
+      std::memcpy(name, f.data(), k);
+      name[k] = 0;
+    }
+  });
+}
+
 }  // extern "C"

@@ -224,94 +224,173 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
 }
 
 // ---------------------------------------------------------------- wgrad --
+// dW[j][n] = sum_p dy[p][j] * col[p][n],  n = tap*C + c, col = im2col(x)
+// (M = J, N = 9C, K = N*Ho*Wo pixels).  Workgroup = one 144-column slice of
+// n (9 MFMA column tiles) x all J rows x a contiguous pixel range; its four
+// wavefronts split the J row tiles (up to 4) and, when J < 64, the pixel
+// range (reduced through LDS in a fixed order at the end).  Pixel chunks of 32
+// are staged in double-buffered LDS: dy rows (float4 along j) and the gathered
+// im2col rows (float4 along c).  Each workgroup writes one partial dW slice;
+// k_sum_partials adds the partials of all pixel ranges in a fixed order.
+constexpr int WG_KC = 32;    // pixels per LDS chunk
+constexpr int WG_NB = 144;   // n columns per workgroup (9 tiles of 16)
+
 struct WgArgs {
   const float *X;   // conv input [N, Hx, Wx, C]
   const float *DY;  // conv output gradient [N, H, W, J]
-  float *part;      // [gridDim.x][J][9][C]
-  int N, H, W, Hx, Wx, C, J, R, rblk, S;
+  float *part;      // [gridDim.x][J][9C]
+  int N, H, W, Hx, Wx, C, J, S;
+  int pix_per_blk;  // multiple of WG_KC
 };
 
-template <int GB>
+__device__ __forceinline__ int wg_as(int J) { return J + ((16 - J % 32) + 32) % 32; }  // == 16 mod 32
+
 __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
   extern __shared__ __align__(16) float smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
-  const int blk = blockIdx.x;
-  const int n = blk / a.rblk, r0 = (blk % a.rblk) * a.R;
-  const int S = a.S;
-  const int Cp = cpad4(a.C), Cs = Cp + 4;
-  const int HR = (a.R - 1) * S + 3, HC = (a.W - 1) * S + 3;
-  const int npix = a.R * a.W;
-  const int npix4 = (npix + 3) & ~3;
-  const int Js = ((a.J + 15) & ~15) + 4;
-  float *halo = smem;
-  float *dys = smem + HR * HC * Cs;  // [npix4][Js]
+  const int J = a.J, C = a.C, NC = 9 * C;
+  const int jt_n = (J + 15) / 16;                  // j tiles (1..4)
+  const int wgj = jt_n < 4 ? jt_n : 4;            // wavefronts across j tiles
+  const int wgk = 4 / wgj;                         // wavefronts across pixels
+  const int my_jt = wave % wgj, my_kg = wave / wgj;
+  const int AS = wg_as(jt_n * 16);                // dy row stride in LDS
+  constexpr int BS = WG_NB;                       // == 16 mod 32
+  float *Abuf = smem;                              // [2][KC][AS]
+  float *Bbuf = smem + 2 * WG_KC * AS;             // [2][KC][BS]
+  const int n0 = blockIdx.y * WG_NB;
+  const int64_t P = int64_t(a.N) * a.H * a.W;
+  const int64_t p0 = int64_t(blockIdx.x) * a.pix_per_blk;
+  const int nchunk = a.pix_per_blk / WG_KC;
 
-  {
-    const int cq = Cp / 4;
-    for (int e = tid; e < HR * HC * cq; e += 256) {
-      const int c4 = (e % cq) * 4, hc = (e / cq) % HC, hr = e / (cq * HC);
-      const int ir = r0 * S - 1 + hr, ic = hc - 1;
-      float v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (ir >= 0 && ir < a.Hx && ic >= 0 && ic < a.Wx) {
-        const float *src = a.X + ((size_t(n) * a.Hx + ir) * a.Wx + ic) * a.C + c4;
-        if ((a.C & 3) == 0) {
-          float4 t = *reinterpret_cast<const float4 *>(src);
-          v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-        } else {
+  // staging: A = dy[p][0..16*jt_n) as float4, B = im2col[p][n0..n0+144) as float4
+  const int a4 = jt_n * 4;          // float4 per dy row
+  const int b4 = WG_NB / 4;         // 36 float4 per im2col row
+  const int na = WG_KC * a4, nbq = WG_KC * b4;
+  constexpr int MAXA = 2, MAXB = 5;  // per thread: na <= 512, nbq = 1152
+  float4 ra[MAXA], rb[MAXB];
+  auto gload = [&](int ck) {
+    const int64_t pc = p0 + int64_t(ck) * WG_KC;
 #pragma unroll
-          for (int k = 0; k < 4; ++k) v[k] = (c4 + k < a.C) ? src[k] : 0.f;
+    for (int k = 0; k < MAXA; ++k) {
+      const int e = tid + k * 256;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (e < na) {
+        const int pl = e / a4, j4 = (e % a4) * 4;
+        const int64_t p = pc + pl;
+        if (p < P && j4 < J) v = *reinterpret_cast<const float4 *>(a.DY + p * J + j4);
+      }
+      ra[k] = v;
+    }
+#pragma unroll
+    for (int k = 0; k < MAXB; ++k) {
+      const int e = tid + k * 256;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (e < nbq) {
+        const int pl = e / b4, nn = n0 + (e % b4) * 4;
+        const int64_t p = pc + pl;
+        if (p < P && nn < NC) {
+          const int ow = int(p % a.W);
+          const int64_t t = p / a.W;
+          const int oh = int(t % a.H), img = int(t / a.H);
+          if ((C & 3) == 0) {  // the 4 columns are 4 channels of one tap
+            const int tap = nn / C, c = nn % C;
+            const int ih = oh * a.S + tap / 3 - 1, iw = ow * a.S + tap % 3 - 1;
+            if (ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
+              v = *reinterpret_cast<const float4 *>(a.X + ((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c);
+          } else {
+            float vv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int n = nn + u;
+              const int tap = n / C, c = n % C;
+              const int ih = oh * a.S + tap / 3 - 1, iw = ow * a.S + tap % 3 - 1;
+              vv[u] = (n < NC && ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
+                          ? a.X[((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c]
+                          : 0.f;
+            }
+            v = make_float4(vv[0], vv[1], vv[2], vv[3]);
+          }
         }
       }
-      *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = make_float4(v[0], v[1], v[2], v[3]);
+      rb[k] = v;
     }
-    for (int e = tid; e < npix4 * Js; e += 256) {
-      const int p = e / Js, j = e % Js;
-      const int h = r0 + p / a.W, w = p % a.W;
-      float v = 0.f;
-      if (p < npix && h < a.H && j < a.J) v = a.DY[((size_t(n) * a.H + h) * a.W + w) * a.J + j];
-      dys[e] = v;
-    }
-  }
-  __syncthreads();
-
-  const int jsub = (a.J + 15) / 16, csub = (Cp + 15) / 16;
-  const int ngroups = jsub * 9 * csub;  // group = (j subtile, tap, c subtile)
-  for (int g0 = wave; g0 < ngroups; g0 += 4 * GB) {
-    floatx4 acc[GB];
-    int gj[GB], gt[GB], gc[GB];
+  };
+  auto sstore = [&](int buf) {
 #pragma unroll
-    for (int k = 0; k < GB; ++k) {
-      acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
-      int g = g0 + 4 * k;
-      if (g >= ngroups) g = ngroups - 1;  // computed, not stored
-      gj[k] = g / (9 * csub);
-      gt[k] = (g / csub) % 9;
-      gc[k] = g % csub;
-    }
-    for (int p0 = 0; p0 < npix4; p0 += 4) {
-      const int p = p0 + q;
-      const int pp = p < npix ? p : npix - 1;  // its dy row is zero
-      const int rr = pp / a.W, cc = pp % a.W;
-#pragma unroll
-      for (int k = 0; k < GB; ++k) {
-        const float av = dys[p * Js + gj[k] * 16 + i16];
-        const int kh = gt[k] / 3, kw = gt[k] % 3;
-        const int c = gc[k] * 16 + i16;
-        const float bv = c < Cp ? halo[((rr * S + kh) * HC + (cc * S + kw)) * Cs + c] : 0.f;
-        acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[k], 0, 0, 0);
+    for (int k = 0; k < MAXA; ++k) {
+      const int e = tid + k * 256;
+      if (e < na) {
+        const int pl = e / a4, j4 = (e % a4) * 4;
+        *reinterpret_cast<float4 *>(Abuf + (buf * WG_KC + pl) * AS + j4) = ra[k];
       }
     }
 #pragma unroll
-    for (int k = 0; k < GB; ++k) {
-      const int g = g0 + 4 * k;
-      if (g >= ngroups) continue;
-      const int c = gc[k] * 16 + i16;
+    for (int k = 0; k < MAXB; ++k) {
+      const int e = tid + k * 256;
+      if (e < nbq) {
+        const int pl = e / b4, nc4 = (e % b4) * 4;
+        *reinterpret_cast<float4 *>(Bbuf + (buf * WG_KC + pl) * BS + nc4) = rb[k];
+      }
+    }
+  };
+
+  floatx4 acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  gload(0);
+  const bool active = my_kg < wgk;  // with 3 j tiles one wavefront has no work
+  for (int ck = 0; ck < nchunk; ++ck) {
+    const int buf = ck & 1;
+    sstore(buf);
+    __syncthreads();
+    if (ck + 1 < nchunk) gload(ck + 1);
+    if (!active) continue;
+    // this wavefront's pixels of the chunk: [my_kg * KC/wgk, (my_kg+1) * KC/wgk)
+    const int kb = my_kg * (WG_KC / wgk), ke = kb + WG_KC / wgk;
+    const float *Ab = Abuf + buf * WG_KC * AS + my_jt * 16 + i16;
+    const float *Bb = Bbuf + buf * WG_KC * BS + i16;
+    for (int k0 = kb; k0 < ke; k0 += 4) {
+      const float av = Ab[(k0 + q) * AS];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const float bv = Bb[(k0 + q) * BS + t * 16];
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t], 0, 0, 0);
+      }
+    }
+  }
+
+  // reduce the pixel groups of the same j tile in a fixed order (group 0 + 1 + ...)
+  if (wgk > 1) {
+    __syncthreads();
+    float *red = smem;  // [wave][9][4][64]
+    if (my_kg > 0) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[((wave * 9 + t) * 4 + r) * 64 + lane] = acc[t][r];
+    }
+    __syncthreads();
+    if (my_kg == 0) {
+      for (int g = 1; g < wgk; ++g) {
+        const int w2 = g * wgj + my_jt;
+#pragma unroll
+        for (int t = 0; t < 9; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[t][r] += red[((w2 * 9 + t) * 4 + r) * 64 + lane];
+      }
+    }
+  }
+  if (my_kg == 0 && active) {
+    float *dst = a.part + size_t(blockIdx.x) * J * NC;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int n = n0 + t * 16 + i16;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int j = gj[k] * 16 + 4 * q + r;
-        if (j < a.J && c < a.C)
-          a.part[((size_t(blk) * a.J + j) * 9 + gt[k]) * a.C + c] = acc[k][r];
+        const int j = my_jt * 16 + 4 * q + r;
+        if (j < J && n < NC) dst[size_t(j) * NC + n] = acc[t][r];
       }
     }
   }
@@ -352,14 +431,6 @@ size_t conv_lds(int mode, int S, int R, int W, int C, int J) {
   return (halo > red ? halo : red) + size_t(2) * Cp * BN * 4;
 }
 
-size_t wgrad_lds(int S, int R, int W, int C, int J) {
-  const int Cp = (C + 3) & ~3, Cs = Cp + 4;
-  const int HR = (R - 1) * S + 3, HC = (W - 1) * S + 3;
-  const int npix4 = (R * W + 3) & ~3;
-  const int Js = ((J + 15) & ~15) + 4;
-  return (size_t(HR) * HC * Cs + size_t(npix4) * Js) * 4;
-}
-
 // Whole output rows, at most 128 output pixels (8 MFMA row tiles) per
 // workgroup, shrunk until the LDS footprint fits.
 template <class Lds>
@@ -377,8 +448,22 @@ Tile conv_tile(int mode, int S, int H, int W, int C, int J) {
   return tile_for(H, W, [&](int R) { return conv_lds(mode, S, R, W, C, J); });
 }
 
-Tile wgrad_tile(int S, int H, int W, int C, int J) {
-  return tile_for(H, W, [&](int R) { return wgrad_lds(S, R, W, C, J); });
+// Pixels per weight-gradient workgroup: enough workgroups (columns x pixel
+// ranges) to give every compute unit about one, in whole LDS chunks.
+int wgrad_pix(int64_t P, int NC) {
+  const int ny = (NC + WG_NB - 1) / WG_NB;
+  int64_t want = 256 / ny;
+  if (want < 1) want = 1;
+  int64_t ppb = (P + want - 1) / want;
+  ppb = (ppb + WG_KC - 1) / WG_KC * WG_KC;
+  return int(ppb);
+}
+
+size_t wgrad_lds(int J) {
+  const int AS = (((J + 15) / 16) * 16) + ((16 - (((J + 15) / 16) * 16) % 32) + 32) % 32;
+  const size_t stage = size_t(2) * WG_KC * (AS + WG_NB) * 4;
+  const size_t red = size_t(4) * 9 * 4 * 64 * 4;
+  return stage > red ? stage : red;
 }
 
 template <int PSW, int NSUB, int MODE, int S>
@@ -410,7 +495,10 @@ int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J) {
 }
 
 int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J) {
-  return N * wgrad_tile(S, H, W, C, J).rblk;
+  (void)S;
+  const int64_t P = int64_t(N) * H * W;
+  const int ppb = wgrad_pix(P, 9 * C);
+  return int((P + ppb - 1) / ppb);
 }
 
 bool conv3x3_supported(int mode, int S, int H, int W, int C, int J) {
@@ -418,8 +506,7 @@ bool conv3x3_supported(int mode, int S, int H, int W, int C, int J) {
   if (((C + 3) & ~3) * BN > 2048) return false;  // per-tap weight staging
   if (W > 128) return false;                      // <= 2 row tiles per wavefront
   if (conv_lds(mode, S, conv_tile(mode, S, H, W, C, J).R, W, C, J) > kMaxLds) return false;
-  if (mode == CONV_FWD && wgrad_lds(S, wgrad_tile(S, H, W, C, J).R, W, C, J) > kMaxLds)
-    return false;
+  if (mode == CONV_FWD && (J > 64 || wgrad_lds(J) > kMaxLds)) return false;
   return true;
 }
 
@@ -442,12 +529,15 @@ void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const flo
 
 void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float *part, float *dW,
                    int N, int H, int W, int Hx, int Wx, int C, int J) {
-  Tile t = wgrad_tile(S, H, W, C, J);
-  WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, t.R, t.rblk, S};
-  const int nb = N * t.rblk;
-  hipLaunchKernelGGL((k_conv3x3_wgrad<4>), dim3(nb), dim3(256), wgrad_lds(S, t.R, W, C, J), st, a);
-  const int E = J * 9 * C;
-  hipLaunchKernelGGL(k_sum_partials, dim3((E + 15) / 16), dim3(256), 0, st, part, nb, E, dW);
+  const int64_t P = int64_t(N) * H * W;
+  const int NC = 9 * C;
+  const int ppb = wgrad_pix(P, NC);
+  const int nbx = int((P + ppb - 1) / ppb);
+  WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, S, ppb};
+  dim3 grid(nbx, (NC + WG_NB - 1) / WG_NB);
+  hipLaunchKernelGGL(k_conv3x3_wgrad, grid, dim3(256), wgrad_lds(J), st, a);
+  const int E = J * NC;
+  hipLaunchKernelGGL(k_sum_partials, dim3((E + 15) / 16), dim3(256), 0, st, part, nbx, E, dW);
 }
 
 }  // namespace ckpt

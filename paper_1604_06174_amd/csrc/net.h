@@ -11,6 +11,62 @@
 
 namespace ckpt {
 
+// Optional HIP-event timing of one kernel family (the net's dominant kernel):
+// every launch of the family is bracketed by an event pair on its stream;
+// durations are read back (synchronising) only when the totals are requested.
+struct KernelTimer {
+  bool enabled = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;
+  std::vector<double> fl, by;
+  size_t used = 0;
+  uint64_t launches = 0;
+  double ms = 0, flops = 0, bytes = 0;
+
+  void begin(hipStream_t s) {
+    if (!enabled) return;
+    if (used == pool.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) fail(CKPT_E_HIP, "hipEventCreate failed");
+      if (hipEventCreate(&b) != hipSuccess) fail(CKPT_E_HIP, "hipEventCreate failed");
+      pool.emplace_back(a, b);
+    }
+    (void)hipEventRecord(pool[used].first, s);
+  }
+  void end(hipStream_t s, double f, double b) {
+    if (!enabled) return;
+    (void)hipEventRecord(pool[used].second, s);
+    fl.push_back(f);
+    by.push_back(b);
+    ++used;
+  }
+  void harvest() {
+    for (size_t k = 0; k < used; ++k) {
+      float t = 0.f;
+      if (hipEventSynchronize(pool[k].second) != hipSuccess ||
+          hipEventElapsedTime(&t, pool[k].first, pool[k].second) != hipSuccess)
+        fail(CKPT_E_HIP, "kernel timing: event query failed");
+      ms += t;
+      flops += fl[k];
+      bytes += by[k];
+      ++launches;
+    }
+    used = 0;
+    fl.clear();
+    by.clear();
+  }
+  void reset() {
+    harvest();
+    launches = 0;
+    ms = flops = bytes = 0;
+  }
+  ~KernelTimer() {
+    for (auto &e : pool) {
+      (void)hipEventDestroy(e.first);
+      (void)hipEventDestroy(e.second);
+    }
+  }
+};
+
 // Everything a unit launcher needs besides its own tensors.
 struct StepCtx {
   hipStream_t s = nullptr;
@@ -35,6 +91,8 @@ class Net {
   std::vector<Tensor> params;
   uint64_t param_bytes = 0;
   uint64_t ks_bytes = 0;          // operator workspace (not part of the peak)
+  KernelTimer timer;              // times `timed_family` launches when enabled
+  std::string timed_family;       // kernel-name prefix of the timed family
 
   virtual ~Net() = default;
 

@@ -29,27 +29,41 @@ class MlpNet : public Net {
       bi.push_back(add_param("u" + std::to_string(i) + ".b", uint64_t(D)));
     }
     ks_bytes = 256;  // loss scalar
+    timed_family = "k_gemm_f32";
+  }
+
+  // algorithmic cost of one [M,K] x [K,N] product: operands read once,
+  // result written once (+ the epilogue's extra tensors)
+  static double gf(double M, double N, double K) { return 2.0 * M * N * K; }
+  static double gb(double M, double N, double K, double extra) {
+    return 4.0 * (M * K + K * N + M * N) + extra;
   }
 
   void fwd(int32_t i, const void *x, void *y, void *saved, StepCtx &c) override {
+    timer.begin(c.s);
     gemm_f32(c.s, B, D, D, static_cast<const float *>(x), D, false, P(c, wi[i]), D, false,
              static_cast<float *>(y), D, GEMM_EPI_MLPFWD, nullptr, 0, P(c, bi[i]),
              static_cast<float *>(saved), D);
+    timer.end(c.s, gf(B, D, D), gb(B, D, D, 4.0 * D + 4.0 * B * D));
     c.launches += 1;
   }
 
   void bwd(int32_t i, const void *g, void *dx, const void *x, const void *, const void *saved,
            void *q, StepCtx &c) override {
-    const float *gf = static_cast<const float *>(g);
+    const float *gp = static_cast<const float *>(g);
     float *dr = static_cast<float *>(q);
-    mlp_relu_bwd(c.s, B, D, gf, static_cast<const float *>(saved), dr, G(c, bi[i]));
+    mlp_relu_bwd(c.s, B, D, gp, static_cast<const float *>(saved), dr, G(c, bi[i]));
     // dW = x^T dr : [D_in, D_out] = [D, B] x [B, D]
+    timer.begin(c.s);
     gemm_f32(c.s, D, D, B, static_cast<const float *>(x), D, true, dr, D, false, G(c, wi[i]), D,
              GEMM_EPI_STORE);
+    timer.end(c.s, gf(D, D, B), gb(D, D, B, 0));
     c.launches += 2;
     if (dx) {  // dx = g + dr W^T
+      timer.begin(c.s);
       gemm_f32(c.s, B, D, D, dr, D, false, P(c, wi[i]), D, true, static_cast<float *>(dx), D,
-               GEMM_EPI_ADD, gf, D);
+               GEMM_EPI_ADD, gp, D);
+      timer.end(c.s, gf(B, D, D), gb(B, D, D, 4.0 * B * D));
       c.launches += 1;
     }
   }

@@ -112,9 +112,27 @@ class ResNetBasic : public Net {
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
     ks_bytes = off;
+    timed_family = "k_conv3x3<";
   }
 
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
+
+  // conv3x3 launch bracketed by the kernel timer.  Algorithmic work of a 3x3
+  // convolution with output [N, ho, ho, cout] and input channels cin (the same
+  // for its forward and its data gradient): 2 * N*ho*ho * cout * 9*cin flops;
+  // bytes = kernel input + weights + kernel output + epilogue tensors read.
+  void conv(StepCtx &c, int mode, int s, int epi, const float *X, const float *Wt, float *Y, int H,
+            int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1, int Eh, int Ew,
+            int Ec, int ho, int cin, int cout) {
+    const double fl = 2.0 * N * ho * ho * double(cout) * 9.0 * cin;
+    double by = 4.0 * (double(N) * Hx * Wx * C + 9.0 * cin * cout + double(N) * H * W * J);
+    if (epi == CONV_EPI_MASK) by += 4.0 * N * H * W * J;
+    if (epi == CONV_EPI_SC1 || epi == CONV_EPI_SC2) by += 2 * 4.0 * N * Eh * Ew * std::min(Ec, J);
+    timer.begin(c.s);
+    conv3x3(c.s, mode, s, epi, X, Wt, Y, N, H, W, Hx, Wx, C, J, E0, E1, Eh, Ew, Ec,
+            epi == CONV_EPI_STATS ? bnpart(c) : nullptr);
+    timer.end(c.s, fl, by);
+  }
   float *ksf(StepCtx &c, uint64_t off) const { return reinterpret_cast<float *>(c.ks + off); }
 
   void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
@@ -127,8 +145,8 @@ class ResNetBasic : public Net {
     if (k.w2 < 0) {  // stem
       float *cv = reinterpret_cast<float *>(sv);
       float *st = reinterpret_cast<float *>(sv + t);
-      conv3x3(c.s, CONV_FWD, 1, CONV_EPI_STATS, x, P(c, k.w1), cv, N, S, S, S, S, 3, C0, nullptr,
-              nullptr, 0, 0, 0, bnpart(c));
+      conv(c, CONV_FWD, 1, CONV_EPI_STATS, x, P(c, k.w1), cv, S, S, S, S, 3, C0, nullptr, nullptr,
+           0, 0, 0, S, 3, C0);
       bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st);
       bn_apply(c.s, BN_RES_NONE, np, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, y);
       c.launches += 3;
@@ -141,13 +159,13 @@ class ResNetBasic : public Net {
     float *st1 = reinterpret_cast<float *>(sv + 3 * t);
     float *st2 = reinterpret_cast<float *>(sv + 3 * t + sb);
     const int ho = k.hout;
-    conv3x3(c.s, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, N, ho, ho, k.hin, k.hin,
-            k.cin, k.cout, nullptr, nullptr, 0, 0, 0, bnpart(c));
+    conv(c, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin,
+         k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
                     k.cout, np, st1);
     bn_apply(c.s, BN_RES_NONE, np, k.cout, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, r1);
-    conv3x3(c.s, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, N, ho, ho, ho, ho, k.cout, k.cout,
-            nullptr, nullptr, 0, 0, 0, bnpart(c));
+    conv(c, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
+         nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout);
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
                     np, st2);
     bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),
@@ -187,16 +205,17 @@ class ResNetBasic : public Net {
     // second BN (its input gradient is g masked by the block's final ReLU)
     bn_backward(c.s, np, k.cout, g, y, c2, st2, P(c, k.g2), bnpart(c), sums, G(c, k.g2), G(c, k.b2), Qb);
     // conv2: data gradient masked by the first ReLU, and weight gradient
-    conv3x3(c.s, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, N, ho, ho, ho, ho, k.cout, k.cout,
-            r1);
+    conv(c, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, ho, ho, ho, ho, k.cout, k.cout, r1,
+         nullptr, 0, 0, 0, ho, k.cout, k.cout);
     conv3x3_wgrad(c.s, 1, r1, Qb, wpart, G(c, k.w2), N, ho, ho, ho, ho, k.cout, k.cout);
     // first BN
     bn_backward(c.s, np, k.cout, Pb, nullptr, c1, st1, P(c, k.g1), bnpart(c), sums, G(c, k.g1),
                 G(c, k.b1), Qb);
     c.launches += 9;
     if (dxv) {  // conv1 data gradient plus the shortcut's gradient
-      conv3x3(c.s, CONV_DGRAD, k.stride, k.stride == 1 ? CONV_EPI_SC1 : CONV_EPI_SC2, Qb, P(c, k.w1),
-              static_cast<float *>(dxv), N, k.hin, k.hin, ho, ho, k.cout, k.cin, g, y, ho, ho, k.cout);
+      conv(c, CONV_DGRAD, k.stride, k.stride == 1 ? CONV_EPI_SC1 : CONV_EPI_SC2, Qb, P(c, k.w1),
+           static_cast<float *>(dxv), k.hin, k.hin, ho, ho, k.cout, k.cin, g, y, ho, ho, k.cout, ho,
+           k.cin, k.cout);
       c.launches += 1;
     }
     conv3x3_wgrad(c.s, k.stride, x, Qb, wpart, G(c, k.w1), N, ho, ho, k.hin, k.hin, k.cin, k.cout);

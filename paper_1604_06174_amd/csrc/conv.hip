@@ -223,6 +223,234 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
   }
 }
 
+// ------------------------------------------------ specialised fwd / dgrad --
+// Same computation as k_conv3x3 for channel counts that are multiples of 16
+// and compile-time shapes.  Each lane fetches a float4 of 4 consecutive
+// channels of its pixel (ds_read_b128) and of its output channel's weights,
+// and feeds them to 4 successive MFMA k-steps: step u pairs channel
+// c0 + 4q + u of both operands, so the 4 steps cover channels c0..c0+15.
+// Workgroup = RB output rows x BN output channels; each wavefront owns
+// RB*W/64 pixel tiles of 16 and all BN/16 channel tiles.
+template <int C, int J, int W, int S, int MODE, int EPI, int RB, int BN>
+__global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
+  constexpr int NS = BN / 16;
+  constexpr int NPIX = RB * W;
+  static_assert(NPIX % 64 == 0 && C % 16 == 0 && BN % 16 == 0, "tile shape");
+  constexpr int PSW = NPIX / 64;
+  constexpr int Cs = C + 4;
+  constexpr int C4 = C / 4;
+  constexpr int HR = MODE == CONV_FWD ? (RB - 1) * S + 3 : RB + 2;
+  constexpr int HC = MODE == CONV_FWD ? (W - 1) * S + 3 : W + 2;
+  constexpr int WX = MODE == CONV_FWD ? W * S : W / S;  // input width
+  extern __shared__ __align__(16) float smem[];
+  float *halo = smem;
+  float *Bs = smem + HR * HC * Cs;  // [2][BN][Cs]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, q = lane >> 4;
+  const int rblk = (a.H + RB - 1) / RB;
+  const int n = blockIdx.x / rblk, r0 = (blockIdx.x % rblk) * RB;
+  const int j0 = blockIdx.y * BN;
+  const int Hx = a.Hx;
+
+  for (int e = tid; e < HR * HC * C4; e += 256) {
+    const int c4 = e % C4, hc = (e / C4) % HC, hr = e / (C4 * HC);
+    int ir, ic;
+    bool ok;
+    if (MODE == CONV_FWD) {
+      ir = r0 * S - 1 + hr;
+      ic = hc - 1;
+      ok = ir >= 0 && ir < Hx && ic >= 0 && ic < WX;
+    } else {
+      const int ur = r0 - 1 + hr, uc = hc - 1;
+      ir = ur / S;
+      ic = uc / S;
+      ok = ur >= 0 && uc >= 0 && (ur % S) == 0 && (uc % S) == 0 && ir < Hx && ic < WX;
+    }
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ok) v = *reinterpret_cast<const float4 *>(a.X + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4);
+    *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + 4 * c4) = v;
+  }
+
+  // weights of one tap into Bs[buf][jj][c]
+  constexpr int BE = MODE == CONV_FWD ? BN * C4 : BN * C;
+  constexpr int BPT = (BE + 255) / 256;
+  float4 bq[MODE == CONV_FWD ? BPT : 1];
+  float bsr[MODE == CONV_FWD ? 1 : BPT];
+  auto bload = [&](int tap) {
+#pragma unroll
+    for (int k = 0; k < BPT; ++k) {
+      const int e = tid + k * 256;
+      if constexpr (MODE == CONV_FWD) {
+        const int jj = e / C4, c4 = e % C4, j = j0 + jj;
+        bq[k] = (e < BE && j < J) ? *reinterpret_cast<const float4 *>(a.Wt + (size_t(j) * 9 + tap) * C + 4 * c4)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        const int c = e / BN, jj = e % BN, j = j0 + jj;
+        bsr[k] = (e < BE && j < J) ? a.Wt[(size_t(c) * 9 + tap) * J + j] : 0.f;
+      }
+    }
+  };
+  auto bstore = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < BPT; ++k) {
+      const int e = tid + k * 256;
+      if (e >= BE) continue;
+      if constexpr (MODE == CONV_FWD) {
+        const int jj = e / C4, c4 = e % C4;
+        *reinterpret_cast<float4 *>(Bs + (buf * BN + jj) * Cs + 4 * c4) = bq[k];
+      } else {
+        const int c = e / BN, jj = e % BN;
+        Bs[(buf * BN + jj) * Cs + c] = bsr[k];
+      }
+    }
+  };
+  bload(0);
+  bstore(0);
+  __syncthreads();
+
+  int pr[PSW], pc[PSW];
+#pragma unroll
+  for (int s = 0; s < PSW; ++s) {
+    const int p = (wave * PSW + s) * 16 + i16;
+    pr[s] = p / W;
+    pc[s] = p % W;
+  }
+  floatx4 acc[PSW][NS];
+#pragma unroll
+  for (int s = 0; s < PSW; ++s)
+#pragma unroll
+    for (int t = 0; t < NS; ++t) acc[s][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int tap = 0; tap < 9; ++tap) {
+    const int kh = tap / 3, kw = tap % 3, buf = tap & 1;
+    if (tap + 1 < 9) bload(tap + 1);
+    int hoff[PSW];
+#pragma unroll
+    for (int s = 0; s < PSW; ++s)
+      hoff[s] = MODE == CONV_FWD ? ((pr[s] * S + kh) * HC + pc[s] * S + kw) * Cs + 4 * q
+                                 : ((pr[s] + 2 - kh) * HC + pc[s] + 2 - kw) * Cs + 4 * q;
+    const float *Bt = Bs + (buf * BN + i16) * Cs + 4 * q;
+#pragma unroll
+    for (int c0 = 0; c0 < C; c0 += 16) {
+      float4 av[PSW], bv[NS];
+#pragma unroll
+      for (int s = 0; s < PSW; ++s) av[s] = *reinterpret_cast<const float4 *>(halo + hoff[s] + c0);
+#pragma unroll
+      for (int t = 0; t < NS; ++t) bv[t] = *reinterpret_cast<const float4 *>(Bt + t * 16 * Cs + c0);
+#pragma unroll
+      for (int s = 0; s < PSW; ++s)
+#pragma unroll
+        for (int t = 0; t < NS; ++t) {
+          acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].x, bv[t].x, acc[s][t], 0, 0, 0);
+          acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].y, bv[t].y, acc[s][t], 0, 0, 0);
+          acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].z, bv[t].z, acc[s][t], 0, 0, 0);
+          acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].w, bv[t].w, acc[s][t], 0, 0, 0);
+        }
+    }
+    if (tap + 1 < 9) bstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  double s1[NS], s2[NS];
+#pragma unroll
+  for (int t = 0; t < NS; ++t) s1[t] = s2[t] = 0.0;
+#pragma unroll
+  for (int s = 0; s < PSW; ++s) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int p = (wave * PSW + s) * 16 + 4 * q + r;
+      const int rr = p / W, cc = p % W;
+      const int h = r0 + rr;
+      if (h >= a.H) continue;
+#pragma unroll
+      for (int t = 0; t < NS; ++t) {
+        const int j = j0 + t * 16 + i16;
+        if (j >= J) continue;
+        const size_t o = ((size_t(n) * a.H + h) * W + cc) * J + j;
+        float v = acc[s][t][r];
+        if (EPI == CONV_EPI_STATS) {
+          s1[t] += double(v);
+          s2[t] += double(v) * double(v);
+        } else if (EPI == CONV_EPI_MASK) {
+          v = a.E0[o] > 0.f ? v : 0.f;
+        } else if (EPI == CONV_EPI_SC1) {
+          v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
+        } else if (EPI == CONV_EPI_SC2) {
+          if (((h | cc) & 1) == 0) {
+            const size_t o2 = ((size_t(n) * a.Eh + (h >> 1)) * a.Ew + (cc >> 1)) * a.Ec + j;
+            v += a.E1[o2] > 0.f ? a.E0[o2] : 0.f;
+          }
+        }
+        a.Y[o] = v;
+      }
+    }
+  }
+  if (EPI == CONV_EPI_STATS) {
+    double *red = reinterpret_cast<double *>(smem);
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      red[((wave * 4 + q) * 2 + 0) * BN + t * 16 + i16] = s1[t];
+      red[((wave * 4 + q) * 2 + 1) * BN + t * 16 + i16] = s2[t];
+    }
+    __syncthreads();
+    if (tid < 2 * BN) {
+      const int which = tid / BN, jj = tid % BN;
+      double acc2 = 0.0;
+      for (int k = 0; k < 16; ++k) acc2 += red[(k * 2 + which) * BN + jj];
+      if (j0 + jj < J) a.stats[(size_t(blockIdx.x) * 2 + which) * J + j0 + jj] = acc2;
+    }
+  }
+}
+
+template <int C, int J, int W, int S, int MODE, int RB, int BN>
+constexpr size_t spec_lds() {
+  constexpr int Cs = C + 4;
+  constexpr int HR = MODE == CONV_FWD ? (RB - 1) * S + 3 : RB + 2;
+  constexpr int HC = MODE == CONV_FWD ? (W - 1) * S + 3 : W + 2;
+  constexpr size_t st = size_t(HR * HC * Cs + 2 * BN * Cs) * 4;
+  constexpr size_t red = size_t(16) * 2 * BN * 8;
+  return st > red ? st : red;
+}
+
+struct SpecUse {
+  int RB = 0, BN = 0;
+};
+
+// One row of the specialisation table; returns whether it matches the launch.
+template <int C, int J, int W, int S, int MODE, int EPI, int RB, int BN>
+bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
+  if (mode != MODE || s != S || epi != EPI || a.C != C || a.J != J || a.W != W) return false;
+  if (a.Wx != (MODE == CONV_FWD ? W * S : W / S)) return false;
+  static_assert(spec_lds<C, J, W, S, MODE, RB, BN>() <= 64 * 1024, "LDS");
+  if (u) *u = {RB, BN};
+  if (launch) {
+    dim3 grid(a.N * ((a.H + RB - 1) / RB), (J + BN - 1) / BN);
+    constexpr size_t lds = spec_lds<C, J, W, S, MODE, RB, BN>();
+    hipLaunchKernelGGL((k_conv3x3s<C, J, W, S, MODE, EPI, RB, BN>), grid, dim3(256), lds, st, a);
+  }
+  return true;
+}
+
+// The CIFAR-shaped network's convolutions: 16/32/64 channels at 32/16/8 pixels.
+bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
+  constexpr int F = CONV_FWD, D = CONV_DGRAD;
+  constexpr int STATS = CONV_EPI_STATS, MASK = CONV_EPI_MASK, SC1 = CONV_EPI_SC1, SC2 = CONV_EPI_SC2;
+  return spec_try<16, 16, 32, 1, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 32, 16, 2, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 64, 8, 2, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, D, MASK, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, D, MASK, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, D, MASK, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, D, SC1, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, D, SC1, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, D, SC1, 8, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 16, 32, 2, D, SC2, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 32, 16, 2, D, SC2, 8, 16>(a, mode, s, epi, st, launch, u);
+}
+
 // ---------------------------------------------------------------- wgrad --
 // dW[j][n] = sum_p dy[p][j] * col[p][n],  n = tap*C + c, col = im2col(x)
 // (M = J, N = 9C, K = N*Ho*Wo pixels).  Workgroup = one 144-column slice of
@@ -245,11 +473,16 @@ struct WgArgs {
 
 __device__ __forceinline__ int wg_as(int J) { return J + ((16 - J % 32) + 32) % 32; }  // == 16 mod 32
 
+// CT, JT, WT, HT, ST: compile-time channel counts, output width/height and
+// stride (0 = take the runtime value): the network's few shapes get
+// instantiations whose index arithmetic folds to shifts and multiplies.
+template <int CT, int JT, int WT, int HT, int ST>
 __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
   extern __shared__ __align__(16) float smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
-  const int J = a.J, C = a.C, NC = 9 * C;
+  const int J = JT ? JT : a.J, C = CT ? CT : a.C, NC = 9 * C;
+  const int OW = WT ? WT : a.W, OH = HT ? HT : a.H, SS = ST ? ST : a.S;
   const int jt_n = (J + 15) / 16;                  // j tiles (1..4)
   const int wgj = jt_n < 4 ? jt_n : 4;            // wavefronts across j tiles
   const int wgk = 4 / wgj;                         // wavefronts across pixels
@@ -259,8 +492,8 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
   float *Abuf = smem;                              // [2][KC][AS]
   float *Bbuf = smem + 2 * WG_KC * AS;             // [2][KC][BS]
   const int n0 = blockIdx.y * WG_NB;
-  const int64_t P = int64_t(a.N) * a.H * a.W;
-  const int64_t p0 = int64_t(blockIdx.x) * a.pix_per_blk;
+  const int P = a.N * OH * OW;
+  const int p0 = blockIdx.x * a.pix_per_blk;
   const int nchunk = a.pix_per_blk / WG_KC;
 
   // staging: A = dy[p][0..16*jt_n) as float4, B = im2col[p][n0..n0+144) as float4
@@ -270,15 +503,15 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
   constexpr int MAXA = 2, MAXB = 5;  // per thread: na <= 512, nbq = 1152
   float4 ra[MAXA], rb[MAXB];
   auto gload = [&](int ck) {
-    const int64_t pc = p0 + int64_t(ck) * WG_KC;
+    const int pc = p0 + ck * WG_KC;
 #pragma unroll
     for (int k = 0; k < MAXA; ++k) {
       const int e = tid + k * 256;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (e < na) {
         const int pl = e / a4, j4 = (e % a4) * 4;
-        const int64_t p = pc + pl;
-        if (p < P && j4 < J) v = *reinterpret_cast<const float4 *>(a.DY + p * J + j4);
+        const int p = pc + pl;
+        if (p < P && j4 < J) v = *reinterpret_cast<const float4 *>(a.DY + size_t(p) * J + j4);
       }
       ra[k] = v;
     }
@@ -288,14 +521,14 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (e < nbq) {
         const int pl = e / b4, nn = n0 + (e % b4) * 4;
-        const int64_t p = pc + pl;
+        const int p = pc + pl;
         if (p < P && nn < NC) {
-          const int ow = int(p % a.W);
-          const int64_t t = p / a.W;
-          const int oh = int(t % a.H), img = int(t / a.H);
+          const int ow = p % OW;
+          const int t = p / OW;
+          const int oh = t % OH, img = t / OH;
           if ((C & 3) == 0) {  // the 4 columns are 4 channels of one tap
             const int tap = nn / C, c = nn % C;
-            const int ih = oh * a.S + tap / 3 - 1, iw = ow * a.S + tap % 3 - 1;
+            const int ih = oh * SS + tap / 3 - 1, iw = ow * SS + tap % 3 - 1;
             if (ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
               v = *reinterpret_cast<const float4 *>(a.X + ((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c);
           } else {
@@ -304,7 +537,7 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
             for (int u = 0; u < 4; ++u) {
               const int n = nn + u;
               const int tap = n / C, c = n % C;
-              const int ih = oh * a.S + tap / 3 - 1, iw = ow * a.S + tap % 3 - 1;
+              const int ih = oh * SS + tap / 3 - 1, iw = ow * SS + tap % 3 - 1;
               vv[u] = (n < NC && ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
                           ? a.X[((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c]
                           : 0.f;
@@ -490,7 +723,22 @@ void launch_mode(const ConvArgs &a, int mode, int S, int epi, size_t lds, dim3 g
 
 }  // namespace
 
+static ConvArgs shape_args(int mode, int S, int N, int H, int W, int C, int J) {
+  ConvArgs a{};
+  a.N = N;
+  a.H = H;
+  a.W = W;
+  a.C = C;
+  a.J = J;
+  a.Wx = mode == CONV_FWD ? W * S : W / S;
+  return a;
+}
+
 int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J) {
+  SpecUse u;
+  // the statistics partials are indexed by blockIdx.x only
+  if (spec_dispatch(shape_args(mode, S, N, H, W, C, J), mode, S, CONV_EPI_STATS, nullptr, false, &u))
+    return N * ((H + u.RB - 1) / u.RB);
   return N * conv_tile(mode, S, H, W, C, J).rblk;
 }
 
@@ -516,6 +764,7 @@ void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const flo
   Tile t = conv_tile(mode, S, H, W, C, J);
   const int NSUB = J > 16 ? 2 : 1;
   ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats};
+  if (spec_dispatch(a, mode, S, epi, st, true, nullptr)) return;
   dim3 grid(N * t.rblk, (J + 16 * NSUB - 1) / (16 * NSUB));
   const size_t lds = conv_lds(mode, S, t.R, W, C, J);
   if (t.psw == 1) {
@@ -535,7 +784,19 @@ void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float
   const int nbx = int((P + ppb - 1) / ppb);
   WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, S, ppb};
   dim3 grid(nbx, (NC + WG_NB - 1) / WG_NB);
-  hipLaunchKernelGGL(k_conv3x3_wgrad, grid, dim3(256), wgrad_lds(J), st, a);
+  const size_t lds = wgrad_lds(J);
+#define CKPT_WG(C_, J_, W_, S_)                                                              \
+  if (C == C_ && J == J_ && W == W_ && H == W_ && S == S_) {                                 \
+    hipLaunchKernelGGL((k_conv3x3_wgrad<C_, J_, W_, W_, S_>), grid, dim3(256), lds, st, a); \
+  } else
+  CKPT_WG(3, 16, 32, 1)
+  CKPT_WG(16, 16, 32, 1)
+  CKPT_WG(16, 32, 16, 2)
+  CKPT_WG(32, 32, 16, 1)
+  CKPT_WG(32, 64, 8, 2)
+  CKPT_WG(64, 64, 8, 1)
+  hipLaunchKernelGGL((k_conv3x3_wgrad<0, 0, 0, 0, 0>), grid, dim3(256), lds, st, a);
+#undef CKPT_WG
   const int E = J * NC;
   hipLaunchKernelGGL(k_sum_partials, dim3((E + 15) / 16), dim3(256), 0, st, part, nbx, E, dW);
 }

@@ -112,7 +112,7 @@ class ResNetBasic : public Net {
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
     ks_bytes = off;
-    timed_family = "k_conv3x3<";
+    timed_family = "k_conv3x3< and k_conv3x3s<";
   }
 
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }

@@ -629,23 +629,198 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
   }
 }
 
-// out[e] = sum over b of part[b][e], b in a fixed order: 16 slices of b,
-// then the slices in order.
+// ------------------------------------------- specialised weight gradient --
+// Compile-time shapes.  Workgroup = TPB tiles of RB output rows of one image
+// x one 144-column slice of n = tap*C + c (NT <= 9 tiles of 16).  The input
+// halo of a tile (zero outside the image) and its dy rows are staged in LDS
+// once; the im2col operand is read straight from the halo with per-lane tap
+// offsets, so every input element is fetched from memory once per tile.
+// Wavefronts split the J row tiles and, when J < 64, the tile's pixels
+// (summed through LDS in a fixed order at the end).
+template <int C, int J, int W, int S, int RB, int TPB>
+__global__ __launch_bounds__(256) void k_wgrad_s(WgArgs a) {
+  constexpr int NC = 9 * C;
+  constexpr int Cp = (C + 3) & ~3;
+  constexpr int Cs = Cp + 4;
+  constexpr int HR = (RB - 1) * S + 3, HC = (W - 1) * S + 3;
+  constexpr int NPIX = RB * W;
+  constexpr int JT = (J + 15) / 16;
+  constexpr int WGJ = JT < 4 ? JT : 4;
+  constexpr int WGK = 4 / WGJ;
+  static_assert(WGJ * WGK == 4 && NPIX % (4 * WGK) == 0, "wave split");
+  constexpr int JS = JT * 16 + (((16 - (JT * 16) % 32) + 32) % 32);  // == 16 (mod 32)
+  constexpr int NTT = (NC + 15) / 16;
+  constexpr int WX = W * S;
+  extern __shared__ __align__(16) float smem[];
+  float *halo = smem;
+  float *dys = smem + HR * HC * Cs;  // [NPIX][JS]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, q = lane >> 4;
+  const int my_jt = wave % WGJ, my_kg = wave / WGJ;
+  const int n0 = blockIdx.y * 144;
+  const int NT = min(9, NTT - blockIdx.y * 9);  // n tiles in this slice
+  const int rblk = (a.H + RB - 1) / RB;
+  const int ntiles = a.N * rblk;
+
+  // per-lane im2col column offsets within the halo (tap shift + channel)
+  int boff[9];
+  bool bok[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    const int nn = n0 + t * 16 + i16;
+    const int tap = nn / C, c = nn % C;
+    bok[t] = t < NT && nn < NC;
+    boff[t] = bok[t] ? ((tap / 3) * HC + tap % 3) * Cs + c : 0;
+  }
+  floatx4 acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int tt = 0; tt < TPB; ++tt) {
+    const int g = blockIdx.x * TPB + tt;
+    if (g >= ntiles) break;
+    const int img = g / rblk, r0 = (g % rblk) * RB;
+    if (tt > 0) __syncthreads();
+    for (int e = tid; e < HR * HC * (Cp / 4); e += 256) {
+      const int c4 = (e % (Cp / 4)) * 4, hc = (e / (Cp / 4)) % HC, hr = e / ((Cp / 4) * HC);
+      const int ir = r0 * S - 1 + hr, ic = hc - 1;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (ir >= 0 && ir < a.Hx && ic >= 0 && ic < WX) {
+        const float *src = a.X + ((size_t(img) * a.Hx + ir) * WX + ic) * C + c4;
+        if constexpr (C % 4 == 0) {
+          v = *reinterpret_cast<const float4 *>(src);
+        } else {
+          float vv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) vv[u] = (c4 + u < C) ? src[u] : 0.f;
+          v = make_float4(vv[0], vv[1], vv[2], vv[3]);
+        }
+      }
+      *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = v;
+    }
+    for (int e = tid; e < NPIX * (JT * 4); e += 256) {
+      const int j4 = (e % (JT * 4)) * 4, p = e / (JT * 4);
+      const int h = r0 + p / W, w = p % W;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (h < a.H && j4 < J) v = *reinterpret_cast<const float4 *>(a.DY + ((size_t(img) * a.H + h) * W + w) * J + j4);
+      *reinterpret_cast<float4 *>(dys + p * JS + j4) = v;
+    }
+    __syncthreads();
+    constexpr int PK = NPIX / WGK;
+    const int kb = my_kg * PK;
+    const float *Ab = dys + my_jt * 16 + i16;
+    for (int k0 = kb; k0 < kb + PK; k0 += 4) {
+      const int p = k0 + q;
+      const int pb = ((p / W) * S * HC + (p % W) * S) * Cs;
+      const float av = Ab[p * JS];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const float bv = bok[t] ? halo[pb + boff[t]] : 0.f;
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t], 0, 0, 0);
+      }
+    }
+  }
+
+  if constexpr (WGK > 1) {
+    __syncthreads();
+    float *red = smem;  // [wave][9][4][64]
+    if (my_kg > 0) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[((wave * 9 + t) * 4 + r) * 64 + lane] = acc[t][r];
+    }
+    __syncthreads();
+    if (my_kg == 0) {
+      for (int k = 1; k < WGK; ++k) {
+        const int w2 = k * WGJ + my_jt;
+#pragma unroll
+        for (int t = 0; t < 9; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[t][r] += red[((w2 * 9 + t) * 4 + r) * 64 + lane];
+      }
+    }
+  }
+  if (my_kg == 0) {
+    float *dst = a.part + size_t(blockIdx.x) * J * NC;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int nn = n0 + t * 16 + i16;
+      if (!bok[t]) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = my_jt * 16 + 4 * q + r;
+        if (j < J) dst[size_t(j) * NC + nn] = acc[t][r];
+      }
+    }
+  }
+}
+
+template <int C, int J, int W, int S, int RB>
+constexpr size_t wgs_lds() {
+  constexpr int Cs = ((C + 3) & ~3) + 4;
+  constexpr int HR = (RB - 1) * S + 3, HC = (W - 1) * S + 3;
+  constexpr int JT = (J + 15) / 16;
+  constexpr int JS = JT * 16 + (((16 - (JT * 16) % 32) + 32) % 32);
+  constexpr size_t st = size_t(HR * HC * Cs + RB * W * JS) * 4;
+  constexpr size_t red = size_t(4) * 9 * 4 * 64 * 4;
+  return st > red ? st : red;
+}
+
+struct WgUse {
+  int nbx = 0;
+};
+
+template <int C, int J, int W, int S, int RB, int TPB>
+bool wgs_try(const WgArgs &a, hipStream_t st, bool launch, WgUse *u) {
+  if (a.C != C || a.J != J || a.W != W || a.S != S || a.Wx != W * S) return false;
+  static_assert(wgs_lds<C, J, W, S, RB>() <= 64 * 1024, "LDS");
+  const int ntiles = a.N * ((a.H + RB - 1) / RB);
+  const int nbx = (ntiles + TPB - 1) / TPB;
+  if (u) u->nbx = nbx;
+  if (launch) {
+    dim3 grid(nbx, (9 * C + 143) / 144);
+    constexpr size_t lds = wgs_lds<C, J, W, S, RB>();
+    hipLaunchKernelGGL((k_wgrad_s<C, J, W, S, RB, TPB>), grid, dim3(256), lds, st, a);
+  }
+  return true;
+}
+
+bool wgs_dispatch(const WgArgs &a, hipStream_t st, bool launch, WgUse *u) {
+  return wgs_try<3, 16, 32, 1, 8, 1>(a, st, launch, u) ||
+         wgs_try<16, 16, 32, 1, 8, 1>(a, st, launch, u) ||
+         wgs_try<16, 32, 16, 2, 4, 2>(a, st, launch, u) ||
+         wgs_try<32, 32, 16, 1, 8, 1>(a, st, launch, u) ||
+         wgs_try<32, 64, 8, 2, 8, 1>(a, st, launch, u);
+}
+
+// out[e] = sum over b of part[b][e], b in a fixed order: SL slices of b
+// (slice k takes b = k, k + SL, ...), then the slices in order.  A workgroup
+// covers 256 / SL consecutive e; SL = 64 for small E, 16 otherwise.
+template <int SL>
 __global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ part, int nb,
                                                       int E, float *__restrict__ out) {
-  __shared__ float red[16][16];
-  const int ex = threadIdx.x & 15, sl = threadIdx.x >> 4;
-  const int e = blockIdx.x * 16 + ex;
+  constexpr int ES = 256 / SL;
+  __shared__ float red[SL][ES];
+  const int ex = threadIdx.x % ES, sl = threadIdx.x / ES;
+  const int e = blockIdx.x * ES + ex;
   float s = 0.f;
   if (e < E)
-    for (int b = sl; b < nb; b += 16) s += part[size_t(b) * E + e];
+    for (int b = sl; b < nb; b += SL) s += part[size_t(b) * E + e];
   red[sl][ex] = s;
   __syncthreads();
   if (sl == 0 && e < E) {
     float t = 0.f;
-    for (int k = 0; k < 16; ++k) t += red[k][ex];
+    for (int k = 0; k < SL; ++k) t += red[k][ex];
     out[e] = t;
   }
+}
+
+void sum_partials(hipStream_t st, const float *part, int nb, int E, float *out) {
+  if (E < 16 * 2048)
+    hipLaunchKernelGGL((k_sum_partials<64>), dim3((E + 3) / 4), dim3(256), 0, st, part, nb, E, out);
+  else
+    hipLaunchKernelGGL((k_sum_partials<16>), dim3((E + 15) / 16), dim3(256), 0, st, part, nb, E, out);
 }
 
 struct Tile {
@@ -743,7 +918,10 @@ int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J) {
 }
 
 int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J) {
-  (void)S;
+  WgArgs wa{};
+  wa.N = N; wa.H = H; wa.W = W; wa.Wx = W * S; wa.C = C; wa.J = J; wa.S = S;
+  WgUse u;
+  if (wgs_dispatch(wa, nullptr, false, &u)) return u.nbx;
   const int64_t P = int64_t(N) * H * W;
   const int ppb = wgrad_pix(P, 9 * C);
   return int((P + ppb - 1) / ppb);
@@ -783,6 +961,13 @@ void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float
   const int ppb = wgrad_pix(P, NC);
   const int nbx = int((P + ppb - 1) / ppb);
   WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, S, ppb};
+  {
+    WgUse u;
+    if (wgs_dispatch(a, st, true, &u)) {
+      sum_partials(st, part, u.nbx, J * NC, dW);
+      return;
+    }
+  }
   dim3 grid(nbx, (NC + WG_NB - 1) / WG_NB);
   const size_t lds = wgrad_lds(J);
 #define CKPT_WG(C_, J_, W_, S_)                                                              \
@@ -797,8 +982,7 @@ void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float
   CKPT_WG(64, 64, 8, 1)
   hipLaunchKernelGGL((k_conv3x3_wgrad<0, 0, 0, 0, 0>), grid, dim3(256), lds, st, a);
 #undef CKPT_WG
-  const int E = J * NC;
-  hipLaunchKernelGGL(k_sum_partials, dim3((E + 15) / 16), dim3(256), 0, st, part, nbx, E, dW);
+  sum_partials(st, part, nbx, J * NC, dW);
 }
 
 }  // namespace ckpt

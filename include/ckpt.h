@@ -114,15 +114,20 @@ void plan_free(ckpt_plan *plan);
 /* ---- networks --------------------------------------------------------- */
 #define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
 #define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */
+#define CKPT_NET_LSTM              3 /* LSTM steps, each with a softmax head          */
 
 typedef struct ckpt_net_desc {
   int32_t kind;          /* CKPT_NET_*                                             */
   int32_t batch;         /* samples per step                                       */
-  int32_t depth;         /* MLP: blocks.  RESNET_BASIC: basic blocks per stage    */
-  int32_t width;         /* MLP: width.   RESNET_BASIC: first-stage channels      */
-  int32_t image;         /* RESNET_BASIC: input side (square images, 3 channels)  */
-  int32_t n_classes;     /* RESNET_BASIC: classifier outputs                       */
-  int32_t reserved[10];  /* must be zero                                           */
+  int32_t depth;         /* MLP: blocks.  RESNET_BASIC: basic blocks per stage.
+                            LSTM: time steps T                                     */
+  int32_t width;         /* MLP: width.   RESNET_BASIC: first-stage channels.
+                            LSTM: hidden size H                                    */
+  int32_t image;         /* RESNET_BASIC: input side (square images, 3 channels).
+                            LSTM: input size E                                     */
+  int32_t n_classes;     /* RESNET_BASIC: classifier outputs.  LSTM: vocabulary V */
+  int32_t grad_chunk;    /* LSTM: time steps per weight-gradient chunk (0 = 32)    */
+  int32_t reserved[9];   /* must be zero                                           */
 } ckpt_net_desc;
 
 /*
@@ -138,6 +143,15 @@ typedef struct ckpt_net_desc {
  *                 [4 width, n_classes] + bias, softmax cross-entropy averaged
  *                 over the batch.  Conv weights [Cout,3,3,Cin]; input f32 NHWC
  *                 [batch, image, image, 3]; target int32 [batch].
+ *   LSTM:         n = T units, one per time step: z = x_t W_x + h W_h + b with
+ *                 gates i, f, g, o in column blocks of H, c = f c + i g,
+ *                 h = o tanh c; per-step head logits = h W_o + b_o, softmax
+ *                 cross-entropy averaged over T*batch (section 5.3's long
+ *                 unrolled LSTM).  Parameters W_x [E,4H], W_h [H,4H], b [4H],
+ *                 W_o [H,V], b_o [V]; input bf16 [T, batch, E]; target int32
+ *                 [T, batch].  GEMM operands are bf16 (weights rounded once per
+ *                 step), accumulation and the cell state fp32, h bf16.  Sizes
+ *                 must be multiples of 8.
  * Errors: CKPT_E_INVALID for a null pointer, an unknown kind or a
  *   non-positive or inconsistent size.
  */
@@ -153,6 +167,14 @@ int net_units(const ckpt_net *net, int32_t *n);
  * scratch.  Every tensor is rounded up to 256 bytes.
  */
 int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q);
+
+/*
+ * net_grad_bytes -- the gradient part of the static layout: one gradient slot
+ * (the gradient of a boundary; two are used in turn) and the unit kind's
+ * fixed gradient buffers (the LSTM's weight-gradient chunk buffers; 0 for the
+ * others).  Either output may be null.
+ */
+int net_grad_bytes(const ckpt_net *net, uint64_t *slot, uint64_t *extra);
 
 /* net_layer_sizes -- plan_checkpoints inputs: layer_bytes[i] = a_i + b_{i+1},
  * cut_bytes[i] = b_{i+1} (0 for the last unit).  Host arrays of n entries. */
@@ -185,8 +207,10 @@ int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt, 
 int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *bytes);
 
 typedef struct ckpt_batch {
-  const void *input;   /* device: MLP f32 [batch,width]; RESNET_BASIC f32 NHWC images */
-  const void *target;  /* device: MLP f32 [batch,width]; RESNET_BASIC int32 [batch]   */
+  const void *input;   /* device: MLP f32 [batch,width]; RESNET_BASIC f32 NHWC images;
+                          LSTM bf16 [T,batch,E]                                        */
+  const void *target;  /* device: MLP f32 [batch,width]; RESNET_BASIC int32 [batch];
+                          LSTM int32 [T,batch]                                         */
 } ckpt_batch;
 
 typedef struct ckpt_step_stats {

@@ -43,7 +43,10 @@ operator workspace, section 5.1):
 * ARENA -- the largest of (a) every forward-sweep unit's transient need
            (input if it lives in the arena) + internals + (output if it is not
            stored), and (b) every re-run segment's sum of internals + outputs.
-* GRAD  -- two gradient slots of max_{1<=i<=n} b_i and one scratch of max q_i.
+* GRAD  -- two gradient slots (each the size of the largest boundary's
+           gradient: max_{1<=i<=n} b_i unless the unit kind says otherwise),
+           one scratch of max q_i, plus any fixed gradient buffers of the
+           unit kind (the LSTM's weight-gradient chunk buffers).
 * PEAK  -- CKPT + ARENA + GRAD.
 
 Parity: pinned by brute force over all cut sets for n <= 16, Alg. 3
@@ -219,16 +222,20 @@ def _sweep_needs(b, a, lo, hi, stored):
     return needs
 
 
-def grad_bytes(b, q):
+def grad_bytes(b, q, slot=None, extra=0):
     n = len(q)
-    return 2 * max(b[1:n + 1]) + max(q)
+    if slot is None:
+        slot = max(b[1:n + 1])
+    return 2 * slot + max(q) + extra
 
 
-def account(p: Plan, b: Sequence[int], a: Sequence[int], q: Sequence[int]) -> Accounting:
-    """b has n+1 entries (x_0..x_n), a and q have n entries."""
+def account(p: Plan, b: Sequence[int], a: Sequence[int], q: Sequence[int], slot=None,
+            extra: int = 0) -> Accounting:
+    """b has n+1 entries (x_0..x_n), a and q have n entries; slot and extra
+    describe the gradient buffers when they differ from the boundaries."""
     n = p.n
     assert len(b) == n + 1 and len(a) == n and len(q) == n
-    G = grad_bytes(b, q)
+    G = grad_bytes(b, q, slot, extra)
     if p.mode == RECURSIVE:
         arena = 0
         stack: List[int] = []

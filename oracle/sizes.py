@@ -20,6 +20,17 @@ Unit kinds (fp32 unless stated):
 * basic block (Cin -> Cout, output side S): a = conv1 output, relu(bn1)
   output, conv2 output (3 x 4NSSCout) + two BN mean/rstd pairs (2 x 8Cout);
   q = two [N,S,S,Cout] tensors.
+* LSTM step (batch B, hidden H, vocabulary V; bf16 GEMM operands): b = h
+  (bf16, 2BH) + c (fp32, 4BH); a = activated gates i,f,g,o (fp32, 16BH) +
+  the softmax gradient of its head (fp32, 4BV); q = the total hidden-state
+  gradient (fp32, 4BH).  The gradient slot holds (dh, dc) in fp32 (2 x 4BH),
+  and the weight gradients of the shared parameters are accumulated over
+  fixed chunks of C time steps, which needs per-chunk copies of dz (bf16,
+  C*B*4H*2), the head gradient (bf16, C*B*V*2) and h_{t-1}, h_t (bf16, 2 x
+  C*B*H*2): those chunk buffers are counted with the gradient buffers.
+
+``grad_layout`` returns (gradient slot bytes, extra gradient bytes); for the
+feed-forward chains the slot is the largest boundary and there is no extra.
 
 Parity: the accounting that consumes these tables is pinned in
 tests/test_oracle_planner.py; the tables themselves are restated layout
@@ -59,7 +70,30 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
                 q.append(2 * t)
             b.append(t)
         return b, a, q
+    if k == "lstm":
+        B, H, V, n = cfg["batch"], cfg["hidden"], cfg["vocab"], structure.n
+        bb = align(2 * B * H) + align(4 * B * H)
+        aa = align(16 * B * H) + align(4 * B * V)
+        qq = align(4 * B * H)
+        return [bb] * (n + 1), [aa] * n, [qq] * n
     raise NotImplementedError(f"size table for {k}")
+
+
+LSTM_GRAD_CHUNK = 32
+
+
+def grad_layout(structure, grad_chunk=None):
+    """(gradient slot bytes, extra gradient bytes) of the static layout;
+    grad_chunk is the LSTM's weight-gradient chunk (None or 0: the default)."""
+    b, _, _ = tables(structure)
+    if structure.kind == "lstm":
+        cfg = structure.cfg
+        B, H, V = cfg["batch"], cfg["hidden"], cfg["vocab"]
+        C = grad_chunk or LSTM_GRAD_CHUNK
+        slot = 2 * align(4 * B * H)
+        extra = align(C * B * 4 * H * 2) + align(C * B * V * 2) + 2 * align(C * B * H * 2)
+        return slot, extra
+    return max(b[1:]), 0
 
 
 def layer_and_cut_bytes(structure):

@@ -22,7 +22,7 @@ _lib = C.CDLL(LIB_PATH)
 OK, E_INVALID, E_WORKSPACE, E_MISMATCH, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4
 FLAG_KEEP_LAST = 1
-NET_MLP, NET_RESNET_BASIC = 1, 2
+NET_MLP, NET_RESNET_BASIC, NET_LSTM = 1, 2, 3
 
 _u64p = C.POINTER(C.c_uint64)
 _i32p = C.POINTER(C.c_int32)
@@ -31,7 +31,7 @@ _i32p = C.POINTER(C.c_int32)
 class NetDesc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("batch", C.c_int32), ("depth", C.c_int32),
                 ("width", C.c_int32), ("image", C.c_int32), ("n_classes", C.c_int32),
-                ("reserved", C.c_int32 * 10)]
+                ("grad_chunk", C.c_int32), ("reserved", C.c_int32 * 9)]
 
 
 class Batch(C.Structure):
@@ -66,6 +66,7 @@ _sig("net_destroy", None, [C.c_void_p])
 _sig("net_units", C.c_int, [C.c_void_p, _i32p])
 _sig("net_unit_sizes", C.c_int, [C.c_void_p, _u64p, _u64p, _u64p])
 _sig("net_layer_sizes", C.c_int, [C.c_void_p, _u64p, _u64p])
+_sig("net_grad_bytes", C.c_int, [C.c_void_p, _u64p, _u64p])
 _sig("net_param_bytes", C.c_int, [C.c_void_p, _u64p])
 _sig("net_param_count", C.c_int, [C.c_void_p, _i32p])
 _sig("net_param_info", C.c_int, [C.c_void_p, C.c_int32, C.c_char_p, C.c_int32, _u64p, _u64p])
@@ -80,7 +81,7 @@ _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch
 
 EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
             "plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
-            "net_layer_sizes", "net_param_bytes", "net_param_count", "net_param_info",
+            "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
             "train_step"]
 
@@ -165,8 +166,8 @@ class Net:
     """Owner of a library net object (host descriptor)."""
 
     def __init__(self, kind: int, batch: int, depth: int, width: int, image: int = 0,
-                 n_classes: int = 0):
-        d = NetDesc(kind, batch, depth, width, image, n_classes)
+                 n_classes: int = 0, grad_chunk: int = 0):
+        d = NetDesc(kind, batch, depth, width, image, n_classes, grad_chunk)
         h = C.c_void_p()
         _check(_lib.net_create(C.byref(d), C.byref(h)))
         self._h = h
@@ -192,6 +193,11 @@ class Net:
         lb, cb = (C.c_uint64 * n)(), (C.c_uint64 * n)()
         _check(_lib.net_layer_sizes(self._h, lb, cb))
         return list(lb), list(cb)
+
+    def grad_bytes(self) -> Tuple[int, int]:
+        slot, extra = C.c_uint64(), C.c_uint64()
+        _check(_lib.net_grad_bytes(self._h, C.byref(slot), C.byref(extra)))
+        return slot.value, extra.value
 
     def param_bytes(self) -> int:
         v = C.c_uint64()
@@ -239,8 +245,8 @@ class Net:
 
 
 def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,
-               n_classes: int = 0) -> Net:
-    return Net(kind, batch, depth, width, image, n_classes)
+               n_classes: int = 0, grad_chunk: int = 0) -> Net:
+    return Net(kind, batch, depth, width, image, n_classes, grad_chunk)
 
 
 def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,

@@ -108,10 +108,13 @@ int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
     *out = nullptr;
     for (int32_t r : desc->reserved)
       if (r != 0) ckpt::fail(CKPT_E_INVALID, "net_create: reserved fields must be zero");
+    if (desc->kind != CKPT_NET_LSTM && desc->grad_chunk != 0)
+      ckpt::fail(CKPT_E_INVALID, "net_create: grad_chunk applies to LSTM only");
     auto h = std::make_unique<ckpt_net>();
     switch (desc->kind) {
       case CKPT_NET_MLP: h->net = ckpt::make_mlp_net(*desc); break;
       case CKPT_NET_RESNET_BASIC: h->net = ckpt::make_resnet_basic_net(*desc); break;
+      case CKPT_NET_LSTM: h->net = ckpt::make_lstm_net(*desc); break;
       default: ckpt::fail(CKPT_E_INVALID, "net_create: unknown network kind");
     }
     *out = h.release();
@@ -135,6 +138,14 @@ int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q) {
     if (b) std::memcpy(b, N.b.data(), N.b.size() * 8);
     if (a) std::memcpy(a, N.a.data(), N.a.size() * 8);
     if (q) std::memcpy(q, N.q.data(), N.q.size() * 8);
+  });
+}
+
+int net_grad_bytes(const ckpt_net *net, uint64_t *slot, uint64_t *extra) {
+  return guarded([&] {
+    need(net, "net_grad_bytes");
+    if (slot) *slot = net->net->slot_bytes();
+    if (extra) *extra = net->net->grad_extra;
   });
 }
 
@@ -189,7 +200,7 @@ int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt_b
     need(plan, "plan_accounting(plan)");
     if (plan->p.n != net->net->n)
       ckpt::fail(CKPT_E_MISMATCH, "plan_accounting: plan n differs from the net's unit count");
-    auto acc = ckpt::account(plan->p, net->net->b, net->net->a, net->net->q);
+    auto acc = net->net->accounting(plan->p);
     if (ckpt_b) *ckpt_b = acc.ckpt;
     if (arena) *arena = acc.arena;
     if (grad) *grad = acc.grad;
@@ -204,7 +215,7 @@ int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *by
     need(bytes, "net_workspace_bytes(bytes)");
     if (plan->p.n != net->net->n)
       ckpt::fail(CKPT_E_MISMATCH, "net_workspace_bytes: plan n differs from the net's unit count");
-    auto acc = ckpt::account(plan->p, net->net->b, net->net->a, net->net->q);
+    auto acc = net->net->accounting(plan->p);
     *bytes = ckpt::workspace_bytes(*net->net, acc);
   });
 }

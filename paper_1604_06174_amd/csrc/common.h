@@ -51,9 +51,10 @@ struct Accounting {
 Plan make_plan(int32_t n, const uint64_t *layer_bytes, const uint64_t *cut_bytes, uint64_t budget,
                int32_t mode, const int32_t *user_cuts, int32_t n_user_cuts, int32_t flags);
 std::vector<uint8_t> serialize(const Plan &p);
-// b: n+1 entries, a and q: n entries
+// b: n+1 entries, a and q: n entries; slot = gradient slot bytes (0: the
+// largest boundary), extra = fixed gradient buffers
 Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
-                   const std::vector<uint64_t> &q);
+                   const std::vector<uint64_t> &q, uint64_t slot = 0, uint64_t extra = 0);
 uint64_t recursive_extra(int32_t n);
 
 }  // namespace ckpt

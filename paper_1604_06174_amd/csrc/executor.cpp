@@ -201,7 +201,7 @@ uint64_t workspace_bytes(const Net &net, const Accounting &acc) {
 void run_train_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
                     const Plan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
                     float *loss_host, uint64_t *peak, ckpt_step_stats *stats) {
-  Accounting acc = account(p, net.b, net.a, net.q);
+  Accounting acc = net.accounting(p);
   const uint64_t need = workspace_bytes(net, acc);
   if (ws_bytes < need)
     fail(CKPT_E_WORKSPACE, "train_step: workspace has " + std::to_string(ws_bytes) +
@@ -216,11 +216,14 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
   char *arena = ckpt + align256(acc.ckpt);
   char *grad = arena + align256(acc.arena);
   c.ks = grad + align256(acc.grad);
-  uint64_t maxb = 0;
-  for (int32_t i = 1; i <= net.n; ++i) maxb = std::max(maxb, net.b[size_t(i)]);
+  const uint64_t slot = net.slot_bytes();
+  uint64_t maxq = 0;
+  for (int32_t i = 0; i < net.n; ++i) maxq = std::max(maxq, net.q[size_t(i)]);
+  c.gextra = grad + 2 * slot + maxq;
 
-  Exec e{net, c, acc, ckpt, arena, {grad, grad + maxb}, grad + 2 * maxb};
+  Exec e{net, c, acc, ckpt, arena, {grad, grad + slot}, grad + 2 * slot};
   (void)hipGetLastError();  // clear a stale error left by the caller
+  net.begin_step(c);
   if (p.mode == CKPT_RECURSIVE)
     e.recursive(p, batch.input);
   else

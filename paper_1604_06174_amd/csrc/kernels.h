@@ -62,4 +62,26 @@ void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X,
                      const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
                      float *G, float *dW, float *db, float *loss);
 
+// ---- bf16 GEMM (gemm_bf16.hip) ----
+// C[M,N] fp32 = op(A) op(B) (+ bias | + D).  A is bf16, or fp32 rounded to
+// bf16 on load (a_fp32); B is bf16.  ak / bk: the operand is stored with k
+// contiguous (A[m*lda + k], B[n*ldb + k]); otherwise A[k*lda + m], B[k*ldb + n].
+void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
+               const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D = nullptr,
+               int ldd = 0, const float *bias = nullptr);
+
+// ---- LSTM step kernels (lstm.hip) ----
+void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst);  // dst[c][r]
+void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst);
+void lstm_fwd_point(hipStream_t s, int B, int H, const float *z, const float *c_prev, float *gates,
+                    void *h_out, float *c_out);
+void softmax_ce_rows(hipStream_t s, int rows, int V, const float *logits, const int *labels,
+                     float scale, float *dlog, float *loss_rows);
+void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first);
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dh, const float *dc_in, const float *gates,
+                    const float *c_t, const float *c_prev, const void *h_prev, const void *h_t, void *dz,
+                    float *dc_prev, void *hp_copy, void *hc_copy, float *db, bool first);
+void loss_reduce(hipStream_t s, int64_t rows, const float *v, float scale, float *loss);
+void fill_f32(hipStream_t s, int64_t n, float *p, float v);
+
 }  // namespace ckpt

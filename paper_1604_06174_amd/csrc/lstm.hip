@@ -1,0 +1,245 @@
+// Pointwise and row kernels of the LSTM step with its softmax head.
+//   gates  i, f, g, o = sigma(z_i), sigma(z_f), tanh(z_g), sigma(z_o)
+//          (z columns [0,H), [H,2H), [2H,3H), [3H,4H))
+//   cell   c_t = f c_{t-1} + i g,   h_t = o tanh(c_t)   (c fp32, h rounded to bf16)
+//   head   softmax cross-entropy of a [B, V] row block; the gradient
+//          (p - onehot) * scale is kept in fp32
+// Column sums for the bias gradients run over the batch rows in order inside
+// one thread, and accumulate across time steps in backward order, so they are
+// bit-reproducible.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace ckpt {
+namespace {
+
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+// dst[c][r] = bf16(src[r][c]) for src [R][C] fp32, through 32x32 LDS tiles.
+__global__ __launch_bounds__(256) void k_transpose_bf16(int R, int C, const float *__restrict__ src,
+                                                        __bf16 *__restrict__ dst) {
+  __shared__ float t[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) {
+    const int r = r0 + k, c = c0 + tx;
+    t[k][tx] = (r < R && c < C) ? src[size_t(r) * C + c] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int c = c0 + k, r = r0 + tx;
+    if (c < C && r < R) dst[size_t(c) * R + r] = (__bf16)t[tx][k];
+  }
+}
+
+__global__ __launch_bounds__(256) void k_cvt_bf16(int64_t n, const float *__restrict__ src,
+                                                  __bf16 *__restrict__ dst) {
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < n; e += int64_t(gridDim.x) * 256)
+    dst[e] = (__bf16)src[e];
+}
+
+// one thread per (b, j)
+__global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const float *__restrict__ z,
+                                                        const float *__restrict__ c_prev,
+                                                        float *__restrict__ gates,
+                                                        __bf16 *__restrict__ h_out,
+                                                        float *__restrict__ c_out) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= B * H) return;
+  const int b = e / H, j = e % H;
+  const float *zr = z + size_t(b) * 4 * H;
+  const float ig = sigm(zr[j]), fg = sigm(zr[H + j]), gg = tanhf(zr[2 * H + j]), og = sigm(zr[3 * H + j]);
+  const float cp = c_prev ? c_prev[e] : 0.f;
+  const float c = fg * cp + ig * gg;
+  float *gr = gates + size_t(b) * 4 * H;
+  gr[j] = ig;
+  gr[H + j] = fg;
+  gr[2 * H + j] = gg;
+  gr[3 * H + j] = og;
+  c_out[e] = c;
+  h_out[e] = (__bf16)(og * tanhf(c));
+}
+
+// One workgroup per row: loss_row = log sum exp(l - max) + max - l[label];
+// dlog = (softmax - onehot) * scale.  A label outside [0, V) gives a NaN loss
+// for the row and no one-hot term.
+__global__ __launch_bounds__(256) void k_softmax_ce_rows(int V, const float *__restrict__ logits,
+                                                         const int *__restrict__ labels, float scale,
+                                                         float *__restrict__ dlog,
+                                                         float *__restrict__ loss_rows) {
+  __shared__ float red[256];
+  const int row = blockIdx.x, t = threadIdx.x;
+  const float *l = logits + size_t(row) * V;
+  float mx = -INFINITY;
+  for (int v = t; v < V; v += 256) mx = fmaxf(mx, l[v]);
+  red[t] = mx;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float se = 0.f;
+  for (int v = t; v < V; v += 256) se += expf(l[v] - mx);
+  red[t] = se;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] += red[t + w];
+    __syncthreads();
+  }
+  se = red[0];
+  const int lab = labels[row];
+  const bool ok = lab >= 0 && lab < V;
+  if (t == 0) loss_rows[row] = ok ? (logf(se) + mx) - l[lab] : NAN;
+  const float inv = 1.0f / se;
+  float *d = dlog + size_t(row) * V;
+  for (int v = t; v < V; v += 256) d[v] = (expf(l[v] - mx) * inv - (v == lab ? 1.f : 0.f)) * scale;
+}
+
+// Workgroup = 64 columns x 4 row groups (rows b = rg, rg + 4, ...); the
+// column sums of the groups are combined in order ((s0 + s1) + s2) + s3.
+
+// dl_bf[b][v] = bf16(dlog[b][v]);  db_o[v] (+)= sum_b dlog[b][v]
+__global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float *__restrict__ dlog,
+                                                       __bf16 *__restrict__ dl_bf,
+                                                       float *__restrict__ db_o, int first) {
+  __shared__ float part[4][64];
+  const int cx = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int v = blockIdx.x * 64 + cx;
+  float s = 0.f;
+  if (v < V)
+    for (int b = rg; b < B; b += 4) {
+      const float d = dlog[size_t(b) * V + v];
+      dl_bf[size_t(b) * V + v] = (__bf16)d;
+      s += d;
+    }
+  part[rg][cx] = s;
+  __syncthreads();
+  if (rg == 0 && v < V) {
+    const float t = ((part[0][cx] + part[1][cx]) + part[2][cx]) + part[3][cx];
+    db_o[v] = first ? t : db_o[v] + t;
+  }
+}
+
+// Gate backward for hidden unit j and rows b = rg, rg + 4, ...
+__global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const float *__restrict__ dh,
+                                                        const float *__restrict__ dc_in,
+                                                        const float *__restrict__ gates,
+                                                        const float *__restrict__ c_t,
+                                                        const float *__restrict__ c_prev,
+                                                        const __bf16 *__restrict__ h_prev,
+                                                        const __bf16 *__restrict__ h_t,
+                                                        __bf16 *__restrict__ dz,
+                                                        float *__restrict__ dc_prev,
+                                                        __bf16 *__restrict__ hp_copy,
+                                                        __bf16 *__restrict__ hc_copy,
+                                                        float *__restrict__ db, int first) {
+  __shared__ float part[4][4][64];
+  const int cx = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + cx;
+  float sm[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < H)
+    for (int b = rg; b < B; b += 4) {
+      const size_t e = size_t(b) * H + j;
+      const float *gr = gates + size_t(b) * 4 * H;
+      const float ig = gr[j], fg = gr[H + j], gg = gr[2 * H + j], og = gr[3 * H + j];
+      const float tc = tanhf(c_t[e]);
+      const float dhv = dh[e];
+      const float dct = dc_in[e] + dhv * og * (1.f - tc * tc);
+      const float cp = c_prev ? c_prev[e] : 0.f;
+      const float zv[4] = {dct * gg * ig * (1.f - ig), dct * cp * fg * (1.f - fg),
+                           dct * ig * (1.f - gg * gg), dhv * tc * og * (1.f - og)};
+      __bf16 *dr = dz + size_t(b) * 4 * H;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        dr[k * H + j] = (__bf16)zv[k];
+        sm[k] += zv[k];
+      }
+      if (dc_prev) dc_prev[e] = dct * fg;
+      hp_copy[e] = h_prev ? h_prev[e] : (__bf16)0.f;
+      hc_copy[e] = h_t[e];
+    }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) part[k][rg][cx] = sm[k];
+  __syncthreads();
+  if (rg == 0 && j < H) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float t = ((part[k][0][cx] + part[k][1][cx]) + part[k][2][cx]) + part[k][3][cx];
+      db[k * H + j] = first ? t : db[k * H + j] + t;
+    }
+  }
+}
+
+// loss = scale * sum of rows (fixed order: thread t takes rows t, t+1024, ...)
+__global__ __launch_bounds__(1024) void k_loss_reduce(int64_t rows, const float *__restrict__ v,
+                                                      float scale, float *__restrict__ loss) {
+  __shared__ float red[1024];
+  float s = 0.f;
+  for (int64_t r = threadIdx.x; r < rows; r += 1024) s += v[r];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) loss[0] = red[0] * scale;
+}
+
+__global__ __launch_bounds__(256) void k_fill_f32(int64_t n, float *__restrict__ p, float v) {
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < n; e += int64_t(gridDim.x) * 256) p[e] = v;
+}
+
+inline int grid_for(int64_t n) {
+  int64_t g = (n + 255) / 256;
+  return int(g < 1 ? 1 : (g > 8192 ? 8192 : g));
+}
+
+}  // namespace
+
+void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst) {
+  hipLaunchKernelGGL(k_transpose_bf16, dim3((C + 31) / 32, (R + 31) / 32), dim3(256), 0, s, R, C,
+                     src, static_cast<__bf16 *>(dst));
+}
+
+void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst) {
+  hipLaunchKernelGGL(k_cvt_bf16, dim3(grid_for(n)), dim3(256), 0, s, n, src, static_cast<__bf16 *>(dst));
+}
+
+void lstm_fwd_point(hipStream_t s, int B, int H, const float *z, const float *c_prev, float *gates,
+                    void *h_out, float *c_out) {
+  hipLaunchKernelGGL(k_lstm_fwd_point, dim3((B * H + 255) / 256), dim3(256), 0, s, B, H, z, c_prev,
+                     gates, static_cast<__bf16 *>(h_out), c_out);
+}
+
+void softmax_ce_rows(hipStream_t s, int rows, int V, const float *logits, const int *labels,
+                     float scale, float *dlog, float *loss_rows) {
+  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(256), 0, s, V, logits, labels, scale, dlog,
+                     loss_rows);
+}
+
+void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {
+  hipLaunchKernelGGL(k_head_bwd_prep, dim3((V + 63) / 64), dim3(256), 0, s, B, V, dlog,
+                     static_cast<__bf16 *>(dl_bf), db_o, first ? 1 : 0);
+}
+
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dh, const float *dc_in, const float *gates,
+                    const float *c_t, const float *c_prev, const void *h_prev, const void *h_t, void *dz,
+                    float *dc_prev, void *hp_copy, void *hc_copy, float *db, bool first) {
+  hipLaunchKernelGGL(k_lstm_bwd_point, dim3((H + 63) / 64), dim3(256), 0, s, B, H, dh, dc_in, gates,
+                     c_t, c_prev, static_cast<const __bf16 *>(h_prev), static_cast<const __bf16 *>(h_t),
+                     static_cast<__bf16 *>(dz), dc_prev, static_cast<__bf16 *>(hp_copy),
+                     static_cast<__bf16 *>(hc_copy), db, first ? 1 : 0);
+}
+
+void loss_reduce(hipStream_t s, int64_t rows, const float *v, float scale, float *loss) {
+  hipLaunchKernelGGL(k_loss_reduce, dim3(1), dim3(1024), 0, s, rows, v, scale, loss);
+}
+
+void fill_f32(hipStream_t s, int64_t n, float *p, float v) {
+  hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(n)), dim3(256), 0, s, n, p, v);
+}
+
+}  // namespace ckpt

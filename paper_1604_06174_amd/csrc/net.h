@@ -75,6 +75,7 @@ struct StepCtx {
   const void *input = nullptr;    // device, batch input
   const void *target = nullptr;   // device, batch targets
   char *ks = nullptr;             // device operator workspace (net.ks_bytes)
+  char *gextra = nullptr;         // device fixed gradient buffers (net.grad_extra)
   uint64_t launches = 0;
 };
 
@@ -91,6 +92,8 @@ class Net {
   std::vector<Tensor> params;
   uint64_t param_bytes = 0;
   uint64_t ks_bytes = 0;          // operator workspace (not part of the peak)
+  uint64_t gslot_bytes = 0;       // one gradient slot (0: the largest boundary)
+  uint64_t grad_extra = 0;        // fixed gradient buffers (part of the peak)
   KernelTimer timer;              // times `timed_family` launches when enabled
   std::string timed_family;       // kernel-name prefix of the timed family
 
@@ -103,6 +106,8 @@ class Net {
   // parameter gradients.
   virtual void bwd(int32_t i, const void *g, void *dx, const void *x, const void *y,
                    const void *saved, void *q, StepCtx &c) = 0;
+  // Called once at the start of every step, before any unit runs.
+  virtual void begin_step(StepCtx &) {}
   // Head: x_n -> g = dL/dx_n (+ head parameter gradients), loss into ks.
   virtual void head(const void *xn, void *g, StepCtx &c) = 0;
   // Device address of the f32 loss after the step.
@@ -110,6 +115,14 @@ class Net {
 
   const float *P(const StepCtx &c, int k) const { return c.params + params[size_t(k)].off / 4; }
   float *G(const StepCtx &c, int k) const { return c.grads + params[size_t(k)].off / 4; }
+
+  Accounting accounting(const Plan &p) const { return account(p, b, a, q, gslot_bytes, grad_extra); }
+  uint64_t slot_bytes() const {
+    if (gslot_bytes) return gslot_bytes;
+    uint64_t m = 0;
+    for (size_t i = 1; i < b.size(); ++i) m = b[i] > m ? b[i] : m;
+    return m;
+  }
 
  protected:
   int add_param(const std::string &name, uint64_t numel) {
@@ -121,5 +134,6 @@ class Net {
 
 std::unique_ptr<Net> make_mlp_net(const ckpt_net_desc &d);
 std::unique_ptr<Net> make_resnet_basic_net(const ckpt_net_desc &d);
+std::unique_ptr<Net> make_lstm_net(const ckpt_net_desc &d);
 
 }  // namespace ckpt

@@ -1,0 +1,196 @@
+// Single-layer LSTM unrolled over T steps with a softmax head at every step
+// (the long-sequence recurrent workload of the paper's section 5.3).  Unit t
+// maps the state (h_{t-1}, c_{t-1}) to (h_t, c_t) and adds the step's
+// cross-entropy to the loss; the chain's own head is empty (g = 0).
+//
+//   z_t      = x_t W_x + h_{t-1} W_h + b          bf16 operands, fp32 accumulation
+//   gates    i, f, g, o;  c_t = f c_{t-1} + i g;  h_t = o tanh(c_t)   (c fp32, h bf16)
+//   logits_t = h_t W_o + b_o;  loss += sum_b CE(logits_t[b], label_t[b]) / (T B)
+//
+// Shared parameters: their gradients are summed in backward order, T-1 -> 0.
+// Weight gradients are computed per fixed chunk of C aligned steps (one GEMM
+// over the chunk's C*B rows, accumulated chunk after chunk in backward order);
+// the chunk grouping does not depend on the plan, so every plan gives the same
+// bytes.  Bias gradients accumulate step by step.
+//
+// Static layout: boundary b = h (bf16 [B,H]) | c (fp32 [B,H]); saved a = gates
+// (fp32 [B,4H]) | softmax gradient (fp32 [B,V]); scratch q = total dh (fp32
+// [B,H]); gradient slot = dh | dc (fp32); extra gradient buffers = the chunk's
+// dz (bf16 [C*B,4H]), head gradient (bf16 [C*B,V]), h_{t-1} and h_t copies
+// (bf16 [C*B,H]).
+#include "kernels.h"
+#include "net.h"
+
+namespace ckpt {
+namespace {
+
+class LstmNet : public Net {
+ public:
+  int T, B, E, H, V, C;
+  int pWx, pWh, pb, pWo, pbo;
+  uint64_t hb, cb;  // boundary parts
+  uint64_t ga, da;  // saved parts: gates, dlog
+  // operator workspace offsets
+  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_z, k_logits, k_lossrows, k_loss;
+  // extra gradient buffer offsets
+  uint64_t x_dz, x_dl, x_hp, x_hc;
+
+  explicit LstmNet(const ckpt_net_desc &d) {
+    desc = d;
+    T = d.depth;
+    B = d.batch;
+    H = d.width;
+    E = d.image;
+    V = d.n_classes;
+    C = d.grad_chunk > 0 ? d.grad_chunk : 32;
+    n = T;
+    pWx = add_param("W_x", uint64_t(E) * 4 * H);
+    pWh = add_param("W_h", uint64_t(H) * 4 * H);
+    pb = add_param("b", uint64_t(4) * H);
+    pWo = add_param("W_o", uint64_t(H) * V);
+    pbo = add_param("b_o", uint64_t(V));
+    hb = align256(2ull * B * H);
+    cb = align256(4ull * B * H);
+    ga = align256(16ull * B * H);
+    da = align256(4ull * B * V);
+    b.assign(size_t(n) + 1, hb + cb);
+    a.assign(size_t(n), ga + da);
+    q.assign(size_t(n), align256(4ull * B * H));
+    gslot_bytes = 2 * align256(4ull * B * H);
+    uint64_t off = 0;
+    auto take = [&](uint64_t bytes) {
+      uint64_t o = off;
+      off += align256(bytes);
+      return o;
+    };
+    x_dz = take(uint64_t(C) * B * 4 * H * 2);
+    x_dl = take(uint64_t(C) * B * V * 2);
+    x_hp = take(uint64_t(C) * B * H * 2);
+    x_hc = take(uint64_t(C) * B * H * 2);
+    grad_extra = off;
+    off = 0;
+    k_wxt = take(uint64_t(E) * 4 * H * 2);
+    k_wht = take(uint64_t(H) * 4 * H * 2);
+    k_wh = take(uint64_t(H) * 4 * H * 2);
+    k_wot = take(uint64_t(H) * V * 2);
+    k_wo = take(uint64_t(H) * V * 2);
+    k_z = take(uint64_t(B) * 4 * H * 4);
+    k_logits = take(uint64_t(B) * V * 4);
+    k_lossrows = take(uint64_t(T) * B * 4);
+    k_loss = take(4);
+    ks_bytes = off;
+    timed_family = "k_gemm_bf16";
+  }
+
+  char *K(StepCtx &c, uint64_t o) const { return c.ks + o; }
+  float *Kf(StepCtx &c, uint64_t o) const { return reinterpret_cast<float *>(c.ks + o); }
+  char *X(StepCtx &c, uint64_t o) const { return c.gextra + o; }
+
+  void gemm(StepCtx &c, int M, int N, int Kd, const void *A, bool a32, int lda, bool ak,
+            const void *Bm, int ldb, bool bk, float *Cm, int ldc, int epi, const float *D = nullptr,
+            int ldd = 0, const float *bias = nullptr) {
+    timer.begin(c.s);
+    gemm_bf16(c.s, M, N, Kd, A, a32, lda, ak, Bm, ldb, bk, Cm, ldc, epi, D, ldd, bias);
+    timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
+    c.launches += 1;
+  }
+
+  void begin_step(StepCtx &c) override {
+    // bf16 copies of the weights in the layouts the GEMMs read (k contiguous)
+    transpose_bf16(c.s, E, 4 * H, P(c, pWx), K(c, k_wxt));  // [4H][E]
+    transpose_bf16(c.s, H, 4 * H, P(c, pWh), K(c, k_wht));  // [4H][H]
+    cvt_bf16(c.s, int64_t(H) * 4 * H, P(c, pWh), K(c, k_wh));  // [H][4H]
+    transpose_bf16(c.s, H, V, P(c, pWo), K(c, k_wot));        // [V][H]
+    cvt_bf16(c.s, int64_t(H) * V, P(c, pWo), K(c, k_wo));      // [H][V]
+    c.launches += 5;
+  }
+
+  void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
+    const char *x = static_cast<const char *>(xv);
+    char *y = static_cast<char *>(yv);
+    char *sv = static_cast<char *>(saved);
+    const void *xt = static_cast<const char *>(c.input) + size_t(i) * B * E * 2;
+    const int *lab = static_cast<const int *>(c.target) + size_t(i) * B;
+    float *z = Kf(c, k_z);
+    gemm(c, B, 4 * H, E, xt, false, E, true, K(c, k_wxt), E, true, z, 4 * H, GEMM_EPI_STORE, nullptr,
+         0, P(c, pb));
+    if (i > 0)
+      gemm(c, B, 4 * H, H, x, false, H, true, K(c, k_wht), H, true, z, 4 * H, GEMM_EPI_ADD, z, 4 * H);
+    const float *c_prev = i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr;
+    float *gates = reinterpret_cast<float *>(sv);
+    lstm_fwd_point(c.s, B, H, z, c_prev, gates, y, reinterpret_cast<float *>(y + hb));
+    float *logits = Kf(c, k_logits);
+    gemm(c, B, V, H, y, false, H, true, K(c, k_wot), H, true, logits, V, GEMM_EPI_STORE, nullptr, 0,
+         P(c, pbo));
+    softmax_ce_rows(c.s, B, V, logits, lab, 1.0f / (float(T) * float(B)),
+                    reinterpret_cast<float *>(sv + ga), Kf(c, k_lossrows) + size_t(i) * B);
+    c.launches += 2;
+  }
+
+  void bwd(int32_t i, const void *gv, void *dxv, const void *xv, const void *yv, const void *saved,
+           void *qv, StepCtx &c) override {
+    const char *g = static_cast<const char *>(gv);
+    const char *x = static_cast<const char *>(xv);
+    const char *y = static_cast<const char *>(yv);
+    const char *sv = static_cast<const char *>(saved);
+    char *dx = static_cast<char *>(dxv);
+    const uint64_t gh = align256(4ull * B * H);  // dh part of a gradient slot
+    const int t0 = (i / C) * C;
+    const size_t row = size_t(i - t0) * B;
+    const bool first_step = i == n - 1;
+    char *dl = X(c, x_dl) + row * V * 2;
+    char *dz = X(c, x_dz) + row * 4 * H * 2;
+    char *hp = X(c, x_hp) + row * H * 2;
+    char *hc = X(c, x_hc) + row * H * 2;
+    head_bwd_prep(c.s, B, V, reinterpret_cast<const float *>(sv + ga), dl, G(c, pbo), first_step);
+    float *dh = static_cast<float *>(qv);
+    gemm(c, B, H, V, dl, false, V, true, K(c, k_wo), V, true, dh, H, GEMM_EPI_ADD,
+         reinterpret_cast<const float *>(g), H);
+    lstm_bwd_point(c.s, B, H, dh, reinterpret_cast<const float *>(g + gh),
+                   reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
+                   i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
+                   dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc, G(c, pb), first_step);
+    c.launches += 2;
+    if (dx)
+      gemm(c, B, H, 4 * H, dz, false, 4 * H, true, K(c, k_wh), 4 * H, true,
+           reinterpret_cast<float *>(dx), H, GEMM_EPI_STORE);
+    if (i == t0) {  // the chunk [t0, t0 + C) is complete: its weight gradients
+      const int rows = (std::min(t0 + C, int(n)) - t0) * B;
+      const bool first_chunk = t0 + C >= n;
+      const int epi = first_chunk ? GEMM_EPI_STORE : GEMM_EPI_ADD;
+      const void *xs = static_cast<const char *>(c.input) + size_t(t0) * B * E * 2;
+      gemm(c, E, 4 * H, rows, xs, false, E, false, X(c, x_dz), 4 * H, false, G(c, pWx), 4 * H, epi,
+           G(c, pWx), 4 * H);
+      gemm(c, H, 4 * H, rows, X(c, x_hp), false, H, false, X(c, x_dz), 4 * H, false, G(c, pWh), 4 * H,
+           epi, G(c, pWh), 4 * H);
+      gemm(c, H, V, rows, X(c, x_hc), false, H, false, X(c, x_dl), V, false, G(c, pWo), V, epi,
+           G(c, pWo), V);
+    }
+  }
+
+  void head(const void *, void *g, StepCtx &c) override {
+    fill_f32(c.s, int64_t(gslot_bytes / 4), static_cast<float *>(g), 0.f);
+    loss_reduce(c.s, int64_t(T) * B, Kf(c, k_lossrows), 1.0f / (float(T) * float(B)), Kf(c, k_loss));
+    c.launches += 2;
+  }
+
+  const float *loss_ptr(const StepCtx &c) const override {
+    return reinterpret_cast<const float *>(c.ks + k_loss);
+  }
+};
+
+}  // namespace
+
+std::unique_ptr<Net> make_lstm_net(const ckpt_net_desc &d) {
+  if (d.batch <= 0 || d.depth <= 0 || d.width <= 0 || d.image <= 0 || d.n_classes <= 0 ||
+      d.grad_chunk < 0)
+    fail(CKPT_E_INVALID, "net_create: LSTM needs positive batch, steps, hidden, input and vocabulary");
+  if (d.width % 8 != 0 || d.image % 8 != 0 || d.n_classes % 8 != 0)
+    fail(CKPT_E_UNSUPPORTED, "net_create: LSTM sizes must be multiples of 8");
+  if (int64_t(d.depth) * d.batch * d.image > (int64_t(1) << 31) ||
+      int64_t(d.batch) * d.n_classes * 32 > (int64_t(1) << 31))
+    fail(CKPT_E_INVALID, "net_create: LSTM tensors too large");
+  return std::make_unique<LstmNet>(d);
+}
+
+}  // namespace ckpt

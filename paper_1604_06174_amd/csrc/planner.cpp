@@ -189,13 +189,13 @@ static void rec_account(RecState &st, int32_t lo, int32_t hi) {
 }
 
 Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
-                   const std::vector<uint64_t> &q) {
+                   const std::vector<uint64_t> &q, uint64_t slot, uint64_t extra) {
   const int32_t n = p.n;
   Accounting acc;
   uint64_t maxb = 0, maxq = 0;
   for (int32_t i = 1; i <= n; ++i) maxb = std::max(maxb, b[i]);
   for (int32_t i = 0; i < n; ++i) maxq = std::max(maxq, q[i]);
-  acc.grad = 2 * maxb + maxq;
+  acc.grad = 2 * (slot ? slot : maxb) + maxq + extra;
   if (p.mode == CKPT_RECURSIVE) {
     RecState st{b, a};
     if (n == 1) {

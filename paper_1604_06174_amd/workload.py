@@ -14,7 +14,6 @@ import torch
 
 from . import ckpt as K
 
-_KINDS = {"mlp": K.NET_MLP, "resnet_basic": K.NET_RESNET_BASIC}
 
 
 def net_for(cfg: Dict) -> K.Net:
@@ -24,6 +23,9 @@ def net_for(cfg: Dict) -> K.Net:
     if kind == "resnet_basic":
         return K.net_create(K.NET_RESNET_BASIC, cfg["batch"], cfg["blocks_per_stage"],
                             cfg.get("base", 16), cfg.get("image", 32), cfg.get("classes", 10))
+    if kind == "lstm":
+        return K.net_create(K.NET_LSTM, cfg["batch"], cfg["T"], cfg["hidden"], cfg["input"],
+                            cfg["vocab"], cfg.get("grad_chunk", 0))
     raise K.CkptError(K.E_UNSUPPORTED, f"no GPU network for workload kind {kind!r}")
 
 
@@ -45,6 +47,8 @@ class GpuStep:
             host[off // 4: off // 4 + numel] = v
         self.params.copy_(torch.from_numpy(host))
         self.input = torch.from_numpy(np.ascontiguousarray(inp)).to(self.device)
+        if cfg["kind"] == "lstm":  # the recurrent input is consumed as bf16
+            self.input = self.input.to(torch.bfloat16).contiguous()
         self.target = torch.from_numpy(np.ascontiguousarray(target)).to(self.device)
         self._ws = None
         self.loss_dev = torch.zeros(1, dtype=torch.float32, device=self.device)

@@ -96,7 +96,10 @@ WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
                  dict(kind="mlp", depth=7, width=40, batch=3),
                  dict(kind="resnet_basic", blocks_per_stage=18, base=16, batch=128, image=32,
                       classes=10),
-                 dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=3, image=12, classes=5)]
+                 dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=3, image=12, classes=5),
+                 dict(kind="lstm", T=4096, batch=64, input=1024, hidden=1024, vocab=10000),
+                 dict(kind="lstm", T=16384, batch=64, input=1024, hidden=1024, vocab=10000),
+                 dict(kind="lstm", T=13, batch=3, input=16, hidden=24, vocab=40, grad_chunk=4)]
 
 
 @pytest.mark.parametrize("cfg", WORKLOADS_CPU)
@@ -108,6 +111,8 @@ def test_net_tables_and_accounting_match_oracle(cfg):
     assert (b, a, q) == tuple(SZ.tables(st))
     lb, cb = net.layer_sizes()
     assert (lb, cb) == SZ.layer_and_cut_bytes(st)
+    slot, extra = SZ.grad_layout(st, cfg.get("grad_chunk"))
+    assert net.grad_bytes() == (slot, extra)
     n = st.n
     modes = [(PL.NONE, 0, 0), (PL.SQRT, 0, 0), (PL.SQRT, 8, PL.FLAG_KEEP_LAST),
              (PL.GREEDY, sum(lb) // 10, 0), (PL.RECURSIVE, 0, 0)]
@@ -115,7 +120,7 @@ def test_net_tables_and_accounting_match_oracle(cfg):
         lp = _lib_plan(n, lb, cb, budget, mode, flags=flags)
         op = PL.plan(n, lb, cb, budget, mode, flags=flags)
         acc = net.accounting(lp)
-        oacc = PL.account(op, b, a, q)
+        oacc = PL.account(op, b, a, q, slot, extra)
         assert (acc["ckpt"], acc["arena"], acc["grad"], acc["peak"]) == \
             (oacc.ckpt, oacc.arena, oacc.grad, oacc.peak)
         assert net.workspace_bytes(lp) >= acc["peak"]
@@ -123,7 +128,8 @@ def test_net_tables_and_accounting_match_oracle(cfg):
 
 @pytest.mark.parametrize("cfg", [dict(kind="mlp", depth=5, width=40, batch=3),
                                  dict(kind="resnet_basic", blocks_per_stage=3, base=8, batch=2,
-                                      image=16, classes=7)])
+                                      image=16, classes=7),
+                                 dict(kind="lstm", T=5, batch=2, input=16, hidden=8, vocab=24)])
 def test_param_layout_names_match_structure(cfg):
     from paper_1604_06174_amd.workload import net_for
     net = net_for(cfg)

@@ -45,9 +45,10 @@ def _plan_args(cfg, net):
     raise ValueError(mode)
 
 
-def _cpu_baseline(cfg, sample_batch):
+def _cpu_baseline(cfg, sample_batch, d_full):
     """The oracle's own checkpointed executor (Alg. 1 with the same plan) on a
-    smaller batch of the same network; samples/s = sample batch / wall time."""
+    smaller batch of the same network (the same parameters, the first samples
+    of the batch); samples/s = sample batch / wall time."""
     import numpy as np
     import synth
     from oracle import nets, planner as PL, schedule as SCH, sizes as SZ
@@ -69,19 +70,20 @@ def _cpu_baseline(cfg, sample_batch):
         c["batch"] = sample_batch
         what = f"{sample_batch} of its {cfg['batch']} samples"
         n_samples = sample_batch
-    d = synth.make(c)
-    chain = nets.Chain(d["structure"], d["params"])
-    lb, cb = SZ.layer_and_cut_bytes(d["structure"])
-    n = d["structure"].n
+    structure = synth.structure(c)
+    inp, tgt = d_full["input"][:sample_batch], d_full["target"][:sample_batch]
+    chain = nets.Chain(structure, d_full["params"])
+    lb, cb = SZ.layer_and_cut_bytes(structure)
+    n = structure.n
     mode = {"sqrt": PL.SQRT, "greedy": PL.GREEDY, "recursive": PL.RECURSIVE}[cfg.get("plan", "sqrt")]
     budget = int(cfg.get("stride", 0)) if mode == PL.SQRT else int(sum(lb) * cfg.get("budget_frac", 0.1))
     if mode == PL.SQRT:
         budget = min(budget, n) if budget else 0
     t0 = time.perf_counter()
     if mode == PL.RECURSIVE:
-        SCH.recursive_step(chain, d["input"], d["target"])
+        SCH.recursive_step(chain, inp, tgt)
     else:
-        SCH.segment_step(chain, d["input"], d["target"], PL.plan(n, lb, cb, budget, mode))
+        SCH.segment_step(chain, inp, tgt, PL.plan(n, lb, cb, budget, mode))
     dt = time.perf_counter() - t0
     return {"value": n_samples * scale / dt, "unit": "samples/s", "cores": int(threads),
             "kind": "oracle",
@@ -95,7 +97,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="cifar110")
-    ap.add_argument("--cpu-sample", type=int, default=128, help="batch of the CPU oracle sample (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="batch (LSTM: time steps) of the CPU oracle sample; 0 skips it, -1 picks "
+                         "about 10-30 s of oracle work for the workload")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -163,11 +167,14 @@ def main():
             "hbm_gbs_algorithmic": round(kt["bytes"] / (kt["ms"] / 1e3) / 1e9, 1) if kt["ms"] > 0 else 0}
 
     cpu = None
-    if args.cpu_sample > 0:
+    sample = args.cpu_sample
+    if sample < 0:
+        sample = {"lstm": 16, "resnet_bottleneck": 1}.get(cfg["kind"], 128)
+    if sample > 0:
         if cfg["kind"] == "lstm":
-            cpu = _cpu_baseline(cfg, min(16, cfg["T"]))
+            cpu = _cpu_baseline(cfg, min(sample, cfg["T"]), d)
         else:
-            cpu = _cpu_baseline(cfg, min(args.cpu_sample, cfg["batch"]))
+            cpu = _cpu_baseline(cfg, min(sample, cfg["batch"]), d)
 
     batch = cfg["batch"]
     out = {

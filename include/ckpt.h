@@ -115,19 +115,24 @@ void plan_free(ckpt_plan *plan);
 #define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
 #define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */
 #define CKPT_NET_LSTM              3 /* LSTM steps, each with a softmax head          */
+#define CKPT_NET_RESNET_BOTTLENECK 4 /* 7x7 stem + bottleneck stages + FC-CE, bf16     */
 
 typedef struct ckpt_net_desc {
   int32_t kind;          /* CKPT_NET_*                                             */
   int32_t batch;         /* samples per step                                       */
   int32_t depth;         /* MLP: blocks.  RESNET_BASIC: basic blocks per stage.
-                            LSTM: time steps T                                     */
+                            LSTM: time steps T.  RESNET_BOTTLENECK: stages (1-4)   */
   int32_t width;         /* MLP: width.   RESNET_BASIC: first-stage channels.
-                            LSTM: hidden size H                                    */
-  int32_t image;         /* RESNET_BASIC: input side (square images, 3 channels).
+                            LSTM: hidden size H.
+                            RESNET_BOTTLENECK: first-stage bottleneck width        */
+  int32_t image;         /* RESNET_*: input side (square images, 3 channels).
                             LSTM: input size E                                     */
-  int32_t n_classes;     /* RESNET_BASIC: classifier outputs.  LSTM: vocabulary V */
+  int32_t n_classes;     /* RESNET_*: classifier outputs.  LSTM: vocabulary V      */
   int32_t grad_chunk;    /* LSTM: time steps per weight-gradient chunk (0 = 32)    */
-  int32_t reserved[9];   /* must be zero                                           */
+  int32_t stage_blocks[4]; /* RESNET_BOTTLENECK: blocks per stage (zero past depth) */
+  int32_t expansion;     /* RESNET_BOTTLENECK: output channels / bottleneck width  */
+  int32_t stem_channels; /* RESNET_BOTTLENECK: channels of the stem's output       */
+  int32_t reserved[3];   /* must be zero                                           */
 } ckpt_net_desc;
 
 /*
@@ -152,8 +157,23 @@ typedef struct ckpt_net_desc {
  *                 [T, batch].  GEMM operands are bf16 (weights rounded once per
  *                 step), accumulation and the cell state fp32, h bf16.  Sizes
  *                 must be multiples of 8.
- * Errors: CKPT_E_INVALID for a null pointer, an unknown kind or a
- *   non-positive or inconsistent size.
+ *   RESNET_BOTTLENECK: n = 1 + sum(stage_blocks) units: stem conv7x7/2 (pad 3)
+ *                 3 -> stem_channels + BN + ReLU + max pool 3x3/2 (pad 1); then
+ *                 per stage t bottleneck blocks conv1x1 (width 2^t) - BN - ReLU
+ *                 - conv3x3 (stride 2 in the first block of stages t > 0) - BN
+ *                 - ReLU - conv1x1 (expansion x width 2^t) - BN, + shortcut
+ *                 (projection conv1x1 with the block's stride + BN in each
+ *                 stage's first block, else identity), ReLU; head as
+ *                 RESNET_BASIC (section 5.2's deep residual network).  Parameter
+ *                 order per block: W1, gamma1, beta1, W2, gamma2, beta2, W3,
+ *                 gamma3, beta3 [, Wp, gammap, betap]; conv weights [Cout, R, R,
+ *                 Cin].  Input bf16 NHWC [batch, image, image, 3]; target int32
+ *                 [batch].  Activations bf16, convolutions accumulate in fp32,
+ *                 batch-norm statistics from float64 sums.  Channel counts must
+ *                 be powers of two in [8, 2048] (CKPT_E_UNSUPPORTED otherwise)
+ *                 and every stride-2 stage input side even.
+ * Errors: CKPT_E_INVALID for a null pointer, an unknown kind, a field another
+ *   kind uses set to non-zero, or a non-positive or inconsistent size.
  */
 int net_create(const ckpt_net_desc *desc, ckpt_net **out);
 void net_destroy(ckpt_net *net);

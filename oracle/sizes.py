@@ -29,8 +29,21 @@ Unit kinds (fp32 unless stated):
   C*B*4H*2), the head gradient (bf16, C*B*V*2) and h_{t-1}, h_t (bf16, 2 x
   C*B*H*2): those chunk buffers are counted with the gradient buffers.
 
+* bottleneck ResNet (bf16 activations; B(m, c) = a bf16 tensor of m pixels x
+  c channels, F(m, c) the fp32 one): b_0 = the bf16 image batch.
+  - stem (conv7x7/2 output side s, C0 channels, m = N s s): a = conv output
+    and ReLU output (2 x B(m, C0)) + BN mean/rstd (8 C0); q = the max-pool
+    input gradient F(m, C0) + the BN input gradient B(m, C0); the boundary is
+    the pooled output.
+  - bottleneck (width w, output channels Co, mi / mo input / output pixels):
+    a = c1, r1 (B(mi, w) each), c2, r2 (B(mo, w) each), c3 (B(mo, Co)),
+    [cp (B(mo, Co))], BN pairs 8w, 8w, 8Co [, 8Co]; q = max(B(mo, Co),
+    B(mi, w)) + F(mi, w) + B(mo, w) [+ B(mo, Co)].
+  The gradient slot holds the largest fp32 boundary gradient.
+
 ``grad_layout`` returns (gradient slot bytes, extra gradient bytes); for the
-feed-forward chains the slot is the largest boundary and there is no extra.
+fp32 feed-forward chains the slot is the largest boundary and there is no
+extra.
 
 Parity: the accounting that consumes these tables is pinned in
 tests/test_oracle_planner.py; the tables themselves are restated layout
@@ -70,6 +83,34 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
                 q.append(2 * t)
             b.append(t)
         return b, a, q
+    if k == "resnet_bottleneck":
+        N = cfg["batch"]
+
+        def bf(m, c):
+            return align(2 * m * c)
+
+        def f32(m, c):
+            return align(4 * m * c)
+
+        img = cfg["image"]
+        side = (img + 2 * 3 - 7) // 2 + 1
+        b.append(bf(N * img * img, 3))
+        for u in structure.units:
+            if u.kind == "stem7":
+                m = N * side * side
+                a.append(2 * bf(m, u.cout) + align(8 * u.cout))
+                q.append(f32(m, u.cout) + bf(m, u.cout))
+            else:
+                mi, mo, w, co = N * u.hin * u.hin, N * u.hout * u.hout, u.width, u.cout
+                aa = 2 * bf(mi, w) + 2 * bf(mo, w) + bf(mo, co) + 2 * align(8 * w) + align(8 * co)
+                qq = max(bf(mo, co), bf(mi, w)) + f32(mi, w) + bf(mo, w)
+                if u.proj:
+                    aa += bf(mo, co) + align(8 * co)
+                    qq += bf(mo, co)
+                a.append(aa)
+                q.append(qq)
+            b.append(bf(N * u.hout * u.hout, u.cout))
+        return b, a, q
     if k == "lstm":
         B, H, V, n = cfg["batch"], cfg["hidden"], cfg["vocab"], structure.n
         bb = align(2 * B * H) + align(4 * B * H)
@@ -93,6 +134,9 @@ def grad_layout(structure, grad_chunk=None):
         slot = 2 * align(4 * B * H)
         extra = align(C * B * 4 * H * 2) + align(C * B * V * 2) + 2 * align(C * B * H * 2)
         return slot, extra
+    if structure.kind == "resnet_bottleneck":
+        N = structure.cfg["batch"]
+        return max(align(4 * N * u.hout * u.hout * u.cout) for u in structure.units), 0
     return max(b[1:]), 0
 
 

@@ -57,15 +57,25 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
 
 @dataclass
 class Prec:
+    """Working precision.  ``jitter`` (with ``rng``) multiplies every value by
+    (1 + jitter * N(0, 1)) just before it is rounded to bf16: a model of the
+    float32 accumulation error of another evaluation order, used only to
+    measure how far such errors can move a result (conditioning)."""
     dtype: type = np.float64
     bf16: bool = False
+    jitter: float = 0.0
+    rng: object = None
 
     def cast(self, x):
         return np.asarray(x, dtype=self.dtype)
 
     def st(self, x):
         """A tensor the GPU stores in bf16 (activation or GEMM operand)."""
-        return bf16_round(x).astype(self.dtype) if self.bf16 else x
+        if not self.bf16:
+            return x
+        if self.jitter:
+            x = np.asarray(x) * (1.0 + self.jitter * self.rng.standard_normal(np.shape(x)))
+        return bf16_round(x).astype(self.dtype)
 
 
 F64 = Prec(np.float64, False)

@@ -22,7 +22,7 @@ _lib = C.CDLL(LIB_PATH)
 OK, E_INVALID, E_WORKSPACE, E_MISMATCH, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4
 FLAG_KEEP_LAST = 1
-NET_MLP, NET_RESNET_BASIC, NET_LSTM = 1, 2, 3
+NET_MLP, NET_RESNET_BASIC, NET_LSTM, NET_RESNET_BOTTLENECK = 1, 2, 3, 4
 
 _u64p = C.POINTER(C.c_uint64)
 _i32p = C.POINTER(C.c_int32)
@@ -31,7 +31,9 @@ _i32p = C.POINTER(C.c_int32)
 class NetDesc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("batch", C.c_int32), ("depth", C.c_int32),
                 ("width", C.c_int32), ("image", C.c_int32), ("n_classes", C.c_int32),
-                ("grad_chunk", C.c_int32), ("reserved", C.c_int32 * 9)]
+                ("grad_chunk", C.c_int32), ("stage_blocks", C.c_int32 * 4),
+                ("expansion", C.c_int32), ("stem_channels", C.c_int32),
+                ("reserved", C.c_int32 * 3)]
 
 
 class Batch(C.Structure):
@@ -166,8 +168,13 @@ class Net:
     """Owner of a library net object (host descriptor)."""
 
     def __init__(self, kind: int, batch: int, depth: int, width: int, image: int = 0,
-                 n_classes: int = 0, grad_chunk: int = 0):
-        d = NetDesc(kind, batch, depth, width, image, n_classes, grad_chunk)
+                 n_classes: int = 0, grad_chunk: int = 0, stage_blocks: Sequence[int] = (),
+                 expansion: int = 0, stem_channels: int = 0):
+        sb = list(stage_blocks) + [0] * (4 - len(stage_blocks))
+        if len(sb) != 4:
+            raise CkptError(E_INVALID, "stage_blocks: at most 4 stages")
+        d = NetDesc(kind, batch, depth, width, image, n_classes, grad_chunk,
+                    (C.c_int32 * 4)(*sb), expansion, stem_channels)
         h = C.c_void_p()
         _check(_lib.net_create(C.byref(d), C.byref(h)))
         self._h = h
@@ -239,14 +246,16 @@ class Net:
                     kernel=name.value.decode())
 
     def __del__(self):
-        if getattr(self, "_h", None) is not None and self._h.value:
+        if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:
             _lib.net_destroy(self._h)
             self._h = None
 
 
 def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,
-               n_classes: int = 0, grad_chunk: int = 0) -> Net:
-    return Net(kind, batch, depth, width, image, n_classes, grad_chunk)
+               n_classes: int = 0, grad_chunk: int = 0, stage_blocks: Sequence[int] = (),
+               expansion: int = 0, stem_channels: int = 0) -> Net:
+    return Net(kind, batch, depth, width, image, n_classes, grad_chunk, stage_blocks, expansion,
+               stem_channels)
 
 
 def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,

@@ -191,9 +191,10 @@ __global__ __launch_bounds__(256) void k_bn_bwd_apply(int64_t P, int J, const fl
 }
 
 // ---- head: global average pool -> FC -> softmax cross-entropy ----
-// One workgroup per sample.
+// One workgroup per sample; X is fp32 or bf16 NHWC.
+template <typename TX>
 __global__ __launch_bounds__(256) void k_head_sample(int N, int HW, int C, int K,
-                                                     const float *__restrict__ X,
+                                                     const TX *__restrict__ X,
                                                      const float *__restrict__ Wf,
                                                      const float *__restrict__ bf,
                                                      const int *__restrict__ labels,
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(256) void k_head_sample(int N, int HW, int C, int K
   const float inv = 1.0f / float(HW);
   for (int c = t; c < C; c += 256) {
     float s = 0.f;
-    for (int p = 0; p < HW; ++p) s += X[(size_t(n) * HW + p) * C + c];
+    for (int p = 0; p < HW; ++p) s += float(X[(size_t(n) * HW + p) * C + c]);
     pl[c] = s * inv;
     pooled[size_t(n) * C + c] = s * inv;
   }
@@ -311,6 +312,12 @@ void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m
                      nullptr, nullptr);
 }
 
+void bn_finalize_bwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *sums,
+                     float *dgamma, float *dbeta) {
+  hipLaunchKernelGGL((k_bn_finalize<false>), dim3(J), dim3(256), 0, s, part, nb, J, double(m), sums,
+                     dgamma, dbeta);
+}
+
 void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const float *st,
               const float *gamma, const float *beta, const float *X, int H, int W, int Cx, float *Y) {
   const int g = ew_grid(P * (J / 4));
@@ -344,8 +351,19 @@ void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X,
                      const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
                      float *G, float *dW, float *db, float *loss) {
   const size_t lds = size_t(C + K + 256) * 4;
-  hipLaunchKernelGGL(k_head_sample, dim3(N), dim3(256), lds, s, N, HW, C, K, X, Wf, bf, labels,
+  hipLaunchKernelGGL(k_head_sample<float>, dim3(N), dim3(256), lds, s, N, HW, C, K, X, Wf, bf, labels,
                      pooled, dlog, lossn, G);
+  const int tot = C * K + K + 1;
+  hipLaunchKernelGGL(k_head_params, dim3((tot + 255) / 256), dim3(256), 0, s, N, C, K, pooled,
+                     dlog, lossn, dW, db, loss);
+}
+
+void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void *X, const float *Wf,
+                          const float *bf, const int *labels, float *pooled, float *dlog,
+                          float *lossn, float *G, float *dW, float *db, float *loss) {
+  const size_t lds = size_t(C + K + 256) * 4;
+  hipLaunchKernelGGL(k_head_sample<__bf16>, dim3(N), dim3(256), lds, s, N, HW, C, K,
+                     static_cast<const __bf16 *>(X), Wf, bf, labels, pooled, dlog, lossn, G);
   const int tot = C * K + K + 1;
   hipLaunchKernelGGL(k_head_params, dim3((tot + 255) / 256), dim3(256), 0, s, N, C, K, pooled,
                      dlog, lossn, dW, db, loss);

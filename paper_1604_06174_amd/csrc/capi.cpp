@@ -110,11 +110,17 @@ int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
       if (r != 0) ckpt::fail(CKPT_E_INVALID, "net_create: reserved fields must be zero");
     if (desc->kind != CKPT_NET_LSTM && desc->grad_chunk != 0)
       ckpt::fail(CKPT_E_INVALID, "net_create: grad_chunk applies to LSTM only");
+    if (desc->kind != CKPT_NET_RESNET_BOTTLENECK &&
+        (desc->stage_blocks[0] | desc->stage_blocks[1] | desc->stage_blocks[2] |
+         desc->stage_blocks[3] | desc->expansion | desc->stem_channels) != 0)
+      ckpt::fail(CKPT_E_INVALID,
+                 "net_create: stage_blocks, expansion and stem_channels apply to RESNET_BOTTLENECK only");
     auto h = std::make_unique<ckpt_net>();
     switch (desc->kind) {
       case CKPT_NET_MLP: h->net = ckpt::make_mlp_net(*desc); break;
       case CKPT_NET_RESNET_BASIC: h->net = ckpt::make_resnet_basic_net(*desc); break;
       case CKPT_NET_LSTM: h->net = ckpt::make_lstm_net(*desc); break;
+      case CKPT_NET_RESNET_BOTTLENECK: h->net = ckpt::make_resnet_bottleneck_net(*desc); break;
       default: ckpt::fail(CKPT_E_INVALID, "net_create: unknown network kind");
     }
     *out = h.release();

@@ -816,12 +816,16 @@ __global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ 
   }
 }
 
+}  // namespace
+
 void sum_partials(hipStream_t st, const float *part, int nb, int E, float *out) {
   if (E < 16 * 2048)
     hipLaunchKernelGGL((k_sum_partials<64>), dim3((E + 3) / 4), dim3(256), 0, st, part, nb, E, out);
   else
     hipLaunchKernelGGL((k_sum_partials<16>), dim3((E + 15) / 16), dim3(256), 0, st, part, nb, E, out);
 }
+
+namespace {
 
 struct Tile {
   int R, rblk, psw;

@@ -7,7 +7,7 @@
 
 namespace ckpt {
 
-enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2 };
+enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4 };
 
 // C = epilogue(op(A) op(B)); see gemm_f32.hip for the operand conventions.
 void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool ta, const float *B,
@@ -61,14 +61,82 @@ void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Y
 void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X, const float *Wf,
                      const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
                      float *G, float *dW, float *db, float *loss);
+// the same head over a bf16 X
+void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void *X, const float *Wf,
+                          const float *bf, const int *labels, float *pooled, float *dlog,
+                          float *lossn, float *G, float *dW, float *db, float *loss);
+// sums[0..J) = mean(ds), sums[J..2J) = mean(ds xhat), dgamma, dbeta from the
+// backward partials (sum ds, sum ds xhat) of nb workgroups over m values
+void bn_finalize_bwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *sums,
+                     float *dgamma, float *dbeta);
 
-// ---- bf16 GEMM (gemm_bf16.hip) ----
+// ---- bf16 batch norm, stem im2col and max pool (bneck.hip) ----
+enum { BNB_RES_NONE = 0, BNB_RES_ID = 1, BNB_RES_BN = 2 };
+// Y = bf16(relu(gamma (C - mean) rstd + beta [+ X | + gp (X - meanp) rstdp + bp]))
+// over P pixels x J channels (bf16 NHWC; st / stp = mean | rstd).
+void bnb_apply(hipStream_t s, int res, int64_t P, int J, const void *Cv, const float *st,
+               const float *gamma, const float *beta, const void *X, const float *stp,
+               const float *gp, const float *bp, void *Y);
+int bnb_partial_blocks(int64_t P, int J);
+// D (bf16) = dL/dC of the batch norm with ds = [Ym > 0] G (Ym may be null);
+// writes dgamma, dbeta.  part: bnb_partial_blocks * 2J doubles; sums: 2J floats.
+void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
+                  const float *st, const float *gamma, double *part, float *sums, float *dgamma,
+                  float *dbeta, void *D);
+// col [N*Ho*Wo, 147] bf16 = 7x7 / stride 2 / pad 3 patches of X [N, H, W, 3]
+void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, const void *X, void *col);
+// 3x3 / stride 2 / pad 1 max pool of R [N, H, W, C] into Y [N, Ho, Wo, C] (bf16)
+void maxpool_fwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const void *R, void *Y);
+// dR (fp32) = gradient of the max pool: each window's G goes to its first maximum
+void maxpool_bwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const float *G,
+                 const void *R, const void *Y, float *dR);
+
+// ---- bf16 GEMM (gemm_bf16.hip, gemm_bf16_conv.hip) ----
 // C[M,N] fp32 = op(A) op(B) (+ bias | + D).  A is bf16, or fp32 rounded to
 // bf16 on load (a_fp32); B is bf16.  ak / bk: the operand is stored with k
 // contiguous (A[m*lda + k], B[n*ldb + k]); otherwise A[k*lda + m], B[k*ldb + n].
 void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D = nullptr,
                int ldd = 0, const float *bias = nullptr);
+// Options: splits > 1 = split-K, C receives splits partial [M, ldc] products
+// (STORE); ADDMASK: C = acc + (mask > 0 ? D : 0), mask bf16 shaped like D;
+// BF16STATS: Cb (bf16, ldc) = round(acc) and stats[row block][2][N] float64
+// sums of the rounded values and squares (row blocks: gemm_bf16_row_blocks).
+struct GemmX {
+  int splits = 1;
+  const void *mask = nullptr;
+  void *Cb = nullptr;
+  double *stats = nullptr;
+};
+void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
+                const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D,
+                int ldd, const float *bias, const GemmX &x);
+int gemm_bf16_row_blocks(int M, int N);
+int gemm_bf16_tiles(int M, int N);
+// out[e] = sum_b part[b*E + e], b in a fixed order
+void sum_partials(hipStream_t s, const float *part, int nb, int E, float *out);
+
+// Convolution of NHWC bf16 tensors as implicit GEMM: input [N, H, W, Ci],
+// output [N, Ho, Wo, Co], weights [Co, R, R, Ci] (bf16), stride S in {1, 2},
+// padding P; Ci and Co powers of two, at least 8.
+struct ConvGeo {
+  int N, H, W, Ci, Ho, Wo, Co, R, S, P;
+};
+bool conv_bf16_supported(const ConvGeo &g);
+// Yb = bf16(conv(X, Wt)); stats[row block][2][Co] as for BF16STATS
+// (row blocks: gemm_bf16_row_blocks(N*Ho*Wo, Co)).
+void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *Wt, void *Yb,
+                   double *stats);
+// DX [N, H, W, Ci] fp32 = data gradient of DY [N, Ho, Wo, Co] (bf16) through
+// Wt; epi STORE, ADD (+ D) or ADDMASK (+ D where mask > 0), D and mask shaped
+// like DX.
+void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void *Wt, float *DX,
+                     int epi, const float *D = nullptr, const void *mask = nullptr);
+// dW [Co, R, R, Ci] fp32 = weight gradient from X (bf16 input) and DY (bf16
+// output gradient); split-K over the N*Ho*Wo pixels with `splits` partials
+// in part (splits * Co*R*R*Ci floats), added in a fixed order.
+void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void *DY, float *part,
+                     int splits, float *dW);
 
 // ---- LSTM step kernels (lstm.hip) ----
 void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst);  // dst[c][r]

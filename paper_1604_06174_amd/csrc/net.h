@@ -135,5 +135,6 @@ class Net {
 std::unique_ptr<Net> make_mlp_net(const ckpt_net_desc &d);
 std::unique_ptr<Net> make_resnet_basic_net(const ckpt_net_desc &d);
 std::unique_ptr<Net> make_lstm_net(const ckpt_net_desc &d);
+std::unique_ptr<Net> make_resnet_bottleneck_net(const ckpt_net_desc &d);
 
 }  // namespace ckpt

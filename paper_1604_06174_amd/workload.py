@@ -26,6 +26,15 @@ def net_for(cfg: Dict) -> K.Net:
     if kind == "lstm":
         return K.net_create(K.NET_LSTM, cfg["batch"], cfg["T"], cfg["hidden"], cfg["input"],
                             cfg["vocab"], cfg.get("grad_chunk", 0))
+    if kind == "resnet_bottleneck":
+        sb = tuple(cfg["stage_blocks"])
+        widths = tuple(cfg.get("widths", (64, 128, 256, 512)))[:len(sb)]
+        w0 = widths[0]
+        if any(w != w0 << t for t, w in enumerate(widths)):
+            raise K.CkptError(K.E_UNSUPPORTED, "bottleneck widths must double per stage")
+        return K.net_create(K.NET_RESNET_BOTTLENECK, cfg["batch"], len(sb), w0,
+                            cfg.get("image", 224), cfg.get("classes", 1000), 0, sb,
+                            cfg.get("expansion", 4), cfg.get("stem_channels", 64))
     raise K.CkptError(K.E_UNSUPPORTED, f"no GPU network for workload kind {kind!r}")
 
 
@@ -47,7 +56,7 @@ class GpuStep:
             host[off // 4: off // 4 + numel] = v
         self.params.copy_(torch.from_numpy(host))
         self.input = torch.from_numpy(np.ascontiguousarray(inp)).to(self.device)
-        if cfg["kind"] == "lstm":  # the recurrent input is consumed as bf16
+        if cfg["kind"] in ("lstm", "resnet_bottleneck"):  # consumed as bf16
             self.input = self.input.to(torch.bfloat16).contiguous()
         self.target = torch.from_numpy(np.ascontiguousarray(target)).to(self.device)
         self._ws = None

@@ -99,7 +99,11 @@ WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
                  dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=3, image=12, classes=5),
                  dict(kind="lstm", T=4096, batch=64, input=1024, hidden=1024, vocab=10000),
                  dict(kind="lstm", T=16384, batch=64, input=1024, hidden=1024, vocab=10000),
-                 dict(kind="lstm", T=13, batch=3, input=16, hidden=24, vocab=40, grad_chunk=4)]
+                 dict(kind="lstm", T=13, batch=3, input=16, hidden=24, vocab=40, grad_chunk=4),
+                 dict(kind="resnet_bottleneck", stage_blocks=(32, 64, 205, 32), batch=32,
+                      image=224, classes=1000),
+                 dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1), widths=(8, 16, 32),
+                      expansion=2, stem_channels=16, image=32, batch=3, classes=10)]
 
 
 @pytest.mark.parametrize("cfg", WORKLOADS_CPU)
@@ -129,7 +133,10 @@ def test_net_tables_and_accounting_match_oracle(cfg):
 @pytest.mark.parametrize("cfg", [dict(kind="mlp", depth=5, width=40, batch=3),
                                  dict(kind="resnet_basic", blocks_per_stage=3, base=8, batch=2,
                                       image=16, classes=7),
-                                 dict(kind="lstm", T=5, batch=2, input=16, hidden=8, vocab=24)])
+                                 dict(kind="lstm", T=5, batch=2, input=16, hidden=8, vocab=24),
+                                 dict(kind="resnet_bottleneck", stage_blocks=(2, 2),
+                                      widths=(8, 16), expansion=4, stem_channels=8, image=16,
+                                      batch=2, classes=7)])
 def test_param_layout_names_match_structure(cfg):
     from paper_1604_06174_amd.workload import net_for
     net = net_for(cfg)
@@ -145,6 +152,22 @@ def test_net_create_errors():
     assert ei.value.code == K.E_INVALID
     with pytest.raises(K.CkptError):
         K.net_create(K.NET_MLP, 0, 4, 4)
+    # fields of another kind
+    with pytest.raises(K.CkptError) as ei:
+        K.net_create(K.NET_MLP, 2, 4, 8, stage_blocks=(1,))
+    assert ei.value.code == K.E_INVALID
+    B = K.NET_RESNET_BOTTLENECK
+    # stage_blocks past depth, non-positive stage, channel counts, odd stride-2 side
+    for args, kw, code in [((2, 2, 8, 32, 10), dict(stage_blocks=(1, 1, 1), expansion=4, stem_channels=8), K.E_INVALID),
+                           ((2, 2, 8, 32, 10), dict(stage_blocks=(1, 0), expansion=4, stem_channels=8), K.E_INVALID),
+                           ((2, 2, 12, 32, 10), dict(stage_blocks=(1, 1), expansion=4, stem_channels=8), K.E_UNSUPPORTED),
+                           ((2, 2, 8, 32, 10), dict(stage_blocks=(1, 1), expansion=3, stem_channels=8), K.E_UNSUPPORTED),
+                           ((2, 2, 8, 32, 10), dict(stage_blocks=(1, 1), expansion=4, stem_channels=4), K.E_UNSUPPORTED),
+                           ((2, 2, 8, 20, 10), dict(stage_blocks=(1, 1), expansion=4, stem_channels=8), K.E_UNSUPPORTED),
+                           ((2, 5, 8, 32, 10), dict(stage_blocks=(1, 1), expansion=4, stem_channels=8), K.E_INVALID)]:
+        with pytest.raises(K.CkptError) as ei:
+            K.net_create(B, *args, **kw)
+        assert ei.value.code == code, (args, kw)
 
 
 def test_train_step_rejects_before_launch():

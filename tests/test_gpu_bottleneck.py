@@ -1,0 +1,121 @@
+"""GPU parity of the bf16 bottleneck ResNet checkpointed step against the oracle.
+
+The GPU rounds to bf16 at the points the oracle's ``Prec(bf16=True)`` mode
+does (input, weights, conv outputs, ReLU outputs, block outputs and the
+batch-norm input gradients), so the reference is that oracle in float64.
+
+Conditioning.  This network is chaotic at the bf16 rounding level: a value
+whose float32 accumulation lands on the other side of a bf16 rounding
+midpoint shifts its channel's batch-norm statistics, which moves every value
+of the channel and flips further roundings downstream.  Perturbing the
+oracle's values by 1e-7 (relative, Gaussian) just before each bf16 rounding
+-- the size of float32 accumulation error -- moves its loss by up to 1e-2 and
+single gradient tensors by far more than the bf16 bar on every configuration
+with more than one block, and so does any other evaluation order, the GPU's
+included.  The bar is therefore statistical: over six such perturbed oracle
+runs (seeded), take per gradient tensor the largest max-abs relative and L2
+relative deviation from the unperturbed oracle, and the largest loss
+deviation; the GPU may deviate by at most 3x those plus 2e-2 (the bf16 bar)
+per tensor, and 3x plus 1e-5 on the loss.  Every plan must also give the
+no-checkpoint run's gradient bytes, the oracle's peak bytes and its
+unit-forward count.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import nets, planner as PL, sizes as SZ, units as U
+
+pytestmark = pytest.mark.gpu
+
+JITTER, REPS = 1e-7, 6
+
+
+def _maxrel(g, o):
+    g = np.asarray(g, np.float64).reshape(-1)
+    o = np.asarray(o, np.float64).reshape(-1)
+    return float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-30))
+
+
+def _l2rel(g, o):
+    g = np.asarray(g, np.float64).reshape(-1)
+    o = np.asarray(o, np.float64).reshape(-1)
+    return float(np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-30))
+
+
+CASES = {
+    # stem + one stride-1 projection block
+    "b1": dict(kind="resnet_bottleneck", stage_blocks=(1,), widths=(8,), expansion=4,
+               stem_channels=8, image=16, batch=2, classes=7, seed=91),
+    # + identity blocks and a stride-2 projection stage
+    "b22": dict(kind="resnet_bottleneck", stage_blocks=(2, 2), widths=(8, 16), expansion=4,
+                stem_channels=8, image=16, batch=2, classes=7, seed=91),
+    # four stages down to 1 x 1, stem 16
+    "b2111": dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1, 1), widths=(8, 16, 32, 64),
+                  expansion=4, stem_channels=16, image=32, batch=2, classes=10, seed=91),
+    # expansion 2, a single image
+    "b121": dict(kind="resnet_bottleneck", stage_blocks=(1, 2, 1), widths=(8, 16, 32), expansion=2,
+                 stem_channels=8, image=32, batch=1, classes=5, seed=92),
+    # the real stage-1/2 channel counts: several GEMM tiles, split-K weight gradients
+    "wide": dict(kind="resnet_bottleneck", stage_blocks=(1, 1), widths=(64, 128), expansion=4,
+                 stem_channels=64, image=64, batch=4, classes=100, seed=83),
+}
+
+
+def _envelope(d):
+    chain = lambda prec: nets.Chain(d["structure"], d["params"], prec)
+    l0, g0 = nets.full_storage_step(chain(U.Prec(np.float64, True)), d["input"], d["target"])
+    em = {k: 0.0 for k in g0}
+    el = {k: 0.0 for k in g0}
+    lmax = 0.0
+    for s in range(REPS):
+        prec = U.Prec(np.float64, True, JITTER, np.random.default_rng(700 + s))
+        l1, g1 = nets.full_storage_step(chain(prec), d["input"], d["target"])
+        lmax = max(lmax, abs(l1 - l0) / abs(l0))
+        for k in g0:
+            em[k] = max(em[k], _maxrel(g1[k], g0[k]))
+            el[k] = max(el[k], _l2rel(g1[k], g0[k]))
+    return l0, g0, lmax, em, el
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_bottleneck_parity_all_modes(case):
+    import torch
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = CASES[case]
+    print(f"[bottleneck parity] case={case} cfg={cfg}", flush=True)
+    d = synth.make(cfg)
+    l0, g0, lmax, em, el = _envelope(d)
+    st = d["structure"]
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    b, a, q = SZ.tables(st)
+    slot, extra = SZ.grad_layout(st)
+    lb, cb = SZ.layer_and_cut_bytes(st)
+    n = st.n
+    modes = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
+             ("greedy", PL.GREEDY, sum(lb) // 3, None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
+             ("user_keep", PL.USER, 0, [0], PL.FLAG_KEEP_LAST)]
+    ref = None
+    for name, mode, budget, user, flags in modes:
+        plan = step.plan(mode, budget, user, flags)
+        step.grads.fill_(float("nan"))
+        loss, peak, stats = step.run(plan)
+        torch.cuda.synchronize()
+        op = PL.plan(n, lb, cb, budget, mode, user, flags)
+        assert peak == PL.account(op, b, a, q, slot, extra).peak, name
+        assert stats["unit_forwards"] == PL.unit_forwards(op), name
+        gbytes = step.grads_bytes()
+        if ref is None:
+            ref = gbytes
+            g = step.grads_host()
+            dl = abs(loss - l0) / abs(l0)
+            print(f"  loss {loss:.6f} oracle {l0:.6f} dev {dl:.1e} (envelope {lmax:.1e})", flush=True)
+            assert dl <= 3 * lmax + 1e-5, (dl, lmax)
+            for k, v in g0.items():
+                m, l = _maxrel(g[k], v), _l2rel(g[k], v)
+                assert m <= 3 * em[k] + 2e-2, (k, m, em[k])
+                assert l <= 3 * el[k] + 2e-2, (k, l, el[k])
+            worst = max(g0, key=lambda k: _maxrel(g[k], g0[k]))
+            print(f"  worst tensor {worst}: {_maxrel(g[worst], g0[worst]):.1e} "
+                  f"(envelope {em[worst]:.1e})", flush=True)
+        assert gbytes == ref, f"{name}: gradients differ from the no-checkpoint run"

@@ -98,7 +98,7 @@ def test_mlp1024_recursive_full_size():
     _check_band(d, loss, g, "mlp1024")
 
 
-def _lstm_full(name, mode, budget, extra_forwards=None):
+def _identity_full(name, mode, budget, extra_forwards=None, budget_frac=None):
     import torch
     from paper_1604_06174_amd import ckpt as K
     from paper_1604_06174_amd.workload import GpuStep
@@ -106,11 +106,14 @@ def _lstm_full(name, mode, budget, extra_forwards=None):
     print(f"[full size] {name}: drawing inputs", flush=True)
     d = synth.make(cfg)
     step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    target = d["target"]
     del d
     st = synth.structure(cfg)
     b, a, q = SZ.tables(st)
     slot, extra = SZ.grad_layout(st)
     lb, cb = SZ.layer_and_cut_bytes(st)
+    if budget_frac is not None:
+        budget = int(sum(lb) * budget_frac)
     plan = step.plan(mode, budget)
     loss, peak, stats = step.run(plan)
     torch.cuda.synchronize()
@@ -126,14 +129,17 @@ def _lstm_full(name, mode, budget, extra_forwards=None):
     assert loss2 == loss
     assert step.grads_bytes() == gbytes, "checkpointed gradients differ from the no-checkpoint run"
     print(f"[full size] {name}: no-checkpoint run identical", flush=True)
+    g = step.grads.cpu().numpy()
+    assert np.isfinite(g).all() and np.isfinite(loss)
+    return loss, stats, step.grads_host(), target
 
 
 def test_lstm4096_full_size_identity():
-    _lstm_full("lstm4096", PL.SQRT, 64)
+    _identity_full("lstm4096", PL.SQRT, 64)
 
 
 def test_lstm16384_recursive_full_size_identity():
-    _lstm_full("lstm16384", PL.RECURSIVE, 0, extra_forwards=122880)
+    _identity_full("lstm16384", PL.RECURSIVE, 0, extra_forwards=122880)
 
 
 def test_lstm_full_width_prefix_parity():
@@ -161,3 +167,23 @@ def test_lstm_full_width_prefix_parity():
     print(f"[full size] lstm full-width prefix worst {worst}, vs float64 {worst64}", flush=True)
     assert worst[0] <= 1e-2
     assert worst64[0] <= 2e-2
+
+
+def test_resnet1000_greedy_full_size_identity():
+    """The 334-unit bf16 bottleneck ResNet at batch 32 (224 x 224), greedy
+    plan at 10% of the full-storage bytes: the same bit-identity, peak and
+    unit-forward checks (the oracle cannot run this size; the unit math is
+    pinned by the small cases of the bottleneck tests), plus what softmax
+    cross-entropy fixes at any size: with dlog = (p - onehot) / N, the bias
+    gradient plus the label frequencies is a mean of probability vectors
+    (entries in [0, 1], summing to 1), and every row of the FC weight
+    gradient sums to zero."""
+    loss, _, g, target = _identity_full("resnet1000", PL.GREEDY, 0, budget_frac=0.1)
+    assert loss > 0
+    N, K = target.shape[0], 1000
+    pbar = g["head.b"].astype(np.float64) + np.bincount(target, minlength=K) / N
+    assert pbar.min() >= -1e-6 and pbar.max() <= 1 + 1e-6
+    assert abs(pbar.sum() - 1.0) <= 1e-5
+    W = g["head.W"].astype(np.float64).reshape(-1, K)
+    assert np.all(np.abs(W.sum(axis=1)) <= 1e-5 * np.abs(W).sum(axis=1) + 1e-9)
+

@@ -17,7 +17,25 @@ LIB_PATH = os.path.join(_HERE, "libckpt.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1604_06174_amd.build`")
 
+# The library links libamdhip64.so.7.  PyTorch ships its own HIP runtime under
+# the unversioned name libamdhip64.so; if the library were mapped first, torch
+# would load that second copy (and a second HSA runtime) into the process.
+# Importing torch first lets the library bind to torch's runtime by soname.
+import torch  # noqa: E402,F401  (loads the process's one HIP runtime)
+
 _lib = C.CDLL(LIB_PATH)
+
+
+def _hip_runtimes():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({ln.split()[-1] for ln in f if "libamdhip64.so" in ln})
+    except OSError:
+        return []
+
+
+if len(_hip_runtimes()) > 1:
+    raise ImportError("two HIP runtimes are mapped into this process: " + ", ".join(_hip_runtimes()))
 
 OK, E_INVALID, E_WORKSPACE, E_MISMATCH, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4

@@ -194,3 +194,9 @@ def test_train_step_rejects_before_launch():
     with pytest.raises(K.CkptError) as ei:
         K.train_step(net, fake, fake, 0, fake, plan, fake, need)
     assert ei.value.code == K.E_INVALID
+
+
+def test_single_hip_runtime_in_process():
+    """The binding maps the library after torch, so the process holds one HIP
+    runtime (torch's) whatever the import order of the caller."""
+    assert len(K._hip_runtimes()) == 1, K._hip_runtimes()

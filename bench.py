@@ -36,6 +36,8 @@ def _plan_args(cfg, net):
     from paper_1604_06174_amd import ckpt as K
     lb, _ = net.layer_sizes()
     mode = cfg.get("plan", "sqrt")
+    if mode == "search":
+        return "search", None, "search"
     if mode == "sqrt":
         return K.SQRT, int(cfg.get("stride", 0)), "sqrt"
     if mode == "greedy":
@@ -75,15 +77,22 @@ def _cpu_baseline(cfg, sample_batch, d_full):
     chain = nets.Chain(structure, d_full["params"])
     lb, cb = SZ.layer_and_cut_bytes(structure)
     n = structure.n
-    mode = {"sqrt": PL.SQRT, "greedy": PL.GREEDY, "recursive": PL.RECURSIVE}[cfg.get("plan", "sqrt")]
-    budget = int(cfg.get("stride", 0)) if mode == PL.SQRT else int(sum(lb) * cfg.get("budget_frac", 0.1))
-    if mode == PL.SQRT:
-        budget = min(budget, n) if budget else 0
+    pname = cfg.get("plan", "sqrt")
+    if pname == "search":
+        b, a, q = SZ.tables(structure)
+        slot, extra = SZ.grad_layout(structure, cfg.get("grad_chunk"))
+        oplan = PL.search(n, lb, cb, b, a, q, slot, extra)[0]
+    else:
+        mode = {"sqrt": PL.SQRT, "greedy": PL.GREEDY, "recursive": PL.RECURSIVE}[pname]
+        budget = int(cfg.get("stride", 0)) if mode == PL.SQRT else int(sum(lb) * cfg.get("budget_frac", 0.1))
+        if mode == PL.SQRT:
+            budget = min(budget, n) if budget else 0
+        oplan = None if mode == PL.RECURSIVE else PL.plan(n, lb, cb, budget, mode)
     t0 = time.perf_counter()
-    if mode == PL.RECURSIVE:
+    if oplan is None:
         SCH.recursive_step(chain, inp, tgt)
     else:
-        SCH.segment_step(chain, inp, tgt, PL.plan(n, lb, cb, budget, mode))
+        SCH.segment_step(chain, inp, tgt, oplan)
     dt = time.perf_counter() - t0
     return {"value": n_samples * scale / dt, "unit": "samples/s", "cores": int(threads),
             "kind": "oracle",
@@ -97,6 +106,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="cifar110")
+    ap.add_argument("--plan", default=None, choices=["sqrt", "greedy", "recursive", "search"],
+                    help="override the workload's plan (search: the appendix-A budget search)")
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="batch (LSTM: time steps) of the CPU oracle sample; 0 skips it, -1 picks "
                          "about 10-30 s of oracle work for the workload")
@@ -117,8 +128,13 @@ def main():
     cfg = dict(synth.WORKLOADS[args.workload])
     d = synth.make(cfg)
     step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    if args.plan:
+        cfg["plan"] = args.plan
     mode, budget, mode_name = _plan_args(cfg, step.net)
-    plan = step.plan(mode, budget)
+    if mode == "search":
+        plan, budget, _ = step.net.search_plan()
+    else:
+        plan = step.plan(mode, budget)
     none = step.plan(K.NONE)
     acc = step.net.accounting(plan)
     acc_none = step.net.accounting(none)

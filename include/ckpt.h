@@ -111,6 +111,28 @@ int plan_serialize(const ckpt_plan *plan, uint8_t *buf, uint64_t cap, uint64_t *
 
 void plan_free(ckpt_plan *plan);
 
+/*
+ * plan_search -- the search over Alg. 3's budget B of the paper's appendix A:
+ * run Alg. 3 with B = 0 to get x (kept bytes) and y (largest segment), set
+ * B0 = floor(sqrt(x y)), try B0 and six budgets evenly spaced from
+ * floor(B0 / sqrt 2) to floor(sqrt(2) B0) (integer steps j (hi - lo) / 5,
+ * j = 0..5), and return the GREEDY plan whose exact PEAK under the static
+ * layout below is lowest (ties: the smaller budget).  The returned plan is
+ * identical to plan_checkpoints(GREEDY, *budget, flags).
+ *   layer_bytes, cut_bytes: [n] as for plan_checkpoints (host).
+ *   b [n+1], a [n], q [n]: the layout tables of net_unit_sizes (host).
+ *   grad_slot: bytes of one gradient slot (0: the largest b_i, i >= 1);
+ *   grad_extra: fixed gradient buffers (net_grad_bytes gives both).
+ *   flags: CKPT_FLAG_KEEP_LAST or 0.
+ *   out: new plan (free with plan_free); budget, peak: nullable outputs.
+ * Errors: CKPT_E_INVALID as plan_checkpoints (null arrays, n <= 0,
+ *   cut_bytes[n-1] != 0, unknown flags).
+ */
+int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
+                const uint64_t *b, const uint64_t *a, const uint64_t *q, uint64_t grad_slot,
+                uint64_t grad_extra, int32_t flags, ckpt_plan **out, uint64_t *budget,
+                uint64_t *peak);
+
 /* ---- networks --------------------------------------------------------- */
 #define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
 #define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */

@@ -280,3 +280,37 @@ def account(p: Plan, b: Sequence[int], a: Sequence[int], q: Sequence[int], slot=
 
 def unit_forwards(p: Plan) -> int:
     return p.n + p.extra_forwards
+
+
+# --------------------------------------------------------------------------
+# search over Alg. 3's budget (appendix A)
+# --------------------------------------------------------------------------
+
+def search_candidates(layer_bytes: Sequence[int], cut_bytes: Sequence[int]) -> List[int]:
+    """The budgets the appendix-A search tries: run Alg. 3 with B = 0 to get
+    x (kept bytes) and y (largest segment), take B0 = floor(sqrt(x y)), then a
+    six-point grid on [B0/sqrt(2), sqrt(2) B0].  Reading: the grid is evenly
+    spaced between floor(B0/sqrt 2) and floor(sqrt(2) B0) (integer square
+    roots, integer steps j (hi - lo) // 5), and B0 itself is a candidate too.
+    Returned ascending, without repeats."""
+    _, x, y = greedy_alg3(layer_bytes, cut_bytes, 0)
+    b0 = math.isqrt(x * y)
+    lo = math.isqrt(b0 * b0 // 2)
+    hi = math.isqrt(2 * b0 * b0)
+    grid = [lo + (hi - lo) * j // 5 for j in range(6)]
+    return sorted(set(grid + [b0]))
+
+
+def search(n: int, layer_bytes: Sequence[int], cut_bytes: Sequence[int], b: Sequence[int],
+           a: Sequence[int], q: Sequence[int], slot=None, extra: int = 0, flags: int = 0):
+    """Appendix A: the GREEDY plan of the candidate budget with the lowest
+    exact PEAK of the static layout (ties: the smaller budget).  Returns
+    (plan, budget, peak)."""
+    best = None
+    for B in search_candidates(layer_bytes, cut_bytes):
+        p = plan(n, layer_bytes, cut_bytes, B, GREEDY, flags=flags)
+        pk = account(p, b, a, q, slot, extra).peak
+        if best is None or pk < best[2]:
+            best = (p, B, pk)
+    return best
+

@@ -81,6 +81,8 @@ _sig("plan_info", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, _u64p, _u64p, _u64p
 _sig("plan_cuts", C.c_int, [C.c_void_p, _i32p, C.c_int32, _i32p])
 _sig("plan_serialize", C.c_int, [C.c_void_p, C.POINTER(C.c_uint8), C.c_uint64, _u64p])
 _sig("plan_free", None, [C.c_void_p])
+_sig("plan_search", C.c_int, [C.c_int32, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_uint64, C.c_uint64,
+                              C.c_int32, C.POINTER(C.c_void_p), _u64p, _u64p])
 _sig("net_create", C.c_int, [C.POINTER(NetDesc), C.POINTER(C.c_void_p)])
 _sig("net_destroy", None, [C.c_void_p])
 _sig("net_units", C.c_int, [C.c_void_p, _i32p])
@@ -100,7 +102,7 @@ _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch
                              C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
 
 EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
-            "plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
+            "plan_free", "plan_search", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
             "train_step"]
@@ -224,6 +226,13 @@ class Net:
         _check(_lib.net_grad_bytes(self._h, C.byref(slot), C.byref(extra)))
         return slot.value, extra.value
 
+    def search_plan(self, flags: int = 0) -> Tuple["Plan", int, int]:
+        """Appendix A's budget search over this net's layout tables."""
+        lb, cb = self.layer_sizes()
+        b, a, q = self.unit_sizes()
+        slot, extra = self.grad_bytes()
+        return plan_search(lb, cb, b, a, q, slot, extra, flags)
+
     def param_bytes(self) -> int:
         v = C.c_uint64()
         _check(_lib.net_param_bytes(self._h, C.byref(v)))
@@ -267,6 +276,20 @@ class Net:
         if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:
             _lib.net_destroy(self._h)
             self._h = None
+
+
+def plan_search(layer_bytes: Sequence[int], cut_bytes: Sequence[int], b: Sequence[int],
+                a: Sequence[int], q: Sequence[int], grad_slot: int = 0, grad_extra: int = 0,
+                flags: int = 0) -> Tuple["Plan", int, int]:
+    """Appendix A's budget search; returns (GREEDY plan, chosen budget, exact peak)."""
+    n = len(layer_bytes)
+    arr = lambda v, k: (C.c_uint64 * max(k, 1))(*[int(x) for x in v])
+    h = C.c_void_p()
+    bud, pk = C.c_uint64(), C.c_uint64()
+    _check(_lib.plan_search(n, arr(layer_bytes, n), arr(cut_bytes, n), arr(b, n + 1), arr(a, n),
+                            arr(q, n), int(grad_slot), int(grad_extra), flags, C.byref(h),
+                            C.byref(bud), C.byref(pk)))
+    return Plan(h.value), bud.value, pk.value
 
 
 def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,

@@ -101,6 +101,28 @@ int plan_serialize(const ckpt_plan *plan, uint8_t *buf, uint64_t cap, uint64_t *
 
 void plan_free(ckpt_plan *plan) { delete plan; }
 
+int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
+                const uint64_t *b, const uint64_t *a, const uint64_t *q, uint64_t grad_slot,
+                uint64_t grad_extra, int32_t flags, ckpt_plan **out, uint64_t *budget,
+                uint64_t *peak) {
+  return guarded([&] {
+    need(out, "plan_search(out)");
+    *out = nullptr;
+    if (n_layers <= 0) ckpt::fail(CKPT_E_INVALID, "plan_search: n_layers must be positive");
+    need(layer_bytes, "plan_search(layer_bytes)");
+    need(cut_bytes, "plan_search(cut_bytes)");
+    need(b, "plan_search(b)");
+    need(a, "plan_search(a)");
+    need(q, "plan_search(q)");
+    const size_t n = size_t(n_layers);
+    std::vector<uint64_t> bv(b, b + n + 1), av(a, a + n), qv(q, q + n);
+    auto p = std::make_unique<ckpt_plan>();
+    p->p = ckpt::search_plan(n_layers, layer_bytes, cut_bytes, bv, av, qv, grad_slot, grad_extra,
+                             flags, budget, peak);
+    *out = p.release();
+  });
+}
+
 int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
   return guarded([&] {
     need(desc, "net_create(desc)");

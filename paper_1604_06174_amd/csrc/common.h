@@ -56,5 +56,11 @@ std::vector<uint8_t> serialize(const Plan &p);
 Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
                    const std::vector<uint64_t> &q, uint64_t slot = 0, uint64_t extra = 0);
 uint64_t recursive_extra(int32_t n);
+// Appendix A's budget search: the candidate budgets (ascending) and the GREEDY
+// plan of the candidate with the lowest exact peak (ties: smaller budget).
+std::vector<uint64_t> search_candidates(int32_t n, const uint64_t *lb, const uint64_t *cb);
+Plan search_plan(int32_t n, const uint64_t *lb, const uint64_t *cb, const std::vector<uint64_t> &b,
+                 const std::vector<uint64_t> &a, const std::vector<uint64_t> &q, uint64_t slot,
+                 uint64_t extra, int32_t flags, uint64_t *budget, uint64_t *peak);
 
 }  // namespace ckpt

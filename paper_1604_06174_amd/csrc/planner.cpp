@@ -231,4 +231,52 @@ Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vec
   return acc;
 }
 
+// ---------------------------------------------------- budget search --
+// Appendix A: Alg. 3 with B = 0 gives x and y; B0 = floor(sqrt(x y)); the
+// candidates are B0 and six evenly spaced budgets from floor(B0 / sqrt 2) to
+// floor(sqrt(2) B0), all from exact integer square roots.
+static uint64_t isqrt128(unsigned __int128 v) {
+  uint64_t lo = 0, hi = ~uint64_t(0);
+  while (lo < hi) {  // largest r with r*r <= v
+    const uint64_t mid = lo + (hi - lo) / 2 + 1;
+    if ((unsigned __int128)mid * mid <= v) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+std::vector<uint64_t> search_candidates(int32_t n, const uint64_t *lb, const uint64_t *cb) {
+  const Plan z = make_plan(n, lb, cb, 0, CKPT_GREEDY, nullptr, 0, 0);
+  const uint64_t b0 = isqrt128((unsigned __int128)z.x * z.y);
+  const unsigned __int128 sq = (unsigned __int128)b0 * b0;
+  const uint64_t lo = isqrt128(sq / 2), hi = isqrt128(sq * 2);
+  std::vector<uint64_t> c{b0};
+  for (uint64_t j = 0; j < 6; ++j) c.push_back(lo + uint64_t((unsigned __int128)(hi - lo) * j / 5));
+  std::sort(c.begin(), c.end());
+  c.erase(std::unique(c.begin(), c.end()), c.end());
+  return c;
+}
+
+Plan search_plan(int32_t n, const uint64_t *lb, const uint64_t *cb, const std::vector<uint64_t> &b,
+                 const std::vector<uint64_t> &a, const std::vector<uint64_t> &q, uint64_t slot,
+                 uint64_t extra, int32_t flags, uint64_t *budget, uint64_t *peak) {
+  bool have = false;
+  Plan best;
+  uint64_t best_b = 0, best_pk = 0;
+  for (uint64_t B : search_candidates(n, lb, cb)) {
+    Plan p = make_plan(n, lb, cb, B, CKPT_GREEDY, nullptr, 0, flags);
+    const uint64_t pk = account(p, b, a, q, slot, extra).peak();
+    if (!have || pk < best_pk) {  // candidates ascend: ties keep the smaller budget
+      have = true;
+      best = std::move(p);
+      best_b = B;
+      best_pk = pk;
+    }
+  }
+  if (budget) *budget = best_b;
+  if (peak) *peak = best_pk;
+  return best;
+}
+
 }  // namespace ckpt
+

@@ -200,3 +200,46 @@ def test_single_hip_runtime_in_process():
     """The binding maps the library after torch, so the process holds one HIP
     runtime (torch's) whatever the import order of the caller."""
     assert len(K._hip_runtimes()) == 1, K._hip_runtimes()
+
+
+def test_plan_search_matches_oracle_fuzz():
+    rng = np.random.default_rng(77)
+    for it in range(200):
+        n = int(rng.integers(1, 60))
+        b = [int(v) for v in rng.integers(1, 1 << 20, n + 1)]
+        a = [int(v) for v in rng.integers(0, 1 << 22, n)]
+        q = [int(v) for v in rng.integers(0, 1 << 20, n)]
+        lb = [a[i] + b[i + 1] for i in range(n)]
+        cb = [b[i + 1] if rng.random() < 0.85 else 0 for i in range(n - 1)] + [0]
+        slot = int(rng.integers(0, 1 << 21)) if it % 3 == 0 else 0
+        extra = int(rng.integers(0, 1 << 20)) if it % 5 == 0 else 0
+        flags = K.FLAG_KEEP_LAST if it % 2 else 0
+        lp, B, peak = K.plan_search(lb, cb, b, a, q, slot, extra, flags)
+        op, OB, opeak = PL.search(n, lb, cb, b, a, q, slot or None, extra, flags)
+        assert (B, peak) == (OB, opeak), it
+        assert lp.serialize() == op.serialize(), it
+
+
+def test_plan_search_on_workload_tables():
+    """The search on the real layouts (x*y exceeds 64 bits on the bf16 ResNet)."""
+    from paper_1604_06174_amd.workload import net_for
+    for name in ("cifar110", "resnet1000", "lstm4096", "mlp1024"):
+        cfg = synth.WORKLOADS[name]
+        net = net_for(cfg)
+        lp, B, peak = net.search_plan()
+        st = synth.structure(cfg)
+        b, a, q = SZ.tables(st)
+        lb, cb = SZ.layer_and_cut_bytes(st)
+        slot, extra = SZ.grad_layout(st)
+        op, OB, opeak = PL.search(st.n, lb, cb, b, a, q, slot, extra)
+        assert (B, peak) == (OB, opeak) and lp.serialize() == op.serialize(), name
+        assert net.accounting(lp)["peak"] == peak
+
+
+def test_plan_search_errors():
+    with pytest.raises(K.CkptError) as ei:
+        K.plan_search([1, 2], [1, 1], [1, 1, 1], [1, 1], [1, 1])
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError) as ei:
+        K.plan_search([1, 2], [1, 0], [1, 1, 1], [1, 1], [1, 1], flags=8)
+    assert ei.value.code == K.E_INVALID

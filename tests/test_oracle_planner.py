@@ -221,3 +221,50 @@ def test_size_tables_match_kept_tensors(cfg):
         assert kept == a[i], (i, kept, a[i])
         assert SZ.align(y.nbytes) == b[i + 1]
         x = y
+
+
+# ---- appendix-A search over the budget ----------------------------------
+
+def test_search_hand_traced_golden():
+    with open(os.path.join(GOLDEN, "search_small.json")) as f:
+        g = json.load(f)
+    lb, cb = g["layer_bytes"], g["cut_bytes"]
+    _, x, y = PL.greedy_alg3(lb, cb, 0)
+    assert (x, y) == (g["x0"], g["y0"])
+    assert math.isqrt(x * y) == g["b0"]
+    assert PL.search_candidates(lb, cb) == g["candidates"]
+    for B, cuts in g["cuts"].items():
+        assert PL.plan(len(lb), lb, cb, int(B), PL.GREEDY).cuts == cuts
+
+
+@pytest.mark.parametrize("n,s,c", [(16, 1000, 300), (100, 4096, 512), (334, 77, 5)])
+def test_search_candidates_closed_form_uniform(n, s, c):
+    """Uniform layers: B = 0 keeps all n-1 candidates, x = (n-1) c, y = s."""
+    lb, cb = [s] * n, [c] * (n - 1) + [0]
+    b0 = math.isqrt((n - 1) * c * s)
+    cands = PL.search_candidates(lb, cb)
+    assert b0 in cands and len(cands) <= 7
+    assert min(cands) == math.isqrt(b0 * b0 // 2) == math.floor(b0 / math.sqrt(2))
+    assert max(cands) == math.isqrt(2 * b0 * b0)
+    assert all(b0 / math.sqrt(2) - 1 <= B <= math.sqrt(2) * b0 for B in cands)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_search_returns_lowest_exact_peak(seed):
+    rng = np.random.default_rng(4000 + seed)
+    n = int(rng.integers(1, 40))
+    b = [int(v) for v in rng.integers(1, 5000, n + 1)]
+    a = [int(v) for v in rng.integers(0, 9000, n)]
+    q = [int(v) for v in rng.integers(0, 3000, n)]
+    lb = [a[i] + b[i + 1] for i in range(n)]
+    cb = [b[i + 1] if rng.random() < 0.8 else 0 for i in range(n - 1)] + [0]
+    flags = PL.FLAG_KEEP_LAST if seed % 2 else 0
+    p, B, peak = PL.search(n, lb, cb, b, a, q, None, 0, flags)
+    peaks = {C: PL.account(PL.plan(n, lb, cb, C, PL.GREEDY, flags=flags), b, a, q).peak
+             for C in PL.search_candidates(lb, cb)}
+    assert peak == min(peaks.values())
+    assert B == min(C for C, v in peaks.items() if v == peak)
+    assert p.serialize() == PL.plan(n, lb, cb, B, PL.GREEDY, flags=flags).serialize()
+    # never worse than the plain B0 run it refines
+    b0 = math.isqrt(PL.greedy_alg3(lb, cb, 0)[1] * PL.greedy_alg3(lb, cb, 0)[2])
+    assert peak <= peaks[b0]

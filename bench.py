@@ -47,6 +47,27 @@ def _plan_args(cfg, net):
     raise ValueError(mode)
 
 
+def _traffic(workload):
+    """Measured HBM bytes per launch of the dominant kernel family, from the
+    calibrated rocprofv3 FETCH_SIZE / WRITE_SIZE runs recorded in
+    profiles/traffic.json; None when none was recorded for this workload or
+    when a source file the counters were taken on has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)["workloads"][workload]
+        h = hashlib.sha256()
+        for src in rec["sources"]:
+            with open(os.path.join(ROOT, src), "rb") as f:
+                h.update(f.read())
+    except (OSError, KeyError, ValueError):
+        return None
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
+    return rec
+
+
 def _cpu_baseline(cfg, sample_batch, d_full):
     """The oracle's own checkpointed executor (Alg. 1 with the same plan) on a
     smaller batch of the same network (the same parameters, the first samples
@@ -175,8 +196,13 @@ def main():
     dtype = cfg.get("dtype", "f32")  # "bf16": bf16 GEMM operands, fp32 accumulation
     achieved = kt["flops"] / (kt["ms"] / 1e3) / 1e12 if kt["ms"] > 0 else 0.0
     peak = PEAK_TFLOPS[dtype]
+    tr = _traffic(args.workload)
+    alg_bytes = kt["bytes"] / max(kt["launches"], 1)
     roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "frac": round(achieved / peak, 4),
+            "traffic": tr["traffic_bytes_per_launch"] if tr else None,
+            "algorithmic_bytes_per_launch": round(alg_bytes),
+            "traffic_over_algorithmic": round(tr["traffic_bytes_per_launch"] / alg_bytes, 3) if tr else None,
             "kernel": kt["kernel"], "launches": kt["launches"],
             "avg_launch_us": round(kt["ms"] * 1e3 / max(kt["launches"], 1), 3),
             "flops_per_launch": kt["flops"] / max(kt["launches"], 1),

@@ -1,4 +1,6 @@
 // Dense bf16 GEMM entry points (kernel and conventions in gemm_bf16_kernel.h).
+#include <algorithm>
+
 #include "gemm_bf16_kernel.h"
 
 namespace ckpt {
@@ -49,6 +51,59 @@ void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, i
                const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D, int ldd,
                const float *bias) {
   gemm_bf16x(s, M, N, K, A, a_fp32, lda, ak, B, ldb, bk, C, ldc, epi, D, ldd, bias, GemmX{});
+}
+
+namespace {
+
+// C[m, n] = sum over z = 0..ns-1 (in order) of part[z][m][n] (+ D[m, n]) (+ bias[n]);
+// four consecutive columns per thread (N % 4 == 0).
+__global__ __launch_bounds__(256) void k_sum_slices(const float *__restrict__ part, int ns, int M,
+                                                    int N, float *__restrict__ C, int ldc,
+                                                    const float *__restrict__ D, int ldd,
+                                                    const float *__restrict__ bias) {
+  const int NQ = N / 4;
+  const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= int64_t(M) * NQ) return;
+  const int m = int(e / NQ), n = int(e % NQ) * 4;
+  const size_t slice = size_t(M) * N, o = size_t(m) * N + n;
+  float4 acc = *reinterpret_cast<const float4 *>(part + o);
+  for (int z = 1; z < ns; ++z) {
+    const float4 v = *reinterpret_cast<const float4 *>(part + z * slice + o);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  if (D) {
+    const float *d = D + size_t(m) * ldd + n;
+    acc.x += d[0]; acc.y += d[1]; acc.z += d[2]; acc.w += d[3];
+  }
+  if (bias) {
+    acc.x += bias[n]; acc.y += bias[n + 1]; acc.z += bias[n + 2]; acc.w += bias[n + 3];
+  }
+  float *c = C + size_t(m) * ldc + n;
+  c[0] = acc.x; c[1] = acc.y; c[2] = acc.z; c[3] = acc.w;
+}
+
+}  // namespace
+
+int gemm_bf16_splits(int M, int N, int K) {
+  const int tiles = gemm_bf16_tiles(M, N);
+  int s = (512 + tiles - 1) / tiles;
+  s = std::min(s, std::max(1, K / (4 * KS)));  // at least four k-slices per split
+  return std::max(s, 1);
+}
+
+void gemm_bf16_part(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
+                    const void *B, int ldb, bool bk, float *part, int splits) {
+  GemmX x;
+  x.splits = splits;
+  gemm_bf16x(s, M, N, K, A, a_fp32, lda, ak, B, ldb, bk, part, N, GEMM_EPI_STORE, nullptr, 0,
+             nullptr, x);
+}
+
+void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, float *C, int ldc,
+                const float *D, int ldd, const float *bias) {
+  const int64_t e = int64_t(M) * (N / 4);
+  hipLaunchKernelGGL(k_sum_slices, dim3(unsigned((e + 255) / 256)), dim3(256), 0, s, part, nslices,
+                     M, N, C, ldc, D, ldd, bias);
 }
 
 int gemm_bf16_row_blocks(int M, int N) {

@@ -113,6 +113,15 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
                 int ldd, const float *bias, const GemmX &x);
 int gemm_bf16_row_blocks(int M, int N);
 int gemm_bf16_tiles(int M, int N);
+// Split-K for short, wide products: gemm_bf16_part writes `splits` partial
+// [M, N] products (contiguous slices) of op(A) op(B) over consecutive k
+// ranges; sum_slices adds nslices such slices in order, then D and bias:
+// C = sum_z part[z] (+ D) (+ bias[n]).  N must be a multiple of 4.
+int gemm_bf16_splits(int M, int N, int K);
+void gemm_bf16_part(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
+                    const void *B, int ldb, bool bk, float *part, int splits);
+void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, float *C, int ldc,
+                const float *D = nullptr, int ldd = 0, const float *bias = nullptr);
 // out[e] = sum_b part[b*E + e], b in a fixed order
 void sum_partials(hipStream_t s, const float *part, int nb, int E, float *out);
 

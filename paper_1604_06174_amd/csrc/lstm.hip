@@ -64,38 +64,63 @@ __global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const floa
 // One workgroup per row: loss_row = log sum exp(l - max) + max - l[label];
 // dlog = (softmax - onehot) * scale.  A label outside [0, V) gives a NaN loss
 // for the row and no one-hot term.
-__global__ __launch_bounds__(256) void k_softmax_ce_rows(int V, const float *__restrict__ logits,
-                                                         const int *__restrict__ labels, float scale,
-                                                         float *__restrict__ dlog,
-                                                         float *__restrict__ loss_rows) {
-  __shared__ float red[256];
-  const int row = blockIdx.x, t = threadIdx.x;
+// One workgroup of 1024 threads per row: each thread keeps its (at most
+// SM_PER) logits in registers; max and sum are reduced by wavefront
+// butterflies and then across the 16 wavefronts in a fixed order.
+constexpr int SM_THREADS = 1024, SM_PER = 16;
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(SM_THREADS) void k_softmax_ce_rows(int V, const float *__restrict__ logits,
+                                                                const int *__restrict__ labels, float scale,
+                                                                float *__restrict__ dlog,
+                                                                float *__restrict__ loss_rows) {
+  __shared__ float red[SM_THREADS / 64];
+  const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const float *l = logits + size_t(row) * V;
+  float x[SM_PER];
   float mx = -INFINITY;
-  for (int v = t; v < V; v += 256) mx = fmaxf(mx, l[v]);
-  red[t] = mx;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
-    __syncthreads();
+#pragma unroll
+  for (int k = 0; k < SM_PER; ++k) {
+    const int v = t + k * SM_THREADS;
+    x[k] = v < V ? l[v] : -INFINITY;
+    mx = fmaxf(mx, x[k]);
   }
+  mx = wave_max(mx);
+  if (lane == 0) red[w] = mx;
+  __syncthreads();
   mx = red[0];
+  for (int k = 1; k < SM_THREADS / 64; ++k) mx = fmaxf(mx, red[k]);
   __syncthreads();
   float se = 0.f;
-  for (int v = t; v < V; v += 256) se += expf(l[v] - mx);
-  red[t] = se;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (t < w) red[t] += red[t + w];
-    __syncthreads();
+#pragma unroll
+  for (int k = 0; k < SM_PER; ++k) {
+    const int v = t + k * SM_THREADS;
+    x[k] = v < V ? expf(x[k] - mx) : 0.f;
+    se += x[k];
   }
-  se = red[0];
+  se = wave_sum(se);
+  if (lane == 0) red[w] = se;
+  __syncthreads();
+  se = 0.f;
+  for (int k = 0; k < SM_THREADS / 64; ++k) se += red[k];
   const int lab = labels[row];
   const bool ok = lab >= 0 && lab < V;
   if (t == 0) loss_rows[row] = ok ? (logf(se) + mx) - l[lab] : NAN;
   const float inv = 1.0f / se;
   float *d = dlog + size_t(row) * V;
-  for (int v = t; v < V; v += 256) d[v] = (expf(l[v] - mx) * inv - (v == lab ? 1.f : 0.f)) * scale;
+#pragma unroll
+  for (int k = 0; k < SM_PER; ++k) {
+    const int v = t + k * SM_THREADS;
+    if (v < V) d[v] = (x[k] * inv - (v == lab ? 1.f : 0.f)) * scale;
+  }
 }
 
 // Workgroup = 64 columns x 4 row groups (rows b = rg, rg + 4, ...); the
@@ -216,8 +241,8 @@ void lstm_fwd_point(hipStream_t s, int B, int H, const float *z, const float *c_
 
 void softmax_ce_rows(hipStream_t s, int rows, int V, const float *logits, const int *labels,
                      float scale, float *dlog, float *loss_rows) {
-  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(256), 0, s, V, logits, labels, scale, dlog,
-                     loss_rows);
+  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(SM_THREADS), 0, s, V, logits, labels, scale,
+                     dlog, loss_rows);
 }
 
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {

@@ -18,6 +18,8 @@
 // [B,H]); gradient slot = dh | dc (fp32); extra gradient buffers = the chunk's
 // dz (bf16 [C*B,4H]), head gradient (bf16 [C*B,V]), h_{t-1} and h_t copies
 // (bf16 [C*B,H]).
+#include <algorithm>
+
 #include "kernels.h"
 #include "net.h"
 
@@ -31,7 +33,9 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_z, k_logits, k_lossrows, k_loss;
+  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_z, k_logits, k_lossrows, k_loss, k_part;
+  // split-K counts: input and recurrent parts of z, logits, dh (head), dh_{t-1}
+  int s_x, s_h, s_l, s_dh, s_dx;
   // extra gradient buffer offsets
   uint64_t x_dz, x_dl, x_hp, x_hc;
 
@@ -78,6 +82,14 @@ class LstmNet : public Net {
     k_logits = take(uint64_t(B) * V * 4);
     k_lossrows = take(uint64_t(T) * B * 4);
     k_loss = take(4);
+    s_x = gemm_bf16_splits(B, 4 * H, E);
+    s_h = gemm_bf16_splits(B, 4 * H, H);
+    s_l = gemm_bf16_splits(B, V, H);
+    s_dh = gemm_bf16_splits(B, H, V);
+    s_dx = gemm_bf16_splits(B, H, 4 * H);
+    const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(s_l) * B * V,
+                                    uint64_t(std::max(s_dh, s_dx)) * B * H});
+    k_part = take(part * 4);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
   }
@@ -92,6 +104,20 @@ class LstmNet : public Net {
     timer.begin(c.s);
     gemm_bf16(c.s, M, N, Kd, A, a32, lda, ak, Bm, ldb, bk, Cm, ldc, epi, D, ldd, bias);
     timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
+    c.launches += 1;
+  }
+  // split-K partial products into slices [z0, z0 + splits) of the partial buffer
+  void gemm_part(StepCtx &c, int M, int N, int Kd, const void *A, int lda, const void *Bm, int ldb,
+                 int z0, int splits) {
+    timer.begin(c.s);
+    gemm_bf16_part(c.s, M, N, Kd, A, false, lda, true, Bm, ldb, true,
+                   Kf(c, k_part) + size_t(z0) * M * N, splits);
+    timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * splits * M * N);
+    c.launches += 1;
+  }
+  void sum_parts(StepCtx &c, int ns, int M, int N, float *Cm, const float *D = nullptr, int ldd = 0,
+                 const float *bias = nullptr) {
+    sum_slices(c.s, Kf(c, k_part), ns, M, N, Cm, N, D, ldd, bias);
     c.launches += 1;
   }
 
@@ -112,16 +138,17 @@ class LstmNet : public Net {
     const void *xt = static_cast<const char *>(c.input) + size_t(i) * B * E * 2;
     const int *lab = static_cast<const int *>(c.target) + size_t(i) * B;
     float *z = Kf(c, k_z);
-    gemm(c, B, 4 * H, E, xt, false, E, true, K(c, k_wxt), E, true, z, 4 * H, GEMM_EPI_STORE, nullptr,
-         0, P(c, pb));
-    if (i > 0)
-      gemm(c, B, 4 * H, H, x, false, H, true, K(c, k_wht), H, true, z, 4 * H, GEMM_EPI_ADD, z, 4 * H);
+    // z = x_t W_x + h_{t-1} W_h + b: both products split over k into one
+    // slice buffer, summed in order with the bias
+    gemm_part(c, B, 4 * H, E, xt, E, K(c, k_wxt), E, 0, s_x);
+    if (i > 0) gemm_part(c, B, 4 * H, H, x, H, K(c, k_wht), H, s_x, s_h);
+    sum_parts(c, s_x + (i > 0 ? s_h : 0), B, 4 * H, z, nullptr, 0, P(c, pb));
     const float *c_prev = i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr;
     float *gates = reinterpret_cast<float *>(sv);
     lstm_fwd_point(c.s, B, H, z, c_prev, gates, y, reinterpret_cast<float *>(y + hb));
     float *logits = Kf(c, k_logits);
-    gemm(c, B, V, H, y, false, H, true, K(c, k_wot), H, true, logits, V, GEMM_EPI_STORE, nullptr, 0,
-         P(c, pbo));
+    gemm_part(c, B, V, H, y, H, K(c, k_wot), H, 0, s_l);
+    sum_parts(c, s_l, B, V, logits, nullptr, 0, P(c, pbo));
     softmax_ce_rows(c.s, B, V, logits, lab, 1.0f / (float(T) * float(B)),
                     reinterpret_cast<float *>(sv + ga), Kf(c, k_lossrows) + size_t(i) * B);
     c.launches += 2;
@@ -144,16 +171,18 @@ class LstmNet : public Net {
     char *hc = X(c, x_hc) + row * H * 2;
     head_bwd_prep(c.s, B, V, reinterpret_cast<const float *>(sv + ga), dl, G(c, pbo), first_step);
     float *dh = static_cast<float *>(qv);
-    gemm(c, B, H, V, dl, false, V, true, K(c, k_wo), V, true, dh, H, GEMM_EPI_ADD,
-         reinterpret_cast<const float *>(g), H);
+    // total dh = (head gradient) W_o^T + the incoming dh
+    gemm_part(c, B, H, V, dl, V, K(c, k_wo), V, 0, s_dh);
+    sum_parts(c, s_dh, B, H, dh, reinterpret_cast<const float *>(g), H);
     lstm_bwd_point(c.s, B, H, dh, reinterpret_cast<const float *>(g + gh),
                    reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
                    i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
                    dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc, G(c, pb), first_step);
     c.launches += 2;
-    if (dx)
-      gemm(c, B, H, 4 * H, dz, false, 4 * H, true, K(c, k_wh), 4 * H, true,
-           reinterpret_cast<float *>(dx), H, GEMM_EPI_STORE);
+    if (dx) {
+      gemm_part(c, B, H, 4 * H, dz, 4 * H, K(c, k_wh), 4 * H, 0, s_dx);
+      sum_parts(c, s_dx, B, H, reinterpret_cast<float *>(dx));
+    }
     if (i == t0) {  // the chunk [t0, t0 + C) is complete: its weight gradients
       const int rows = (std::min(t0 + C, int(n)) - t0) * B;
       const bool first_chunk = t0 + C >= n;
@@ -187,6 +216,8 @@ std::unique_ptr<Net> make_lstm_net(const ckpt_net_desc &d) {
     fail(CKPT_E_INVALID, "net_create: LSTM needs positive batch, steps, hidden, input and vocabulary");
   if (d.width % 8 != 0 || d.image % 8 != 0 || d.n_classes % 8 != 0)
     fail(CKPT_E_UNSUPPORTED, "net_create: LSTM sizes must be multiples of 8");
+  if (d.n_classes > 16384)
+    fail(CKPT_E_UNSUPPORTED, "net_create: LSTM vocabulary above 16384");
   if (int64_t(d.depth) * d.batch * d.image > (int64_t(1) << 31) ||
       int64_t(d.batch) * d.n_classes * 32 > (int64_t(1) << 31))
     fail(CKPT_E_INVALID, "net_create: LSTM tensors too large");

@@ -13,7 +13,7 @@ CASES = {
     "mlp": dict(kind="mlp", depth=23, width=64, batch=16, seed=61),
     "resnet_basic": dict(kind="resnet_basic", blocks_per_stage=3, base=8, batch=4, image=16,
                          classes=10, seed=62),
-    "lstm": dict(kind="lstm", T=21, batch=8, input=32, hidden=32, vocab=50, grad_chunk=4, seed=63),
+    "lstm": dict(kind="lstm", T=21, batch=8, input=32, hidden=32, vocab=56, grad_chunk=4, seed=63),
     "resnet_bottleneck": dict(kind="resnet_bottleneck", stage_blocks=(3, 2), widths=(8, 16),
                               expansion=4, stem_channels=8, image=16, batch=2, classes=7, seed=64),
 }

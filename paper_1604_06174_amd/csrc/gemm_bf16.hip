@@ -34,11 +34,13 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
   if (M <= 0 || N <= 0) return;
   const int splits = x.splits < 1 ? 1 : x.splits;
   const Args a = make_args(M, N, K, A, lda, B, ldb, C, ldc, D, ldd, bias, x);
-#define CKPT_GB(AK_, BK_)                                                            \
-  if (ak == AK_ && bk == BK_) {                                                      \
-    if (a_fp32) pick_tile<AK_, BK_, float, G_DENSE, G_DENSE>(a, epi, splits, s);     \
-    else pick_tile<AK_, BK_, __bf16, G_DENSE, G_DENSE>(a, epi, splits, s);           \
-    return;                                                                          \
+  const bool safe = !a_fp32 && safe8(a, ak, bk);
+#define CKPT_GB(AK_, BK_)                                                                  \
+  if (ak == AK_ && bk == BK_) {                                                            \
+    if (a_fp32) pick_tile<AK_, BK_, float, G_DENSE, G_DENSE, false>(a, epi, splits, s);    \
+    else if (safe) pick_tile<AK_, BK_, __bf16, G_DENSE, G_DENSE, true>(a, epi, splits, s); \
+    else pick_tile<AK_, BK_, __bf16, G_DENSE, G_DENSE, false>(a, epi, splits, s);          \
+    return;                                                                                \
   }
   CKPT_GB(true, true)
   CKPT_GB(true, false)

@@ -44,7 +44,7 @@ void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *W
   a.ldc = N;
   a.Cb = static_cast<__bf16 *>(Yb);
   a.stats = stats;
-  pick_tile<true, true, __bf16, GA_FWD, G_DENSE>(a, GEMM_EPI_BF16STATS, 1, s);
+  pick_tile<true, true, __bf16, GA_FWD, G_DENSE, true>(a, GEMM_EPI_BF16STATS, 1, s);
 }
 
 void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void *Wt, float *DX,
@@ -58,7 +58,7 @@ void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void
   a.D = D;
   a.ldd = N;
   a.Ym = static_cast<const __bf16 *>(mask);
-  pick_tile<true, false, __bf16, GA_DGRAD, GB_WDGRAD>(a, epi, 1, s);
+  pick_tile<true, false, __bf16, GA_DGRAD, GB_WDGRAD, true>(a, epi, 1, s);
 }
 
 void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void *DY, float *part,
@@ -73,7 +73,7 @@ void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void 
   a.B = static_cast<const __bf16 *>(X);
   a.C = splits > 1 ? part : dW;
   a.ldc = N;
-  pick_tile<false, false, __bf16, G_DENSE, GB_WGRAD>(a, GEMM_EPI_STORE, splits, s);
+  pick_tile<false, false, __bf16, G_DENSE, GB_WGRAD, true>(a, GEMM_EPI_STORE, splits, s);
   if (splits > 1) sum_partials(s, part, splits, M * N, dW);
 }
 

@@ -24,11 +24,12 @@
 //
 // Block = 256 threads = 4 wavefronts in a WM x WN grid; each wavefront owns a
 // (BM/WM) x (BN/WN) tile of 16x16 accumulators.  K advances in slices of 32
-// through double-buffered LDS stored k-contiguous ([m][k] and [n][k]), so
-// every lane reads its MFMA operand (8 consecutive k of one row) as one
-// 16-byte LDS load.  Operands stored the other way round are transposed while
-// they are written to LDS.  Every output element is reduced over K in one
-// fixed order (bit-reproducible).
+// through double-buffered LDS, with the global loads of a slice issued two
+// slices ahead.  A k-contiguous operand is stored [row][k], so every lane
+// reads its MFMA operand (8 consecutive k of one row) as one 16-byte LDS
+// load; a k-major operand stays k-major in LDS and reaches the matrix cores
+// through gfx950's transposing LDS read.  Every output element is reduced
+// over K in one fixed order (bit-reproducible).
 //
 // Epilogues: STORE C = acc (+ bias[n]); ADD C = acc + D (D may alias C);
 // ADDMASK C = acc + (Ym > 0 ? D : 0) with Ym bf16 shaped like D;
@@ -77,46 +78,55 @@ struct Args {
   float inv_wo, inv_ho;
 };
 
-__device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void zero8(__bf16 r[8]) {
-#pragma unroll
-  for (int u = 0; u < 8; ++u) r[u] = (__bf16)0.f;
+// A staged operand chunk: 8 bf16 in four dwords, kept as one vector so that
+// its global load stays in flight until the chunk is written to LDS.
+__device__ __forceinline__ u32x4 zero_chunk() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// 16-byte load of p when ok, else of the always-valid `safe` address, the
+// result zeroed when !ok: no branch around the load.
+__device__ __forceinline__ u32x4 masked16(const void *p, const void *safe, bool ok) {
+  const u32x4 v = *reinterpret_cast<const u32x4 *>(ok ? p : safe);
+  const unsigned m = ok ? 0xffffffffu : 0u;
+  return u32x4{v.x & m, v.y & m, v.z & m, v.w & m};
 }
 
-__device__ __forceinline__ void vload8(__bf16 r[8], const __bf16 *p) {
-  const bf16x8 v = *reinterpret_cast<const bf16x8 *>(p);
-#pragma unroll
-  for (int u = 0; u < 8; ++u) r[u] = v[u];
+__device__ __forceinline__ unsigned pack2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return unsigned(__builtin_bit_cast(unsigned short, a)) |
+         (unsigned(__builtin_bit_cast(unsigned short, b)) << 16);
 }
 
-// 8 consecutive elements of row `row` starting at column `col` of a
-// row-major [rows, cols] matrix of T, zero outside, as bf16.
-template <typename T>
-__device__ __forceinline__ void ld8(__bf16 r[8], const T *base, int row, int col, int rows, int cols,
-                                    int ld) {
-  const bool inrow = row < rows;
-  const T *p = base + size_t(row) * ld + col;
-  if (inrow && col + 7 < cols && (ld % 8 == 0)) {
-    if constexpr (std::is_same<T, float>::value) {
-      const float4 a = *reinterpret_cast<const float4 *>(p);
-      const float4 b = *reinterpret_cast<const float4 *>(p + 4);
-      r[0] = to_bf16(a.x); r[1] = to_bf16(a.y); r[2] = to_bf16(a.z); r[3] = to_bf16(a.w);
-      r[4] = to_bf16(b.x); r[5] = to_bf16(b.y); r[6] = to_bf16(b.z); r[7] = to_bf16(b.w);
-    } else {
-      vload8(r, p);
-    }
+// 8 consecutive elements of row `row` from column `col` of a row-major
+// [rows, cols] matrix of T, zero outside, as bf16.  SAFE: cols and ld are
+// multiples of 8 (T = bf16), so a chunk is wholly inside or outside.
+template <bool SAFE, typename T>
+__device__ __forceinline__ u32x4 ld8(const T *base, int row, int col, int rows, int cols, int ld) {
+  if constexpr (SAFE) {
+    return masked16(base + size_t(row) * ld + col, base, row < rows && col < cols);
   } else {
+    const bool inrow = row < rows;
+    const T *p = base + size_t(row) * ld + col;
+    float f[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (inrow && col + u < cols) {
-        if constexpr (std::is_same<T, float>::value) r[u] = to_bf16(p[u]);
-        else r[u] = p[u];
-      } else {
-        r[u] = (__bf16)0.f;
-      }
-    }
+    for (int u = 0; u < 8; ++u) f[u] = (inrow && col + u < cols) ? float(p[u]) : 0.f;
+    return u32x4{pack2(f[0], f[1]), pack2(f[2], f[3]), pack2(f[4], f[5]), pack2(f[6], f[7])};
   }
+}
+
+// MFMA operand (8 consecutive k of one row) from a k-major LDS tile with the
+// transposing read: within each 16-lane group, lane 4t + s points at k-row t
+// (then t + 4, `step` bytes further) and columns 4s..4s+3 of the group's 16
+// rows, and lane i receives column i of k-rows 0..3 (then 4..7).
+typedef short short4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8 tr_operand(const unsigned char *p, int step) {
+  typedef __attribute__((address_space(3))) short4v lds_short4;
+  const short4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(p));
+  const short4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(p + step));
+  typedef short short8v __attribute__((ext_vector_type(8)));
+  const short8v v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
 }
 
 // q = x / d for 0 <= x < 2^24 (float estimate, then corrected)
@@ -153,24 +163,22 @@ __device__ __forceinline__ RowPix row_pixel(const Args &p, int m, int h, int w) 
 }
 
 template <int GA>
-__device__ __forceinline__ void gatherA(__bf16 r[8], const Args &p, const __bf16 *A, const RowPix &rp,
-                                        int k, int kend) {
-  if (!rp.ok || k >= kend) { zero8(r); return; }
+__device__ __forceinline__ u32x4 gatherA(const Args &p, const __bf16 *A, const RowPix &rp, int k, int kend) {
   const int C = 1 << p.cshift;
   const int tap = k >> p.cshift, ch = k & (C - 1);
   int kh, kw;
   tap_hw(tap, p.R, kh, kw);
   if constexpr (GA == GA_FWD) {
     const int hi = rp.y * p.S + kh - p.P, wi = rp.x * p.S + kw - p.P;
-    if (hi < 0 || hi >= p.H || wi < 0 || wi >= p.W) { zero8(r); return; }
-    vload8(r, A + ((size_t(rp.img) * p.H + hi) * p.W + wi) * C + ch);
+    const bool ok = rp.ok && k < kend && hi >= 0 && hi < p.H && wi >= 0 && wi < p.W;
+    return masked16(A + ((size_t(rp.img) * p.H + hi) * p.W + wi) * C + ch, A, ok);
   } else {
     const int t = rp.y + p.P - kh, u = rp.x + p.P - kw;
     const int sm = p.S - 1;  // S in {1, 2}
-    if (t < 0 || u < 0 || (t & sm) || (u & sm)) { zero8(r); return; }
     const int ho = t >> sm, wo = u >> sm;
-    if (ho >= p.Ho || wo >= p.Wo) { zero8(r); return; }
-    vload8(r, A + ((size_t(rp.img) * p.Ho + ho) * p.Wo + wo) * C + ch);
+    const bool ok = rp.ok && k < kend && t >= 0 && u >= 0 && !(t & sm) && !(u & sm) && ho < p.Ho &&
+                    wo < p.Wo;
+    return masked16(A + ((size_t(rp.img) * p.Ho + ho) * p.Wo + wo) * C + ch, A, ok);
   }
 }
 
@@ -190,26 +198,23 @@ __device__ __forceinline__ ColTap col_tap(const Args &p, int n) {
   return c;
 }
 
-__device__ __forceinline__ void gatherB_wgrad(__bf16 r[8], const Args &p, const ColTap &ct, int k,
-                                              int kend) {
-  if (!ct.ok || k >= kend) { zero8(r); return; }
+__device__ __forceinline__ u32x4 gatherB_wgrad(const Args &p, const ColTap &ct, int k, int kend) {
   const int t = divq(k, p.Wo, p.inv_wo);
   const int wo = k - t * p.Wo;
   const int img = divq(t, p.Ho, p.inv_ho);
   const int ho = t - img * p.Ho;
   const int hi = ho * p.S + ct.kh - p.P, wi = wo * p.S + ct.kw - p.P;
-  if (hi < 0 || hi >= p.H || wi < 0 || wi >= p.W) { zero8(r); return; }
-  vload8(r, p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch);
+  const bool ok = ct.ok && k < kend && hi >= 0 && hi < p.H && wi >= 0 && wi < p.W;
+  return masked16(p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch, p.B, ok);
 }
 
-__device__ __forceinline__ void gatherB_wdgrad(__bf16 r[8], const Args &p, int k, int n, int kend) {
-  if (k >= kend || n >= p.N) { zero8(r); return; }
+__device__ __forceinline__ u32x4 gatherB_wdgrad(const Args &p, int k, int n, int kend) {
   const int Co = 1 << p.cshift;
   const int tap = k >> p.cshift, co = k & (Co - 1);
-  vload8(r, p.B + (size_t(co) * p.R * p.R + tap) * p.N + n);
+  return masked16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, p.B, k < kend && n < p.N);
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB>
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB, bool SAFE>
 __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   constexpr int TM = BM / WM / 16, TN = BN / WN / 16;  // 16x16 tiles per wavefront
   static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "wave grid");
@@ -217,9 +222,19 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   static_assert(GB == G_DENSE || !BK, "B gathers are n-contiguous");
   constexpr int CHA = BM * KS / 8, CHB = BN * KS / 8;  // 8-element chunks per slice
   constexpr int PA = (CHA + 255) / 256, PB = (CHB + 255) / 256;
-  __shared__ __align__(16) __bf16 As[2][BM][KP];
-  __shared__ __align__(16) __bf16 Bs[2][BN][KP];
-  static_assert(EPI != GEMM_EPI_BF16STATS || WM * 4 * 2 * BN * 8 <= int(sizeof(As)), "stats scratch");
+  constexpr int WC = BN / WN;                           // columns per wavefront
+  constexpr int SP = WC + 4;                            // staging row pitch (floats)
+  // LDS operand tiles, double-buffered.  A k-contiguous operand is stored
+  // [buf][row][k] (pitch KP); a k-major one is stored as it arrives,
+  // [buf][k][row] (pitch rows + 16), and read back through the transposing
+  // LDS read (two 8-byte reads give a lane its 8 consecutive k).
+  constexpr int PA_K = BM + 16, PB_K = BN + 16;
+  constexpr int SZA = AK ? 2 * BM * KP * 2 : 2 * KS * PA_K * 2;
+  constexpr int SZB = BK ? 2 * BN * KP * 2 : 2 * KS * PB_K * 2;
+  __shared__ __align__(16) unsigned char smA[SZA];
+  __shared__ __align__(16) unsigned char smB[SZB];
+  static_assert(EPI != GEMM_EPI_BF16STATS || WM * 4 * 2 * BN * 8 <= SZA, "stats scratch");
+  static_assert(4 * 16 * SP * 4 <= SZA, "epilogue staging");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
@@ -248,58 +263,54 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     }
   }
 
-  __bf16 ra[PA][8], rb[PB][8];
-  auto gload = [&](int k0) {
+  // Every thread loads its chunks unconditionally (threads past a tile's
+  // chunk count load a duplicate and skip the LDS store), so the load
+  // counters are static and the loads stay in flight across the MFMAs.
+  auto gload = [&](u32x4 (&ra)[PA], u32x4 (&rb)[PB], int k0) {
 #pragma unroll
     for (int c = 0; c < PA; ++c) {
-      const int e = tid + c * 256;
-      if (e < CHA) {
-        if (AK) {  // chunk = 8 k of one m
-          const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          if constexpr (GA != G_DENSE)
-            gatherA<GA>(ra[c], p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
-          else
-            ld8<TA>(ra[c], A, m0 + mr, k0 + kc, p.M, kend, p.lda);
-        } else {   // chunk = 8 m of one k
-          const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
-          ld8<TA>(ra[c], A, k0 + kr, m0 + mc, kend, p.M, p.lda);
-        }
+      const int e = min(tid + c * 256, CHA - 1);
+      if (AK) {  // chunk = 8 k of one m
+        const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+        if constexpr (GA != G_DENSE)
+          ra[c] = gatherA<GA>(p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
+        else
+          ra[c] = ld8<SAFE, TA>(A, m0 + mr, k0 + kc, p.M, kend, p.lda);
+      } else {   // chunk = 8 m of one k
+        const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
+        ra[c] = ld8<SAFE, TA>(A, k0 + kr, m0 + mc, kend, p.M, p.lda);
       }
     }
 #pragma unroll
     for (int c = 0; c < PB; ++c) {
-      const int e = tid + c * 256;
-      if (e < CHB) {
-        if (BK) {
-          const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          ld8<__bf16>(rb[c], p.B, n0 + nr, k0 + kc, p.N, kend, p.ldb);
-        } else {
-          const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
-          if constexpr (GB == GB_WGRAD)
-            gatherB_wgrad(rb[c], p, ctap[c], k0 + kr, kend);
-          else if constexpr (GB == GB_WDGRAD)
-            gatherB_wdgrad(rb[c], p, k0 + kr, n0 + nc, kend);
-          else
-            ld8<__bf16>(rb[c], p.B, k0 + kr, n0 + nc, kend, p.N, p.ldb);
-        }
+      const int e = min(tid + c * 256, CHB - 1);
+      if (BK) {
+        const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+        rb[c] = ld8<SAFE, __bf16>(p.B, n0 + nr, k0 + kc, p.N, kend, p.ldb);
+      } else {
+        const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
+        if constexpr (GB == GB_WGRAD)
+          rb[c] = gatherB_wgrad(p, ctap[c], k0 + kr, kend);
+        else if constexpr (GB == GB_WDGRAD)
+          rb[c] = gatherB_wdgrad(p, k0 + kr, n0 + nc, kend);
+        else
+          rb[c] = ld8<SAFE, __bf16>(p.B, k0 + kr, n0 + nc, kend, p.N, p.ldb);
       }
     }
   };
-  auto sstore = [&](int buf) {
+  // k-contiguous chunks go to LDS as one 16-byte store; the others are
+  // transposed into eight 2-byte stores.
+  auto sstore = [&](const u32x4 (&ra)[PA], const u32x4 (&rb)[PB], int buf) {
 #pragma unroll
     for (int c = 0; c < PA; ++c) {
       const int e = tid + c * 256;
       if (e < CHA) {
         if (AK) {
           const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          bf16x8 v;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = ra[c][u];
-          *reinterpret_cast<bf16x8 *>(&As[buf][mr][kc]) = v;
+          *reinterpret_cast<u32x4 *>(smA + ((buf * BM + mr) * KP + kc) * 2) = ra[c];
         } else {
           const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) As[buf][mc + u][kr] = ra[c][u];
+          *reinterpret_cast<u32x4 *>(smA + ((buf * KS + kr) * PA_K + mc) * 2) = ra[c];
         }
       }
     }
@@ -309,14 +320,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       if (e < CHB) {
         if (BK) {
           const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          bf16x8 v;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = rb[c][u];
-          *reinterpret_cast<bf16x8 *>(&Bs[buf][nr][kc]) = v;
+          *reinterpret_cast<u32x4 *>(smB + ((buf * BN + nr) * KP + kc) * 2) = rb[c];
         } else {
           const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) Bs[buf][nc + u][kr] = rb[c][u];
+          *reinterpret_cast<u32x4 *>(smB + ((buf * KS + kr) * PB_K + nc) * 2) = rb[c];
         }
       }
     }
@@ -328,28 +335,56 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = kend > kbeg ? (kend - kbeg + KS - 1) / KS : 0;
-  if (nk > 0) gload(kbeg);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    sstore(buf);
-    __syncthreads();
-    if (kt + 1 < nk) gload(kbeg + (kt + 1) * KS);
+  auto compute = [&](int buf) {
     bf16x8 av[TM], bv[TN];
 #pragma unroll
-    for (int a = 0; a < TM; ++a) av[a] = *reinterpret_cast<const bf16x8 *>(&As[buf][wm + a * 16 + i16][8 * q]);
+    for (int a = 0; a < TM; ++a) {
+      if constexpr (AK)
+        av[a] = *reinterpret_cast<const bf16x8 *>(smA + ((buf * BM + wm + a * 16 + i16) * KP + 8 * q) * 2);
+      else
+        av[a] = tr_operand(smA + ((buf * KS + 8 * q + (i16 >> 2)) * PA_K + wm + a * 16 + 4 * (i16 & 3)) * 2,
+                           4 * PA_K * 2);
+    }
 #pragma unroll
-    for (int b = 0; b < TN; ++b) bv[b] = *reinterpret_cast<const bf16x8 *>(&Bs[buf][wn + b * 16 + i16][8 * q]);
+    for (int b = 0; b < TN; ++b) {
+      if constexpr (BK)
+        bv[b] = *reinterpret_cast<const bf16x8 *>(smB + ((buf * BN + wn + b * 16 + i16) * KP + 8 * q) * 2);
+      else
+        bv[b] = tr_operand(smB + ((buf * KS + 8 * q + (i16 >> 2)) * PB_K + wn + b * 16 + 4 * (i16 & 3)) * 2,
+                           4 * PB_K * 2);
+    }
 #pragma unroll
     for (int a = 0; a < TM; ++a)
 #pragma unroll
       for (int b = 0; b < TN; ++b)
         acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+  };
+
+  // Two register stages: the loads of slice kt + 2 are issued right after
+  // slice kt is stored to LDS, so each load has two slices of MFMA work to
+  // arrive.  Slice kt is stored to LDS buffer kt & 1.
+  // Loads at or past kend return zeros without touching memory, so the loop
+  // runs an even number of slices with unconditional loads (a trailing
+  // all-zero slice adds exact zeros) and the load counters stay static.
+  const int nk = kend > kbeg ? (kend - kbeg + KS - 1) / KS : 0;
+  u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
+  gload(ra0, rb0, kbeg);
+  gload(ra1, rb1, kbeg + KS);
+  for (int kt = 0; kt < nk; kt += 2) {
+    sstore(ra0, rb0, 0);
+    __syncthreads();
+    gload(ra0, rb0, kbeg + (kt + 2) * KS);
+    compute(0);
+    sstore(ra1, rb1, 1);
+    __syncthreads();
+    gload(ra1, rb1, kbeg + (kt + 3) * KS);
+    compute(1);
   }
 
   if constexpr (EPI == GEMM_EPI_BF16STATS) {
-    // per column: sums over this wavefront's rows, then over the lane groups
-    // and the WM wavefronts sharing the column, in a fixed order
+    // per column: sums of the bf16-rounded values over this wavefront's rows,
+    // then over the lane groups and the WM wavefronts sharing the column, in
+    // a fixed order
     double s1[TN], s2[TN];
 #pragma unroll
     for (int b = 0; b < TN; ++b) s1[b] = s2[b] = 0.0;
@@ -360,16 +395,15 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = m0 + wm + a * 16 + 4 * q + r, n = n0 + wn + b * 16 + i16;
+          const float h = float((__bf16)acc[a][b][r]);
+          acc[a][b][r] = h;
           if (m < p.M && n < p.N) {
-            const __bf16 h = (__bf16)acc[a][b][r];
-            p.Cb[size_t(m) * p.ldc + n] = h;
-            const double v = double(float(h));
-            s1[b] += v;
-            s2[b] += v * v;
+            s1[b] += double(h);
+            s2[b] += double(h) * double(h);
           }
         }
     __syncthreads();
-    double *red = reinterpret_cast<double *>(&As[0][0][0]);  // [WM*4][2][BN]
+    double *red = reinterpret_cast<double *>(smA);  // [WM*4][2][BN]
     const int wr = wave / WN;
 #pragma unroll
     for (int b = 0; b < TN; ++b) {
@@ -384,69 +418,136 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       for (int k = 0; k < WM * 4; ++k) t += red[(k * 2 + which) * BN + col];
       if (n0 + col < p.N) p.stats[(size_t(blockIdx.y) * 2 + which) * p.N + n0 + col] = t;
     }
-  } else {
-    float *Cz = p.C + size_t(blockIdx.z) * p.M * p.ldc;
+  }
+
+  // Epilogue through LDS: each wavefront stages 16 rows x WC columns of its
+  // tile at a time, then writes whole rows with 16-byte stores (and reads D
+  // and the mask the same way).
+  float *stage = reinterpret_cast<float *>(smA) + wave * 16 * SP;
+  float *Cz = p.C + size_t(blockIdx.z) * p.M * p.ldc;
+  constexpr int VEC = EPI == GEMM_EPI_BF16STATS ? 8 : 4;  // output elements per lane
+  constexpr int LPR = WC / VEC;                           // lanes per row
+  constexpr int RPP = 64 / LPR;                           // rows per pass
+  static_assert(WC % VEC == 0 && 64 % LPR == 0 && 16 % RPP == 0, "epilogue layout");
+  const bool vec_ok = (p.ldc % VEC == 0) &&
+                      (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_BF16STATS || p.ldd % 4 == 0);
 #pragma unroll
-    for (int a = 0; a < TM; ++a)
+  for (int a = 0; a < TM; ++a) {
+    __syncthreads();
 #pragma unroll
-      for (int b = 0; b < TN; ++b)
+    for (int b = 0; b < TN; ++b)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m0 + wm + a * 16 + 4 * q + r, n = n0 + wn + b * 16 + i16;
-          if (m < p.M && n < p.N) {
-            float v = acc[a][b][r];
-            if (EPI == GEMM_EPI_ADD) {
-              v += p.D[size_t(m) * p.ldd + n];
-            } else if (EPI == GEMM_EPI_ADDMASK) {
-              const size_t o = size_t(m) * p.ldd + n;
-              if (float(p.Ym[o]) > 0.f) v += p.D[o];
-            } else if (p.bias) {
-              v += p.bias[n];
-            }
-            Cz[size_t(m) * p.ldc + n] = v;
-          }
+      for (int r = 0; r < 4; ++r) stage[(4 * q + r) * SP + b * 16 + i16] = acc[a][b][r];
+    __syncthreads();
+#pragma unroll
+    for (int pass = 0; pass < 16 / RPP; ++pass) {
+      const int rr = pass * RPP + lane / LPR, cc = (lane % LPR) * VEC;
+      const int m = m0 + wm + a * 16 + rr, n = n0 + wn + cc;
+      if (m >= p.M || n >= p.N) continue;
+      float v[VEC];
+#pragma unroll
+      for (int u = 0; u < VEC; ++u) v[u] = stage[rr * SP + cc + u];
+      const bool full = vec_ok && n + VEC <= p.N;
+      if constexpr (EPI == GEMM_EPI_BF16STATS) {
+        __bf16 *dst = p.Cb + size_t(m) * p.ldc + n;
+        if (full) {
+          bf16x8 h;
+#pragma unroll
+          for (int u = 0; u < 8; ++u) h[u] = (__bf16)v[u];
+          *reinterpret_cast<bf16x8 *>(dst) = h;
+        } else {
+          for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = (__bf16)v[u];
         }
+      } else {
+        if (EPI == GEMM_EPI_ADD || EPI == GEMM_EPI_ADDMASK) {
+          const size_t o = size_t(m) * p.ldd + n;
+          if (full) {
+            const float4 d = *reinterpret_cast<const float4 *>(p.D + o);
+            float dv[4] = {d.x, d.y, d.z, d.w};
+            if (EPI == GEMM_EPI_ADDMASK) {
+#pragma unroll
+              for (int u = 0; u < 4; ++u) dv[u] = float(p.Ym[o + u]) > 0.f ? dv[u] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] += dv[u];
+          } else {
+            for (int u = 0; u < VEC && n + u < p.N; ++u) {
+              float d = p.D[o + u];
+              if (EPI == GEMM_EPI_ADDMASK && !(float(p.Ym[o + u]) > 0.f)) d = 0.f;
+              v[u] += d;
+            }
+          }
+        } else if (p.bias) {
+          for (int u = 0; u < VEC && n + u < p.N; ++u) v[u] += p.bias[n + u];
+        }
+        float *dst = Cz + size_t(m) * p.ldc + n;
+        if (full)
+          *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        else
+          for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = v[u];
+      }
+    }
   }
 }
 
-// Tile by shape: 128x128 when that alone fills the GPU, else 64x64, else 64x32.
+// Tiles by shape: large tiles while they still give at least half the compute
+// units a workgroup (workgroups here are latency-bound, so fewer larger tiles
+// win), and a tile width that follows N.
 struct Tile {
   int BM, BN;
 };
 
+inline long tiles_for(int M, int N, int BM, int BN) {
+  return long((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+}
+
 inline Tile tile_of(int M, int N) {
-  const long big = long((M + 127) / 128) * ((N + 127) / 128);
-  if (M >= 256 && big >= 128) return {128, 128};
-  if (long((M + 63) / 64) * ((N + 63) / 64) >= 64) return {64, 64};
+  if (N <= 32) return {64, 32};
+  if (N <= 64) {
+    if (tiles_for(M, N, 256, 64) >= 256) return {256, 64};
+    if (tiles_for(M, N, 128, 64) >= 128) return {128, 64};
+    return {64, 64};
+  }
+  if (M >= 256 && tiles_for(M, N, 128, 128) >= 128) return {128, 128};
+  if (tiles_for(M, N, 64, 64) >= 64) return {64, 64};
   return {64, 32};
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB>
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
 void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
   dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
   if (epi == GEMM_EPI_ADD) {
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
     return;
   }
   if constexpr (std::is_same<TA, __bf16>::value) {
     if (epi == GEMM_EPI_ADDMASK) {
-      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
       return;
     }
     if (epi == GEMM_EPI_BF16STATS) {
-      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
       return;
     }
   }
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
 }
 
-template <bool AK, bool BK, typename TA, int GA, int GB>
+template <bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
 void pick_tile(const Args &a, int epi, int splits, hipStream_t s) {
   const Tile t = tile_of(a.M, a.N);
-  if (t.BM == 128) launch_epi<128, 128, 2, 2, AK, BK, TA, GA, GB>(a, epi, splits, s);
-  else if (t.BN == 64) launch_epi<64, 64, 2, 2, AK, BK, TA, GA, GB>(a, epi, splits, s);
-  else launch_epi<64, 32, 4, 1, AK, BK, TA, GA, GB>(a, epi, splits, s);
+  if (t.BM == 256) launch_epi<256, 64, 4, 1, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+  else if (t.BM == 128 && t.BN == 128) launch_epi<128, 128, 2, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+  else if (t.BM == 128) launch_epi<128, 64, 2, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+  else if (t.BN == 64) launch_epi<64, 64, 2, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+  else launch_epi<64, 32, 4, 1, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+}
+
+// Every dense chunk is wholly inside or outside its operand when the
+// contiguous extent and the leading dimension are multiples of 8.
+inline bool safe8(const Args &a, bool ak, bool bk) {
+  const int acols = ak ? a.K : a.M, bcols = bk ? a.K : a.N;
+  return acols % 8 == 0 && a.lda % 8 == 0 && bcols % 8 == 0 && a.ldb % 8 == 0;
 }
 
 }  // namespace gb

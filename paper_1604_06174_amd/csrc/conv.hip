@@ -436,19 +436,21 @@ bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool 
 bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
   constexpr int F = CONV_FWD, D = CONV_DGRAD;
   constexpr int STATS = CONV_EPI_STATS, MASK = CONV_EPI_MASK, SC1 = CONV_EPI_SC1, SC2 = CONV_EPI_SC2;
-  return spec_try<16, 16, 32, 1, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
-         spec_try<16, 32, 16, 2, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<32, 32, 16, 1, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<32, 64, 8, 2, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<64, 64, 8, 1, F, STATS, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<16, 16, 32, 1, D, MASK, 8, 16>(a, mode, s, epi, st, launch, u) ||
-         spec_try<32, 32, 16, 1, D, MASK, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<64, 64, 8, 1, D, MASK, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<16, 16, 32, 1, D, SC1, 8, 16>(a, mode, s, epi, st, launch, u) ||
-         spec_try<32, 32, 16, 1, D, SC1, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<64, 64, 8, 1, D, SC1, 8, 32>(a, mode, s, epi, st, launch, u) ||
-         spec_try<32, 16, 32, 2, D, SC2, 8, 16>(a, mode, s, epi, st, launch, u) ||
-         spec_try<64, 32, 16, 2, D, SC2, 8, 16>(a, mode, s, epi, st, launch, u);
+  // rows per workgroup and output channels per workgroup as measured best on
+  // MI355X for these shapes
+  return spec_try<16, 16, 32, 1, F, STATS, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 32, 16, 2, F, STATS, 4, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 64, 8, 2, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, D, MASK, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, D, MASK, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, D, MASK, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, D, SC1, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, D, SC1, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, D, SC1, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 16, 32, 2, D, SC2, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 32, 16, 2, D, SC2, 4, 16>(a, mode, s, epi, st, launch, u);
 }
 
 // ---------------------------------------------------------------- wgrad --

@@ -129,6 +129,9 @@ def main():
     ap.add_argument("--workload", default="cifar110")
     ap.add_argument("--plan", default=None, choices=["sqrt", "greedy", "recursive", "search"],
                     help="override the workload's plan (search: the appendix-A budget search)")
+    ap.add_argument("--drop-bn-relu", action="store_true",
+                    help="CIFAR-shaped net: keep only convolution outputs and re-form batch norm + "
+                         "ReLU from them when read")
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="batch (LSTM: time steps) of the CPU oracle sample; 0 skips it, -1 picks "
                          "about 10-30 s of oracle work for the workload")
@@ -147,6 +150,11 @@ def main():
     from paper_1604_06174_amd.workload import GpuStep
 
     cfg = dict(synth.WORKLOADS[args.workload])
+    if args.drop_bn_relu:
+        if cfg["kind"] != "resnet_basic":
+            print(json.dumps({"error": "--drop-bn-relu applies to the CIFAR-shaped network"}))
+            sys.exit(2)
+        cfg["drop_bn_relu"] = 1
     d = synth.make(cfg)
     step = GpuStep(cfg, d["params"], d["input"], d["target"])
     if args.plan:
@@ -232,7 +240,8 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": args.workload, "kind": cfg["kind"], "batch": batch,
+        "config": {"workload": args.workload + ("+drop_bn_relu" if args.drop_bn_relu else ""),
+                   "kind": cfg["kind"], "batch": batch,
                    "units": step.net.n, "plan": mode_name,
                    "stride_or_budget": budget, "cuts": len(plan.cuts())},
         "peak_activation_gb": round(acc["peak"] / 1e9, 6),

@@ -154,7 +154,10 @@ typedef struct ckpt_net_desc {
   int32_t stage_blocks[4]; /* RESNET_BOTTLENECK: blocks per stage (zero past depth) */
   int32_t expansion;     /* RESNET_BOTTLENECK: output channels / bottleneck width  */
   int32_t stem_channels; /* RESNET_BOTTLENECK: channels of the stem's output       */
-  int32_t reserved[3];   /* must be zero                                           */
+  int32_t drop_bn_relu;  /* RESNET_BASIC: 1 = keep only convolution outputs and
+                            re-form relu(bn(.)) from them and their statistics
+                            when read (smaller saved internals, same gradients)  */
+  int32_t reserved[2];   /* must be zero                                           */
 } ckpt_net_desc;
 
 /*

@@ -19,7 +19,9 @@ Unit kinds (fp32 unless stated):
   q = one [N,S,S,C] tensor.
 * basic block (Cin -> Cout, output side S): a = conv1 output, relu(bn1)
   output, conv2 output (3 x 4NSSCout) + two BN mean/rstd pairs (2 x 8Cout);
-  q = two [N,S,S,Cout] tensors.
+  q = two [N,S,S,Cout] tensors.  With the "drop bn-relu" layout (section
+  4.2: keep the convolution outputs, recompute batch norm + ReLU) the relu(bn1)
+  output is not kept: a = 2 x 4NSSCout + 2 x 8Cout.
 * LSTM step (batch B, hidden H, vocabulary V; bf16 GEMM operands): b = h
   (bf16, 2BH) + c (fp32, 4BH); a = activated gates i,f,g,o (fp32, 16BH) +
   the softmax gradient of its head (fp32, 4BV); q = the total hidden-state
@@ -79,7 +81,7 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
                 a.append(t + st)
                 q.append(t)
             else:
-                a.append(3 * t + 2 * st)
+                a.append((2 if cfg.get("drop_bn_relu") else 3) * t + 2 * st)
                 q.append(2 * t)
             b.append(t)
         return b, a, q

@@ -51,7 +51,7 @@ class NetDesc(C.Structure):
                 ("width", C.c_int32), ("image", C.c_int32), ("n_classes", C.c_int32),
                 ("grad_chunk", C.c_int32), ("stage_blocks", C.c_int32 * 4),
                 ("expansion", C.c_int32), ("stem_channels", C.c_int32),
-                ("reserved", C.c_int32 * 3)]
+                ("drop_bn_relu", C.c_int32), ("reserved", C.c_int32 * 2)]
 
 
 class Batch(C.Structure):
@@ -189,12 +189,12 @@ class Net:
 
     def __init__(self, kind: int, batch: int, depth: int, width: int, image: int = 0,
                  n_classes: int = 0, grad_chunk: int = 0, stage_blocks: Sequence[int] = (),
-                 expansion: int = 0, stem_channels: int = 0):
+                 expansion: int = 0, stem_channels: int = 0, drop_bn_relu: int = 0):
         sb = list(stage_blocks) + [0] * (4 - len(stage_blocks))
         if len(sb) != 4:
             raise CkptError(E_INVALID, "stage_blocks: at most 4 stages")
         d = NetDesc(kind, batch, depth, width, image, n_classes, grad_chunk,
-                    (C.c_int32 * 4)(*sb), expansion, stem_channels)
+                    (C.c_int32 * 4)(*sb), expansion, stem_channels, drop_bn_relu)
         h = C.c_void_p()
         _check(_lib.net_create(C.byref(d), C.byref(h)))
         self._h = h
@@ -294,9 +294,9 @@ def plan_search(layer_bytes: Sequence[int], cut_bytes: Sequence[int], b: Sequenc
 
 def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,
                n_classes: int = 0, grad_chunk: int = 0, stage_blocks: Sequence[int] = (),
-               expansion: int = 0, stem_channels: int = 0) -> Net:
+               expansion: int = 0, stem_channels: int = 0, drop_bn_relu: int = 0) -> Net:
     return Net(kind, batch, depth, width, image, n_classes, grad_chunk, stage_blocks, expansion,
-               stem_channels)
+               stem_channels, drop_bn_relu)
 
 
 def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,

@@ -138,7 +138,7 @@ __global__ __launch_bounds__(256) void k_bn_apply(int64_t P, int J, const float 
     float cv[4] = {c.x, c.y, c.z, c.w}, o[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      o[k] = gamma[c0 + k] * ((cv[k] - st[c0 + k]) * st[J + c0 + k]) + beta[c0 + k];
+      o[k] = __builtin_fmaf(gamma[c0 + k], (cv[k] - st[c0 + k]) * st[J + c0 + k], beta[c0 + k]);
     if (RES == BN_RES_ID) {
       const float4 x = *reinterpret_cast<const float4 *>(X + p * J + c0);
       o[0] += x.x; o[1] += x.y; o[2] += x.z; o[3] += x.w;

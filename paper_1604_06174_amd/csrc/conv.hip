@@ -42,7 +42,18 @@ struct ConvArgs {
   const float *E0, *E1;  // epilogue operands (MASK: E0; SC: E0 = g, E1 = y)
   int Eh, Ew, Ec;        // SC2: dims of g and y
   double *stats;         // STATS: [gridDim.x][2][J]
+  const float *tst, *tg, *tb;  // optional bn_relu: FWD input / DGRAD MASK transform
 };
+
+// bn_relu of four consecutive channels c..c+3 (C = channel count of the
+// statistics: st = mean[C] | rstd[C])
+__device__ __forceinline__ float4 bn_relu4(float4 v, const float *st, const float *g, const float *b,
+                                           int c, int C) {
+  return make_float4(bn_relu(v.x, st[c], st[C + c], g[c], b[c]),
+                     bn_relu(v.y, st[c + 1], st[C + c + 1], g[c + 1], b[c + 1]),
+                     bn_relu(v.z, st[c + 2], st[C + c + 2], g[c + 2], b[c + 2]),
+                     bn_relu(v.w, st[c + 3], st[C + c + 3], g[c + 3], b[c + 3]));
+}
 
 __device__ __forceinline__ int cpad4(int c) { return (c + 3) & ~3; }
 
@@ -91,6 +102,12 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
         } else {
 #pragma unroll
           for (int k = 0; k < 4; ++k) v[k] = (c4 + k < a.C) ? src[k] : 0.f;
+        }
+        if (MODE == CONV_FWD && a.tst) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (c4 + k < a.C)
+              v[k] = bn_relu(v[k], a.tst[c4 + k], a.tst[a.C + c4 + k], a.tg[c4 + k], a.tb[c4 + k]);
         }
       }
       *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = make_float4(v[0], v[1], v[2], v[3]);
@@ -191,7 +208,8 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
           s1[t] += double(v);
           s2[t] += double(v) * double(v);
         } else if (EPI == CONV_EPI_MASK) {
-          v = a.E0[o] > 0.f ? v : 0.f;
+          const float e = a.tst ? bn_relu(a.E0[o], a.tst[j], a.tst[a.J + j], a.tg[j], a.tb[j]) : a.E0[o];
+          v = e > 0.f ? v : 0.f;
         } else if (EPI == CONV_EPI_SC1) {
           v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
         } else if (EPI == CONV_EPI_SC2) {
@@ -267,7 +285,10 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
       ok = ur >= 0 && uc >= 0 && (ur % S) == 0 && (uc % S) == 0 && ir < Hx && ic < WX;
     }
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (ok) v = *reinterpret_cast<const float4 *>(a.X + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4);
+    if (ok) {
+      v = *reinterpret_cast<const float4 *>(a.X + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4);
+      if (MODE == CONV_FWD && a.tst) v = bn_relu4(v, a.tst, a.tg, a.tb, 4 * c4, C);
+    }
     *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + 4 * c4) = v;
   }
 
@@ -372,7 +393,8 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
           s1[t] += double(v);
           s2[t] += double(v) * double(v);
         } else if (EPI == CONV_EPI_MASK) {
-          v = a.E0[o] > 0.f ? v : 0.f;
+          const float e = a.tst ? bn_relu(a.E0[o], a.tst[j], a.tst[a.J + j], a.tg[j], a.tb[j]) : a.E0[o];
+          v = e > 0.f ? v : 0.f;
         } else if (EPI == CONV_EPI_SC1) {
           v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
         } else if (EPI == CONV_EPI_SC2) {
@@ -471,6 +493,7 @@ struct WgArgs {
   float *part;      // [gridDim.x][J][9C]
   int N, H, W, Hx, Wx, C, J, S;
   int pix_per_blk;  // multiple of WG_KC
+  const float *tst, *tg, *tb;  // optional bn_relu of the input X
 };
 
 __device__ __forceinline__ int wg_as(int J) { return J + ((16 - J % 32) + 32) % 32; }  // == 16 mod 32
@@ -531,8 +554,10 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
           if ((C & 3) == 0) {  // the 4 columns are 4 channels of one tap
             const int tap = nn / C, c = nn % C;
             const int ih = oh * SS + tap / 3 - 1, iw = ow * SS + tap % 3 - 1;
-            if (ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
+            if (ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx) {
               v = *reinterpret_cast<const float4 *>(a.X + ((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c);
+              if (a.tst) v = bn_relu4(v, a.tst, a.tg, a.tb, c, C);
+            }
           } else {
             float vv[4];
 #pragma unroll
@@ -540,9 +565,9 @@ __global__ __launch_bounds__(256) void k_conv3x3_wgrad(WgArgs a) {
               const int n = nn + u;
               const int tap = n / C, c = n % C;
               const int ih = oh * SS + tap / 3 - 1, iw = ow * SS + tap % 3 - 1;
-              vv[u] = (n < NC && ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx)
-                          ? a.X[((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c]
-                          : 0.f;
+              const bool in = n < NC && ih >= 0 && ih < a.Hx && iw >= 0 && iw < a.Wx;
+              vv[u] = in ? a.X[((size_t(img) * a.Hx + ih) * a.Wx + iw) * C + c] : 0.f;
+              if (in && a.tst) vv[u] = bn_relu(vv[u], a.tst[c], a.tst[C + c], a.tg[c], a.tb[c]);
             }
             v = make_float4(vv[0], vv[1], vv[2], vv[3]);
           }
@@ -691,10 +716,14 @@ __global__ __launch_bounds__(256) void k_wgrad_s(WgArgs a) {
         const float *src = a.X + ((size_t(img) * a.Hx + ir) * WX + ic) * C + c4;
         if constexpr (C % 4 == 0) {
           v = *reinterpret_cast<const float4 *>(src);
+          if (a.tst) v = bn_relu4(v, a.tst, a.tg, a.tb, c4, C);
         } else {
           float vv[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) vv[u] = (c4 + u < C) ? src[u] : 0.f;
+          for (int u = 0; u < 4; ++u) {
+            vv[u] = (c4 + u < C) ? src[u] : 0.f;
+            if (c4 + u < C && a.tst) vv[u] = bn_relu(vv[u], a.tst[c4 + u], a.tst[C + c4 + u], a.tg[c4 + u], a.tb[c4 + u]);
+          }
           v = make_float4(vv[0], vv[1], vv[2], vv[3]);
         }
       }
@@ -944,10 +973,11 @@ bool conv3x3_supported(int mode, int S, int H, int W, int C, int J) {
 
 void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
              int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1,
-             int Eh, int Ew, int Ec, double *stats) {
+             int Eh, int Ew, int Ec, double *stats, const float *tst, const float *tg,
+             const float *tb) {
   Tile t = conv_tile(mode, S, H, W, C, J);
   const int NSUB = J > 16 ? 2 : 1;
-  ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats};
+  ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats, tst, tg, tb};
   if (spec_dispatch(a, mode, S, epi, st, true, nullptr)) return;
   dim3 grid(N * t.rblk, (J + 16 * NSUB - 1) / (16 * NSUB));
   const size_t lds = conv_lds(mode, S, t.R, W, C, J);
@@ -961,12 +991,13 @@ void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const flo
 }
 
 void conv3x3_wgrad(hipStream_t st, int S, const float *X, const float *DY, float *part, float *dW,
-                   int N, int H, int W, int Hx, int Wx, int C, int J) {
+                   int N, int H, int W, int Hx, int Wx, int C, int J, const float *tst,
+                   const float *tg, const float *tb) {
   const int64_t P = int64_t(N) * H * W;
   const int NC = 9 * C;
   const int ppb = wgrad_pix(P, NC);
   const int nbx = int((P + ppb - 1) / ppb);
-  WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, S, ppb};
+  WgArgs a{X, DY, part, N, H, W, Hx, Wx, C, J, S, ppb, tst, tg, tb};
   {
     WgUse u;
     if (wgs_dispatch(a, st, true, &u)) {

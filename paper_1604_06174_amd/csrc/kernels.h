@@ -7,6 +7,14 @@
 
 namespace ckpt {
 
+// relu(gamma (x - mean) rstd + beta) with one explicit rounding sequence, so
+// that every kernel that forms a batch-norm + ReLU output (the apply kernel,
+// and the convolutions that form it on the fly from the convolution output
+// and its statistics) produces the same bits.
+__device__ __forceinline__ float bn_relu(float x, float mean, float rstd, float g, float b) {
+  return fmaxf(__builtin_fmaf(g, (x - mean) * rstd, b), 0.f);
+}
+
 enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4 };
 
 // C = epilogue(op(A) op(B)); see gemm_f32.hip for the operand conventions.
@@ -34,17 +42,23 @@ enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 =
 // stride-S forward conv, X = dy).  Epilogue operands: MASK E0 = mask tensor
 // shaped like Y; SC1 E0 = g, E1 = y shaped like Y; SC2 E0 = g, E1 = y of dims
 // [N, Eh, Ew, Ec].  STATS writes [blocks][2][J] float64 channel sums.
+// Optional batch-norm + ReLU transform (tst = mean | rstd, tg = gamma,
+// tb = beta): FWD applies bn_relu to every in-image input value (channel c);
+// DGRAD with MASK takes the mask as bn_relu(E0) (channel j) instead of E0.
 void conv3x3(hipStream_t s, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
              int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0 = nullptr,
              const float *E1 = nullptr, int Eh = 0, int Ew = 0, int Ec = 0,
-             double *stats = nullptr);
+             double *stats = nullptr, const float *tst = nullptr, const float *tg = nullptr,
+             const float *tb = nullptr);
 int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J);
 int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J);
 bool conv3x3_supported(int mode, int S, int H, int W, int C, int J);
 // dW[J,3,3,C] of a stride-S forward conv with input X[N,Hx,Wx,C] and output
 // gradient DY[N,H,W,J]; part holds conv3x3_wgrad_blocks * J*9*C floats.
+// Optional input transform bn_relu (tst, tg, tb) as for the forward.
 void conv3x3_wgrad(hipStream_t s, int S, const float *X, const float *DY, float *part, float *dW,
-                   int N, int H, int W, int Hx, int Wx, int C, int J);
+                   int N, int H, int W, int Hx, int Wx, int C, int J, const float *tst = nullptr,
+                   const float *tg = nullptr, const float *tb = nullptr);
 
 // ---- batch norm and the classifier head (bn.hip) ----
 enum { BN_RES_NONE = 0, BN_RES_ID = 1, BN_RES_A = 2 };

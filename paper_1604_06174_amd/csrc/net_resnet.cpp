@@ -12,6 +12,12 @@
 // mean/rstd pair of Cout floats each, both rounded up to 256 bytes):
 //   stem   a = c | st            q = dc
 //   block  a = c1 | r1 | c2 | st1 | st2     q = two T buffers
+// With drop_bn_relu the blocks keep only the convolution outputs, a = c1 | c2
+// | st1 | st2, and r1 = relu(bn1(c1)) is formed on the fly from c1 and its
+// statistics wherever it is read (the second convolution's input, its data
+// gradient's ReLU mask and its weight gradient's input): the "drop bn-relu"
+// memory plan the paper applies to the conv-BN-activation pipeline
+// (section 4.2), with the same bits as the stored r1.
 // The boundary b_i is the unit's input tensor (b_0 = the image batch).
 #include <algorithm>
 
@@ -29,6 +35,7 @@ struct Blk {
 class ResNetBasic : public Net {
  public:
   int N, S, C0, K, nb;
+  bool drop;  // r1 recomputed from c1 instead of kept
   std::vector<Blk> u;
   int hw, hb;  // head parameter indices
   // operator workspace offsets (bytes)
@@ -42,6 +49,7 @@ class ResNetBasic : public Net {
     C0 = d.width;
     K = d.n_classes;
     nb = d.depth;
+    drop = d.drop_bn_relu != 0;
     auto T = [&](int h, int c) { return align256(uint64_t(N) * h * h * c * 4); };
     b.push_back(align256(uint64_t(N) * S * S * 3 * 4));
     {
@@ -70,7 +78,7 @@ class ResNetBasic : public Net {
         k.b2 = add_param(p + "beta2", cout);
         u.push_back(k);
         const uint64_t t = T(k.hout, cout);
-        a.push_back(3 * t + 2 * align256(8ull * cout));
+        a.push_back((drop ? 2 : 3) * t + 2 * align256(8ull * cout));
         q.push_back(2 * t);
         b.push_back(t);
         cin = cout;
@@ -117,20 +125,38 @@ class ResNetBasic : public Net {
 
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
 
+  // a block's saved tensors: c1 | [r1] | c2 | st1 | st2
+  struct Saved {
+    float *c1, *r1, *c2, *st1, *st2;
+  };
+  Saved saved_of(const Blk &k, char *sv) const {
+    const uint64_t t = align256(uint64_t(N) * k.hout * k.hout * k.cout * 4);
+    const uint64_t sb = align256(8ull * k.cout);
+    const int nt = drop ? 2 : 3;
+    Saved s;
+    s.c1 = reinterpret_cast<float *>(sv);
+    s.r1 = drop ? nullptr : reinterpret_cast<float *>(sv + t);
+    s.c2 = reinterpret_cast<float *>(sv + (nt - 1) * t);
+    s.st1 = reinterpret_cast<float *>(sv + nt * t);
+    s.st2 = reinterpret_cast<float *>(sv + nt * t + sb);
+    return s;
+  }
+
   // conv3x3 launch bracketed by the kernel timer.  Algorithmic work of a 3x3
   // convolution with output [N, ho, ho, cout] and input channels cin (the same
   // for its forward and its data gradient): 2 * N*ho*ho * cout * 9*cin flops;
   // bytes = kernel input + weights + kernel output + epilogue tensors read.
   void conv(StepCtx &c, int mode, int s, int epi, const float *X, const float *Wt, float *Y, int H,
             int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1, int Eh, int Ew,
-            int Ec, int ho, int cin, int cout) {
+            int Ec, int ho, int cin, int cout, const float *tst = nullptr, const float *tg = nullptr,
+            const float *tb = nullptr) {
     const double fl = 2.0 * N * ho * ho * double(cout) * 9.0 * cin;
     double by = 4.0 * (double(N) * Hx * Wx * C + 9.0 * cin * cout + double(N) * H * W * J);
     if (epi == CONV_EPI_MASK) by += 4.0 * N * H * W * J;
     if (epi == CONV_EPI_SC1 || epi == CONV_EPI_SC2) by += 2 * 4.0 * N * Eh * Ew * std::min(Ec, J);
     timer.begin(c.s);
     conv3x3(c.s, mode, s, epi, X, Wt, Y, N, H, W, Hx, Wx, C, J, E0, E1, Eh, Ew, Ec,
-            epi == CONV_EPI_STATS ? bnpart(c) : nullptr);
+            epi == CONV_EPI_STATS ? bnpart(c) : nullptr, tst, tg, tb);
     timer.end(c.s, fl, by);
   }
   float *ksf(StepCtx &c, uint64_t off) const { return reinterpret_cast<float *>(c.ks + off); }
@@ -152,20 +178,22 @@ class ResNetBasic : public Net {
       c.launches += 3;
       return;
     }
-    float *c1 = reinterpret_cast<float *>(sv);
-    float *r1 = reinterpret_cast<float *>(sv + t);
-    float *c2 = reinterpret_cast<float *>(sv + 2 * t);
-    const uint64_t sb = align256(8ull * k.cout);
-    float *st1 = reinterpret_cast<float *>(sv + 3 * t);
-    float *st2 = reinterpret_cast<float *>(sv + 3 * t + sb);
+    const Saved sp = saved_of(k, sv);
+    float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2, *st1 = sp.st1, *st2 = sp.st2;
     const int ho = k.hout;
     conv(c, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin,
          k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
                     k.cout, np, st1);
-    bn_apply(c.s, BN_RES_NONE, np, k.cout, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, r1);
-    conv(c, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
-         nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout);
+    if (drop) {  // the second convolution forms relu(bn1(c1)) on its input
+      conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
+           nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1));
+      c.launches -= 1;
+    } else {
+      bn_apply(c.s, BN_RES_NONE, np, k.cout, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, r1);
+      conv(c, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
+           nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout);
+    }
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
                     np, st2);
     bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),
@@ -193,21 +221,22 @@ class ResNetBasic : public Net {
       c.launches += 5;
       return;
     }
-    const float *c1 = reinterpret_cast<const float *>(sv);
-    const float *r1 = reinterpret_cast<const float *>(sv + t);
-    const float *c2 = reinterpret_cast<const float *>(sv + 2 * t);
-    const uint64_t sb = align256(8ull * k.cout);
-    const float *st1 = reinterpret_cast<const float *>(sv + 3 * t);
-    const float *st2 = reinterpret_cast<const float *>(sv + 3 * t + sb);
+    const Saved sp = saved_of(k, const_cast<char *>(sv));
+    const float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2, *st1 = sp.st1, *st2 = sp.st2;
+    // r1 as read by the second convolution's backward: stored, or c1 with its
+    // batch-norm + ReLU transform
+    const float *x2 = drop ? c1 : r1;
+    const float *tst = drop ? st1 : nullptr, *tg = drop ? P(c, k.g1) : nullptr,
+                *tb = drop ? P(c, k.b1) : nullptr;
     float *Pb = static_cast<float *>(qv);
     float *Qb = reinterpret_cast<float *>(static_cast<char *>(qv) + t);
     const int ho = k.hout;
     // second BN (its input gradient is g masked by the block's final ReLU)
     bn_backward(c.s, np, k.cout, g, y, c2, st2, P(c, k.g2), bnpart(c), sums, G(c, k.g2), G(c, k.b2), Qb);
     // conv2: data gradient masked by the first ReLU, and weight gradient
-    conv(c, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, ho, ho, ho, ho, k.cout, k.cout, r1,
-         nullptr, 0, 0, 0, ho, k.cout, k.cout);
-    conv3x3_wgrad(c.s, 1, r1, Qb, wpart, G(c, k.w2), N, ho, ho, ho, ho, k.cout, k.cout);
+    conv(c, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, ho, ho, ho, ho, k.cout, k.cout, x2,
+         nullptr, 0, 0, 0, ho, k.cout, k.cout, tst, tg, tb);
+    conv3x3_wgrad(c.s, 1, x2, Qb, wpart, G(c, k.w2), N, ho, ho, ho, ho, k.cout, k.cout, tst, tg, tb);
     // first BN
     bn_backward(c.s, np, k.cout, Pb, nullptr, c1, st1, P(c, k.g1), bnpart(c), sums, G(c, k.g1),
                 G(c, k.b1), Qb);

@@ -22,7 +22,8 @@ def net_for(cfg: Dict) -> K.Net:
         return K.net_create(K.NET_MLP, cfg["batch"], cfg["depth"], cfg["width"])
     if kind == "resnet_basic":
         return K.net_create(K.NET_RESNET_BASIC, cfg["batch"], cfg["blocks_per_stage"],
-                            cfg.get("base", 16), cfg.get("image", 32), cfg.get("classes", 10))
+                            cfg.get("base", 16), cfg.get("image", 32), cfg.get("classes", 10),
+                            drop_bn_relu=int(bool(cfg.get("drop_bn_relu", 0))))
     if kind == "lstm":
         return K.net_create(K.NET_LSTM, cfg["batch"], cfg["T"], cfg["hidden"], cfg["input"],
                             cfg["vocab"], cfg.get("grad_chunk", 0))

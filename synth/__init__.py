@@ -94,7 +94,8 @@ def mlp_structure(depth: int, width: int, batch: int) -> Structure:
 
 
 def resnet_basic_structure(blocks_per_stage: int, base: int, batch: int,
-                           image: int = 32, classes: int = 10) -> Structure:
+                           image: int = 32, classes: int = 10,
+                           drop_bn_relu: bool = False) -> Structure:
     units = [Unit("stem3", cin=3, cout=base, stride=1, hin=image, hout=image,
                   params=[("u0.W", (base, 3, 3, 3), "he"),
                           ("u0.gamma", (base,), "one"), ("u0.beta", (base,), "zero")])]
@@ -115,7 +116,8 @@ def resnet_basic_structure(blocks_per_stage: int, base: int, batch: int,
             cin, side = cout, hout
     head = [("head.W", (cin, classes), "fc_w"), ("head.b", (classes,), "fc_b")]
     return Structure("resnet_basic", dict(blocks_per_stage=blocks_per_stage, base=base,
-                                          batch=batch, image=image, classes=classes),
+                                          batch=batch, image=image, classes=classes,
+                                          drop_bn_relu=bool(drop_bn_relu)),
                      units, head, (batch, image, image, 3), (batch,), "labels", classes)
 
 
@@ -173,7 +175,8 @@ def structure(cfg: Dict) -> Structure:
         return mlp_structure(cfg["depth"], cfg["width"], cfg["batch"])
     if k == "resnet_basic":
         return resnet_basic_structure(cfg["blocks_per_stage"], cfg.get("base", 16), cfg["batch"],
-                                      cfg.get("image", 32), cfg.get("classes", 10))
+                                      cfg.get("image", 32), cfg.get("classes", 10),
+                                      cfg.get("drop_bn_relu", False))
     if k == "resnet_bottleneck":
         return resnet_bottleneck_structure(tuple(cfg["stage_blocks"]), cfg["batch"],
                                            cfg.get("image", 224), cfg.get("classes", 1000),

@@ -97,6 +97,8 @@ WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
                  dict(kind="resnet_basic", blocks_per_stage=18, base=16, batch=128, image=32,
                       classes=10),
                  dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=3, image=12, classes=5),
+                 dict(kind="resnet_basic", blocks_per_stage=18, base=16, batch=128, image=32,
+                      classes=10, drop_bn_relu=1),
                  dict(kind="lstm", T=4096, batch=64, input=1024, hidden=1024, vocab=10000),
                  dict(kind="lstm", T=16384, batch=64, input=1024, hidden=1024, vocab=10000),
                  dict(kind="lstm", T=13, batch=3, input=16, hidden=24, vocab=40, grad_chunk=4),
@@ -155,6 +157,9 @@ def test_net_create_errors():
     # fields of another kind
     with pytest.raises(K.CkptError) as ei:
         K.net_create(K.NET_MLP, 2, 4, 8, stage_blocks=(1,))
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError) as ei:  # drop bn-relu is a RESNET_BASIC layout
+        K.net_create(K.NET_MLP, 2, 4, 8, drop_bn_relu=1)
     assert ei.value.code == K.E_INVALID
     B = K.NET_RESNET_BOTTLENECK
     # stage_blocks past depth, non-positive stage, channel counts, odd stride-2 side

@@ -187,3 +187,26 @@ def test_resnet1000_greedy_full_size_identity():
     W = g["head.W"].astype(np.float64).reshape(-1, K)
     assert np.all(np.abs(W.sum(axis=1)) <= 1e-5 * np.abs(W).sum(axis=1) + 1e-9)
 
+
+def test_cifar110_drop_bn_relu_full_size_same_bits():
+    """The full CIFAR-shaped net with the drop bn-relu layout: the sqrt plan
+    gives the stored layout's loss and gradient bytes, with the oracle's
+    smaller peak."""
+    import torch
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = synth.WORKLOADS["cifar110"]
+    print("[full size] cifar110 drop bn-relu", flush=True)
+    d = synth.make(cfg)
+    keep = GpuStep(cfg, d["params"], d["input"], d["target"])
+    cfg_d = dict(cfg, drop_bn_relu=1)
+    drop = GpuStep(cfg_d, d["params"], d["input"], d["target"])
+    st = synth.structure(cfg_d)
+    b, a, q = SZ.tables(st)
+    lb, cb = SZ.layer_and_cut_bytes(st)
+    l0, _, _ = keep.run(keep.plan(PL.SQRT, 0))
+    l1, peak, _ = drop.run(drop.plan(PL.SQRT, 0))
+    torch.cuda.synchronize()
+    assert peak == PL.account(PL.plan(st.n, lb, cb, 0, PL.SQRT), b, a, q).peak
+    assert l1 == l0
+    assert drop.grads_bytes() == keep.grads_bytes()
+

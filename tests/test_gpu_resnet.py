@@ -75,3 +75,30 @@ def test_resnet_step_parity_all_modes(case):
         if ref is None:
             ref = gb
         assert gb == ref, f"{name}: gradients differ from the no-checkpoint run"
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_drop_bn_relu_same_bits(case):
+    """The drop bn-relu layout (convolution outputs kept, relu(bn1) formed on
+    the fly from them) gives the stored layout's loss and gradient bytes for
+    every plan, with the oracle's smaller peak."""
+    import torch
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = dict(CASES[case])
+    print(f"[drop bn-relu] case={case}", flush=True)
+    d = synth.make(cfg)
+    keep = GpuStep(cfg, d["params"], d["input"], d["target"])
+    cfg_d = dict(cfg, drop_bn_relu=1)
+    drop = GpuStep(cfg_d, d["params"], d["input"], d["target"])
+    st = synth.structure(cfg_d)
+    b, a, q = SZ.tables(st)
+    lb, cb = SZ.layer_and_cut_bytes(st)
+    n = st.n
+    for mode, budget in ((PL.NONE, 0), (PL.SQRT, 0), (PL.GREEDY, sum(lb) // 3), (PL.RECURSIVE, 0)):
+        l0, _, _ = keep.run(keep.plan(mode, budget))
+        l1, peak, stats = drop.run(drop.plan(mode, budget))
+        torch.cuda.synchronize()
+        op = PL.plan(n, lb, cb, budget, mode)
+        assert peak == PL.account(op, b, a, q).peak, mode
+        assert l1 == l0, mode
+        assert drop.grads_bytes() == keep.grads_bytes(), mode

@@ -164,14 +164,21 @@ void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void 
 // ---- LSTM step kernels (lstm.hip) ----
 void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst);  // dst[c][r]
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst);
-void lstm_fwd_point(hipStream_t s, int B, int H, const float *z, const float *c_prev, float *gates,
-                    void *h_out, float *c_out);
-void softmax_ce_rows(hipStream_t s, int rows, int V, const float *logits, const int *labels,
-                     float scale, float *dlog, float *loss_rows);
+// Split-K inputs: zpart / lpart / dhpart hold ns partial slices of the
+// product, added in slice order before the bias (or the incoming dh), exactly
+// as sum_slices would.
+void lstm_fwd_point(hipStream_t s, int B, int H, const float *zpart, int ns, const float *bias,
+                    const float *c_prev, float *gates, void *h_out, float *c_out);
+void softmax_ce_rows(hipStream_t s, int rows, int V, const float *lpart, int ns, const float *bias,
+                     const int *labels, float scale, float *dlog, float *loss_rows);
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first);
-void lstm_bwd_point(hipStream_t s, int B, int H, const float *dh, const float *dc_in, const float *gates,
-                    const float *c_t, const float *c_prev, const void *h_prev, const void *h_t, void *dz,
-                    float *dc_prev, void *hp_copy, void *hc_copy, float *db, bool first);
+// dbp receives ceil(B/4) records [4H] of bias-gradient column sums (one per
+// block of 4 batch rows); db_chunk adds a run of such records into db.
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dh_in,
+                    const float *dc_in, const float *gates, const float *c_t, const float *c_prev,
+                    const void *h_prev, const void *h_t, void *dz, float *dc_prev, void *hp_copy,
+                    void *hc_copy, float *dbp);
+void db_chunk(hipStream_t s, int N, int nrec, const float *rec, float *db, bool first);
 void loss_reduce(hipStream_t s, int64_t rows, const float *v, float scale, float *loss);
 void fill_f32(hipStream_t s, int64_t n, float *p, float v);
 

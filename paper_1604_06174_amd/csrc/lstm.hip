@@ -4,9 +4,8 @@
 //   cell   c_t = f c_{t-1} + i g,   h_t = o tanh(c_t)   (c fp32, h rounded to bf16)
 //   head   softmax cross-entropy of a [B, V] row block; the gradient
 //          (p - onehot) * scale is kept in fp32
-// Column sums for the bias gradients run over the batch rows in order inside
-// one thread, and accumulate across time steps in backward order, so they are
-// bit-reproducible.
+// Every sum (split-K slices, bias-gradient columns) runs in an order fixed by
+// the shapes alone, so a step is bit-reproducible whatever the schedule.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -15,6 +14,32 @@ namespace ckpt {
 namespace {
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+// NV elements o[0..NV) of a split-K product: each element's ns partial
+// slices (slice stride `slice`) added in slice order -- the order sum_slices
+// uses.  Slices are fetched U at a time for all NV elements before any of
+// them is added, so the loads of a round are in flight together.
+template <int NV, int U>
+__device__ __forceinline__ void slices_sum(const float *__restrict__ part, int ns, size_t slice,
+                                           const size_t (&o)[NV], float (&v)[NV]) {
+#pragma unroll
+  for (int k = 0; k < NV; ++k) v[k] = part[o[k]];
+  int z = 1;
+  for (; z + U <= ns; z += U) {
+    float t[U][NV];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int k = 0; k < NV; ++k) t[u][k] = part[(z + u) * slice + o[k]];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int k = 0; k < NV; ++k) v[k] += t[u][k];
+  }
+  for (; z < ns; ++z)
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] += part[z * slice + o[k]];
+}
 
 // dst[c][r] = bf16(src[r][c]) for src [R][C] fp32, through 32x32 LDS tiles.
 __global__ __launch_bounds__(256) void k_transpose_bf16(int R, int C, const float *__restrict__ src,
@@ -39,8 +64,9 @@ __global__ __launch_bounds__(256) void k_cvt_bf16(int64_t n, const float *__rest
     dst[e] = (__bf16)src[e];
 }
 
-// one thread per (b, j)
-__global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const float *__restrict__ z,
+// one thread per (b, j); z = sum of the ns partial slices [B, 4H] + bias
+__global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const float *__restrict__ zpart,
+                                                        int ns, const float *__restrict__ bias,
                                                         const float *__restrict__ c_prev,
                                                         float *__restrict__ gates,
                                                         __bf16 *__restrict__ h_out,
@@ -48,8 +74,14 @@ __global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const floa
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= B * H) return;
   const int b = e / H, j = e % H;
-  const float *zr = z + size_t(b) * 4 * H;
-  const float ig = sigm(zr[j]), fg = sigm(zr[H + j]), gg = tanhf(zr[2 * H + j]), og = sigm(zr[3 * H + j]);
+  const size_t r = size_t(b) * 4 * H + j;
+  const size_t o[4] = {r, r + H, r + 2 * H, r + 3 * H};
+  float z[4];
+  slices_sum<4, 4>(zpart, ns, size_t(B) * 4 * H, o, z);
+  const float ig = sigm(z[0] + bias[j]);
+  const float fg = sigm(z[1] + bias[H + j]);
+  const float gg = tanhf(z[2] + bias[2 * H + j]);
+  const float og = sigm(z[3] + bias[3 * H + j]);
   const float cp = c_prev ? c_prev[e] : 0.f;
   const float c = fg * cp + ig * gg;
   float *gr = gates + size_t(b) * 4 * H;
@@ -78,19 +110,30 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-__global__ __launch_bounds__(SM_THREADS) void k_softmax_ce_rows(int V, const float *__restrict__ logits,
+// logits = sum of the ns partial slices [rows, V] + bias
+__global__ __launch_bounds__(SM_THREADS) void k_softmax_ce_rows(int V, const float *__restrict__ lpart,
+                                                                int ns, size_t slice,
+                                                                const float *__restrict__ bias,
                                                                 const int *__restrict__ labels, float scale,
                                                                 float *__restrict__ dlog,
                                                                 float *__restrict__ loss_rows) {
   __shared__ float red[SM_THREADS / 64];
+  __shared__ float lab_logit;
   const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const float *l = logits + size_t(row) * V;
+  const size_t r0 = size_t(row) * V;
+  const int lab = labels[row];
   float x[SM_PER];
+  size_t o[SM_PER];
+  // columns past V read column V - 1 (in bounds) and are dropped below
+#pragma unroll
+  for (int k = 0; k < SM_PER; ++k) o[k] = r0 + min(t + k * SM_THREADS, V - 1);
+  slices_sum<SM_PER, 1>(lpart, ns, slice, o, x);
   float mx = -INFINITY;
 #pragma unroll
   for (int k = 0; k < SM_PER; ++k) {
     const int v = t + k * SM_THREADS;
-    x[k] = v < V ? l[v] : -INFINITY;
+    x[k] = v < V ? x[k] + bias[v] : -INFINITY;
+    if (v == lab) lab_logit = x[k];
     mx = fmaxf(mx, x[k]);
   }
   mx = wave_max(mx);
@@ -111,9 +154,8 @@ __global__ __launch_bounds__(SM_THREADS) void k_softmax_ce_rows(int V, const flo
   __syncthreads();
   se = 0.f;
   for (int k = 0; k < SM_THREADS / 64; ++k) se += red[k];
-  const int lab = labels[row];
   const bool ok = lab >= 0 && lab < V;
-  if (t == 0) loss_rows[row] = ok ? (logf(se) + mx) - l[lab] : NAN;
+  if (t == 0) loss_rows[row] = ok ? (logf(se) + mx) - lab_logit : NAN;
   const float inv = 1.0f / se;
   float *d = dlog + size_t(row) * V;
 #pragma unroll
@@ -148,8 +190,13 @@ __global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float
   }
 }
 
-// Gate backward for hidden unit j and rows b = rg, rg + 4, ...
-__global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const float *__restrict__ dh,
+// Gate backward, one thread per (b, j): workgroup = 64 hidden units x 4
+// batch rows (blockIdx.y = row block).  dh = the ns partial slices [B, H] of
+// the head gradient's product, in order, + the incoming dh (dh_in, [B, H]).
+// The workgroup's bias-gradient column sums over its 4 rows, ((r0 + r1) + r2)
+// + r3, go to dbp[blockIdx.y][4H]; k_db_chunk adds them up.
+__global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const float *__restrict__ dhpart,
+                                                        int ns, const float *__restrict__ dh_in,
                                                         const float *__restrict__ dc_in,
                                                         const float *__restrict__ gates,
                                                         const float *__restrict__ c_t,
@@ -160,41 +207,69 @@ __global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const floa
                                                         float *__restrict__ dc_prev,
                                                         __bf16 *__restrict__ hp_copy,
                                                         __bf16 *__restrict__ hc_copy,
-                                                        float *__restrict__ db, int first) {
+                                                        float *__restrict__ dbp) {
   __shared__ float part[4][4][64];
   const int cx = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int j = blockIdx.x * 64 + cx;
-  float sm[4] = {0.f, 0.f, 0.f, 0.f};
-  if (j < H)
-    for (int b = rg; b < B; b += 4) {
-      const size_t e = size_t(b) * H + j;
-      const float *gr = gates + size_t(b) * 4 * H;
-      const float ig = gr[j], fg = gr[H + j], gg = gr[2 * H + j], og = gr[3 * H + j];
-      const float tc = tanhf(c_t[e]);
-      const float dhv = dh[e];
-      const float dct = dc_in[e] + dhv * og * (1.f - tc * tc);
-      const float cp = c_prev ? c_prev[e] : 0.f;
-      const float zv[4] = {dct * gg * ig * (1.f - ig), dct * cp * fg * (1.f - fg),
-                           dct * ig * (1.f - gg * gg), dhv * tc * og * (1.f - og)};
-      __bf16 *dr = dz + size_t(b) * 4 * H;
+  const int j = blockIdx.x * 64 + cx, b = blockIdx.y * 4 + rg;
+  float zv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < H && b < B) {
+    const size_t e = size_t(b) * H + j;
+    const size_t oe[1] = {e};
+    float dh[1];
+    slices_sum<1, 8>(dhpart, ns, size_t(B) * H, oe, dh);
+    const float dhv = dh[0] + dh_in[e];
+    const float *gr = gates + size_t(b) * 4 * H;
+    const float ig = gr[j], fg = gr[H + j], gg = gr[2 * H + j], og = gr[3 * H + j];
+    const float tc = tanhf(c_t[e]);
+    const float dct = dc_in[e] + dhv * og * (1.f - tc * tc);
+    const float cp = c_prev ? c_prev[e] : 0.f;
+    zv[0] = dct * gg * ig * (1.f - ig);
+    zv[1] = dct * cp * fg * (1.f - fg);
+    zv[2] = dct * ig * (1.f - gg * gg);
+    zv[3] = dhv * tc * og * (1.f - og);
+    __bf16 *dr = dz + size_t(b) * 4 * H;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        dr[k * H + j] = (__bf16)zv[k];
-        sm[k] += zv[k];
-      }
-      if (dc_prev) dc_prev[e] = dct * fg;
-      hp_copy[e] = h_prev ? h_prev[e] : (__bf16)0.f;
-      hc_copy[e] = h_t[e];
-    }
+    for (int k = 0; k < 4; ++k) dr[k * H + j] = (__bf16)zv[k];
+    if (dc_prev) dc_prev[e] = dct * fg;
+    hp_copy[e] = h_prev ? h_prev[e] : (__bf16)0.f;
+    hc_copy[e] = h_t[e];
+  }
 #pragma unroll
-  for (int k = 0; k < 4; ++k) part[k][rg][cx] = sm[k];
+  for (int k = 0; k < 4; ++k) part[k][rg][cx] = zv[k];
   __syncthreads();
-  if (rg == 0 && j < H) {
+  if (j < H) {
+    const int k = rg;  // row group rg writes gate k's column sum
+    const float t = ((part[k][0][cx] + part[k][1][cx]) + part[k][2][cx]) + part[k][3][cx];
+    dbp[size_t(blockIdx.y) * 4 * H + size_t(k) * H + j] = t;
+  }
+}
+
+// db[n] (+)= the nrec records rec[r][n] (record stride N), r = 0 .. nrec-1:
+// workgroup = 64 columns x 4 groups of consecutive records; each group adds
+// its records in order, the groups combine as ((g0 + g1) + g2) + g3.
+__global__ __launch_bounds__(256) void k_db_chunk(int N, int nrec, const float *__restrict__ rec,
+                                                  float *__restrict__ db, int first) {
+  __shared__ float part[4][64];
+  const int cx = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + cx;
+  const int per = (nrec + 3) / 4, r0 = min(nrec, g * per), r1 = min(nrec, r0 + per);
+  float s = 0.f;
+  if (n < N) {
+    int r = r0;
+    for (; r + 8 <= r1; r += 8) {
+      float t[8];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float t = ((part[k][0][cx] + part[k][1][cx]) + part[k][2][cx]) + part[k][3][cx];
-      db[k * H + j] = first ? t : db[k * H + j] + t;
+      for (int u = 0; u < 8; ++u) t[u] = rec[size_t(r + u) * N + n];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += t[u];
     }
+    for (; r < r1; ++r) s += rec[size_t(r) * N + n];
+  }
+  part[g][cx] = s;
+  __syncthreads();
+  if (g == 0 && n < N) {
+    const float t = ((part[0][cx] + part[1][cx]) + part[2][cx]) + part[3][cx];
+    db[n] = first ? t : db[n] + t;
   }
 }
 
@@ -233,16 +308,16 @@ void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst) {
   hipLaunchKernelGGL(k_cvt_bf16, dim3(grid_for(n)), dim3(256), 0, s, n, src, static_cast<__bf16 *>(dst));
 }
 
-void lstm_fwd_point(hipStream_t s, int B, int H, const float *z, const float *c_prev, float *gates,
-                    void *h_out, float *c_out) {
-  hipLaunchKernelGGL(k_lstm_fwd_point, dim3((B * H + 255) / 256), dim3(256), 0, s, B, H, z, c_prev,
-                     gates, static_cast<__bf16 *>(h_out), c_out);
+void lstm_fwd_point(hipStream_t s, int B, int H, const float *zpart, int ns, const float *bias,
+                    const float *c_prev, float *gates, void *h_out, float *c_out) {
+  hipLaunchKernelGGL(k_lstm_fwd_point, dim3((B * H + 255) / 256), dim3(256), 0, s, B, H, zpart, ns,
+                     bias, c_prev, gates, static_cast<__bf16 *>(h_out), c_out);
 }
 
-void softmax_ce_rows(hipStream_t s, int rows, int V, const float *logits, const int *labels,
-                     float scale, float *dlog, float *loss_rows) {
-  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(SM_THREADS), 0, s, V, logits, labels, scale,
-                     dlog, loss_rows);
+void softmax_ce_rows(hipStream_t s, int rows, int V, const float *lpart, int ns, const float *bias,
+                     const int *labels, float scale, float *dlog, float *loss_rows) {
+  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(SM_THREADS), 0, s, V, lpart, ns,
+                     size_t(rows) * V, bias, labels, scale, dlog, loss_rows);
 }
 
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {
@@ -250,13 +325,18 @@ void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, 
                      static_cast<__bf16 *>(dl_bf), db_o, first ? 1 : 0);
 }
 
-void lstm_bwd_point(hipStream_t s, int B, int H, const float *dh, const float *dc_in, const float *gates,
-                    const float *c_t, const float *c_prev, const void *h_prev, const void *h_t, void *dz,
-                    float *dc_prev, void *hp_copy, void *hc_copy, float *db, bool first) {
-  hipLaunchKernelGGL(k_lstm_bwd_point, dim3((H + 63) / 64), dim3(256), 0, s, B, H, dh, dc_in, gates,
-                     c_t, c_prev, static_cast<const __bf16 *>(h_prev), static_cast<const __bf16 *>(h_t),
-                     static_cast<__bf16 *>(dz), dc_prev, static_cast<__bf16 *>(hp_copy),
-                     static_cast<__bf16 *>(hc_copy), db, first ? 1 : 0);
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dh_in,
+                    const float *dc_in, const float *gates, const float *c_t, const float *c_prev,
+                    const void *h_prev, const void *h_t, void *dz, float *dc_prev, void *hp_copy,
+                    void *hc_copy, float *dbp) {
+  hipLaunchKernelGGL(k_lstm_bwd_point, dim3((H + 63) / 64, (B + 3) / 4), dim3(256), 0, s, B, H, dhpart,
+                     ns, dh_in, dc_in, gates, c_t, c_prev, static_cast<const __bf16 *>(h_prev),
+                     static_cast<const __bf16 *>(h_t), static_cast<__bf16 *>(dz), dc_prev,
+                     static_cast<__bf16 *>(hp_copy), static_cast<__bf16 *>(hc_copy), dbp);
+}
+
+void db_chunk(hipStream_t s, int N, int nrec, const float *rec, float *db, bool first) {
+  hipLaunchKernelGGL(k_db_chunk, dim3((N + 63) / 64), dim3(256), 0, s, N, nrec, rec, db, first ? 1 : 0);
 }
 
 void loss_reduce(hipStream_t s, int64_t rows, const float *v, float scale, float *loss) {

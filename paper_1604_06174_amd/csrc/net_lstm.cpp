@@ -33,7 +33,7 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_z, k_logits, k_lossrows, k_loss, k_part;
+  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part;
   // split-K counts: input and recurrent parts of z, logits, dh (head), dh_{t-1}
   int s_x, s_h, s_l, s_dh, s_dx;
   // extra gradient buffer offsets
@@ -78,8 +78,9 @@ class LstmNet : public Net {
     k_wh = take(uint64_t(H) * 4 * H * 2);
     k_wot = take(uint64_t(H) * V * 2);
     k_wo = take(uint64_t(H) * V * 2);
-    k_z = take(uint64_t(B) * 4 * H * 4);
-    k_logits = take(uint64_t(B) * V * 4);
+    // bias-gradient column sums of one chunk: per step, one [4H] record per
+    // block of 4 batch rows
+    k_dbp = take(uint64_t(C) * ((B + 3) / 4) * 4 * H * 4);
     k_lossrows = take(uint64_t(T) * B * 4);
     k_loss = take(4);
     s_x = gemm_bf16_splits(B, 4 * H, E);
@@ -137,19 +138,17 @@ class LstmNet : public Net {
     char *sv = static_cast<char *>(saved);
     const void *xt = static_cast<const char *>(c.input) + size_t(i) * B * E * 2;
     const int *lab = static_cast<const int *>(c.target) + size_t(i) * B;
-    float *z = Kf(c, k_z);
     // z = x_t W_x + h_{t-1} W_h + b: both products split over k into one
-    // slice buffer, summed in order with the bias
+    // slice buffer that the pointwise kernel adds up in order with the bias
     gemm_part(c, B, 4 * H, E, xt, E, K(c, k_wxt), E, 0, s_x);
     if (i > 0) gemm_part(c, B, 4 * H, H, x, H, K(c, k_wht), H, s_x, s_h);
-    sum_parts(c, s_x + (i > 0 ? s_h : 0), B, 4 * H, z, nullptr, 0, P(c, pb));
     const float *c_prev = i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr;
     float *gates = reinterpret_cast<float *>(sv);
-    lstm_fwd_point(c.s, B, H, z, c_prev, gates, y, reinterpret_cast<float *>(y + hb));
-    float *logits = Kf(c, k_logits);
+    lstm_fwd_point(c.s, B, H, Kf(c, k_part), s_x + (i > 0 ? s_h : 0), P(c, pb), c_prev, gates, y,
+                   reinterpret_cast<float *>(y + hb));
+    // logits = h_t W_o + b_o, summed from its slices by the softmax kernel
     gemm_part(c, B, V, H, y, H, K(c, k_wot), H, 0, s_l);
-    sum_parts(c, s_l, B, V, logits, nullptr, 0, P(c, pbo));
-    softmax_ce_rows(c.s, B, V, logits, lab, 1.0f / (float(T) * float(B)),
+    softmax_ce_rows(c.s, B, V, Kf(c, k_part), s_l, P(c, pbo), lab, 1.0f / (float(T) * float(B)),
                     reinterpret_cast<float *>(sv + ga), Kf(c, k_lossrows) + size_t(i) * B);
     c.launches += 2;
   }
@@ -165,27 +164,33 @@ class LstmNet : public Net {
     const int t0 = (i / C) * C;
     const size_t row = size_t(i - t0) * B;
     const bool first_step = i == n - 1;
+    const int t_end = std::min(t0 + C, int(n)), rb = (B + 3) / 4;
     char *dl = X(c, x_dl) + row * V * 2;
     char *dz = X(c, x_dz) + row * 4 * H * 2;
     char *hp = X(c, x_hp) + row * H * 2;
     char *hc = X(c, x_hc) + row * H * 2;
     head_bwd_prep(c.s, B, V, reinterpret_cast<const float *>(sv + ga), dl, G(c, pbo), first_step);
-    float *dh = static_cast<float *>(qv);
-    // total dh = (head gradient) W_o^T + the incoming dh
+    (void)qv;
+    // total dh = (head gradient) W_o^T + the incoming dh, added up from the
+    // product's slices by the pointwise kernel
     gemm_part(c, B, H, V, dl, V, K(c, k_wo), V, 0, s_dh);
-    sum_parts(c, s_dh, B, H, dh, reinterpret_cast<const float *>(g), H);
-    lstm_bwd_point(c.s, B, H, dh, reinterpret_cast<const float *>(g + gh),
+    lstm_bwd_point(c.s, B, H, Kf(c, k_part), s_dh, reinterpret_cast<const float *>(g),
+                   reinterpret_cast<const float *>(g + gh),
                    reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
                    i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
-                   dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc, G(c, pb), first_step);
+                   dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc,
+                   Kf(c, k_dbp) + size_t(t_end - 1 - i) * rb * 4 * H);
     c.launches += 2;
     if (dx) {
       gemm_part(c, B, H, 4 * H, dz, 4 * H, K(c, k_wh), 4 * H, 0, s_dx);
       sum_parts(c, s_dx, B, H, reinterpret_cast<float *>(dx));
     }
     if (i == t0) {  // the chunk [t0, t0 + C) is complete: its weight gradients
-      const int rows = (std::min(t0 + C, int(n)) - t0) * B;
+      const int rows = (t_end - t0) * B;
       const bool first_chunk = t0 + C >= n;
+      // b: the chunk's records in backward order of the steps
+      db_chunk(c.s, 4 * H, (t_end - t0) * rb, Kf(c, k_dbp), G(c, pb), first_chunk);
+      c.launches += 1;
       const int epi = first_chunk ? GEMM_EPI_STORE : GEMM_EPI_ADD;
       const void *xs = static_cast<const char *>(c.input) + size_t(t0) * B * E * 2;
       gemm(c, E, 4 * H, rows, xs, false, E, false, X(c, x_dz), 4 * H, false, G(c, pWx), 4 * H, epi,

@@ -43,7 +43,7 @@ def _plan_args(cfg, net):
     if mode == "greedy":
         return K.GREEDY, int(sum(lb) * cfg.get("budget_frac", 0.1)), "greedy"
     if mode == "recursive":
-        return K.RECURSIVE, 0, "recursive"
+        return K.RECURSIVE, int(cfg.get("fanout", 1)), "recursive"
     raise ValueError(mode)
 
 
@@ -111,7 +111,7 @@ def _cpu_baseline(cfg, sample_batch, d_full):
         oplan = None if mode == PL.RECURSIVE else PL.plan(n, lb, cb, budget, mode)
     t0 = time.perf_counter()
     if oplan is None:
-        SCH.recursive_step(chain, inp, tgt)
+        SCH.recursive_step(chain, inp, tgt, int(cfg.get("fanout", 1)))
     else:
         SCH.segment_step(chain, inp, tgt, oplan)
     dt = time.perf_counter() - t0
@@ -129,6 +129,8 @@ def main():
     ap.add_argument("--workload", default="cifar110")
     ap.add_argument("--plan", default=None, choices=["sqrt", "greedy", "recursive", "search"],
                     help="override the workload's plan (search: the appendix-A budget search)")
+    ap.add_argument("--fanout", type=int, default=0,
+                    help="recursive plan: boundaries stored per level (section 4.4's k; default 1)")
     ap.add_argument("--drop-bn-relu", action="store_true",
                     help="CIFAR-shaped net: keep only convolution outputs and re-form batch norm + "
                          "ReLU from them when read")
@@ -159,6 +161,11 @@ def main():
     step = GpuStep(cfg, d["params"], d["input"], d["target"])
     if args.plan:
         cfg["plan"] = args.plan
+    if args.fanout:
+        if cfg.get("plan") != "recursive":
+            print(json.dumps({"error": "--fanout applies to the recursive plan"}))
+            sys.exit(2)
+        cfg["fanout"] = args.fanout
     mode, budget, mode_name = _plan_args(cfg, step.net)
     if mode == "search":
         plan, budget, _ = step.net.search_plan()
@@ -243,7 +250,8 @@ def main():
         "config": {"workload": args.workload + ("+drop_bn_relu" if args.drop_bn_relu else ""),
                    "kind": cfg["kind"], "batch": batch,
                    "units": step.net.n, "plan": mode_name,
-                   "stride_or_budget": budget, "cuts": len(plan.cuts())},
+                   "stride_or_budget": budget, "cuts": len(plan.cuts()),
+                   **({"fanout": budget} if mode_name == "recursive" else {})},
         "peak_activation_gb": round(acc["peak"] / 1e9, 6),
         "peak_activation_gb_no_ckpt": round(acc_none["peak"] / 1e9, 6),
         "recompute_overhead_x": round(ms / ms_none, 4),

@@ -45,7 +45,7 @@ extern "C" {
 #define CKPT_NONE      0  /* one segment, activations of the first forward kept     */
 #define CKPT_SQRT      1  /* section 4.3, Eq. 1: ceil(sqrt n) equal segments         */
 #define CKPT_GREEDY    2  /* Alg. 3: budget-driven greedy segmentation               */
-#define CKPT_RECURSIVE 3  /* section 4.4, Eq. 2-3 with k = 1: O(log n) boundaries    */
+#define CKPT_RECURSIVE 3  /* section 4.4, Eq. 2-3: k splits per level, k log_{k+1} n */
 #define CKPT_USER      4  /* explicit cut list: the user-set mirror attribute (4.5)  */
 
 /* plan flags */
@@ -66,7 +66,11 @@ typedef struct ckpt_net ckpt_net;
  *                entry must be 0: the chain's output feeds the loss (Alg. 1).
  *   budget       GREEDY: Alg. 3's per-segment budget B (bytes).  SQRT: the
  *                stride (units per segment) if > 0, else ceil(sqrt n).
- *                Ignored by the other modes.
+ *                RECURSIVE: the fan-out k of section 4.4 (boundaries stored
+ *                per level; 0 means 1, at most 2^31 - 1): a range of L > 1
+ *                units splits into at most k + 1 parts at
+ *                floor(j L / (k+1)), j = 1..k, repeats dropped; the parts
+ *                are handled last to first.  Ignored by the other modes.
  *   mode         CKPT_NONE .. CKPT_USER.
  *   user_cuts    host [n_user_cuts], CKPT_USER only: strictly ascending
  *                candidate positions below n-1.
@@ -75,7 +79,8 @@ typedef struct ckpt_net ckpt_net;
  * Errors: CKPT_E_INVALID for n <= 0, null pointers, cut_bytes[n-1] != 0, an
  *   unknown mode, or a user cut list that is unsorted, repeated, out of range
  *   or on a non-candidate; CKPT_E_UNSUPPORTED for RECURSIVE on a chain with a
- *   non-candidate boundary.
+ *   non-candidate boundary; CKPT_E_INVALID for a RECURSIVE fan-out of 2^31
+ *   or more.
  */
 int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
                      uint64_t budget, int32_t mode, const int32_t *user_cuts,
@@ -84,7 +89,7 @@ int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64
 /*
  * plan_info -- summary of a plan.  Any output pointer may be null.
  *   mode, n_layers, n_cuts   as planned (RECURSIVE reports 0 cuts: its split
- *                            tree is implicit, midpoint splits of every range)
+ *                            tree is implicit, the fan-out splits of every range)
  *   x, y                     Alg. 3's outputs for the plan's cut set: kept
  *                            boundary bytes, and the largest segment total
  *                            among segments ending at a cut (0 for RECURSIVE)
@@ -102,8 +107,9 @@ int plan_cuts(const ckpt_plan *plan, int32_t *cuts, int32_t cap, int32_t *n_cuts
 
 /*
  * plan_serialize -- canonical little-endian bytes of the plan:
- *   "CKPL" u32 version=1, u32 mode, u32 keep_last, u32 n, u32 n_cuts,
- *   i32 cuts[n_cuts], u64 x, u64 y, u64 extra_unit_forwards.
+ *   "CKPL" u32 version=2, u32 mode, u32 keep_last, u32 fanout (RECURSIVE's
+ *   k, else 0), u32 n, u32 n_cuts, i32 cuts[n_cuts], u64 x, u64 y,
+ *   u64 extra_unit_forwards.
  * buf (host, cap bytes) may be null to query *len.  CKPT_E_INVALID if cap is
  * too small for a non-null buf.
  */

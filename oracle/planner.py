@@ -23,10 +23,14 @@ Modes:
                candidate where temp > B, cut, add the cut's bytes to x, raise y
                to temp and reset temp to 0.  x and y are returned exactly as
                Alg. 3 computes them (y only sees segments that end at a cut).
-* RECURSIVE -- section 4.4 with k = 1 (Eq. 2-3): a segment of length L > 1 is
-               split at a + floor(L/2); its first half's boundary is stored,
-               and each half is handled the same way; a single unit is
-               re-forwarded once.
+* RECURSIVE -- section 4.4 (Eq. 2-3) with k stored splits per level (``budget``
+               gives k; 0 means k = 1): a range [lo, lo + L) with L > 1 is
+               split into at most k + 1 parts at lo + floor(j L / (k+1)),
+               j = 1..k (repeated or end points dropped); one forward sweep
+               stores the split boundaries, then the parts are handled the
+               same way from last to first, each split point dropped once its
+               part is done; a single unit is re-forwarded once.  The stored
+               boundaries follow g(n) = k + g(n / (k+1)), i.e. k log_{k+1} n.
 * USER      -- an explicit cut list (the user-set mirror attribute of
                section 4.5).
 
@@ -62,7 +66,7 @@ from typing import List, Optional, Sequence
 NONE, SQRT, GREEDY, RECURSIVE, USER = 0, 1, 2, 3, 4
 FLAG_KEEP_LAST = 1
 MAGIC = b"CKPL"
-VERSION = 1
+VERSION = 2
 
 
 class PlanError(ValueError):
@@ -82,6 +86,7 @@ class Plan:
     y: int = 0
     extra_forwards: int = 0
     keep_last: bool = False
+    fanout: int = 0          # RECURSIVE: k stored splits per level; 0 otherwise
 
     def segments(self):
         """Half-open [begin, end) segments of a one-level plan."""
@@ -93,8 +98,8 @@ class Plan:
         return out
 
     def serialize(self) -> bytes:
-        body = struct.pack("<4sIIIII", MAGIC, VERSION, self.mode, 1 if self.keep_last else 0,
-                           self.n, len(self.cuts))
+        body = struct.pack("<4sIIIIII", MAGIC, VERSION, self.mode, 1 if self.keep_last else 0,
+                           self.fanout, self.n, len(self.cuts))
         body += struct.pack(f"<{len(self.cuts)}i", *self.cuts)
         body += struct.pack("<QQQ", self.x, self.y, self.extra_forwards)
         return body
@@ -146,17 +151,36 @@ def sqrt_cuts(n, cut_bytes, stride):
     return cuts
 
 
-def recursive_extra(n: int) -> int:
-    """Unit forwards done after the first full forward, by the recursion below."""
+def rec_splits(lo: int, hi: int, k: int) -> List[int]:
+    """The split points of [lo, hi) for fan-out k: lo + floor(j L / (k+1)) for
+    j = 1..k, keeping those strictly inside the range, without repeats."""
+    L = hi - lo
+    pts = []
+    for j in range(1, k + 1):
+        m = lo + (j * L) // (k + 1)
+        if lo < m < hi and (not pts or m > pts[-1]):
+            pts.append(m)
+    return pts
+
+
+def rec_parts(lo: int, hi: int, k: int):
+    """The parts [lo, m_1), [m_1, m_2), ..., [m_last, hi) of a split range."""
+    e = [lo] + rec_splits(lo, hi, k) + [hi]
+    return [(e[t], e[t + 1]) for t in range(len(e) - 1)]
+
+
+def recursive_extra(n: int, k: int = 1) -> int:
+    """Unit forwards done after the first full forward, by the recursion: a
+    range of one unit is re-forwarded once; a longer range re-runs the sweep
+    up to its last split point, then its parts."""
     def R(a, b):
         if b - a == 1:
             return 1
-        m = a + (b - a) // 2
-        return (m - a) + R(m, b) + R(a, m)
+        parts = rec_parts(a, b, k)
+        return (parts[-1][0] - a) + sum(R(p, q) for (p, q) in parts)
     if n == 1:
         return R(0, 1)
-    m = n // 2
-    return R(m, n) + R(0, m)
+    return sum(R(p, q) for (p, q) in rec_parts(0, n, k))
 
 
 def plan(n: int, layer_bytes: Sequence[int], cut_bytes: Sequence[int], budget: int, mode: int,
@@ -183,7 +207,10 @@ def plan(n: int, layer_bytes: Sequence[int], cut_bytes: Sequence[int], budget: i
     elif mode == RECURSIVE:
         if any(cut_bytes[i] == 0 for i in range(n - 1)):
             raise Unsupported("the recursive schedule needs every boundary to be a candidate")
-        return Plan(RECURSIVE, n, [], 0, 0, recursive_extra(n), False)
+        k = budget if budget > 0 else 1
+        if k >= 1 << 31:
+            raise PlanError("the recursion fan-out must fit in 31 bits")
+        return Plan(RECURSIVE, n, [], 0, 0, recursive_extra(n, k), False, k)
     else:
         raise PlanError(f"unknown mode {mode}")
     x, y = xy_of_cuts(layer_bytes, cut_bytes, cuts)
@@ -237,34 +264,44 @@ def account(p: Plan, b: Sequence[int], a: Sequence[int], q: Sequence[int], slot=
     assert len(b) == n + 1 and len(a) == n and len(q) == n
     G = grad_bytes(b, q, slot, extra)
     if p.mode == RECURSIVE:
+        k = p.fanout
         arena = 0
         stack: List[int] = []
         ckpt_max = 0
+
+        def handle_parts(parts):
+            # split boundaries of parts[1:] are on the stack; the last part
+            # is handled first and its boundary dropped after it
+            nonlocal ckpt_max
+            for t in range(len(parts) - 1, -1, -1):
+                R(*parts[t])
+                if t > 0:
+                    stack.pop()
 
         def R(lo, hi):
             nonlocal arena, ckpt_max
             if hi - lo == 1:
                 arena = max(arena, a[lo] + b[lo + 1])
                 return
-            m = lo + (hi - lo) // 2
-            arena = max(arena, *_sweep_needs(b, a, lo, m, {m - 1}))
-            stack.append(b[m])
+            parts = rec_parts(lo, hi, k)
+            splits = [q for (q, _) in parts[1:]]
+            arena = max(arena, *_sweep_needs(b, a, lo, splits[-1], {m - 1 for m in splits}))
+            for m in splits:
+                stack.append(b[m])
             ckpt_max = max(ckpt_max, sum(stack))
-            R(m, hi)
-            stack.pop()
-            R(lo, m)
+            handle_parts(parts)
 
         if n == 1:
             arena = max(arena, *_sweep_needs(b, a, 0, 1, set()))
             R(0, 1)
         else:
-            m = n // 2
-            arena = max(arena, *_sweep_needs(b, a, 0, n, {m - 1}))
-            stack.append(b[m])
+            parts = rec_parts(0, n, k)
+            splits = [q for (q, _) in parts[1:]]
+            arena = max(arena, *_sweep_needs(b, a, 0, n, {m - 1 for m in splits}))
+            for m in splits:
+                stack.append(b[m])
             ckpt_max = max(ckpt_max, sum(stack))
-            R(m, n)
-            stack.pop()
-            R(0, m)
+            handle_parts(parts)
         return Accounting(ckpt_max, arena, G)
     cuts = set(p.cuts)
     segs = p.segments()

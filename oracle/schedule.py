@@ -88,7 +88,12 @@ def segment_step(chain: Chain, inp, target, plan: PL.Plan):
     return loss, grads, cnt.fwd
 
 
-def recursive_step(chain: Chain, inp, target):
+def recursive_step(chain: Chain, inp, target, k: int = 1):
+    """Section 4.4's recursion with k stored splits per level (parts from
+    planner.rec_parts): forward a range up to its last split point storing the
+    split boundaries, handle the parts last to first, drop each boundary once
+    its part is done; a single unit is re-forwarded and back-propagated.
+    Returns (loss, grads, unit forwards, the most boundaries stored at once)."""
     inp = chain.prec.cast(inp)
     cnt = _Counter()
     n = chain.n
@@ -96,41 +101,45 @@ def recursive_step(chain: Chain, inp, target):
     grads = chain.zero_grads()
     state = {"g": None}
 
-    def run_forward(lo, hi, x, keep_at=None):
-        """Forward [lo, hi) from x; return (x_hi, stored x_{keep_at} or None)."""
+    def run_forward(lo, hi, x, keep, first=False):
+        """Forward [lo, hi) from x; return (x_hi, {m: x_m for m in keep})."""
         nonlocal loss
-        kept = None
+        kept = {}
         v = x
         for i in range(lo, hi):
-            v, _, _ = _fwd(chain, i, v, inp, target, cnt)
-            if keep_at is not None and i + 1 == keep_at:
-                kept = v
+            v, _, lp = _fwd(chain, i, v, inp, target, cnt)
+            if first:
+                loss += lp  # the loss parts are taken from the first forward only
+            if i + 1 in keep:
+                kept[i + 1] = v
         return v, kept
+
+    def handle(parts, x_lo, kept):
+        for t in range(len(parts) - 1, -1, -1):
+            p, q = parts[t]
+            R(p, q, kept[p] if t > 0 else x_lo)
+            if t > 0:
+                del kept[p]
+                cnt.live_ckpts -= 1
 
     def R(lo, hi, x_lo):
         if hi - lo == 1:
             y, s, _ = _fwd(chain, lo, x_lo, inp, target, cnt)
             state["g"] = _bwd_unit(chain, lo, state["g"], x_lo, y, s, inp, target, grads)
             return
-        m = lo + (hi - lo) // 2
-        _, x_m = run_forward(lo, m, x_lo, keep_at=m)
-        cnt.live_ckpts += 1
+        parts = PL.rec_parts(lo, hi, k)
+        splits = [p for (p, _) in parts[1:]]
+        _, kept = run_forward(lo, splits[-1], x_lo, set(splits))
+        cnt.live_ckpts += len(splits)
         cnt.max_live_ckpts = max(cnt.max_live_ckpts, cnt.live_ckpts)
-        R(m, hi, x_m)
-        cnt.live_ckpts -= 1
-        del x_m
-        R(lo, m, x_lo)
+        handle(parts, x_lo, kept)
 
     x0 = chain.x0(inp)
-    # first forward: the loss parts are accumulated here only
-    v = x0
-    x_mid = None
-    mid = n // 2 if n > 1 else None
-    for i in range(n):
-        v, _, lp = _fwd(chain, i, v, inp, target, cnt)
-        loss += lp
-        if mid is not None and i + 1 == mid:
-            x_mid = v
+    parts = PL.rec_parts(0, n, k) if n > 1 else [(0, 1)]
+    splits = [p for (p, _) in parts[1:]]
+    v, kept = run_forward(0, n, x0, set(splits), first=True)
+    cnt.live_ckpts = len(splits)
+    cnt.max_live_ckpts = cnt.live_ckpts
     hl, g, hgrads = chain.head(v, target)
     loss += hl
     for name, val in hgrads.items():
@@ -139,10 +148,5 @@ def recursive_step(chain: Chain, inp, target):
     if n == 1:
         R(0, 1, x0)
     else:
-        cnt.live_ckpts = 1
-        cnt.max_live_ckpts = 1
-        R(mid, n, x_mid)
-        cnt.live_ckpts = 0
-        x_mid = None
-        R(0, mid, x0)
+        handle(parts, x0, kept)
     return loss, grads, cnt.fwd, cnt.max_live_ckpts

@@ -27,6 +27,7 @@ struct Plan {
   int32_t mode = CKPT_NONE;
   int32_t n = 0;
   bool keep_last = false;
+  int32_t fanout = 0;          // RECURSIVE: k stored splits per level; 0 otherwise
   std::vector<int32_t> cuts;   // ascending; cut c keeps x_{c+1}
   uint64_t x = 0, y = 0, extra = 0;
 
@@ -55,7 +56,11 @@ std::vector<uint8_t> serialize(const Plan &p);
 // largest boundary), extra = fixed gradient buffers
 Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
                    const std::vector<uint64_t> &q, uint64_t slot = 0, uint64_t extra = 0);
-uint64_t recursive_extra(int32_t n);
+uint64_t recursive_extra(int32_t n, int32_t k);
+// Section 4.4's split of [lo, hi) for fan-out k: the boundaries
+// lo + floor(j (hi - lo) / (k+1)), j = 1..k, strictly inside, ascending,
+// without repeats.
+std::vector<int32_t> rec_splits(int32_t lo, int32_t hi, int32_t k);
 // Appendix A's budget search: the candidate budgets (ascending) and the GREEDY
 // plan of the candidate with the lowest exact peak (ties: smaller budget).
 std::vector<uint64_t> search_candidates(int32_t n, const uint64_t *lb, const uint64_t *cb);

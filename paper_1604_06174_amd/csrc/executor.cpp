@@ -7,10 +7,12 @@
 // segment's first forward already writes the localtemp layout and is not
 // re-run.
 //
-// RECURSIVE follows section 4.4 with k = 1: the first sweep keeps x_m for
-// m = floor(n/2); a range [lo, hi) of length > 1 runs [lo, m') forward from its
-// input, pushes x_{m'} on the checkpoint stack, handles [m', hi), pops, then
-// handles [lo, m'); a single unit is re-run and back-propagated.
+// RECURSIVE follows section 4.4 with k stored splits per level: the first
+// sweep keeps the top-level split boundaries; a range [lo, hi) of length > 1
+// runs forward from its input up to its last split point, pushing each split
+// boundary on the checkpoint stack, then handles its parts last to first,
+// popping each boundary after its part; a single unit is re-run and
+// back-propagated.
 //
 // Workspace layout (each region 256-byte aligned, sizes from the planner's
 // accounting so that the reported peak is exactly what is used):
@@ -155,6 +157,35 @@ struct Exec {
 
   uint64_t stack_top = 0;
 
+  int32_t fanout = 1;
+
+  // Forward [lo, sweep_hi) from x keeping the split boundaries of [lo, hi)
+  // on the checkpoint stack; returns x_{sweep_hi} and the boundaries' slots.
+  const void *push_splits(int32_t lo, int32_t hi, int32_t sweep_hi, const void *x,
+                          std::vector<int32_t> &s, std::vector<char *> &slot) {
+    s = rec_splits(lo, hi, fanout);
+    slot.resize(s.size());
+    for (size_t t = 0; t < s.size(); ++t) {
+      slot[t] = ckpt + stack_top;
+      stack_top += net.b[size_t(s[t])];
+    }
+    return sweep(lo, sweep_hi, x, [&](int32_t i) -> void * {
+      auto it = std::lower_bound(s.begin(), s.end(), i + 1);
+      return (it != s.end() && *it == i + 1) ? slot[size_t(it - s.begin())] : nullptr;
+    });
+  }
+
+  // the parts of [lo, hi), last to first; each split boundary is popped once
+  // its part is done
+  void parts(int32_t lo, int32_t hi, const void *x, const std::vector<int32_t> &s,
+             const std::vector<char *> &slot) {
+    for (size_t t = s.size() + 1; t-- > 0;) {
+      const int32_t p_lo = t == 0 ? lo : s[t - 1], p_hi = t == s.size() ? hi : s[t];
+      rec(p_lo, p_hi, t == 0 ? x : slot[t - 1]);
+      if (t > 0) stack_top -= net.b[size_t(s[t - 1])];
+    }
+  }
+
   void rec(int32_t lo, int32_t hi, const void *x) {
     if (hi - lo == 1) {
       std::vector<void *> saved, out;
@@ -162,17 +193,16 @@ struct Exec {
       backward_segment(lo, hi, x, saved, out);
       return;
     }
-    const int32_t m = lo + (hi - lo) / 2;
-    char *slot = ckpt + stack_top;
-    stack_top += net.b[size_t(m)];
-    sweep(lo, m, x, [&](int32_t i) -> void * { return i == m - 1 ? slot : nullptr; });
-    rec(m, hi, slot);
-    stack_top -= net.b[size_t(m)];
-    rec(lo, m, x);
+    std::vector<int32_t> s;
+    std::vector<char *> slot;
+    push_splits(lo, hi, rec_splits(lo, hi, fanout).back(), x, s, slot);
+    parts(lo, hi, x, s, slot);
   }
 
   void recursive(const Plan &p, const void *x0) {
     const int32_t n = p.n;
+    fanout = p.fanout;
+    stack_top = 0;
     if (n == 1) {
       const void *xn = sweep(0, 1, x0, [](int32_t) -> void * { return nullptr; });
       net.head(xn, gslot[0], c);
@@ -180,15 +210,12 @@ struct Exec {
       rec(0, 1, x0);
       return;
     }
-    const int32_t m = n / 2;
-    char *slot = ckpt;
-    stack_top = net.b[size_t(m)];
-    const void *xn = sweep(0, n, x0, [&](int32_t i) -> void * { return i == m - 1 ? slot : nullptr; });
+    std::vector<int32_t> s;
+    std::vector<char *> slot;
+    const void *xn = push_splits(0, n, n, x0, s, slot);  // the first forward: the whole chain
     net.head(xn, gslot[0], c);
     cur = 0;
-    rec(m, n, slot);
-    stack_top = 0;
-    rec(0, m, x0);
+    parts(0, n, x0, s, slot);
   }
 };
 

@@ -9,9 +9,10 @@
 //   GREEDY     Alg. 3: running total of per-unit bytes; cut at a candidate
 //              whose running total exceeds the budget B (strict), then restart
 //              the total.  x, y reported as Alg. 3 computes them.
-//   RECURSIVE  section 4.4 with k = 1 (Eq. 2-3, g(n) = log2 n): split every
-//              range of length L > 1 at floor(L/2), keep the midpoint
-//              boundary while the right half is handled, then the left half.
+//   RECURSIVE  section 4.4 (Eq. 2-3, g(n) = k + g(n/(k+1)) = k log_{k+1} n):
+//              split every range of length L > 1 into at most k + 1 parts at
+//              floor(j L / (k+1)), keep the split boundaries while the parts
+//              are handled last to first, dropping each after its part.
 //   USER       caller's cut list (the user-settable mirror attribute, 4.5).
 //   NONE       one segment with the first forward's activations kept.
 #include <algorithm>
@@ -35,16 +36,43 @@ static uint64_t ceil_isqrt(uint64_t n) {
   return r * r == n ? r : r + 1;
 }
 
-static uint64_t rec_range(int32_t a, int32_t b) {
-  if (b - a == 1) return 1;
-  int32_t m = a + (b - a) / 2;
-  return uint64_t(m - a) + rec_range(m, b) + rec_range(a, m);
+std::vector<int32_t> rec_splits(int32_t lo, int32_t hi, int32_t k) {
+  std::vector<int32_t> s;
+  const int64_t L = int64_t(hi) - lo;
+  // k >= L - 1 gives every point lo+1 .. hi-1, exactly as k = L - 1 does
+  // (steps of L/(k+1) <= 1 reach each integer), so cap the loop there
+  const int64_t kk = std::min<int64_t>(k, L - 1);
+  for (int64_t j = 1; j <= kk; ++j) {
+    const int64_t m = lo + j * L / (kk + 1);
+    if (m > lo && m < hi && (s.empty() || m > s.back())) s.push_back(int32_t(m));
+  }
+  return s;
 }
 
-uint64_t recursive_extra(int32_t n) {
-  if (n == 1) return rec_range(0, 1);
-  int32_t m = n / 2;
-  return rec_range(m, n) + rec_range(0, m);
+// unit forwards re-run for [a, b): the sweep up to the last split, then the
+// parts (a single unit: one re-forward)
+static uint64_t rec_range(int32_t a, int32_t b, int32_t k) {
+  if (b - a == 1) return 1;
+  const std::vector<int32_t> s = rec_splits(a, b, k);
+  uint64_t t = uint64_t(s.back() - a);
+  int32_t lo = a;
+  for (int32_t m : s) {
+    t += rec_range(lo, m, k);
+    lo = m;
+  }
+  return t + rec_range(lo, b, k);
+}
+
+uint64_t recursive_extra(int32_t n, int32_t k) {
+  if (n == 1) return rec_range(0, 1, k);
+  const std::vector<int32_t> s = rec_splits(0, n, k);
+  uint64_t t = 0;
+  int32_t lo = 0;
+  for (int32_t m : s) {
+    t += rec_range(lo, m, k);
+    lo = m;
+  }
+  return t + rec_range(lo, n, k);
 }
 
 static void xy_of_cuts(const uint64_t *lb, const uint64_t *cb, const std::vector<int32_t> &cuts,
@@ -120,8 +148,11 @@ Plan make_plan(int32_t n, const uint64_t *lb, const uint64_t *cb, uint64_t budge
         if (cb[i] == 0)
           fail(CKPT_E_UNSUPPORTED,
                "plan_checkpoints: the recursive schedule needs every boundary to be a candidate");
+      if (budget >= (uint64_t(1) << 31))
+        fail(CKPT_E_INVALID, "plan_checkpoints: the recursion fan-out must fit in 31 bits");
       p.keep_last = false;
-      p.extra = recursive_extra(n);
+      p.fanout = budget > 0 ? int32_t(budget) : 1;
+      p.extra = recursive_extra(n, p.fanout);
       return p;
     default:
       fail(CKPT_E_INVALID, "plan_checkpoints: unknown mode");
@@ -143,9 +174,10 @@ static void put64(std::vector<uint8_t> &v, uint64_t x) {
 
 std::vector<uint8_t> serialize(const Plan &p) {
   std::vector<uint8_t> v = {'C', 'K', 'P', 'L'};
-  put32(v, 1);
+  put32(v, 2);
   put32(v, uint32_t(p.mode));
   put32(v, p.keep_last ? 1u : 0u);
+  put32(v, uint32_t(p.fanout));
   put32(v, uint32_t(p.n));
   put32(v, uint32_t(p.cuts.size()));
   for (int32_t c : p.cuts) put32(v, uint32_t(c));
@@ -171,21 +203,33 @@ static uint64_t sweep_need(const std::vector<uint64_t> &b, const std::vector<uin
 
 struct RecState {
   const std::vector<uint64_t> &b, &a;
+  int32_t k;
   uint64_t arena = 0, stack = 0, stack_max = 0;
 };
 
+static void rec_account(RecState &st, int32_t lo, int32_t hi);
+
+// A forward sweep over [lo, last split) keeps every split boundary; the parts
+// are then handled last to first, each split boundary dropped after its part.
+static void rec_sweep_and_parts(RecState &st, int32_t lo, int32_t hi, int32_t sweep_hi) {
+  const std::vector<int32_t> s = rec_splits(lo, hi, st.k);
+  auto is_split_out = [&s](int32_t i) { return std::binary_search(s.begin(), s.end(), i + 1); };
+  st.arena = std::max(st.arena, sweep_need(st.b, st.a, lo, sweep_hi, is_split_out));
+  for (int32_t m : s) st.stack += st.b[size_t(m)];
+  st.stack_max = std::max(st.stack_max, st.stack);
+  for (size_t t = s.size() + 1; t-- > 0;) {
+    const int32_t p_lo = t == 0 ? lo : s[t - 1], p_hi = t == s.size() ? hi : s[t];
+    rec_account(st, p_lo, p_hi);
+    if (t > 0) st.stack -= st.b[size_t(s[t - 1])];
+  }
+}
+
 static void rec_account(RecState &st, int32_t lo, int32_t hi) {
   if (hi - lo == 1) {
-    st.arena = std::max(st.arena, st.a[lo] + st.b[lo + 1]);
+    st.arena = std::max(st.arena, st.a[size_t(lo)] + st.b[size_t(lo) + 1]);
     return;
   }
-  int32_t m = lo + (hi - lo) / 2;
-  st.arena = std::max(st.arena, sweep_need(st.b, st.a, lo, m, [m](int32_t i) { return i == m - 1; }));
-  st.stack += st.b[m];
-  st.stack_max = std::max(st.stack_max, st.stack);
-  rec_account(st, m, hi);
-  st.stack -= st.b[m];
-  rec_account(st, lo, m);
+  rec_sweep_and_parts(st, lo, hi, rec_splits(lo, hi, st.k).back());
 }
 
 Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vector<uint64_t> &a,
@@ -197,18 +241,12 @@ Accounting account(const Plan &p, const std::vector<uint64_t> &b, const std::vec
   for (int32_t i = 0; i < n; ++i) maxq = std::max(maxq, q[i]);
   acc.grad = 2 * (slot ? slot : maxb) + maxq + extra;
   if (p.mode == CKPT_RECURSIVE) {
-    RecState st{b, a};
+    RecState st{b, a, p.fanout};
     if (n == 1) {
       st.arena = sweep_need(b, a, 0, 1, [](int32_t) { return false; });
       rec_account(st, 0, 1);
     } else {
-      int32_t m = n / 2;
-      st.arena = sweep_need(b, a, 0, n, [m](int32_t i) { return i == m - 1; });
-      st.stack = b[m];
-      st.stack_max = st.stack;
-      rec_account(st, m, n);
-      st.stack = 0;
-      rec_account(st, 0, m);
+      rec_sweep_and_parts(st, 0, n, n);  // the first forward runs the whole chain
     }
     acc.ckpt = st.stack_max;
     acc.arena = st.arena;

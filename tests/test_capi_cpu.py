@@ -59,6 +59,9 @@ def test_planner_fuzz_matches_oracle():
                 _compare(n, lb, cb, budget, mode, flags=flags)
         if all(c > 0 for c in cb[:-1]):
             _compare(n, lb, cb, 0, PL.RECURSIVE)
+            if n < 2000:
+                for k in (2, 3, int(rng.integers(1, n + 3))):
+                    _compare(n, lb, cb, k, PL.RECURSIVE)
         cands = [i for i in range(n - 1) if cb[i] > 0]
         if cands:
             k = int(rng.integers(0, min(len(cands), 20) + 1))
@@ -70,6 +73,8 @@ def test_planner_edge_cases():
     _compare(1, [5], [0], 0, PL.SQRT)
     _compare(1, [5], [0], 0, PL.GREEDY)
     _compare(1, [5], [0], 0, PL.RECURSIVE)
+    _compare(1, [5], [0], 6, PL.RECURSIVE)
+    _compare(2, [5, 5], [3, 0], 9, PL.RECURSIVE)
     _compare(2, [5, 5], [0, 0], 0, PL.GREEDY)          # no candidates
     _compare(2, [0, 0], [3, 0], 0, PL.GREEDY)          # zero-size units never exceed B = 0
     _compare(7, [1] * 7, [1] * 6 + [0], 10 ** 12, PL.SQRT)
@@ -121,7 +126,8 @@ def test_net_tables_and_accounting_match_oracle(cfg):
     assert net.grad_bytes() == (slot, extra)
     n = st.n
     modes = [(PL.NONE, 0, 0), (PL.SQRT, 0, 0), (PL.SQRT, 8, PL.FLAG_KEEP_LAST),
-             (PL.GREEDY, sum(lb) // 10, 0), (PL.RECURSIVE, 0, 0)]
+             (PL.GREEDY, sum(lb) // 10, 0), (PL.RECURSIVE, 0, 0), (PL.RECURSIVE, 2, 0),
+             (PL.RECURSIVE, 5, 0)]
     for mode, budget, flags in modes:
         lp = _lib_plan(n, lb, cb, budget, mode, flags=flags)
         op = PL.plan(n, lb, cb, budget, mode, flags=flags)
@@ -247,4 +253,19 @@ def test_plan_search_errors():
     assert ei.value.code == K.E_INVALID
     with pytest.raises(K.CkptError) as ei:
         K.plan_search([1, 2], [1, 0], [1, 1, 1], [1, 1], [1, 1], flags=8)
+    assert ei.value.code == K.E_INVALID
+
+
+def test_recursive_fanout_huge_k_is_every_boundary():
+    """A fan-out beyond n - 1 splits the top level at every boundary (and the
+    library does not loop k times to find that out)."""
+    n = 50
+    lb, cb = [7] * n, [3] * (n - 1) + [0]
+    big = _lib_plan(n, lb, cb, (1 << 31) - 1, PL.RECURSIVE)
+    ref = PL.plan(n, lb, cb, n - 1, PL.RECURSIVE)
+    bb, rb = big.serialize(), ref.serialize()
+    assert bb[:16] == rb[:16] and bb[20:] == rb[20:]   # all but the fan-out field
+    assert big.info()["extra_unit_forwards"] == n
+    with pytest.raises(K.CkptError) as ei:
+        _lib_plan(n, lb, cb, 1 << 31, PL.RECURSIVE)
     assert ei.value.code == K.E_INVALID

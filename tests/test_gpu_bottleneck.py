@@ -94,6 +94,7 @@ def test_bottleneck_parity_all_modes(case):
     n = st.n
     modes = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
              ("greedy", PL.GREEDY, sum(lb) // 3, None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
+             ("recursive_k2", PL.RECURSIVE, 2, None, 0),
              ("user_keep", PL.USER, 0, [0], PL.FLAG_KEEP_LAST)]
     ref = None
     for name, mode, budget, user, flags in modes:

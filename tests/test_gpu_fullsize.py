@@ -15,7 +15,8 @@
   identity with the no-checkpoint run, exact peak, n + n(log2 n + 1)/2 unit
   forwards, loss within 1e-4; gradients by the same float32 band (a float32
   evaluation flips ~17 of its 2.7e8 ReLU decisions; 1.4e-2 on the tensors
-  next to a flip, 2.8e-5 in relative L2).
+  next to a flip, 2.8e-5 in relative L2).  With fan-out 3 (section 4.4's
+  k log_{k+1} n): bit identity, exact peak and the recursion's unit forwards.
 """
 import numpy as np
 import pytest
@@ -98,6 +99,15 @@ def test_mlp1024_recursive_full_size():
     _check_band(d, loss, g, "mlp1024")
 
 
+def test_mlp1024_recursive_fanout3_full_size():
+    cfg = synth.WORKLOADS["mlp1024"]
+    print("[full size] mlp1024 recursive plan, fan-out 3", flush=True)
+    # bit identity with the no-checkpoint run (whose gradients the fan-out 1
+    # test holds to the oracle), exact peak, the recursion's unit forwards
+    d, loss, g, stats = _run_pair(cfg, PL.RECURSIVE, 3)
+    assert stats["unit_forwards"] == d["structure"].n + PL.recursive_extra(1024, 3)
+
+
 def _identity_full(name, mode, budget, extra_forwards=None, budget_frac=None):
     import torch
     from paper_1604_06174_amd import ckpt as K
@@ -140,6 +150,10 @@ def test_lstm4096_full_size_identity():
 
 def test_lstm16384_recursive_full_size_identity():
     _identity_full("lstm16384", PL.RECURSIVE, 0, extra_forwards=122880)
+
+
+def test_lstm16384_recursive_fanout3_full_size_identity():
+    _identity_full("lstm16384", PL.RECURSIVE, 3, extra_forwards=PL.recursive_extra(16384, 3))
 
 
 def test_lstm_full_width_prefix_parity():

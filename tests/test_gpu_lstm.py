@@ -52,6 +52,7 @@ def test_lstm_step_parity_all_modes(case):
     modes = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
              ("stride2_keep", PL.SQRT, 2, None, PL.FLAG_KEEP_LAST),
              ("greedy", PL.GREEDY, sum(lb) // 3, None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
+             ("recursive_k3", PL.RECURSIVE, 3, None, 0),
              ("user", PL.USER, 0, [0, n - 2], 0)]
     ref = None
     for name, mode, budget, user, flags in modes:

@@ -31,7 +31,8 @@ def _modes(n, lb):
     out = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
            ("sqrt_keep", PL.SQRT, 0, None, PL.FLAG_KEEP_LAST),
            ("greedy", PL.GREEDY, sum(lb) // 5, None, 0),
-           ("recursive", PL.RECURSIVE, 0, None, 0)]
+           ("recursive", PL.RECURSIVE, 0, None, 0),
+           ("recursive_k3", PL.RECURSIVE, 3, None, 0)]
     if n > 3:
         out.append(("user", PL.USER, 0, [0, n // 2, n - 2], 0))
     return out

@@ -14,6 +14,12 @@
 * Recompute: one-level plans run exactly 2n unit forwards (one extra forward
   pass, section 4.3); the recursive plan runs n + n(log2 n + 1)/2 for powers of
   two.
+* Fan-out k (section 4.4, g(n) = k + g(n/(k+1))): for n = (k+1)^p on a uniform
+  chain the recursion stores k p boundaries at most (k log_{k+1} n), PEAK is
+  (k p + 6) b for p >= 2 and the extra unit forwards solve R(L) = L k/(k+1) + (k+1)
+  R(L/(k+1)), R(1) = 1, i.e. n (1 + (p - 1) k/(k+1)).  With k >= n - 1 the
+  top level stores every boundary: the accounting equals that of the
+  one-level plan cutting at every unit (a separate code path), for any sizes.
 * The per-unit byte tables agree with the nbytes of the tensors the float32
   oracle actually keeps.
 """
@@ -196,7 +202,7 @@ def test_serialize_layout():
     p = PL.plan(5, [10] * 5, [4, 4, 4, 4, 0], 2, PL.SQRT)
     blob = p.serialize()
     assert blob[:4] == b"CKPL"
-    assert len(blob) == 24 + 4 * len(p.cuts) + 24
+    assert len(blob) == 28 + 4 * len(p.cuts) + 24
     assert p.cuts == [1, 3]
 
 
@@ -268,3 +274,61 @@ def test_search_returns_lowest_exact_peak(seed):
     # never worse than the plain B0 run it refines
     b0 = math.isqrt(PL.greedy_alg3(lb, cb, 0)[1] * PL.greedy_alg3(lb, cb, 0)[2])
     assert peak <= peaks[b0]
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 7])
+def test_recursive_fanout_closed_forms(k):
+    bsz = 256
+    for p in range(1, 8):
+        n = (k + 1) ** p
+        if n > 40000:
+            break
+        b, a, q = _uniform(n, bsz)
+        lb, cb = _lc(b, a)
+        pl = PL.plan(n, lb, cb, k, PL.RECURSIVE)
+        assert pl.fanout == k
+        acc = PL.account(pl, b, a, q)
+        assert acc.ckpt == k * p * bsz, (k, p)
+        if p >= 2:  # some sweep then holds a unit's input, internals and output
+            assert acc.peak == (k * p + 6) * bsz, (k, p)
+        # n (1 + (p - 1) k / (k + 1)), exact in integers
+        assert pl.extra_forwards * (k + 1) == n * (k + 1 + (p - 1) * k), (k, p)
+
+
+def test_recursive_fanout_one_is_the_default():
+    n = 37
+    b, a, q = _uniform(n)
+    lb, cb = _lc(b, a)
+    p0 = PL.plan(n, lb, cb, 0, PL.RECURSIVE)
+    p1 = PL.plan(n, lb, cb, 1, PL.RECURSIVE)
+    assert p0.serialize() == p1.serialize() and p0.fanout == 1
+
+
+@pytest.mark.parametrize("n", [2, 3, 5, 9, 14])
+def test_recursive_wide_fanout_is_every_cut(n):
+    rng = np.random.default_rng(n)
+    for _ in range(5):
+        b = [int(v) for v in rng.integers(1, 1000, n + 1)]
+        a = [int(v) for v in rng.integers(0, 1000, n)]
+        q = [int(v) for v in rng.integers(0, 1000, n)]
+        lb, cb = _lc(b, a)
+        for k in (n - 1, n, 3 * n):
+            pr = PL.plan(n, lb, cb, k, PL.RECURSIVE)
+            assert PL.rec_splits(0, n, k) == list(range(1, n))
+            pu = PL.plan(n, lb, cb, 0, PL.USER, list(range(n - 1)))
+            ar, au = PL.account(pr, b, a, q), PL.account(pu, b, a, q)
+            assert (ar.ckpt, ar.arena, ar.grad) == (au.ckpt, au.arena, au.grad)
+            assert pr.extra_forwards == pu.extra_forwards == n
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 5])
+def test_rec_parts_cover_the_range(k):
+    for lo in range(0, 4):
+        for L in range(2, 40):
+            parts = PL.rec_parts(lo, lo + L, k)
+            assert parts[0][0] == lo and parts[-1][1] == lo + L
+            assert all(p < q for (p, q) in parts)
+            assert all(parts[t][1] == parts[t + 1][0] for t in range(len(parts) - 1))
+            assert len(parts) == min(k + 1, L)
+            sizes = [q - p for (p, q) in parts]
+            assert max(sizes) - min(sizes) <= 1

@@ -85,3 +85,29 @@ def test_sqrt_plan_on_cfg_shapes_accounting():
     assert (acc.ckpt, acc.arena, acc.grad) == (7 * 65536, 16 * 65536, 3 * 65536)
     none = PL.account(PL.plan(st.n, lb, cb, 0, PL.NONE), b, a, q)
     assert none.peak == 128 * 65536 + 3 * 65536
+
+
+@pytest.mark.parametrize("k", [2, 3, 5])
+def test_recursive_fanout_equals_full_storage(k):
+    """Section 4.4 with k splits per level: same bits as full storage, the
+    planner's unit-forward count, and k log_{k+1} n live boundaries at n = (k+1)^2."""
+    n = (k + 1) ** 2
+    cfg = dict(kind="mlp", depth=n, width=4, batch=2, seed=70 + k, w_var=0.1)
+    d = synth.make(cfg)
+    chain = nets.Chain(d["structure"], d["params"])
+    loss, grads = nets.full_storage_step(chain, d["input"], d["target"])
+    l3, g3, fwd, live = SCH.recursive_step(chain, d["input"], d["target"], k)
+    assert l3 == loss
+    _same(grads, g3)
+    p = PL.plan(n, [1] * n, [1] * (n - 1) + [0], k, PL.RECURSIVE)
+    assert fwd == n + p.extra_forwards
+    assert live == 2 * k
+    for name in ("lstm", "cnn", "bottleneck"):
+        d = synth.make(TINY[name])
+        chain = nets.Chain(d["structure"], d["params"])
+        loss, grads = nets.full_storage_step(chain, d["input"], d["target"])
+        l3, g3, fwd, _ = SCH.recursive_step(chain, d["input"], d["target"], k)
+        assert l3 == loss
+        _same(grads, g3)
+        m = chain.n
+        assert fwd == m + PL.plan(m, [1] * m, [1] * (m - 1) + [0], k, PL.RECURSIVE).extra_forwards

@@ -1,15 +1,23 @@
-// fp32 GEMM on CDNA4 matrix cores (v_mfma_f32_32x32x2f32 / 16x16x4f32).
+// fp32 GEMM on CDNA4 matrix cores (v_mfma_f32_32x32x2f32).
 //
 //   C[M,N] = epilogue( op(A)[M,K] * op(B)[K,N] )
 //   op(A)(m,k) = TA ? A[k*lda + m] : A[m*lda + k]
 //   op(B)(k,n) = TB ? B[n*ldb + k] : B[k*ldb + n]
 //
-// Block = 256 threads = 4 wavefronts in a 2x2 grid; each wavefront owns a
-// WT x WT output tile (WT = 32 -> one 32x32x2 MFMA accumulator, WT = 16 -> one
-// 16x16x4 accumulator); block tile (2 WT) x (2 WT), K staged through LDS in
-// slices of 16 with double buffering (global loads of slice k+1 are in flight
-// while slice k is multiplied).  Every output element is reduced over K in one
-// fixed order, so results do not depend on the launch or on buffer addresses.
+// Block = 256 threads = 4 wavefronts; each wavefront owns a 32 x 32 output
+// tile (one 32x32x2 accumulator, 16 floats per lane).  Two shapes:
+//   KS = 1  block tile 64 x 64, waves in a 2 x 2 grid, K slices of 32;
+//   KS = 4  block tile 32 x 32, the four waves split every K slice of 128
+//           into quarters and their accumulators are added in LDS in wave
+//           order ((w0 + w1) + w2) + w3 -- four times the waves for GEMMs
+//           whose output has few 64 x 64 tiles.
+// Operand slices are staged through LDS k-contiguous ([m][k] and [n][k],
+// rows padded by 4 floats), double-buffered, with the global loads of the
+// next two slices in flight during the current slice's MFMAs.  Within a
+// wave's 32-wide k range, MFMA j takes k = 16 h + j in lane half h (h = lane / 32) for both
+// operands -- a fixed permutation of the reduction, so each lane reads 16
+// consecutive floats (four 16-byte LDS reads) per operand.  Every output
+// element is reduced over K in one order fixed by the shape alone.
 //
 // Epilogues:
 //   STORE    C = acc
@@ -18,18 +26,14 @@
 //                                               requires !TA and K == N)
 #include <hip/hip_runtime.h>
 
-#include <type_traits>
-
 #include "kernels.h"
 
 namespace ckpt {
 
-typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int BK = 16;
 constexpr int PAD = 4;
 
 struct GemmArgs {
@@ -45,148 +49,199 @@ struct GemmArgs {
   const float *bias;  // MLPFWD
   float *Z;           // MLPFWD
   int ldz;
-  int vecA, vecB;  // float4 loads allowed (leading dims and bases 16-byte aligned)
 };
 
-// Load 4 consecutive elements of a row-major [rows, cols] matrix, zero outside.
-__device__ __forceinline__ void ld4(float r[4], const float *base, int row, int col, int rows,
-                                    int cols, int ld, int vec) {
-  if (vec && row < rows && col + 3 < cols) {
-    float4 v = *reinterpret_cast<const float4 *>(base + size_t(row) * ld + col);
-    r[0] = v.x; r[1] = v.y; r[2] = v.z; r[3] = v.w;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      r[j] = (row < rows && col + j < cols) ? base[size_t(row) * ld + col + j] : 0.f;
+// 4 consecutive elements of a row-major [rows, cols] matrix, zero outside.
+// Branch-free (an outside address is replaced by the base and the value by
+// zero), so the loads of a slice stay in flight together.  VEC: one 16-byte
+// load; needs ld and cols multiples of 4 and a 16-byte aligned base, so a
+// chunk is either wholly inside or wholly outside.
+template <bool VEC>
+__device__ __forceinline__ float4 ld4(const float *base, int row, int col, int rows, int cols,
+                                      int ld) {
+  if (VEC) {
+    const bool ok = row < rows && col < cols;
+    const float4 v = *reinterpret_cast<const float4 *>(ok ? base + size_t(row) * ld + col : base);
+    return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+  float r[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bool ok = row < rows && col + j < cols;
+    const float v = base[ok ? size_t(row) * ld + col + j : 0];
+    r[j] = ok ? v : 0.f;
+  }
+  return make_float4(r[0], r[1], r[2], r[3]);
 }
 
-template <int WT, bool TA, bool TB, int EPI>
+template <int KS, bool TA, bool TB, int EPI, bool VEC>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
-  constexpr int BMN = 2 * WT;                 // block tile side
-  constexpr int CH_A = BMN * BK / 4;          // float4 chunks per operand slice
-  __shared__ float As[2][BK][BMN + PAD];
-  __shared__ float Bs[2][BK][BMN + PAD];
+  constexpr int BM = KS == 1 ? 64 : 32, BN = BM;  // block tile
+  constexpr int BK = 32 * KS;                      // k slice
+  constexpr int LD = BK + PAD;                     // LDS row stride (floats)
+  constexpr int NCH = BM * BK / 4 / 256;           // float4 chunks per thread per operand
+  static_assert(NCH * 256 * 4 == BM * BK, "tile / thread mismatch");
+  __shared__ __attribute__((aligned(16))) float smem[2 * (BM + BN) * LD];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.y * BMN, n0 = blockIdx.x * BMN;
-  const int wm = (wave >> 1) * WT, wn = (wave & 1) * WT;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kw = KS == 1 ? 0 : wave;                         // k quarter of this wave
+  const int wm = KS == 1 ? (wave >> 1) * 32 : 0, wn = KS == 1 ? (wave & 1) * 32 : 0;
 
-  float ra[4], rb[4];
-  auto gload = [&](int k0) {
-    if (tid < CH_A) {
-      if (!TA) {  // A row-major [M,K]: chunk = 4 k's of one row
-        int mr = tid / (BK / 4), kc = (tid % (BK / 4)) * 4;
-        ld4(ra, p.A, m0 + mr, k0 + kc, p.M, p.K, p.lda, p.vecA);
-      } else {    // A stored [K,M]: chunk = 4 m's of one k
-        int kr = tid / (BMN / 4), mc = (tid % (BMN / 4)) * 4;
-        ld4(ra, p.A, k0 + kr, m0 + mc, p.K, p.M, p.lda, p.vecA);
+  auto gload = [&](float4 (&ra)[NCH], float4 (&rb)[NCH], int k0) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 256 * c;
+      if (!TA) {  // A row-major [M,K]: a chunk is 4 k's of one row
+        ra[c] = ld4<VEC>(p.A, m0 + ch / (BK / 4), k0 + (ch % (BK / 4)) * 4, p.M, p.K, p.lda);
+      } else {    // A stored [K,M]: a chunk is 4 m's of one k
+        ra[c] = ld4<VEC>(p.A, k0 + ch / (BM / 4), m0 + (ch % (BM / 4)) * 4, p.K, p.M, p.lda);
       }
-      if (!TB) {  // B row-major [K,N]
-        int kr = tid / (BMN / 4), nc = (tid % (BMN / 4)) * 4;
-        ld4(rb, p.B, k0 + kr, n0 + nc, p.K, p.N, p.ldb, p.vecB);
-      } else {    // B stored [N,K]
-        int nr = tid / (BK / 4), kc = (tid % (BK / 4)) * 4;
-        ld4(rb, p.B, n0 + nr, k0 + kc, p.N, p.K, p.ldb, p.vecB);
+      if (TB) {   // B stored [N,K]: 4 k's of one n
+        rb[c] = ld4<VEC>(p.B, n0 + ch / (BK / 4), k0 + (ch % (BK / 4)) * 4, p.N, p.K, p.ldb);
+      } else {    // B row-major [K,N]: 4 n's of one k
+        rb[c] = ld4<VEC>(p.B, k0 + ch / (BN / 4), n0 + (ch % (BN / 4)) * 4, p.K, p.N, p.ldb);
       }
     }
   };
-  auto sstore = [&](int buf) {
-    if (tid < CH_A) {
+  auto sstore = [&](const float4 (&ra)[NCH], const float4 (&rb)[NCH], int buf) {
+    float *As = smem + buf * (BM + BN) * LD, *Bs = As + BM * LD;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 256 * c;
       if (!TA) {
-        int mr = tid / (BK / 4), kc = (tid % (BK / 4)) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) As[buf][kc + j][mr] = ra[j];
+        *reinterpret_cast<float4 *>(As + (ch / (BK / 4)) * LD + (ch % (BK / 4)) * 4) = ra[c];
       } else {
-        int kr = tid / (BMN / 4), mc = (tid % (BMN / 4)) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) As[buf][kr][mc + j] = ra[j];
+        const int k = ch / (BM / 4), m = (ch % (BM / 4)) * 4;
+        As[(m + 0) * LD + k] = ra[c].x;
+        As[(m + 1) * LD + k] = ra[c].y;
+        As[(m + 2) * LD + k] = ra[c].z;
+        As[(m + 3) * LD + k] = ra[c].w;
       }
-      if (!TB) {
-        int kr = tid / (BMN / 4), nc = (tid % (BMN / 4)) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Bs[buf][kr][nc + j] = rb[j];
+      if (TB) {
+        *reinterpret_cast<float4 *>(Bs + (ch / (BK / 4)) * LD + (ch % (BK / 4)) * 4) = rb[c];
       } else {
-        int nr = tid / (BK / 4), kc = (tid % (BK / 4)) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Bs[buf][kc + j][nr] = rb[j];
+        const int k = ch / (BN / 4), n = (ch % (BN / 4)) * 4;
+        Bs[(n + 0) * LD + k] = rb[c].x;
+        Bs[(n + 1) * LD + k] = rb[c].y;
+        Bs[(n + 2) * LD + k] = rb[c].z;
+        Bs[(n + 3) * LD + k] = rb[c].w;
       }
     }
   };
 
-  using acc_t = typename std::conditional<WT == 32, floatx16, floatx4>::type;
-  acc_t acc;
+  floatx16 acc;
 #pragma unroll
-  for (int r = 0; r < (WT == 32 ? 16 : 4); ++r) acc[r] = 0.f;
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 
+  const int h = lane >> 5, l32 = lane & 31;
+  auto compute = [&](int buf) {
+    const float *As = smem + buf * (BM + BN) * LD, *Bs = As + BM * LD;
+    const float *pa = As + (wm + l32) * LD + kw * 32 + h * 16;
+    const float *pb = Bs + (wn + l32) * LD + kw * 32 + h * 16;
+    float4 a4[4], b4[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      a4[q] = *reinterpret_cast<const float4 *>(pa + 4 * q);
+      b4[q] = *reinterpret_cast<const float4 *>(pb + 4 * q);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q].x, b4[q].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q].y, b4[q].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q].z, b4[q].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q].w, b4[q].w, acc, 0, 0, 0);
+    }
+  };
+
+  // slices kt+1 and kt+2 are in flight in registers while slice kt is
+  // multiplied out of LDS buffer kt & 1
   const int nk = (p.K + BK - 1) / BK;
-  gload(0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    sstore(buf);
+  float4 ra0[NCH], rb0[NCH], ra1[NCH], rb1[NCH];
+  gload(ra0, rb0, 0);
+  if (nk > 1) gload(ra1, rb1, BK);
+  sstore(ra0, rb0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * BK);
+    compute(0);
+    if (kt + 1 < nk) sstore(ra1, rb1, 1);
     __syncthreads();
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    if constexpr (WT == 32) {
-#pragma unroll
-      for (int kk = 0; kk < BK; kk += 2) {
-        float a = As[buf][kk + (lane >> 5)][wm + (lane & 31)];
-        float b = Bs[buf][kk + (lane >> 5)][wn + (lane & 31)];
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < BK; kk += 4) {
-        float a = As[buf][kk + (lane >> 4)][wm + (lane & 15)];
-        float b = Bs[buf][kk + (lane >> 4)][wn + (lane & 15)];
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-      }
+    if (kt + 1 < nk) {
+      if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * BK);
+      compute(1);
+      if (kt + 2 < nk) sstore(ra0, rb0, 0);
+      __syncthreads();
     }
   }
 
-  // epilogue: accumulator register r of this lane holds element (row, col)
-#pragma unroll
-  for (int r = 0; r < (WT == 32 ? 16 : 4); ++r) {
-    int row, col;
-    if (WT == 32) {
-      row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      col = lane & 31;
-    } else {
-      row = 4 * (lane >> 4) + r;
-      col = lane & 15;
-    }
-    const int m = m0 + wm + row, n = n0 + wn + col;
+  // accumulator register r of a lane holds element (row, col) of its 32x32 tile
+  auto rc = [&](int r, int &row, int &col) {
+    row = 8 * (r >> 2) + 4 * h + (r & 3);
+    col = l32;
+  };
+  auto emit = [&](int m, int n, float v) {
     if (m < p.M && n < p.N) {
-      float v = acc[r];
       if (EPI == GEMM_EPI_STORE) {
         p.C[size_t(m) * p.ldc + n] = v;
       } else if (EPI == GEMM_EPI_ADD) {
         p.C[size_t(m) * p.ldc + n] = v + p.D[size_t(m) * p.ldd + n];
       } else {  // MLPFWD
-        float z = v + p.bias[n];
+        const float z = v + p.bias[n];
         p.Z[size_t(m) * p.ldz + n] = z;
         p.C[size_t(m) * p.ldc + n] = p.A[size_t(m) * p.lda + n] + fmaxf(z, 0.f);
       }
     }
+  };
+  if (KS == 1) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      int row, col;
+      rc(r, row, col);
+      emit(m0 + wm + row, n0 + wn + col, acc[r]);
+    }
+  } else {
+    // the four k quarters, added in wave order (the last loop iteration's
+    // barrier has retired every read of the staging buffers)
+    float *red = smem;  // [4][32][33]
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      int row, col;
+      rc(r, row, col);
+      red[(wave * 32 + row) * 33 + col] = acc[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = tid; e < 32 * 32; e += 256) {
+      const int row = e >> 5, col = e & 31;
+      const float v = ((red[row * 33 + col] + red[(32 + row) * 33 + col]) + red[(64 + row) * 33 + col]) +
+                      red[(96 + row) * 33 + col];
+      emit(m0 + row, n0 + col, v);
+    }
   }
 }
 
-template <int WT, bool TA, bool TB, int EPI>
-void launch(const GemmArgs &a, hipStream_t s) {
-  dim3 grid((a.N + 2 * WT - 1) / (2 * WT), (a.M + 2 * WT - 1) / (2 * WT));
-  hipLaunchKernelGGL((k_gemm_f32<WT, TA, TB, EPI>), grid, dim3(256), 0, s, a);
+template <int KS, bool TA, bool TB, int EPI>
+void launch(const GemmArgs &a, bool vec, hipStream_t s) {
+  constexpr int T = KS == 1 ? 64 : 32;
+  dim3 grid((a.N + T - 1) / T, (a.M + T - 1) / T);
+  if (vec)
+    hipLaunchKernelGGL((k_gemm_f32<KS, TA, TB, EPI, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemm_f32<KS, TA, TB, EPI, false>), grid, dim3(256), 0, s, a);
 }
 
-template <int WT>
-void dispatch(const GemmArgs &a, bool ta, bool tb, int epi, hipStream_t s) {
+template <int KS>
+void dispatch(const GemmArgs &a, bool ta, bool tb, int epi, bool vec, hipStream_t s) {
   if (epi == GEMM_EPI_MLPFWD) {
-    launch<WT, false, false, GEMM_EPI_MLPFWD>(a, s);
+    launch<KS, false, false, GEMM_EPI_MLPFWD>(a, vec, s);
     return;
   }
-#define CKPT_GEMM_CASE(TA_, TB_)                                        \
-  if (ta == TA_ && tb == TB_) {                                         \
-    if (epi == GEMM_EPI_STORE) launch<WT, TA_, TB_, GEMM_EPI_STORE>(a, s); \
-    else launch<WT, TA_, TB_, GEMM_EPI_ADD>(a, s);                       \
-    return;                                                             \
+#define CKPT_GEMM_CASE(TA_, TB_)                                               \
+  if (ta == TA_ && tb == TB_) {                                                \
+    if (epi == GEMM_EPI_STORE) launch<KS, TA_, TB_, GEMM_EPI_STORE>(a, vec, s); \
+    else launch<KS, TA_, TB_, GEMM_EPI_ADD>(a, vec, s);                         \
+    return;                                                                    \
   }
   CKPT_GEMM_CASE(false, false)
   CKPT_GEMM_CASE(false, true)
@@ -203,16 +258,18 @@ void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool 
               int ldb, bool tb, float *C, int ldc, int epi, const float *D, int ldd,
               const float *bias, float *Z, int ldz) {
   if (M <= 0 || N <= 0) return;
-  GemmArgs a{M, N, K, A, lda, B, ldb, C, ldc, D, ldd, bias, Z, ldz, 0, 0};
-  a.vecA = (lda % 4 == 0) && al16(A);
-  a.vecB = (ldb % 4 == 0) && al16(B);
-  // 64x64 block tiles when they alone give at least one block per compute
-  // unit; 32x32 tiles otherwise, so that small GEMMs still spread out.
-  long tiles64 = long((M + 63) / 64) * ((N + 63) / 64);
+  GemmArgs a{M, N, K, A, lda, B, ldb, C, ldc, D, ldd, bias, Z, ldz};
+  // 16-byte operand loads when every contiguous extent and leading dimension
+  // is a multiple of 4 floats and both bases are 16-byte aligned
+  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && al16(A) && al16(B) &&
+                   (ta ? M : K) % 4 == 0 && (tb ? K : N) % 4 == 0;
+  // 64x64 tiles when they alone give a block per compute unit; otherwise
+  // 32x32 tiles with the k range split over the block's four waves
+  const long tiles64 = long((M + 63) / 64) * ((N + 63) / 64);
   if (tiles64 >= 256)
-    dispatch<32>(a, ta, tb, epi, s);
+    dispatch<1>(a, ta, tb, epi, vec, s);
   else
-    dispatch<16>(a, ta, tb, epi, s);
+    dispatch<4>(a, ta, tb, epi, vec, s);
 }
 
 }  // namespace ckpt

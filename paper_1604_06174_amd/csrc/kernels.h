@@ -24,8 +24,11 @@ void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool 
 
 // Residual-MLP backward prologue: dr = g * [z > 0]; db[n] = sum_m dr[m, n]
 // (fixed summation order).  [rows, cols] row-major.
+// dr = g * [z > 0] and db = column sums of dr (rows in a fixed order); pdb is
+// workspace of mlp_relu_row_blocks(rows) * cols floats.
+int mlp_relu_row_blocks(int rows);
 void mlp_relu_bwd(hipStream_t s, int rows, int cols, const float *g, const float *z, float *dr,
-                  float *db);
+                  float *db, float *pdb);
 
 // Mean-squared-error head: loss_out[0] = sum((y-t)^2)/count, g = 2 (y-t)/count.
 void mse_head(hipStream_t s, int64_t count, const float *y, const float *t, float *g,

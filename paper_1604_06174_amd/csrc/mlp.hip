@@ -8,26 +8,57 @@
 namespace ckpt {
 namespace {
 
-// One block per 64 columns; 4 row groups per block.  dr = g * [z > 0];
-// db[n] = ((s0 + s1) + s2) + s3 where s_j sums rows j, j+4, ... in order.
+// Workgroup = 64 columns x 4 row groups over a block of 16 rows (blockIdx.y);
+// dr = g * [z > 0]; the workgroup's column sums over its rows, ((s0 + s1) +
+// s2) + s3 with s_j = rows j, j+4, .. in order, go to pdb[blockIdx.y][cols].
 __global__ __launch_bounds__(256) void k_mlp_relu_bwd(int rows, int cols, const float *__restrict__ g,
                                                       const float *__restrict__ z,
-                                                      float *__restrict__ dr, float *__restrict__ db) {
+                                                      float *__restrict__ dr, float *__restrict__ pdb) {
   __shared__ float part[4][64];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int n = blockIdx.x * 64 + tx;
+  const int n = blockIdx.x * 64 + tx, r0 = blockIdx.y * 16 + ty;
   float s = 0.f;
   if (n < cols) {
-    for (int m = ty; m < rows; m += 4) {
-      size_t i = size_t(m) * cols + n;
-      float v = z[i] > 0.f ? g[i] : 0.f;
-      dr[i] = v;
-      s += v;
+    float gv[4], zv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = r0 + 4 * i;
+      const size_t e = size_t(m < rows ? m : 0) * cols + n;
+      gv[i] = g[e];
+      zv[i] = z[e];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = r0 + 4 * i;
+      if (m < rows) {
+        const float v = zv[i] > 0.f ? gv[i] : 0.f;
+        dr[size_t(m) * cols + n] = v;
+        s += v;
+      }
     }
   }
   part[ty][tx] = s;
   __syncthreads();
-  if (ty == 0 && n < cols) db[n] = ((part[0][tx] + part[1][tx]) + part[2][tx]) + part[3][tx];
+  if (ty == 0 && n < cols)
+    pdb[size_t(blockIdx.y) * cols + n] = ((part[0][tx] + part[1][tx]) + part[2][tx]) + part[3][tx];
+}
+
+// db[n] = sum over r < R of pdb[r][n], in order of r
+__global__ __launch_bounds__(256) void k_colsum_rows(int R, int cols, const float *__restrict__ pdb,
+                                                     float *__restrict__ db) {
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= cols) return;
+  float s = 0.f;
+  int r = 0;
+  for (; r + 8 <= R; r += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = pdb[size_t(r + u) * cols + n];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += t[u];
+  }
+  for (; r < R; ++r) s += pdb[size_t(r) * cols + n];
+  db[n] = s;
 }
 
 // Single block of 1024 threads: thread t sums elements t, t+1024, ...; then a
@@ -56,9 +87,14 @@ __global__ void k_copy_scalar(const float *src, float *dst) { dst[0] = src[0]; }
 
 }  // namespace
 
+int mlp_relu_row_blocks(int rows) { return (rows + 15) / 16; }
+
 void mlp_relu_bwd(hipStream_t s, int rows, int cols, const float *g, const float *z, float *dr,
-                  float *db) {
-  hipLaunchKernelGGL(k_mlp_relu_bwd, dim3((cols + 63) / 64), dim3(256), 0, s, rows, cols, g, z, dr, db);
+                  float *db, float *pdb) {
+  const int R = mlp_relu_row_blocks(rows);
+  hipLaunchKernelGGL(k_mlp_relu_bwd, dim3((cols + 63) / 64, R), dim3(256), 0, s, rows, cols, g, z, dr,
+                     pdb);
+  hipLaunchKernelGGL(k_colsum_rows, dim3((cols + 255) / 256), dim3(256), 0, s, R, cols, pdb, db);
 }
 
 void mse_head(hipStream_t s, int64_t count, const float *y, const float *t, float *g, float *loss_out) {

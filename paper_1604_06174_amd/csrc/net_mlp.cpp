@@ -28,7 +28,8 @@ class MlpNet : public Net {
       wi.push_back(add_param("u" + std::to_string(i) + ".W", uint64_t(D) * D));
       bi.push_back(add_param("u" + std::to_string(i) + ".b", uint64_t(D)));
     }
-    ks_bytes = 256;  // loss scalar
+    // loss scalar | bias-gradient partial sums of the ReLU backward
+    ks_bytes = 256 + align256(uint64_t(mlp_relu_row_blocks(B)) * D * 4);
     timed_family = "k_gemm_f32";
   }
 
@@ -52,13 +53,14 @@ class MlpNet : public Net {
            void *q, StepCtx &c) override {
     const float *gp = static_cast<const float *>(g);
     float *dr = static_cast<float *>(q);
-    mlp_relu_bwd(c.s, B, D, gp, static_cast<const float *>(saved), dr, G(c, bi[i]));
+    mlp_relu_bwd(c.s, B, D, gp, static_cast<const float *>(saved), dr, G(c, bi[i]),
+                 reinterpret_cast<float *>(c.ks + 256));
     // dW = x^T dr : [D_in, D_out] = [D, B] x [B, D]
     timer.begin(c.s);
     gemm_f32(c.s, D, D, B, static_cast<const float *>(x), D, true, dr, D, false, G(c, wi[i]), D,
              GEMM_EPI_STORE);
     timer.end(c.s, gf(D, D, B), gb(D, D, B, 0));
-    c.launches += 2;
+    c.launches += 3;
     if (dx) {  // dx = g + dr W^T
       timer.begin(c.s);
       gemm_f32(c.s, B, D, D, dr, D, false, P(c, wi[i]), D, true, static_cast<float *>(dx), D,

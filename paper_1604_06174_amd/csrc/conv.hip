@@ -249,6 +249,9 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
 // c0 + 4q + u of both operands, so the 4 steps cover channels c0..c0+15.
 // Workgroup = RB output rows x BN output channels; each wavefront owns
 // RB*W/64 pixel tiles of 16 and all BN/16 channel tiles.
+template <int C, int J, int W, int S, int MODE, int RB, int BN>
+constexpr size_t spec_lds();
+
 template <int C, int J, int W, int S, int MODE, int EPI, int RB, int BN>
 __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
   constexpr int NS = BN / 16;
@@ -260,9 +263,9 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
   constexpr int HR = MODE == CONV_FWD ? (RB - 1) * S + 3 : RB + 2;
   constexpr int HC = MODE == CONV_FWD ? (W - 1) * S + 3 : W + 2;
   constexpr int WX = MODE == CONV_FWD ? W * S : W / S;  // input width
-  extern __shared__ __align__(16) float smem[];
+  __shared__ __align__(16) float smem[spec_lds<C, J, W, S, MODE, RB, BN>() / 4];
   float *halo = smem;
-  float *Bs = smem + HR * HC * Cs;  // [2][BN][Cs]
+  float *Ws = smem + HR * HC * Cs;  // all nine taps: [9][BN][Cs]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
   const int rblk = (a.H + RB - 1) / RB;
@@ -270,63 +273,98 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
   const int j0 = blockIdx.y * BN;
   const int Hx = a.Hx;
 
-  for (int e = tid; e < HR * HC * C4; e += 256) {
-    const int c4 = e % C4, hc = (e / C4) % HC, hr = e / (C4 * HC);
-    int ir, ic;
-    bool ok;
-    if (MODE == CONV_FWD) {
-      ir = r0 * S - 1 + hr;
-      ic = hc - 1;
-      ok = ir >= 0 && ir < Hx && ic >= 0 && ic < WX;
-    } else {
-      const int ur = r0 - 1 + hr, uc = hc - 1;
-      ir = ur / S;
-      ic = uc / S;
-      ok = ur >= 0 && uc >= 0 && (ur % S) == 0 && (uc % S) == 0 && ir < Hx && ic < WX;
+  // One load phase: the input halo and the weights of all nine taps are
+  // fetched together (every load issued before any is used; an outside
+  // address is replaced by the base and its value by zero), so the tap loop
+  // below runs out of LDS with no further waits.  256 is a multiple of C4,
+  // so a thread's halo chunks all hold channels 4 c4 .. 4 c4 + 3.
+  {
+    constexpr int HE = HR * HC * C4, NH = (HE + 255) / 256;
+    static_assert(256 % C4 == 0, "channel chunk per thread");
+    // weights: fwd Wt[j][tap][c] (float4 chunks of c), dgrad Wt[c][tap][j]
+    constexpr int WE = MODE == CONV_FWD ? 9 * BN * C4 : 9 * BN * C, NW = (WE + 255) / 256;
+    float4 hv[NH];
+    bool hok[NH];
+    float4 wq[MODE == CONV_FWD ? NW : 1];
+    float wsr[MODE == CONV_FWD ? 1 : NW];
+#pragma unroll
+    for (int k = 0; k < NH; ++k) {
+      const int e = tid + 256 * k;
+      const int c4 = e % C4, hc = (e / C4) % HC, hr = e / (C4 * HC);
+      int ir, ic;
+      bool ok;
+      if (MODE == CONV_FWD) {
+        ir = r0 * S - 1 + hr;
+        ic = hc - 1;
+        ok = ir >= 0 && ir < Hx && ic >= 0 && ic < WX;
+      } else {
+        const int ur = r0 - 1 + hr, uc = hc - 1;
+        ir = ur / S;
+        ic = uc / S;
+        ok = ur >= 0 && uc >= 0 && (ur % S) == 0 && (uc % S) == 0 && ir < Hx && ic < WX;
+      }
+      ok = ok && e < HE;
+      const float4 v = *reinterpret_cast<const float4 *>(
+          ok ? a.X + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4 : a.X);
+      hv[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+      hok[k] = ok;
     }
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (ok) {
-      v = *reinterpret_cast<const float4 *>(a.X + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4);
-      if (MODE == CONV_FWD && a.tst) v = bn_relu4(v, a.tst, a.tg, a.tb, 4 * c4, C);
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      const int e = tid + 256 * k;
+      if constexpr (MODE == CONV_FWD) {
+        const int jj = e / (9 * C4), tap = (e / C4) % 9, c4 = e % C4, j = j0 + jj;
+        const bool ok = e < WE && j < J;
+        const float4 v = *reinterpret_cast<const float4 *>(
+            ok ? a.Wt + (size_t(j) * 9 + tap) * C + 4 * c4 : a.Wt);
+        wq[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        const int c = e / (9 * BN), tap = (e / BN) % 9, jj = e % BN, j = j0 + jj;
+        const bool ok = e < WE && j < J;
+        const float v = a.Wt[ok ? (size_t(c) * 9 + tap) * J + j : 0];
+        wsr[k] = ok ? v : 0.f;
+      }
     }
-    *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + 4 * c4) = v;
+    if (MODE == CONV_FWD && a.tst) {  // relu(bn(.)) of the stored convolution output
+      const int c = 4 * (tid % C4);
+      float tm[4], tr[4], tg[4], tb[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        tm[u] = a.tst[c + u];
+        tr[u] = a.tst[C + c + u];
+        tg[u] = a.tg[c + u];
+        tb[u] = a.tb[c + u];
+      }
+#pragma unroll
+      for (int k = 0; k < NH; ++k)
+        if (hok[k])
+          hv[k] = make_float4(bn_relu(hv[k].x, tm[0], tr[0], tg[0], tb[0]),
+                              bn_relu(hv[k].y, tm[1], tr[1], tg[1], tb[1]),
+                              bn_relu(hv[k].z, tm[2], tr[2], tg[2], tb[2]),
+                              bn_relu(hv[k].w, tm[3], tr[3], tg[3], tb[3]));
+    }
+#pragma unroll
+    for (int k = 0; k < NH; ++k) {
+      const int e = tid + 256 * k;
+      if (e < HE) {
+        const int c4 = e % C4, hc = (e / C4) % HC, hr = e / (C4 * HC);
+        *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + 4 * c4) = hv[k];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      const int e = tid + 256 * k;
+      if (e < WE) {
+        if constexpr (MODE == CONV_FWD) {
+          const int jj = e / (9 * C4), tap = (e / C4) % 9, c4 = e % C4;
+          *reinterpret_cast<float4 *>(Ws + (tap * BN + jj) * Cs + 4 * c4) = wq[k];
+        } else {
+          const int c = e / (9 * BN), tap = (e / BN) % 9, jj = e % BN;
+          Ws[(tap * BN + jj) * Cs + c] = wsr[k];
+        }
+      }
+    }
   }
-
-  // weights of one tap into Bs[buf][jj][c]
-  constexpr int BE = MODE == CONV_FWD ? BN * C4 : BN * C;
-  constexpr int BPT = (BE + 255) / 256;
-  float4 bq[MODE == CONV_FWD ? BPT : 1];
-  float bsr[MODE == CONV_FWD ? 1 : BPT];
-  auto bload = [&](int tap) {
-#pragma unroll
-    for (int k = 0; k < BPT; ++k) {
-      const int e = tid + k * 256;
-      if constexpr (MODE == CONV_FWD) {
-        const int jj = e / C4, c4 = e % C4, j = j0 + jj;
-        bq[k] = (e < BE && j < J) ? *reinterpret_cast<const float4 *>(a.Wt + (size_t(j) * 9 + tap) * C + 4 * c4)
-                                  : make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {
-        const int c = e / BN, jj = e % BN, j = j0 + jj;
-        bsr[k] = (e < BE && j < J) ? a.Wt[(size_t(c) * 9 + tap) * J + j] : 0.f;
-      }
-    }
-  };
-  auto bstore = [&](int buf) {
-#pragma unroll
-    for (int k = 0; k < BPT; ++k) {
-      const int e = tid + k * 256;
-      if (e >= BE) continue;
-      if constexpr (MODE == CONV_FWD) {
-        const int jj = e / C4, c4 = e % C4;
-        *reinterpret_cast<float4 *>(Bs + (buf * BN + jj) * Cs + 4 * c4) = bq[k];
-      } else {
-        const int c = e / BN, jj = e % BN;
-        Bs[(buf * BN + jj) * Cs + c] = bsr[k];
-      }
-    }
-  };
-  bload(0);
-  bstore(0);
   __syncthreads();
 
   int pr[PSW], pc[PSW];
@@ -343,14 +381,13 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
     for (int t = 0; t < NS; ++t) acc[s][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   for (int tap = 0; tap < 9; ++tap) {
-    const int kh = tap / 3, kw = tap % 3, buf = tap & 1;
-    if (tap + 1 < 9) bload(tap + 1);
+    const int kh = tap / 3, kw = tap % 3;
     int hoff[PSW];
 #pragma unroll
     for (int s = 0; s < PSW; ++s)
       hoff[s] = MODE == CONV_FWD ? ((pr[s] * S + kh) * HC + pc[s] * S + kw) * Cs + 4 * q
                                  : ((pr[s] + 2 - kh) * HC + pc[s] + 2 - kw) * Cs + 4 * q;
-    const float *Bt = Bs + (buf * BN + i16) * Cs + 4 * q;
+    const float *Bt = Ws + (tap * BN + i16) * Cs + 4 * q;
 #pragma unroll
     for (int c0 = 0; c0 < C; c0 += 16) {
       float4 av[PSW], bv[NS];
@@ -368,10 +405,44 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
           acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].w, bv[t].w, acc[s][t], 0, 0, 0);
         }
     }
-    if (tap + 1 < 9) bstore(buf ^ 1);
-    __syncthreads();
   }
 
+  // epilogue operands (forward activations for the ReLU mask, the
+  // shortcut's input and mask) fetched for all of the lane's outputs before
+  // any is used; outside elements read the base and are never stored
+  float e0[PSW][4][NS], e1[PSW][4][NS];
+  if constexpr (EPI != CONV_EPI_STATS) {
+#pragma unroll
+    for (int s = 0; s < PSW; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int p = (wave * PSW + s) * 16 + 4 * q + r;
+        const int rr = p / W, cc = p % W, h = r0 + rr;
+#pragma unroll
+        for (int t = 0; t < NS; ++t) {
+          const int j = j0 + t * 16 + i16;
+          bool ok = h < a.H && j < J;
+          size_t o = ((size_t(n) * a.H + h) * W + cc) * J + j;
+          if (EPI == CONV_EPI_SC2) {
+            ok = ok && ((h | cc) & 1) == 0;
+            o = ((size_t(n) * a.Eh + (h >> 1)) * a.Ew + (cc >> 1)) * a.Ec + j;
+          }
+          e0[s][r][t] = a.E0[ok ? o : 0];
+          if (EPI != CONV_EPI_MASK) e1[s][r][t] = a.E1[ok ? o : 0];
+        }
+      }
+  }
+  float tm[NS], tr[NS], tg[NS], tb[NS];
+  if (EPI == CONV_EPI_MASK && a.tst) {
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      const int j = j0 + t * 16 + i16, jc = j < J ? j : 0;
+      tm[t] = a.tst[jc];
+      tr[t] = a.tst[a.J + jc];
+      tg[t] = a.tg[jc];
+      tb[t] = a.tb[jc];
+    }
+  }
   double s1[NS], s2[NS];
 #pragma unroll
   for (int t = 0; t < NS; ++t) s1[t] = s2[t] = 0.0;
@@ -393,15 +464,12 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
           s1[t] += double(v);
           s2[t] += double(v) * double(v);
         } else if (EPI == CONV_EPI_MASK) {
-          const float e = a.tst ? bn_relu(a.E0[o], a.tst[j], a.tst[a.J + j], a.tg[j], a.tb[j]) : a.E0[o];
+          const float e = a.tst ? bn_relu(e0[s][r][t], tm[t], tr[t], tg[t], tb[t]) : e0[s][r][t];
           v = e > 0.f ? v : 0.f;
         } else if (EPI == CONV_EPI_SC1) {
-          v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
+          v += e1[s][r][t] > 0.f ? e0[s][r][t] : 0.f;
         } else if (EPI == CONV_EPI_SC2) {
-          if (((h | cc) & 1) == 0) {
-            const size_t o2 = ((size_t(n) * a.Eh + (h >> 1)) * a.Ew + (cc >> 1)) * a.Ec + j;
-            v += a.E1[o2] > 0.f ? a.E0[o2] : 0.f;
-          }
+          if (((h | cc) & 1) == 0) v += e1[s][r][t] > 0.f ? e0[s][r][t] : 0.f;
         }
         a.Y[o] = v;
       }
@@ -430,7 +498,7 @@ constexpr size_t spec_lds() {
   constexpr int Cs = C + 4;
   constexpr int HR = MODE == CONV_FWD ? (RB - 1) * S + 3 : RB + 2;
   constexpr int HC = MODE == CONV_FWD ? (W - 1) * S + 3 : W + 2;
-  constexpr size_t st = size_t(HR * HC * Cs + 2 * BN * Cs) * 4;
+  constexpr size_t st = size_t(HR * HC * Cs + 9 * BN * Cs) * 4;
   constexpr size_t red = size_t(16) * 2 * BN * 8;
   return st > red ? st : red;
 }
@@ -444,12 +512,11 @@ template <int C, int J, int W, int S, int MODE, int EPI, int RB, int BN>
 bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
   if (mode != MODE || s != S || epi != EPI || a.C != C || a.J != J || a.W != W) return false;
   if (a.Wx != (MODE == CONV_FWD ? W * S : W / S)) return false;
-  static_assert(spec_lds<C, J, W, S, MODE, RB, BN>() <= 64 * 1024, "LDS");
+  static_assert(spec_lds<C, J, W, S, MODE, RB, BN>() <= 96 * 1024, "LDS");
   if (u) *u = {RB, BN};
   if (launch) {
     dim3 grid(a.N * ((a.H + RB - 1) / RB), (J + BN - 1) / BN);
-    constexpr size_t lds = spec_lds<C, J, W, S, MODE, RB, BN>();
-    hipLaunchKernelGGL((k_conv3x3s<C, J, W, S, MODE, EPI, RB, BN>), grid, dim3(256), lds, st, a);
+    hipLaunchKernelGGL((k_conv3x3s<C, J, W, S, MODE, EPI, RB, BN>), grid, dim3(256), 0, st, a);
   }
   return true;
 }

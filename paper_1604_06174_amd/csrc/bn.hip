@@ -91,7 +91,22 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ 
   __shared__ double r0[256], r1[256];
   const int j = blockIdx.x;
   double a = 0, b = 0;
-  for (int k = threadIdx.x; k < nb; k += 256) {
+  // k = tid, tid + 256, ... in order; four partials in flight per round
+  int k = threadIdx.x;
+  for (; k + 3 * 256 < nb; k += 4 * 256) {
+    double ta[4], tb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      ta[u] = part[(size_t(k + 256 * u) * 2 + 0) * J + j];
+      tb[u] = part[(size_t(k + 256 * u) * 2 + 1) * J + j];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      a += ta[u];
+      b += tb[u];
+    }
+  }
+  for (; k < nb; k += 256) {
     a += part[(size_t(k) * 2 + 0) * J + j];
     b += part[(size_t(k) * 2 + 1) * J + j];
   }

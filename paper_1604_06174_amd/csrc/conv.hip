@@ -903,8 +903,18 @@ __global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ 
   const int ex = threadIdx.x % ES, sl = threadIdx.x / ES;
   const int e = blockIdx.x * ES + ex;
   float s = 0.f;
-  if (e < E)
-    for (int b = sl; b < nb; b += SL) s += part[size_t(b) * E + e];
+  if (e < E) {
+    // b = sl, sl + SL, ... in order; sixteen loads in flight per round
+    int b = sl;
+    for (; b + 15 * SL < nb; b += 16 * SL) {
+      float t[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) t[u] = part[size_t(b + u * SL) * E + e];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) s += t[u];
+    }
+    for (; b < nb; b += SL) s += part[size_t(b) * E + e];
+  }
   red[sl][ex] = s;
   __syncthreads();
   if (sl == 0 && e < E) {

@@ -895,13 +895,21 @@ bool wgs_dispatch(const WgArgs &a, hipStream_t st, bool launch, WgUse *u) {
 // out[e] = sum over b of part[b][e], b in a fixed order: SL slices of b
 // (slice k takes b = k, k + SL, ...), then the slices in order.  A workgroup
 // covers 256 / SL consecutive e; SL = 64 for small E, 16 otherwise.
+// Workgroups are dispatched to the eight XCDs (each with its own L2) in
+// turn; consecutive column groups are mapped to one XCD so that the cache
+// lines they share are fetched from HBM once, not once per XCD.
+__device__ __forceinline__ int xcd_grouped(int id, int G) {
+  const int q = G / 8, r = G % 8, x = id % 8, k = id / 8;
+  return x * q + (x < r ? x : r) + k;
+}
+
 template <int SL>
 __global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ part, int nb,
                                                       int E, float *__restrict__ out) {
   constexpr int ES = 256 / SL;
   __shared__ float red[SL][ES];
   const int ex = threadIdx.x % ES, sl = threadIdx.x / ES;
-  const int e = blockIdx.x * ES + ex;
+  const int e = xcd_grouped(blockIdx.x, gridDim.x) * ES + ex;
   float s = 0.f;
   if (e < E) {
     // b = sl, sl + SL, ... in order; sixteen loads in flight per round

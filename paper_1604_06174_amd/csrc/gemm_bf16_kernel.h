@@ -35,7 +35,7 @@
 // ADDMASK C = acc + (Ym > 0 ? D : 0) with Ym bf16 shaped like D;
 // BF16STATS Cb = bf16(acc) and, per workgroup row of tiles, float64 sums of
 // the rounded values and their squares per column (batch-norm statistics:
-// stats[blockIdx.y][2][N]).  Split-K (gridDim.z > 1): workgroup z reduces the
+// stats[m tile][2][N]).  Split-K (gridDim.z > 1): workgroup z reduces the
 // k range [z*kper, (z+1)*kper) and stores its partial product to
 // C + z*M*ldc (STORE only); the partials are then added in z order.
 #pragma once
@@ -238,8 +238,23 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kbeg = blockIdx.z * p.kper;
+  // Workgroups go to the eight XCDs (one L2 each) in turn; the linear
+  // workgroup id is remapped so that each XCD takes a contiguous run of
+  // tiles (n fastest, then m, then the k split): the n tiles of one m tile,
+  // and neighbouring m tiles whose gathers share input rows, read their
+  // operands through one L2.
+  int tn, tm, tz;
+  {
+    const int G = gridDim.x * gridDim.y * gridDim.z;
+    const int id = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int q8 = G / 8, r8 = G % 8, x8 = id % 8;
+    const int L = x8 * q8 + (x8 < r8 ? x8 : r8) + id / 8;
+    tn = L % gridDim.x;
+    tm = (L / gridDim.x) % gridDim.y;
+    tz = L / (gridDim.x * gridDim.y);
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = tz * p.kper;
   const int kend = min(p.K, kbeg + p.kper);
   const int wm = (wave / WN) * (BM / WM), wn = (wave % WN) * (BN / WN);
   const TA *A = static_cast<const TA *>(p.A);
@@ -416,7 +431,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       const int which = tid / BN, col = tid % BN;
       double t = 0.0;
       for (int k = 0; k < WM * 4; ++k) t += red[(k * 2 + which) * BN + col];
-      if (n0 + col < p.N) p.stats[(size_t(blockIdx.y) * 2 + which) * p.N + n0 + col] = t;
+      if (n0 + col < p.N) p.stats[(size_t(tm) * 2 + which) * p.N + n0 + col] = t;
     }
   }
 
@@ -424,7 +439,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   // tile at a time, then writes whole rows with 16-byte stores (and reads D
   // and the mask the same way).
   float *stage = reinterpret_cast<float *>(smA) + wave * 16 * SP;
-  float *Cz = p.C + size_t(blockIdx.z) * p.M * p.ldc;
+  float *Cz = p.C + size_t(tz) * p.M * p.ldc;
   constexpr int VEC = EPI == GEMM_EPI_BF16STATS ? 8 : 4;  // output elements per lane
   constexpr int LPR = WC / VEC;                           // lanes per row
   constexpr int RPP = 64 / LPR;                           // rows per pass

@@ -4,7 +4,8 @@
 
 Every source under csrc/ is compiled with hipcc for gfx950 and linked into
 paper_1604_06174_amd/libckpt.so.  Packed-fp32 instructions are disabled for
-all device code.
+all device code.  probes/peaks.hip (the attainable-peak measurement quoted
+next to the roofline fractions) is built into probes/peaks.
 """
 from __future__ import annotations
 
@@ -56,6 +57,13 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, OUT)
+    probe = os.path.join(HERE, "probes", "peaks")
+    cmd = [HIPCC, "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-Xclang", "-target-feature",
+           "-Xclang", "-packed-fp32-ops", "-o", probe + ".tmp", probe + ".hip"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on probes/peaks.hip:\n{r.stdout}\n{r.stderr}")
+    os.replace(probe + ".tmp", probe)
     return OUT
 
 

@@ -139,6 +139,77 @@ int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *c
                 uint64_t grad_extra, int32_t flags, ckpt_plan **out, uint64_t *budget,
                 uint64_t *peak);
 
+/* ---- gradient graphs with mirror nodes (Alg. 2) and the static allocator
+ *      of section 3 (liveness counters, in-place writes, memory sharing) ---- */
+#define CKPT_NODE_INPLACE  1 /* the operator may write its output over its first input */
+#define CKPT_NODE_GRAD_OUT 2 /* its backward reads the node's own output               */
+#define CKPT_NODE_GRAD_IN  4 /* its backward reads the node's inputs                   */
+
+#define CKPT_ALLOC_NONE    0 /* every output its own memory                           */
+#define CKPT_ALLOC_INPLACE 1 /* + in-place writes over a dead first input              */
+#define CKPT_ALLOC_SHARE   2 /* + sharing: dead outputs' memory recycled               */
+
+#define CKPT_GNODE_FORWARD 0 /* kinds of the nodes of a planned gradient graph          */
+#define CKPT_GNODE_MIRROR  1
+#define CKPT_GNODE_GRAD    2
+
+typedef struct ckpt_graph_plan ckpt_graph_plan;
+
+/*
+ * graph_plan -- Alg. 2's gradient-graph construction followed by section 3's
+ * static memory allocation, for a forward computation graph at any
+ * granularity.
+ *   n_nodes    forward nodes (> 0), listed in a topological order.
+ *   pred_ptr   host [n_nodes + 1]: CSR offsets into pred_idx (pred_ptr[0] = 0,
+ *              non-decreasing).
+ *   pred_idx   host [pred_ptr[n_nodes]]: the inputs of node v are
+ *              pred_idx[pred_ptr[v] .. pred_ptr[v+1]), each < v.
+ *   out_bytes  host [n_nodes]: bytes of each node's output.
+ *   flags      host [n_nodes]: CKPT_NODE_* bits -- in-place capability and the
+ *              minimum dependencies of the node's backward (section 3).
+ *   mirror     host [n_nodes] or null (all 0): Alg. 2's m(v) >= 0, how many
+ *              times v is recomputed for the backward pass (0: its output is
+ *              kept); ignored for nodes without inputs.
+ *   strategy   CKPT_ALLOC_*.
+ * Construction: round k = 1 .. max m mirrors, in topological order, every v
+ * with m(v) >= k on top of the current mirrors of its inputs.  The execution
+ * order is the forward graph, then for v from last to first the not yet
+ * scheduled ancestors of v's gradient node (in creation order) and the
+ * gradient node, which reads the successors' gradient nodes, v's (latest)
+ * output if CKPT_NODE_GRAD_OUT and its inputs' if CKPT_NODE_GRAD_IN, and
+ * produces the gradients of v's inputs (the sum of their bytes).
+ * Allocation: one pass over that order with a liveness counter per output;
+ * an in-place node whose first input's counter is 1 reuses that input's
+ * memory (strategies INPLACE, SHARE); under SHARE an output whose counter
+ * reaches 0 returns its memory to a pool, from which a new output takes the
+ * smallest block that fits (lowest id on ties).  The peak is the total of
+ * the memory blocks assigned before execution.
+ *   out        receives the plan (free with graph_plan_free).
+ * Errors: CKPT_E_INVALID for n_nodes <= 0, null arrays, an input that is not
+ *   an earlier node, negative mirror counts, unknown flags or strategy.
+ */
+int graph_plan(int32_t n_nodes, const int32_t *pred_ptr, const int32_t *pred_idx,
+               const uint64_t *out_bytes, const int32_t *flags, const int32_t *mirror,
+               int32_t strategy, ckpt_graph_plan **out);
+
+/* graph_plan_info -- nodes executed (forward, mirror and gradient), mirror
+ * nodes executed, memory blocks and the peak bytes.  Outputs nullable. */
+int graph_plan_info(const ckpt_graph_plan *plan, int32_t *n_exec, int32_t *n_mirror,
+                    int32_t *n_blocks, uint64_t *peak_bytes);
+
+/* graph_plan_schedule -- the execution order, one entry per executed node:
+ * kind (CKPT_GNODE_*), the forward node it derives from, and the memory block
+ * its output uses (-1: no output).  Host arrays of cap entries (each may be
+ * null); *n_exec gets the full count (the copy is truncated to cap). */
+int graph_plan_schedule(const ckpt_graph_plan *plan, int32_t *kind, int32_t *of, int32_t *block,
+                        int32_t cap, int32_t *n_exec);
+
+/* graph_plan_blocks -- bytes of each memory block, host [cap]; *n_blocks gets
+ * the full count. */
+int graph_plan_blocks(const ckpt_graph_plan *plan, uint64_t *bytes, int32_t cap, int32_t *n_blocks);
+
+void graph_plan_free(ckpt_graph_plan *plan);
+
 /* ---- networks --------------------------------------------------------- */
 #define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
 #define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */

@@ -83,6 +83,12 @@ _sig("plan_serialize", C.c_int, [C.c_void_p, C.POINTER(C.c_uint8), C.c_uint64, _
 _sig("plan_free", None, [C.c_void_p])
 _sig("plan_search", C.c_int, [C.c_int32, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_uint64, C.c_uint64,
                               C.c_int32, C.POINTER(C.c_void_p), _u64p, _u64p])
+_sig("graph_plan", C.c_int, [C.c_int32, _i32p, _i32p, _u64p, _i32p, _i32p, C.c_int32,
+                             C.POINTER(C.c_void_p)])
+_sig("graph_plan_info", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, _u64p])
+_sig("graph_plan_schedule", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, C.c_int32, _i32p])
+_sig("graph_plan_blocks", C.c_int, [C.c_void_p, _u64p, C.c_int32, _i32p])
+_sig("graph_plan_free", None, [C.c_void_p])
 _sig("net_create", C.c_int, [C.POINTER(NetDesc), C.POINTER(C.c_void_p)])
 _sig("net_destroy", None, [C.c_void_p])
 _sig("net_units", C.c_int, [C.c_void_p, _i32p])
@@ -102,7 +108,8 @@ _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch
                              C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
 
 EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
-            "plan_free", "plan_search", "net_create", "net_destroy", "net_units", "net_unit_sizes",
+            "plan_free", "plan_search", "graph_plan", "graph_plan_info", "graph_plan_schedule",
+            "graph_plan_blocks", "graph_plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
             "train_step"]
@@ -181,6 +188,62 @@ def plan_checkpoints(layer_bytes: Sequence[int], cut_bytes: Sequence[int], budge
                                  ucarr if user_cuts is not None else None, len(uc), flags,
                                  C.byref(h)))
     return Plan(h.value)
+
+
+# --------------------------------------------------------------- graphs --
+NODE_INPLACE, NODE_GRAD_OUT, NODE_GRAD_IN = 1, 2, 4
+ALLOC_NONE, ALLOC_INPLACE, ALLOC_SHARE = 0, 1, 2
+GNODE_FORWARD, GNODE_MIRROR, GNODE_GRAD = 0, 1, 2
+
+
+class GraphPlan:
+    """Owner of a library gradient-graph plan (Alg. 2 + the section-3 allocator)."""
+
+    def __init__(self, handle: int):
+        self._h = C.c_void_p(handle)
+
+    def info(self) -> Dict[str, int]:
+        ne, nm, nb, pk = C.c_int32(), C.c_int32(), C.c_int32(), C.c_uint64()
+        _check(_lib.graph_plan_info(self._h, C.byref(ne), C.byref(nm), C.byref(nb), C.byref(pk)))
+        return dict(n_exec=ne.value, n_mirror=nm.value, n_blocks=nb.value, peak=pk.value)
+
+    def schedule(self):
+        """[(kind, forward node, memory block)] in execution order."""
+        n = C.c_int32()
+        _check(_lib.graph_plan_schedule(self._h, None, None, None, 0, C.byref(n)))
+        k, o, b = [(C.c_int32 * max(1, n.value))() for _ in range(3)]
+        _check(_lib.graph_plan_schedule(self._h, k, o, b, n.value, C.byref(n)))
+        return list(zip(k[:n.value], o[:n.value], b[:n.value]))
+
+    def blocks(self) -> List[int]:
+        n = C.c_int32()
+        _check(_lib.graph_plan_blocks(self._h, None, 0, C.byref(n)))
+        buf = (C.c_uint64 * max(1, n.value))()
+        _check(_lib.graph_plan_blocks(self._h, buf, n.value, C.byref(n)))
+        return list(buf[:n.value])
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:
+            _lib.graph_plan_free(self._h)
+            self._h = None
+
+
+def graph_plan(pred: Sequence[Sequence[int]], out_bytes: Sequence[int], flags: Sequence[int],
+               mirror: Optional[Sequence[int]] = None, strategy: int = ALLOC_SHARE,
+               n_nodes: Optional[int] = None) -> GraphPlan:
+    n = len(pred) if n_nodes is None else n_nodes
+    ptr = [0]
+    idx: List[int] = []
+    for p in pred:
+        idx.extend(int(u) for u in p)
+        ptr.append(len(idx))
+    ptr_a = (C.c_int32 * len(ptr))(*ptr)
+    idx_a = (C.c_int32 * max(1, len(idx)))(*idx)
+    fl = (C.c_int32 * max(1, len(flags)))(*[int(f) for f in flags])
+    mi = None if mirror is None else (C.c_int32 * max(1, len(mirror)))(*[int(m) for m in mirror])
+    h = C.c_void_p()
+    _check(_lib.graph_plan(n, ptr_a, idx_a, _u64arr(out_bytes), fl, mi, strategy, C.byref(h)))
+    return GraphPlan(h.value)
 
 
 # ----------------------------------------------------------------- nets --

@@ -3,6 +3,7 @@
 // argument has been checked.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 #include <memory>
 
@@ -13,6 +14,9 @@ struct ckpt_plan {
 };
 struct ckpt_net {
   std::unique_ptr<ckpt::Net> net;
+};
+struct ckpt_graph_plan {
+  ckpt::GraphPlan p;
 };
 
 namespace ckpt {
@@ -122,6 +126,59 @@ int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *c
     *out = p.release();
   });
 }
+
+int graph_plan(int32_t n_nodes, const int32_t *pred_ptr, const int32_t *pred_idx,
+               const uint64_t *out_bytes, const int32_t *flags, const int32_t *mirror,
+               int32_t strategy, ckpt_graph_plan **out) {
+  return guarded([&] {
+    need(out, "graph_plan(out)");
+    *out = nullptr;
+    auto p = std::make_unique<ckpt_graph_plan>();
+    p->p = ckpt::make_graph_plan(n_nodes, pred_ptr, pred_idx, out_bytes, flags, mirror, strategy);
+    *out = p.release();
+  });
+}
+
+int graph_plan_info(const ckpt_graph_plan *plan, int32_t *n_exec, int32_t *n_mirror,
+                    int32_t *n_blocks, uint64_t *peak_bytes) {
+  return guarded([&] {
+    need(plan, "graph_plan_info");
+    if (n_exec) *n_exec = int32_t(plan->p.order.size());
+    if (n_mirror) *n_mirror = plan->p.n_mirror;
+    if (n_blocks) *n_blocks = int32_t(plan->p.tag_bytes.size());
+    if (peak_bytes) *peak_bytes = plan->p.peak;
+  });
+}
+
+int graph_plan_schedule(const ckpt_graph_plan *plan, int32_t *kind, int32_t *of, int32_t *block,
+                        int32_t cap, int32_t *n_exec) {
+  return guarded([&] {
+    need(plan, "graph_plan_schedule");
+    if (cap < 0) ckpt::fail(CKPT_E_INVALID, "graph_plan_schedule: negative cap");
+    const auto &p = plan->p;
+    if (n_exec) *n_exec = int32_t(p.order.size());
+    const size_t k = std::min(size_t(cap), p.order.size());
+    for (size_t i = 0; i < k; ++i) {
+      const int32_t w = p.order[i];
+      if (kind) kind[i] = p.nodes[size_t(w)].kind;
+      if (of) of[i] = p.nodes[size_t(w)].of;
+      if (block) block[i] = p.tag_of[size_t(w)];
+    }
+  });
+}
+
+int graph_plan_blocks(const ckpt_graph_plan *plan, uint64_t *bytes, int32_t cap, int32_t *n_blocks) {
+  return guarded([&] {
+    need(plan, "graph_plan_blocks");
+    if (cap < 0) ckpt::fail(CKPT_E_INVALID, "graph_plan_blocks: negative cap");
+    const auto &tb = plan->p.tag_bytes;
+    if (n_blocks) *n_blocks = int32_t(tb.size());
+    if (bytes)
+      for (size_t i = 0; i < std::min(size_t(cap), tb.size()); ++i) bytes[i] = tb[i];
+  });
+}
+
+void graph_plan_free(ckpt_graph_plan *plan) { delete plan; }
 
 int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
   return guarded([&] {

@@ -68,4 +68,24 @@ Plan search_plan(int32_t n, const uint64_t *lb, const uint64_t *cb, const std::v
                  const std::vector<uint64_t> &a, const std::vector<uint64_t> &q, uint64_t slot,
                  uint64_t extra, int32_t flags, uint64_t *budget, uint64_t *peak);
 
+// ------------------------------------------------------ gradient graphs --
+struct GraphNode {
+  int32_t kind, of;              // CKPT_GNODE_*, the forward node it derives from
+  std::vector<int32_t> inputs;   // node ids it reads
+  uint64_t bytes;                // output bytes
+  bool inplace;
+};
+struct GraphPlan {
+  std::vector<GraphNode> nodes;
+  std::vector<int32_t> order;    // execution order
+  std::vector<int32_t> tag_of;   // node id -> memory block (-1: none)
+  std::vector<uint64_t> tag_bytes;
+  uint64_t peak = 0;
+  int32_t n_mirror = 0;
+};
+// Alg. 2 and the section-3 allocator (graph.cpp)
+GraphPlan make_graph_plan(int32_t n, const int32_t *pred_ptr, const int32_t *pred_idx,
+                          const uint64_t *out_bytes, const int32_t *flags, const int32_t *mirror,
+                          int32_t strategy);
+
 }  // namespace ckpt

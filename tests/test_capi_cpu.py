@@ -269,3 +269,54 @@ def test_recursive_fanout_huge_k_is_every_boundary():
     with pytest.raises(K.CkptError) as ei:
         _lib_plan(n, lb, cb, 1 << 31, PL.RECURSIVE)
     assert ei.value.code == K.E_INVALID
+
+
+# ---------------------------------------------------------------- graphs --
+from oracle import graph as OG  # noqa: E402
+from synth import graphs as SG  # noqa: E402
+
+
+def _graph_same(pred, ob, fl, mi, strategy):
+    op = OG.plan(pred, ob, fl, mi, strategy)
+    lp = K.graph_plan(pred, ob, fl, mi, strategy)
+    sch = lp.schedule()
+    want = [(op.nodes[w].kind, op.nodes[w].of, op.tag_of[w]) for w in op.order]
+    assert sch == want
+    assert lp.blocks() == op.tag_bytes
+    info = lp.info()
+    assert (info["peak"], info["n_mirror"], info["n_exec"], info["n_blocks"]) == \
+        (op.peak, op.n_mirror, len(op.order), len(op.tag_bytes))
+    return op
+
+
+def test_graph_plan_fuzz_matches_oracle():
+    import test_oracle_graph as T
+    rng = np.random.default_rng(5)
+    for _ in range(150):
+        pred, ob, fl, mi = T.random_dag(rng, int(rng.integers(1, 60)))
+        for strategy in (K.ALLOC_NONE, K.ALLOC_INPLACE, K.ALLOC_SHARE):
+            _graph_same(pred, ob, fl, mi if rng.random() < 0.8 else None, strategy)
+
+
+@pytest.mark.parametrize("g", [SG.two_layer(), SG.mlp(40, 16, 3),
+                               SG.resnet_basic(3, 8, 4, 16, 10),
+                               SG.resnet_bottleneck((2, 2, 3, 2), 2, 64, 10)])
+def test_graph_plan_network_graphs_match_oracle(g):
+    nb = len(g["block_out"])
+    for m in (SG.mirror_none(g), SG.mirror_bn_relu(g), SG.mirror_segments(g, max(1, nb // 3))):
+        for strategy in (K.ALLOC_NONE, K.ALLOC_INPLACE, K.ALLOC_SHARE):
+            _graph_same(g["pred"], g["bytes"], g["flags"], m, strategy)
+
+
+@pytest.mark.parametrize("args", [
+    ([[], [1]], [1, 1], [0, 0], None, 2),             # input not an earlier node
+    ([[], [0]], [1, 1], [0, 8], None, 2),             # unknown flag bit
+    ([[], [0]], [1, 1], [0, 0], [0, -1], 2),          # negative mirror count
+    ([[], [0]], [1, 1], [0, 0], None, 3),             # unknown strategy
+])
+def test_graph_plan_errors(args):
+    with pytest.raises(K.CkptError) as ei:
+        K.graph_plan(*args)
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError):
+        K.graph_plan([], [], [], None, 2, n_nodes=0)

@@ -211,6 +211,8 @@ int graph_plan_blocks(const ckpt_graph_plan *plan, uint64_t *bytes, int32_t cap,
 void graph_plan_free(ckpt_graph_plan *plan);
 
 /* ---- networks --------------------------------------------------------- */
+/* (the node-graph calls net_node_graph, graph_workspace_bytes and
+ *  train_step_graph follow train_step below) */
 #define CKPT_NET_MLP               1 /* y = x + relu(x W + b) blocks, MSE head        */
 #define CKPT_NET_RESNET_BASIC      2 /* CIFAR stem + 3 stages of basic blocks + FC-CE */
 #define CKPT_NET_LSTM              3 /* LSTM steps, each with a softmax head          */
@@ -367,6 +369,49 @@ typedef struct ckpt_step_stats {
 int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
                const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
+
+/*
+ * net_node_graph -- the net's forward graph at operator granularity, in the
+ * form graph_plan takes (section 3's computation graph; Alg. 2 plans mirror
+ * counts on it).  Provided for CKPT_NET_MLP: node 0 is the input; block i is
+ * 1 + 3i fully connected (x W + b, backward reads its input), 2 + 3i ReLU
+ * (in place, backward reads its output), 3 + 3i add (ReLU output + block
+ * input, in place); node 3n + 1 is the MSE loss (its output is the loss
+ * gradient).  Every node's output is one [batch, width] f32 tensor.
+ *   n_nodes: receives the node count; pred_ptr host [n_nodes + 1], pred_idx
+ *   host [edges], out_bytes, flags host [n_nodes]: filled when cap_nodes and
+ *   cap_edges are large enough (query with null arrays first); *n_edges gets
+ *   the edge count.
+ * Errors: CKPT_E_UNSUPPORTED for other nets; CKPT_E_INVALID for a null net
+ *   or arrays that are too small.
+ */
+int net_node_graph(const ckpt_net *net, int32_t *n_nodes, int32_t *n_edges, int32_t *pred_ptr,
+                   int32_t *pred_idx, uint64_t *out_bytes, int32_t *flags, int32_t cap_nodes,
+                   int32_t cap_edges);
+
+/* graph_workspace_bytes -- workspace train_step_graph needs for a graph plan
+ * of this net's node graph: the plan's memory blocks (each 256-byte aligned)
+ * plus the operator workspace (partial sums, loss, one tensor for adding the
+ * gradients of a node with several readers).  CKPT_E_MISMATCH if the plan is
+ * not of net_node_graph's graph, CKPT_E_UNSUPPORTED for nets without one. */
+int graph_workspace_bytes(const ckpt_net *net, const ckpt_graph_plan *plan, uint64_t *bytes);
+
+/*
+ * train_step_graph -- one training step over the node graph in the order and
+ * memory blocks of a graph plan (Alg. 2's gradient graph with mirror nodes:
+ * the forward graph, then each gradient node preceded by the mirrors it needs;
+ * every output in its planned block).  Arguments as for train_step, with a
+ * graph plan of net_node_graph's graph and a workspace of
+ * graph_workspace_bytes; *peak receives the plan's planned bytes.  stats:
+ * unit_forwards = forward and mirror nodes run, unit_backwards = gradient
+ * nodes run, arena_bytes = planned bytes.  The gradients equal train_step's
+ * bit for bit for every plan.
+ * Errors: as train_step; CKPT_E_UNSUPPORTED for nets without a node graph.
+ */
+int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+                     const ckpt_graph_plan *plan, void *workspace, uint64_t workspace_bytes,
+                     void *stream, float *loss_dev, float *loss_host, uint64_t *peak,
+                     ckpt_step_stats *stats);
 
 /*
  * Kernel timing for benchmarks.  net_timing_enable(net, 1) makes every later

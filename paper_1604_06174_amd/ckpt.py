@@ -90,6 +90,9 @@ _sig("graph_plan_schedule", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, C.c_int32
 _sig("graph_plan_blocks", C.c_int, [C.c_void_p, _u64p, C.c_int32, _i32p])
 _sig("graph_plan_free", None, [C.c_void_p])
 _sig("net_create", C.c_int, [C.POINTER(NetDesc), C.POINTER(C.c_void_p)])
+_sig("net_node_graph", C.c_int, [C.c_void_p, _i32p, _i32p, _i32p, _i32p, _u64p, _i32p, C.c_int32,
+                                 C.c_int32])
+_sig("graph_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
 _sig("net_destroy", None, [C.c_void_p])
 _sig("net_units", C.c_int, [C.c_void_p, _i32p])
 _sig("net_unit_sizes", C.c_int, [C.c_void_p, _u64p, _u64p, _u64p])
@@ -106,10 +109,14 @@ _sig("net_timing_read", C.c_int, [C.c_void_p, _u64p, C.POINTER(C.c_double), C.PO
 _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
                              C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
                              C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
+_sig("train_step_graph", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
+                                   C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
+                                   C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
 
 EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
             "plan_free", "plan_search", "graph_plan", "graph_plan_info", "graph_plan_schedule",
-            "graph_plan_blocks", "graph_plan_free", "net_create", "net_destroy", "net_units", "net_unit_sizes",
+            "graph_plan_blocks", "graph_plan_free", "net_node_graph", "graph_workspace_bytes",
+            "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
             "train_step"]
@@ -323,6 +330,23 @@ class Net:
         _check(_lib.net_workspace_bytes(self._h, plan.handle, C.byref(v)))
         return v.value
 
+    def node_graph(self) -> Dict:
+        """The net's operator-level graph: pred lists, bytes and flags."""
+        n, e = C.c_int32(), C.c_int32()
+        _check(_lib.net_node_graph(self._h, C.byref(n), C.byref(e), None, None, None, None, 0, 0))
+        ptr = (C.c_int32 * (n.value + 1))()
+        idx = (C.c_int32 * max(1, e.value))()
+        by = (C.c_uint64 * n.value)()
+        fl = (C.c_int32 * n.value)()
+        _check(_lib.net_node_graph(self._h, C.byref(n), C.byref(e), ptr, idx, by, fl, n.value, e.value))
+        pred = [list(idx[ptr[v]:ptr[v + 1]]) for v in range(n.value)]
+        return dict(pred=pred, bytes=list(by), flags=list(fl))
+
+    def graph_workspace_bytes(self, plan: "GraphPlan") -> int:
+        v = C.c_uint64()
+        _check(_lib.graph_workspace_bytes(self._h, plan._h, C.byref(v)))
+        return v.value
+
     def timing_enable(self, on: bool = True):
         _check(_lib.net_timing_enable(self._h, 1 if on else 0))
 
@@ -360,6 +384,25 @@ def net_create(kind: int, batch: int, depth: int, width: int, image: int = 0,
                expansion: int = 0, stem_channels: int = 0, drop_bn_relu: int = 0) -> Net:
     return Net(kind, batch, depth, width, image, n_classes, grad_chunk, stage_blocks, expansion,
                stem_channels, drop_bn_relu)
+
+
+def train_step_graph(net: Net, params, grads, batch_input, batch_target, plan: GraphPlan, workspace,
+                     workspace_bytes: int, stream=None, loss_dev=None, want_loss: bool = True):
+    """One step over the net's node graph in a graph plan's order and memory
+    blocks; returns (loss or None, planned bytes, stats dict)."""
+    b = Batch(_addr(batch_input), _addr(batch_target))
+    loss = C.c_float()
+    peak = C.c_uint64()
+    st = StepStats()
+    s = None
+    if stream is not None:
+        s = stream if isinstance(stream, int) else int(stream.cuda_stream)
+    ld = _addr(loss_dev)
+    _check(_lib.train_step_graph(net.handle, _addr(params), _addr(grads), C.byref(b), plan._h,
+                                 _addr(workspace), int(workspace_bytes), s,
+                                 C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
+                                 C.byref(loss) if want_loss else None, C.byref(peak), C.byref(st)))
+    return (loss.value if want_loss else None), peak.value, st.as_dict()
 
 
 def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,

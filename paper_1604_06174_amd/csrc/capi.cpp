@@ -24,6 +24,10 @@ uint64_t workspace_bytes(const Net &net, const Accounting &acc);
 void run_train_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
                     const Plan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
                     float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
+uint64_t graph_workspace_bytes(const Net &net, const GraphPlan &p);
+void run_graph_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
+                    const GraphPlan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
+                    float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
 }  // namespace ckpt
 
 namespace {
@@ -326,6 +330,59 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
     if (plan->p.n != net->net->n)
       ckpt::fail(CKPT_E_MISMATCH, "train_step: plan n differs from the net's unit count");
     ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
+                         *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
+                         static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
+  });
+}
+
+int net_node_graph(const ckpt_net *net, int32_t *n_nodes, int32_t *n_edges, int32_t *pred_ptr,
+                   int32_t *pred_idx, uint64_t *out_bytes, int32_t *flags, int32_t cap_nodes,
+                   int32_t cap_edges) {
+  return guarded([&] {
+    need(net, "net_node_graph");
+    ckpt::Net::NodeGraph g;
+    if (!net->net->node_graph(g))
+      ckpt::fail(CKPT_E_UNSUPPORTED, "net_node_graph: this net has no node graph");
+    const int32_t n = int32_t(g.bytes.size()), e = int32_t(g.idx.size());
+    if (n_nodes) *n_nodes = n;
+    if (n_edges) *n_edges = e;
+    if (!pred_ptr && !pred_idx && !out_bytes && !flags) return;
+    if (cap_nodes < n || cap_edges < e || !pred_ptr || !out_bytes || !flags || (e > 0 && !pred_idx))
+      ckpt::fail(CKPT_E_INVALID, "net_node_graph: output arrays missing or too small");
+    std::copy(g.ptr.begin(), g.ptr.end(), pred_ptr);
+    std::copy(g.idx.begin(), g.idx.end(), pred_idx);
+    std::copy(g.bytes.begin(), g.bytes.end(), out_bytes);
+    std::copy(g.flags.begin(), g.flags.end(), flags);
+  });
+}
+
+int graph_workspace_bytes(const ckpt_net *net, const ckpt_graph_plan *plan, uint64_t *bytes) {
+  return guarded([&] {
+    need(net, "graph_workspace_bytes(net)");
+    need(plan, "graph_workspace_bytes(plan)");
+    need(bytes, "graph_workspace_bytes(bytes)");
+    *bytes = ckpt::graph_workspace_bytes(*net->net, plan->p);
+  });
+}
+
+int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+                     const ckpt_graph_plan *plan, void *workspace, uint64_t workspace_bytes,
+                     void *stream, float *loss_dev, float *loss_host, uint64_t *peak,
+                     ckpt_step_stats *stats) {
+  return guarded([&] {
+    need(net, "train_step_graph(net)");
+    need(params, "train_step_graph(params)");
+    need(grads, "train_step_graph(grads)");
+    need(batch, "train_step_graph(batch)");
+    need(batch->input, "train_step_graph(batch.input)");
+    need(batch->target, "train_step_graph(batch.target)");
+    need(plan, "train_step_graph(plan)");
+    need(workspace, "train_step_graph(workspace)");
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+      ckpt::fail(CKPT_E_INVALID, "train_step_graph: workspace must be 256-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
+      ckpt::fail(CKPT_E_INVALID, "train_step_graph: params and grads must be 256-byte aligned");
+    ckpt::run_graph_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
                          *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
                          static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
   });

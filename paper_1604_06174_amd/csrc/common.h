@@ -77,6 +77,8 @@ struct GraphNode {
 };
 struct GraphPlan {
   std::vector<GraphNode> nodes;
+  int32_t n_forward = 0;         // forward nodes (ids 0 .. n_forward-1)
+  std::vector<int32_t> flags;    // their CKPT_NODE_* flags
   std::vector<int32_t> order;    // execution order
   std::vector<int32_t> tag_of;   // node id -> memory block (-1: none)
   std::vector<uint64_t> tag_bytes;

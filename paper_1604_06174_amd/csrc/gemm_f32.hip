@@ -24,8 +24,10 @@
 //   ADD      C = acc + D                      (backward: dx = dy + dr W^T)
 //   MLPFWD   Z = acc + bias;  C = A + relu(Z) (residual block y = x + relu(xW+b);
 //                                               requires !TA and K == N)
+//   BIAS     C = acc + bias
 #include <hip/hip_runtime.h>
 
+#include "common.h"
 #include "kernels.h"
 
 namespace ckpt {
@@ -186,6 +188,8 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
         p.C[size_t(m) * p.ldc + n] = v;
       } else if (EPI == GEMM_EPI_ADD) {
         p.C[size_t(m) * p.ldc + n] = v + p.D[size_t(m) * p.ldd + n];
+      } else if (EPI == GEMM_EPI_BIAS) {
+        p.C[size_t(m) * p.ldc + n] = v + p.bias[n];
       } else {  // MLPFWD
         const float z = v + p.bias[n];
         p.Z[size_t(m) * p.ldz + n] = z;
@@ -235,6 +239,11 @@ template <int KS>
 void dispatch(const GemmArgs &a, bool ta, bool tb, int epi, bool vec, hipStream_t s) {
   if (epi == GEMM_EPI_MLPFWD) {
     launch<KS, false, false, GEMM_EPI_MLPFWD>(a, vec, s);
+    return;
+  }
+  if (epi == GEMM_EPI_BIAS) {
+    if (ta || tb) fail(CKPT_E_UNSUPPORTED, "gemm_f32: the bias epilogue takes untransposed operands");
+    launch<KS, false, false, GEMM_EPI_BIAS>(a, vec, s);
     return;
   }
 #define CKPT_GEMM_CASE(TA_, TB_)                                               \

@@ -54,6 +54,8 @@ GraphPlan make_graph_plan(int32_t n, const int32_t *pred_ptr, const int32_t *pre
     mmax = std::max(mmax, m[size_t(v)]);
   }
   GraphPlan p;
+  p.n_forward = n;
+  p.flags.assign(flags, flags + n);
   auto add = [&](int32_t kind, int32_t of, std::vector<int32_t> ins, uint64_t bytes, bool inplace) {
     p.nodes.push_back(GraphNode{kind, of, std::move(ins), bytes, inplace});
     return int32_t(p.nodes.size() - 1);

@@ -15,7 +15,8 @@ __device__ __forceinline__ float bn_relu(float x, float mean, float rstd, float 
   return fmaxf(__builtin_fmaf(g, (x - mean) * rstd, b), 0.f);
 }
 
-enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4 };
+enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4,
+       GEMM_EPI_BIAS = 5 };
 
 // C = epilogue(op(A) op(B)); see gemm_f32.hip for the operand conventions.
 void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool ta, const float *B,
@@ -36,6 +37,13 @@ void mse_head(hipStream_t s, int64_t count, const float *y, const float *t, floa
 
 // Copy one f32 scalar (device to device) -- used to publish the loss.
 void copy_scalar(hipStream_t s, const float *src, float *dst);
+// column sums of g [rows, cols] in the same order as mlp_relu_bwd's
+void mlp_colsum(hipStream_t s, int rows, int cols, const float *g, float *db, float *pdb);
+// elementwise operators of node-level graphs (outputs may alias inputs)
+void ew_relu(hipStream_t s, int64_t n, const float *x, float *y);                  // y = max(x, 0)
+void ew_add(hipStream_t s, int64_t n, const float *a, const float *b, float *y);   // y = a + b
+void ew_relu_bwd(hipStream_t s, int64_t n, const float *dy, const float *y, float *dx);  // dy [y > 0]
+void ew_copy(hipStream_t s, int64_t n, const float *x, float *y);
 
 // ---- 3x3 convolutions (conv.hip) ----
 enum { CONV_FWD = 0, CONV_DGRAD = 1 };

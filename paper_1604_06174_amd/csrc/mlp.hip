@@ -9,8 +9,10 @@ namespace ckpt {
 namespace {
 
 // Workgroup = 64 columns x 4 row groups over a block of 16 rows (blockIdx.y);
-// dr = g * [z > 0]; the workgroup's column sums over its rows, ((s0 + s1) +
-// s2) + s3 with s_j = rows j, j+4, .. in order, go to pdb[blockIdx.y][cols].
+// MASK: dr = g * [z > 0], else the sums are of g itself; the workgroup's
+// column sums over its rows, ((s0 + s1) + s2) + s3 with s_j = rows j, j+4, ..
+// in order, go to pdb[blockIdx.y][cols].
+template <bool MASK>
 __global__ __launch_bounds__(256) void k_mlp_relu_bwd(int rows, int cols, const float *__restrict__ g,
                                                       const float *__restrict__ z,
                                                       float *__restrict__ dr, float *__restrict__ pdb) {
@@ -25,14 +27,14 @@ __global__ __launch_bounds__(256) void k_mlp_relu_bwd(int rows, int cols, const 
       const int m = r0 + 4 * i;
       const size_t e = size_t(m < rows ? m : 0) * cols + n;
       gv[i] = g[e];
-      zv[i] = z[e];
+      zv[i] = MASK ? z[e] : 0.f;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = r0 + 4 * i;
       if (m < rows) {
-        const float v = zv[i] > 0.f ? gv[i] : 0.f;
-        dr[size_t(m) * cols + n] = v;
+        const float v = MASK ? (zv[i] > 0.f ? gv[i] : 0.f) : gv[i];
+        if (MASK) dr[size_t(m) * cols + n] = v;
         s += v;
       }
     }
@@ -85,6 +87,27 @@ __global__ __launch_bounds__(1024) void k_mse_head(int64_t count, const float *_
 
 __global__ void k_copy_scalar(const float *src, float *dst) { dst[0] = src[0]; }
 
+// Elementwise operators of the node-level graph (any of the pointers may
+// alias the output: every thread reads its element before writing it).
+enum { EW_RELU = 0, EW_ADD = 1, EW_RELU_BWD = 2, EW_COPY = 3 };
+template <int OP>
+__global__ __launch_bounds__(256) void k_elementwise(int64_t n, const float *a, const float *b, float *y) {
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < n; e += int64_t(gridDim.x) * 256) {
+    const float x = a[e];
+    float v;
+    if (OP == EW_RELU) v = fmaxf(x, 0.f);
+    else if (OP == EW_ADD) v = x + b[e];
+    else if (OP == EW_RELU_BWD) v = b[e] > 0.f ? x : 0.f;
+    else v = x;
+    y[e] = v;
+  }
+}
+
+int ew_blocks(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return int(b < 4096 ? (b > 0 ? b : 1) : 4096);
+}
+
 }  // namespace
 
 int mlp_relu_row_blocks(int rows) { return (rows + 15) / 16; }
@@ -92,9 +115,29 @@ int mlp_relu_row_blocks(int rows) { return (rows + 15) / 16; }
 void mlp_relu_bwd(hipStream_t s, int rows, int cols, const float *g, const float *z, float *dr,
                   float *db, float *pdb) {
   const int R = mlp_relu_row_blocks(rows);
-  hipLaunchKernelGGL(k_mlp_relu_bwd, dim3((cols + 63) / 64, R), dim3(256), 0, s, rows, cols, g, z, dr,
-                     pdb);
+  hipLaunchKernelGGL(k_mlp_relu_bwd<true>, dim3((cols + 63) / 64, R), dim3(256), 0, s, rows, cols, g, z,
+                     dr, pdb);
   hipLaunchKernelGGL(k_colsum_rows, dim3((cols + 255) / 256), dim3(256), 0, s, R, cols, pdb, db);
+}
+
+void mlp_colsum(hipStream_t s, int rows, int cols, const float *g, float *db, float *pdb) {
+  const int R = mlp_relu_row_blocks(rows);
+  hipLaunchKernelGGL(k_mlp_relu_bwd<false>, dim3((cols + 63) / 64, R), dim3(256), 0, s, rows, cols, g,
+                     nullptr, nullptr, pdb);
+  hipLaunchKernelGGL(k_colsum_rows, dim3((cols + 255) / 256), dim3(256), 0, s, R, cols, pdb, db);
+}
+
+void ew_relu(hipStream_t s, int64_t n, const float *x, float *y) {
+  hipLaunchKernelGGL(k_elementwise<EW_RELU>, dim3(ew_blocks(n)), dim3(256), 0, s, n, x, nullptr, y);
+}
+void ew_add(hipStream_t s, int64_t n, const float *a, const float *b, float *y) {
+  hipLaunchKernelGGL(k_elementwise<EW_ADD>, dim3(ew_blocks(n)), dim3(256), 0, s, n, a, b, y);
+}
+void ew_relu_bwd(hipStream_t s, int64_t n, const float *dy, const float *y, float *dx) {
+  hipLaunchKernelGGL(k_elementwise<EW_RELU_BWD>, dim3(ew_blocks(n)), dim3(256), 0, s, n, dy, y, dx);
+}
+void ew_copy(hipStream_t s, int64_t n, const float *x, float *y) {
+  hipLaunchKernelGGL(k_elementwise<EW_COPY>, dim3(ew_blocks(n)), dim3(256), 0, s, n, x, nullptr, y);
 }
 
 void mse_head(hipStream_t s, int64_t count, const float *y, const float *t, float *g, float *loss_out) {

@@ -113,6 +113,23 @@ class Net {
   // Device address of the f32 loss after the step.
   virtual const float *loss_ptr(const StepCtx &c) const = 0;
 
+  // ---- node-granularity graph (nets that provide one): nodes in a
+  // topological order with their inputs (CSR), output bytes and CKPT_NODE_*
+  // flags, the form graph_plan takes.
+  struct NodeGraph {
+    std::vector<int32_t> ptr, idx, flags;
+    std::vector<uint64_t> bytes;
+  };
+  virtual bool node_graph(NodeGraph &) const { return false; }
+  // Forward operator of node v: its inputs (in order) -> out.
+  virtual void node_fwd(int32_t, const std::vector<const void *> &, void *, StepCtx &) {}
+  // Backward operator of node v: dy = dL/d(v's output) (null for the loss
+  // node), y = v's output (when its backward reads it), ins = v's inputs
+  // (when read) -> out = the gradients of v's inputs, concatenated in input
+  // order.  Writes v's parameter gradients.
+  virtual void node_bwd(int32_t, const void *, const void *, const std::vector<const void *> &, void *,
+                        StepCtx &) {}
+
   const float *P(const StepCtx &c, int k) const { return c.params + params[size_t(k)].off / 4; }
   float *G(const StepCtx &c, int k) const { return c.grads + params[size_t(k)].off / 4; }
 

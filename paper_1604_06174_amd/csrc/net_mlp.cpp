@@ -77,6 +77,92 @@ class MlpNet : public Net {
     c.launches += 1;
   }
 
+  // Node graph: 0 data; block i: 1 + 3i fully connected (x W + b), 2 + 3i ReLU,
+  // 3 + 3i add (ReLU output + block input); 3n + 1 the MSE loss, whose output
+  // is the loss gradient.  Every tensor is [B, D] f32.  The operators and their
+  // order of arithmetic are those of the fused unit, so any plan of this graph
+  // gives the chain's gradients bit for bit.
+  bool node_graph(NodeGraph &g) const override {
+    const uint64_t t = uint64_t(B) * D * 4;
+    g.ptr.assign(1, 0);
+    g.idx.clear();
+    g.flags.clear();
+    g.bytes.clear();
+    auto node = [&](std::initializer_list<int32_t> ins, int32_t fl) {
+      for (int32_t u : ins) g.idx.push_back(u);
+      g.ptr.push_back(int32_t(g.idx.size()));
+      g.flags.push_back(fl);
+      g.bytes.push_back(t);
+    };
+    node({}, 0);
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t x = 3 * i;
+      node({x}, CKPT_NODE_GRAD_IN);                         // fully connected
+      node({x + 1}, CKPT_NODE_INPLACE | CKPT_NODE_GRAD_OUT);  // ReLU
+      node({x + 2, x}, CKPT_NODE_INPLACE);                   // add
+    }
+    node({3 * n}, CKPT_NODE_GRAD_OUT);                      // loss
+    return true;
+  }
+
+  void node_fwd(int32_t v, const std::vector<const void *> &ins, void *out, StepCtx &c) override {
+    const int64_t t = int64_t(B) * D;
+    float *y = static_cast<float *>(out);
+    if (v == 0) {
+      if (hipMemcpyAsync(y, c.input, size_t(t) * 4, hipMemcpyDeviceToDevice, c.s) != hipSuccess)
+        fail(CKPT_E_HIP, "train_step_graph: input copy failed");
+    } else if (v == 3 * n + 1) {
+      mse_head(c.s, t, static_cast<const float *>(ins[0]), static_cast<const float *>(c.target), y,
+               reinterpret_cast<float *>(c.ks));
+    } else {
+      const int i = (v - 1) / 3, k = (v - 1) % 3;
+      const float *x = static_cast<const float *>(ins[0]);
+      if (k == 0) {
+        timer.begin(c.s);
+        gemm_f32(c.s, B, D, D, x, D, false, P(c, wi[i]), D, false, y, D, GEMM_EPI_BIAS, nullptr, 0,
+                 P(c, bi[i]), nullptr, 0);
+        timer.end(c.s, gf(B, D, D), gb(B, D, D, 4.0 * D));
+      } else if (k == 1) {
+        ew_relu(c.s, t, x, y);
+      } else {
+        ew_add(c.s, t, x, static_cast<const float *>(ins[1]), y);
+      }
+    }
+    c.launches += 1;
+  }
+
+  void node_bwd(int32_t v, const void *dyv, const void *yv, const std::vector<const void *> &ins,
+                void *out, StepCtx &c) override {
+    const int64_t t = int64_t(B) * D;
+    const float *dy = static_cast<const float *>(dyv);
+    float *o = static_cast<float *>(out);
+    if (v == 0) return;  // the input has no gradient to form
+    if (v == 3 * n + 1) {  // the loss node's output is dL/dx_n already
+      ew_copy(c.s, t, static_cast<const float *>(yv), o);
+      c.launches += 1;
+      return;
+    }
+    const int i = (v - 1) / 3, k = (v - 1) % 3;
+    if (k == 0) {  // fully connected: dx = dy W^T, dW = x^T dy, db = column sums of dy
+      const float *x = static_cast<const float *>(ins[0]);
+      timer.begin(c.s);
+      gemm_f32(c.s, B, D, D, dy, D, false, P(c, wi[i]), D, true, o, D, GEMM_EPI_STORE);
+      timer.end(c.s, gf(B, D, D), gb(B, D, D, 0));
+      timer.begin(c.s);
+      gemm_f32(c.s, D, D, B, x, D, true, dy, D, false, G(c, wi[i]), D, GEMM_EPI_STORE);
+      timer.end(c.s, gf(D, D, B), gb(D, D, B, 0));
+      mlp_colsum(c.s, B, D, dy, G(c, bi[i]), reinterpret_cast<float *>(c.ks + 256));
+      c.launches += 4;
+    } else if (k == 1) {  // ReLU: the mask from its output
+      ew_relu_bwd(c.s, t, dy, static_cast<const float *>(yv), o);
+      c.launches += 1;
+    } else {  // add: both inputs receive dy
+      ew_copy(c.s, t, dy, o);
+      ew_copy(c.s, t, dy, o + t);
+      c.launches += 2;
+    }
+  }
+
   const float *loss_ptr(const StepCtx &c) const override {
     return reinterpret_cast<const float *>(c.ks);
   }

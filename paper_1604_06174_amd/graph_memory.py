@@ -1,6 +1,7 @@
 """Memory of each allocation strategy on a workload's node-granularity graph.
 
     python -m paper_1604_06174_amd.graph_memory [--workload cifar110]
+    python -m paper_1604_06174_amd.graph_memory --workload mlp64 --run [--steps 20]
 
 Builds the workload's forward graph at operator granularity, runs the
 library's graph planner (Alg. 2 gradient-graph construction + section 3's
@@ -9,6 +10,11 @@ in-place + sharing, drop bn-relu (batch-norm and ReLU results mirrored), and a
 segmented sublinear plan (every node mirrored except the outputs of every
 s-th block, s = ceil(sqrt(blocks))) -- and prints one JSON line per strategy
 with the planned bytes, the mirror nodes executed and the planning time.
+With --run (nets whose library object provides the node graph: the residual
+MLP) each plan is also executed on the GPU by train_step_graph -- synthetic
+inputs of the workload, a warm-up step, then --steps timed steps between HIP
+events -- and the line gains ms/step, the workspace bytes and the chain
+executor's no-checkpoint ms/step for comparison.
 """
 from __future__ import annotations
 
@@ -40,21 +46,50 @@ def strategies(g):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="cifar110")
+    ap.add_argument("--run", action="store_true")
+    ap.add_argument("--steps", type=int, default=20)
     args = ap.parse_args()
     import synth
     from synth import graphs as SG
     from paper_1604_06174_amd import ckpt as K
     cfg = synth.WORKLOADS[args.workload]
     g = SG.for_workload(cfg)
+    step = timed = None
+    if args.run:
+        import torch
+        from paper_1604_06174_amd.workload import GpuStep
+        d = synth.make(cfg)
+        step = GpuStep(cfg, d["params"], d["input"], d["target"])
+        del d
+        s = torch.cuda.current_stream()
+
+        def timed(fn):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(args.steps):
+                fn()
+            e1.record(s)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / args.steps
+
+        none = step.plan(K.NONE)
+        chain_ms = timed(lambda: step.run(none, stream=s, want_loss=False))
     for name, mirror, strategy in strategies(g):
         t0 = time.perf_counter()
         plan = K.graph_plan(g["pred"], g["bytes"], g["flags"], mirror, strategy)
         dt = time.perf_counter() - t0
         info = plan.info()
-        print(json.dumps({"workload": args.workload, "nodes": len(g["op"]), "strategy": name,
-                          "planned_gb": round(info["peak"] / 1e9, 6),
-                          "mirror_nodes": info["n_mirror"], "executed_nodes": info["n_exec"],
-                          "plan_ms": round(dt * 1e3, 3)}), flush=True)
+        rec = {"workload": args.workload, "nodes": len(g["op"]), "strategy": name,
+               "planned_gb": round(info["peak"] / 1e9, 6), "mirror_nodes": info["n_mirror"],
+               "executed_nodes": info["n_exec"], "plan_ms": round(dt * 1e3, 3)}
+        if args.run:
+            gp = step.graph_plan(mirror, strategy)
+            rec["ms_per_step"] = round(timed(lambda: step.run_graph(gp, stream=s, want_loss=False)), 4)
+            rec["workspace_gb"] = round(step.net.graph_workspace_bytes(gp) / 1e9, 6)
+            rec["chain_no_ckpt_ms_per_step"] = round(chain_ms, 4)
+        print(json.dumps(rec), flush=True)
     return 0
 
 

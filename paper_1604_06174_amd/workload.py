@@ -80,6 +80,20 @@ class GpuStep:
         return K.train_step(self.net, self.params, self.grads, self.input, self.target, plan, ws,
                             ws.numel(), s, self.loss_dev, want_loss)
 
+    def graph_plan(self, mirror=None, strategy: int = K.ALLOC_SHARE) -> K.GraphPlan:
+        g = self.net.node_graph()
+        return K.graph_plan(g["pred"], g["bytes"], g["flags"], mirror, strategy)
+
+    def run_graph(self, plan: K.GraphPlan, stream: Optional[torch.cuda.Stream] = None,
+                  want_loss: bool = True):
+        need = self.net.graph_workspace_bytes(plan)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        return K.train_step_graph(self.net, self.params, self.grads, self.input, self.target, plan,
+                                  self._ws, self._ws.numel(), s, self.loss_dev, want_loss)
+
     def grads_host(self) -> Dict[str, np.ndarray]:
         g = self.grads.cpu().numpy()
         return {name: g[off // 4: off // 4 + numel].copy() for name, off, numel in self.layout}

@@ -320,3 +320,31 @@ def test_graph_plan_errors(args):
     assert ei.value.code == K.E_INVALID
     with pytest.raises(K.CkptError):
         K.graph_plan([], [], [], None, 2, n_nodes=0)
+
+
+@pytest.mark.parametrize("cfg", [dict(kind="mlp", depth=9, width=72, batch=37),
+                                 dict(kind="mlp", depth=64, width=256, batch=64),
+                                 dict(kind="mlp", depth=1, width=8, batch=1)])
+def test_mlp_node_graph_is_the_synth_graph(cfg):
+    from paper_1604_06174_amd.workload import net_for
+    net = net_for(cfg)
+    g = net.node_graph()
+    sg = SG.mlp(cfg["depth"], cfg["width"], cfg["batch"])
+    assert (g["pred"], g["bytes"], g["flags"]) == (sg["pred"], sg["bytes"], sg["flags"])
+    p = K.graph_plan(g["pred"], g["bytes"], g["flags"], SG.mirror_segments(sg, 2), K.ALLOC_SHARE)
+    need = net.graph_workspace_bytes(p)
+    assert need >= p.info()["peak"]
+
+
+def test_node_graph_errors():
+    from paper_1604_06174_amd.workload import net_for
+    cnn = net_for(dict(kind="resnet_basic", blocks_per_stage=1, base=4, batch=2, image=8, classes=3))
+    with pytest.raises(K.CkptError) as ei:
+        cnn.node_graph()
+    assert ei.value.code == K.E_UNSUPPORTED
+    mlp = net_for(dict(kind="mlp", depth=3, width=8, batch=2))
+    other = SG.mlp(4, 8, 2)  # a plan of a different graph
+    p = K.graph_plan(other["pred"], other["bytes"], other["flags"], None, K.ALLOC_SHARE)
+    with pytest.raises(K.CkptError) as ei:
+        mlp.graph_workspace_bytes(p)
+    assert ei.value.code == K.E_MISMATCH

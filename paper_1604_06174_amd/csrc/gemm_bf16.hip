@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256) void k_sum_slices(const float *__restrict__ pa
 int gemm_bf16_splits(int M, int N, int K) {
   const int tiles = gemm_bf16_tiles(M, N);
   int s = (512 + tiles - 1) / tiles;
-  s = std::min(s, std::max(1, K / (4 * KS)));  // at least four k-slices per split
+  s = std::min(s, std::max(1, K / 128));  // at least 128 k per split
   return std::max(s, 1);
 }
 

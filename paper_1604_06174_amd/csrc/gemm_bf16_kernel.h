@@ -53,8 +53,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 namespace gb {
 
-constexpr int KS = 32;      // k per LDS slice
-constexpr int KP = KS + 8;  // padded row (bf16 elements): 80-byte rows
+constexpr int KS = 64;      // k per LDS slice: two 32-deep MFMA steps
+constexpr int KP = KS + 8;  // padded row (bf16 elements): 144-byte rows
 
 enum { G_DENSE = 0, GA_FWD = 1, GA_DGRAD = 2, GB_WGRAD = 3, GB_WDGRAD = 4 };
 
@@ -350,29 +350,35 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  // one slice: KS / 32 MFMA k-steps; step s reads k 32 s + 8 q .. + 7
   auto compute = [&](int buf) {
-    bf16x8 av[TM], bv[TN];
 #pragma unroll
-    for (int a = 0; a < TM; ++a) {
-      if constexpr (AK)
-        av[a] = *reinterpret_cast<const bf16x8 *>(smA + ((buf * BM + wm + a * 16 + i16) * KP + 8 * q) * 2);
-      else
-        av[a] = tr_operand(smA + ((buf * KS + 8 * q + (i16 >> 2)) * PA_K + wm + a * 16 + 4 * (i16 & 3)) * 2,
-                           4 * PA_K * 2);
+    for (int ks = 0; ks < KS; ks += 32) {
+      bf16x8 av[TM], bv[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        if constexpr (AK)
+          av[a] = *reinterpret_cast<const bf16x8 *>(smA + ((buf * BM + wm + a * 16 + i16) * KP + ks + 8 * q) * 2);
+        else
+          av[a] = tr_operand(
+              smA + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PA_K + wm + a * 16 + 4 * (i16 & 3)) * 2,
+              4 * PA_K * 2);
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        if constexpr (BK)
+          bv[b] = *reinterpret_cast<const bf16x8 *>(smB + ((buf * BN + wn + b * 16 + i16) * KP + ks + 8 * q) * 2);
+        else
+          bv[b] = tr_operand(
+              smB + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PB_K + wn + b * 16 + 4 * (i16 & 3)) * 2,
+              4 * PB_K * 2);
+      }
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
     }
-#pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      if constexpr (BK)
-        bv[b] = *reinterpret_cast<const bf16x8 *>(smB + ((buf * BN + wn + b * 16 + i16) * KP + 8 * q) * 2);
-      else
-        bv[b] = tr_operand(smB + ((buf * KS + 8 * q + (i16 >> 2)) * PB_K + wn + b * 16 + 4 * (i16 & 3)) * 2,
-                           4 * PB_K * 2);
-    }
-#pragma unroll
-    for (int a = 0; a < TM; ++a)
-#pragma unroll
-      for (int b = 0; b < TN; ++b)
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
   };
 
   // Two register stages: the loads of slice kt + 2 are issued right after

@@ -134,6 +134,9 @@ def main():
     ap.add_argument("--drop-bn-relu", action="store_true",
                     help="CIFAR-shaped net: keep only convolution outputs and re-form batch norm + "
                          "ReLU from them when read")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time each step recorded once as a HIP graph and replayed "
+                         "(step_graph_create / step_graph_launch)")
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="batch (LSTM: time steps) of the CPU oracle sample; 0 skips it, -1 picks "
                          "about 10-30 s of oracle work for the workload")
@@ -175,7 +178,7 @@ def main():
     acc = step.net.accounting(plan)
     acc_none = step.net.accounting(none)
     step.workspace(none)  # the larger workspace serves both plans
-    s = torch.cuda.current_stream()
+    s = torch.cuda.Stream()  # a created stream (default priority): steps can be recorded on it
 
     def run(p, k):
         st = None
@@ -187,18 +190,28 @@ def main():
     run(none, args.warmup)
     torch.cuda.synchronize()
 
-    def timed(p):
+    def timed(launch):
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(s)
-        run(p, args.steps)
+        for _ in range(args.steps):
+            launch()
         e1.record(s)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps
 
-    ms = timed(plan)
-    ms_none = timed(none)
+    ms = timed(lambda: step.run(plan, stream=s, want_loss=False))
+    ms_none = timed(lambda: step.run(none, stream=s, want_loss=False))
+    graph_ms = None
+    if args.graph:  # each step recorded once as a HIP graph, then replayed
+        graphs = {"plan": step.record(plan, s), "none": step.record(none, s)}
+        for g in graphs.values():
+            for _ in range(args.warmup):
+                g.launch(s)
+        torch.cuda.synchronize()
+        graph_ms = {"ms_per_step": round(timed(lambda: graphs["plan"].launch(s)), 4),
+                    "ms_per_step_no_ckpt": round(timed(lambda: graphs["none"].launch(s)), 4)}
     loss = float(step.loss_dev.item())
 
     # second timed pass: HIP events around every launch of the dominant kernel
@@ -256,6 +269,7 @@ def main():
         "peak_activation_gb_no_ckpt": round(acc_none["peak"] / 1e9, 6),
         "recompute_overhead_x": round(ms / ms_none, 4),
         "ms_per_step_no_ckpt": round(ms_none, 4),
+        **({"hip_graph_replay": graph_ms} if graph_ms else {}),
         "unit_forwards_per_step": stats["unit_forwards"],
         "kernel_launches_per_step": stats["kernel_launches"],
         "loss": loss,

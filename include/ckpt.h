@@ -371,6 +371,38 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
 
 /*
+ * Recorded steps.  A checkpointed step is a fixed sequence of small kernels
+ * (the plan fixes every launch and every buffer: section 4's static plan);
+ * recording it once as a HIP graph and launching the graph replaces the
+ * per-kernel host submissions with one.
+ *
+ * step_graph_create -- record one train_step with these arguments (loss to
+ *   loss_dev only; no host loss, no peak) on `stream` and instantiate it.
+ *   Nothing runs while recording.  stream must be a created stream (not the
+ *   default one) that is not already being captured; kernel timing must be
+ *   off.  *out receives the recorded step; stats (nullable) the step's
+ *   counters.  The recorded step keeps the addresses of params, grads, the
+ *   batch buffers, workspace and loss_dev: they must stay allocated while it
+ *   exists, and each launch reads their contents at that time.
+ * step_graph_launch -- enqueue the recorded step on `stream` (null = default);
+ *   its results are those of train_step with the same arguments, bit for bit.
+ *   Launches on one stream run in order; two launches of one recorded step
+ *   that overlap in time (different streams, no ordering) race on its buffers.
+ * step_graph_free -- release a recorded step (null is a no-op); launches
+ *   already enqueued complete normally.
+ * Errors: as train_step; CKPT_E_INVALID for the default stream, a stream
+ *   under capture or timing on; CKPT_E_HIP when recording, instantiation or
+ *   the launch fails.
+ */
+typedef struct ckpt_step_graph ckpt_step_graph;
+int step_graph_create(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+                      const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes,
+                      void *stream, float *loss_dev, ckpt_step_graph **out,
+                      ckpt_step_stats *stats);
+int step_graph_launch(ckpt_step_graph *graph, void *stream);
+void step_graph_free(ckpt_step_graph *graph);
+
+/*
  * net_node_graph -- the net's forward graph at operator granularity, in the
  * form graph_plan takes (section 3's computation graph; Alg. 2 plans mirror
  * counts on it).  Provided for CKPT_NET_MLP: node 0 is the input; block i is

@@ -109,6 +109,12 @@ _sig("net_timing_read", C.c_int, [C.c_void_p, _u64p, C.POINTER(C.c_double), C.PO
 _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
                              C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
                              C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
+_sig("step_graph_create", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch),
+                                    C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p,
+                                    C.POINTER(C.c_float), C.POINTER(C.c_void_p),
+                                    C.POINTER(StepStats)])
+_sig("step_graph_launch", C.c_int, [C.c_void_p, C.c_void_p])
+_sig("step_graph_free", None, [C.c_void_p])
 _sig("train_step_graph", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
                                    C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
                                    C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
@@ -119,7 +125,7 @@ EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "pl
             "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
-            "train_step"]
+            "train_step", "step_graph_create", "step_graph_launch", "step_graph_free"]
 
 
 class CkptError(RuntimeError):
@@ -421,3 +427,47 @@ def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, w
                            C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
                            C.byref(loss) if want_loss else None, C.byref(peak), C.byref(st)))
     return (loss.value if want_loss else None), peak.value, st.as_dict()
+
+
+class StepGraph:
+    """A train_step recorded as a HIP graph (step_graph_create).  Holds
+    references to the buffers the recording uses so they outlive it."""
+
+    def __init__(self, handle: int, keep, stats: Dict):
+        self._h = handle
+        self._keep = keep
+        self.stats = stats
+
+    def launch(self, stream=None):
+        s = None
+        if stream is not None:
+            s = stream if isinstance(stream, int) else int(stream.cuda_stream)
+        _check(_lib.step_graph_launch(self._h, s))
+
+    def close(self):
+        if self._h:
+            _lib.step_graph_free(self._h)
+            self._h = None
+            self._keep = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def step_graph_create(net: Net, params, grads, batch_input, batch_target, plan: Plan, workspace,
+                      workspace_bytes: int, stream, loss_dev=None) -> StepGraph:
+    """Record one train_step (loss to loss_dev) on a non-default stream."""
+    b = Batch(_addr(batch_input), _addr(batch_target))
+    st = StepStats()
+    s = stream if isinstance(stream, int) else int(stream.cuda_stream)
+    ld = _addr(loss_dev)
+    out = C.c_void_p()
+    _check(_lib.step_graph_create(net.handle, _addr(params), _addr(grads), C.byref(b), plan.handle,
+                                  _addr(workspace), int(workspace_bytes), s,
+                                  C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
+                                  C.byref(out), C.byref(st)))
+    keep = (net, plan, params, grads, batch_input, batch_target, workspace, loss_dev)
+    return StepGraph(out.value, keep, st.as_dict())

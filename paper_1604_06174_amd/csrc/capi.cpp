@@ -18,6 +18,15 @@ struct ckpt_net {
 struct ckpt_graph_plan {
   ckpt::GraphPlan p;
 };
+// a recorded training step: the captured graph and its executable form
+struct ckpt_step_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  ~ckpt_step_graph() {
+    if (exec) (void)hipGraphExecDestroy(exec);
+    if (graph) (void)hipGraphDestroy(graph);
+  }
+};
 
 namespace ckpt {
 uint64_t workspace_bytes(const Net &net, const Accounting &acc);
@@ -53,6 +62,26 @@ int guarded(F &&f) {
 
 void need(const void *p, const char *what) {
   if (!p) ckpt::fail(CKPT_E_INVALID, std::string(what) + ": null pointer");
+}
+
+// the argument checks train_step and step_graph_create share
+void check_step_args(const char *fn, const ckpt_net *net, const void *params, const void *grads,
+                     const ckpt_batch *batch, const ckpt_plan *plan, const void *workspace) {
+  const std::string f(fn);
+  need(net, (f + "(net)").c_str());
+  need(params, (f + "(params)").c_str());
+  need(grads, (f + "(grads)").c_str());
+  need(batch, (f + "(batch)").c_str());
+  need(batch->input, (f + "(batch.input)").c_str());
+  need(batch->target, (f + "(batch.target)").c_str());
+  need(plan, (f + "(plan)").c_str());
+  need(workspace, (f + "(workspace)").c_str());
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    ckpt::fail(CKPT_E_INVALID, f + ": workspace must be 256-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
+    ckpt::fail(CKPT_E_INVALID, f + ": params and grads must be 256-byte aligned");
+  if (plan->p.n != net->net->n)
+    ckpt::fail(CKPT_E_MISMATCH, f + ": plan n differs from the net's unit count");
 }
 }  // namespace
 
@@ -315,25 +344,63 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
                const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats) {
   return guarded([&] {
-    need(net, "train_step(net)");
-    need(params, "train_step(params)");
-    need(grads, "train_step(grads)");
-    need(batch, "train_step(batch)");
-    need(batch->input, "train_step(batch.input)");
-    need(batch->target, "train_step(batch.target)");
-    need(plan, "train_step(plan)");
-    need(workspace, "train_step(workspace)");
-    if (reinterpret_cast<uintptr_t>(workspace) & 255)
-      ckpt::fail(CKPT_E_INVALID, "train_step: workspace must be 256-byte aligned");
-    if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
-      ckpt::fail(CKPT_E_INVALID, "train_step: params and grads must be 256-byte aligned");
-    if (plan->p.n != net->net->n)
-      ckpt::fail(CKPT_E_MISMATCH, "train_step: plan n differs from the net's unit count");
+    check_step_args("train_step", net, params, grads, batch, plan, workspace);
     ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
                          *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
                          static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
   });
 }
+
+int step_graph_create(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+                      const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes,
+                      void *stream, float *loss_dev, ckpt_step_graph **out,
+                      ckpt_step_stats *stats) {
+  return guarded([&] {
+    need(out, "step_graph_create(out)");
+    *out = nullptr;
+    check_step_args("step_graph_create", net, params, grads, batch, plan, workspace);
+    if (!stream)
+      ckpt::fail(CKPT_E_INVALID, "step_graph_create: capture needs a stream other than the default one");
+    if (net->net->timer.enabled)
+      ckpt::fail(CKPT_E_INVALID, "step_graph_create: turn kernel timing off before recording");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(s, &cs);
+    if (e != hipSuccess)
+      ckpt::fail(CKPT_E_HIP, std::string("step_graph_create: ") + hipGetErrorString(e));
+    if (cs != hipStreamCaptureStatusNone)
+      ckpt::fail(CKPT_E_INVALID, "step_graph_create: the stream is already being captured");
+    auto g = std::make_unique<ckpt_step_graph>();
+    e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess)
+      ckpt::fail(CKPT_E_HIP, std::string("step_graph_create: ") + hipGetErrorString(e));
+    try {
+      ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
+                           *batch, plan->p, static_cast<char *>(workspace), workspace_bytes, s,
+                           loss_dev, nullptr, nullptr, stats);
+    } catch (...) {
+      hipGraph_t partial = nullptr;
+      (void)hipStreamEndCapture(s, &partial);
+      if (partial) (void)hipGraphDestroy(partial);
+      throw;
+    }
+    e = hipStreamEndCapture(s, &g->graph);
+    if (e == hipSuccess) e = hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0);
+    if (e != hipSuccess)
+      ckpt::fail(CKPT_E_HIP, std::string("step_graph_create: ") + hipGetErrorString(e));
+    *out = g.release();
+  });
+}
+
+int step_graph_launch(ckpt_step_graph *graph, void *stream) {
+  return guarded([&] {
+    need(graph, "step_graph_launch(graph)");
+    const hipError_t e = hipGraphLaunch(graph->exec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) ckpt::fail(CKPT_E_HIP, std::string("step_graph_launch: ") + hipGetErrorString(e));
+  });
+}
+
+void step_graph_free(ckpt_step_graph *graph) { delete graph; }
 
 int net_node_graph(const ckpt_net *net, int32_t *n_nodes, int32_t *n_edges, int32_t *pred_ptr,
                    int32_t *pred_idx, uint64_t *out_bytes, int32_t *flags, int32_t cap_nodes,

@@ -80,6 +80,13 @@ class GpuStep:
         return K.train_step(self.net, self.params, self.grads, self.input, self.target, plan, ws,
                             ws.numel(), s, self.loss_dev, want_loss)
 
+    def record(self, plan: K.Plan, stream: torch.cuda.Stream) -> K.StepGraph:
+        """One step under `plan` recorded as a HIP graph on a non-default stream;
+        launching it repeats run(plan) on the same buffers."""
+        ws = self.workspace(plan)
+        return K.step_graph_create(self.net, self.params, self.grads, self.input, self.target, plan,
+                                   ws, ws.numel(), stream, self.loss_dev)
+
     def graph_plan(self, mirror=None, strategy: int = K.ALLOC_SHARE) -> K.GraphPlan:
         g = self.net.node_graph()
         return K.graph_plan(g["pred"], g["bytes"], g["flags"], mirror, strategy)

@@ -205,6 +205,19 @@ def test_train_step_rejects_before_launch():
     with pytest.raises(K.CkptError) as ei:
         K.train_step(net, fake, fake, 0, fake, plan, fake, need)
     assert ei.value.code == K.E_INVALID
+    # recording a step: the same argument checks, and the default stream is refused
+    with pytest.raises(K.CkptError) as ei:
+        K.step_graph_create(net, fake, fake, fake, fake, other, fake, need, fake)
+    assert ei.value.code == K.E_MISMATCH
+    with pytest.raises(K.CkptError) as ei:
+        K.step_graph_create(net, fake, fake, fake, fake, plan, fake + 16, need, fake)
+    assert ei.value.code == K.E_INVALID
+    with pytest.raises(K.CkptError) as ei:
+        K.step_graph_create(net, fake, fake, fake, fake, plan, fake, need, 0)
+    assert ei.value.code == K.E_INVALID and "default" in str(ei.value)
+    with pytest.raises(K.CkptError) as ei:
+        K.StepGraph(0, None, {}).launch(fake)
+    assert ei.value.code == K.E_INVALID
 
 
 def test_single_hip_runtime_in_process():

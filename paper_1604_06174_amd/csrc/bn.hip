@@ -2,7 +2,7 @@
 // its backward, and the global-average-pool + FC + softmax cross-entropy head.
 // NHWC fp32 tensors; channel counts are multiples of 4 so every thread moves
 // one float4 of channels.  Channel sums are accumulated in float64 and
-// reduced in a fixed order (per-workgroup partials, then a tree), so the
+// reduced in a fixed order (per-workgroup partials, then a fixed combine), so the
 // results are bit-reproducible and insensitive to cancellation in
 // E[x^2] - E[x]^2.
 #include <hip/hip_runtime.h>
@@ -73,13 +73,18 @@ __global__ __launch_bounds__(256) void k_bn_bwd_partials(int P, int J, int PB, c
   if (pl == 0) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      part[(size_t(blockIdx.x) * 2 + 0) * J + c0 + k] = red[0][threadIdx.x][k];
-      part[(size_t(blockIdx.x) * 2 + 1) * J + c0 + k] = red[1][threadIdx.x][k];
+      part[size_t(c0 + k) * gridDim.x + blockIdx.x] = red[0][threadIdx.x][k];
+      part[(size_t(J) + c0 + k) * gridDim.x + blockIdx.x] = red[1][threadIdx.x][k];
     }
   }
 }
 
-// One workgroup per channel: sum the per-workgroup partials in a fixed order.
+// One workgroup per channel j: the per-workgroup partials of the two sums are
+// stored channel-major (part[(w * J + j) * nb + k], w = 0, 1), so a channel's
+// partials are contiguous and read with coalesced loads.  Fixed order: thread
+// t adds k = t, t + 256, ... in turn, each wavefront combines its 64 lanes by
+// a butterfly (the value lane 0 ends with), and the four wavefront sums are
+// added in wavefront order.
 //   FWD: partials are (sum v, sum v^2) -> out0 = mean, out1 = rstd
 //   BWD: partials are (sum ds, sum ds*xhat) -> out0 = mean(ds),
 //        out1 = mean(ds*xhat); dgamma = sum ds*xhat, dbeta = sum ds
@@ -88,17 +93,17 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ 
                                                      double m, float *__restrict__ out,
                                                      float *__restrict__ dgamma,
                                                      float *__restrict__ dbeta) {
-  __shared__ double r0[256], r1[256];
+  __shared__ double r0[4], r1[4];
   const int j = blockIdx.x;
+  const double *p0 = part + size_t(j) * nb, *p1 = part + (size_t(J) + j) * nb;
   double a = 0, b = 0;
-  // k = tid, tid + 256, ... in order; four partials in flight per round
   int k = threadIdx.x;
-  for (; k + 3 * 256 < nb; k += 4 * 256) {
+  for (; k + 3 * 256 < nb; k += 4 * 256) {  // four partials of each sum in flight
     double ta[4], tb[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      ta[u] = part[(size_t(k + 256 * u) * 2 + 0) * J + j];
-      tb[u] = part[(size_t(k + 256 * u) * 2 + 1) * J + j];
+      ta[u] = p0[k + 256 * u];
+      tb[u] = p1[k + 256 * u];
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -107,31 +112,34 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ 
     }
   }
   for (; k < nb; k += 256) {
-    a += part[(size_t(k) * 2 + 0) * J + j];
-    b += part[(size_t(k) * 2 + 1) * J + j];
+    a += p0[k];
+    b += p1[k];
   }
-  r0[threadIdx.x] = a;
-  r1[threadIdx.x] = b;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off);
+    b += __shfl_xor(b, off);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    r0[wave] = a;
+    r1[wave] = b;
+  }
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) {
-      r0[threadIdx.x] += r0[threadIdx.x + w];
-      r1[threadIdx.x] += r1[threadIdx.x + w];
-    }
-    __syncthreads();
-  }
   if (threadIdx.x == 0) {
+    const double sa = ((r0[0] + r0[1]) + r0[2]) + r0[3];
+    const double sb = ((r1[0] + r1[1]) + r1[2]) + r1[3];
     if (FWD) {
-      const double mean = r0[0] / m;
-      double var = r1[0] / m - mean * mean;
+      const double mean = sa / m;
+      double var = sb / m - mean * mean;
       if (var < 0) var = 0;
       out[j] = float(mean);
       out[J + j] = float(1.0 / sqrt(var + double(BN_EPS)));
     } else {
-      out[j] = float(r0[0] / m);
-      out[J + j] = float(r1[0] / m);
-      dbeta[j] = float(r0[0]);
-      dgamma[j] = float(r1[0]);
+      out[j] = float(sa / m);
+      out[J + j] = float(sb / m);
+      dbeta[j] = float(sa);
+      dgamma[j] = float(sb);
     }
   }
 }

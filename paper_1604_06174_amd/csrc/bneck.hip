@@ -141,8 +141,8 @@ __global__ __launch_bounds__(256) void k_bnb_bwd_partials(int P, int J, int PB, 
   if (pl == 0) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      part[(size_t(blockIdx.x) * 2 + 0) * J + c0 + k] = red[0][threadIdx.x][k];
-      part[(size_t(blockIdx.x) * 2 + 1) * J + c0 + k] = red[1][threadIdx.x][k];
+      part[size_t(c0 + k) * gridDim.x + blockIdx.x] = red[0][threadIdx.x][k];
+      part[(size_t(J) + c0 + k) * gridDim.x + blockIdx.x] = red[1][threadIdx.x][k];
     }
   }
 }

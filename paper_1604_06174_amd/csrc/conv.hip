@@ -13,7 +13,8 @@
 //          samples) and correlated with the flipped kernel:
 //          in = dy_up[n, h + 1 - kh, w + 1 - kw, c], B = W[c, kh, kw, j]
 // Epilogues: STATS (store, plus per-workgroup float64 sums of v and v^2 per
-// channel for batch-norm statistics), MASK (store acc * [m > 0]), SC1 / SC2
+// channel for batch-norm statistics, stored channel-major: all workgroups'
+// sums of one channel are contiguous), MASK (store acc * [m > 0]), SC1 / SC2
 // (add the shortcut's gradient g * [y > 0]: identity, or the option-A
 // subsample-and-zero-pad shortcut of a stride-2 block).
 //
@@ -41,7 +42,7 @@ struct ConvArgs {
   int R, rblk;      // output rows per workgroup, workgroups per image
   const float *E0, *E1;  // epilogue operands (MASK: E0; SC: E0 = g, E1 = y)
   int Eh, Ew, Ec;        // SC2: dims of g and y
-  double *stats;         // STATS: [gridDim.x][2][J]
+  double *stats;         // STATS: [2][J][gridDim.x] (sum v, sum v^2; channel-major)
   const float *tst, *tg, *tb;  // optional bn_relu: FWD input / DGRAD MASK transform
 };
 
@@ -236,7 +237,7 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
       const int which = tid / BN, jj = tid % BN;
       double acc2 = 0.0;
       for (int k = 0; k < 16; ++k) acc2 += red[(k * 2 + which) * BN + jj];
-      if (j0 + jj < a.J) a.stats[(size_t(blk) * 2 + which) * a.J + j0 + jj] = acc2;
+      if (j0 + jj < a.J) a.stats[(size_t(which) * a.J + j0 + jj) * gridDim.x + blk] = acc2;
     }
   }
 }
@@ -488,7 +489,7 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
       const int which = tid / BN, jj = tid % BN;
       double acc2 = 0.0;
       for (int k = 0; k < 16; ++k) acc2 += red[(k * 2 + which) * BN + jj];
-      if (j0 + jj < J) a.stats[(size_t(blockIdx.x) * 2 + which) * J + j0 + jj] = acc2;
+      if (j0 + jj < J) a.stats[(size_t(which) * J + j0 + jj) * gridDim.x + blockIdx.x] = acc2;
     }
   }
 }

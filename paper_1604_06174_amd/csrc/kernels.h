@@ -52,7 +52,7 @@ enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 =
 // Y[N,H,W,J] = conv of X[N,Hx,Wx,C] (FWD: stride S; DGRAD: gradient of a
 // stride-S forward conv, X = dy).  Epilogue operands: MASK E0 = mask tensor
 // shaped like Y; SC1 E0 = g, E1 = y shaped like Y; SC2 E0 = g, E1 = y of dims
-// [N, Eh, Ew, Ec].  STATS writes [blocks][2][J] float64 channel sums.
+// [N, Eh, Ew, Ec].  STATS writes [2][J][blocks] float64 channel sums.
 // Optional batch-norm + ReLU transform (tst = mean | rstd, tg = gamma,
 // tb = beta): FWD applies bn_relu to every in-image input value (channel c);
 // DGRAD with MASK takes the mask as bn_relu(E0) (channel j) instead of E0.
@@ -125,7 +125,7 @@ void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, i
                int ldd = 0, const float *bias = nullptr);
 // Options: splits > 1 = split-K, C receives splits partial [M, ldc] products
 // (STORE); ADDMASK: C = acc + (mask > 0 ? D : 0), mask bf16 shaped like D;
-// BF16STATS: Cb (bf16, ldc) = round(acc) and stats[row block][2][N] float64
+// BF16STATS: Cb (bf16, ldc) = round(acc) and stats[2][N][row blocks] float64
 // sums of the rounded values and squares (row blocks: gemm_bf16_row_blocks).
 struct GemmX {
   int splits = 1;

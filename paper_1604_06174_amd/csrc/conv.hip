@@ -24,6 +24,7 @@
 // in a fixed order.  No atomics anywhere: results are bit-reproducible.
 #include <hip/hip_runtime.h>
 
+#include "common.h"
 #include "kernels.h"
 
 namespace ckpt {
@@ -44,6 +45,7 @@ struct ConvArgs {
   int Eh, Ew, Ec;        // SC2: dims of g and y
   double *stats;         // STATS: [2][J][gridDim.x] (sum v, sum v^2; channel-major)
   const float *tst, *tg, *tb;  // optional bn_relu: FWD input / DGRAD MASK transform
+  float *rout;  // FWD, stride 1, with tst: the transformed input rows the workgroup owns
 };
 
 // bn_relu of four consecutive channels c..c+3 (C = channel count of the
@@ -109,6 +111,10 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
           for (int k = 0; k < 4; ++k)
             if (c4 + k < a.C)
               v[k] = bn_relu(v[k], a.tst[c4 + k], a.tst[a.C + c4 + k], a.tg[c4 + k], a.tb[c4 + k]);
+          // stride 1: halo rows 1..R are this workgroup's own output rows
+          if (MODE == CONV_FWD && S == 1 && a.rout && blockIdx.y == 0 && hr >= 1 && hr <= a.R)
+            *reinterpret_cast<float4 *>(a.rout + ((size_t(n) * a.Hx + ir) * a.Wx + ic) * a.C + c4) =
+                make_float4(v[0], v[1], v[2], v[3]);
         }
       }
       *reinterpret_cast<float4 *>(halo + (hr * HC + hc) * Cs + c4) = make_float4(v[0], v[1], v[2], v[3]);
@@ -343,6 +349,18 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
                               bn_relu(hv[k].y, tm[1], tr[1], tg[1], tb[1]),
                               bn_relu(hv[k].z, tm[2], tr[2], tg[2], tb[2]),
                               bn_relu(hv[k].w, tm[3], tr[3], tg[3], tb[3]));
+      // stride 1: halo rows 1..RB are this workgroup's own output rows; the
+      // first channel block stores them (every element once over the grid)
+      if (S == 1 && a.rout && blockIdx.y == 0) {
+#pragma unroll
+        for (int k = 0; k < NH; ++k) {
+          const int e = tid + 256 * k;
+          const int c4 = e % C4, hc = (e / C4) % HC, hr = e / (C4 * HC);
+          const int ir = r0 - 1 + hr, ic = hc - 1;
+          if (hok[k] && hr >= 1 && hr <= RB)
+            *reinterpret_cast<float4 *>(a.rout + ((size_t(n) * Hx + ir) * WX + ic) * C + 4 * c4) = hv[k];
+        }
+      }
     }
 #pragma unroll
     for (int k = 0; k < NH; ++k) {
@@ -765,6 +783,8 @@ __global__ __launch_bounds__(256) void k_wgrad_s(WgArgs a) {
     const int nn = n0 + t * 16 + i16;
     const int tap = nn / C, c = nn % C;
     bok[t] = t < NT && nn < NC;
+    // a column outside the slice reads the halo's first element: its
+    // accumulator is never stored
     boff[t] = bok[t] ? ((tap / 3) * HC + tap % 3) * Cs + c : 0;
   }
   floatx4 acc[9];
@@ -805,18 +825,30 @@ __global__ __launch_bounds__(256) void k_wgrad_s(WgArgs a) {
       *reinterpret_cast<float4 *>(dys + p * JS + j4) = v;
     }
     __syncthreads();
-    constexpr int PK = NPIX / WGK;
+    // k steps of 4 pixels: the ten LDS operands of step s + 1 are read before
+    // the nine MFMAs of step s are issued (the scheduling barriers keep that
+    // order), so LDS latency overlaps matrix-core work
+    constexpr int PK = NPIX / WGK, NSTEP = PK / 4;
     const int kb = my_kg * PK;
     const float *Ab = dys + my_jt * 16 + i16;
-    for (int k0 = kb; k0 < kb + PK; k0 += 4) {
-      const int p = k0 + q;
+    float av[2], bv[2][9];
+    auto rd = [&](int st, float &a1, float (&b1)[9]) {
+      const int p = kb + 4 * st + q;
       const int pb = ((p / W) * S * HC + (p % W) * S) * Cs;
-      const float av = Ab[p * JS];
+      a1 = Ab[p * JS];
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const float bv = bok[t] ? halo[pb + boff[t]] : 0.f;
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t], 0, 0, 0);
-      }
+      for (int t = 0; t < 9; ++t) b1[t] = halo[pb + boff[t]];
+    };
+    rd(0, av[0], bv[0]);
+#pragma unroll 2
+    for (int st = 0; st < NSTEP; ++st) {
+      const int cur = st & 1;
+      if (st + 1 < NSTEP) rd(st + 1, av[cur ^ 1], bv[cur ^ 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[cur], bv[cur][t], acc[t], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -1062,10 +1094,12 @@ bool conv3x3_supported(int mode, int S, int H, int W, int C, int J) {
 void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
              int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1,
              int Eh, int Ew, int Ec, double *stats, const float *tst, const float *tg,
-             const float *tb) {
+             const float *tb, float *rout) {
+  if (rout && (mode != CONV_FWD || S != 1 || !tst || (C & 3) != 0))
+    fail(CKPT_E_INVALID, "conv3x3: the transformed input is stored only by a stride-1 forward with a transform");
   Tile t = conv_tile(mode, S, H, W, C, J);
   const int NSUB = J > 16 ? 2 : 1;
-  ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats, tst, tg, tb};
+  ConvArgs a{X, Wt, Y, N, H, W, Hx, Wx, C, J, t.R, t.rblk, E0, E1, Eh, Ew, Ec, stats, tst, tg, tb, rout};
   if (spec_dispatch(a, mode, S, epi, st, true, nullptr)) return;
   dim3 grid(N * t.rblk, (J + 16 * NSUB - 1) / (16 * NSUB));
   const size_t lds = conv_lds(mode, S, t.R, W, C, J);

@@ -56,11 +56,13 @@ enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 =
 // Optional batch-norm + ReLU transform (tst = mean | rstd, tg = gamma,
 // tb = beta): FWD applies bn_relu to every in-image input value (channel c);
 // DGRAD with MASK takes the mask as bn_relu(E0) (channel j) instead of E0.
+// rout (stride-1 FWD with the transform, C a multiple of 4): the transformed
+// input [N,Hx,Wx,C] is also stored, every element once.
 void conv3x3(hipStream_t s, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
              int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0 = nullptr,
              const float *E1 = nullptr, int Eh = 0, int Ew = 0, int Ec = 0,
              double *stats = nullptr, const float *tst = nullptr, const float *tg = nullptr,
-             const float *tb = nullptr);
+             const float *tb = nullptr, float *rout = nullptr);
 int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J);
 int conv3x3_wgrad_blocks(int S, int N, int H, int W, int C, int J);
 bool conv3x3_supported(int mode, int S, int H, int W, int C, int J);

@@ -12,12 +12,14 @@
 // mean/rstd pair of Cout floats each, both rounded up to 256 bytes):
 //   stem   a = c | st            q = dc
 //   block  a = c1 | r1 | c2 | st1 | st2     q = two T buffers
+// The second convolution reads c1 and forms r1 = relu(bn1(c1)) as it loads
+// it; when r1 is kept it stores r1 as well (no separate batch-norm pass).
 // With drop_bn_relu the blocks keep only the convolution outputs, a = c1 | c2
-// | st1 | st2, and r1 = relu(bn1(c1)) is formed on the fly from c1 and its
-// statistics wherever it is read (the second convolution's input, its data
-// gradient's ReLU mask and its weight gradient's input): the "drop bn-relu"
-// memory plan the paper applies to the conv-BN-activation pipeline
-// (section 4.2), with the same bits as the stored r1.
+// | st1 | st2, and r1 is formed on the fly from c1 and its statistics
+// wherever it is read (the second convolution's input, its data gradient's
+// ReLU mask and its weight gradient's input): the "drop bn-relu" memory plan
+// the paper applies to the conv-BN-activation pipeline (section 4.2), with the
+// same bits as the stored r1.
 // The boundary b_i is the unit's input tensor (b_0 = the image batch).
 #include <algorithm>
 
@@ -149,14 +151,15 @@ class ResNetBasic : public Net {
   void conv(StepCtx &c, int mode, int s, int epi, const float *X, const float *Wt, float *Y, int H,
             int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1, int Eh, int Ew,
             int Ec, int ho, int cin, int cout, const float *tst = nullptr, const float *tg = nullptr,
-            const float *tb = nullptr) {
+            const float *tb = nullptr, float *rout = nullptr) {
     const double fl = 2.0 * N * ho * ho * double(cout) * 9.0 * cin;
     double by = 4.0 * (double(N) * Hx * Wx * C + 9.0 * cin * cout + double(N) * H * W * J);
     if (epi == CONV_EPI_MASK) by += 4.0 * N * H * W * J;
     if (epi == CONV_EPI_SC1 || epi == CONV_EPI_SC2) by += 2 * 4.0 * N * Eh * Ew * std::min(Ec, J);
+    if (rout) by += 4.0 * N * Hx * Wx * C;  // the transformed input, written once
     timer.begin(c.s);
     conv3x3(c.s, mode, s, epi, X, Wt, Y, N, H, W, Hx, Wx, C, J, E0, E1, Eh, Ew, Ec,
-            epi == CONV_EPI_STATS ? bnpart(c) : nullptr, tst, tg, tb);
+            epi == CONV_EPI_STATS ? bnpart(c) : nullptr, tst, tg, tb, rout);
     timer.end(c.s, fl, by);
   }
   float *ksf(StepCtx &c, uint64_t off) const { return reinterpret_cast<float *>(c.ks + off); }
@@ -185,15 +188,11 @@ class ResNetBasic : public Net {
          k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
                     k.cout, np, st1);
-    if (drop) {  // the second convolution forms relu(bn1(c1)) on its input
-      conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
-           nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1));
-      c.launches -= 1;
-    } else {
-      bn_apply(c.s, BN_RES_NONE, np, k.cout, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, r1);
-      conv(c, CONV_FWD, 1, CONV_EPI_STATS, r1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout,
-           nullptr, nullptr, 0, 0, 0, ho, k.cout, k.cout);
-    }
+    // the second convolution forms r1 = relu(bn1(c1)) on its input; when r1
+    // is kept it also stores it (the rows each workgroup owns)
+    conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout, nullptr,
+         nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1), drop ? nullptr : r1);
+    c.launches -= 1;
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
                     np, st2);
     bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),

@@ -224,7 +224,8 @@ def main():
     dtype = cfg.get("dtype", "f32")  # "bf16": bf16 GEMM operands, fp32 accumulation
     achieved = kt["flops"] / (kt["ms"] / 1e3) / 1e12 if kt["ms"] > 0 else 0.0
     peak = PEAK_TFLOPS[dtype]
-    tr = _traffic(args.workload)
+    # counters were taken on the workload's default layout and plan family only
+    tr = None if args.drop_bn_relu else _traffic(args.workload)
     alg_bytes = kt["bytes"] / max(kt["launches"], 1)
     roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),

@@ -34,22 +34,35 @@ __global__ __launch_bounds__(256) void k_bn_bwd_partials(int P, int J, int PB, c
   }
   double s1[4] = {0, 0, 0, 0}, s2[4] = {0, 0, 0, 0};
   if (pl < PL) {
-    for (int p = p0 + pl; p < p1; p += PL) {
-      const size_t o = size_t(p) * J + c0;
-      const float4 g = *reinterpret_cast<const float4 *>(G + o);
-      const float4 c = *reinterpret_cast<const float4 *>(Cv + o);
-      float gv[4] = {g.x, g.y, g.z, g.w}, cv[4] = {c.x, c.y, c.z, c.w};
-      if (MASKED) {
-        const float4 y = *reinterpret_cast<const float4 *>(Ym + o);
-        float yv[4] = {y.x, y.y, y.z, y.w};
+    // pixels p0 + pl, + PL, + 2 PL, ... in turn; the loads of four of them are
+    // issued before any is used (a pixel past the range reads p and is skipped)
+    for (int p = p0 + pl; p < p1; p += 4 * PL) {
+      float4 g[4], c[4], y[4];
+      bool ok[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) gv[k] = yv[k] > 0.f ? gv[k] : 0.f;
+      for (int u = 0; u < 4; ++u) {
+        const int pp = p + u * PL;
+        ok[u] = pp < p1;
+        const size_t o = size_t(ok[u] ? pp : p) * J + c0;
+        g[u] = *reinterpret_cast<const float4 *>(G + o);
+        c[u] = *reinterpret_cast<const float4 *>(Cv + o);
+        if (MASKED) y[u] = *reinterpret_cast<const float4 *>(Ym + o);
       }
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float xh = (cv[k] - mean[k]) * rstd[k];
-        s1[k] += double(gv[k]);
-        s2[k] += double(gv[k]) * double(xh);
+      for (int u = 0; u < 4; ++u) {
+        if (!ok[u]) continue;
+        float gv[4] = {g[u].x, g[u].y, g[u].z, g[u].w}, cv[4] = {c[u].x, c[u].y, c[u].z, c[u].w};
+        if (MASKED) {
+          const float yv[4] = {y[u].x, y[u].y, y[u].z, y[u].w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) gv[k] = yv[k] > 0.f ? gv[k] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float xh = (cv[k] - mean[k]) * rstd[k];
+          s1[k] += double(gv[k]);
+          s2[k] += double(gv[k]) * double(xh);
+        }
       }
     }
   }
@@ -79,31 +92,55 @@ __global__ __launch_bounds__(256) void k_bn_bwd_partials(int P, int J, int PB, c
   }
 }
 
-// One workgroup per channel j: the per-workgroup partials of the two sums are
-// stored channel-major (part[(w * J + j) * nb + k], w = 0, 1), so a channel's
-// partials are contiguous and read with coalesced loads.  Fixed order: thread
-// t adds k = t, t + 256, ... in turn, each wavefront combines its 64 lanes by
-// a butterfly (the value lane 0 ends with), and the four wavefront sums are
-// added in wavefront order.
+// One workgroup per channel j; the per-workgroup partials k = 0..nb-1 of the
+// two sums w = 0, 1 are stored either channel-major, part[(w * J + j) * nb + k]
+// (a channel's partials contiguous: coalesced loads; for producers that write
+// few channels per workgroup), or block-major, part[(k * 2 + w) * J + j] (each
+// workgroup's sums contiguous: coalesced stores for producers that write many
+// channels).  Fixed order either way: thread t adds k = t, t + 256, ... in
+// turn, each wavefront combines its 64 lanes by a butterfly (the value lane 0
+// ends with), and the four wavefront sums are added in wavefront order.
 //   FWD: partials are (sum v, sum v^2) -> out0 = mean, out1 = rstd
 //   BWD: partials are (sum ds, sum ds*xhat) -> out0 = mean(ds),
 //        out1 = mean(ds*xhat); dgamma = sum ds*xhat, dbeta = sum ds
+// channel j's statistics from its two sums over m values
 template <bool FWD>
+__device__ __forceinline__ void finalize_channel(int j, int J, double sa, double sb, double m,
+                                                 float *__restrict__ out, float *__restrict__ dgamma,
+                                                 float *__restrict__ dbeta) {
+  if (FWD) {
+    const double mean = sa / m;
+    double var = sb / m - mean * mean;
+    if (var < 0) var = 0;
+    out[j] = float(mean);
+    out[J + j] = float(1.0 / sqrt(var + double(BN_EPS)));
+  } else {
+    out[j] = float(sa / m);
+    out[J + j] = float(sb / m);
+    dbeta[j] = float(sa);
+    dgamma[j] = float(sb);
+  }
+}
+
+template <bool FWD, bool CM>
 __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ part, int nb, int J,
                                                      double m, float *__restrict__ out,
                                                      float *__restrict__ dgamma,
                                                      float *__restrict__ dbeta) {
   __shared__ double r0[4], r1[4];
   const int j = blockIdx.x;
-  const double *p0 = part + size_t(j) * nb, *p1 = part + (size_t(J) + j) * nb;
+  // element k of sum w at p_w[k * step]
+  const double *p0 = CM ? part + size_t(j) * nb : part + j;
+  const double *p1 = CM ? part + (size_t(J) + j) * nb : part + J + j;
+  const size_t step = CM ? 1 : size_t(2) * J;
   double a = 0, b = 0;
   int k = threadIdx.x;
   for (; k + 3 * 256 < nb; k += 4 * 256) {  // four partials of each sum in flight
     double ta[4], tb[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      ta[u] = p0[k + 256 * u];
-      tb[u] = p1[k + 256 * u];
+      ta[u] = p0[(k + 256 * u) * step];
+      tb[u] = p1[(k + 256 * u) * step];
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -112,8 +149,8 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ 
     }
   }
   for (; k < nb; k += 256) {
-    a += p0[k];
-    b += p1[k];
+    a += p0[k * step];
+    b += p1[k * step];
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -126,21 +163,55 @@ __global__ __launch_bounds__(256) void k_bn_finalize(const double *__restrict__ 
     r1[wave] = b;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const double sa = ((r0[0] + r0[1]) + r0[2]) + r0[3];
-    const double sb = ((r1[0] + r1[1]) + r1[2]) + r1[3];
-    if (FWD) {
-      const double mean = sa / m;
-      double var = sb / m - mean * mean;
-      if (var < 0) var = 0;
-      out[j] = float(mean);
-      out[J + j] = float(1.0 / sqrt(var + double(BN_EPS)));
-    } else {
-      out[j] = float(sa / m);
-      out[J + j] = float(sb / m);
-      dbeta[j] = float(sa);
-      dgamma[j] = float(sb);
+  if (threadIdx.x == 0)
+    finalize_channel<FWD>(j, J, ((r0[0] + r0[1]) + r0[2]) + r0[3], ((r1[0] + r1[1]) + r1[2]) + r1[3], m,
+                          out, dgamma, dbeta);
+}
+
+// Block-major partials of many channels: a workgroup takes 16 consecutive
+// channels (16 lanes read 128 contiguous bytes per partial) and splits the nb
+// partials into 16 slices; slice s adds k = s, s + 16, ... in turn (eight
+// loads in flight), and the 16 slice sums of a channel are added in slice
+// order.
+template <bool FWD>
+__global__ __launch_bounds__(256) void k_bn_finalize_wide(const double *__restrict__ part, int nb, int J,
+                                                          double m, float *__restrict__ out,
+                                                          float *__restrict__ dgamma,
+                                                          float *__restrict__ dbeta) {
+  __shared__ double r0[16][17], r1[16][17];
+  const int cl = threadIdx.x % 16, sl = threadIdx.x / 16;
+  const int j = blockIdx.x * 16 + cl;
+  double a = 0, b = 0;
+  if (j < J) {
+    int k = sl;
+    for (; k + 7 * 16 < nb; k += 8 * 16) {
+      double ta[8], tb[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        ta[u] = part[(size_t(k + 16 * u) * 2 + 0) * J + j];
+        tb[u] = part[(size_t(k + 16 * u) * 2 + 1) * J + j];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        a += ta[u];
+        b += tb[u];
+      }
     }
+    for (; k < nb; k += 16) {
+      a += part[(size_t(k) * 2 + 0) * J + j];
+      b += part[(size_t(k) * 2 + 1) * J + j];
+    }
+  }
+  r0[sl][cl] = a;
+  r1[sl][cl] = b;
+  __syncthreads();
+  if (sl == 0 && j < J) {
+    double sa = 0, sb = 0;
+    for (int t = 0; t < 16; ++t) {
+      sa += r0[t][cl];
+      sb += r1[t][cl];
+    }
+    finalize_channel<FWD>(j, J, sa, sb, m, out, dgamma, dbeta);
   }
 }
 
@@ -330,15 +401,33 @@ static int64_t bn_pb(int64_t P, int J) {
   return (P + nb - 1) / nb;
 }
 
-void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st) {
-  hipLaunchKernelGGL((k_bn_finalize<true>), dim3(J), dim3(256), 0, s, part, nb, J, double(m), st,
-                     nullptr, nullptr);
+// block-major partials of this many channels or more take the tiled finalize
+constexpr int BN_WIDE_J = 512;
+
+void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st,
+                     bool channel_major) {
+  if (!channel_major && J >= BN_WIDE_J)
+    hipLaunchKernelGGL((k_bn_finalize_wide<true>), dim3((J + 15) / 16), dim3(256), 0, s, part, nb, J,
+                       double(m), st, nullptr, nullptr);
+  else if (channel_major)
+    hipLaunchKernelGGL((k_bn_finalize<true, true>), dim3(J), dim3(256), 0, s, part, nb, J, double(m),
+                       st, nullptr, nullptr);
+  else
+    hipLaunchKernelGGL((k_bn_finalize<true, false>), dim3(J), dim3(256), 0, s, part, nb, J, double(m),
+                       st, nullptr, nullptr);
 }
 
 void bn_finalize_bwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *sums,
-                     float *dgamma, float *dbeta) {
-  hipLaunchKernelGGL((k_bn_finalize<false>), dim3(J), dim3(256), 0, s, part, nb, J, double(m), sums,
-                     dgamma, dbeta);
+                     float *dgamma, float *dbeta, bool channel_major) {
+  if (!channel_major && J >= BN_WIDE_J)
+    hipLaunchKernelGGL((k_bn_finalize_wide<false>), dim3((J + 15) / 16), dim3(256), 0, s, part, nb, J,
+                       double(m), sums, dgamma, dbeta);
+  else if (channel_major)
+    hipLaunchKernelGGL((k_bn_finalize<false, true>), dim3(J), dim3(256), 0, s, part, nb, J, double(m),
+                       sums, dgamma, dbeta);
+  else
+    hipLaunchKernelGGL((k_bn_finalize<false, false>), dim3(J), dim3(256), 0, s, part, nb, J, double(m),
+                       sums, dgamma, dbeta);
 }
 
 void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const float *st,
@@ -361,8 +450,7 @@ void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Y
     hipLaunchKernelGGL((k_bn_bwd_partials<true>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, Ym, Cv, st, part);
   else
     hipLaunchKernelGGL((k_bn_bwd_partials<false>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, Ym, Cv, st, part);
-  hipLaunchKernelGGL((k_bn_finalize<false>), dim3(J), dim3(256), 0, s, part, nb, J, double(P), sums,
-                     dgamma, dbeta);
+  bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta, true);
   const int g = ew_grid(P * (J / 4));
   if (Ym)
     hipLaunchKernelGGL((k_bn_bwd_apply<true>), dim3(g), dim3(256), 0, s, P, J, G, Ym, Cv, st, gamma, sums, D);

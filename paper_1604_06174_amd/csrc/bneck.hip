@@ -103,22 +103,33 @@ __global__ __launch_bounds__(256) void k_bnb_bwd_partials(int P, int J, int PB, 
 #pragma unroll
   for (int k = 0; k < 8; ++k) s1[k] = s2[k] = 0.0;
   if (pl < PL) {
-    for (int p = p0 + pl; p < p1; p += PL) {
-      const size_t o = size_t(p) * J + c0;
-      float g[8], c[8];
-      load8f(G + o, g);
-      load8(Cv + o, c);
-      if (MASKED) {
-        float y[8];
-        load8(Ym + o, y);
+    // pixels p0 + pl, + PL, + 2 PL, ... in turn; the loads of four of them are
+    // issued before any is used (a pixel past the range reads p and is skipped)
+    for (int p = p0 + pl; p < p1; p += 4 * PL) {
+      float g[4][8], c[4][8], y[4][8];
+      bool ok[4];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) g[k] = y[k] > 0.f ? g[k] : 0.f;
+      for (int u = 0; u < 4; ++u) {
+        const int pp = p + u * PL;
+        ok[u] = pp < p1;
+        const size_t o = size_t(ok[u] ? pp : p) * J + c0;
+        load8f(G + o, g[u]);
+        load8(Cv + o, c[u]);
+        if (MASKED) load8(Ym + o, y[u]);
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float xh = (c[k] - mean[k]) * rstd[k];
-        s1[k] += double(g[k]);
-        s2[k] += double(g[k]) * double(xh);
+      for (int u = 0; u < 4; ++u) {
+        if (!ok[u]) continue;
+        if (MASKED) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) g[u][k] = y[u][k] > 0.f ? g[u][k] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float xh = (c[u][k] - mean[k]) * rstd[k];
+          s1[k] += double(g[u][k]);
+          s2[k] += double(g[u][k]) * double(xh);
+        }
       }
     }
   }
@@ -141,8 +152,8 @@ __global__ __launch_bounds__(256) void k_bnb_bwd_partials(int P, int J, int PB, 
   if (pl == 0) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      part[size_t(c0 + k) * gridDim.x + blockIdx.x] = red[0][threadIdx.x][k];
-      part[(size_t(J) + c0 + k) * gridDim.x + blockIdx.x] = red[1][threadIdx.x][k];
+      part[(size_t(blockIdx.x) * 2 + 0) * J + c0 + k] = red[0][threadIdx.x][k];
+      part[(size_t(blockIdx.x) * 2 + 1) * J + c0 + k] = red[1][threadIdx.x][k];
     }
   }
 }
@@ -311,7 +322,7 @@ void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Y
     hipLaunchKernelGGL((k_bnb_bwd_partials<true>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
   else
     hipLaunchKernelGGL((k_bnb_bwd_partials<false>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
-  bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta);
+  bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta, false);
   const int g = ew_grid(P * (J / 8));
   __bf16 *d = static_cast<__bf16 *>(D);
   if (ym)

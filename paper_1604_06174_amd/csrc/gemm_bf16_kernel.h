@@ -35,7 +35,7 @@
 // ADDMASK C = acc + (Ym > 0 ? D : 0) with Ym bf16 shaped like D;
 // BF16STATS Cb = bf16(acc) and, per workgroup row of tiles, float64 sums of
 // the rounded values and their squares per column (batch-norm statistics:
-// stats[2][N][m tiles], channel-major).  Split-K (gridDim.z > 1): workgroup z reduces the
+// stats[m tile][2][N], block-major).  Split-K (gridDim.z > 1): workgroup z reduces the
 // k range [z*kper, (z+1)*kper) and stores its partial product to
 // C + z*M*ldc (STORE only); the partials are then added in z order.
 #pragma once
@@ -437,7 +437,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       const int which = tid / BN, col = tid % BN;
       double t = 0.0;
       for (int k = 0; k < WM * 4; ++k) t += red[(k * 2 + which) * BN + col];
-      if (n0 + col < p.N) p.stats[(size_t(which) * p.N + n0 + col) * gridDim.y + tm] = t;
+      if (n0 + col < p.N) p.stats[(size_t(tm) * 2 + which) * p.N + n0 + col] = t;
     }
   }
 

@@ -76,8 +76,11 @@ void conv3x3_wgrad(hipStream_t s, int S, const float *X, const float *DY, float 
 // ---- batch norm and the classifier head (bn.hip) ----
 enum { BN_RES_NONE = 0, BN_RES_ID = 1, BN_RES_A = 2 };
 int bn_partial_blocks(int64_t P, int J);
-// st[0..J) = mean, st[J..2J) = rstd from conv STATS partials over m values.
-void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st);
+// st[0..J) = mean, st[J..2J) = rstd from the partial sums (sum v, sum v^2) of
+// nb workgroups over m values, stored channel-major ([2][J][nb]: conv STATS)
+// or block-major ([nb][2][J]: bf16 GEMM BF16STATS).
+void bn_finalize_fwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *st,
+                     bool channel_major);
 // Y = relu(gamma (C - mean) rstd + beta [+ shortcut(X)]) over P pixels x J.
 void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const float *st,
               const float *gamma, const float *beta, const float *X, int H, int W, int Cx, float *Y);
@@ -93,9 +96,10 @@ void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void
                           const float *bf, const int *labels, float *pooled, float *dlog,
                           float *lossn, float *G, float *dW, float *db, float *loss);
 // sums[0..J) = mean(ds), sums[J..2J) = mean(ds xhat), dgamma, dbeta from the
-// backward partials (sum ds, sum ds xhat) of nb workgroups over m values
+// backward partials (sum ds, sum ds xhat) of nb workgroups over m values, in
+// either layout (fp32 backward partials: channel-major; bf16: block-major)
 void bn_finalize_bwd(hipStream_t s, const double *part, int nb, int J, int64_t m, float *sums,
-                     float *dgamma, float *dbeta);
+                     float *dgamma, float *dbeta, bool channel_major);
 
 // ---- bf16 batch norm, stem im2col and max pool (bneck.hip) ----
 enum { BNB_RES_NONE = 0, BNB_RES_ID = 1, BNB_RES_BN = 2 };
@@ -127,7 +131,7 @@ void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, i
                int ldd = 0, const float *bias = nullptr);
 // Options: splits > 1 = split-K, C receives splits partial [M, ldc] products
 // (STORE); ADDMASK: C = acc + (mask > 0 ? D : 0), mask bf16 shaped like D;
-// BF16STATS: Cb (bf16, ldc) = round(acc) and stats[2][N][row blocks] float64
+// BF16STATS: Cb (bf16, ldc) = round(acc) and stats[row block][2][N] float64
 // sums of the rounded values and squares (row blocks: gemm_bf16_row_blocks).
 struct GemmX {
   int splits = 1;

@@ -193,7 +193,7 @@ class Bottleneck : public Net {
     gemm_bf16x(c.s, int(m), co, ci, x, false, ci, true, Wb(c, wk), ci, true, nullptr, co,
                GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
     tend(c, double(m), co, ci, 2.0 * (double(m) * ci + double(ci) * co), 2.0 * double(m) * co);
-    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), co), co, m, st);
+    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), co), co, m, st, false);
     c.launches += 1;
   }
 
@@ -204,7 +204,7 @@ class Bottleneck : public Net {
     conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, statsbuf(c));
     tend(c, double(m), g.Co, kd, 2.0 * (double(g.N) * g.H * g.W * g.Ci + kd * g.Co),
          2.0 * double(m) * g.Co);
-    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), g.Co), g.Co, m, st);
+    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), g.Co), g.Co, m, st, false);
     c.launches += 1;
   }
 
@@ -254,7 +254,7 @@ class Bottleneck : public Net {
       gemm_bf16x(c.s, int(m), C0, 147, c.ks + ks_col, false, 147, true, Wb(c, k.W1), 147, true,
                  nullptr, C0, GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
       tend(c, double(m), C0, 147, 2.0 * (double(m) * 147 + 147.0 * C0), 2.0 * double(m) * C0);
-      bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), C0), C0, m, st);
+      bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), C0), C0, m, st, false);
       bnb_apply(c.s, BNB_RES_NONE, m, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
                 nullptr, nullptr, r);
       maxpool_fwd(c.s, N, side, side, C0, k.hout, k.hout, r, yv);

@@ -176,7 +176,7 @@ class ResNetBasic : public Net {
       float *st = reinterpret_cast<float *>(sv + t);
       conv(c, CONV_FWD, 1, CONV_EPI_STATS, x, P(c, k.w1), cv, S, S, S, S, 3, C0, nullptr, nullptr,
            0, 0, 0, S, 3, C0);
-      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st);
+      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st, true);
       bn_apply(c.s, BN_RES_NONE, np, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, y);
       c.launches += 3;
       return;
@@ -187,14 +187,14 @@ class ResNetBasic : public Net {
     conv(c, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin,
          k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
-                    k.cout, np, st1);
+                    k.cout, np, st1, true);
     // the second convolution forms r1 = relu(bn1(c1)) on its input; when r1
     // is kept it also stores it (the rows each workgroup owns)
     conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout, nullptr,
          nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1), drop ? nullptr : r1);
     c.launches -= 1;
     bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
-                    np, st2);
+                    np, st2, true);
     bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),
              P(c, k.b2), x, ho, ho, k.cin, y);
     c.launches += 6;

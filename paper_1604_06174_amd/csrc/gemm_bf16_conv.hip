@@ -19,6 +19,7 @@ Args conv_args(const ConvGeo &g, int M, int N, int K, int gathered_c) {
   Args a{};
   a.M = M; a.N = N; a.K = K;
   a.H = g.H; a.W = g.W; a.Ho = g.Ho; a.Wo = g.Wo; a.R = g.R; a.S = g.S; a.P = g.P;
+  a.rmagic = (65536 + g.R - 1) / g.R;
   a.cshift = log2_exact(gathered_c);
   a.inv_wo = 1.0f / float(g.Wo);
   a.inv_ho = 1.0f / float(g.Ho);
@@ -30,7 +31,7 @@ Args conv_args(const ConvGeo &g, int M, int N, int K, int gathered_c) {
 
 bool conv_bf16_supported(const ConvGeo &g) {
   auto ok_c = [](int c) { return c >= 8 && log2_exact(c) >= 0; };
-  return ok_c(g.Ci) && ok_c(g.Co) && (g.S == 1 || g.S == 2) && g.R >= 1 && g.P >= 0 &&
+  return ok_c(g.Ci) && ok_c(g.Co) && (g.S == 1 || g.S == 2) && g.R >= 1 && g.R <= 16 && g.P >= 0 &&
          g.Ho == (g.H + 2 * g.P - g.R) / g.S + 1 && g.Wo == (g.W + 2 * g.P - g.R) / g.S + 1;
 }
 

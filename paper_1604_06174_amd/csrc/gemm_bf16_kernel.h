@@ -75,6 +75,7 @@ struct Args {
   int kper;          // split-K: k per workgroup (multiple of 32)
   // gather geometry
   int H, W, Ho, Wo, R, S, P, cshift;
+  int rmagic;  // ceil(2^16 / R): t / R = (t * rmagic) >> 16 for the tap indices used
   float inv_wo, inv_ho;
 };
 
@@ -84,12 +85,19 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // its global load stays in flight until the chunk is written to LDS.
 __device__ __forceinline__ u32x4 zero_chunk() { return u32x4{0u, 0u, 0u, 0u}; }
 
-// 16-byte load of p when ok, else of the always-valid `safe` address, the
-// result zeroed when !ok: no branch around the load.
-__device__ __forceinline__ u32x4 masked16(const void *p, const void *safe, bool ok) {
-  const u32x4 v = *reinterpret_cast<const u32x4 *>(ok ? p : safe);
-  const unsigned m = ok ? 0xffffffffu : 0u;
-  return u32x4{v.x & m, v.y & m, v.z & m, v.w & m};
+// 16 zero bytes in device memory: a chunk outside its operand is loaded from
+// here.  No loaded value then needs masking, so nothing waits for a load
+// before the chunk is written to LDS a slice later (a mask applied right after
+// the load made the compiler wait for every load of the iteration at the end
+// of each k-loop iteration).
+static __device__ __align__(16) const unsigned g_zero16[4] = {0u, 0u, 0u, 0u};
+
+// 16-byte load of p when ok, else of the zero chunk: no branch around the load.
+// The pointer is cast to the global address space so that the load is a
+// global (not flat) load, counted by the vector-memory counter only.
+typedef __attribute__((address_space(1))) const u32x4 global_u32x4;
+__device__ __forceinline__ u32x4 masked16(const void *p, bool ok) {
+  return *(global_u32x4 *)(ok ? p : static_cast<const void *>(g_zero16));
 }
 
 __device__ __forceinline__ unsigned pack2(float lo, float hi) {
@@ -104,7 +112,7 @@ __device__ __forceinline__ unsigned pack2(float lo, float hi) {
 template <bool SAFE, typename T>
 __device__ __forceinline__ u32x4 ld8(const T *base, int row, int col, int rows, int cols, int ld) {
   if constexpr (SAFE) {
-    return masked16(base + size_t(row) * ld + col, base, row < rows && col < cols);
+    return masked16(base + size_t(row) * ld + col, (row < rows) & (col < cols));
   } else {
     const bool inrow = row < rows;
     const T *p = base + size_t(row) * ld + col;
@@ -138,10 +146,12 @@ __device__ __forceinline__ int divq(int x, int d, float inv) {
   return q;
 }
 
-// kernel tap (kh, kw) of tap index t = kh*R + kw, R in {1, 3} or general
-__device__ __forceinline__ void tap_hw(int t, int R, int &kh, int &kw) {
-  kh = R == 1 ? 0 : (R == 3 ? (t * 11) >> 5 : t / R);
-  kw = t - kh * R;
+// kernel tap (kh, kw) of tap index t = kh*R + kw by a multiply and shift
+// (exact while t (R - 1) < 2^16), so the gathers stay free of branches and the
+// compiler keeps counting their loads across the k loop
+__device__ __forceinline__ void tap_hw(int t, const Args &p, int &kh, int &kw) {
+  kh = (t * p.rmagic) >> 16;
+  kw = t - kh * p.R;
 }
 
 // Per-chunk row state of the A gathers: the output (GA_FWD) or input
@@ -167,18 +177,18 @@ __device__ __forceinline__ u32x4 gatherA(const Args &p, const __bf16 *A, const R
   const int C = 1 << p.cshift;
   const int tap = k >> p.cshift, ch = k & (C - 1);
   int kh, kw;
-  tap_hw(tap, p.R, kh, kw);
+  tap_hw(tap, p, kh, kw);
   if constexpr (GA == GA_FWD) {
     const int hi = rp.y * p.S + kh - p.P, wi = rp.x * p.S + kw - p.P;
-    const bool ok = rp.ok && k < kend && hi >= 0 && hi < p.H && wi >= 0 && wi < p.W;
-    return masked16(A + ((size_t(rp.img) * p.H + hi) * p.W + wi) * C + ch, A, ok);
+    const bool ok = rp.ok & (k < kend) & (hi >= 0) & (hi < p.H) & (wi >= 0) & (wi < p.W);
+    return masked16(A + ((size_t(rp.img) * p.H + hi) * p.W + wi) * C + ch, ok);
   } else {
     const int t = rp.y + p.P - kh, u = rp.x + p.P - kw;
     const int sm = p.S - 1;  // S in {1, 2}
     const int ho = t >> sm, wo = u >> sm;
-    const bool ok = rp.ok && k < kend && t >= 0 && u >= 0 && !(t & sm) && !(u & sm) && ho < p.Ho &&
-                    wo < p.Wo;
-    return masked16(A + ((size_t(rp.img) * p.Ho + ho) * p.Wo + wo) * C + ch, A, ok);
+    const bool ok = rp.ok & (k < kend) & (t >= 0) & (u >= 0) & !(t & sm) & !(u & sm) & (ho < p.Ho) &
+                    (wo < p.Wo);
+    return masked16(A + ((size_t(rp.img) * p.Ho + ho) * p.Wo + wo) * C + ch, ok);
   }
 }
 
@@ -194,7 +204,7 @@ __device__ __forceinline__ ColTap col_tap(const Args &p, int n) {
   const int C = 1 << p.cshift;
   const int t = (c.ok ? n : 0) >> p.cshift;
   c.ch = (c.ok ? n : 0) & (C - 1);
-  tap_hw(t, p.R, c.kh, c.kw);
+  tap_hw(t, p, c.kh, c.kw);
   return c;
 }
 
@@ -204,14 +214,14 @@ __device__ __forceinline__ u32x4 gatherB_wgrad(const Args &p, const ColTap &ct, 
   const int img = divq(t, p.Ho, p.inv_ho);
   const int ho = t - img * p.Ho;
   const int hi = ho * p.S + ct.kh - p.P, wi = wo * p.S + ct.kw - p.P;
-  const bool ok = ct.ok && k < kend && hi >= 0 && hi < p.H && wi >= 0 && wi < p.W;
-  return masked16(p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch, p.B, ok);
+  const bool ok = ct.ok & (k < kend) & (hi >= 0) & (hi < p.H) & (wi >= 0) & (wi < p.W);
+  return masked16(p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch, ok);
 }
 
 __device__ __forceinline__ u32x4 gatherB_wdgrad(const Args &p, int k, int n, int kend) {
   const int Co = 1 << p.cshift;
   const int tap = k >> p.cshift, co = k & (Co - 1);
-  return masked16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, p.B, k < kend && n < p.N);
+  return masked16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, (k < kend) & (n < p.N));
 }
 
 template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB, bool SAFE>
@@ -319,7 +329,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
     for (int c = 0; c < PA; ++c) {
       const int e = tid + c * 256;
-      if (e < CHA) {
+      if (CHA % 256 == 0 || e < CHA) {
         if (AK) {
           const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
           *reinterpret_cast<u32x4 *>(smA + ((buf * BM + mr) * KP + kc) * 2) = ra[c];
@@ -332,7 +342,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
     for (int c = 0; c < PB; ++c) {
       const int e = tid + c * 256;
-      if (e < CHB) {
+      if (CHB % 256 == 0 || e < CHB) {
         if (BK) {
           const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
           *reinterpret_cast<u32x4 *>(smB + ((buf * BN + nr) * KP + kc) * 2) = rb[c];

@@ -393,15 +393,17 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 
   // Two register stages: the loads of slice kt + 2 are issued right after
   // slice kt is stored to LDS, so each load has two slices of MFMA work to
-  // arrive.  Slice kt is stored to LDS buffer kt & 1.
-  // Loads at or past kend return zeros without touching memory, so the loop
-  // runs an even number of slices with unconditional loads (a trailing
-  // all-zero slice adds exact zeros) and the load counters stay static.
+  // arrive.  Slice kt is stored to LDS buffer kt & 1.  The loop body has no
+  // branches (a branch there makes the compiler wait for every outstanding
+  // load at each iteration): it runs while two more slices follow, its loads
+  // at or past kend return zeros, and the last one or two slices are
+  // multiplied after it.
   const int nk = kend > kbeg ? (kend - kbeg + KS - 1) / KS : 0;
   u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
   gload(ra0, rb0, kbeg);
   gload(ra1, rb1, kbeg + KS);
-  for (int kt = 0; kt < nk; kt += 2) {
+  int kt = 0;
+  for (; kt + 2 < nk; kt += 2) {  // no branches in the body (see above)
     sstore(ra0, rb0, 0);
     __syncthreads();
     gload(ra0, rb0, kbeg + (kt + 2) * KS);
@@ -410,6 +412,16 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     __syncthreads();
     gload(ra1, rb1, kbeg + (kt + 3) * KS);
     compute(1);
+  }
+  if (kt < nk) {  // the last one or two slices, without further loads
+    sstore(ra0, rb0, 0);
+    __syncthreads();
+    compute(0);
+    if (kt + 1 < nk) {
+      sstore(ra1, rb1, 1);
+      __syncthreads();
+      compute(1);
+    }
   }
 
   if constexpr (EPI == GEMM_EPI_BF16STATS) {

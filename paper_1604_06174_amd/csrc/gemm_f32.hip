@@ -53,25 +53,33 @@ struct GemmArgs {
   int ldz;
 };
 
+// 16 zero bytes in device memory: an element outside its operand is loaded
+// from here, so no loaded value is masked afterwards and nothing waits for a
+// load before it is written to LDS a slice later.
+static __device__ __align__(16) const float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const f32x4 global_f32x4;
+typedef __attribute__((address_space(1))) const float global_float;
+
 // 4 consecutive elements of a row-major [rows, cols] matrix, zero outside.
-// Branch-free (an outside address is replaced by the base and the value by
-// zero), so the loads of a slice stay in flight together.  VEC: one 16-byte
-// load; needs ld and cols multiples of 4 and a 16-byte aligned base, so a
-// chunk is either wholly inside or wholly outside.
+// Branch-free (an outside address is replaced by the zero chunk), so the loads
+// of a slice stay in flight together; the pointers are cast to the global
+// address space so that the loads are global loads.  VEC: one 16-byte load;
+// needs ld and cols multiples of 4 and a 16-byte aligned base, so a chunk is
+// either wholly inside or wholly outside.
 template <bool VEC>
 __device__ __forceinline__ float4 ld4(const float *base, int row, int col, int rows, int cols,
                                       int ld) {
   if (VEC) {
-    const bool ok = row < rows && col < cols;
-    const float4 v = *reinterpret_cast<const float4 *>(ok ? base + size_t(row) * ld + col : base);
-    return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+    const bool ok = (row < rows) & (col < cols);
+    const f32x4 v = *(global_f32x4 *)(ok ? base + size_t(row) * ld + col : g_zero4);
+    return make_float4(v.x, v.y, v.z, v.w);
   }
   float r[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const bool ok = row < rows && col + j < cols;
-    const float v = base[ok ? size_t(row) * ld + col + j : 0];
-    r[j] = ok ? v : 0.f;
+    const bool ok = (row < rows) & (col + j < cols);
+    r[j] = *(global_float *)(ok ? base + size_t(row) * ld + col + j : g_zero4);
   }
   return make_float4(r[0], r[1], r[2], r[3]);
 }
@@ -157,24 +165,32 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
   };
 
   // slices kt+1 and kt+2 are in flight in registers while slice kt is
-  // multiplied out of LDS buffer kt & 1
+  // multiplied out of LDS buffer kt & 1.  The loop body has no branches (a
+  // branch there makes the compiler wait for every load at each iteration):
+  // it runs while two more slices follow, with loads at or past K returning
+  // zeros; the last one or two slices are multiplied after it.
   const int nk = (p.K + BK - 1) / BK;
   float4 ra0[NCH], rb0[NCH], ra1[NCH], rb1[NCH];
   gload(ra0, rb0, 0);
-  if (nk > 1) gload(ra1, rb1, BK);
+  gload(ra1, rb1, BK);
   sstore(ra0, rb0, 0);
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * BK);
+  int kt = 0;
+  for (; kt + 2 < nk; kt += 2) {
+    gload(ra0, rb0, (kt + 2) * BK);
     compute(0);
-    if (kt + 1 < nk) sstore(ra1, rb1, 1);
+    sstore(ra1, rb1, 1);
     __syncthreads();
-    if (kt + 1 < nk) {
-      if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * BK);
-      compute(1);
-      if (kt + 2 < nk) sstore(ra0, rb0, 0);
-      __syncthreads();
-    }
+    gload(ra1, rb1, (kt + 3) * BK);
+    compute(1);
+    sstore(ra0, rb0, 0);
+    __syncthreads();
+  }
+  compute(0);  // slice kt
+  if (kt + 1 < nk) {
+    sstore(ra1, rb1, 1);
+    __syncthreads();
+    compute(1);
   }
 
   // accumulator register r of a lane holds element (row, col) of its 32x32 tile

@@ -1,6 +1,7 @@
 // Dense bf16 GEMM entry points (kernel and conventions in gemm_bf16_kernel.h).
 #include <algorithm>
 
+#include "common.h"
 #include "gemm_bf16_kernel.h"
 
 namespace ckpt {
@@ -99,6 +100,26 @@ void gemm_bf16_part(hipStream_t s, int M, int N, int K, const void *A, bool a_fp
   x.splits = splits;
   gemm_bf16x(s, M, N, K, A, a_fp32, lda, ak, B, ldb, bk, part, N, GEMM_EPI_STORE, nullptr, 0,
              nullptr, x);
+}
+
+int gemm_bf16_kper(int K, int splits) {
+  if (splits < 1) splits = 1;
+  const int kper = ((K + splits - 1) / splits + KS - 1) / KS * KS;
+  return kper < KS ? KS : kper;
+}
+
+void gemm_bf16_part_cat(hipStream_t s, int M, int N, int K1, const void *A1, int lda1, int K2,
+                        const void *A2, int lda2, const void *B, int ldb, float *part, int splits) {
+  if (M <= 0 || N <= 0) return;
+  if (K1 % 8 || K2 % 8 || lda1 % 8 || lda2 % 8 || ldb % 8)
+    fail(CKPT_E_UNSUPPORTED, "gemm_bf16_part_cat: k extents and strides must be multiples of 8");
+  GemmX x;
+  x.splits = splits;
+  Args a = make_args(M, N, K1 + K2, A1, lda1, B, ldb, part, N, nullptr, 0, nullptr, x);
+  a.A2 = static_cast<const __bf16 *>(A2);
+  a.lda2 = lda2;
+  a.K1 = K1;
+  pick_tile<true, true, __bf16, GA_CAT, G_DENSE, true>(a, GEMM_EPI_STORE, x.splits, s);
 }
 
 void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, float *C, int ldc,

@@ -20,6 +20,8 @@
 //             -> x[n, ho*S + kh - P, wo*S + kw - P, ci]        (weight gradient)
 //   GB_WDGRAD B(k, n): k = (kh, kw, co), n = ci -> W[co, kh, kw, ci]  (the
 //             forward weights [Co, R, R, Ci] read as the data gradient's B)
+//   GA_CAT    A(m, k) = A[m, k] for k < K1, A2[m, k - K1] after: two
+//             k-contiguous bf16 operands side by side along k
 // Out-of-image taps read zero.
 //
 // Block = 256 threads = 4 wavefronts in a WM x WN grid; each wavefront owns a
@@ -56,7 +58,7 @@ namespace gb {
 constexpr int KS = 64;      // k per LDS slice: two 32-deep MFMA steps
 constexpr int KP = KS + 8;  // padded row (bf16 elements): 144-byte rows
 
-enum { G_DENSE = 0, GA_FWD = 1, GA_DGRAD = 2, GB_WGRAD = 3, GB_WDGRAD = 4 };
+enum { G_DENSE = 0, GA_FWD = 1, GA_DGRAD = 2, GB_WGRAD = 3, GB_WDGRAD = 4, GA_CAT = 5 };
 
 struct Args {
   int M, N, K;
@@ -76,6 +78,8 @@ struct Args {
   // gather geometry
   int H, W, Ho, Wo, R, S, P, cshift;
   int rmagic;  // ceil(2^16 / R): t / R = (t * rmagic) >> 16 for the tap indices used
+  const __bf16 *A2;  // GA_CAT: the second operand, from k = K1 on
+  int lda2, K1;
   float inv_wo, inv_ho;
 };
 
@@ -270,9 +274,9 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   const TA *A = static_cast<const TA *>(p.A);
 
   // fixed per-chunk gather state
-  RowPix rpix[GA != G_DENSE ? PA : 1];
+  RowPix rpix[(GA == GA_FWD || GA == GA_DGRAD) ? PA : 1];
   ColTap ctap[GB == GB_WGRAD ? PB : 1];
-  if constexpr (GA != G_DENSE) {
+  if constexpr (GA == GA_FWD || GA == GA_DGRAD) {
 #pragma unroll
     for (int c = 0; c < PA; ++c) {
       const int e = min(tid + c * 256, CHA - 1);
@@ -297,7 +301,13 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       const int e = min(tid + c * 256, CHA - 1);
       if (AK) {  // chunk = 8 k of one m
         const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-        if constexpr (GA != G_DENSE)
+        if constexpr (GA == GA_CAT) {  // k < K1 from A, the rest from A2 (no branch)
+          const int kk = k0 + kc, m = m0 + mr;
+          const bool second = kk >= p.K1;
+          const __bf16 *base = second ? p.A2 : reinterpret_cast<const __bf16 *>(A);
+          const size_t off = size_t(m) * (second ? p.lda2 : p.lda) + (second ? kk - p.K1 : kk);
+          ra[c] = masked16(base + off, (m < p.M) & (kk < kend));
+        } else if constexpr (GA != G_DENSE)
           ra[c] = gatherA<GA>(p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
         else
           ra[c] = ld8<SAFE, TA>(A, m0 + mr, k0 + kc, p.M, kend, p.lda);

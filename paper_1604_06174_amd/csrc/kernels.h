@@ -153,6 +153,14 @@ void gemm_bf16_part(hipStream_t s, int M, int N, int K, const void *A, bool a_fp
                     const void *B, int ldb, bool bk, float *part, int splits);
 void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, float *C, int ldc,
                 const float *D = nullptr, int ldd = 0, const float *bias = nullptr);
+// k per split of gemm_bf16_part over K with `splits` splits
+int gemm_bf16_kper(int K, int splits);
+// gemm_bf16_part of [A1 | A2] (bf16, k contiguous, K1 + K2 columns) times B
+// ([N, ldb] bf16, k contiguous over K1 + K2): one launch, `splits` partial
+// [M, N] products over consecutive k ranges.  K1, K2, lda1, lda2 and ldb
+// multiples of 8.
+void gemm_bf16_part_cat(hipStream_t s, int M, int N, int K1, const void *A1, int lda1, int K2,
+                        const void *A2, int lda2, const void *B, int ldb, float *part, int splits);
 // out[e] = sum_b part[b*E + e], b in a fixed order
 void sum_partials(hipStream_t s, const float *part, int nb, int E, float *out);
 
@@ -179,7 +187,8 @@ void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void 
                      int splits, float *dW);
 
 // ---- LSTM step kernels (lstm.hip) ----
-void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst);  // dst[c][r]
+// dst[c * ld + r] = bf16(src[r * C + c]) (ld = R when 0)
+void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst, int ld = 0);
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst);
 // Split-K inputs: zpart / lpart / dhpart hold ns partial slices of the
 // product, added in slice order before the bias (or the incoming dh), exactly

@@ -43,7 +43,7 @@ __device__ __forceinline__ void slices_sum(const float *__restrict__ part, int n
 
 // dst[c][r] = bf16(src[r][c]) for src [R][C] fp32, through 32x32 LDS tiles.
 __global__ __launch_bounds__(256) void k_transpose_bf16(int R, int C, const float *__restrict__ src,
-                                                        __bf16 *__restrict__ dst) {
+                                                        __bf16 *__restrict__ dst, int ld) {
   __shared__ float t[32][33];
   const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void k_transpose_bf16(int R, int C, const floa
   __syncthreads();
   for (int k = ty; k < 32; k += 8) {
     const int c = c0 + k, r = r0 + tx;
-    if (c < C && r < R) dst[size_t(c) * R + r] = (__bf16)t[tx][k];
+    if (c < C && r < R) dst[size_t(c) * ld + r] = (__bf16)t[tx][k];
   }
 }
 
@@ -299,9 +299,9 @@ inline int grid_for(int64_t n) {
 
 }  // namespace
 
-void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst) {
+void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst, int ld) {
   hipLaunchKernelGGL(k_transpose_bf16, dim3((C + 31) / 32, (R + 31) / 32), dim3(256), 0, s, R, C,
-                     src, static_cast<__bf16 *>(dst));
+                     src, static_cast<__bf16 *>(dst), ld > 0 ? ld : R);
 }
 
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst) {

@@ -33,7 +33,8 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wxt, k_wht, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part;
+  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part;
+  bool zcat;  // z = [x_t | h_{t-1}] [W_x; W_h] as one product (same slices as the two)
   // split-K counts: input and recurrent parts of z, logits, dh (head), dh_{t-1}
   int s_x, s_h, s_l, s_dh, s_dx;
   // extra gradient buffer offsets
@@ -73,8 +74,7 @@ class LstmNet : public Net {
     x_hc = take(uint64_t(C) * B * H * 2);
     grad_extra = off;
     off = 0;
-    k_wxt = take(uint64_t(E) * 4 * H * 2);
-    k_wht = take(uint64_t(H) * 4 * H * 2);
+    k_wcat = take(uint64_t(E + H) * 4 * H * 2);  // [4H][E + H]: W_x^T | W_h^T
     k_wh = take(uint64_t(H) * 4 * H * 2);
     k_wot = take(uint64_t(H) * V * 2);
     k_wo = take(uint64_t(H) * V * 2);
@@ -85,6 +85,10 @@ class LstmNet : public Net {
     k_loss = take(4);
     s_x = gemm_bf16_splits(B, 4 * H, E);
     s_h = gemm_bf16_splits(B, 4 * H, H);
+    // one launch for both parts of z when its k splits fall exactly on the two
+    // parts' own splits (then every slice holds the same sums in the same order)
+    zcat = E == H && s_x == s_h && gemm_bf16_kper(E, s_x) * s_x == E &&
+           gemm_bf16_kper(E + H, s_x + s_h) == gemm_bf16_kper(E, s_x) && E % 8 == 0;
     s_l = gemm_bf16_splits(B, V, H);
     s_dh = gemm_bf16_splits(B, H, V);
     s_dx = gemm_bf16_splits(B, H, 4 * H);
@@ -124,8 +128,8 @@ class LstmNet : public Net {
 
   void begin_step(StepCtx &c) override {
     // bf16 copies of the weights in the layouts the GEMMs read (k contiguous)
-    transpose_bf16(c.s, E, 4 * H, P(c, pWx), K(c, k_wxt));  // [4H][E]
-    transpose_bf16(c.s, H, 4 * H, P(c, pWh), K(c, k_wht));  // [4H][H]
+    transpose_bf16(c.s, E, 4 * H, P(c, pWx), K(c, k_wcat), E + H);              // [4H][0, E)
+    transpose_bf16(c.s, H, 4 * H, P(c, pWh), K(c, k_wcat) + size_t(E) * 2, E + H);  // [4H][E, E + H)
     cvt_bf16(c.s, int64_t(H) * 4 * H, P(c, pWh), K(c, k_wh));  // [H][4H]
     transpose_bf16(c.s, H, V, P(c, pWo), K(c, k_wot));        // [V][H]
     cvt_bf16(c.s, int64_t(H) * V, P(c, pWo), K(c, k_wo));      // [H][V]
@@ -140,8 +144,17 @@ class LstmNet : public Net {
     const int *lab = static_cast<const int *>(c.target) + size_t(i) * B;
     // z = x_t W_x + h_{t-1} W_h + b: both products split over k into one
     // slice buffer that the pointwise kernel adds up in order with the bias
-    gemm_part(c, B, 4 * H, E, xt, E, K(c, k_wxt), E, 0, s_x);
-    if (i > 0) gemm_part(c, B, 4 * H, H, x, H, K(c, k_wht), H, s_x, s_h);
+    if (i > 0 && zcat) {
+      timer.begin(c.s);
+      gemm_bf16_part_cat(c.s, B, 4 * H, E, xt, E, H, x, H, K(c, k_wcat), E + H, Kf(c, k_part),
+                         s_x + s_h);
+      timer.end(c.s, 2.0 * B * 4 * H * (E + H),
+                2.0 * (double(B) * (E + H) + double(E + H) * 4 * H) + 4.0 * (s_x + s_h) * B * 4 * H);
+      c.launches += 1;
+    } else {
+      gemm_part(c, B, 4 * H, E, xt, E, K(c, k_wcat), E + H, 0, s_x);
+      if (i > 0) gemm_part(c, B, 4 * H, H, x, H, K(c, k_wcat) + size_t(E) * 2, E + H, s_x, s_h);
+    }
     const float *c_prev = i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr;
     float *gates = reinterpret_cast<float *>(sv);
     lstm_fwd_point(c.s, B, H, Kf(c, k_part), s_x + (i > 0 ? s_h : 0), P(c, pb), c_prev, gates, y,

@@ -89,19 +89,21 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // its global load stays in flight until the chunk is written to LDS.
 __device__ __forceinline__ u32x4 zero_chunk() { return u32x4{0u, 0u, 0u, 0u}; }
 
-// 16 zero bytes in device memory: a chunk outside its operand is loaded from
-// here.  No loaded value then needs masking, so nothing waits for a load
-// before the chunk is written to LDS a slice later (a mask applied right after
-// the load made the compiler wait for every load of the iteration at the end
-// of each k-loop iteration).
-static __device__ __align__(16) const unsigned g_zero16[4] = {0u, 0u, 0u, 0u};
+// 4 KB of zeros in device memory: a chunk outside its operand is loaded from
+// here (16 bytes per thread of the workgroup, so the zero loads spread over
+// many cache lines instead of all meeting on one).  No loaded value then needs
+// masking, so nothing waits for a load before the chunk is written to LDS a
+// slice later (a mask applied right after the load made the compiler wait for
+// every load of the iteration at the end of each k-loop iteration).
+static __device__ __align__(16) const unsigned g_zero_area[1024] = {};
 
-// 16-byte load of p when ok, else of the zero chunk: no branch around the load.
-// The pointer is cast to the global address space so that the load is a
-// global (not flat) load, counted by the vector-memory counter only.
+// 16-byte load of p when ok, else of the thread's zero chunk: no branch around
+// the load.  The pointer is cast to the global address space so that the load
+// is a global (not flat) load, counted by the vector-memory counter only.
 typedef __attribute__((address_space(1))) const u32x4 global_u32x4;
 __device__ __forceinline__ u32x4 masked16(const void *p, bool ok) {
-  return *(global_u32x4 *)(ok ? p : static_cast<const void *>(g_zero16));
+  const void *z = g_zero_area + 4 * (threadIdx.x & 255);
+  return *(global_u32x4 *)(ok ? p : z);
 }
 
 __device__ __forceinline__ unsigned pack2(float lo, float hi) {
@@ -405,22 +407,24 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   // slice kt is stored to LDS, so each load has two slices of MFMA work to
   // arrive.  Slice kt is stored to LDS buffer kt & 1.  The loop body has no
   // branches (a branch there makes the compiler wait for every outstanding
-  // load at each iteration): it runs while two more slices follow, its loads
-  // at or past kend return zeros, and the last one or two slices are
-  // multiplied after it.
+  // load at each iteration): it runs while two more slices follow, and the
+  // last one or two slices are multiplied after it.
   const int nk = kend > kbeg ? (kend - kbeg + KS - 1) / KS : 0;
+  // k origin of slice s; a slice past the range re-reads the last one (real,
+  // spread-out addresses; it is never multiplied)
+  auto kslice = [&](int s) { return kbeg + max(0, min(s, nk - 1)) * KS; };
   u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
-  gload(ra0, rb0, kbeg);
-  gload(ra1, rb1, kbeg + KS);
+  gload(ra0, rb0, kslice(0));
+  gload(ra1, rb1, kslice(1));
   int kt = 0;
   for (; kt + 2 < nk; kt += 2) {  // no branches in the body (see above)
     sstore(ra0, rb0, 0);
     __syncthreads();
-    gload(ra0, rb0, kbeg + (kt + 2) * KS);
+    gload(ra0, rb0, kslice(kt + 2));
     compute(0);
     sstore(ra1, rb1, 1);
     __syncthreads();
-    gload(ra1, rb1, kbeg + (kt + 3) * KS);
+    gload(ra1, rb1, kslice(kt + 3));
     compute(1);
   }
   if (kt < nk) {  // the last one or two slices, without further loads

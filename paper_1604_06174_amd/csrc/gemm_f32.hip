@@ -53,10 +53,11 @@ struct GemmArgs {
   int ldz;
 };
 
-// 16 zero bytes in device memory: an element outside its operand is loaded
-// from here, so no loaded value is masked afterwards and nothing waits for a
-// load before it is written to LDS a slice later.
-static __device__ __align__(16) const float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
+// 4 KB of zeros in device memory: an element outside its operand is loaded
+// from here (16 bytes per thread, spread over many cache lines), so no loaded
+// value is masked afterwards and nothing waits for a load before it is
+// written to LDS a slice later.
+static __device__ __align__(16) const float g_zero_area[1024] = {};
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) const f32x4 global_f32x4;
 typedef __attribute__((address_space(1))) const float global_float;
@@ -72,14 +73,15 @@ __device__ __forceinline__ float4 ld4(const float *base, int row, int col, int r
                                       int ld) {
   if (VEC) {
     const bool ok = (row < rows) & (col < cols);
-    const f32x4 v = *(global_f32x4 *)(ok ? base + size_t(row) * ld + col : g_zero4);
+    const float *z = g_zero_area + 4 * (threadIdx.x & 255);
+    const f32x4 v = *(global_f32x4 *)(ok ? base + size_t(row) * ld + col : z);
     return make_float4(v.x, v.y, v.z, v.w);
   }
   float r[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const bool ok = (row < rows) & (col + j < cols);
-    r[j] = *(global_float *)(ok ? base + size_t(row) * ld + col + j : g_zero4);
+    r[j] = *(global_float *)(ok ? base + size_t(row) * ld + col + j : g_zero_area + 4 * (threadIdx.x & 255));
   }
   return make_float4(r[0], r[1], r[2], r[3]);
 }
@@ -167,21 +169,24 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
   // slices kt+1 and kt+2 are in flight in registers while slice kt is
   // multiplied out of LDS buffer kt & 1.  The loop body has no branches (a
   // branch there makes the compiler wait for every load at each iteration):
-  // it runs while two more slices follow, with loads at or past K returning
-  // zeros; the last one or two slices are multiplied after it.
+  // it runs while two more slices follow, and the last one or two slices are
+  // multiplied after it.
   const int nk = (p.K + BK - 1) / BK;
+  // k origin of slice s; a slice past K re-reads the last one (real,
+  // spread-out addresses; it is never multiplied)
+  auto kslice = [&](int s) { return max(0, min(s, nk - 1)) * BK; };
   float4 ra0[NCH], rb0[NCH], ra1[NCH], rb1[NCH];
-  gload(ra0, rb0, 0);
-  gload(ra1, rb1, BK);
+  gload(ra0, rb0, kslice(0));
+  gload(ra1, rb1, kslice(1));
   sstore(ra0, rb0, 0);
   __syncthreads();
   int kt = 0;
   for (; kt + 2 < nk; kt += 2) {
-    gload(ra0, rb0, (kt + 2) * BK);
+    gload(ra0, rb0, kslice(kt + 2));
     compute(0);
     sstore(ra1, rb1, 1);
     __syncthreads();
-    gload(ra1, rb1, (kt + 3) * BK);
+    gload(ra1, rb1, kslice(kt + 3));
     compute(1);
     sstore(ra0, rb0, 0);
     __syncthreads();

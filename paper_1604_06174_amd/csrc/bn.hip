@@ -441,6 +441,16 @@ void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const f
     hipLaunchKernelGGL((k_bn_apply<BN_RES_A>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
 }
 
+void bn_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const float *Ym,
+                       const float *Cv, const float *st, const float *gamma, const float *sums,
+                       float *D) {
+  const int g = ew_grid(P * (J / 4));
+  if (Ym)
+    hipLaunchKernelGGL((k_bn_bwd_apply<true>), dim3(g), dim3(256), 0, s, P, J, G, Ym, Cv, st, gamma, sums, D);
+  else
+    hipLaunchKernelGGL((k_bn_bwd_apply<false>), dim3(g), dim3(256), 0, s, P, J, G, Ym, Cv, st, gamma, sums, D);
+}
+
 void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Ym, const float *Cv,
                  const float *st, const float *gamma, double *part, float *sums, float *dgamma,
                  float *dbeta, float *D) {

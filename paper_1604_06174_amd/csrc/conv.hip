@@ -217,6 +217,12 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
         } else if (EPI == CONV_EPI_MASK) {
           const float e = a.tst ? bn_relu(a.E0[o], a.tst[j], a.tst[a.J + j], a.tg[j], a.tb[j]) : a.E0[o];
           v = e > 0.f ? v : 0.f;
+        } else if (EPI == CONV_EPI_MASKSTATS) {
+          const float c = a.E0[o], mean = a.tst[j], rs = a.tst[a.J + j];
+          v = bn_relu(c, mean, rs, a.tg[j], a.tb[j]) > 0.f ? v : 0.f;
+          const float xh = (c - mean) * rs;
+          s1[t] += double(v);
+          s2[t] += double(v) * double(xh);
         } else if (EPI == CONV_EPI_SC1) {
           v += a.E1[o] > 0.f ? a.E0[o] : 0.f;
         } else if (EPI == CONV_EPI_SC2) {
@@ -229,7 +235,7 @@ __global__ __launch_bounds__(256) void k_conv3x3(ConvArgs a) {
       }
     }
   }
-  if (EPI == CONV_EPI_STATS) {
+  if (EPI == CONV_EPI_STATS || EPI == CONV_EPI_MASKSTATS) {
     // per-channel sums over the workgroup: lanes (q) then waves, fixed order
     double *red = reinterpret_cast<double *>(smem);  // halo is no longer read
     __syncthreads();
@@ -447,12 +453,12 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
             o = ((size_t(n) * a.Eh + (h >> 1)) * a.Ew + (cc >> 1)) * a.Ec + j;
           }
           e0[s][r][t] = a.E0[ok ? o : 0];
-          if (EPI != CONV_EPI_MASK) e1[s][r][t] = a.E1[ok ? o : 0];
+          if (EPI != CONV_EPI_MASK && EPI != CONV_EPI_MASKSTATS) e1[s][r][t] = a.E1[ok ? o : 0];
         }
       }
   }
   float tm[NS], tr[NS], tg[NS], tb[NS];
-  if (EPI == CONV_EPI_MASK && a.tst) {
+  if ((EPI == CONV_EPI_MASK && a.tst) || EPI == CONV_EPI_MASKSTATS) {
 #pragma unroll
     for (int t = 0; t < NS; ++t) {
       const int j = j0 + t * 16 + i16, jc = j < J ? j : 0;
@@ -485,6 +491,11 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
         } else if (EPI == CONV_EPI_MASK) {
           const float e = a.tst ? bn_relu(e0[s][r][t], tm[t], tr[t], tg[t], tb[t]) : e0[s][r][t];
           v = e > 0.f ? v : 0.f;
+        } else if (EPI == CONV_EPI_MASKSTATS) {
+          v = bn_relu(e0[s][r][t], tm[t], tr[t], tg[t], tb[t]) > 0.f ? v : 0.f;
+          const float xh = (e0[s][r][t] - tm[t]) * tr[t];
+          s1[t] += double(v);
+          s2[t] += double(v) * double(xh);
         } else if (EPI == CONV_EPI_SC1) {
           v += e1[s][r][t] > 0.f ? e0[s][r][t] : 0.f;
         } else if (EPI == CONV_EPI_SC2) {
@@ -494,7 +505,7 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
       }
     }
   }
-  if (EPI == CONV_EPI_STATS) {
+  if (EPI == CONV_EPI_STATS || EPI == CONV_EPI_MASKSTATS) {
     double *red = reinterpret_cast<double *>(smem);
     __syncthreads();
 #pragma unroll
@@ -543,7 +554,8 @@ bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool 
 // The CIFAR-shaped network's convolutions: 16/32/64 channels at 32/16/8 pixels.
 bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
   constexpr int F = CONV_FWD, D = CONV_DGRAD;
-  constexpr int STATS = CONV_EPI_STATS, MASK = CONV_EPI_MASK, SC1 = CONV_EPI_SC1, SC2 = CONV_EPI_SC2;
+  constexpr int STATS = CONV_EPI_STATS, MASK = CONV_EPI_MASK, SC1 = CONV_EPI_SC1, SC2 = CONV_EPI_SC2,
+                MST = CONV_EPI_MASKSTATS;
   // rows per workgroup and output channels per workgroup as measured best on
   // MI355X for these shapes
   return spec_try<16, 16, 32, 1, F, STATS, 4, 16>(a, mode, s, epi, st, launch, u) ||
@@ -554,6 +566,9 @@ bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, 
          spec_try<16, 16, 32, 1, D, MASK, 4, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<32, 32, 16, 1, D, MASK, 4, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<64, 64, 8, 1, D, MASK, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, D, MST, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, D, MST, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, D, MST, 8, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<16, 16, 32, 1, D, SC1, 4, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<32, 32, 16, 1, D, SC1, 4, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<64, 64, 8, 1, D, SC1, 8, 16>(a, mode, s, epi, st, launch, u) ||
@@ -1034,6 +1049,7 @@ void launch_conv(const ConvArgs &a, int epi, size_t lds, dim3 grid, hipStream_t 
   switch (epi) {
     case CONV_EPI_STATS: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STATS>), grid, dim3(256), lds, st, a); break;
     case CONV_EPI_MASK: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASK>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_MASKSTATS: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASKSTATS>), grid, dim3(256), lds, st, a); break;
     case CONV_EPI_SC1: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC1>), grid, dim3(256), lds, st, a); break;
     case CONV_EPI_SC2: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC2>), grid, dim3(256), lds, st, a); break;
     default: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STORE>), grid, dim3(256), lds, st, a); break;
@@ -1066,8 +1082,10 @@ static ConvArgs shape_args(int mode, int S, int N, int H, int W, int C, int J) {
 
 int conv3x3_blocks(int mode, int S, int N, int H, int W, int C, int J) {
   SpecUse u;
-  // the statistics partials are indexed by blockIdx.x only
-  if (spec_dispatch(shape_args(mode, S, N, H, W, C, J), mode, S, CONV_EPI_STATS, nullptr, false, &u))
+  // the statistics partials are indexed by blockIdx.x only (STATS in the
+  // forward, MASKSTATS in the data gradient)
+  if (spec_dispatch(shape_args(mode, S, N, H, W, C, J), mode, S,
+                    mode == CONV_FWD ? CONV_EPI_STATS : CONV_EPI_MASKSTATS, nullptr, false, &u))
     return N * ((H + u.RB - 1) / u.RB);
   return N * conv_tile(mode, S, H, W, C, J).rblk;
 }
@@ -1095,6 +1113,8 @@ void conv3x3(hipStream_t st, int mode, int S, int epi, const float *X, const flo
              int N, int H, int W, int Hx, int Wx, int C, int J, const float *E0, const float *E1,
              int Eh, int Ew, int Ec, double *stats, const float *tst, const float *tg,
              const float *tb, float *rout) {
+  if (epi == CONV_EPI_MASKSTATS && (mode != CONV_DGRAD || !tst || !tg || !tb || !stats || !E0))
+    fail(CKPT_E_INVALID, "conv3x3: MASKSTATS needs a data gradient, the mask operand, its statistics and stats");
   if (rout && (mode != CONV_FWD || S != 1 || !tst || (C & 3) != 0))
     fail(CKPT_E_INVALID, "conv3x3: the transformed input is stored only by a stride-1 forward with a transform");
   Tile t = conv_tile(mode, S, H, W, C, J);

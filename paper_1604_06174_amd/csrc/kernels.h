@@ -47,7 +47,8 @@ void ew_copy(hipStream_t s, int64_t n, const float *x, float *y);
 
 // ---- 3x3 convolutions (conv.hip) ----
 enum { CONV_FWD = 0, CONV_DGRAD = 1 };
-enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 = 3, CONV_EPI_SC2 = 4 };
+enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 = 3, CONV_EPI_SC2 = 4,
+       CONV_EPI_MASKSTATS = 5 };
 
 // Y[N,H,W,J] = conv of X[N,Hx,Wx,C] (FWD: stride S; DGRAD: gradient of a
 // stride-S forward conv, X = dy).  Epilogue operands: MASK E0 = mask tensor
@@ -56,6 +57,10 @@ enum { CONV_EPI_STORE = 0, CONV_EPI_STATS = 1, CONV_EPI_MASK = 2, CONV_EPI_SC1 =
 // Optional batch-norm + ReLU transform (tst = mean | rstd, tg = gamma,
 // tb = beta): FWD applies bn_relu to every in-image input value (channel c);
 // DGRAD with MASK takes the mask as bn_relu(E0) (channel j) instead of E0.
+// MASKSTATS (DGRAD, transform required): MASK with the mask bn_relu(E0), and
+// per-workgroup float64 sums of ds and ds * xhat per channel, ds = the masked
+// output, xhat = (E0 - mean) rstd: the partial sums of the batch-norm backward
+// of E0's batch norm, stored like STATS ([2][J][blocks]).
 // rout (stride-1 FWD with the transform, C a multiple of 4): the transformed
 // input [N,Hx,Wx,C] is also stored, every element once.
 void conv3x3(hipStream_t s, int mode, int S, int epi, const float *X, const float *Wt, float *Y,
@@ -88,6 +93,10 @@ void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const f
 void bn_backward(hipStream_t s, int64_t P, int J, const float *G, const float *Ym, const float *Cv,
                  const float *st, const float *gamma, double *part, float *sums, float *dgamma,
                  float *dbeta, float *D);
+// the element pass alone, D = dL/dC from the finalized sums (bn_finalize_bwd)
+void bn_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const float *Ym,
+                       const float *Cv, const float *st, const float *gamma, const float *sums,
+                       float *D);
 void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X, const float *Wf,
                      const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
                      float *G, float *dW, float *db, float *loss);

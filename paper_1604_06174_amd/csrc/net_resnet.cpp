@@ -106,6 +106,10 @@ class ResNetBasic : public Net {
                        k.cout * 9 * conv_in[c] * 4);
       }
       bnpart = std::max<uint64_t>(bnpart, uint64_t(bn_partial_blocks(np, k.cout)) * 2 * k.cout * 8);
+      if (k.w2 >= 0)  // the second convolution's data gradient sums the first BN's backward
+        bnpart = std::max<uint64_t>(
+            bnpart, uint64_t(conv3x3_blocks(CONV_DGRAD, 1, N, k.hout, k.hout, k.cout, k.cout)) * 2 *
+                        k.cout * 8);
     }
     const int CL = u.back().cout;
     uint64_t off = 0;
@@ -154,12 +158,13 @@ class ResNetBasic : public Net {
             const float *tb = nullptr, float *rout = nullptr) {
     const double fl = 2.0 * N * ho * ho * double(cout) * 9.0 * cin;
     double by = 4.0 * (double(N) * Hx * Wx * C + 9.0 * cin * cout + double(N) * H * W * J);
-    if (epi == CONV_EPI_MASK) by += 4.0 * N * H * W * J;
+    if (epi == CONV_EPI_MASK || epi == CONV_EPI_MASKSTATS) by += 4.0 * N * H * W * J;
     if (epi == CONV_EPI_SC1 || epi == CONV_EPI_SC2) by += 2 * 4.0 * N * Eh * Ew * std::min(Ec, J);
     if (rout) by += 4.0 * N * Hx * Wx * C;  // the transformed input, written once
     timer.begin(c.s);
     conv3x3(c.s, mode, s, epi, X, Wt, Y, N, H, W, Hx, Wx, C, J, E0, E1, Eh, Ew, Ec,
-            epi == CONV_EPI_STATS ? bnpart(c) : nullptr, tst, tg, tb, rout);
+            (epi == CONV_EPI_STATS || epi == CONV_EPI_MASKSTATS) ? bnpart(c) : nullptr, tst, tg, tb,
+            rout);
     timer.end(c.s, fl, by);
   }
   float *ksf(StepCtx &c, uint64_t off) const { return reinterpret_cast<float *>(c.ks + off); }
@@ -232,14 +237,18 @@ class ResNetBasic : public Net {
     const int ho = k.hout;
     // second BN (its input gradient is g masked by the block's final ReLU)
     bn_backward(c.s, np, k.cout, g, y, c2, st2, P(c, k.g2), bnpart(c), sums, G(c, k.g2), G(c, k.b2), Qb);
-    // conv2: data gradient masked by the first ReLU, and weight gradient
-    conv(c, CONV_DGRAD, 1, CONV_EPI_MASK, Qb, P(c, k.w2), Pb, ho, ho, ho, ho, k.cout, k.cout, x2,
-         nullptr, 0, 0, 0, ho, k.cout, k.cout, tst, tg, tb);
+    // conv2: data gradient masked by the first ReLU, formed from c1 and its
+    // statistics (the same bits as the stored relu(bn1(c1))), with the first
+    // BN backward's partial sums over the masked gradient and c1 in its
+    // epilogue; and conv2's weight gradient
+    conv(c, CONV_DGRAD, 1, CONV_EPI_MASKSTATS, Qb, P(c, k.w2), Pb, ho, ho, ho, ho, k.cout, k.cout, c1,
+         nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1));
     conv3x3_wgrad(c.s, 1, x2, Qb, wpart, G(c, k.w2), N, ho, ho, ho, ho, k.cout, k.cout, tst, tg, tb);
-    // first BN
-    bn_backward(c.s, np, k.cout, Pb, nullptr, c1, st1, P(c, k.g1), bnpart(c), sums, G(c, k.g1),
-                G(c, k.b1), Qb);
-    c.launches += 9;
+    // first BN: finalize those sums, then its element pass
+    bn_finalize_bwd(c.s, bnpart(c), conv3x3_blocks(CONV_DGRAD, 1, N, ho, ho, k.cout, k.cout), k.cout,
+                    np, sums, G(c, k.g1), G(c, k.b1), true);
+    bn_backward_apply(c.s, np, k.cout, Pb, nullptr, c1, st1, P(c, k.g1), sums, Qb);
+    c.launches += 8;
     if (dxv) {  // conv1 data gradient plus the shortcut's gradient
       conv(c, CONV_DGRAD, k.stride, k.stride == 1 ? CONV_EPI_SC1 : CONV_EPI_SC2, Qb, P(c, k.w1),
            static_cast<float *>(dxv), k.hin, k.hin, ho, ho, k.cout, k.cin, g, y, ho, ho, k.cout, ho,

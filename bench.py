@@ -14,7 +14,9 @@ Printed (one JSON line): samples/s of the checkpointed step, its peak
 activation bytes (exact, from the static layout), the recompute overhead
 (step time / the same kernels without checkpointing), the dominant kernel's
 roofline position from HIP events recorded around its launches in a second
-timed pass, and the CPU oracle's checkpointed step on a bounded sample.
+timed pass (against MFMA peak when the family's arithmetic intensity is at or
+above the ridge point, else against HBM bandwidth; both fractions are given),
+and the CPU oracle's checkpointed step on a bounded sample.
 """
 from __future__ import annotations
 
@@ -222,20 +224,31 @@ def main():
     step.net.timing_enable(False)
 
     dtype = cfg.get("dtype", "f32")  # "bf16": bf16 GEMM operands, fp32 accumulation
-    achieved = kt["flops"] / (kt["ms"] / 1e3) / 1e12 if kt["ms"] > 0 else 0.0
-    peak = PEAK_TFLOPS[dtype]
+    tflops = kt["flops"] / (kt["ms"] / 1e3) / 1e12 if kt["ms"] > 0 else 0.0
+    gbs = kt["bytes"] / (kt["ms"] / 1e3) / 1e9 if kt["ms"] > 0 else 0.0
+    peak_f = PEAK_TFLOPS[dtype]
+    # roofline placement: below the ridge (peak flops / peak bandwidth) the
+    # family's arithmetic intensity bounds it by HBM, above it by MFMA
+    ai = kt["flops"] / kt["bytes"] if kt["bytes"] > 0 else float("inf")
+    ridge = peak_f * 1e12 / (HBM_GBS * 1e9)
+    if ai >= ridge:
+        bound, achieved, peak, unit = "mfma", tflops, peak_f, "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", gbs, HBM_GBS, "GB/s"
     # counters were taken on the workload's default layout and plan family only
     tr = None if args.drop_bn_relu else _traffic(args.workload)
     alg_bytes = kt["bytes"] / max(kt["launches"], 1)
-    roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+    roof = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4),
+            "arithmetic_intensity": round(ai, 2), "ridge": round(ridge, 2),
+            "frac_mfma": round(tflops / peak_f, 4), "frac_hbm": round(gbs / HBM_GBS, 4),
             "traffic": tr["traffic_bytes_per_launch"] if tr else None,
             "algorithmic_bytes_per_launch": round(alg_bytes),
             "traffic_over_algorithmic": round(tr["traffic_bytes_per_launch"] / alg_bytes, 3) if tr else None,
             "kernel": kt["kernel"], "launches": kt["launches"],
             "avg_launch_us": round(kt["ms"] * 1e3 / max(kt["launches"], 1), 3),
             "flops_per_launch": kt["flops"] / max(kt["launches"], 1),
-            "hbm_gbs_algorithmic": round(kt["bytes"] / (kt["ms"] / 1e3) / 1e9, 1) if kt["ms"] > 0 else 0}
+            "tflops_algorithmic": round(tflops, 3), "hbm_gbs_algorithmic": round(gbs, 1)}
 
     cpu = None
     sample = args.cpu_sample

@@ -323,7 +323,14 @@ void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Y
   else
     hipLaunchKernelGGL((k_bnb_bwd_partials<false>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
   bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta, false);
+  bnb_backward_apply(s, P, J, G, Ym, Cv, st, gamma, sums, D);
+}
+
+void bnb_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const void *Ym,
+                        const void *Cv, const float *st, const float *gamma, const float *sums,
+                        void *D) {
   const int g = ew_grid(P * (J / 8));
+  const __bf16 *ym = static_cast<const __bf16 *>(Ym), *c = static_cast<const __bf16 *>(Cv);
   __bf16 *d = static_cast<__bf16 *>(D);
   if (ym)
     hipLaunchKernelGGL((k_bnb_bwd_apply<true>), dim3(g), dim3(256), 0, s, P, J, G, ym, c, st, gamma, sums, d);

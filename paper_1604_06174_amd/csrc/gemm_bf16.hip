@@ -23,6 +23,8 @@ Args make_args(int M, int N, int K, const void *A, int lda, const void *B, int l
   a.Ym = static_cast<const __bf16 *>(x.mask);
   a.Cb = static_cast<__bf16 *>(x.Cb);
   a.stats = x.stats;
+  a.Cv = static_cast<const __bf16 *>(x.cv);
+  a.bst = x.bst;
   a.kper = kper;
   return a;
 }
@@ -36,6 +38,10 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
   const int splits = x.splits < 1 ? 1 : x.splits;
   const Args a = make_args(M, N, K, A, lda, B, ldb, C, ldc, D, ldd, bias, x);
   const bool safe = !a_fp32 && safe8(a, ak, bk);
+  if (epi == GEMM_EPI_BNBWD &&
+      (!ak || bk || !safe || splits != 1 || ldc != N || !x.mask || !x.cv || !x.bst || !x.stats))
+    fail(CKPT_E_INVALID, "gemm_bf16x: BNBWD takes k-contiguous bf16 A, n-contiguous B, one split, "
+                         "ldc == N and the mask, input, statistics and partial buffers");
 #define CKPT_GB(AK_, BK_)                                                                  \
   if (ak == AK_ && bk == BK_) {                                                            \
     if (a_fp32) pick_tile<AK_, BK_, float, G_DENSE, G_DENSE, false>(a, epi, splits, s);    \

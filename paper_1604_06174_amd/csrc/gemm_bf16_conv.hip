@@ -1,6 +1,7 @@
 // Implicit-GEMM convolutions on the bf16 GEMM (gather modes of
 // gemm_bf16_kernel.h): forward, data gradient and weight gradient of an R x R
 // convolution with stride S in {1, 2} over NHWC bf16 tensors.
+#include "common.h"
 #include "gemm_bf16_kernel.h"
 
 namespace ckpt {
@@ -49,7 +50,10 @@ void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *W
 }
 
 void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void *Wt, float *DX,
-                     int epi, const float *D, const void *mask) {
+                     int epi, const float *D, const void *mask, const void *Cv, const float *bst,
+                     double *stats) {
+  if (epi == GEMM_EPI_BNBWD && (!mask || !Cv || !bst || !stats))
+    fail(CKPT_E_INVALID, "conv_bf16_dgrad: BNBWD needs the mask, input, statistics and partial buffers");
   const int M = g.N * g.H * g.W, N = g.Ci, K = g.R * g.R * g.Co;
   Args a = conv_args(g, M, N, K, g.Co);
   a.A = DY;
@@ -59,6 +63,9 @@ void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void
   a.D = D;
   a.ldd = N;
   a.Ym = static_cast<const __bf16 *>(mask);
+  a.Cv = static_cast<const __bf16 *>(Cv);
+  a.bst = bst;
+  a.stats = stats;
   pick_tile<true, false, __bf16, GA_DGRAD, GB_WDGRAD, true>(a, epi, 1, s);
 }
 

@@ -51,6 +51,7 @@
 namespace ckpt {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 namespace gb {
@@ -71,9 +72,11 @@ struct Args {
   const float *D;
   int ldd;
   const float *bias;
-  const __bf16 *Ym;  // ADDMASK mask
+  const __bf16 *Ym;  // ADDMASK / BNBWD mask
   __bf16 *Cb;        // BF16STATS output
-  double *stats;     // BF16STATS partial sums
+  double *stats;     // BF16STATS / BNBWD partial sums
+  const __bf16 *Cv;  // BNBWD: the batch norm's input, [M, N]
+  const float *bst;  // BNBWD: its mean [N] and 1/std [N]
   int kper;          // split-K: k per workgroup (multiple of 32)
   // gather geometry
   int H, W, Ho, Wo, R, S, P, cshift;
@@ -250,6 +253,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   __shared__ __align__(16) unsigned char smA[SZA];
   __shared__ __align__(16) unsigned char smB[SZB];
   static_assert(EPI != GEMM_EPI_BF16STATS || WM * 4 * 2 * BN * 8 <= SZA, "stats scratch");
+  static_assert(EPI != GEMM_EPI_BNBWD || WM * (64 / (WC / 4)) * 2 * BN * 8 <= SZA, "bnbwd scratch");
   static_assert(4 * 16 * SP * 4 <= SZA, "epilogue staging");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -487,7 +491,21 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   constexpr int RPP = 64 / LPR;                           // rows per pass
   static_assert(WC % VEC == 0 && 64 % LPR == 0 && 16 % RPP == 0, "epilogue layout");
   const bool vec_ok = (p.ldc % VEC == 0) &&
-                      (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_BF16STATS || p.ldd % 4 == 0);
+                      (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_BF16STATS || EPI == GEMM_EPI_BNBWD ||
+                       p.ldd % 4 == 0);
+  // BNBWD: each lane owns the same VEC columns in every pass; per column the
+  // batch norm's mean and 1/std, and float64 sums of ds and ds * xhat
+  float bmean[EPI == GEMM_EPI_BNBWD ? VEC : 1], brstd[EPI == GEMM_EPI_BNBWD ? VEC : 1];
+  double bs1[EPI == GEMM_EPI_BNBWD ? VEC : 1], bs2[EPI == GEMM_EPI_BNBWD ? VEC : 1];
+  if constexpr (EPI == GEMM_EPI_BNBWD) {
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      const int n = n0 + wn + (lane % LPR) * VEC + u;
+      bmean[u] = n < p.N ? p.bst[n] : 0.f;
+      brstd[u] = n < p.N ? p.bst[p.N + n] : 0.f;
+      bs1[u] = bs2[u] = 0.0;
+    }
+  }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
     __syncthreads();
@@ -515,6 +533,38 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
         } else {
           for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = (__bf16)v[u];
         }
+      } else if constexpr (EPI == GEMM_EPI_BNBWD) {
+        // ds = [Ym > 0] v, stored; xhat = (Cv - mean) / std
+        const size_t o = size_t(m) * p.ldc + n;
+        float y[VEC], cv[VEC];
+        if (full) {
+          const bf16x4 yh = *reinterpret_cast<const bf16x4 *>(p.Ym + o);
+          const bf16x4 ch = *reinterpret_cast<const bf16x4 *>(p.Cv + o);
+#pragma unroll
+          for (int u = 0; u < VEC; ++u) {
+            y[u] = float(yh[u]);
+            cv[u] = float(ch[u]);
+          }
+        } else {
+#pragma unroll
+          for (int u = 0; u < VEC; ++u) {
+            const bool in = n + u < p.N;
+            y[u] = in ? float(p.Ym[o + u]) : 0.f;
+            cv[u] = in ? float(p.Cv[o + u]) : 0.f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < VEC; ++u) {
+          v[u] = y[u] > 0.f ? v[u] : 0.f;
+          const float xh = (cv[u] - bmean[u]) * brstd[u];
+          bs1[u] += double(v[u]);
+          bs2[u] += double(v[u]) * double(xh);
+        }
+        float *dst = Cz + o;
+        if (full)
+          *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        else
+          for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = v[u];
       } else {
         if (EPI == GEMM_EPI_ADD || EPI == GEMM_EPI_ADDMASK) {
           const size_t o = size_t(m) * p.ldd + n;
@@ -543,6 +593,26 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
         else
           for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = v[u];
       }
+    }
+  }
+  if constexpr (EPI == GEMM_EPI_BNBWD) {
+    // per column: over the RPP lanes of a wavefront that share it, then over
+    // the WM wavefronts, in a fixed order; block-major partials
+    // [row tile][sum][column] as BF16STATS stores them
+    __syncthreads();
+    double *red = reinterpret_cast<double *>(smA);  // [WM * RPP][2][BN]
+    const int slot = (wave / WN) * RPP + lane / LPR, col0 = wn + (lane % LPR) * VEC;
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      red[(slot * 2 + 0) * BN + col0 + u] = bs1[u];
+      red[(slot * 2 + 1) * BN + col0 + u] = bs2[u];
+    }
+    __syncthreads();
+    if (tid < 2 * BN) {
+      const int which = tid / BN, col = tid % BN;
+      double t = 0.0;
+      for (int k = 0; k < WM * RPP; ++k) t += red[(k * 2 + which) * BN + col];
+      if (n0 + col < p.N) p.stats[(size_t(tm) * 2 + which) * p.N + n0 + col] = t;
     }
   }
 }
@@ -585,6 +655,13 @@ void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
     if (epi == GEMM_EPI_BF16STATS) {
       hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
       return;
+    }
+    // instantiated for the operand forms the host wrappers accept only
+    if constexpr (AK && !BK && SAFE) {
+      if (epi == GEMM_EPI_BNBWD) {
+        hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        return;
+      }
     }
   }
   hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE>), grid, dim3(256), 0, s, a);

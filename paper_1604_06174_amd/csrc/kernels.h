@@ -15,8 +15,15 @@ __device__ __forceinline__ float bn_relu(float x, float mean, float rstd, float 
   return fmaxf(__builtin_fmaf(g, (x - mean) * rstd, b), 0.f);
 }
 
+// GEMM_EPI_BNBWD (bf16 GEMM, k-contiguous bf16 A, n-contiguous B, one k
+// split, ldc == N): the product is the gradient G that reaches a batch norm's
+// output through a ReLU; the epilogue stores ds = [Ym > 0] G into C and
+// writes, per row tile of the GEMM, the float64 column sums of ds and of
+// ds * xhat, xhat = (Cv - mean) * rstd, block-major [row tile][2][N] (the
+// batch-norm backward's partial sums, so only its finalize and element pass
+// remain).
 enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4,
-       GEMM_EPI_BIAS = 5 };
+       GEMM_EPI_BIAS = 5, GEMM_EPI_BNBWD = 6 };
 
 // C = epilogue(op(A) op(B)); see gemm_f32.hip for the operand conventions.
 void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool ta, const float *B,
@@ -123,6 +130,11 @@ int bnb_partial_blocks(int64_t P, int J);
 void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
                   const float *st, const float *gamma, double *part, float *sums, float *dgamma,
                   float *dbeta, void *D);
+// The element pass of bnb_backward alone, given the finalized sums (2J floats:
+// mean of ds, mean of ds * xhat); Ym may be null (G already masked).
+void bnb_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const void *Ym,
+                        const void *Cv, const float *st, const float *gamma, const float *sums,
+                        void *D);
 // col [N*Ho*Wo, 147] bf16 = 7x7 / stride 2 / pad 3 patches of X [N, H, W, 3]
 void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, const void *X, void *col);
 // 3x3 / stride 2 / pad 1 max pool of R [N, H, W, C] into Y [N, Ho, Wo, C] (bf16)
@@ -144,9 +156,11 @@ void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, i
 // sums of the rounded values and squares (row blocks: gemm_bf16_row_blocks).
 struct GemmX {
   int splits = 1;
-  const void *mask = nullptr;
-  void *Cb = nullptr;
-  double *stats = nullptr;
+  const void *mask = nullptr;  // ADDMASK, BNBWD
+  void *Cb = nullptr;          // BF16STATS
+  double *stats = nullptr;     // BF16STATS, BNBWD
+  const void *cv = nullptr;    // BNBWD: the batch norm's input (bf16, [M, N])
+  const float *bst = nullptr;  // BNBWD: its mean [N] and 1/std [N]
 };
 void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                 const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D,
@@ -185,10 +199,12 @@ bool conv_bf16_supported(const ConvGeo &g);
 void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *Wt, void *Yb,
                    double *stats);
 // DX [N, H, W, Ci] fp32 = data gradient of DY [N, Ho, Wo, Co] (bf16) through
-// Wt; epi STORE, ADD (+ D) or ADDMASK (+ D where mask > 0), D and mask shaped
-// like DX.
+// Wt; epi STORE, ADD (+ D), ADDMASK (+ D where mask > 0) or BNBWD (mask, Cv,
+// bst and stats as for gemm_bf16x; stats gets gemm_bf16_row_blocks(M, Ci)
+// row tiles, M = N*H*W), D, mask and Cv shaped like DX.
 void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void *Wt, float *DX,
-                     int epi, const float *D = nullptr, const void *mask = nullptr);
+                     int epi, const float *D = nullptr, const void *mask = nullptr,
+                     const void *Cv = nullptr, const float *bst = nullptr, double *stats = nullptr);
 // dW [Co, R, R, Ci] fp32 = weight gradient from X (bf16 input) and DY (bf16
 // output gradient); split-K over the N*Ho*Wo pixels with `splits` partials
 // in part (splits * Co*R*R*Ci floats), added in a fixed order.

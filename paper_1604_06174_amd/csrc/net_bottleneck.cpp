@@ -126,6 +126,8 @@ class Bottleneck : public Net {
     auto st_need = [&](int64_t m, int j) {
       stats = std::max<uint64_t>(stats, uint64_t(gemm_bf16_row_blocks(int(m), j)) * 2 * j * 8);
       bnpart = std::max<uint64_t>(bnpart, uint64_t(bnb_partial_blocks(m, j)) * 2 * j * 8);
+      // the data-gradient GEMMs that form the batch-norm backward's partials
+      bnpart = std::max<uint64_t>(bnpart, uint64_t(gemm_bf16_row_blocks(int(m), j)) * 2 * j * 8);
       jmax = std::max(jmax, j);
     };
     auto wp_need = [&](int M, int Nn, int64_t Kd) {
@@ -333,24 +335,40 @@ class Bottleneck : public Net {
     c.launches += k.proj ? 6 : 3;
     // conv3 (1x1): weight and data gradients
     wgrad_1x1(c, k.cout, k.w, mo, qA, r2, G(c, k.W3));
+    // its epilogue masks the product by the second ReLU and adds up the second
+    // BN's backward sums (partials per row tile of the GEMM)
     tbeg(c);
-    gemm_bf16(c.s, int(mo), k.w, k.cout, qA, false, k.cout, true, Wb(c, k.W3), k.w, false, qB, k.w,
-              GEMM_EPI_STORE);
-    tend(c, double(mo), k.w, k.cout, 2.0 * (double(mo) * k.cout + double(k.cout) * k.w),
+    {
+      GemmX gx;
+      gx.mask = r2;
+      gx.cv = c2;
+      gx.bst = st2;
+      gx.stats = bnpart(c);
+      gemm_bf16x(c.s, int(mo), k.w, k.cout, qA, false, k.cout, true, Wb(c, k.W3), k.w, false, qB,
+                 k.w, GEMM_EPI_BNBWD, nullptr, 0, nullptr, gx);
+    }
+    tend(c, double(mo), k.w, k.cout,
+         2.0 * (double(mo) * k.cout + double(k.cout) * k.w) + 4.0 * double(mo) * k.w,
          4.0 * double(mo) * k.w);
-    // second BN, masked by the second ReLU
-    bnb_backward(c.s, mo, k.w, qB, r2, c2, st2, P(c, k.g2), bnpart(c), sums, G(c, k.g2), G(c, k.b2), qC);
-    c.launches += 3;
+    // second BN: finalize and element pass
+    bn_finalize_bwd(c.s, bnpart(c), gemm_bf16_row_blocks(int(mo), k.w), k.w, mo, sums, G(c, k.g2),
+                    G(c, k.b2), false);
+    bnb_backward_apply(c.s, mo, k.w, qB, nullptr, c2, st2, P(c, k.g2), sums, qC);
+    c.launches += 2;
     // conv2 (3x3, stride s)
     const ConvGeo g2{N, k.hin, k.hin, k.w, k.hout, k.hout, k.w, 3, k.stride, 1};
     wgrad_conv(c, g2, r1, qC, G(c, k.W2));
+    // with the first ReLU's mask and the first BN's backward sums in its epilogue
     tbeg(c);
-    conv_bf16_dgrad(c.s, g2, qC, Wb(c, k.W2), qB, GEMM_EPI_STORE);
-    tend(c, double(mi), k.w, 9.0 * k.w, 2.0 * (double(mo) * k.w + 9.0 * k.w * k.w),
+    conv_bf16_dgrad(c.s, g2, qC, Wb(c, k.W2), qB, GEMM_EPI_BNBWD, nullptr, r1, c1, st1, bnpart(c));
+    tend(c, double(mi), k.w, 9.0 * k.w,
+         2.0 * (double(mo) * k.w + 9.0 * k.w * k.w) + 4.0 * double(mi) * k.w,
          4.0 * double(mi) * k.w);
-    // first BN, masked by the first ReLU
-    bnb_backward(c.s, mi, k.w, qB, r1, c1, st1, P(c, k.g1), bnpart(c), sums, G(c, k.g1), G(c, k.b1), qA);
-    c.launches += 3;
+    // first BN: finalize and element pass
+    bn_finalize_bwd(c.s, bnpart(c), gemm_bf16_row_blocks(int(mi), k.w), k.w, mi, sums, G(c, k.g1),
+                    G(c, k.b1), false);
+    bnb_backward_apply(c.s, mi, k.w, qB, nullptr, c1, st1, P(c, k.g1), sums, qA);
+    c.launches += 2;
     // conv1 (1x1)
     wgrad_1x1(c, k.w, k.cin, mi, qA, xv, G(c, k.W1));
     if (dxv) {

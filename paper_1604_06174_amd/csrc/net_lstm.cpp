@@ -111,13 +111,15 @@ class LstmNet : public Net {
     timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
     c.launches += 1;
   }
-  // split-K partial products into slices [z0, z0 + splits) of the partial buffer
+  // split-K partial products into slices [z0, z0 + splits) of the partial buffer.
+  // Algorithmic bytes: each operand read once and the product written once
+  // (the slices are this implementation's, not the product's, traffic).
   void gemm_part(StepCtx &c, int M, int N, int Kd, const void *A, int lda, const void *Bm, int ldb,
                  int z0, int splits) {
     timer.begin(c.s);
     gemm_bf16_part(c.s, M, N, Kd, A, false, lda, true, Bm, ldb, true,
                    Kf(c, k_part) + size_t(z0) * M * N, splits);
-    timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * splits * M * N);
+    timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
     c.launches += 1;
   }
   void sum_parts(StepCtx &c, int ns, int M, int N, float *Cm, const float *D = nullptr, int ldd = 0,
@@ -149,7 +151,7 @@ class LstmNet : public Net {
       gemm_bf16_part_cat(c.s, B, 4 * H, E, xt, E, H, x, H, K(c, k_wcat), E + H, Kf(c, k_part),
                          s_x + s_h);
       timer.end(c.s, 2.0 * B * 4 * H * (E + H),
-                2.0 * (double(B) * (E + H) + double(E + H) * 4 * H) + 4.0 * (s_x + s_h) * B * 4 * H);
+                2.0 * (double(B) * (E + H) + double(E + H) * 4 * H) + 4.0 * B * 4 * H);
       c.launches += 1;
     } else {
       gemm_part(c, B, 4 * H, E, xt, E, K(c, k_wcat), E + H, 0, s_x);

@@ -93,9 +93,9 @@ __global__ __launch_bounds__(256) void k_sum_slices(const float *__restrict__ pa
 
 }  // namespace
 
-int gemm_bf16_splits(int M, int N, int K) {
+int gemm_bf16_splits(int M, int N, int K, int target) {
   const int tiles = gemm_bf16_tiles(M, N);
-  int s = (512 + tiles - 1) / tiles;
+  int s = (target + tiles - 1) / tiles;
   s = std::min(s, std::max(1, K / 128));  // at least 128 k per split
   return std::max(s, 1);
 }

@@ -171,7 +171,8 @@ int gemm_bf16_tiles(int M, int N);
 // [M, N] products (contiguous slices) of op(A) op(B) over consecutive k
 // ranges; sum_slices adds nslices such slices in order, then D and bias:
 // C = sum_z part[z] (+ D) (+ bias[n]).  N must be a multiple of 4.
-int gemm_bf16_splits(int M, int N, int K);
+// (splits chosen so that about `target` workgroups run, at least 128 k each)
+int gemm_bf16_splits(int M, int N, int K, int target = 512);
 void gemm_bf16_part(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                     const void *B, int ldb, bool bk, float *part, int splits);
 void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, float *C, int ldc,

@@ -83,13 +83,18 @@ class LstmNet : public Net {
     k_dbp = take(uint64_t(C) * ((B + 3) / 4) * 4 * H * 4);
     k_lossrows = take(uint64_t(T) * B * 4);
     k_loss = take(4);
-    s_x = gemm_bf16_splits(B, 4 * H, E);
-    s_h = gemm_bf16_splits(B, 4 * H, H);
+    // The forward's slices are read back by one small pointwise or softmax
+    // launch right away, so it takes fewer, longer splits (about 128
+    // workgroups per part: 256 for z over [x_t | h_{t-1}] at the
+    // 1024/1024/64 shape, 4 slices instead of 16, and one slice for the
+    // logits); the backward's products keep about 512 workgroups.
+    s_x = gemm_bf16_splits(B, 4 * H, E, 128);
+    s_h = gemm_bf16_splits(B, 4 * H, H, 128);
     // one launch for both parts of z when its k splits fall exactly on the two
     // parts' own splits (then every slice holds the same sums in the same order)
     zcat = E == H && s_x == s_h && gemm_bf16_kper(E, s_x) * s_x == E &&
            gemm_bf16_kper(E + H, s_x + s_h) == gemm_bf16_kper(E, s_x) && E % 8 == 0;
-    s_l = gemm_bf16_splits(B, V, H);
+    s_l = gemm_bf16_splits(B, V, H, 128);
     s_dh = gemm_bf16_splits(B, H, V);
     s_dx = gemm_bf16_splits(B, H, 4 * H);
     const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(s_l) * B * V,

@@ -73,7 +73,9 @@ struct Exec {
         next = dst ? EXTERNAL : BOTTOM;
       }
       (void)ai;
+      c.keep_saved = false;
       net.fwd(i, cur_x, y, saved, c);
+      c.keep_saved = true;
       ++fwd_count;
       cur_x = y;
       pos = next;
@@ -255,6 +257,7 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
     e.recursive(p, batch.input);
   else
     e.one_level(p, batch.input);
+  net.end_step(c);
   if (loss_dev) {
     copy_scalar(s, net.loss_ptr(c), loss_dev);
     ++c.launches;

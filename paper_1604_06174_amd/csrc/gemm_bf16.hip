@@ -25,6 +25,7 @@ Args make_args(int M, int N, int K, const void *A, int lda, const void *B, int l
   a.stats = x.stats;
   a.Cv = static_cast<const __bf16 *>(x.cv);
   a.bst = x.bst;
+  a.rstat = x.rstat;
   a.kper = kper;
   return a;
 }
@@ -42,6 +43,10 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
       (!ak || bk || !safe || splits != 1 || ldc != N || !x.mask || !x.cv || !x.bst || !x.stats))
     fail(CKPT_E_INVALID, "gemm_bf16x: BNBWD takes k-contiguous bf16 A, n-contiguous B, one split, "
                          "ldc == N and the mask, input, statistics and partial buffers");
+  if (epi == GEMM_EPI_ROWSOFTMAX &&
+      (!ak || !bk || !safe || splits != 1 || ldc != N || N % 4 != 0 || !bias || !x.rstat))
+    fail(CKPT_E_INVALID, "gemm_bf16x: ROWSOFTMAX takes k-contiguous bf16 A and B, one split, "
+                         "ldc == N, N % 4 == 0, a bias and the row-statistics buffer");
 #define CKPT_GB(AK_, BK_)                                                                  \
   if (ak == AK_ && bk == BK_) {                                                            \
     if (a_fp32) pick_tile<AK_, BK_, float, G_DENSE, G_DENSE, false>(a, epi, splits, s);    \
@@ -138,6 +143,11 @@ void sum_slices(hipStream_t s, const float *part, int nslices, int M, int N, flo
 int gemm_bf16_row_blocks(int M, int N) {
   const Tile t = tile_of(M, N);
   return (M + t.BM - 1) / t.BM;
+}
+
+int gemm_bf16_col_blocks(int M, int N) {
+  const Tile t = tile_of(M, N);
+  return (N + t.BN - 1) / t.BN;
 }
 
 int gemm_bf16_tiles(int M, int N) {

@@ -77,6 +77,7 @@ struct Args {
   double *stats;     // BF16STATS / BNBWD partial sums
   const __bf16 *Cv;  // BNBWD: the batch norm's input, [M, N]
   const float *bst;  // BNBWD: its mean [N] and 1/std [N]
+  float *rstat;      // ROWSOFTMAX: per row and column tile, (max, sum of exp(x - max))
   int kper;          // split-K: k per workgroup (multiple of 32)
   // gather geometry
   int H, W, Ho, Wo, R, S, P, cshift;
@@ -254,6 +255,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   __shared__ __align__(16) unsigned char smB[SZB];
   static_assert(EPI != GEMM_EPI_BF16STATS || WM * 4 * 2 * BN * 8 <= SZA, "stats scratch");
   static_assert(EPI != GEMM_EPI_BNBWD || WM * (64 / (WC / 4)) * 2 * BN * 8 <= SZA, "bnbwd scratch");
+  // ROWSOFTMAX: each wavefront column's (max, sum of exp) per row of the tile
+  __shared__ float rsm[EPI == GEMM_EPI_ROWSOFTMAX ? WN * BM * 2 : 1];
   static_assert(4 * 16 * SP * 4 <= SZA, "epilogue staging");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -492,7 +495,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   static_assert(WC % VEC == 0 && 64 % LPR == 0 && 16 % RPP == 0, "epilogue layout");
   const bool vec_ok = (p.ldc % VEC == 0) &&
                       (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_BF16STATS || EPI == GEMM_EPI_BNBWD ||
-                       p.ldd % 4 == 0);
+                       EPI == GEMM_EPI_ROWSOFTMAX || p.ldd % 4 == 0);
   // BNBWD: each lane owns the same VEC columns in every pass; per column the
   // batch norm's mean and 1/std, and float64 sums of ds and ds * xhat
   float bmean[EPI == GEMM_EPI_BNBWD ? VEC : 1], brstd[EPI == GEMM_EPI_BNBWD ? VEC : 1];
@@ -518,6 +521,40 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     for (int pass = 0; pass < 16 / RPP; ++pass) {
       const int rr = pass * RPP + lane / LPR, cc = (lane % LPR) * VEC;
       const int m = m0 + wm + a * 16 + rr, n = n0 + wn + cc;
+      if constexpr (EPI == GEMM_EPI_ROWSOFTMAX) {
+        // C = product + bias; the LPR lanes that share a row combine their
+        // (max, sum of exp) pairs by a butterfly (every lane takes part)
+        const bool row_ok = m < p.M;
+        float v[VEC], lm = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < VEC; ++u) {
+          const bool ok = row_ok && n + u < p.N;
+          v[u] = ok ? stage[rr * SP + cc + u] + p.bias[n + u] : -INFINITY;
+          lm = fmaxf(lm, v[u]);
+        }
+        float ls = 0.f;
+#pragma unroll
+        for (int u = 0; u < VEC; ++u) ls += lm == -INFINITY ? 0.f : expf(v[u] - lm);
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) {
+          const float om = __shfl_xor(lm, o, 64), os = __shfl_xor(ls, o, 64);
+          const float mx = fmaxf(lm, om);
+          ls = mx == -INFINITY ? 0.f : ls * expf(lm - mx) + os * expf(om - mx);
+          lm = mx;
+        }
+        if (lane % LPR == 0) {
+          rsm[((wave % WN) * BM + wm + a * 16 + rr) * 2 + 0] = lm;
+          rsm[((wave % WN) * BM + wm + a * 16 + rr) * 2 + 1] = ls;
+        }
+        if (row_ok && n < p.N) {
+          float *dst = Cz + size_t(m) * p.ldc + n;
+          if (vec_ok && n + VEC <= p.N)
+            *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+          else
+            for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = v[u];
+        }
+        continue;
+      }
       if (m >= p.M || n >= p.N) continue;
       float v[VEC];
 #pragma unroll
@@ -595,6 +632,23 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       }
     }
   }
+  if constexpr (EPI == GEMM_EPI_ROWSOFTMAX) {
+    // per row: the WN wavefront columns' pairs combined in order, stored as
+    // rstat[row][column tile][2]
+    __syncthreads();
+    if (tid < BM && m0 + tid < p.M) {
+      float lm = rsm[tid * 2], ls = rsm[tid * 2 + 1];
+      for (int w = 1; w < WN; ++w) {
+        const float om = rsm[(w * BM + tid) * 2], os = rsm[(w * BM + tid) * 2 + 1];
+        const float mx = fmaxf(lm, om);
+        ls = mx == -INFINITY ? 0.f : ls * expf(lm - mx) + os * expf(om - mx);
+        lm = mx;
+      }
+      float *r = p.rstat + (size_t(m0 + tid) * gridDim.x + tn) * 2;
+      r[0] = lm;
+      r[1] = ls;
+    }
+  }
   if constexpr (EPI == GEMM_EPI_BNBWD) {
     // per column: over the RPP lanes of a wavefront that share it, then over
     // the WM wavefronts, in a fixed order; block-major partials
@@ -660,6 +714,12 @@ void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
     if constexpr (AK && !BK && SAFE) {
       if (epi == GEMM_EPI_BNBWD) {
         hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        return;
+      }
+    }
+    if constexpr (AK && BK && SAFE && GA == G_DENSE && GB == G_DENSE) {
+      if (epi == GEMM_EPI_ROWSOFTMAX) {
+        hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
         return;
       }
     }

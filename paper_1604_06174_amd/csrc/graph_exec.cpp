@@ -130,6 +130,7 @@ void run_graph_step(Net &net, const float *params, float *grads, const ckpt_batc
     net.node_bwd(v, dy, y, ins, at(w), c);
     ++bwd;
   }
+  net.end_step(c);
   if (loss_dev) {
     copy_scalar(s, net.loss_ptr(c), loss_dev);
     ++c.launches;

@@ -22,8 +22,12 @@ __device__ __forceinline__ float bn_relu(float x, float mean, float rstd, float 
 // ds * xhat, xhat = (Cv - mean) * rstd, block-major [row tile][2][N] (the
 // batch-norm backward's partial sums, so only its finalize and element pass
 // remain).
+// GEMM_EPI_ROWSOFTMAX (bf16 GEMM, k-contiguous dense A and B, one k split,
+// ldc == N, N % 4 == 0): C = product + bias[n]; per row m and column tile t
+// (gemm_bf16_col_blocks(M, N) tiles) rstat[(m * tiles + t) * 2] = the row's
+// maximum over the tile's columns and the sum of exp(C - maximum) over them.
 enum { GEMM_EPI_STORE = 0, GEMM_EPI_ADD = 1, GEMM_EPI_MLPFWD = 2, GEMM_EPI_BF16STATS = 3, GEMM_EPI_ADDMASK = 4,
-       GEMM_EPI_BIAS = 5, GEMM_EPI_BNBWD = 6 };
+       GEMM_EPI_BIAS = 5, GEMM_EPI_BNBWD = 6, GEMM_EPI_ROWSOFTMAX = 7 };
 
 // C = epilogue(op(A) op(B)); see gemm_f32.hip for the operand conventions.
 void gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, bool ta, const float *B,
@@ -161,11 +165,13 @@ struct GemmX {
   double *stats = nullptr;     // BF16STATS, BNBWD
   const void *cv = nullptr;    // BNBWD: the batch norm's input (bf16, [M, N])
   const float *bst = nullptr;  // BNBWD: its mean [N] and 1/std [N]
+  float *rstat = nullptr;      // ROWSOFTMAX: [M][column tiles][2]
 };
 void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                 const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D,
                 int ldd, const float *bias, const GemmX &x);
 int gemm_bf16_row_blocks(int M, int N);
+int gemm_bf16_col_blocks(int M, int N);
 int gemm_bf16_tiles(int M, int N);
 // Split-K for short, wide products: gemm_bf16_part writes `splits` partial
 // [M, N] products (contiguous slices) of op(A) op(B) over consecutive k
@@ -221,8 +227,12 @@ void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst);
 // as sum_slices would.
 void lstm_fwd_point(hipStream_t s, int B, int H, const float *zpart, int ns, const float *bias,
                     const float *c_prev, float *gates, void *h_out, float *c_out);
-void softmax_ce_rows(hipStream_t s, int rows, int V, const float *lpart, int ns, const float *bias,
-                     const int *labels, float scale, float *dlog, float *loss_rows);
+// Softmax cross-entropy rows: loss_rows[r] = logsumexp(l[r]) - l[r][label],
+// dlog = (softmax - onehot) * scale, from the logits [rows, V] (bias
+// included) and the per row and column tile (max, sum of exp) pairs that
+// GEMM_EPI_ROWSOFTMAX wrote (nt tiles per row); V % 4 == 0.
+void softmax_ce_tiles(hipStream_t s, int rows, int V, const float *logits, int nt, const float *rstat,
+                      const int *labels, float scale, float *dlog, float *loss_rows);
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first);
 // dbp receives ceil(B/4) records [4H] of bias-gradient column sums (one per
 // block of 4 batch rows); db_chunk adds a run of such records into db.

@@ -8,6 +8,7 @@
 // the shapes alone, so a step is bit-reproducible whatever the schedule.
 #include <hip/hip_runtime.h>
 
+#include "common.h"
 #include "kernels.h"
 
 namespace ckpt {
@@ -93,75 +94,51 @@ __global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const floa
   h_out[e] = (__bf16)(og * tanhf(c));
 }
 
-// One workgroup per row: loss_row = log sum exp(l - max) + max - l[label];
-// dlog = (softmax - onehot) * scale.  A label outside [0, V) gives a NaN loss
-// for the row and no one-hot term.
-// One workgroup of 1024 threads per row: each thread keeps its (at most
-// SM_PER) logits in registers; max and sum are reduced by wavefront
-// butterflies and then across the 16 wavefronts in a fixed order.
-constexpr int SM_THREADS = 1024, SM_PER = 16;
-
-__device__ __forceinline__ float wave_max(float v) {
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+// (m, s) <- the pair for the union of two column sets: m the larger maximum,
+// s both sums rescaled to it (0 while both sets are empty)
+__device__ __forceinline__ void lse_combine(float &m, float &s, float om, float os) {
+  const float mx = fmaxf(m, om);
+  s = mx == -INFINITY ? 0.f : s * expf(m - mx) + os * expf(om - mx);
+  m = mx;
 }
 
-// logits = sum of the ns partial slices [rows, V] + bias
-__global__ __launch_bounds__(SM_THREADS) void k_softmax_ce_rows(int V, const float *__restrict__ lpart,
-                                                                int ns, size_t slice,
-                                                                const float *__restrict__ bias,
-                                                                const int *__restrict__ labels, float scale,
-                                                                float *__restrict__ dlog,
-                                                                float *__restrict__ loss_rows) {
-  __shared__ float red[SM_THREADS / 64];
-  __shared__ float lab_logit;
-  const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const size_t r0 = size_t(row) * V;
+// Softmax cross-entropy: loss_row = log sum exp(l - max) + max - l[label],
+// dlog = (softmax - onehot) * scale (a label outside [0, V) gives a NaN loss
+// for the row and no one-hot term), from the logits l (bias included) and
+// each row's (max, sum of exp) pairs per column tile of the product that
+// wrote them.  Every
+// wavefront combines its row's pairs itself (lane j takes tiles j, j + 64,
+// ... in order, then a butterfly, whose pairwise combinations are symmetric),
+// so all workgroups of a row use the same maximum and sum with no exchange
+// between them.  Workgroup = 1024 columns of one row, four per thread.
+__global__ __launch_bounds__(256) void k_softmax_ce_tiles(int V, const float *__restrict__ logits, int nt,
+                                                          const float *__restrict__ rstat,
+                                                          const int *__restrict__ labels, float scale,
+                                                          float *__restrict__ dlog,
+                                                          float *__restrict__ loss_rows) {
+  const int row = blockIdx.y, lane = threadIdx.x & 63;
+  const float *rs = rstat + size_t(row) * nt * 2;
+  float m = -INFINITY, se = 0.f;
+  for (int j = lane; j < nt; j += 64) lse_combine(m, se, rs[2 * j], rs[2 * j + 1]);
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, 64), os = __shfl_xor(se, o, 64);
+    lse_combine(m, se, om, os);
+  }
   const int lab = labels[row];
-  float x[SM_PER];
-  size_t o[SM_PER];
-  // columns past V read column V - 1 (in bounds) and are dropped below
-#pragma unroll
-  for (int k = 0; k < SM_PER; ++k) o[k] = r0 + min(t + k * SM_THREADS, V - 1);
-  slices_sum<SM_PER, 1>(lpart, ns, slice, o, x);
-  float mx = -INFINITY;
-#pragma unroll
-  for (int k = 0; k < SM_PER; ++k) {
-    const int v = t + k * SM_THREADS;
-    x[k] = v < V ? x[k] + bias[v] : -INFINITY;
-    if (v == lab) lab_logit = x[k];
-    mx = fmaxf(mx, x[k]);
-  }
-  mx = wave_max(mx);
-  if (lane == 0) red[w] = mx;
-  __syncthreads();
-  mx = red[0];
-  for (int k = 1; k < SM_THREADS / 64; ++k) mx = fmaxf(mx, red[k]);
-  __syncthreads();
-  float se = 0.f;
-#pragma unroll
-  for (int k = 0; k < SM_PER; ++k) {
-    const int v = t + k * SM_THREADS;
-    x[k] = v < V ? expf(x[k] - mx) : 0.f;
-    se += x[k];
-  }
-  se = wave_sum(se);
-  if (lane == 0) red[w] = se;
-  __syncthreads();
-  se = 0.f;
-  for (int k = 0; k < SM_THREADS / 64; ++k) se += red[k];
-  const bool ok = lab >= 0 && lab < V;
-  if (t == 0) loss_rows[row] = ok ? (logf(se) + mx) - lab_logit : NAN;
   const float inv = 1.0f / se;
-  float *d = dlog + size_t(row) * V;
+  const int v0 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  const float *x = logits + size_t(row) * V;
+  if (v0 < V) {
+    const float4 xv = *reinterpret_cast<const float4 *>(x + v0);
+    const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+    float d[4];
 #pragma unroll
-  for (int k = 0; k < SM_PER; ++k) {
-    const int v = t + k * SM_THREADS;
-    if (v < V) d[v] = (x[k] * inv - (v == lab ? 1.f : 0.f)) * scale;
+    for (int u = 0; u < 4; ++u) d[u] = (expf(xs[u] - m) * inv - (v0 + u == lab ? 1.f : 0.f)) * scale;
+    *reinterpret_cast<float4 *>(dlog + size_t(row) * V + v0) = make_float4(d[0], d[1], d[2], d[3]);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const bool ok = lab >= 0 && lab < V;
+    loss_rows[row] = ok ? (logf(se) + m) - x[lab] : NAN;
   }
 }
 
@@ -177,10 +154,23 @@ __global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float
   const int v = blockIdx.x * 64 + cx;
   float s = 0.f;
   if (v < V)
-    for (int b = rg; b < B; b += 4) {
-      const float d = dlog[size_t(b) * V + v];
-      dl_bf[size_t(b) * V + v] = (__bf16)d;
-      s += d;
+    // rows rg, rg + 4, ... eight at a time: the eight loads are issued before
+    // any is used; the sum still runs over the rows in order
+    for (int b0 = rg; b0 < B; b0 += 32) {
+      float d[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int b = b0 + 4 * u;
+        d[u] = b < B ? dlog[size_t(b) * V + v] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int b = b0 + 4 * u;
+        if (b < B) {
+          dl_bf[size_t(b) * V + v] = (__bf16)d[u];
+          s += d[u];
+        }
+      }
     }
   part[rg][cx] = s;
   __syncthreads();
@@ -314,10 +304,13 @@ void lstm_fwd_point(hipStream_t s, int B, int H, const float *zpart, int ns, con
                      bias, c_prev, gates, static_cast<__bf16 *>(h_out), c_out);
 }
 
-void softmax_ce_rows(hipStream_t s, int rows, int V, const float *lpart, int ns, const float *bias,
-                     const int *labels, float scale, float *dlog, float *loss_rows) {
-  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(rows), dim3(SM_THREADS), 0, s, V, lpart, ns,
-                     size_t(rows) * V, bias, labels, scale, dlog, loss_rows);
+void softmax_ce_tiles(hipStream_t s, int rows, int V, const float *logits, int nt, const float *rstat,
+                      const int *labels, float scale, float *dlog, float *loss_rows) {
+  if (V % 4 != 0 || reinterpret_cast<uintptr_t>(logits) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(dlog) % 16 != 0)
+    fail(CKPT_E_INVALID, "softmax_ce_tiles: V must be a multiple of 4 and the rows 16-byte aligned");
+  hipLaunchKernelGGL(k_softmax_ce_tiles, dim3((V + 1023) / 1024, rows), dim3(256), 0, s, V, logits, nt,
+                     rstat, labels, scale, dlog, loss_rows);
 }
 
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {

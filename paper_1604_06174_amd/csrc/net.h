@@ -77,6 +77,9 @@ struct StepCtx {
   char *ks = nullptr;             // device operator workspace (net.ks_bytes)
   char *gextra = nullptr;         // device fixed gradient buffers (net.grad_extra)
   uint64_t launches = 0;
+  // false while a forward sweep runs whose saved internals are discarded
+  // (they are formed again by the unit's re-run before its backward)
+  bool keep_saved = true;
 };
 
 class Net {
@@ -100,14 +103,19 @@ class Net {
   virtual ~Net() = default;
 
   // Unit i forward: x (x_i) -> y (x_{i+1}); saved internals written to `saved`.
+  // Every unit runs exactly one forward with c.keep_saved set before its
+  // backward; a forward with it clear may leave out work whose only results
+  // are saved internals (and loss terms, which the kept forward then adds).
   virtual void fwd(int32_t i, const void *x, void *y, void *saved, StepCtx &c) = 0;
   // Unit i backward: g = dL/dx_{i+1} -> dx = dL/dx_i (dx is null for unit 0),
   // reading x, y and saved; q is the unit's gradient scratch.  Writes unit i's
   // parameter gradients.
   virtual void bwd(int32_t i, const void *g, void *dx, const void *x, const void *y,
                    const void *saved, void *q, StepCtx &c) = 0;
-  // Called once at the start of every step, before any unit runs.
+  // Called once at the start of every step, before any unit runs, and once at
+  // its end, after the last backward.
   virtual void begin_step(StepCtx &) {}
+  virtual void end_step(StepCtx &) {}
   // Head: x_n -> g = dL/dx_n (+ head parameter gradients), loss into ks.
   virtual void head(const void *xn, void *g, StepCtx &c) = 0;
   // Device address of the f32 loss after the step.

@@ -13,6 +13,12 @@
 // the chunk grouping does not depend on the plan, so every plan gives the same
 // bytes.  Bias gradients accumulate step by step.
 //
+// The head of a step (logits, softmax gradient, loss rows) feeds only the
+// unit's saved internals and the loss, so a forward whose saved internals are
+// discarded (a checkpointed step's forward sweeps) runs the recurrence alone;
+// the head runs in the unit's kept forward, once per step in every plan, and
+// the loss rows are reduced after the last backward.
+//
 // Static layout: boundary b = h (bf16 [B,H]) | c (fp32 [B,H]); saved a = gates
 // (fp32 [B,4H]) | softmax gradient (fp32 [B,V]); scratch q = total dh (fp32
 // [B,H]); gradient slot = dh | dc (fp32); extra gradient buffers = the chunk's
@@ -33,10 +39,11 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part;
+  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part, k_rstat;
   bool zcat;  // z = [x_t | h_{t-1}] [W_x; W_h] as one product (same slices as the two)
-  // split-K counts: input and recurrent parts of z, logits, dh (head), dh_{t-1}
-  int s_x, s_h, s_l, s_dh, s_dx;
+  // split-K counts: input and recurrent parts of z, dh (head), dh_{t-1}; the
+  // logits are one product (their softmax statistics come from its epilogue)
+  int s_x, s_h, s_dh, s_dx;
   // extra gradient buffer offsets
   uint64_t x_dz, x_dl, x_hp, x_hc;
 
@@ -83,23 +90,22 @@ class LstmNet : public Net {
     k_dbp = take(uint64_t(C) * ((B + 3) / 4) * 4 * H * 4);
     k_lossrows = take(uint64_t(T) * B * 4);
     k_loss = take(4);
-    // The forward's slices are read back by one small pointwise or softmax
-    // launch right away, so it takes fewer, longer splits (about 128
-    // workgroups per part: 256 for z over [x_t | h_{t-1}] at the
-    // 1024/1024/64 shape, 4 slices instead of 16, and one slice for the
-    // logits); the backward's products keep about 512 workgroups.
+    // z's slices are read back by the pointwise launch right away, so it takes
+    // fewer, longer splits (about 128 workgroups per part: 256 for z over
+    // [x_t | h_{t-1}] at the 1024/1024/64 shape, 4 slices instead of 16); the
+    // backward's products keep about 512 workgroups.
     s_x = gemm_bf16_splits(B, 4 * H, E, 128);
     s_h = gemm_bf16_splits(B, 4 * H, H, 128);
     // one launch for both parts of z when its k splits fall exactly on the two
     // parts' own splits (then every slice holds the same sums in the same order)
     zcat = E == H && s_x == s_h && gemm_bf16_kper(E, s_x) * s_x == E &&
            gemm_bf16_kper(E + H, s_x + s_h) == gemm_bf16_kper(E, s_x) && E % 8 == 0;
-    s_l = gemm_bf16_splits(B, V, H, 128);
     s_dh = gemm_bf16_splits(B, H, V);
     s_dx = gemm_bf16_splits(B, H, 4 * H);
-    const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(s_l) * B * V,
+    const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(B) * V,
                                     uint64_t(std::max(s_dh, s_dx)) * B * H});
     k_part = take(part * 4);
+    k_rstat = take(uint64_t(B) * gemm_bf16_col_blocks(B, V) * 2 * 4);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
   }
@@ -166,10 +172,24 @@ class LstmNet : public Net {
     float *gates = reinterpret_cast<float *>(sv);
     lstm_fwd_point(c.s, B, H, Kf(c, k_part), s_x + (i > 0 ? s_h : 0), P(c, pb), c_prev, gates, y,
                    reinterpret_cast<float *>(y + hb));
-    // logits = h_t W_o + b_o, summed from its slices by the softmax kernel
-    gemm_part(c, B, V, H, y, H, K(c, k_wot), H, 0, s_l);
-    softmax_ce_rows(c.s, B, V, Kf(c, k_part), s_l, P(c, pbo), lab, 1.0f / (float(T) * float(B)),
-                    reinterpret_cast<float *>(sv + ga), Kf(c, k_lossrows) + size_t(i) * B);
+    c.launches += 1;
+    // The head feeds only the saved softmax gradient and the step's loss term:
+    // a forward whose saved internals are discarded leaves it to the unit's
+    // re-run, so it runs once per step as without checkpointing.
+    if (!c.keep_saved) return;
+    // logits = h_t W_o + b_o, with each row's (max, sum of exp) per column
+    // tile formed in the product's epilogue; then the softmax pass
+    {
+      GemmX gx;
+      gx.rstat = Kf(c, k_rstat);
+      timer.begin(c.s);
+      gemm_bf16x(c.s, B, V, H, y, false, H, true, K(c, k_wot), H, true, Kf(c, k_part), V,
+                 GEMM_EPI_ROWSOFTMAX, nullptr, 0, P(c, pbo), gx);
+      timer.end(c.s, 2.0 * B * V * H, 2.0 * (double(B) * H + double(H) * V) + 4.0 * B * V);
+    }
+    softmax_ce_tiles(c.s, B, V, Kf(c, k_part), gemm_bf16_col_blocks(B, V), Kf(c, k_rstat), lab,
+                     1.0f / (float(T) * float(B)), reinterpret_cast<float *>(sv + ga),
+                     Kf(c, k_lossrows) + size_t(i) * B);
     c.launches += 2;
   }
 
@@ -224,8 +244,14 @@ class LstmNet : public Net {
 
   void head(const void *, void *g, StepCtx &c) override {
     fill_f32(c.s, int64_t(gslot_bytes / 4), static_cast<float *>(g), 0.f);
+    c.launches += 1;
+  }
+
+  // the loss: every step's rows are in place once each unit has run its kept
+  // forward, i.e. after the last backward
+  void end_step(StepCtx &c) override {
     loss_reduce(c.s, int64_t(T) * B, Kf(c, k_lossrows), 1.0f / (float(T) * float(B)), Kf(c, k_loss));
-    c.launches += 2;
+    c.launches += 1;
   }
 
   const float *loss_ptr(const StepCtx &c) const override {

@@ -509,6 +509,15 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       bs1[u] = bs2[u] = 0.0;
     }
   }
+  // ROWSOFTMAX: the bias of the lane's VEC columns (-inf past N), loaded once
+  float rbias[EPI == GEMM_EPI_ROWSOFTMAX ? VEC : 1];
+  if constexpr (EPI == GEMM_EPI_ROWSOFTMAX) {
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      const int n = n0 + wn + (lane % LPR) * VEC + u;
+      rbias[u] = n < p.N ? p.bias[n] : -INFINITY;
+    }
+  }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
     __syncthreads();
@@ -522,26 +531,25 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
       const int rr = pass * RPP + lane / LPR, cc = (lane % LPR) * VEC;
       const int m = m0 + wm + a * 16 + rr, n = n0 + wn + cc;
       if constexpr (EPI == GEMM_EPI_ROWSOFTMAX) {
-        // C = product + bias; the LPR lanes that share a row combine their
-        // (max, sum of exp) pairs by a butterfly (every lane takes part)
+        // C = product + bias; the LPR lanes that share a row reduce by
+        // butterflies (every lane takes part)
         const bool row_ok = m < p.M;
         float v[VEC], lm = -INFINITY;
 #pragma unroll
         for (int u = 0; u < VEC; ++u) {
-          const bool ok = row_ok && n + u < p.N;
-          v[u] = ok ? stage[rr * SP + cc + u] + p.bias[n + u] : -INFINITY;
+          v[u] = row_ok ? stage[rr * SP + cc + u] + rbias[u] : -INFINITY;
           lm = fmaxf(lm, v[u]);
         }
+        // the row's maximum over the wavefront's columns first, then the sum
+        // of exp(x - maximum), one hardware exp per element (relative error
+        // about 1e-6 in the softmax denominator)
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) lm = fmaxf(lm, __shfl_xor(lm, o, 64));
         float ls = 0.f;
 #pragma unroll
-        for (int u = 0; u < VEC; ++u) ls += lm == -INFINITY ? 0.f : expf(v[u] - lm);
+        for (int u = 0; u < VEC; ++u) ls += lm == -INFINITY ? 0.f : __expf(v[u] - lm);
 #pragma unroll
-        for (int o = 1; o < LPR; o <<= 1) {
-          const float om = __shfl_xor(lm, o, 64), os = __shfl_xor(ls, o, 64);
-          const float mx = fmaxf(lm, om);
-          ls = mx == -INFINITY ? 0.f : ls * expf(lm - mx) + os * expf(om - mx);
-          lm = mx;
-        }
+        for (int o = 1; o < LPR; o <<= 1) ls += __shfl_xor(ls, o, 64);
         if (lane % LPR == 0) {
           rsm[((wave % WN) * BM + wm + a * 16 + rr) * 2 + 0] = lm;
           rsm[((wave % WN) * BM + wm + a * 16 + rr) * 2 + 1] = ls;

@@ -21,7 +21,9 @@
 //
 // Static layout: boundary b = h (bf16 [B,H]) | c (fp32 [B,H]); saved a = gates
 // (fp32 [B,4H]) | softmax gradient (fp32 [B,V]); scratch q = total dh (fp32
-// [B,H]); gradient slot = dh | dc (fp32); extra gradient buffers = the chunk's
+// [B,H]); gradient slot = dh | dc (fp32; dh_{t-1} travels instead as the
+// split-K slices of dz W_h^T in operator workspace, added up by the previous
+// step's gate backward); extra gradient buffers = the chunk's
 // dz (bf16 [C*B,4H]), head gradient (bf16 [C*B,V]), h_{t-1} and h_t copies
 // (bf16 [C*B,H]).
 #include <algorithm>
@@ -39,7 +41,7 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part, k_rstat;
+  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part, k_rstat, k_dxp;
   bool zcat;  // z = [x_t | h_{t-1}] [W_x; W_h] as one product (same slices as the two)
   // split-K counts: input and recurrent parts of z, dh (head), dh_{t-1}; the
   // logits are one product (their softmax statistics come from its epilogue)
@@ -103,8 +105,9 @@ class LstmNet : public Net {
     s_dh = gemm_bf16_splits(B, H, V);
     s_dx = gemm_bf16_splits(B, H, 4 * H);
     const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(B) * V,
-                                    uint64_t(std::max(s_dh, s_dx)) * B * H});
+                                    uint64_t(s_dh) * B * H});
     k_part = take(part * 4);
+    k_dxp = take(uint64_t(s_dx) * B * H * 4);
     k_rstat = take(uint64_t(B) * gemm_bf16_col_blocks(B, V) * 2 * 4);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
@@ -131,11 +134,6 @@ class LstmNet : public Net {
     gemm_bf16_part(c.s, M, N, Kd, A, false, lda, true, Bm, ldb, true,
                    Kf(c, k_part) + size_t(z0) * M * N, splits);
     timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
-    c.launches += 1;
-  }
-  void sum_parts(StepCtx &c, int ns, int M, int N, float *Cm, const float *D = nullptr, int ldd = 0,
-                 const float *bias = nullptr) {
-    sum_slices(c.s, Kf(c, k_part), ns, M, N, Cm, N, D, ldd, bias);
     c.launches += 1;
   }
 
@@ -214,7 +212,9 @@ class LstmNet : public Net {
     // total dh = (head gradient) W_o^T + the incoming dh, added up from the
     // product's slices by the pointwise kernel
     gemm_part(c, B, H, V, dl, V, K(c, k_wo), V, 0, s_dh);
-    lstm_bwd_point(c.s, B, H, Kf(c, k_part), s_dh, reinterpret_cast<const float *>(g),
+    // the incoming dh: the slices the next step's backward left in k_dxp
+    // (the last step's incoming gradient is zero)
+    lstm_bwd_point(c.s, B, H, Kf(c, k_part), s_dh, Kf(c, k_dxp), first_step ? 0 : s_dx,
                    reinterpret_cast<const float *>(g + gh),
                    reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
                    i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
@@ -222,8 +222,14 @@ class LstmNet : public Net {
                    Kf(c, k_dbp) + size_t(t_end - 1 - i) * rb * 4 * H);
     c.launches += 2;
     if (dx) {
-      gemm_part(c, B, H, 4 * H, dz, 4 * H, K(c, k_wh), 4 * H, 0, s_dx);
-      sum_parts(c, s_dx, B, H, reinterpret_cast<float *>(dx));
+      // dh_{t-1} = dz W_h^T, left as its split-K slices for the previous
+      // step's gate backward to add up (no separate sum launch); the slot's
+      // dh part is not written
+      timer.begin(c.s);
+      gemm_bf16_part(c.s, B, H, 4 * H, dz, false, 4 * H, true, K(c, k_wh), 4 * H, true, Kf(c, k_dxp),
+                     s_dx);
+      timer.end(c.s, 2.0 * B * H * 4 * H, 2.0 * (double(B) * 4 * H + 4.0 * H * H) + 4.0 * B * H);
+      c.launches += 1;
     }
     if (i == t0) {  // the chunk [t0, t0 + C) is complete: its weight gradients
       const int rows = (t_end - t0) * B;

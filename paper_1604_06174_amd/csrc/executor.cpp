@@ -40,6 +40,7 @@ struct Exec {
   char *ckpt, *arena, *gslot[2], *qbuf;
   int cur = 0;                  // gradient slot holding dL/dx of the current unit
   uint64_t fwd_count = 0, bwd_count = 0;
+  std::vector<char> ran = std::vector<char>(size_t(net.n), 0);  // unit has run a forward this step
 
   // Forward sweep over [lo, hi) starting from x (outside the arena).  Units
   // listed in `stored` write their output to the given address instead of the
@@ -74,7 +75,10 @@ struct Exec {
       }
       (void)ai;
       c.keep_saved = false;
+      c.rerun = ran[size_t(i)] != 0;
       net.fwd(i, cur_x, y, saved, c);
+      ran[size_t(i)] = 1;
+      c.rerun = false;
       c.keep_saved = true;
       ++fwd_count;
       cur_x = y;
@@ -95,7 +99,10 @@ struct Exec {
       void *s = arena + off;
       void *y = arena + off + net.a[size_t(i)];
       off += net.a[size_t(i)] + net.b[size_t(i) + 1];
+      c.rerun = ran[size_t(i)] != 0;
       net.fwd(i, cur_x, y, s, c);
+      ran[size_t(i)] = 1;
+      c.rerun = false;
       ++fwd_count;
       saved[size_t(i - lo)] = s;
       out[size_t(i - lo)] = y;

@@ -80,6 +80,10 @@ struct StepCtx {
   // false while a forward sweep runs whose saved internals are discarded
   // (they are formed again by the unit's re-run before its backward)
   bool keep_saved = true;
+  // true when this unit has already run a forward in this step (from the
+  // same input bits): per-unit reductions computed then, such as batch-norm
+  // statistics kept in operator workspace, may be reused
+  bool rerun = false;
 };
 
 class Net {

@@ -20,6 +20,10 @@
 // ReLU mask and its weight gradient's input): the "drop bn-relu" memory plan
 // the paper applies to the conv-BN-activation pipeline (section 4.2), with the
 // same bits as the stored r1.
+// The st slots of a are reserved (PEAK counts them) but the statistics live
+// in operator workspace, one pair per BN of every unit: a unit's first
+// forward of the step forms them and its re-runs, which see the same input
+// bits, reuse them instead of finalizing the same sums again.
 // The boundary b_i is the unit's input tensor (b_0 = the image batch).
 #include <algorithm>
 
@@ -42,7 +46,8 @@ class ResNetBasic : public Net {
   int hw, hb;  // head parameter indices
   // operator workspace offsets (bytes)
   uint64_t ks_loss = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0, ks_pooled = 0, ks_dlog = 0,
-           ks_lossn = 0;
+           ks_lossn = 0, ks_kst = 0;
+  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics within ks_kst
 
   explicit ResNetBasic(const ckpt_net_desc &d) {
     desc = d;
@@ -125,26 +130,35 @@ class ResNetBasic : public Net {
     ks_pooled = take(4ull * N * CL);
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
+    // every unit's batch-norm statistics (mean | rstd per BN, 256-byte
+    // aligned), kept from its first forward of the step for its re-runs
+    uint64_t kst = 0;
+    for (const Blk &k : u) {
+      kst_off.push_back(kst);
+      kst += (k.w2 >= 0 ? 2 : 1) * align256(8ull * k.cout);
+    }
+    ks_kst = take(kst);
     ks_bytes = off;
     timed_family = "k_conv3x3< and k_conv3x3s<";
   }
 
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
+  // unit i's statistics: BN 1 (or the stem's), then BN 2 at + align256(8 cout)
+  float *kst(const StepCtx &c, int32_t i) const {
+    return reinterpret_cast<float *>(c.ks + ks_kst + kst_off[size_t(i)]);
+  }
 
-  // a block's saved tensors: c1 | [r1] | c2 | st1 | st2
+  // a block's saved tensors: c1 | [r1] | c2 (then the reserved statistics slots)
   struct Saved {
-    float *c1, *r1, *c2, *st1, *st2;
+    float *c1, *r1, *c2;
   };
   Saved saved_of(const Blk &k, char *sv) const {
     const uint64_t t = align256(uint64_t(N) * k.hout * k.hout * k.cout * 4);
-    const uint64_t sb = align256(8ull * k.cout);
     const int nt = drop ? 2 : 3;
     Saved s;
     s.c1 = reinterpret_cast<float *>(sv);
     s.r1 = drop ? nullptr : reinterpret_cast<float *>(sv + t);
     s.c2 = reinterpret_cast<float *>(sv + (nt - 1) * t);
-    s.st1 = reinterpret_cast<float *>(sv + nt * t);
-    s.st2 = reinterpret_cast<float *>(sv + nt * t + sb);
     return s;
   }
 
@@ -178,31 +192,39 @@ class ResNetBasic : public Net {
     const int64_t np = int64_t(N) * k.hout * k.hout;
     if (k.w2 < 0) {  // stem
       float *cv = reinterpret_cast<float *>(sv);
-      float *st = reinterpret_cast<float *>(sv + t);
+      float *st = kst(c, i);
+      (void)t;
       conv(c, CONV_FWD, 1, CONV_EPI_STATS, x, P(c, k.w1), cv, S, S, S, S, 3, C0, nullptr, nullptr,
            0, 0, 0, S, 3, C0);
-      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st, true);
+      if (!c.rerun)
+        bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, S, S, 3, C0), C0, np, st, true);
       bn_apply(c.s, BN_RES_NONE, np, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, 0, 0, 0, y);
-      c.launches += 3;
+      c.launches += c.rerun ? 2 : 3;
       return;
     }
     const Saved sp = saved_of(k, sv);
-    float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2, *st1 = sp.st1, *st2 = sp.st2;
+    float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2;
+    // the statistics are formed by the unit's first forward of the step; a
+    // re-run (same input bits, so the same sums) reuses them and skips both
+    // finalize launches
+    float *st1 = kst(c, i), *st2 = st1 + align256(8ull * k.cout) / 4;
     const int ho = k.hout;
     conv(c, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin,
          k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
-    bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
-                    k.cout, np, st1, true);
+    if (!c.rerun)
+      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
+                      k.cout, np, st1, true);
     // the second convolution forms r1 = relu(bn1(c1)) on its input; when r1
     // is kept it also stores it (the rows each workgroup owns)
     conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout, nullptr,
          nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1), drop ? nullptr : r1);
     c.launches -= 1;
-    bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
-                    np, st2, true);
+    if (!c.rerun)
+      bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,
+                      np, st2, true);
     bn_apply(c.s, k.stride == 1 ? BN_RES_ID : BN_RES_A, np, k.cout, c2, st2, P(c, k.g2),
              P(c, k.b2), x, ho, ho, k.cin, y);
-    c.launches += 6;
+    c.launches += c.rerun ? 4 : 6;
   }
 
   void bwd(int32_t i, const void *gv, void *dxv, const void *xv, const void *yv, const void *saved,
@@ -218,7 +240,8 @@ class ResNetBasic : public Net {
     float *wpart = ksf(c, ks_wpart);
     if (k.w2 < 0) {  // stem: no input gradient
       const float *cv = reinterpret_cast<const float *>(sv);
-      const float *st = reinterpret_cast<const float *>(sv + t);
+      const float *st = kst(c, i);
+      (void)t;
       float *dc = static_cast<float *>(qv);
       bn_backward(c.s, np, C0, g, y, cv, st, P(c, k.g1), bnpart(c), sums, G(c, k.g1), G(c, k.b1), dc);
       conv3x3_wgrad(c.s, 1, x, dc, wpart, G(c, k.w1), N, S, S, S, S, 3, C0);
@@ -226,7 +249,8 @@ class ResNetBasic : public Net {
       return;
     }
     const Saved sp = saved_of(k, const_cast<char *>(sv));
-    const float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2, *st1 = sp.st1, *st2 = sp.st2;
+    const float *c1 = sp.c1, *r1 = sp.r1, *c2 = sp.c2;
+    const float *st1 = kst(c, i), *st2 = st1 + align256(8ull * k.cout) / 4;
     // r1 as read by the second convolution's backward: stored, or c1 with its
     // batch-norm + ReLU transform
     const float *x2 = drop ? c1 : r1;

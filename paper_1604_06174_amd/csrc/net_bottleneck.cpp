@@ -20,6 +20,10 @@
 //   stem   a = c | r | st                          q = dr (F) | dc
 //   block  a = c1 | r1 | c2 | r2 | c3 | [cp] | st1 | st2 | st3 | [stp]
 //          q = dc3/dc1 | dr2/dr1 (F) | dc2 | [dcp]
+// The st slots of a are reserved (PEAK counts them) but the statistics live
+// in operator workspace, per BN of every unit: a unit's first forward of the
+// step forms them and its re-runs, which see the same input bits, reuse them
+// instead of finalizing the same sums again.
 // The boundary b_i is the unit's input (b_0 = the bf16 image batch).
 #include <algorithm>
 
@@ -42,7 +46,8 @@ class Bottleneck : public Net {
   std::vector<BUnit> u;
   int hw, hb;
   uint64_t ks_wbf = 0, ks_col = 0, ks_stats = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0,
-           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0;
+           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0, ks_kst = 0;
+  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics within ks_kst
   uint64_t wpart_floats = 0;
 
   static uint64_t bf(int64_t m, int c) { return align256(uint64_t(m) * c * 2); }
@@ -166,6 +171,15 @@ class Bottleneck : public Net {
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
     ks_loss = take(4);
+    // every unit's batch-norm statistics (st1 | st2 | st3 [| stp], the stem's
+    // st), kept from its first forward of the step for its re-runs
+    uint64_t kst = 0;
+    for (const BUnit &k : u) {
+      kst_off.push_back(kst);
+      kst += k.stem ? align256(8ull * C0)
+                    : 2 * align256(8ull * k.w) + (k.proj ? 2 : 1) * align256(8ull * k.cout);
+    }
+    ks_kst = take(kst);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
   }
@@ -176,6 +190,16 @@ class Bottleneck : public Net {
   }
   double *statsbuf(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_stats); }
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
+  // unit i's statistics: st1, st2, st3, stp at 0, S, 2 S, 2 S + align256(8 cout),
+  // S = align256(8 w) (the stem's st at 0)
+  float *kst(const StepCtx &c, int32_t i, int which) const {
+    const BUnit &k = u[size_t(i)];
+    const uint64_t o = which == 0   ? 0
+                       : which == 1 ? align256(8ull * k.w)
+                       : which == 2 ? 2 * align256(8ull * k.w)
+                                    : 2 * align256(8ull * k.w) + align256(8ull * k.cout);
+    return reinterpret_cast<float *>(c.ks + ks_kst + kst_off[size_t(i)] + o);
+  }
   float *ksf(StepCtx &c, uint64_t o) const { return reinterpret_cast<float *>(c.ks + o); }
 
   // timed GEMM-family launches: 2 M N K flops; bytes = operands read once +
@@ -187,6 +211,7 @@ class Bottleneck : public Net {
   }
 
   // forward 1x1 convolution (stride 1) with BN statistics, then the stats
+  // (not on a re-run, which reuses the unit's kept statistics)
   void fwd_1x1(StepCtx &c, int64_t m, int ci, int co, const void *x, int wk, void *out, float *st) {
     tbeg(c);
     GemmX gx;
@@ -195,8 +220,10 @@ class Bottleneck : public Net {
     gemm_bf16x(c.s, int(m), co, ci, x, false, ci, true, Wb(c, wk), ci, true, nullptr, co,
                GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
     tend(c, double(m), co, ci, 2.0 * (double(m) * ci + double(ci) * co), 2.0 * double(m) * co);
-    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), co), co, m, st, false);
-    c.launches += 1;
+    if (!c.rerun) {
+      bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), co), co, m, st, false);
+      c.launches += 1;
+    }
   }
 
   void fwd_conv(StepCtx &c, const ConvGeo &g, const void *x, int wk, void *out, float *st) {
@@ -206,8 +233,10 @@ class Bottleneck : public Net {
     conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, statsbuf(c));
     tend(c, double(m), g.Co, kd, 2.0 * (double(g.N) * g.H * g.W * g.Ci + kd * g.Co),
          2.0 * double(m) * g.Co);
-    bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), g.Co), g.Co, m, st, false);
-    c.launches += 1;
+    if (!c.rerun) {
+      bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), g.Co), g.Co, m, st, false);
+      c.launches += 1;
+    }
   }
 
   // dW [M, Nn] = sum over k of A(m, k) B(k, n), A = dY^T ([Kd, M] bf16), B = X ([Kd, Nn] bf16)
@@ -247,7 +276,7 @@ class Bottleneck : public Net {
     if (k.stem) {
       const int64_t m = int64_t(N) * side * side;
       char *cv = sv, *r = sv + bf(m, C0);
-      float *st = reinterpret_cast<float *>(sv + 2 * bf(m, C0));
+      float *st = kst(c, i, 0);
       im2col7(c.s, N, S, S, side, side, xv, c.ks + ks_col);
       tbeg(c);
       GemmX gx;
@@ -256,21 +285,17 @@ class Bottleneck : public Net {
       gemm_bf16x(c.s, int(m), C0, 147, c.ks + ks_col, false, 147, true, Wb(c, k.W1), 147, true,
                  nullptr, C0, GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
       tend(c, double(m), C0, 147, 2.0 * (double(m) * 147 + 147.0 * C0), 2.0 * double(m) * C0);
-      bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), C0), C0, m, st, false);
+      if (!c.rerun) bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), C0), C0, m, st, false);
       bnb_apply(c.s, BNB_RES_NONE, m, C0, cv, st, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
                 nullptr, nullptr, r);
       maxpool_fwd(c.s, N, side, side, C0, k.hout, k.hout, r, yv);
-      c.launches += 4;
+      c.launches += c.rerun ? 3 : 4;
       return;
     }
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
     char *c1 = sv, *r1 = c1 + bf(mi, k.w), *c2 = r1 + bf(mi, k.w), *r2 = c2 + bf(mo, k.w);
     char *c3 = r2 + bf(mo, k.w), *cp = c3 + bf(mo, k.cout);
-    char *stb = cp + (k.proj ? bf(mo, k.cout) : 0);
-    float *st1 = reinterpret_cast<float *>(stb);
-    float *st2 = reinterpret_cast<float *>(stb + align256(8ull * k.w));
-    float *st3 = reinterpret_cast<float *>(stb + 2 * align256(8ull * k.w));
-    float *stp = reinterpret_cast<float *>(stb + 2 * align256(8ull * k.w) + align256(8ull * k.cout));
+    float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
     fwd_1x1(c, mi, k.cin, k.w, xv, k.W1, c1, st1);
     bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
               nullptr, nullptr, r1);
@@ -304,7 +329,7 @@ class Bottleneck : public Net {
     if (k.stem) {  // no input gradient
       const int64_t m = int64_t(N) * side * side;
       const char *cv = sv, *r = sv + bf(m, C0);
-      const float *st = reinterpret_cast<const float *>(sv + 2 * bf(m, C0));
+      const float *st = kst(c, i, 0);
       float *dr = reinterpret_cast<float *>(qb);
       char *dc = qb + f32(m, C0);
       maxpool_bwd(c.s, N, side, side, C0, k.hout, k.hout, g, r, yv, dr);
@@ -317,12 +342,7 @@ class Bottleneck : public Net {
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
     const char *c1 = sv, *r1 = c1 + bf(mi, k.w), *c2 = r1 + bf(mi, k.w), *r2 = c2 + bf(mo, k.w);
     const char *c3 = r2 + bf(mo, k.w), *cp = c3 + bf(mo, k.cout);
-    const char *stb = cp + (k.proj ? bf(mo, k.cout) : 0);
-    const float *st1 = reinterpret_cast<const float *>(stb);
-    const float *st2 = reinterpret_cast<const float *>(stb + align256(8ull * k.w));
-    const float *st3 = reinterpret_cast<const float *>(stb + 2 * align256(8ull * k.w));
-    const float *stp =
-        reinterpret_cast<const float *>(stb + 2 * align256(8ull * k.w) + align256(8ull * k.cout));
+    const float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
     char *qA = qb;                                         // dc3, then dc1
     float *qB = reinterpret_cast<float *>(qA + std::max(bf(mo, k.cout), bf(mi, k.w)));  // dr2, dr1
     char *qC = reinterpret_cast<char *>(qB) + f32(mi, k.w);  // dc2

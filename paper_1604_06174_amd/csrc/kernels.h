@@ -222,6 +222,8 @@ void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void 
 // dst[c * ld + r] = bf16(src[r * C + c]) (ld = R when 0)
 void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst, int ld = 0);
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst);
+// dst (bf16, row stride ld) = src [R][C] fp32
+void cvt_bf16_rows(hipStream_t s, int R, int C, const float *src, void *dst, int ld);
 // Split-K inputs: zpart / lpart / dhpart hold ns partial slices of the
 // product, added in slice order before the bias (or the incoming dh), exactly
 // as sum_slices would.

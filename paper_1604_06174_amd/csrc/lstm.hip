@@ -65,6 +65,14 @@ __global__ __launch_bounds__(256) void k_cvt_bf16(int64_t n, const float *__rest
     dst[e] = (__bf16)src[e];
 }
 
+// dst[r * ld + c] = bf16(src[r * C + c]) for src [R][C] fp32
+__global__ __launch_bounds__(256) void k_cvt_bf16_rows(int R, int C, const float *__restrict__ src,
+                                                       __bf16 *__restrict__ dst, int ld) {
+  const int64_t n = int64_t(R) * C;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < n; e += int64_t(gridDim.x) * 256)
+    dst[(e / C) * ld + e % C] = (__bf16)src[e];
+}
+
 // one thread per (b, j); z = sum of the ns partial slices [B, 4H] + bias
 __global__ __launch_bounds__(256) void k_lstm_fwd_point(int B, int H, const float *__restrict__ zpart,
                                                         int ns, const float *__restrict__ bias,
@@ -296,6 +304,11 @@ inline int grid_for(int64_t n) {
 void transpose_bf16(hipStream_t s, int R, int C, const float *src, void *dst, int ld) {
   hipLaunchKernelGGL(k_transpose_bf16, dim3((C + 31) / 32, (R + 31) / 32), dim3(256), 0, s, R, C,
                      src, static_cast<__bf16 *>(dst), ld > 0 ? ld : R);
+}
+
+void cvt_bf16_rows(hipStream_t s, int R, int C, const float *src, void *dst, int ld) {
+  hipLaunchKernelGGL(k_cvt_bf16_rows, dim3(grid_for(int64_t(R) * C)), dim3(256), 0, s, R, C, src,
+                     static_cast<__bf16 *>(dst), ld);
 }
 
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst) {

@@ -21,9 +21,9 @@
 //
 // Static layout: boundary b = h (bf16 [B,H]) | c (fp32 [B,H]); saved a = gates
 // (fp32 [B,4H]) | softmax gradient (fp32 [B,V]); scratch q = total dh (fp32
-// [B,H]); gradient slot = dh | dc (fp32; dh_{t-1} travels instead as the
-// split-K slices of dz W_h^T in operator workspace, added up by the previous
-// step's gate backward); extra gradient buffers = the chunk's
+// [B,H]); gradient slot = dh | dc (fp32; only dc is written: the previous
+// step's backward forms dz_t W_h^T itself, in one product with its own head
+// gradient); extra gradient buffers = the chunk's
 // dz (bf16 [C*B,4H]), head gradient (bf16 [C*B,V]), h_{t-1} and h_t copies
 // (bf16 [C*B,H]).
 #include <algorithm>
@@ -41,11 +41,12 @@ class LstmNet : public Net {
   uint64_t hb, cb;  // boundary parts
   uint64_t ga, da;  // saved parts: gates, dlog
   // operator workspace offsets
-  uint64_t k_wcat, k_wh, k_wot, k_wo, k_dbp, k_lossrows, k_loss, k_part, k_rstat, k_dxp;
+  uint64_t k_wcat, k_wot, k_wob, k_dbp, k_lossrows, k_loss, k_part, k_rstat;
   bool zcat;  // z = [x_t | h_{t-1}] [W_x; W_h] as one product (same slices as the two)
-  // split-K counts: input and recurrent parts of z, dh (head), dh_{t-1}; the
+  // split-K counts: input and recurrent parts of z, the last step's dh (head
+  // only), every other step's dh (head and recurrence in one product); the
   // logits are one product (their softmax statistics come from its epilogue)
-  int s_x, s_h, s_dh, s_dx;
+  int s_x, s_h, s_dh, s_dm;
   // extra gradient buffer offsets
   uint64_t x_dz, x_dl, x_hp, x_hc;
 
@@ -84,9 +85,9 @@ class LstmNet : public Net {
     grad_extra = off;
     off = 0;
     k_wcat = take(uint64_t(E + H) * 4 * H * 2);  // [4H][E + H]: W_x^T | W_h^T
-    k_wh = take(uint64_t(H) * 4 * H * 2);
+
     k_wot = take(uint64_t(H) * V * 2);
-    k_wo = take(uint64_t(H) * V * 2);
+    k_wob = take(uint64_t(H) * (V + 4 * H) * 2);  // [H][V + 4H]: W_o | W_h
     // bias-gradient column sums of one chunk: per step, one [4H] record per
     // block of 4 batch rows
     k_dbp = take(uint64_t(C) * ((B + 3) / 4) * 4 * H * 4);
@@ -103,11 +104,10 @@ class LstmNet : public Net {
     zcat = E == H && s_x == s_h && gemm_bf16_kper(E, s_x) * s_x == E &&
            gemm_bf16_kper(E + H, s_x + s_h) == gemm_bf16_kper(E, s_x) && E % 8 == 0;
     s_dh = gemm_bf16_splits(B, H, V);
-    s_dx = gemm_bf16_splits(B, H, 4 * H);
+    s_dm = gemm_bf16_splits(B, H, V + 4 * H);
     const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(B) * V,
-                                    uint64_t(s_dh) * B * H});
+                                    uint64_t(std::max(s_dh, s_dm)) * B * H});
     k_part = take(part * 4);
-    k_dxp = take(uint64_t(s_dx) * B * H * 4);
     k_rstat = take(uint64_t(B) * gemm_bf16_col_blocks(B, V) * 2 * 4);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
@@ -141,9 +141,9 @@ class LstmNet : public Net {
     // bf16 copies of the weights in the layouts the GEMMs read (k contiguous)
     transpose_bf16(c.s, E, 4 * H, P(c, pWx), K(c, k_wcat), E + H);              // [4H][0, E)
     transpose_bf16(c.s, H, 4 * H, P(c, pWh), K(c, k_wcat) + size_t(E) * 2, E + H);  // [4H][E, E + H)
-    cvt_bf16(c.s, int64_t(H) * 4 * H, P(c, pWh), K(c, k_wh));  // [H][4H]
+    cvt_bf16_rows(c.s, H, 4 * H, P(c, pWh), K(c, k_wob) + size_t(V) * 2, V + 4 * H);  // [H][V, V + 4H)
     transpose_bf16(c.s, H, V, P(c, pWo), K(c, k_wot));        // [V][H]
-    cvt_bf16(c.s, int64_t(H) * V, P(c, pWo), K(c, k_wo));      // [H][V]
+    cvt_bf16_rows(c.s, H, V, P(c, pWo), K(c, k_wob), V + 4 * H);                    // [H][0, V)
     c.launches += 5;
   }
 
@@ -209,28 +209,32 @@ class LstmNet : public Net {
     char *hc = X(c, x_hc) + row * H * 2;
     head_bwd_prep(c.s, B, V, reinterpret_cast<const float *>(sv + ga), dl, G(c, pbo), first_step);
     (void)qv;
-    // total dh = (head gradient) W_o^T + the incoming dh, added up from the
-    // product's slices by the pointwise kernel
-    gemm_part(c, B, H, V, dl, V, K(c, k_wo), V, 0, s_dh);
-    // the incoming dh: the slices the next step's backward left in k_dxp
-    // (the last step's incoming gradient is zero)
-    lstm_bwd_point(c.s, B, H, Kf(c, k_part), s_dh, Kf(c, k_dxp), first_step ? 0 : s_dx,
+    // total dh = dl_t W_o^T + dz_{t+1} W_h^T (the incoming dh; none at the
+    // last step): one split-K product over [dl_t | dz_{t+1}] and [W_o | W_h],
+    // its slices added up by the gate backward.  dz_{t+1} is the next step's
+    // row of the chunk buffer (row 0 of it when t + 1 began a chunk; nothing
+    // has written that row since).
+    int ns = s_dh;
+    if (first_step) {
+      gemm_part(c, B, H, V, dl, V, K(c, k_wob), V + 4 * H, 0, s_dh);
+    } else {
+      const int t1 = i + 1;
+      const char *dzn = X(c, x_dz) + size_t(t1 - (t1 / C) * C) * B * 4 * H * 2;
+      timer.begin(c.s);
+      gemm_bf16_part_cat(c.s, B, H, V, dl, V, 4 * H, dzn, 4 * H, K(c, k_wob), V + 4 * H,
+                         Kf(c, k_part), s_dm);
+      timer.end(c.s, 2.0 * B * H * (V + 4.0 * H),
+                2.0 * (double(B) * (V + 4 * H) + double(V + 4 * H) * H) + 4.0 * B * H);
+      c.launches += 1;
+      ns = s_dm;
+    }
+    lstm_bwd_point(c.s, B, H, Kf(c, k_part), ns, nullptr, 0,
                    reinterpret_cast<const float *>(g + gh),
                    reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
                    i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
                    dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc,
                    Kf(c, k_dbp) + size_t(t_end - 1 - i) * rb * 4 * H);
     c.launches += 2;
-    if (dx) {
-      // dh_{t-1} = dz W_h^T, left as its split-K slices for the previous
-      // step's gate backward to add up (no separate sum launch); the slot's
-      // dh part is not written
-      timer.begin(c.s);
-      gemm_bf16_part(c.s, B, H, 4 * H, dz, false, 4 * H, true, K(c, k_wh), 4 * H, true, Kf(c, k_dxp),
-                     s_dx);
-      timer.end(c.s, 2.0 * B * H * 4 * H, 2.0 * (double(B) * 4 * H + 4.0 * H * H) + 4.0 * B * H);
-      c.launches += 1;
-    }
     if (i == t0) {  // the chunk [t0, t0 + C) is complete: its weight gradients
       const int rows = (t_end - t0) * B;
       const bool first_chunk = t0 + C >= n;

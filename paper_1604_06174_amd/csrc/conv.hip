@@ -436,7 +436,7 @@ __global__ __launch_bounds__(256) void k_conv3x3s(ConvArgs a) {
   // shortcut's input and mask) fetched for all of the lane's outputs before
   // any is used; outside elements read the base and are never stored
   float e0[PSW][4][NS], e1[PSW][4][NS];
-  if constexpr (EPI != CONV_EPI_STATS) {
+  if constexpr (EPI != CONV_EPI_STATS && EPI != CONV_EPI_STORE) {
 #pragma unroll
     for (int s = 0; s < PSW; ++s)
 #pragma unroll
@@ -555,10 +555,16 @@ bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool 
 bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool launch, SpecUse *u) {
   constexpr int F = CONV_FWD, D = CONV_DGRAD;
   constexpr int STATS = CONV_EPI_STATS, MASK = CONV_EPI_MASK, SC1 = CONV_EPI_SC1, SC2 = CONV_EPI_SC2,
-                MST = CONV_EPI_MASKSTATS;
+                MST = CONV_EPI_MASKSTATS, STORE = CONV_EPI_STORE;
   // rows per workgroup and output channels per workgroup as measured best on
-  // MI355X for these shapes
+  // MI355X for these shapes (the forward without statistics: a re-run that
+  // reuses them)
   return spec_try<16, 16, 32, 1, F, STATS, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 16, 32, 1, F, STORE, 4, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<16, 32, 16, 2, F, STORE, 4, 32>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 32, 16, 1, F, STORE, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<32, 64, 8, 2, F, STORE, 8, 16>(a, mode, s, epi, st, launch, u) ||
+         spec_try<64, 64, 8, 1, F, STORE, 8, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<16, 32, 16, 2, F, STATS, 4, 32>(a, mode, s, epi, st, launch, u) ||
          spec_try<32, 32, 16, 1, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||
          spec_try<32, 64, 8, 2, F, STATS, 8, 16>(a, mode, s, epi, st, launch, u) ||

@@ -209,15 +209,16 @@ class ResNetBasic : public Net {
     // finalize launches
     float *st1 = kst(c, i), *st2 = st1 + align256(8ull * k.cout) / 4;
     const int ho = k.hout;
-    conv(c, CONV_FWD, k.stride, CONV_EPI_STATS, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin,
-         k.cout, nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
+    const int epi = c.rerun ? CONV_EPI_STORE : CONV_EPI_STATS;  // no sums on a re-run
+    conv(c, CONV_FWD, k.stride, epi, x, P(c, k.w1), c1, ho, ho, k.hin, k.hin, k.cin, k.cout,
+         nullptr, nullptr, 0, 0, 0, ho, k.cin, k.cout);
     if (!c.rerun)
       bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, k.stride, N, ho, ho, k.cin, k.cout),
                       k.cout, np, st1, true);
     // the second convolution forms r1 = relu(bn1(c1)) on its input; when r1
     // is kept it also stores it (the rows each workgroup owns)
-    conv(c, CONV_FWD, 1, CONV_EPI_STATS, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout, nullptr,
-         nullptr, 0, 0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1), drop ? nullptr : r1);
+    conv(c, CONV_FWD, 1, epi, c1, P(c, k.w2), c2, ho, ho, ho, ho, k.cout, k.cout, nullptr, nullptr, 0,
+         0, 0, ho, k.cout, k.cout, st1, P(c, k.g1), P(c, k.b1), drop ? nullptr : r1);
     c.launches -= 1;
     if (!c.rerun)
       bn_finalize_fwd(c.s, bnpart(c), conv3x3_blocks(CONV_FWD, 1, N, ho, ho, k.cout, k.cout), k.cout,

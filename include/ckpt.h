@@ -39,7 +39,7 @@ extern "C" {
 #define CKPT_E_WORKSPACE   (-2)  /* workspace smaller than net_workspace_bytes  */
 #define CKPT_E_MISMATCH    (-3)  /* plan built for a different unit count        */
 #define CKPT_E_HIP         (-4)  /* a HIP runtime call failed (message has text) */
-#define CKPT_E_UNSUPPORTED (-5)  /* valid request this build does not handle     */
+#define CKPT_E_UNSUPPORTED (-5)  /* valid request the library does not handle    */
 
 /* ---- plan modes (section 4) --------------------------------------------- */
 #define CKPT_NONE      0  /* one segment, activations of the first forward kept     */

@@ -96,7 +96,18 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
   __shared__ __attribute__((aligned(16))) float smem[2 * (BM + BN) * LD];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // Workgroups reach the eight XCDs (one L2 each) in turn; the linear id is
+  // remapped so that each XCD takes a contiguous run of tiles, m fastest: an
+  // XCD then reads a few column tiles of B (plus A) instead of all of B.
+  int tm, tn;
+  {
+    const int G = gridDim.x * gridDim.y, id = blockIdx.x + gridDim.x * blockIdx.y;
+    const int q8 = G / 8, r8 = G % 8, x8 = id % 8;
+    const int L = x8 * q8 + (x8 < r8 ? x8 : r8) + id / 8;
+    tm = L % gridDim.y;
+    tn = L / gridDim.y;
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
   const int kw = KS == 1 ? 0 : wave;                         // k quarter of this wave
   const int wm = KS == 1 ? (wave >> 1) * 32 : 0, wn = KS == 1 ? (wave & 1) * 32 : 0;
 

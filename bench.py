@@ -13,8 +13,8 @@ already resident in HBM.
 Printed (one JSON line): samples/s of the checkpointed step, its peak
 activation bytes (exact, from the static layout), the recompute overhead
 (step time / the same kernels without checkpointing), the dominant kernel's
-roofline position from HIP events recorded around its launches in a second
-timed pass (against MFMA peak when the family's arithmetic intensity is at or
+roofline position from HIP events that its launches stamp with the kernels'
+own start and end, in a second timed pass (against MFMA peak when the family's arithmetic intensity is at or
 above the ridge point, else against HBM bandwidth; both fractions are given),
 and the CPU oracle's checkpointed step on a bounded sample.
 """
@@ -216,7 +216,8 @@ def main():
                     "ms_per_step_no_ckpt": round(timed(lambda: graphs["none"].launch(s)), 4)}
     loss = float(step.loss_dev.item())
 
-    # second timed pass: HIP events around every launch of the dominant kernel
+    # second timed pass: every launch of the dominant kernel family stamps an
+    # event pair with its own start and end
     step.net.timing_enable(True)
     run(plan, args.steps)
     torch.cuda.synchronize()

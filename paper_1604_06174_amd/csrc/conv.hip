@@ -26,6 +26,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace ckpt {
 
@@ -546,7 +547,7 @@ bool spec_try(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, bool 
   if (u) *u = {RB, BN};
   if (launch) {
     dim3 grid(a.N * ((a.H + RB - 1) / RB), (J + BN - 1) / BN);
-    hipLaunchKernelGGL((k_conv3x3s<C, J, W, S, MODE, EPI, RB, BN>), grid, dim3(256), 0, st, a);
+    launch_timed((k_conv3x3s<C, J, W, S, MODE, EPI, RB, BN>), grid, dim3(256), 0, st, a);
   }
   return true;
 }
@@ -1053,12 +1054,12 @@ size_t wgrad_lds(int J) {
 template <int PSW, int NSUB, int MODE, int S>
 void launch_conv(const ConvArgs &a, int epi, size_t lds, dim3 grid, hipStream_t st) {
   switch (epi) {
-    case CONV_EPI_STATS: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STATS>), grid, dim3(256), lds, st, a); break;
-    case CONV_EPI_MASK: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASK>), grid, dim3(256), lds, st, a); break;
-    case CONV_EPI_MASKSTATS: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASKSTATS>), grid, dim3(256), lds, st, a); break;
-    case CONV_EPI_SC1: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC1>), grid, dim3(256), lds, st, a); break;
-    case CONV_EPI_SC2: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC2>), grid, dim3(256), lds, st, a); break;
-    default: hipLaunchKernelGGL((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STORE>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_STATS: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STATS>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_MASK: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASK>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_MASKSTATS: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_MASKSTATS>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_SC1: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC1>), grid, dim3(256), lds, st, a); break;
+    case CONV_EPI_SC2: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_SC2>), grid, dim3(256), lds, st, a); break;
+    default: launch_timed((k_conv3x3<PSW, NSUB, MODE, S, CONV_EPI_STORE>), grid, dim3(256), lds, st, a); break;
   }
 }
 

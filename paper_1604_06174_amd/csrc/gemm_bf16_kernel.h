@@ -47,6 +47,7 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "launch.h"
 
 namespace ckpt {
 
@@ -706,33 +707,33 @@ template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA,
 void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
   dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
   if (epi == GEMM_EPI_ADD) {
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+    launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
     return;
   }
   if constexpr (std::is_same<TA, __bf16>::value) {
     if (epi == GEMM_EPI_ADDMASK) {
-      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
       return;
     }
     if (epi == GEMM_EPI_BF16STATS) {
-      hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
       return;
     }
     // instantiated for the operand forms the host wrappers accept only
     if constexpr (AK && !BK && SAFE) {
       if (epi == GEMM_EPI_BNBWD) {
-        hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
         return;
       }
     }
     if constexpr (AK && BK && SAFE && GA == G_DENSE && GB == G_DENSE) {
       if (epi == GEMM_EPI_ROWSOFTMAX) {
-        hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
         return;
       }
     }
   }
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+  launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
 }
 
 template <bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>

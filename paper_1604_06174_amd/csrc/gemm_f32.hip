@@ -29,6 +29,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace ckpt {
 
@@ -262,9 +263,9 @@ void launch(const GemmArgs &a, bool vec, hipStream_t s) {
   constexpr int T = KS == 1 ? 64 : 32;
   dim3 grid((a.N + T - 1) / T, (a.M + T - 1) / T);
   if (vec)
-    hipLaunchKernelGGL((k_gemm_f32<KS, TA, TB, EPI, true>), grid, dim3(256), 0, s, a);
+    launch_timed((k_gemm_f32<KS, TA, TB, EPI, true>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((k_gemm_f32<KS, TA, TB, EPI, false>), grid, dim3(256), 0, s, a);
+    launch_timed((k_gemm_f32<KS, TA, TB, EPI, false>), grid, dim3(256), 0, s, a);
 }
 
 template <int KS>

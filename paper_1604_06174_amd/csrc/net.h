@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "common.h"
+#include "launch.h"
 
 namespace ckpt {
 
@@ -22,7 +23,10 @@ struct KernelTimer {
   uint64_t launches = 0;
   double ms = 0, flops = 0, bytes = 0;
 
-  void begin(hipStream_t s) {
+  // begin arms an event pair for the next launch of the timed family (see
+  // launch.h: the launch itself stamps the pair with the kernel's start and
+  // end); end books the launch's algorithmic work when one took the pair
+  void begin(hipStream_t) {
     if (!enabled) return;
     if (used == pool.size()) {
       hipEvent_t a, b;
@@ -30,14 +34,21 @@ struct KernelTimer {
       if (hipEventCreate(&b) != hipSuccess) fail(CKPT_E_HIP, "hipEventCreate failed");
       pool.emplace_back(a, b);
     }
-    (void)hipEventRecord(pool[used].first, s);
+    TimedLaunch &t = timed_launch();
+    t.start = pool[used].first;
+    t.stop = pool[used].second;
+    t.armed = true;
+    t.taken = false;
   }
-  void end(hipStream_t s, double f, double b) {
+  void end(hipStream_t, double f, double b) {
     if (!enabled) return;
-    (void)hipEventRecord(pool[used].second, s);
-    fl.push_back(f);
-    by.push_back(b);
-    ++used;
+    TimedLaunch &t = timed_launch();
+    if (t.taken) {
+      fl.push_back(f);
+      by.push_back(b);
+      ++used;
+    }
+    t.armed = t.taken = false;
   }
   void harvest() {
     for (size_t k = 0; k < used; ++k) {

@@ -238,12 +238,11 @@ void softmax_ce_tiles(hipStream_t s, int rows, int V, const float *logits, int n
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first);
 // dbp receives ceil(B/4) records [4H] of bias-gradient column sums (one per
 // block of 4 batch rows); db_chunk adds a run of such records into db.
-// The incoming dh is given as ns_in split-K slices [B, H] (added in order;
-// ns_in = 0: zero).
-void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dhin_part,
-                    int ns_in, const float *dc_in, const float *gates, const float *c_t,
-                    const float *c_prev, const void *h_prev, const void *h_t, void *dz, float *dc_prev,
-                    void *hp_copy, void *hc_copy, float *dbp);
+// dh = the ns split-K slices [B, H] of the product that forms it, in order.
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dc_in,
+                    const float *gates, const float *c_t, const float *c_prev, const void *h_prev,
+                    const void *h_t, void *dz, float *dc_prev, void *hp_copy, void *hc_copy,
+                    float *dbp);
 void db_chunk(hipStream_t s, int N, int nrec, const float *rec, float *db, bool first);
 void loss_reduce(hipStream_t s, int64_t rows, const float *v, float scale, float *loss);
 void fill_f32(hipStream_t s, int64_t n, float *p, float v);

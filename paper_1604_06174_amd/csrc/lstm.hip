@@ -190,14 +190,12 @@ __global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float
 
 // Gate backward, one thread per (b, j): workgroup = 64 hidden units x 4
 // batch rows (blockIdx.y = row block).  dh = the ns partial slices [B, H] of
-// the head gradient's product, in order, + the incoming dh, itself the sum
-// in order of the ns_in slices [B, H] of the next step's dz W_h^T product
-// (none for the last step).
+// the product that forms it (head gradient and, but for the last step, the
+// next step's dz W_h^T), added in order.
 // The workgroup's bias-gradient column sums over its 4 rows, ((r0 + r1) + r2)
 // + r3, go to dbp[blockIdx.y][4H]; k_db_chunk adds them up.
 __global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const float *__restrict__ dhpart,
-                                                        int ns, const float *__restrict__ dhin_part,
-                                                        int ns_in, const float *__restrict__ dc_in,
+                                                        int ns, const float *__restrict__ dc_in,
                                                         const float *__restrict__ gates,
                                                         const float *__restrict__ c_t,
                                                         const float *__restrict__ c_prev,
@@ -217,9 +215,7 @@ __global__ __launch_bounds__(256) void k_lstm_bwd_point(int B, int H, const floa
     const size_t oe[1] = {e};
     float dh[1];
     slices_sum<1, 8>(dhpart, ns, size_t(B) * H, oe, dh);
-    float din[1] = {0.f};
-    if (ns_in > 0) slices_sum<1, 8>(dhin_part, ns_in, size_t(B) * H, oe, din);
-    const float dhv = dh[0] + din[0];
+    const float dhv = dh[0];
     const float *gr = gates + size_t(b) * 4 * H;
     const float ig = gr[j], fg = gr[H + j], gg = gr[2 * H + j], og = gr[3 * H + j];
     const float tc = tanhf(c_t[e]);
@@ -335,12 +331,12 @@ void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, 
                      static_cast<__bf16 *>(dl_bf), db_o, first ? 1 : 0);
 }
 
-void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dhin_part,
-                    int ns_in, const float *dc_in, const float *gates, const float *c_t,
-                    const float *c_prev, const void *h_prev, const void *h_t, void *dz, float *dc_prev,
-                    void *hp_copy, void *hc_copy, float *dbp) {
+void lstm_bwd_point(hipStream_t s, int B, int H, const float *dhpart, int ns, const float *dc_in,
+                    const float *gates, const float *c_t, const float *c_prev, const void *h_prev,
+                    const void *h_t, void *dz, float *dc_prev, void *hp_copy, void *hc_copy,
+                    float *dbp) {
   hipLaunchKernelGGL(k_lstm_bwd_point, dim3((H + 63) / 64, (B + 3) / 4), dim3(256), 0, s, B, H, dhpart,
-                     ns, dhin_part, ns_in, dc_in, gates, c_t, c_prev, static_cast<const __bf16 *>(h_prev),
+                     ns, dc_in, gates, c_t, c_prev, static_cast<const __bf16 *>(h_prev),
                      static_cast<const __bf16 *>(h_t), static_cast<__bf16 *>(dz), dc_prev,
                      static_cast<__bf16 *>(hp_copy), static_cast<__bf16 *>(hc_copy), dbp);
 }

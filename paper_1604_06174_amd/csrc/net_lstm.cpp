@@ -228,8 +228,7 @@ class LstmNet : public Net {
       c.launches += 1;
       ns = s_dm;
     }
-    lstm_bwd_point(c.s, B, H, Kf(c, k_part), ns, nullptr, 0,
-                   reinterpret_cast<const float *>(g + gh),
+    lstm_bwd_point(c.s, B, H, Kf(c, k_part), ns, reinterpret_cast<const float *>(g + gh),
                    reinterpret_cast<const float *>(sv), reinterpret_cast<const float *>(y + hb),
                    i > 0 ? reinterpret_cast<const float *>(x + hb) : nullptr, i > 0 ? x : nullptr, y, dz,
                    dx ? reinterpret_cast<float *>(dx + gh) : nullptr, hp, hc,

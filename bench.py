@@ -1,22 +1,27 @@
 #!/usr/bin/env python3
 """Benchmark of the checkpointed training step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload cifar110]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload resnet1000]
 
-Default workload: the CIFAR-shaped 110-layer residual CNN (stem + 3 x 18 basic
-blocks, batch 128, fp32) with the sqrt(n) schedule (section 4.3).  A step is
-one whole checkpointed train step: forward keeping only segment boundaries,
-loss head, and for every segment in reverse its forward re-run followed by its
-backward, producing every gradient.  Inputs are seeded synthetic tensors
-already resident in HBM.
+Default workload: the ImageNet-shaped ~1000-layer bottleneck ResNet of section
+5.2 (stem + 333 bottleneck blocks split 32/64/205/32, 224x224 input, batch 32,
+bf16 activations, fp32 batch-norm statistics) with the budget-driven greedy
+plan of Alg. 3 at a budget of 10% of the full-storage activation bytes.  A
+step is one whole checkpointed train step: forward keeping only segment
+boundaries, loss head, and for every segment in reverse its forward re-run
+followed by its backward, producing every gradient.  Inputs are seeded
+synthetic tensors already resident in HBM.
 
-Printed (one JSON line): samples/s of the checkpointed step, its peak
-activation bytes (exact, from the static layout), the recompute overhead
-(step time / the same kernels without checkpointing), the dominant kernel's
-roofline position from HIP events that its launches stamp with the kernels'
-own start and end, in a second timed pass (against MFMA peak when the family's arithmetic intensity is at or
-above the ridge point, else against HBM bandwidth; both fractions are given),
-and the CPU oracle's checkpointed step on a bounded sample.
+Printed (one JSON line): samples/s of the checkpointed step (mean over the
+timed steps; the median of the per-step times is given too), its peak
+activation bytes (exact, from the static layout) next to the bytes the step
+measurably wrote in each workspace region, the recompute overhead (step time /
+the same kernels without checkpointing), the dominant kernel's roofline
+position from HIP events that its launches stamp with the kernels' own start
+and end, in a second timed pass (against MFMA peak when the family's
+arithmetic intensity is at or above the ridge point, else against HBM
+bandwidth; both fractions are given), and the CPU oracle's full-storage step
+(float32 NumPy) on a bounded sample.
 """
 from __future__ import annotations
 
@@ -70,13 +75,25 @@ def _traffic(workload):
     return rec
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def _cpu_baseline(cfg, sample_batch, d_full):
-    """The oracle's own checkpointed executor (Alg. 1 with the same plan) on a
-    smaller batch of the same network (the same parameters, the first samples
-    of the batch); samples/s = sample batch / wall time."""
+    """The oracle's plain full-storage training step (float32 NumPy, no bf16
+    rounding) of the same network on a smaller batch (the same parameters, the
+    first samples of the batch; for the LSTM a prefix of the time steps);
+    samples/s = sample / wall time, scaled to the full step."""
     import numpy as np
     import synth
-    from oracle import nets, planner as PL, schedule as SCH, sizes as SZ
+    from oracle import nets, units as U
     try:
         from threadpoolctl import threadpool_info
         threads = max([t.get("num_threads", 1) for t in threadpool_info()
@@ -97,30 +114,55 @@ def _cpu_baseline(cfg, sample_batch, d_full):
         n_samples = sample_batch
     structure = synth.structure(c)
     inp, tgt = d_full["input"][:sample_batch], d_full["target"][:sample_batch]
-    chain = nets.Chain(structure, d_full["params"])
-    lb, cb = SZ.layer_and_cut_bytes(structure)
-    n = structure.n
-    pname = cfg.get("plan", "sqrt")
-    if pname == "search":
-        b, a, q = SZ.tables(structure)
-        slot, extra = SZ.grad_layout(structure, cfg.get("grad_chunk"))
-        oplan = PL.search(n, lb, cb, b, a, q, slot, extra)[0]
-    else:
-        mode = {"sqrt": PL.SQRT, "greedy": PL.GREEDY, "recursive": PL.RECURSIVE}[pname]
-        budget = int(cfg.get("stride", 0)) if mode == PL.SQRT else int(sum(lb) * cfg.get("budget_frac", 0.1))
-        if mode == PL.SQRT:
-            budget = min(budget, n) if budget else 0
-        oplan = None if mode == PL.RECURSIVE else PL.plan(n, lb, cb, budget, mode)
+    chain = nets.Chain(structure, d_full["params"], U.Prec(np.float32, False))
     t0 = time.perf_counter()
-    if oplan is None:
-        SCH.recursive_step(chain, inp, tgt, int(cfg.get("fanout", 1)))
-    else:
-        SCH.segment_step(chain, inp, tgt, oplan)
+    nets.full_storage_step(chain, inp, tgt)
     dt = time.perf_counter() - t0
     return {"value": n_samples * scale / dt, "unit": "samples/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"one float64 NumPy checkpointed step (same plan) of the same network on "
+            "kind": "oracle", "dtype": "f32", "cpu_model": _cpu_model(),
+            "sample": f"one float32 NumPy full-storage step of the same network on "
                       f"{what}, scaled to the full step; {dt:.1f} s wall"}
+
+
+def _touched(ws, lo, hi, chunk=1 << 20):
+    """Bytes from `lo` up to the last byte in [lo, hi) that differs from the
+    0xFF fill (0 when none does); every value the step stores is finite, so an
+    all-ones bf16 / fp32 word marks memory it never wrote."""
+    import torch
+    if hi <= lo:
+        return 0
+    v = ws[lo:hi]
+    n = v.numel()
+    full = n // chunk
+    last = -1
+    if n > full * chunk:
+        tail = (v[full * chunk:] != 255).nonzero()
+        if tail.numel():
+            last = full * chunk + int(tail[-1])
+    if last < 0 and full:
+        hit = (v[:full * chunk].view(full, chunk) != 255).any(dim=1).nonzero()
+        if hit.numel():
+            c = int(hit[-1])
+            last = c * chunk + int((v[c * chunk:(c + 1) * chunk] != 255).nonzero()[-1])
+    return last + 1
+
+
+def _measured_regions(step, plan, acc, stream):
+    """One more step on a workspace filled with 0xFF: per region (kept
+    boundaries, re-run arena, gradient buffers), the extent the step wrote."""
+    import torch
+    al = lambda x: (x + 255) // 256 * 256
+    ws = step.workspace(plan)
+    ws.fill_(255)
+    torch.cuda.synchronize()
+    step.run(plan, stream=stream, want_loss=False)
+    torch.cuda.synchronize()
+    o_ck, o_ar, o_gr = 0, al(acc["ckpt"]), al(acc["ckpt"]) + al(acc["arena"])
+    out = {"ckpt": _touched(ws, o_ck, o_ck + acc["ckpt"]),
+           "arena": _touched(ws, o_ar, o_ar + acc["arena"]),
+           "grad": _touched(ws, o_gr, o_gr + acc["grad"])}
+    out["total"] = sum(out.values())
+    return out
 
 
 def main():
@@ -128,7 +170,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="cifar110")
+    ap.add_argument("--workload", default="resnet1000")
     ap.add_argument("--plan", default=None, choices=["sqrt", "greedy", "recursive", "search"],
                     help="override the workload's plan (search: the appendix-A budget search)")
     ap.add_argument("--fanout", type=int, default=0,
@@ -192,19 +234,24 @@ def main():
     run(none, args.warmup)
     torch.cuda.synchronize()
 
-    def timed(launch):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
+    def timed(launch, per_step=None):
+        # events on the stream the steps run on: one pair around all K steps
+        # (the mean), and one per step (the median)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
-        e0.record(s)
-        for _ in range(args.steps):
+        ev[0].record(s)
+        for k in range(args.steps):
             launch()
-        e1.record(s)
+            ev[k + 1].record(s)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / args.steps
+        if per_step is not None:
+            per_step.extend(ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps))
+        return ev[0].elapsed_time(ev[-1]) / args.steps
 
-    ms = timed(lambda: step.run(plan, stream=s, want_loss=False))
+    step_ms = []
+    ms = timed(lambda: step.run(plan, stream=s, want_loss=False), step_ms)
     ms_none = timed(lambda: step.run(none, stream=s, want_loss=False))
+    ms_median = float(np.median(step_ms))
     graph_ms = None
     if args.graph:  # each step recorded once as a HIP graph, then replayed
         graphs = {"plan": step.record(plan, s), "none": step.record(none, s)}
@@ -215,6 +262,12 @@ def main():
         graph_ms = {"ms_per_step": round(timed(lambda: graphs["plan"].launch(s)), 4),
                     "ms_per_step_no_ckpt": round(timed(lambda: graphs["none"].launch(s)), 4)}
     loss = float(step.loss_dev.item())
+    # bytes the checkpointed step writes in each region of the workspace,
+    # next to the planned (exact) peak; then the device allocator's
+    # high-water mark of the whole process (parameters, gradients, batch,
+    # workspace for the no-checkpoint plan, which is the larger)
+    written = _measured_regions(step, plan, acc, s)
+    device_hwm = torch.cuda.max_memory_allocated()
 
     # second timed pass: every launch of the dominant kernel family stamps an
     # event pair with its own start and end
@@ -254,7 +307,7 @@ def main():
     cpu = None
     sample = args.cpu_sample
     if sample < 0:
-        sample = {"lstm": 16, "resnet_bottleneck": 1}.get(cfg["kind"], 128)
+        sample = {"lstm": 16, "resnet_bottleneck": 1, "resnet_basic": 32}.get(cfg["kind"], 128)
     if sample > 0:
         if cfg["kind"] == "lstm":
             cpu = _cpu_baseline(cfg, min(sample, cfg["T"]), d)
@@ -270,6 +323,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(ms_median, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -282,6 +336,10 @@ def main():
                    **({"fanout": budget} if mode_name == "recursive" else {})},
         "peak_activation_gb": round(acc["peak"] / 1e9, 6),
         "peak_activation_gb_no_ckpt": round(acc_none["peak"] / 1e9, 6),
+        "peak_activation_gb_written": round(written["total"] / 1e9, 6),
+        "peak_regions_bytes": {"planned": {k: acc[k] for k in ("ckpt", "arena", "grad")},
+                               "written": {k: written[k] for k in ("ckpt", "arena", "grad")}},
+        "device_allocated_hwm_gb": round(device_hwm / 1e9, 6),
         "recompute_overhead_x": round(ms / ms_none, 4),
         "ms_per_step_no_ckpt": round(ms_none, 4),
         **({"hip_graph_replay": graph_ms} if graph_ms else {}),

@@ -460,6 +460,139 @@ int net_timing_enable(ckpt_net *net, int32_t enable);
 int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops, double *bytes,
                     char *name, int32_t cap);
 
+/* ---- operator calls -----------------------------------------------------
+ * The single operators the bf16 bottleneck units (section 5.2's deep residual
+ * network, built from the conv-BN-activation pipeline of section 4.2) are
+ * made of, each one launch (or a fixed short sequence) of exactly the kernels
+ * train_step runs, on caller buffers: a caller can check or compose one
+ * operator on inputs of its choice.  Tensors are NHWC, channel counts powers
+ * of two >= 8; "bf16" buffers hold bfloat16, "f32" float, "f64" double.
+ * All buffers are device memory the caller owns and sizes; the library cannot
+ * check their extents (a short buffer is a GPU memory fault).  Work is
+ * enqueued on `stream` (null = the default stream) and nothing is
+ * synchronised.  Arguments are validated before any launch (CKPT_E_INVALID,
+ * CKPT_E_UNSUPPORTED); a failed launch returns CKPT_E_HIP.
+ */
+#define CKPT_EPI_STORE     0 /* C = product                                          */
+#define CKPT_EPI_ADD       1 /* C = product + D (D may alias C)                      */
+#define CKPT_EPI_BF16STATS 3 /* Cb (bf16) = bf16(product); per row tile of the GEMM,
+                                f64 column sums of the rounded values and their
+                                squares: stats[row tile][2][n] (batch-norm input)    */
+#define CKPT_EPI_ADDMASK   4 /* C = product + (mask > 0 ? D : 0), mask bf16 like D   */
+#define CKPT_EPI_BNBWD     6 /* the gradient reaching a batch norm's output through a
+                                ReLU: C = ds = (mask > 0 ? product : 0), and per row
+                                tile f64 column sums of ds and ds * xhat,
+                                xhat = (cv - bst[col]) * bst[n + col], block-major
+                                stats[row tile][2][n]                               */
+
+/* op_gemm_bf16_blocks -- row and column tiles the bf16 GEMM uses for an
+ * [m, n] product (row tiles = the leading dimension of the per-tile stats of
+ * BF16STATS / BNBWD).  Either output may be null. */
+int op_gemm_bf16_blocks(int32_t m, int32_t n, int32_t *row_blocks, int32_t *col_blocks);
+
+/*
+ * op_gemm_bf16 -- C[m, n] (f32) = epi(op(A) op(B)), products accumulated in
+ * fp32 over k in one fixed order (a 1x1 convolution of NHWC tensors is this
+ * product with m = pixels).  A bf16 (or f32 rounded to bf16 on load when
+ * a_fp32, STORE / ADD only); ak: A[i * lda + k] (k contiguous), else
+ * A[k * lda + i]; B bf16, bk: B[j * ldb + k], else B[k * ldb + j]; C / D /
+ * mask / cv row stride ldc / ldd.  splits > 1 (STORE only): C receives
+ * `splits` partial products [m, ldc] over consecutive k ranges, to be added
+ * in order (op_sum_partials).  BF16STATS writes cb (bf16, stride ldc) and
+ * stats instead of C; BNBWD needs k-contiguous bf16 A, n-contiguous B,
+ * ldc == n, one split, mask, cv, bst and stats.  bias (nullable, STORE):
+ * + bias[j].
+ */
+int op_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *a, int32_t a_fp32, int32_t lda,
+                 int32_t ak, const void *b, int32_t ldb, int32_t bk, float *c, int32_t ldc,
+                 int32_t epi, const float *d, int32_t ldd, const float *bias, int32_t splits,
+                 const void *mask, void *cb, double *stats, const void *cv, const float *bst,
+                 void *stream);
+
+/* op_sum_partials -- out[e] = sum over b = 0..nb-1 (in order) of
+ * part[b * count + e], f32, 0 < count < 2^31. */
+int op_sum_partials(const float *part, int32_t nb, int64_t count, float *out, void *stream);
+
+/* Geometry of an r x r convolution with stride s (1 or 2) and zero padding
+ * p: input [n, h, w, ci], output [n, ho, wo, co], weights [co, r, r, ci];
+ * ho = (h + 2p - r) / s + 1, wo likewise; n h w below 2^24. */
+typedef struct ckpt_conv_geo {
+  int32_t n, h, w, ci, ho, wo, co, r, s, p;
+} ckpt_conv_geo;
+
+/* op_conv_bf16_fwd -- y (bf16) = bf16(conv(x, w)), x and w bf16, as an
+ * implicit GEMM (m = n ho wo output pixels, k = r r ci); stats as for
+ * BF16STATS with op_gemm_bf16_blocks(n ho wo, co) row tiles. */
+int op_conv_bf16_fwd(const ckpt_conv_geo *geo, const void *x, const void *w, void *y, double *stats,
+                     void *stream);
+
+/* op_conv_bf16_dgrad -- dx (f32, [n, h, w, ci]) = the data gradient of the
+ * convolution for dy (bf16, [n, ho, wo, co]) through w (bf16), with epilogue
+ * STORE, ADD (+ d), ADDMASK (+ d where mask > 0) or BNBWD (mask, cv, bst,
+ * stats as for op_gemm_bf16 with op_gemm_bf16_blocks(n h w, ci) row tiles);
+ * d, mask and cv shaped like dx (mask, cv bf16). */
+int op_conv_bf16_dgrad(const ckpt_conv_geo *geo, const void *dy, const void *w, float *dx, int32_t epi,
+                       const float *d, const void *mask, const void *cv, const float *bst,
+                       double *stats, void *stream);
+
+/* op_conv_bf16_wgrad -- dw (f32, [co, r, r, ci]) = the weight gradient from x
+ * (bf16 input) and dy (bf16 output gradient), summed over the n ho wo output
+ * pixels; splits > 1 splits that sum into `splits` partials in part (f32,
+ * splits co r r ci) added in a fixed order. */
+int op_conv_bf16_wgrad(const ckpt_conv_geo *geo, const void *x, const void *dy, float *part,
+                       int32_t splits, float *dw, void *stream);
+
+/* op_bn_finalize -- batch-norm statistics from f64 partial sums of nb blocks
+ * over m values per channel, j channels; channel_major: part[2][j][nb], else
+ * part[nb][2][j].  Forward (backward = 0): out[0..j) = mean, out[j..2j) =
+ * 1/sqrt(biased variance + 1e-5) from the sums of v and v^2.  Backward: from
+ * the sums of ds and ds * xhat, out[0..j) = their mean over m, out[j..2j) =
+ * the mean of ds * xhat, dbeta = sum ds, dgamma = sum ds * xhat. */
+int op_bn_finalize(int32_t backward, const double *part, int32_t nb, int32_t j, int64_t m, float *out,
+                   float *dgamma, float *dbeta, int32_t channel_major, void *stream);
+
+/* op_bnb_partial_blocks -- partial-sum blocks op_bnb_backward uses for p
+ * pixels of j channels (its part holds nb * 2j doubles). */
+int op_bnb_partial_blocks(int64_t p, int32_t j, int32_t *nb);
+
+#define CKPT_BNB_RES_NONE 0 /* y = relu(bn(c))                                     */
+#define CKPT_BNB_RES_ID   1 /* y = relu(bn(c) + x), x bf16 like c                   */
+#define CKPT_BNB_RES_BN   2 /* y = relu(bn(c) + bn_p(x)), the projection's batch norm
+                               with statistics stp, scale gp, shift bp             */
+/* op_bnb_apply -- y (bf16, [p, j]) = bf16(relu(gamma (c - mean) rstd + beta
+ * [+ shortcut])), c bf16 [p, j], st = mean [j] | rstd [j] (f32). */
+int op_bnb_apply(int32_t res, int64_t p, int32_t j, const void *c, const float *st, const float *gamma,
+                 const float *beta, const void *x, const float *stp, const float *gp, const float *bp,
+                 void *y, void *stream);
+
+/* op_bnb_backward -- the batch-norm backward for ds = (ym > 0 ? g : 0)
+ * (ym bf16, nullable: ds = g), g f32 [p, j], c the batch norm's bf16 input
+ * with statistics st: dbeta = sum ds, dgamma = sum ds xhat, d (bf16) =
+ * bf16(gamma rstd (ds - mean(ds) - xhat mean(ds xhat))); part holds
+ * op_bnb_partial_blocks(p, j) * 2j doubles, sums 2j floats (the two means).
+ * p < 2^31. */
+int op_bnb_backward(int64_t p, int32_t j, const float *g, const void *ym, const void *c, const float *st,
+                    const float *gamma, double *part, float *sums, float *dgamma, float *dbeta, void *d,
+                    void *stream);
+
+/* op_bnb_backward_apply -- the element pass of op_bnb_backward alone, given
+ * sums (2j floats from op_bn_finalize(backward = 1)). */
+int op_bnb_backward_apply(int64_t p, int32_t j, const float *g, const void *ym, const void *c,
+                          const float *st, const float *gamma, const float *sums, void *d,
+                          void *stream);
+
+/* op_im2col7 -- col (bf16, [n ho wo, 147]) = the 7x7 stride-2 pad-3 patches
+ * of x (bf16 [n, h, w, 3]) in (kh, kw, c) order, zero outside the image. */
+int op_im2col7(int32_t n, int32_t h, int32_t w, int32_t ho, int32_t wo, const void *x, void *col,
+               void *stream);
+
+/* op_maxpool -- 3x3 stride-2 pad-1 max pool of r (bf16 [n, h, w, c]):
+ * forward (backward = 0) out = y (bf16 [n, ho, wo, c]); backward out = dr
+ * (f32 [n, h, w, c]): each window's g (f32 [n, ho, wo, c]) goes to the first
+ * maximum of the window in row-major order (y the forward's output). */
+int op_maxpool(int32_t backward, int32_t n, int32_t h, int32_t w, int32_t c, int32_t ho, int32_t wo,
+               const float *g, const void *r, const void *y, void *out, void *stream);
+
 /* ckpt_last_error -- message of the last failed call on this thread ("" if
  * none). */
 const char *ckpt_last_error(void);

@@ -48,8 +48,9 @@ fp32 feed-forward chains the slot is the largest boundary and there is no
 extra.
 
 Parity: the accounting that consumes these tables is pinned in
-tests/test_oracle_planner.py; the tables themselves are restated layout
-("parity unpinned" beyond equality with the library's own tables).
+tests/test_oracle_planner.py, and the tables themselves against the tensors
+the oracle's own unit forwards keep (every unit kind, the drop bn-relu layout
+included), each counted in the dtype the layout stores it in.
 """
 from __future__ import annotations
 

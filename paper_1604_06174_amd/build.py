@@ -4,10 +4,9 @@
 
 Every source under csrc/ is compiled with hipcc for gfx950 and linked into
 paper_1604_06174_amd/libckpt.so.  Packed-fp32 instructions are disabled for
-all device code.  probes/peaks.hip (the attainable-peak measurement quoted
-next to the roofline fractions) is built into probes/peaks, and
-probes/elementwise_bw.cpp (batch-norm pass bandwidth, linked against the
-library) into probes/elementwise_bw.
+all device code.  Nothing else is built here: the attainable-peak
+microbenchmark beside bench.py (peaks.hip) is a measurement aid with its own
+one-line build command in its header.
 """
 from __future__ import annotations
 
@@ -59,21 +58,6 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, OUT)
-    probe = os.path.join(HERE, "probes", "peaks")
-    cmd = [HIPCC, "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-Xclang", "-target-feature",
-           "-Xclang", "-packed-fp32-ops", "-o", probe + ".tmp", probe + ".hip"]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed on probes/peaks.hip:\n{r.stdout}\n{r.stderr}")
-    os.replace(probe + ".tmp", probe)
-    # bandwidth probe of the batch-norm element passes, linked against the library
-    bw = os.path.join(HERE, "probes", "elementwise_bw")
-    cmd = [HIPCC, "-O2", "-std=c++17", f"--offload-arch={ARCH}", "-o", bw + ".tmp", bw + ".cpp",
-           "-L" + HERE, "-lckpt", "-Wl,-rpath,$ORIGIN/.."]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed on probes/elementwise_bw.cpp:\n{r.stdout}\n{r.stderr}")
-    os.replace(bw + ".tmp", bw)
     return OUT
 
 

@@ -119,7 +119,39 @@ _sig("train_step_graph", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER
                                    C.c_void_p, C.c_uint64, C.c_void_p, C.POINTER(C.c_float),
                                    C.POINTER(C.c_float), _u64p, C.POINTER(StepStats)])
 
-EXPORTED = ["ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
+
+class ConvGeo(C.Structure):
+    _fields_ = [(k, C.c_int32) for k in ("n", "h", "w", "ci", "ho", "wo", "co", "r", "s", "p")]
+
+
+_vp = C.c_void_p
+_sig("op_gemm_bf16_blocks", C.c_int, [C.c_int32, C.c_int32, _i32p, _i32p])
+_sig("op_gemm_bf16", C.c_int, [C.c_int32, C.c_int32, C.c_int32, _vp, C.c_int32, C.c_int32, C.c_int32,
+                               _vp, C.c_int32, C.c_int32, _vp, C.c_int32, C.c_int32, _vp, C.c_int32,
+                               _vp, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp])
+_sig("op_sum_partials", C.c_int, [_vp, C.c_int32, C.c_int64, _vp, _vp])
+_sig("op_conv_bf16_fwd", C.c_int, [C.POINTER(ConvGeo), _vp, _vp, _vp, _vp, _vp])
+_sig("op_conv_bf16_dgrad", C.c_int, [C.POINTER(ConvGeo), _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp,
+                                     _vp, _vp, _vp])
+_sig("op_conv_bf16_wgrad", C.c_int, [C.POINTER(ConvGeo), _vp, _vp, _vp, C.c_int32, _vp, _vp])
+_sig("op_bn_finalize", C.c_int, [C.c_int32, _vp, C.c_int32, C.c_int32, C.c_int64, _vp, _vp, _vp,
+                                 C.c_int32, _vp])
+_sig("op_bnb_partial_blocks", C.c_int, [C.c_int64, C.c_int32, _i32p])
+_sig("op_bnb_apply", C.c_int, [C.c_int32, C.c_int64, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                               _vp, _vp, _vp])
+_sig("op_bnb_backward", C.c_int, [C.c_int64, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                  _vp, _vp])
+_sig("op_bnb_backward_apply", C.c_int, [C.c_int64, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp])
+_sig("op_im2col7", C.c_int, [C.c_int32] * 5 + [_vp, _vp, _vp])
+_sig("op_maxpool", C.c_int, [C.c_int32] * 7 + [_vp, _vp, _vp, _vp, _vp])
+
+EPI_STORE, EPI_ADD, EPI_BF16STATS, EPI_ADDMASK, EPI_BNBWD = 0, 1, 3, 4, 6
+BNB_RES_NONE, BNB_RES_ID, BNB_RES_BN = 0, 1, 2
+
+EXPORTED = ["op_gemm_bf16_blocks", "op_gemm_bf16", "op_sum_partials", "op_conv_bf16_fwd",
+            "op_conv_bf16_dgrad", "op_conv_bf16_wgrad", "op_bn_finalize", "op_bnb_partial_blocks",
+            "op_bnb_apply", "op_bnb_backward", "op_bnb_backward_apply", "op_im2col7", "op_maxpool",
+            "ckpt_last_error", "plan_checkpoints", "plan_info", "plan_cuts", "plan_serialize",
             "plan_free", "plan_search", "graph_plan", "graph_plan_info", "graph_plan_schedule",
             "graph_plan_blocks", "graph_plan_free", "net_node_graph", "graph_workspace_bytes",
             "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
@@ -471,3 +503,85 @@ def step_graph_create(net: Net, params, grads, batch_input, batch_target, plan: 
                                   C.byref(out), C.byref(st)))
     keep = (net, plan, params, grads, batch_input, batch_target, workspace, loss_dev)
     return StepGraph(out.value, keep, st.as_dict())
+
+
+# ------------------------------------------------------------ operators --
+def _s(stream):
+    if stream is None:
+        return None
+    return stream if isinstance(stream, int) else int(stream.cuda_stream)
+
+
+def conv_geo(n, h, w, ci, ho, wo, co, r, s, p) -> ConvGeo:
+    return ConvGeo(n, h, w, ci, ho, wo, co, r, s, p)
+
+
+def op_gemm_bf16_blocks(m: int, n: int) -> Tuple[int, int]:
+    rb, cb = C.c_int32(), C.c_int32()
+    _check(_lib.op_gemm_bf16_blocks(m, n, C.byref(rb), C.byref(cb)))
+    return rb.value, cb.value
+
+
+def op_gemm_bf16(m, n, k, a, lda, ak, b, ldb, bk, c, ldc, epi=EPI_STORE, d=None, ldd=0, bias=None,
+                 splits=1, mask=None, cb=None, stats=None, cv=None, bst=None, a_fp32=False,
+                 stream=None):
+    _check(_lib.op_gemm_bf16(m, n, k, _addr(a), int(a_fp32), lda, int(ak), _addr(b), ldb, int(bk),
+                             _addr(c), ldc, epi, _addr(d), ldd, _addr(bias), splits, _addr(mask),
+                             _addr(cb), _addr(stats), _addr(cv), _addr(bst), _s(stream)))
+
+
+def op_sum_partials(part, nb, count, out, stream=None):
+    _check(_lib.op_sum_partials(_addr(part), nb, count, _addr(out), _s(stream)))
+
+
+def op_conv_bf16_fwd(geo, x, w, y, stats, stream=None):
+    _check(_lib.op_conv_bf16_fwd(C.byref(geo), _addr(x), _addr(w), _addr(y), _addr(stats), _s(stream)))
+
+
+def op_conv_bf16_dgrad(geo, dy, w, dx, epi=EPI_STORE, d=None, mask=None, cv=None, bst=None,
+                       stats=None, stream=None):
+    _check(_lib.op_conv_bf16_dgrad(C.byref(geo), _addr(dy), _addr(w), _addr(dx), epi, _addr(d),
+                                   _addr(mask), _addr(cv), _addr(bst), _addr(stats), _s(stream)))
+
+
+def op_conv_bf16_wgrad(geo, x, dy, part, splits, dw, stream=None):
+    _check(_lib.op_conv_bf16_wgrad(C.byref(geo), _addr(x), _addr(dy), _addr(part), splits, _addr(dw),
+                                   _s(stream)))
+
+
+def op_bn_finalize(backward, part, nb, j, m, out, dgamma=None, dbeta=None, channel_major=False,
+                   stream=None):
+    _check(_lib.op_bn_finalize(int(backward), _addr(part), nb, j, m, _addr(out), _addr(dgamma),
+                               _addr(dbeta), int(channel_major), _s(stream)))
+
+
+def op_bnb_partial_blocks(p: int, j: int) -> int:
+    nb = C.c_int32()
+    _check(_lib.op_bnb_partial_blocks(p, j, C.byref(nb)))
+    return nb.value
+
+
+def op_bnb_apply(res, p, j, c, st, gamma, beta, x=None, stp=None, gp=None, bp=None, y=None,
+                 stream=None):
+    _check(_lib.op_bnb_apply(res, p, j, _addr(c), _addr(st), _addr(gamma), _addr(beta), _addr(x),
+                             _addr(stp), _addr(gp), _addr(bp), _addr(y), _s(stream)))
+
+
+def op_bnb_backward(p, j, g, ym, c, st, gamma, part, sums, dgamma, dbeta, d, stream=None):
+    _check(_lib.op_bnb_backward(p, j, _addr(g), _addr(ym), _addr(c), _addr(st), _addr(gamma),
+                                _addr(part), _addr(sums), _addr(dgamma), _addr(dbeta), _addr(d),
+                                _s(stream)))
+
+
+def op_bnb_backward_apply(p, j, g, ym, c, st, gamma, sums, d, stream=None):
+    _check(_lib.op_bnb_backward_apply(p, j, _addr(g), _addr(ym), _addr(c), _addr(st), _addr(gamma),
+                                      _addr(sums), _addr(d), _s(stream)))
+
+
+def op_im2col7(n, h, w, ho, wo, x, col, stream=None):
+    _check(_lib.op_im2col7(n, h, w, ho, wo, _addr(x), _addr(col), _s(stream)))
+
+
+def op_maxpool(backward, n, h, w, c, ho, wo, r, out, g=None, y=None, stream=None):
+    _check(_lib.op_maxpool(int(backward), n, h, w, c, ho, wo, _addr(g), _addr(r), _addr(y), _addr(out),
+                           _s(stream)))

@@ -41,6 +41,11 @@ void run_graph_step(Net &net, const float *params, float *grads, const ckpt_batc
 
 namespace {
 thread_local std::string g_err;
+}  // namespace
+
+void ckpt::set_last_error(const std::string &msg) { g_err = msg; }
+
+namespace {
 
 template <class F>
 int guarded(F &&f) {

@@ -22,6 +22,9 @@ struct Error : std::exception {
 
 [[noreturn]] inline void fail(int code, const std::string &msg) { throw Error(code, msg); }
 
+// the thread-local message ckpt_last_error() returns
+void set_last_error(const std::string &msg);
+
 // ---------------------------------------------------------------- plans --
 struct Plan {
   int32_t mode = CKPT_NONE;

@@ -6,6 +6,10 @@
 //   accumulator chains on register operands, 256 threads per workgroup, for
 //   several grid sizes; throughput = MFMA flops / event time.
 //   HBM: a float4 device-to-device copy of 1 GiB (bytes read + written).
+//
+// Build and run (not part of the library build):
+//   hipcc -O3 -std=c++17 --offload-arch=gfx950 -Xclang -target-feature \
+//     -Xclang -packed-fp32-ops -o _build/peaks peaks.hip && _build/peaks
 #include <hip/hip_runtime.h>
 
 #include <cstdio>

@@ -20,7 +20,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "ck
 def _declared():
     txt = open(HEADER).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(?:int|void|const char \*)\s*\**\s*([a-z_]+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b(?:int|void|const char \*)\s*\**\s*([a-z_][a-z_0-9]*)\s*\(", txt)))
 
 
 def test_exports_every_declared_symbol():
@@ -361,3 +361,60 @@ def test_node_graph_errors():
     with pytest.raises(K.CkptError) as ei:
         mlp.graph_workspace_bytes(p)
     assert ei.value.code == K.E_MISMATCH
+
+
+# ---- operator calls: argument validation happens before any launch ------
+FAKE = 1 << 40  # never dereferenced: every call below fails validation first
+
+
+@pytest.mark.parametrize("call,code", [
+    # 12 channels: not a power of two
+    (lambda: K.op_conv_bf16_fwd(K.conv_geo(1, 4, 4, 12, 4, 4, 16, 3, 1, 1), FAKE, FAKE, FAKE, FAKE),
+     K.E_UNSUPPORTED),
+    # output side inconsistent with the geometry
+    (lambda: K.op_conv_bf16_fwd(K.conv_geo(1, 4, 4, 16, 3, 3, 16, 3, 1, 1), FAKE, FAKE, FAKE, FAKE),
+     K.E_UNSUPPORTED),
+    # stride 3
+    (lambda: K.op_conv_bf16_wgrad(K.conv_geo(1, 9, 9, 16, 3, 3, 16, 3, 3, 0), FAKE, FAKE, FAKE, 1,
+                                  FAKE), K.E_UNSUPPORTED),
+    # null weights
+    (lambda: K.op_conv_bf16_fwd(K.conv_geo(1, 4, 4, 16, 4, 4, 16, 3, 1, 1), FAKE, None, FAKE, FAKE),
+     K.E_INVALID),
+    # BNBWD without its batch-norm operands
+    (lambda: K.op_conv_bf16_dgrad(K.conv_geo(1, 4, 4, 16, 4, 4, 16, 3, 1, 1), FAKE, FAKE, FAKE,
+                                  K.EPI_BNBWD, mask=FAKE), K.E_INVALID),
+    # split-K with an epilogue other than STORE
+    (lambda: K.op_gemm_bf16(8, 8, 8, FAKE, 8, True, FAKE, 8, True, FAKE, 8, K.EPI_ADD, d=FAKE, ldd=8,
+                            splits=2), K.E_INVALID),
+    # leading dimension shorter than the row
+    (lambda: K.op_gemm_bf16(8, 8, 16, FAKE, 8, True, FAKE, 16, True, FAKE, 8), K.E_INVALID),
+    # BF16STATS without its statistics buffer
+    (lambda: K.op_gemm_bf16(8, 8, 8, FAKE, 8, True, FAKE, 8, True, None, 8, K.EPI_BF16STATS, cb=FAKE),
+     K.E_INVALID),
+    # an fp32 A with a bf16-only epilogue
+    (lambda: K.op_gemm_bf16(8, 8, 8, FAKE, 8, True, FAKE, 8, True, FAKE, 8, K.EPI_ADDMASK, d=FAKE,
+                            ldd=8, mask=FAKE, a_fp32=True), K.E_INVALID),
+    # BNBWD with a k-major A (the epilogue's operand form is fixed)
+    (lambda: K.op_gemm_bf16(8, 8, 8, FAKE, 8, False, FAKE, 8, False, FAKE, 8, K.EPI_BNBWD, mask=FAKE,
+                            cv=FAKE, bst=FAKE, stats=FAKE), K.E_INVALID),
+    (lambda: K.op_bnb_apply(K.BNB_RES_ID, 8, 8, FAKE, FAKE, FAKE, FAKE, y=FAKE), K.E_INVALID),
+    (lambda: K.op_bnb_apply(K.BNB_RES_NONE, 8, 12, FAKE, FAKE, FAKE, FAKE, y=FAKE), K.E_INVALID),
+    (lambda: K.op_bnb_backward(1 << 31, 8, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE),
+     K.E_INVALID),
+    (lambda: K.op_maxpool(False, 1, 8, 8, 16, 5, 4, FAKE, FAKE), K.E_INVALID),
+    (lambda: K.op_maxpool(True, 1, 8, 8, 16, 4, 4, FAKE, FAKE), K.E_INVALID),  # backward without g
+    (lambda: K.op_im2col7(1, 8, 8, 3, 4, FAKE, FAKE), K.E_INVALID),
+    (lambda: K.op_bn_finalize(True, FAKE, 1, 8, 10, FAKE), K.E_INVALID),
+    (lambda: K.op_sum_partials(FAKE, 0, 8, FAKE), K.E_INVALID),
+])
+def test_operator_calls_validate_before_launch(call, code):
+    with pytest.raises(K.CkptError) as e:
+        call()
+    assert e.value.code == code
+    assert K._lib.ckpt_last_error()
+
+
+def test_operator_block_counts():
+    rb, cb = K.op_gemm_bf16_blocks(2 * 56 * 56, 64)
+    assert rb >= 1 and cb >= 1 and rb * 256 >= 2 * 56 * 56 // 64
+    assert K.op_bnb_partial_blocks(6272, 64) >= 1

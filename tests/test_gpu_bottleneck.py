@@ -1,122 +1,101 @@
 """GPU parity of the bf16 bottleneck ResNet checkpointed step against the oracle.
 
 The GPU rounds to bf16 at the points the oracle's ``Prec(bf16=True)`` mode
-does (input, weights, conv outputs, ReLU outputs, block outputs and the
-batch-norm input gradients), so the reference is that oracle in float64.
+does (input, weights, convolution outputs, ReLU outputs, block outputs and
+the batch-norm input gradients).  Two kinds of shapes (bneck_cases):
 
-Conditioning.  This network is chaotic at the bf16 rounding level: a value
-whose float32 accumulation lands on the other side of a bf16 rounding
-midpoint shifts its channel's batch-norm statistics, which moves every value
-of the channel and flips further roundings downstream.  Perturbing the
-oracle's values by 1e-7 (relative, Gaussian) just before each bf16 rounding
--- the size of float32 accumulation error -- moves its loss by up to 1e-2 and
-single gradient tensors by far more than the bf16 bar on every configuration
-with more than one block, and so does any other evaluation order, the GPU's
-included.  The bar is therefore statistical: over six such perturbed oracle
-runs (seeded), take per gradient tensor the largest max-abs relative and L2
-relative deviation from the unperturbed oracle, and the largest loss
-deviation; the GPU may deviate by at most 3x those plus 2e-2 (the bf16 bar)
-per tensor, and 3x plus 1e-5 on the loss.  Every plan must also give the
-no-checkpoint run's gradient bytes, the oracle's peak bytes and its
-unit-forward count.
+* well-posed shapes, asserted first (six oracle runs perturbed by 1e-7 before
+  every bf16 rounding stay within 2e-3 of the unperturbed run on every
+  gradient tensor): the GPU must match the bf16-emulating float64 oracle to
+  5e-3 max-abs relative per gradient tensor and 1e-5 on the loss, and the
+  plain float64 oracle to 5e-3 on the loss (bf16 rounding alone moves the
+  loss by up to 1.4e-3 on these shapes);
+* chaotic shapes (where the same perturbation moves tensors by up to tens of
+  percent): the loss within 2e-2 of the emulating oracle.
+
+On every shape every plan must give the no-checkpoint run's gradient bytes,
+the oracle's peak bytes and its unit-forward count.  The plain float64
+oracle's gradients are printed for reference: rounding to bf16 alone moves
+them by 20-100% on these shapes (the gradients of the parameters under a
+batch norm are small residuals of large sums), so no bf16 implementation can
+be held to them per tensor; the single operators are held to fixed bars
+against float64 at the real widths in test_gpu_ops_bf16.
 """
 import numpy as np
 import pytest
 
 import synth
-from oracle import nets, planner as PL, sizes as SZ, units as U
+from bneck_cases import CHAOTIC, GATE, WELL_POSED, maxrel, oracle_runs
+from oracle import planner as PL, sizes as SZ
 
 pytestmark = pytest.mark.gpu
 
-JITTER, REPS = 1e-7, 6
+MODES = [("none", PL.NONE, None, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
+         ("greedy", PL.GREEDY, "third", None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
+         ("recursive_k2", PL.RECURSIVE, 2, None, 0), ("user_keep", PL.USER, 0, [0], PL.FLAG_KEEP_LAST)]
 
 
-def _maxrel(g, o):
-    g = np.asarray(g, np.float64).reshape(-1)
-    o = np.asarray(o, np.float64).reshape(-1)
-    return float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-30))
-
-
-def _l2rel(g, o):
-    g = np.asarray(g, np.float64).reshape(-1)
-    o = np.asarray(o, np.float64).reshape(-1)
-    return float(np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-30))
-
-
-CASES = {
-    # stem + one stride-1 projection block
-    "b1": dict(kind="resnet_bottleneck", stage_blocks=(1,), widths=(8,), expansion=4,
-               stem_channels=8, image=16, batch=2, classes=7, seed=91),
-    # + identity blocks and a stride-2 projection stage
-    "b22": dict(kind="resnet_bottleneck", stage_blocks=(2, 2), widths=(8, 16), expansion=4,
-                stem_channels=8, image=16, batch=2, classes=7, seed=91),
-    # four stages down to 1 x 1, stem 16
-    "b2111": dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1, 1), widths=(8, 16, 32, 64),
-                  expansion=4, stem_channels=16, image=32, batch=2, classes=10, seed=91),
-    # expansion 2, a single image
-    "b121": dict(kind="resnet_bottleneck", stage_blocks=(1, 2, 1), widths=(8, 16, 32), expansion=2,
-                 stem_channels=8, image=32, batch=1, classes=5, seed=92),
-    # the real stage-1/2 channel counts: several GEMM tiles, split-K weight gradients
-    "wide": dict(kind="resnet_bottleneck", stage_blocks=(1, 1), widths=(64, 128), expansion=4,
-                 stem_channels=64, image=64, batch=4, classes=100, seed=83),
-}
-
-
-def _envelope(d):
-    chain = lambda prec: nets.Chain(d["structure"], d["params"], prec)
-    l0, g0 = nets.full_storage_step(chain(U.Prec(np.float64, True)), d["input"], d["target"])
-    em = {k: 0.0 for k in g0}
-    el = {k: 0.0 for k in g0}
-    lmax = 0.0
-    for s in range(REPS):
-        prec = U.Prec(np.float64, True, JITTER, np.random.default_rng(700 + s))
-        l1, g1 = nets.full_storage_step(chain(prec), d["input"], d["target"])
-        lmax = max(lmax, abs(l1 - l0) / abs(l0))
-        for k in g0:
-            em[k] = max(em[k], _maxrel(g1[k], g0[k]))
-            el[k] = max(el[k], _l2rel(g1[k], g0[k]))
-    return l0, g0, lmax, em, el
-
-
-@pytest.mark.parametrize("case", list(CASES))
-def test_bottleneck_parity_all_modes(case):
+def _all_plans(step, st):
+    """Every plan: exact peak and forward count; returns the no-checkpoint
+    run's (loss, gradients, gradient bytes) and asserts every other plan's
+    gradient bytes equal them."""
     import torch
-    from paper_1604_06174_amd.workload import GpuStep
-    cfg = CASES[case]
-    print(f"[bottleneck parity] case={case} cfg={cfg}", flush=True)
-    d = synth.make(cfg)
-    l0, g0, lmax, em, el = _envelope(d)
-    st = d["structure"]
-    step = GpuStep(cfg, d["params"], d["input"], d["target"])
     b, a, q = SZ.tables(st)
     slot, extra = SZ.grad_layout(st)
     lb, cb = SZ.layer_and_cut_bytes(st)
-    n = st.n
-    modes = [("none", PL.NONE, 0, None, 0), ("sqrt", PL.SQRT, 0, None, 0),
-             ("greedy", PL.GREEDY, sum(lb) // 3, None, 0), ("recursive", PL.RECURSIVE, 0, None, 0),
-             ("recursive_k2", PL.RECURSIVE, 2, None, 0),
-             ("user_keep", PL.USER, 0, [0], PL.FLAG_KEEP_LAST)]
     ref = None
-    for name, mode, budget, user, flags in modes:
+    for name, mode, budget, user, flags in MODES:
+        budget = sum(lb) // 3 if budget == "third" else (budget or 0)
         plan = step.plan(mode, budget, user, flags)
         step.grads.fill_(float("nan"))
         loss, peak, stats = step.run(plan)
         torch.cuda.synchronize()
-        op = PL.plan(n, lb, cb, budget, mode, user, flags)
+        op = PL.plan(st.n, lb, cb, budget, mode, user, flags)
         assert peak == PL.account(op, b, a, q, slot, extra).peak, name
         assert stats["unit_forwards"] == PL.unit_forwards(op), name
         gbytes = step.grads_bytes()
         if ref is None:
-            ref = gbytes
-            g = step.grads_host()
-            dl = abs(loss - l0) / abs(l0)
-            print(f"  loss {loss:.6f} oracle {l0:.6f} dev {dl:.1e} (envelope {lmax:.1e})", flush=True)
-            assert dl <= 3 * lmax + 1e-5, (dl, lmax)
-            for k, v in g0.items():
-                m, l = _maxrel(g[k], v), _l2rel(g[k], v)
-                assert m <= 3 * em[k] + 2e-2, (k, m, em[k])
-                assert l <= 3 * el[k] + 2e-2, (k, l, el[k])
-            worst = max(g0, key=lambda k: _maxrel(g[k], g0[k]))
-            print(f"  worst tensor {worst}: {_maxrel(g[worst], g0[worst]):.1e} "
-                  f"(envelope {em[worst]:.1e})", flush=True)
-        assert gbytes == ref, f"{name}: gradients differ from the no-checkpoint run"
+            ref = (loss, step.grads_host(), gbytes)
+        assert gbytes == ref[2], f"{name}: gradients differ from the no-checkpoint run"
+    return ref
+
+
+@pytest.mark.parametrize("case", list(WELL_POSED))
+def test_bottleneck_parity_well_posed(case):
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = WELL_POSED[case]
+    print(f"[bottleneck parity] well-posed case={case} cfg={cfg}", flush=True)
+    d = synth.make(cfg)
+    (le, ge), (lf, gf), env, lenv = oracle_runs(d)
+    worst_env = max(env.values())
+    assert worst_env <= GATE, f"{case} is not well posed: perturbed oracle moves {worst_env:.2e}"
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    loss, g, _ = _all_plans(step, d["structure"])
+    dl, dlf = abs(loss - le) / abs(le), abs(loss - lf) / abs(lf)
+    print(f"  loss {loss:.7f}: vs emulating oracle {dl:.1e}, vs float64 {dlf:.1e}", flush=True)
+    assert dl <= 1e-5, dl
+    assert dlf <= 5e-3, dlf
+    errs = {k: maxrel(g[k], v) for k, v in ge.items()}
+    w = max(errs, key=errs.get)
+    wf = max(gf, key=lambda k: maxrel(g[k], gf[k]))
+    print(f"  worst tensor vs emulating oracle {w}: {errs[w]:.2e} (perturbation envelope "
+          f"{worst_env:.1e}); vs float64 {wf}: {maxrel(g[wf], gf[wf]):.2e}", flush=True)
+    for k, e in errs.items():
+        assert e <= 5e-3, (k, e)
+
+
+@pytest.mark.parametrize("case", list(CHAOTIC))
+def test_bottleneck_plans_chaotic(case):
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = CHAOTIC[case]
+    print(f"[bottleneck parity] chaotic case={case} cfg={cfg}", flush=True)
+    d = synth.make(cfg)
+    from oracle import nets, units as U
+    le, _ = nets.full_storage_step(nets.Chain(d["structure"], d["params"], U.Prec(np.float64, True)),
+                                   d["input"], d["target"])
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    loss, g, _ = _all_plans(step, d["structure"])
+    dl = abs(loss - le) / abs(le)
+    print(f"  loss {loss:.6f} vs emulating oracle {le:.6f}: {dl:.1e}", flush=True)
+    assert dl <= 2e-2, dl
+    assert all(np.all(np.isfinite(v)) for v in g.values())

@@ -208,24 +208,52 @@ def test_serialize_layout():
 
 @pytest.mark.parametrize("cfg", [dict(kind="mlp", depth=5, width=16, batch=4, seed=1),
                                  dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=2,
-                                      image=8, classes=3, seed=2)])
+                                      image=8, classes=3, seed=2),
+                                 dict(kind="resnet_basic", blocks_per_stage=2, base=4, batch=2,
+                                      image=8, classes=3, seed=2, drop_bn_relu=1),
+                                 dict(kind="resnet_bottleneck", stage_blocks=(2, 1), widths=(8, 16),
+                                      expansion=4, stem_channels=8, image=16, batch=2, classes=5,
+                                      seed=3),
+                                 dict(kind="lstm", T=3, batch=4, input=8, hidden=16, vocab=24,
+                                      seed=4)])
 def test_size_tables_match_kept_tensors(cfg):
-    """a_i and b_{i+1} equal the aligned nbytes of what the float32 oracle keeps."""
+    """a_i and b_{i+1} equal the aligned bytes of what the oracle keeps, each
+    tensor counted in the dtype the static layout stores it in: bf16 for the
+    bottleneck net's activations and the LSTM's h, fp32 otherwise (batch-norm
+    (mean, rstd) pairs as one block).  The bottleneck stem's max-pool window
+    choice ("arg") is not kept: the backward finds the window's first maximum
+    again from the pooled output.  The drop bn-relu layout keeps neither the
+    relu(bn1) output."""
     d = synth.make(cfg)
-    chain = nets.Chain(d["structure"], d["params"], U.Prec(np.float32))
+    kind = cfg["kind"]
+    chain = nets.Chain(d["structure"], d["params"], U.Prec(np.float32, kind == "resnet_bottleneck"))
     b, a, q = SZ.tables(d["structure"])
+    drop = kind == "resnet_basic" and cfg.get("drop_bn_relu")
+
+    def nbytes(name, v, half=False):
+        if isinstance(v, tuple):          # BN (mean, rstd) pair: one fp32 block
+            return SZ.align(sum(4 * t.size for t in v))
+        return SZ.align((2 if half else 4) * v.size)
+
+    def boundary(x):
+        if kind == "lstm":                # (h bf16, c fp32)
+            return nbytes("h", x[0], True) + nbytes("c", x[1])
+        return nbytes("x", x, kind == "resnet_bottleneck")
+
     x = chain.x0(d["input"])
-    assert SZ.align(x.nbytes) == b[0]
+    assert boundary(x) == b[0]
     for i in range(chain.n):
-        y, saved, _ = chain.units[i].fwd(x, chain.P(i))
+        y, saved, _ = chain.units[i].fwd(x, chain.P(i), chain.ext(i, d["input"], d["target"]))
         kept = 0
-        for v in saved.values():
-            if isinstance(v, tuple):          # BN (mean, rstd) pair is stored as one block
-                kept += SZ.align(sum(t.nbytes for t in v))
-            else:
-                kept += SZ.align(v.nbytes)
+        if kind == "lstm":                # the four gates as one [B, 4H] block, then dlog
+            kept = SZ.align(sum(4 * saved[g].size for g in "ifgo")) + nbytes("dlog", saved["dlog"])
+        else:
+            for nm, v in saved.items():
+                if nm == "arg" or (drop and nm == "r1"):
+                    continue
+                kept += nbytes(nm, v, kind == "resnet_bottleneck")
         assert kept == a[i], (i, kept, a[i])
-        assert SZ.align(y.nbytes) == b[i + 1]
+        assert boundary(y) == b[i + 1]
         x = y
 
 

@@ -371,6 +371,28 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
 
 /*
+ * train_step_static -- train_step for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same step with the same arguments minus the
+ * workspace, which is instead a fixed scratch array of
+ * CKPT_STATIC_SCRATCH_BYTES the library holds on each GPU it runs on (from
+ * the first call on that GPU until the process ends).  It calls no
+ * hipMalloc, hipFree or other allocating routine.  The scratch of the calling
+ * thread's current device (hipGetDevice) is used; `stream` must belong to
+ * that device.  Results equal train_step's bit for bit (same kernels, same
+ * layout).  Every call on one GPU shares that GPU's scratch, which keeps the
+ * last call's contents (the step ignores them on entry); calls that overlap
+ * in time on one GPU race on it.
+ * Errors: as train_step; CKPT_E_WORKSPACE when net_workspace_bytes(net, plan)
+ *   exceeds CKPT_STATIC_SCRATCH_BYTES; CKPT_E_INVALID with kernel timing on
+ *   (timing creates events).
+ */
+#define CKPT_STATIC_SCRATCH_BYTES (64u << 20)
+int train_step_static(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
+                      const ckpt_plan *plan, void *stream, float *loss_dev, float *loss_host,
+                      uint64_t *peak, ckpt_step_stats *stats);
+
+/*
  * Recorded steps.  A checkpointed step is a fixed sequence of small kernels
  * (the plan fixes every launch and every buffer: section 4's static plan);
  * recording it once as a HIP graph and launching the graph replaces the

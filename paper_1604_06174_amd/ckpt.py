@@ -113,6 +113,10 @@ _sig("step_graph_create", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTE
                                     C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p,
                                     C.POINTER(C.c_float), C.POINTER(C.c_void_p),
                                     C.POINTER(StepStats)])
+_sig("train_step_static", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
+                                    C.c_void_p, C.POINTER(C.c_float), C.POINTER(C.c_float), _u64p,
+                                    C.POINTER(StepStats)])
+STATIC_SCRATCH_BYTES = 64 << 20
 _sig("step_graph_launch", C.c_int, [C.c_void_p, C.c_void_p])
 _sig("step_graph_free", None, [C.c_void_p])
 _sig("train_step_graph", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
@@ -157,7 +161,7 @@ EXPORTED = ["op_gemm_bf16_blocks", "op_gemm_bf16", "op_sum_partials", "op_conv_b
             "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
             "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
-            "train_step", "step_graph_create", "step_graph_launch", "step_graph_free"]
+            "train_step", "train_step_static", "step_graph_create", "step_graph_launch", "step_graph_free"]
 
 
 class CkptError(RuntimeError):
@@ -458,6 +462,24 @@ def train_step(net: Net, params, grads, batch_input, batch_target, plan: Plan, w
                            _addr(workspace), int(workspace_bytes), s,
                            C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
                            C.byref(loss) if want_loss else None, C.byref(peak), C.byref(st)))
+    return (loss.value if want_loss else None), peak.value, st.as_dict()
+
+
+def train_step_static(net: Net, params, grads, batch_input, batch_target, plan: Plan, stream=None,
+                      loss_dev=None, want_loss: bool = True):
+    """train_step on the library's static per-GPU scratch (no workspace
+    argument); returns (loss or None, peak bytes, stats dict)."""
+    b = Batch(_addr(batch_input), _addr(batch_target))
+    loss = C.c_float()
+    peak = C.c_uint64()
+    st = StepStats()
+    s = None
+    if stream is not None:
+        s = stream if isinstance(stream, int) else int(stream.cuda_stream)
+    ld = _addr(loss_dev)
+    _check(_lib.train_step_static(net.handle, _addr(params), _addr(grads), C.byref(b), plan.handle, s,
+                                  C.cast(C.c_void_p(ld), C.POINTER(C.c_float)) if ld else None,
+                                  C.byref(loss) if want_loss else None, C.byref(peak), C.byref(st)))
     return (loss.value if want_loss else None), peak.value, st.as_dict()
 
 

@@ -7,32 +7,10 @@
 #include <cstring>
 #include <memory>
 
+#include "capi_internal.h"
 #include "net.h"
 
-struct ckpt_plan {
-  ckpt::Plan p;
-};
-struct ckpt_net {
-  std::unique_ptr<ckpt::Net> net;
-};
-struct ckpt_graph_plan {
-  ckpt::GraphPlan p;
-};
-// a recorded training step: the captured graph and its executable form
-struct ckpt_step_graph {
-  hipGraph_t graph = nullptr;
-  hipGraphExec_t exec = nullptr;
-  ~ckpt_step_graph() {
-    if (exec) (void)hipGraphExecDestroy(exec);
-    if (graph) (void)hipGraphDestroy(graph);
-  }
-};
-
 namespace ckpt {
-uint64_t workspace_bytes(const Net &net, const Accounting &acc);
-void run_train_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
-                    const Plan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
-                    float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
 uint64_t graph_workspace_bytes(const Net &net, const GraphPlan &p);
 void run_graph_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
                     const GraphPlan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
@@ -45,51 +23,6 @@ thread_local std::string g_err;
 
 void ckpt::set_last_error(const std::string &msg) { g_err = msg; }
 
-namespace {
-
-template <class F>
-int guarded(F &&f) {
-  try {
-    f();
-    g_err.clear();
-    return CKPT_OK;
-  } catch (const ckpt::Error &e) {
-    g_err = e.msg;
-    return e.code;
-  } catch (const std::bad_alloc &) {
-    g_err = "host allocation failed";
-    return CKPT_E_INVALID;
-  } catch (const std::exception &e) {
-    g_err = e.what();
-    return CKPT_E_INVALID;
-  }
-}
-
-void need(const void *p, const char *what) {
-  if (!p) ckpt::fail(CKPT_E_INVALID, std::string(what) + ": null pointer");
-}
-
-// the argument checks train_step and step_graph_create share
-void check_step_args(const char *fn, const ckpt_net *net, const void *params, const void *grads,
-                     const ckpt_batch *batch, const ckpt_plan *plan, const void *workspace) {
-  const std::string f(fn);
-  need(net, (f + "(net)").c_str());
-  need(params, (f + "(params)").c_str());
-  need(grads, (f + "(grads)").c_str());
-  need(batch, (f + "(batch)").c_str());
-  need(batch->input, (f + "(batch.input)").c_str());
-  need(batch->target, (f + "(batch.target)").c_str());
-  need(plan, (f + "(plan)").c_str());
-  need(workspace, (f + "(workspace)").c_str());
-  if (reinterpret_cast<uintptr_t>(workspace) & 255)
-    ckpt::fail(CKPT_E_INVALID, f + ": workspace must be 256-byte aligned");
-  if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
-    ckpt::fail(CKPT_E_INVALID, f + ": params and grads must be 256-byte aligned");
-  if (plan->p.n != net->net->n)
-    ckpt::fail(CKPT_E_MISMATCH, f + ": plan n differs from the net's unit count");
-}
-}  // namespace
-
 extern "C" {
 
 const char *ckpt_last_error(void) { return g_err.c_str(); }
@@ -97,8 +30,8 @@ const char *ckpt_last_error(void) { return g_err.c_str(); }
 int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *cut_bytes,
                      uint64_t budget, int32_t mode, const int32_t *user_cuts, int32_t n_user_cuts,
                      int32_t flags, ckpt_plan **out) {
-  return guarded([&] {
-    need(out, "plan_checkpoints(out)");
+  return ckpt::guarded([&] {
+    ckpt::need(out, "plan_checkpoints(out)");
     *out = nullptr;
     auto p = std::make_unique<ckpt_plan>();
     p->p = ckpt::make_plan(n_layers, layer_bytes, cut_bytes, budget, mode, user_cuts,
@@ -109,8 +42,8 @@ int plan_checkpoints(int32_t n_layers, const uint64_t *layer_bytes, const uint64
 
 int plan_info(const ckpt_plan *plan, int32_t *mode, int32_t *n_layers, int32_t *n_cuts,
               uint64_t *x, uint64_t *y, uint64_t *extra) {
-  return guarded([&] {
-    need(plan, "plan_info");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "plan_info");
     if (mode) *mode = plan->p.mode;
     if (n_layers) *n_layers = plan->p.n;
     if (n_cuts) *n_cuts = int32_t(plan->p.cuts.size());
@@ -121,8 +54,8 @@ int plan_info(const ckpt_plan *plan, int32_t *mode, int32_t *n_layers, int32_t *
 }
 
 int plan_cuts(const ckpt_plan *plan, int32_t *cuts, int32_t cap, int32_t *n_cuts) {
-  return guarded([&] {
-    need(plan, "plan_cuts");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "plan_cuts");
     const auto &c = plan->p.cuts;
     if (n_cuts) *n_cuts = int32_t(c.size());
     if (cuts && cap > 0) std::memcpy(cuts, c.data(), sizeof(int32_t) * std::min<size_t>(size_t(cap), c.size()));
@@ -130,8 +63,8 @@ int plan_cuts(const ckpt_plan *plan, int32_t *cuts, int32_t cap, int32_t *n_cuts
 }
 
 int plan_serialize(const ckpt_plan *plan, uint8_t *buf, uint64_t cap, uint64_t *len) {
-  return guarded([&] {
-    need(plan, "plan_serialize");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "plan_serialize");
     auto v = ckpt::serialize(plan->p);
     if (len) *len = v.size();
     if (buf) {
@@ -147,15 +80,15 @@ int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *c
                 const uint64_t *b, const uint64_t *a, const uint64_t *q, uint64_t grad_slot,
                 uint64_t grad_extra, int32_t flags, ckpt_plan **out, uint64_t *budget,
                 uint64_t *peak) {
-  return guarded([&] {
-    need(out, "plan_search(out)");
+  return ckpt::guarded([&] {
+    ckpt::need(out, "plan_search(out)");
     *out = nullptr;
     if (n_layers <= 0) ckpt::fail(CKPT_E_INVALID, "plan_search: n_layers must be positive");
-    need(layer_bytes, "plan_search(layer_bytes)");
-    need(cut_bytes, "plan_search(cut_bytes)");
-    need(b, "plan_search(b)");
-    need(a, "plan_search(a)");
-    need(q, "plan_search(q)");
+    ckpt::need(layer_bytes, "plan_search(layer_bytes)");
+    ckpt::need(cut_bytes, "plan_search(cut_bytes)");
+    ckpt::need(b, "plan_search(b)");
+    ckpt::need(a, "plan_search(a)");
+    ckpt::need(q, "plan_search(q)");
     const size_t n = size_t(n_layers);
     std::vector<uint64_t> bv(b, b + n + 1), av(a, a + n), qv(q, q + n);
     auto p = std::make_unique<ckpt_plan>();
@@ -168,8 +101,8 @@ int plan_search(int32_t n_layers, const uint64_t *layer_bytes, const uint64_t *c
 int graph_plan(int32_t n_nodes, const int32_t *pred_ptr, const int32_t *pred_idx,
                const uint64_t *out_bytes, const int32_t *flags, const int32_t *mirror,
                int32_t strategy, ckpt_graph_plan **out) {
-  return guarded([&] {
-    need(out, "graph_plan(out)");
+  return ckpt::guarded([&] {
+    ckpt::need(out, "graph_plan(out)");
     *out = nullptr;
     auto p = std::make_unique<ckpt_graph_plan>();
     p->p = ckpt::make_graph_plan(n_nodes, pred_ptr, pred_idx, out_bytes, flags, mirror, strategy);
@@ -179,8 +112,8 @@ int graph_plan(int32_t n_nodes, const int32_t *pred_ptr, const int32_t *pred_idx
 
 int graph_plan_info(const ckpt_graph_plan *plan, int32_t *n_exec, int32_t *n_mirror,
                     int32_t *n_blocks, uint64_t *peak_bytes) {
-  return guarded([&] {
-    need(plan, "graph_plan_info");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "graph_plan_info");
     if (n_exec) *n_exec = int32_t(plan->p.order.size());
     if (n_mirror) *n_mirror = plan->p.n_mirror;
     if (n_blocks) *n_blocks = int32_t(plan->p.tag_bytes.size());
@@ -190,8 +123,8 @@ int graph_plan_info(const ckpt_graph_plan *plan, int32_t *n_exec, int32_t *n_mir
 
 int graph_plan_schedule(const ckpt_graph_plan *plan, int32_t *kind, int32_t *of, int32_t *block,
                         int32_t cap, int32_t *n_exec) {
-  return guarded([&] {
-    need(plan, "graph_plan_schedule");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "graph_plan_schedule");
     if (cap < 0) ckpt::fail(CKPT_E_INVALID, "graph_plan_schedule: negative cap");
     const auto &p = plan->p;
     if (n_exec) *n_exec = int32_t(p.order.size());
@@ -206,8 +139,8 @@ int graph_plan_schedule(const ckpt_graph_plan *plan, int32_t *kind, int32_t *of,
 }
 
 int graph_plan_blocks(const ckpt_graph_plan *plan, uint64_t *bytes, int32_t cap, int32_t *n_blocks) {
-  return guarded([&] {
-    need(plan, "graph_plan_blocks");
+  return ckpt::guarded([&] {
+    ckpt::need(plan, "graph_plan_blocks");
     if (cap < 0) ckpt::fail(CKPT_E_INVALID, "graph_plan_blocks: negative cap");
     const auto &tb = plan->p.tag_bytes;
     if (n_blocks) *n_blocks = int32_t(tb.size());
@@ -219,9 +152,9 @@ int graph_plan_blocks(const ckpt_graph_plan *plan, uint64_t *bytes, int32_t cap,
 void graph_plan_free(ckpt_graph_plan *plan) { delete plan; }
 
 int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
-  return guarded([&] {
-    need(desc, "net_create(desc)");
-    need(out, "net_create(out)");
+  return ckpt::guarded([&] {
+    ckpt::need(desc, "net_create(desc)");
+    ckpt::need(out, "net_create(out)");
     *out = nullptr;
     for (int32_t r : desc->reserved)
       if (r != 0) ckpt::fail(CKPT_E_INVALID, "net_create: reserved fields must be zero");
@@ -249,16 +182,16 @@ int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
 void net_destroy(ckpt_net *net) { delete net; }
 
 int net_units(const ckpt_net *net, int32_t *n) {
-  return guarded([&] {
-    need(net, "net_units");
-    need(n, "net_units(n)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_units");
+    ckpt::need(n, "net_units(n)");
     *n = net->net->n;
   });
 }
 
 int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q) {
-  return guarded([&] {
-    need(net, "net_unit_sizes");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_unit_sizes");
     const auto &N = *net->net;
     if (b) std::memcpy(b, N.b.data(), N.b.size() * 8);
     if (a) std::memcpy(a, N.a.data(), N.a.size() * 8);
@@ -267,16 +200,16 @@ int net_unit_sizes(const ckpt_net *net, uint64_t *b, uint64_t *a, uint64_t *q) {
 }
 
 int net_grad_bytes(const ckpt_net *net, uint64_t *slot, uint64_t *extra) {
-  return guarded([&] {
-    need(net, "net_grad_bytes");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_grad_bytes");
     if (slot) *slot = net->net->slot_bytes();
     if (extra) *extra = net->net->grad_extra;
   });
 }
 
 int net_layer_sizes(const ckpt_net *net, uint64_t *layer_bytes, uint64_t *cut_bytes) {
-  return guarded([&] {
-    need(net, "net_layer_sizes");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_layer_sizes");
     const auto &N = *net->net;
     for (int32_t i = 0; i < N.n; ++i) {
       if (layer_bytes) layer_bytes[i] = N.a[size_t(i)] + N.b[size_t(i) + 1];
@@ -286,25 +219,25 @@ int net_layer_sizes(const ckpt_net *net, uint64_t *layer_bytes, uint64_t *cut_by
 }
 
 int net_param_bytes(const ckpt_net *net, uint64_t *bytes) {
-  return guarded([&] {
-    need(net, "net_param_bytes");
-    need(bytes, "net_param_bytes(bytes)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_param_bytes");
+    ckpt::need(bytes, "net_param_bytes(bytes)");
     *bytes = net->net->param_bytes;
   });
 }
 
 int net_param_count(const ckpt_net *net, int32_t *count) {
-  return guarded([&] {
-    need(net, "net_param_count");
-    need(count, "net_param_count(count)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_param_count");
+    ckpt::need(count, "net_param_count(count)");
     *count = int32_t(net->net->params.size());
   });
 }
 
 int net_param_info(const ckpt_net *net, int32_t k, char *name, int32_t cap, uint64_t *offset,
                    uint64_t *numel) {
-  return guarded([&] {
-    need(net, "net_param_info");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_param_info");
     const auto &ps = net->net->params;
     if (k < 0 || size_t(k) >= ps.size()) ckpt::fail(CKPT_E_INVALID, "net_param_info: bad index");
     const auto &t = ps[size_t(k)];
@@ -320,9 +253,9 @@ int net_param_info(const ckpt_net *net, int32_t k, char *name, int32_t cap, uint
 
 int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt_b, uint64_t *arena,
                     uint64_t *grad, uint64_t *peak) {
-  return guarded([&] {
-    need(net, "plan_accounting(net)");
-    need(plan, "plan_accounting(plan)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "plan_accounting(net)");
+    ckpt::need(plan, "plan_accounting(plan)");
     if (plan->p.n != net->net->n)
       ckpt::fail(CKPT_E_MISMATCH, "plan_accounting: plan n differs from the net's unit count");
     auto acc = net->net->accounting(plan->p);
@@ -334,10 +267,10 @@ int plan_accounting(const ckpt_net *net, const ckpt_plan *plan, uint64_t *ckpt_b
 }
 
 int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *bytes) {
-  return guarded([&] {
-    need(net, "net_workspace_bytes(net)");
-    need(plan, "net_workspace_bytes(plan)");
-    need(bytes, "net_workspace_bytes(bytes)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_workspace_bytes(net)");
+    ckpt::need(plan, "net_workspace_bytes(plan)");
+    ckpt::need(bytes, "net_workspace_bytes(bytes)");
     if (plan->p.n != net->net->n)
       ckpt::fail(CKPT_E_MISMATCH, "net_workspace_bytes: plan n differs from the net's unit count");
     auto acc = net->net->accounting(plan->p);
@@ -348,8 +281,8 @@ int net_workspace_bytes(const ckpt_net *net, const ckpt_plan *plan, uint64_t *by
 int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch *batch,
                const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes, void *stream,
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats) {
-  return guarded([&] {
-    check_step_args("train_step", net, params, grads, batch, plan, workspace);
+  return ckpt::guarded([&] {
+    ckpt::check_step_args("train_step", net, params, grads, batch, plan, workspace);
     ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
                          *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
                          static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
@@ -360,10 +293,10 @@ int step_graph_create(ckpt_net *net, const void *params, void *grads, const ckpt
                       const ckpt_plan *plan, void *workspace, uint64_t workspace_bytes,
                       void *stream, float *loss_dev, ckpt_step_graph **out,
                       ckpt_step_stats *stats) {
-  return guarded([&] {
-    need(out, "step_graph_create(out)");
+  return ckpt::guarded([&] {
+    ckpt::need(out, "step_graph_create(out)");
     *out = nullptr;
-    check_step_args("step_graph_create", net, params, grads, batch, plan, workspace);
+    ckpt::check_step_args("step_graph_create", net, params, grads, batch, plan, workspace);
     if (!stream)
       ckpt::fail(CKPT_E_INVALID, "step_graph_create: capture needs a stream other than the default one");
     if (net->net->timer.enabled)
@@ -398,8 +331,8 @@ int step_graph_create(ckpt_net *net, const void *params, void *grads, const ckpt
 }
 
 int step_graph_launch(ckpt_step_graph *graph, void *stream) {
-  return guarded([&] {
-    need(graph, "step_graph_launch(graph)");
+  return ckpt::guarded([&] {
+    ckpt::need(graph, "step_graph_launch(graph)");
     const hipError_t e = hipGraphLaunch(graph->exec, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) ckpt::fail(CKPT_E_HIP, std::string("step_graph_launch: ") + hipGetErrorString(e));
   });
@@ -410,8 +343,8 @@ void step_graph_free(ckpt_step_graph *graph) { delete graph; }
 int net_node_graph(const ckpt_net *net, int32_t *n_nodes, int32_t *n_edges, int32_t *pred_ptr,
                    int32_t *pred_idx, uint64_t *out_bytes, int32_t *flags, int32_t cap_nodes,
                    int32_t cap_edges) {
-  return guarded([&] {
-    need(net, "net_node_graph");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_node_graph");
     ckpt::Net::NodeGraph g;
     if (!net->net->node_graph(g))
       ckpt::fail(CKPT_E_UNSUPPORTED, "net_node_graph: this net has no node graph");
@@ -429,10 +362,10 @@ int net_node_graph(const ckpt_net *net, int32_t *n_nodes, int32_t *n_edges, int3
 }
 
 int graph_workspace_bytes(const ckpt_net *net, const ckpt_graph_plan *plan, uint64_t *bytes) {
-  return guarded([&] {
-    need(net, "graph_workspace_bytes(net)");
-    need(plan, "graph_workspace_bytes(plan)");
-    need(bytes, "graph_workspace_bytes(bytes)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "graph_workspace_bytes(net)");
+    ckpt::need(plan, "graph_workspace_bytes(plan)");
+    ckpt::need(bytes, "graph_workspace_bytes(bytes)");
     *bytes = ckpt::graph_workspace_bytes(*net->net, plan->p);
   });
 }
@@ -441,15 +374,15 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
                      const ckpt_graph_plan *plan, void *workspace, uint64_t workspace_bytes,
                      void *stream, float *loss_dev, float *loss_host, uint64_t *peak,
                      ckpt_step_stats *stats) {
-  return guarded([&] {
-    need(net, "train_step_graph(net)");
-    need(params, "train_step_graph(params)");
-    need(grads, "train_step_graph(grads)");
-    need(batch, "train_step_graph(batch)");
-    need(batch->input, "train_step_graph(batch.input)");
-    need(batch->target, "train_step_graph(batch.target)");
-    need(plan, "train_step_graph(plan)");
-    need(workspace, "train_step_graph(workspace)");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "train_step_graph(net)");
+    ckpt::need(params, "train_step_graph(params)");
+    ckpt::need(grads, "train_step_graph(grads)");
+    ckpt::need(batch, "train_step_graph(batch)");
+    ckpt::need(batch->input, "train_step_graph(batch.input)");
+    ckpt::need(batch->target, "train_step_graph(batch.target)");
+    ckpt::need(plan, "train_step_graph(plan)");
+    ckpt::need(workspace, "train_step_graph(workspace)");
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
       ckpt::fail(CKPT_E_INVALID, "train_step_graph: workspace must be 256-byte aligned");
     if ((reinterpret_cast<uintptr_t>(params) & 255) || (reinterpret_cast<uintptr_t>(grads) & 255))
@@ -461,8 +394,8 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
 }
 
 int net_timing_enable(ckpt_net *net, int32_t enable) {
-  return guarded([&] {
-    need(net, "net_timing_enable");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_timing_enable");
     auto &t = net->net->timer;
     t.reset();
     t.enabled = enable != 0;
@@ -471,8 +404,8 @@ int net_timing_enable(ckpt_net *net, int32_t enable) {
 
 int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops, double *bytes,
                     char *name, int32_t cap) {
-  return guarded([&] {
-    need(net, "net_timing_read");
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_timing_read");
     auto &t = net->net->timer;
     t.harvest();
     if (launches) *launches = t.launches;

@@ -418,3 +418,20 @@ def test_operator_block_counts():
     rb, cb = K.op_gemm_bf16_blocks(2 * 56 * 56, 64)
     assert rb >= 1 and cb >= 1 and rb * 256 >= 2 * 56 * 56 // 64
     assert K.op_bnb_partial_blocks(6272, 64) >= 1
+
+
+def test_static_step_rejects_workspace_beyond_its_scratch():
+    """A plan whose workspace exceeds the static scratch is refused before
+    anything touches the GPU (host-side accounting only)."""
+    net = K.net_create(K.NET_MLP, 256, 1024, 1024)
+    lb, cb = net.layer_sizes()
+    plan = K.plan_checkpoints(lb, cb, 0, K.NONE)
+    assert net.workspace_bytes(plan) > K.STATIC_SCRATCH_BYTES
+    with pytest.raises(K.CkptError) as e:
+        K.train_step_static(net, FAKE, FAKE, FAKE, FAKE, plan)
+    assert e.value.code == K.E_WORKSPACE
+    assert b"static scratch" in K._lib.ckpt_last_error()
+    small = K.plan_checkpoints(lb[:4], cb[:3] + [0], 0, K.NONE)   # 4 units: not this net's plan
+    with pytest.raises(K.CkptError) as e:
+        K.train_step_static(net, FAKE, FAKE, FAKE, FAKE, small)
+    assert e.value.code == K.E_MISMATCH

@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include "common.h"
+#include "kernel_args.h"
 #include "kernels.h"
 #include "launch.h"
 
@@ -34,20 +35,6 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
-struct ConvArgs {
-  const float *X;   // kernel input  [N, Hx, Wx, C]
-  const float *Wt;  // weights [Cout, 3, 3, Cin]
-  float *Y;         // kernel output [N, H, W, J]
-  int N, H, W;      // output dims
-  int Hx, Wx;       // input dims
-  int C, J;         // reduction / output channels
-  int R, rblk;      // output rows per workgroup, workgroups per image
-  const float *E0, *E1;  // epilogue operands (MASK: E0; SC: E0 = g, E1 = y)
-  int Eh, Ew, Ec;        // SC2: dims of g and y
-  double *stats;         // STATS: [2][J][gridDim.x] (sum v, sum v^2; channel-major)
-  const float *tst, *tg, *tb;  // optional bn_relu: FWD input / DGRAD MASK transform
-  float *rout;  // FWD, stride 1, with tst: the transformed input rows the workgroup owns
-};
 
 // bn_relu of four consecutive channels c..c+3 (C = channel count of the
 // statistics: st = mean[C] | rstd[C])
@@ -595,14 +582,6 @@ bool spec_dispatch(const ConvArgs &a, int mode, int s, int epi, hipStream_t st, 
 constexpr int WG_KC = 32;    // pixels per LDS chunk
 constexpr int WG_NB = 144;   // n columns per workgroup (9 tiles of 16)
 
-struct WgArgs {
-  const float *X;   // conv input [N, Hx, Wx, C]
-  const float *DY;  // conv output gradient [N, H, W, J]
-  float *part;      // [gridDim.x][J][9C]
-  int N, H, W, Hx, Wx, C, J, S;
-  int pix_per_blk;  // multiple of WG_KC
-  const float *tst, *tg, *tb;  // optional bn_relu of the input X
-};
 
 __device__ __forceinline__ int wg_as(int J) { return J + ((16 - J % 32) + 32) % 32; }  // == 16 mod 32
 

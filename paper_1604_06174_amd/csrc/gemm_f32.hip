@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include "common.h"
+#include "kernel_args.h"
 #include "kernels.h"
 #include "launch.h"
 
@@ -39,20 +40,6 @@ namespace {
 
 constexpr int PAD = 4;
 
-struct GemmArgs {
-  int M, N, K;
-  const float *A;
-  int lda;
-  const float *B;
-  int ldb;
-  float *C;
-  int ldc;
-  const float *D;  // ADD
-  int ldd;
-  const float *bias;  // MLPFWD
-  float *Z;           // MLPFWD
-  int ldz;
-};
 
 // 4 KB of zeros in device memory: an element outside its operand is loaded
 // from here (16 bytes per thread, spread over many cache lines), so no loaded

@@ -1,0 +1,130 @@
+"""Per-launch-kind table of the bf16 GEMM family from a rocprofv3 kernel trace.
+
+    python -m paper_1604_06174_amd.profile_table <run_kernel_trace.csv> <gemm launch log>
+
+The launch log lists every bf16 GEMM launch of one training step with its
+shape (tests/hostcheck/run.py --gemm-log <workload> <file> writes it from a
+host-only dry run of the same step); the trace gives each dispatch's kernel,
+grid and duration.  They are joined on (kernel, grid).  Per launch kind:
+launches per step, M x N x K, algorithmic flops (2 M N K) and bytes (each
+operand read once -- the gathered convolution input as the tensor it is --
+and the result written once, split-K partials not counted), the average
+duration over every traced dispatch of that kind, and the fraction of the
+kind's roofline time max(flops / 2.5 PFLOP/s, bytes / 8 TB/s) that duration
+reaches.  The family line weights every kind by its launches per step.
+"""
+from __future__ import annotations
+
+import csv
+import sys
+from collections import defaultdict
+
+MFMA_BF16 = 2.5e15
+HBM = 8.0e12
+EPI = {0: "STORE", 1: "ADD", 3: "BF16STATS", 4: "ADDMASK", 6: "BNBWD", 7: "ROWSOFTMAX"}
+FORM = {0: "dense", 1: "fwd-gather", 2: "dgrad-gather", 3: "wgrad-gather", 4: "weights", 5: "cat"}
+
+
+def read_log(path):
+    rows = []
+    with open(path) as f:
+        for ln in f:
+            v = ln.split()
+            name = v[0]
+            gx, gy, gz, M, N, K, kper, epi, ga, gb, H, W, Ho, Wo, R, S, cshift, lda = map(int, v[1:])
+            rows.append(dict(name=name, grid=(gx, gy, gz), M=M, N=N, K=K, epi=epi, ga=ga, gb=gb, H=H,
+                             W=W, Ho=Ho, Wo=Wo, R=R, S=S, C=(1 << cshift) if cshift > 0 else 0))
+    return rows
+
+
+def work(r):
+    """(flops, bytes) of one launch."""
+    M, N, K, C = r["M"], r["N"], r["K"], r["C"]
+    if r["ga"] == 1:
+        a = (M // (r["Ho"] * r["Wo"])) * r["H"] * r["W"] * C * 2
+    elif r["ga"] == 2:
+        a = (M // (r["H"] * r["W"])) * r["Ho"] * r["Wo"] * C * 2
+    else:
+        a = M * K * 2
+    if r["gb"] == 3:
+        b = (K // (r["Ho"] * r["Wo"])) * r["H"] * r["W"] * C * 2
+    else:
+        b = N * K * 2
+    mn = M * N
+    out = {3: 2 * mn, 6: 4 * mn + 2 * 2 * mn, 4: 4 * mn + 4 * mn + 2 * mn, 1: 8 * mn}.get(r["epi"], 4 * mn)
+    return 2.0 * M * N * K, float(a + b + out)
+
+
+def prefix(name):
+    """(BM, BN, WM, WN, AK, BK, rest): the instance's template arguments from a
+    mangled name, or the leading ones from a demangled name (rocprofv3 prints
+    some instances demangled, and its demangler garbles the __bf16 type that
+    follows BK, so those are told apart by their grid instead)."""
+    if name.startswith("_Z"):
+        v = name.split("k_gemm_bf16I", 1)[1]
+        parts = []
+        for tok in v.split("E")[:6]:
+            parts.append(tok.replace("Li", "").replace("Lb", ""))
+        return tuple(int(x) for x in parts[:4]) + (parts[4] == "1", parts[5] == "1"), name
+    inner = name.split("k_gemm_bf16<", 1)[1].split(",")
+    nums = [t.strip() for t in inner[:6]]
+    return tuple(int(x) for x in nums[:4]) + (nums[4] == "true", nums[5] == "true"), None
+
+
+def main(trace, log):
+    rows = read_log(log)
+    durs = defaultdict(list)
+    with open(trace) as f:
+        for d in csv.DictReader(f):
+            if "k_gemm_bf16" not in d["Kernel_Name"]:
+                continue
+            wg = int(d["Workgroup_Size_X"])
+            grid = (int(d["Grid_Size_X"]) // wg, int(d["Grid_Size_Y"]), int(d["Grid_Size_Z"]))
+            t = (int(d["End_Timestamp"]) - int(d["Start_Timestamp"])) * 1e-9
+            pre, mangled = prefix(d["Kernel_Name"])
+            durs[(mangled, grid) if mangled else (pre, grid)].append(t)
+    kinds = defaultdict(lambda: dict(n=0))
+    for r in rows:
+        k = (r["name"], r["grid"])
+        e = kinds[k]
+        e["n"] += 1
+        e["r"] = r
+    out = []
+    tot_t = tot_roof = tot_f = tot_b = 0.0
+    missing = 0
+    for k, e in kinds.items():
+        r = e["r"]
+        fl, by = work(r)
+        ds = durs.get(k) or durs.get((prefix(k[0])[0], k[1]))
+        if not ds:
+            missing += e["n"]
+            continue
+        t = sum(ds) / len(ds)
+        roof = max(fl / MFMA_BF16, by / HBM)
+        bound = "mfma" if fl / MFMA_BF16 >= by / HBM else "hbm"
+        out.append((e["n"] * t, r, e["n"], fl, by, t, roof, bound))
+        tot_t += e["n"] * t
+        tot_roof += e["n"] * roof
+        tot_f += e["n"] * fl
+        tot_b += e["n"] * by
+    out.sort(key=lambda x: -x[0])
+    print(f"| share | launches/step | tile x grid | epilogue | A / B | M x N x K | GFLOP | MB | avg us "
+          f"| bound | frac of roofline |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+    for tt, r, n, fl, by, t, roof, bound in out:
+        tile = r["name"].split("ILi")[1].split("E")[0].replace("ELi", "x") if "ILi" in r["name"] else "?"
+        print(f"| {100 * tt / tot_t:.1f}% | {n} | {tile} {r['grid'][0]}x{r['grid'][1]}x{r['grid'][2]} | "
+              f"{EPI.get(r['epi'], r['epi'])} | {FORM[r['ga']]} / {FORM[r['gb']]} | "
+              f"{r['M']} x {r['N']} x {r['K']} | {fl / 1e9:.2f} | {by / 1e6:.1f} | {t * 1e6:.2f} | {bound} | "
+              f"{roof / t:.3f} |")
+    n_all = sum(e["n"] for e in kinds.values())
+    print(f"\nfamily: {n_all} launches per step ({missing} without a traced dispatch), "
+          f"{tot_t * 1e3:.2f} ms of kernel time per step; algorithmic {tot_f / 1e12:.2f} TFLOP and "
+          f"{tot_b / 1e9:.2f} GB per step; roofline time {tot_roof * 1e3:.2f} ms = "
+          f"{tot_roof / tot_t:.3f} of the kernel time; {tot_f / tot_t / 1e12:.1f} TFLOP/s "
+          f"({tot_f / tot_t / MFMA_BF16:.3f} of bf16 peak), {tot_b / tot_t / 1e9:.0f} GB/s "
+          f"({tot_b / tot_t / HBM:.3f} of HBM)")
+
+
+if __name__ == "__main__":
+    main(sys.argv[1], sys.argv[2])

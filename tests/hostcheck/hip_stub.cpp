@@ -202,6 +202,21 @@ void parse(KernelInfo &k) {
 
 uint64_t rows_span(uint64_t rows, uint64_t ld, uint64_t cols) { return rows ? (rows - 1) * ld + cols : 0; }
 
+// HC_GEMM_LOG=<file>: one line per bf16 GEMM launch (mangled name, grid,
+// M, N, K, k per split, epilogue, A and B forms, gather geometry), for
+// attaching shapes to a profiler's per-dispatch records
+void log_gemm(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid, int epi, int ga, int gb) {
+  static FILE *f = [] {
+    const char *p = std::getenv("HC_GEMM_LOG");
+    return p ? std::fopen(p, "w") : nullptr;
+  }();
+  if (!f) return;
+  std::fprintf(f, "%s %u %u %u %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d\n", k.mangled.c_str(), grid.x,
+               grid.y, grid.z, a.M, a.N, a.K, a.kper, epi, ga, gb, a.H, a.W, a.Ho, a.Wo, a.R, a.S, a.cshift,
+               a.lda);
+  std::fflush(f);
+}
+
 // the whole extent of every operand of a bf16 GEMM launch
 void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   using namespace ckpt::gb;
@@ -214,6 +229,7 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   const int EPI = std::atoi(k.targs[7].c_str()), GA = std::atoi(k.targs[8].c_str()),
             GB = std::atoi(k.targs[9].c_str());
   const int BM = std::atoi(k.targs[0].c_str()), BN = std::atoi(k.targs[1].c_str());
+  log_gemm(k, a, grid, EPI, GA, GB);
   const uint64_t M = uint64_t(a.M), N = uint64_t(a.N), K = uint64_t(a.K);
   if (a.M <= 0 || a.N <= 0 || a.K < 0) error(k.pretty + ": non-positive M or N");
   if (grid.x != (N + BN - 1) / BN || grid.y != (M + BM - 1) / BM)

@@ -2,6 +2,7 @@
 preloaded; tests/test_hostcheck.py does that).
 
     LD_PRELOAD=<asan runtime> python tests/hostcheck/run.py [--quick | --plant]
+    LD_PRELOAD=<asan runtime> python tests/hostcheck/run.py --gemm-log resnet1000 <file>
 
 1. Planner, budget search and gradient-graph fuzzing through the instrumented
    library, each result compared with the oracle (as the CPU ABI tests do on
@@ -385,6 +386,17 @@ def dry_runs(quick):
 
 def main():
     quick = "--quick" in sys.argv
+    if "--gemm-log" in sys.argv:
+        # --gemm-log <workload> <file>: the workload's step (its default plan)
+        # with every bf16 GEMM launch written to <file>
+        i = sys.argv.index("--gemm-log")
+        name, path = sys.argv[i + 1], sys.argv[i + 2]
+        os.environ["HC_GEMM_LOG"] = path
+        cfg = dict(synth.WORKLOADS[name], name=name)
+        plan = {"greedy": (PL.GREEDY, "tenth", 0), "sqrt": (PL.SQRT, int(cfg.get("stride", 0)), 0),
+                "recursive": (PL.RECURSIVE, 0, 0)}[cfg["plan"]]
+        dry_step(cfg, [plan])
+        sys.exit(0 if not FAILURES and counters()[1] == 0 else 1)
     if SHORT:
         # a 1x1-convolution product [6272, 256] whose output buffer is one
         # float short: the GEMM's whole-extent check must see it

@@ -57,6 +57,13 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 namespace gb {
 
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+// do three direct-loop stages of a BM x BN tile (plus an epilogue scratch
+// larger than one A stage) leave room for two workgroups per compute unit?
+constexpr bool direct_three_stages(int BM, int BN, int epi_scratch) {
+  return 3 * (BM + BN) * 64 * 2 + (epi_scratch <= BM * 64 * 2 ? 0 : epi_scratch) <= 80 * 1024;
+}
+
 constexpr int KS = 64;      // k per LDS slice: two 32-deep MFMA steps
 constexpr int KP = KS + 8;  // padded row (bf16 elements): 144-byte rows
 
@@ -203,6 +210,33 @@ __device__ __forceinline__ u32x4 gatherA(const Args &p, const __bf16 *A, const R
   }
 }
 
+// The same gathers as addresses for the direct global -> LDS loads: the
+// chunk's source, or the thread's zero slot when it lies outside.
+__device__ __forceinline__ const void *src16(const void *p, bool ok) {
+  return ok ? p : static_cast<const void *>(g_zero_area + 4 * (threadIdx.x & 255));
+}
+
+template <int GA>
+__device__ __forceinline__ const void *gatherA_src(const Args &p, const __bf16 *A, const RowPix &rp, int k,
+                                                   int kend) {
+  const int C = 1 << p.cshift;
+  const int tap = k >> p.cshift, ch = k & (C - 1);
+  int kh, kw;
+  tap_hw(tap, p, kh, kw);
+  if constexpr (GA == GA_FWD) {
+    const int hi = rp.y * p.S + kh - p.P, wi = rp.x * p.S + kw - p.P;
+    const bool ok = rp.ok & (k < kend) & (hi >= 0) & (hi < p.H) & (wi >= 0) & (wi < p.W);
+    return src16(A + ((size_t(rp.img) * p.H + hi) * p.W + wi) * C + ch, ok);
+  } else {
+    const int t = rp.y + p.P - kh, u = rp.x + p.P - kw;
+    const int sm = p.S - 1;
+    const int ho = t >> sm, wo = u >> sm;
+    const bool ok = rp.ok & (k < kend) & (t >= 0) & (u >= 0) & !(t & sm) & !(u & sm) & (ho < p.Ho) &
+                    (wo < p.Wo);
+    return src16(A + ((size_t(rp.img) * p.Ho + ho) * p.Wo + wo) * C + ch, ok);
+  }
+}
+
 // Per-chunk column state of GB_WGRAD: the tap and channel of column n.
 struct ColTap {
   int kh, kw, ch;
@@ -229,13 +263,44 @@ __device__ __forceinline__ u32x4 gatherB_wgrad(const Args &p, const ColTap &ct, 
   return masked16(p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch, ok);
 }
 
+__device__ __forceinline__ const void *gatherB_wgrad_src(const Args &p, const ColTap &ct, int k, int kend) {
+  const int t = divq(k, p.Wo, p.inv_wo);
+  const int wo = k - t * p.Wo;
+  const int img = divq(t, p.Ho, p.inv_ho);
+  const int ho = t - img * p.Ho;
+  const int hi = ho * p.S + ct.kh - p.P, wi = wo * p.S + ct.kw - p.P;
+  const bool ok = ct.ok & (k < kend) & (hi >= 0) & (hi < p.H) & (wi >= 0) & (wi < p.W);
+  return src16(p.B + ((size_t(img) * p.H + hi) * p.W + wi) * (size_t(1) << p.cshift) + ct.ch, ok);
+}
+
+__device__ __forceinline__ const void *gatherB_wdgrad_src(const Args &p, int k, int n, int kend) {
+  const int Co = 1 << p.cshift;
+  const int tap = k >> p.cshift, co = k & (Co - 1);
+  return src16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, (k < kend) & (n < p.N));
+}
+
+// 16 bytes from global memory straight into LDS: lane i of the wavefront
+// writes lds_wave + 16 i (lds_wave must be the same for the whole wavefront).
+typedef __attribute__((address_space(3))) void lds_void_t;
+__device__ __forceinline__ void load_lds16(const void *src, unsigned char *lds_wave) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_t *)lds_wave, 16, 0, 0);
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations
+// of this wavefront are outstanding (the other counters left alone)
+constexpr int vmcnt_le(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+
 __device__ __forceinline__ u32x4 gatherB_wdgrad(const Args &p, int k, int n, int kend) {
   const int Co = 1 << p.cshift;
   const int tap = k >> p.cshift, co = k & (Co - 1);
   return masked16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, (k < kend) & (n < p.N));
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB, bool SAFE>
+// DEEP (direct loop only): three LDS stages even where two workgroups would
+// then not fit a compute unit (for grids with no more tiles than compute
+// units, where a second workgroup per unit would not exist anyway)
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB, bool SAFE,
+          bool DEEP = false>
 __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   constexpr int TM = BM / WM / 16, TN = BN / WN / 16;  // 16x16 tiles per wavefront
   static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "wave grid");
@@ -244,21 +309,25 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   constexpr int CHA = BM * KS / 8, CHB = BN * KS / 8;  // 8-element chunks per slice
   constexpr int PA = (CHA + 255) / 256, PB = (CHB + 255) / 256;
   constexpr int WC = BN / WN;                           // columns per wavefront
-  constexpr int SP = WC + 4;                            // staging row pitch (floats)
-  // LDS operand tiles, double-buffered.  A k-contiguous operand is stored
-  // [buf][row][k] (pitch KP); a k-major one is stored as it arrives,
-  // [buf][k][row] (pitch rows + 16), and read back through the transposing
-  // LDS read (two 8-byte reads give a lane its 8 consecutive k).
-  constexpr int PA_K = BM + 16, PB_K = BN + 16;
-  constexpr int SZA = AK ? 2 * BM * KP * 2 : 2 * KS * PA_K * 2;
-  constexpr int SZB = BK ? 2 * BN * KP * 2 : 2 * KS * PB_K * 2;
-  __shared__ __align__(16) unsigned char smA[SZA];
-  __shared__ __align__(16) unsigned char smB[SZB];
-  static_assert(EPI != GEMM_EPI_BF16STATS || WM * 4 * 2 * BN * 8 <= SZA, "stats scratch");
-  static_assert(EPI != GEMM_EPI_BNBWD || WM * (64 / (WC / 4)) * 2 * BN * 8 <= SZA, "bnbwd scratch");
+  constexpr bool DIRECT = SAFE && std::is_same<TA, __bf16>::value;
+  // staging row pitch (floats): padded for the register-staged loop; unpadded
+  // for the direct loop, whose first stage then holds the staging rows
+  constexpr int SP = DIRECT ? WC : WC + 4;
+  // Two main loops (chosen at compile time):
+  // * direct (aligned bf16 operands): every 16-byte chunk goes from global
+  //   memory straight into LDS (global_load_lds_dwordx4) into a two- or
+  //   three-stage ring, one LDS object per stage and operand so that the compiler knows
+  //   which in-flight loads an LDS read depends on; layouts are unpadded and
+  //   XOR-swizzled so that the MFMA operand reads are free of bank conflicts;
+  // * register-staged (an fp32 A, or rows whose extent is not a multiple of
+  //   8 elements): chunks are loaded into registers two slices ahead and
+  //   written to a double-buffered padded LDS tile.
+  // epilogue scratch: staging rows, and the column sums of BF16STATS / BNBWD
+  constexpr int EPI_SCR = cmax(4 * 16 * SP * 4,
+                               cmax(EPI == GEMM_EPI_BF16STATS ? WM * 4 * 2 * BN * 8 : 0,
+                                    EPI == GEMM_EPI_BNBWD ? WM * (64 / (WC / 4)) * 2 * BN * 8 : 0));
   // ROWSOFTMAX: each wavefront column's (max, sum of exp) per row of the tile
   __shared__ float rsm[EPI == GEMM_EPI_ROWSOFTMAX ? WN * BM * 2 : 1];
-  static_assert(4 * 16 * SP * 4 <= SZA, "epilogue staging");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, q = lane >> 4;
@@ -302,147 +371,328 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     }
   }
 
-  // Every thread loads its chunks unconditionally (threads past a tile's
-  // chunk count load a duplicate and skip the LDS store), so the load
-  // counters are static and the loads stay in flight across the MFMAs.
-  auto gload = [&](u32x4 (&ra)[PA], u32x4 (&rb)[PB], int k0) {
-#pragma unroll
-    for (int c = 0; c < PA; ++c) {
-      const int e = min(tid + c * 256, CHA - 1);
-      if (AK) {  // chunk = 8 k of one m
-        const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-        if constexpr (GA == GA_CAT) {  // k < K1 from A, the rest from A2 (no branch)
-          const int kk = k0 + kc, m = m0 + mr;
-          const bool second = kk >= p.K1;
-          const __bf16 *base = second ? p.A2 : reinterpret_cast<const __bf16 *>(A);
-          const size_t off = size_t(m) * (second ? p.lda2 : p.lda) + (second ? kk - p.K1 : kk);
-          ra[c] = masked16(base + off, (m < p.M) & (kk < kend));
-        } else if constexpr (GA != G_DENSE)
-          ra[c] = gatherA<GA>(p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
-        else
-          ra[c] = ld8<SAFE, TA>(A, m0 + mr, k0 + kc, p.M, kend, p.lda);
-      } else {   // chunk = 8 m of one k
-        const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
-        ra[c] = ld8<SAFE, TA>(A, k0 + kr, m0 + mc, kend, p.M, p.lda);
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < PB; ++c) {
-      const int e = min(tid + c * 256, CHB - 1);
-      if (BK) {
-        const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-        rb[c] = ld8<SAFE, __bf16>(p.B, n0 + nr, k0 + kc, p.N, kend, p.ldb);
-      } else {
-        const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
-        if constexpr (GB == GB_WGRAD)
-          rb[c] = gatherB_wgrad(p, ctap[c], k0 + kr, kend);
-        else if constexpr (GB == GB_WDGRAD)
-          rb[c] = gatherB_wdgrad(p, k0 + kr, n0 + nc, kend);
-        else
-          rb[c] = ld8<SAFE, __bf16>(p.B, k0 + kr, n0 + nc, kend, p.N, p.ldb);
-      }
-    }
-  };
-  // k-contiguous chunks go to LDS as one 16-byte store; the others are
-  // transposed into eight 2-byte stores.
-  auto sstore = [&](const u32x4 (&ra)[PA], const u32x4 (&rb)[PB], int buf) {
-#pragma unroll
-    for (int c = 0; c < PA; ++c) {
-      const int e = tid + c * 256;
-      if (CHA % 256 == 0 || e < CHA) {
-        if (AK) {
-          const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          *reinterpret_cast<u32x4 *>(smA + ((buf * BM + mr) * KP + kc) * 2) = ra[c];
-        } else {
-          const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
-          *reinterpret_cast<u32x4 *>(smA + ((buf * KS + kr) * PA_K + mc) * 2) = ra[c];
-        }
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < PB; ++c) {
-      const int e = tid + c * 256;
-      if (CHB % 256 == 0 || e < CHB) {
-        if (BK) {
-          const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
-          *reinterpret_cast<u32x4 *>(smB + ((buf * BN + nr) * KP + kc) * 2) = rb[c];
-        } else {
-          const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
-          *reinterpret_cast<u32x4 *>(smB + ((buf * KS + kr) * PB_K + nc) * 2) = rb[c];
-        }
-      }
-    }
-  };
-
   floatx4 acc[TM][TN];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // one slice: KS / 32 MFMA k-steps; step s reads k 32 s + 8 q .. + 7
-  auto compute = [&](int buf) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ks += 32) {
-      bf16x8 av[TM], bv[TN];
-#pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        if constexpr (AK)
-          av[a] = *reinterpret_cast<const bf16x8 *>(smA + ((buf * BM + wm + a * 16 + i16) * KP + ks + 8 * q) * 2);
-        else
-          av[a] = tr_operand(
-              smA + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PA_K + wm + a * 16 + 4 * (i16 & 3)) * 2,
-              4 * PA_K * 2);
-      }
-#pragma unroll
-      for (int b = 0; b < TN; ++b) {
-        if constexpr (BK)
-          bv[b] = *reinterpret_cast<const bf16x8 *>(smB + ((buf * BN + wn + b * 16 + i16) * KP + ks + 8 * q) * 2);
-        else
-          bv[b] = tr_operand(
-              smB + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PB_K + wn + b * 16 + 4 * (i16 & 3)) * 2,
-              4 * PB_K * 2);
-      }
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-#pragma unroll
-        for (int b = 0; b < TN; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
-    }
-  };
-
-  // Two register stages: the loads of slice kt + 2 are issued right after
-  // slice kt is stored to LDS, so each load has two slices of MFMA work to
-  // arrive.  Slice kt is stored to LDS buffer kt & 1.  The loop body has no
-  // branches (a branch there makes the compiler wait for every outstanding
-  // load at each iteration): it runs while two more slices follow, and the
-  // last one or two slices are multiplied after it.
   const int nk = kend > kbeg ? (kend - kbeg + KS - 1) / KS : 0;
   // k origin of slice s; a slice past the range re-reads the last one (real,
   // spread-out addresses; it is never multiplied)
   auto kslice = [&](int s) { return kbeg + max(0, min(s, nk - 1)) * KS; };
-  u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
-  gload(ra0, rb0, kslice(0));
-  gload(ra1, rb1, kslice(1));
-  int kt = 0;
-  for (; kt + 2 < nk; kt += 2) {  // no branches in the body (see above)
-    sstore(ra0, rb0, 0);
+  unsigned char *scr;  // epilogue scratch (LDS)
+
+  if constexpr (DIRECT) {
+    // Stage layouts (16-byte chunks, chunk e of a slice at byte 16 e):
+    //   k-contiguous operand: [row][8 chunks of 8 k], the chunk of logical
+    //     k-group g stored in slot g ^ (row & 7);
+    //   k-major operand: [k][rows / 8 chunks of 8 rows], the chunk of
+    //     logical row-group g stored in slot g ^ (2 (k & 3) mod chunks per
+    //     row).
+    constexpr int SZA1 = BM * KS * 2, SZB1 = BN * KS * 2;
+    // three stages when two workgroups still fit in a compute unit's 160 KB
+    // of LDS with them (or DEEP), else two (latency is then hidden by the
+    // other workgroup)
+    constexpr int NS = (DEEP || direct_three_stages(BM, BN, EPI_SCR)) ? 3 : 2;
+    __shared__ __align__(1024) unsigned char sa0[SZA1], sa1[SZA1], sa2[NS == 3 ? SZA1 : 1];
+    __shared__ __align__(1024) unsigned char sb0[SZB1], sb1[SZB1], sb2[NS == 3 ? SZB1 : 1];
+    __shared__ __align__(16) unsigned char sepi[EPI_SCR <= SZA1 ? 1 : EPI_SCR];
+    if constexpr (EPI_SCR <= SZA1) scr = sa0;
+    else scr = sepi;
+    // GB_WGRAD: the tap and channel of each chunk's (swizzled) column, fixed
+    // for the whole k loop (the swizzle depends on the chunk's row in the
+    // slice, not on the slice)
+    ColTap ctapd[GB == GB_WGRAD ? PB : 1];
+    if constexpr (GB == GB_WGRAD && !BK) {
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        constexpr int RC = BN / 8;
+        const int e = c * 256 + tid, kr = e / RC;
+        ctapd[c] = col_tap(p, n0 + ((e % RC) ^ ((2 * (kr & 3)) & (RC - 1))) * 8);
+      }
+    }
+
+    // chunk c*256 + tid of slice s into the stage arrays la, lb
+    auto issue = [&](int s, unsigned char *la, unsigned char *lb) {
+      const int k0 = kslice(s);
+#pragma unroll
+      for (int c = 0; c < PA; ++c) {
+        const int e = c * 256 + tid;
+        const void *src;
+        if (AK) {
+          const int mr = e >> 3, kc = ((e & 7) ^ (mr & 7)) * 8;
+          if constexpr (GA == GA_CAT) {
+            const int kk = k0 + kc, m = m0 + mr;
+            const bool second = kk >= p.K1;
+            const __bf16 *base = second ? p.A2 : reinterpret_cast<const __bf16 *>(A);
+            const size_t off = size_t(m) * (second ? p.lda2 : p.lda) + (second ? kk - p.K1 : kk);
+            src = src16(base + off, (m < p.M) & (kk < kend));
+          } else if constexpr (GA != G_DENSE) {
+            src = gatherA_src<GA>(p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
+          } else {
+            const int m = m0 + mr, kk = k0 + kc;
+            src = src16(A + size_t(m) * p.lda + kk, (m < p.M) & (kk < kend));
+          }
+        } else {
+          constexpr int RC = BM / 8;  // chunks per k row
+          const int kr = e / RC, mc = ((e % RC) ^ ((2 * (kr & 3)) & (RC - 1))) * 8;
+          const int kk = k0 + kr, m = m0 + mc;
+          src = src16(A + size_t(kk) * p.lda + m, (kk < kend) & (m < p.M));
+        }
+        load_lds16(src, la + (c * 256 + wave * 64) * 16);
+      }
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int e = c * 256 + tid;
+        const void *src;
+        if (BK) {
+          const int nr = e >> 3, kc = ((e & 7) ^ (nr & 7)) * 8;
+          const int n = n0 + nr, kk = k0 + kc;
+          src = src16(p.B + size_t(n) * p.ldb + kk, (n < p.N) & (kk < kend));
+        } else {
+          constexpr int RC = BN / 8;
+          const int kr = e / RC, nc = ((e % RC) ^ ((2 * (kr & 3)) & (RC - 1))) * 8;
+          const int kk = k0 + kr, n = n0 + nc;
+          if constexpr (GB == GB_WGRAD) {
+            src = gatherB_wgrad_src(p, ctapd[c], kk, kend);
+          } else if constexpr (GB == GB_WDGRAD) {
+            src = gatherB_wdgrad_src(p, kk, n, kend);
+          } else {
+            src = src16(p.B + size_t(kk) * p.ldb + n, (kk < kend) & (n < p.N));
+          }
+        }
+        load_lds16(src, lb + (c * 256 + wave * 64) * 16);
+      }
+    };
+    // one k step of 32 from stage (sa, sb): the MFMA operands, swizzled back
+    auto compute = [&](const unsigned char *sa, const unsigned char *sb) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 32) {
+        bf16x8 av[TM], bv[TN];
+#pragma unroll
+        for (int a = 0; a < TM; ++a) {
+          if constexpr (AK) {
+            const int r = wm + a * 16 + i16, g = ((ks >> 3) + q) ^ (r & 7);
+            av[a] = *reinterpret_cast<const bf16x8 *>(sa + (r * 8 + g) * 16);
+          } else {
+            constexpr int RC = BM / 8;
+            const int kr = ks + 8 * q + (i16 >> 2), col = wm + a * 16 + 4 * (i16 & 3);
+            const int g = (col >> 3) ^ ((2 * (kr & 3)) & (RC - 1));
+            av[a] = tr_operand(sa + (kr * RC + g) * 16 + (col & 7) * 2, 4 * RC * 16);
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          if constexpr (BK) {
+            const int r = wn + b * 16 + i16, g = ((ks >> 3) + q) ^ (r & 7);
+            bv[b] = *reinterpret_cast<const bf16x8 *>(sb + (r * 8 + g) * 16);
+          } else {
+            constexpr int RC = BN / 8;
+            const int kr = ks + 8 * q + (i16 >> 2), col = wn + b * 16 + 4 * (i16 & 3);
+            const int g = (col >> 3) ^ ((2 * (kr & 3)) & (RC - 1));
+            bv[b] = tr_operand(sb + (kr * RC + g) * 16 + (col & 7) * 2, 4 * RC * 16);
+          }
+        }
+#pragma unroll
+        for (int a = 0; a < TM; ++a)
+#pragma unroll
+          for (int b = 0; b < TN; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+      }
+    };
+    if constexpr (NS == 3) {
+      // Slice kt sits in stage kt % 3.  At step kt each wavefront waits until
+      // only the next slice's loads are outstanding (its own share of slice
+      // kt has landed), then the barrier makes every share visible and tells
+      // that every wavefront is done with slice kt - 1, whose stage then
+      // takes slice kt + 2.  (A bare s_barrier: __syncthreads' fence would
+      // wait for every load in flight.)
+      issue(0, sa0, sb0);
+      issue(1, sa1, sb1);
+      auto step = [&](int kt, const unsigned char *ra, const unsigned char *rb, unsigned char *wa,
+                      unsigned char *wb) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_le(PA + PB));
+        __builtin_amdgcn_s_barrier();
+        issue(kt + 2, wa, wb);
+        compute(ra, rb);
+      };
+      int kt = 0;
+      for (; kt + 3 <= nk; kt += 3) {
+        step(kt, sa0, sb0, sa2, sb2);
+        step(kt + 1, sa1, sb1, sa0, sb0);
+        step(kt + 2, sa2, sb2, sa1, sb1);
+      }
+      if (kt < nk) step(kt, sa0, sb0, sa2, sb2);
+      if (kt + 1 < nk) step(kt + 1, sa1, sb1, sa0, sb0);
+    } else {
+      // two stages: slice kt in stage kt % 2; at step kt every load of slice
+      // kt has landed, and after the barrier the other stage (slice kt - 1)
+      // takes slice kt + 1
+      issue(0, sa0, sb0);
+      auto step = [&](int kt, const unsigned char *ra, const unsigned char *rb, unsigned char *wa,
+                      unsigned char *wb) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
+        __builtin_amdgcn_s_barrier();
+        issue(kt + 1, wa, wb);
+        compute(ra, rb);
+      };
+      int kt = 0;
+      for (; kt + 2 <= nk; kt += 2) {
+        step(kt, sa0, sb0, sa1, sb1);
+        step(kt + 1, sa1, sb1, sa0, sb0);
+      }
+      if (kt < nk) step(kt, sa0, sb0, sa1, sb1);
+    }
+    // every load (the re-reads past the range included) has landed and every
+    // wavefront is done with the stages before the epilogue reuses them
+    __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
     __syncthreads();
-    gload(ra0, rb0, kslice(kt + 2));
-    compute(0);
-    sstore(ra1, rb1, 1);
-    __syncthreads();
-    gload(ra1, rb1, kslice(kt + 3));
-    compute(1);
-  }
-  if (kt < nk) {  // the last one or two slices, without further loads
-    sstore(ra0, rb0, 0);
-    __syncthreads();
-    compute(0);
-    if (kt + 1 < nk) {
+  } else {
+    // register-staged loop: LDS operand tiles, double-buffered.  A
+    // k-contiguous operand is stored [buf][row][k] (pitch KP); a k-major one
+    // is stored as it arrives, [buf][k][row] (pitch rows + 16), and read back
+    // through the transposing LDS read (two 8-byte reads give a lane its 8
+    // consecutive k).
+    constexpr int PA_K = BM + 16, PB_K = BN + 16;
+    constexpr int SZA = AK ? 2 * BM * KP * 2 : 2 * KS * PA_K * 2;
+    constexpr int SZB = BK ? 2 * BN * KP * 2 : 2 * KS * PB_K * 2;
+    __shared__ __align__(16) unsigned char smA[SZA];
+    __shared__ __align__(16) unsigned char smB[SZB];
+    static_assert(EPI_SCR <= SZA, "epilogue scratch fits the A tile");
+    scr = smA;
+    // Every thread loads its chunks unconditionally (threads past a tile's
+    // chunk count load a duplicate and skip the LDS store), so the load
+    // counters are static and the loads stay in flight across the MFMAs.
+    auto gload = [&](u32x4 (&ra)[PA], u32x4 (&rb)[PB], int k0) {
+#pragma unroll
+      for (int c = 0; c < PA; ++c) {
+        const int e = min(tid + c * 256, CHA - 1);
+        if (AK) {  // chunk = 8 k of one m
+          const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+          if constexpr (GA == GA_CAT) {  // k < K1 from A, the rest from A2 (no branch)
+            const int kk = k0 + kc, m = m0 + mr;
+            const bool second = kk >= p.K1;
+            const __bf16 *base = second ? p.A2 : reinterpret_cast<const __bf16 *>(A);
+            const size_t off = size_t(m) * (second ? p.lda2 : p.lda) + (second ? kk - p.K1 : kk);
+            ra[c] = masked16(base + off, (m < p.M) & (kk < kend));
+          } else if constexpr (GA != G_DENSE)
+            ra[c] = gatherA<GA>(p, reinterpret_cast<const __bf16 *>(A), rpix[c], k0 + kc, kend);
+          else
+            ra[c] = ld8<SAFE, TA>(A, m0 + mr, k0 + kc, p.M, kend, p.lda);
+        } else {   // chunk = 8 m of one k
+          const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
+          ra[c] = ld8<SAFE, TA>(A, k0 + kr, m0 + mc, kend, p.M, p.lda);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int e = min(tid + c * 256, CHB - 1);
+        if (BK) {
+          const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+          rb[c] = ld8<SAFE, __bf16>(p.B, n0 + nr, k0 + kc, p.N, kend, p.ldb);
+        } else {
+          const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
+          if constexpr (GB == GB_WGRAD)
+            rb[c] = gatherB_wgrad(p, ctap[c], k0 + kr, kend);
+          else if constexpr (GB == GB_WDGRAD)
+            rb[c] = gatherB_wdgrad(p, k0 + kr, n0 + nc, kend);
+          else
+            rb[c] = ld8<SAFE, __bf16>(p.B, k0 + kr, n0 + nc, kend, p.N, p.ldb);
+        }
+      }
+    };
+    // k-contiguous chunks go to LDS as one 16-byte store; the others are
+    // transposed into eight 2-byte stores.
+    auto sstore = [&](const u32x4 (&ra)[PA], const u32x4 (&rb)[PB], int buf) {
+#pragma unroll
+      for (int c = 0; c < PA; ++c) {
+        const int e = tid + c * 256;
+        if (CHA % 256 == 0 || e < CHA) {
+          if (AK) {
+            const int mr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+            *reinterpret_cast<u32x4 *>(smA + ((buf * BM + mr) * KP + kc) * 2) = ra[c];
+          } else {
+            const int kr = e / (BM / 8), mc = (e % (BM / 8)) * 8;
+            *reinterpret_cast<u32x4 *>(smA + ((buf * KS + kr) * PA_K + mc) * 2) = ra[c];
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int e = tid + c * 256;
+        if (CHB % 256 == 0 || e < CHB) {
+          if (BK) {
+            const int nr = e / (KS / 8), kc = (e % (KS / 8)) * 8;
+            *reinterpret_cast<u32x4 *>(smB + ((buf * BN + nr) * KP + kc) * 2) = rb[c];
+          } else {
+            const int kr = e / (BN / 8), nc = (e % (BN / 8)) * 8;
+            *reinterpret_cast<u32x4 *>(smB + ((buf * KS + kr) * PB_K + nc) * 2) = rb[c];
+          }
+        }
+      }
+    };
+
+    // one slice: KS / 32 MFMA k-steps; step s reads k 32 s + 8 q .. + 7
+    auto compute = [&](int buf) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 32) {
+        bf16x8 av[TM], bv[TN];
+#pragma unroll
+        for (int a = 0; a < TM; ++a) {
+          if constexpr (AK)
+            av[a] = *reinterpret_cast<const bf16x8 *>(smA + ((buf * BM + wm + a * 16 + i16) * KP + ks + 8 * q) * 2);
+          else
+            av[a] = tr_operand(
+                smA + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PA_K + wm + a * 16 + 4 * (i16 & 3)) * 2,
+                4 * PA_K * 2);
+        }
+#pragma unroll
+        for (int b = 0; b < TN; ++b) {
+          if constexpr (BK)
+            bv[b] = *reinterpret_cast<const bf16x8 *>(smB + ((buf * BN + wn + b * 16 + i16) * KP + ks + 8 * q) * 2);
+          else
+            bv[b] = tr_operand(
+                smB + ((buf * KS + ks + 8 * q + (i16 >> 2)) * PB_K + wn + b * 16 + 4 * (i16 & 3)) * 2,
+                4 * PB_K * 2);
+        }
+#pragma unroll
+        for (int a = 0; a < TM; ++a)
+#pragma unroll
+          for (int b = 0; b < TN; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+      }
+    };
+
+    // Two register stages: the loads of slice kt + 2 are issued right after
+    // slice kt is stored to LDS, so each load has two slices of MFMA work to
+    // arrive.  Slice kt is stored to LDS buffer kt & 1.  The loop body has no
+    // branches (a branch there makes the compiler wait for every outstanding
+    // load at each iteration): it runs while two more slices follow, and the
+    // last one or two slices are multiplied after it.
+    u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
+    gload(ra0, rb0, kslice(0));
+    gload(ra1, rb1, kslice(1));
+    int kt = 0;
+    for (; kt + 2 < nk; kt += 2) {  // no branches in the body (see above)
+      sstore(ra0, rb0, 0);
+      __syncthreads();
+      gload(ra0, rb0, kslice(kt + 2));
+      compute(0);
       sstore(ra1, rb1, 1);
       __syncthreads();
+      gload(ra1, rb1, kslice(kt + 3));
       compute(1);
+    }
+    if (kt < nk) {  // the last one or two slices, without further loads
+      sstore(ra0, rb0, 0);
+      __syncthreads();
+      compute(0);
+      if (kt + 1 < nk) {
+        sstore(ra1, rb1, 1);
+        __syncthreads();
+        compute(1);
+      }
     }
   }
 
@@ -468,7 +718,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
           }
         }
     __syncthreads();
-    double *red = reinterpret_cast<double *>(smA);  // [WM*4][2][BN]
+    double *red = reinterpret_cast<double *>(scr);  // [WM*4][2][BN]
     const int wr = wave / WN;
 #pragma unroll
     for (int b = 0; b < TN; ++b) {
@@ -488,7 +738,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   // Epilogue through LDS: each wavefront stages 16 rows x WC columns of its
   // tile at a time, then writes whole rows with 16-byte stores (and reads D
   // and the mask the same way).
-  float *stage = reinterpret_cast<float *>(smA) + wave * 16 * SP;
+  float *stage = reinterpret_cast<float *>(scr) + wave * 16 * SP;
   float *Cz = p.C + size_t(tz) * p.M * p.ldc;
   constexpr int VEC = EPI == GEMM_EPI_BF16STATS ? 8 : 4;  // output elements per lane
   constexpr int LPR = WC / VEC;                           // lanes per row
@@ -663,7 +913,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     // the WM wavefronts, in a fixed order; block-major partials
     // [row tile][sum][column] as BF16STATS stores them
     __syncthreads();
-    double *red = reinterpret_cast<double *>(smA);  // [WM * RPP][2][BN]
+    double *red = reinterpret_cast<double *>(scr);  // [WM * RPP][2][BN]
     const int slot = (wave / WN) * RPP + lane / LPR, col0 = wn + (lane % LPR) * VEC;
 #pragma unroll
     for (int u = 0; u < VEC; ++u) {
@@ -703,37 +953,54 @@ inline Tile tile_of(int M, int N) {
   return {64, 32};
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
-void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE, bool DEEP>
+void launch_epi_s(const Args &a, int epi, int splits, hipStream_t s) {
   dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
   if (epi == GEMM_EPI_ADD) {
-    launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+    launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
     return;
   }
   if constexpr (std::is_same<TA, __bf16>::value) {
     if (epi == GEMM_EPI_ADDMASK) {
-      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
       return;
     }
     if (epi == GEMM_EPI_BF16STATS) {
-      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
       return;
     }
     // instantiated for the operand forms the host wrappers accept only
     if constexpr (AK && !BK && SAFE) {
       if (epi == GEMM_EPI_BNBWD) {
-        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
         return;
       }
     }
     if constexpr (AK && BK && SAFE && GA == G_DENSE && GB == G_DENSE) {
       if (epi == GEMM_EPI_ROWSOFTMAX) {
-        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
         return;
       }
     }
   }
-  launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE>), grid, dim3(256), 0, s, a);
+  launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+}
+
+// The direct loop of the two largest tiles runs with three stages (DEEP)
+// when the grid has no more tiles than the device has compute units, else
+// with two, so that two workgroups share a unit.
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
+void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
+  constexpr bool direct = SAFE && std::is_same<TA, __bf16>::value;
+  constexpr int scr = cmax(4 * 16 * (BN / WN) * 4, 4 * 2 * BN * 8 * 4);  // a bound on any epilogue's scratch
+  if constexpr (direct && !direct_three_stages(BM, BN, scr)) {
+    const long tiles = long((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM) * splits;
+    if (tiles <= 256) {
+      launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, true>(a, epi, splits, s);
+      return;
+    }
+  }
+  launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, false>(a, epi, splits, s);
 }
 
 template <bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>

@@ -220,7 +220,7 @@ void log_gemm(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid, int epi, 
 // the whole extent of every operand of a bf16 GEMM launch
 void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   using namespace ckpt::gb;
-  if (k.targs.size() != 11) {
+  if (k.targs.size() != 12) {
     error(k.pretty + ": unexpected template arguments");
     return;
   }

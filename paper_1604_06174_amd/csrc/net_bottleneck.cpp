@@ -53,11 +53,11 @@ class Bottleneck : public Net {
   static uint64_t bf(int64_t m, int c) { return align256(uint64_t(m) * c * 2); }
   static uint64_t f32(int64_t m, int c) { return align256(uint64_t(m) * c * 4); }
 
-  // weight-gradient split-K: about 1024 workgroups, at least 8 k-slices
-  // each, partials capped at 16M floats
+  // weight-gradient split-K: about 512 workgroups (two per compute unit),
+  // at least 8 k-slices each, partials capped at 16M floats
   static int wsplits(int M, int Nn, int64_t Kd) {
     const int tiles = gemm_bf16_tiles(M, Nn);
-    int64_t s = (1024 + tiles - 1) / tiles;
+    int64_t s = (512 + tiles - 1) / tiles;
     s = std::min<int64_t>(s, Kd / 256);
     s = std::min<int64_t>(s, (int64_t(16) << 20) / (int64_t(M) * Nn));
     return int(std::max<int64_t>(s, 1));

@@ -176,7 +176,7 @@ def main():
     ap.add_argument("--fanout", type=int, default=0,
                     help="recursive plan: boundaries stored per level (section 4.4's k; default 1)")
     ap.add_argument("--drop-bn-relu", action="store_true",
-                    help="CIFAR-shaped net: keep only convolution outputs and re-form batch norm + "
+                    help="residual CNNs: keep only convolution outputs and re-form batch norm + "
                          "ReLU from them when read")
     ap.add_argument("--graph", action="store_true",
                     help="also time each step recorded once as a HIP graph and replayed "
@@ -200,8 +200,8 @@ def main():
 
     cfg = dict(synth.WORKLOADS[args.workload])
     if args.drop_bn_relu:
-        if cfg["kind"] != "resnet_basic":
-            print(json.dumps({"error": "--drop-bn-relu applies to the CIFAR-shaped network"}))
+        if cfg["kind"] not in ("resnet_basic", "resnet_bottleneck"):
+            print(json.dumps({"error": "--drop-bn-relu applies to the residual CNNs"}))
             sys.exit(2)
         cfg["drop_bn_relu"] = 1
     d = synth.make(cfg)

@@ -40,7 +40,9 @@ Unit kinds (fp32 unless stated):
   - bottleneck (width w, output channels Co, mi / mo input / output pixels):
     a = c1, r1 (B(mi, w) each), c2, r2 (B(mo, w) each), c3 (B(mo, Co)),
     [cp (B(mo, Co))], BN pairs 8w, 8w, 8Co [, 8Co]; q = max(B(mo, Co),
-    B(mi, w)) + F(mi, w) + B(mo, w) [+ B(mo, Co)].
+    B(mi, w)) + F(mi, w) + B(mo, w) [+ B(mo, Co)].  With the "drop bn-relu"
+    layout (section 4.2) r1 and r2 are not kept but formed again in the
+    gradient scratch: a loses B(mi, w) + B(mo, w) and q gains them.
   The gradient slot holds the largest fp32 boundary gradient.
 
 ``grad_layout`` returns (gradient slot bytes, extra gradient bytes); for the
@@ -105,8 +107,11 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
                 q.append(f32(m, u.cout) + bf(m, u.cout))
             else:
                 mi, mo, w, co = N * u.hin * u.hin, N * u.hout * u.hout, u.width, u.cout
-                aa = 2 * bf(mi, w) + 2 * bf(mo, w) + bf(mo, co) + 2 * align(8 * w) + align(8 * co)
-                qq = max(bf(mo, co), bf(mi, w)) + f32(mi, w) + bf(mo, w)
+                relus = bf(mi, w) + bf(mo, w)          # r1, r2
+                drop = cfg.get("drop_bn_relu")
+                aa = bf(mi, w) + bf(mo, w) + bf(mo, co) + 2 * align(8 * w) + align(8 * co) + \
+                    (0 if drop else relus)
+                qq = max(bf(mo, co), bf(mi, w)) + f32(mi, w) + bf(mo, w) + (relus if drop else 0)
                 if u.proj:
                     aa += bf(mo, co) + align(8 * co)
                     qq += bf(mo, co)

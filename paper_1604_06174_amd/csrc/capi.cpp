@@ -165,8 +165,11 @@ int net_create(const ckpt_net_desc *desc, ckpt_net **out) {
          desc->stage_blocks[3] | desc->expansion | desc->stem_channels) != 0)
       ckpt::fail(CKPT_E_INVALID,
                  "net_create: stage_blocks, expansion and stem_channels apply to RESNET_BOTTLENECK only");
-    if (desc->drop_bn_relu != 0 && (desc->kind != CKPT_NET_RESNET_BASIC || desc->drop_bn_relu != 1))
-      ckpt::fail(CKPT_E_INVALID, "net_create: drop_bn_relu is 0 or 1 and applies to RESNET_BASIC only");
+    if (desc->drop_bn_relu != 0 &&
+        ((desc->kind != CKPT_NET_RESNET_BASIC && desc->kind != CKPT_NET_RESNET_BOTTLENECK) ||
+         desc->drop_bn_relu != 1))
+      ckpt::fail(CKPT_E_INVALID,
+                 "net_create: drop_bn_relu is 0 or 1 and applies to RESNET_BASIC and RESNET_BOTTLENECK only");
     auto h = std::make_unique<ckpt_net>();
     switch (desc->kind) {
       case CKPT_NET_MLP: h->net = ckpt::make_mlp_net(*desc); break;

@@ -256,6 +256,7 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
   uint64_t maxq = 0;
   for (int32_t i = 0; i < net.n; ++i) maxq = std::max(maxq, net.q[size_t(i)]);
   c.gextra = grad + 2 * slot + maxq;
+  c.q = grad + 2 * slot;
 
   Exec e{net, c, acc, ckpt, arena, {grad, grad + slot}, grad + 2 * slot};
   (void)hipGetLastError();  // clear a stale error left by the caller

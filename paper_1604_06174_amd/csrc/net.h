@@ -87,6 +87,9 @@ struct StepCtx {
   const void *target = nullptr;   // device, batch targets
   char *ks = nullptr;             // device operator workspace (net.ks_bytes)
   char *gextra = nullptr;         // device fixed gradient buffers (net.grad_extra)
+  // device unit gradient scratch (the largest q_i): in use only inside a
+  // unit's backward, so a unit's forward may keep transient tensors there
+  char *q = nullptr;
   uint64_t launches = 0;
   // false while a forward sweep runs whose saved internals are discarded
   // (they are formed again by the unit's re-run before its backward)

@@ -20,6 +20,13 @@
 //   stem   a = c | r | st                          q = dr (F) | dc
 //   block  a = c1 | r1 | c2 | r2 | c3 | [cp] | st1 | st2 | st3 | [stp]
 //          q = dc3/dc1 | dr2/dr1 (F) | dc2 | [dcp]
+// With drop_bn_relu (the "drop bn-relu" plan of section 4.2: keep the
+// convolution outputs, form batch norm + ReLU again when needed) a block
+// keeps a = c1 | c2 | c3 | [cp] | st slots and q = r1 | r2 | (the above):
+// its forward forms r1 and r2 in the gradient scratch (which no unit uses
+// outside its backward), and its backward forms them there again from c1,
+// c2 and the statistics with the same kernel, so every value and gradient
+// is the standard layout's bit for bit.
 // The st slots of a are reserved (PEAK counts them) but the statistics live
 // in operator workspace, per BN of every unit: a unit's first forward of the
 // step forms them and its re-runs, which see the same input bits, reuse them
@@ -43,6 +50,7 @@ struct BUnit {
 class Bottleneck : public Net {
  public:
   int N, S, side, C0, K;
+  bool drop;  // blocks keep no relu(bn(.)) outputs
   std::vector<BUnit> u;
   int hw, hb;
   uint64_t ks_wbf = 0, ks_col = 0, ks_stats = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0,
@@ -69,6 +77,7 @@ class Bottleneck : public Net {
     S = d.image;
     C0 = d.stem_channels;
     K = d.n_classes;
+    drop = d.drop_bn_relu != 0;
     side = (S + 2 * 3 - 7) / 2 + 1;
     const int pooled = (side + 2 - 3) / 2 + 1;
     b.push_back(bf(int64_t(N) * S * S, 3));
@@ -107,12 +116,13 @@ class Bottleneck : public Net {
         }
         u.push_back(k);
         const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
-        uint64_t av = 2 * bf(mi, w) + 2 * bf(mo, w) + bf(mo, cout) + 2 * align256(8ull * w) +
-                      align256(8ull * cout);
+        const uint64_t relus = bf(mi, w) + bf(mo, w);  // r1, r2
+        uint64_t av = bf(mi, w) + bf(mo, w) + bf(mo, cout) + 2 * align256(8ull * w) +
+                      align256(8ull * cout) + (drop ? 0 : relus);
         if (k.proj) av += bf(mo, cout) + align256(8ull * cout);
         a.push_back(av);
         q.push_back(std::max(bf(mo, cout), bf(mi, w)) + f32(mi, w) + bf(mo, w) +
-                    (k.proj ? bf(mo, cout) : 0));
+                    (k.proj ? bf(mo, cout) : 0) + (drop ? relus : 0));
         b.push_back(bf(mo, cout));
         cin = cout;
         h = k.hout;
@@ -293,8 +303,14 @@ class Bottleneck : public Net {
       return;
     }
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
-    char *c1 = sv, *r1 = c1 + bf(mi, k.w), *c2 = r1 + bf(mi, k.w), *r2 = c2 + bf(mo, k.w);
-    char *c3 = r2 + bf(mo, k.w), *cp = c3 + bf(mo, k.cout);
+    char *c1, *r1, *c2, *r2, *c3, *cp;
+    if (drop) {  // r1, r2 transient, in the gradient scratch
+      c1 = sv, c2 = c1 + bf(mi, k.w), c3 = c2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+      r1 = c.q, r2 = r1 + bf(mi, k.w);
+    } else {
+      c1 = sv, r1 = c1 + bf(mi, k.w), c2 = r1 + bf(mi, k.w), r2 = c2 + bf(mo, k.w);
+      c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+    }
     float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
     fwd_1x1(c, mi, k.cin, k.w, xv, k.W1, c1, st1);
     bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
@@ -340,9 +356,24 @@ class Bottleneck : public Net {
       return;
     }
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
-    const char *c1 = sv, *r1 = c1 + bf(mi, k.w), *c2 = r1 + bf(mi, k.w), *r2 = c2 + bf(mo, k.w);
-    const char *c3 = r2 + bf(mo, k.w), *cp = c3 + bf(mo, k.cout);
+    const char *c1, *r1, *c2, *r2, *c3, *cp;
     const float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
+    if (drop) {
+      // r1, r2 formed again from c1, c2 and their statistics (the forward's
+      // kernel on the same bits) at the front of the gradient scratch
+      c1 = sv, c2 = c1 + bf(mi, k.w), c3 = c2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+      char *rr1 = qb, *rr2 = rr1 + bf(mi, k.w);
+      bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
+                nullptr, nullptr, rr1);
+      bnb_apply(c.s, BNB_RES_NONE, mo, k.w, c2, st2, P(c, k.g2), P(c, k.b2), nullptr, nullptr,
+                nullptr, nullptr, rr2);
+      c.launches += 2;
+      r1 = rr1, r2 = rr2;
+      qb = rr2 + bf(mo, k.w);
+    } else {
+      c1 = sv, r1 = c1 + bf(mi, k.w), c2 = r1 + bf(mi, k.w), r2 = c2 + bf(mo, k.w);
+      c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+    }
     char *qA = qb;                                         // dc3, then dc1
     float *qB = reinterpret_cast<float *>(qA + std::max(bf(mo, k.cout), bf(mi, k.w)));  // dr2, dr1
     char *qC = reinterpret_cast<char *>(qB) + f32(mi, k.w);  // dc2

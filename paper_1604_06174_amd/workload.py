@@ -35,7 +35,8 @@ def net_for(cfg: Dict) -> K.Net:
             raise K.CkptError(K.E_UNSUPPORTED, "bottleneck widths must double per stage")
         return K.net_create(K.NET_RESNET_BOTTLENECK, cfg["batch"], len(sb), w0,
                             cfg.get("image", 224), cfg.get("classes", 1000), 0, sb,
-                            cfg.get("expansion", 4), cfg.get("stem_channels", 64))
+                            cfg.get("expansion", 4), cfg.get("stem_channels", 64),
+                            drop_bn_relu=int(bool(cfg.get("drop_bn_relu", 0))))
     raise K.CkptError(K.E_UNSUPPORTED, f"no GPU network for workload kind {kind!r}")
 
 

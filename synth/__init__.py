@@ -124,7 +124,7 @@ def resnet_basic_structure(blocks_per_stage: int, base: int, batch: int,
 def resnet_bottleneck_structure(stage_blocks=(32, 64, 205, 32), batch: int = 32,
                                 image: int = 224, classes: int = 1000,
                                 widths=(64, 128, 256, 512), expansion: int = 4,
-                                stem_channels: int = 64) -> Structure:
+                                stem_channels: int = 64, drop_bn_relu: bool = False) -> Structure:
     side = (image + 2 * 3 - 7) // 2 + 1          # conv7x7/2 pad 3
     pooled = (side + 2 * 1 - 3) // 2 + 1         # maxpool3x3/2 pad 1
     units = [Unit("stem7", cin=3, cout=stem_channels, stride=2, hin=image, hout=pooled,
@@ -154,7 +154,8 @@ def resnet_bottleneck_structure(stage_blocks=(32, 64, 205, 32), batch: int = 32,
     head = [("head.W", (cin, classes), "fc_w"), ("head.b", (classes,), "fc_b")]
     return Structure("resnet_bottleneck",
                      dict(stage_blocks=tuple(stage_blocks), batch=batch, image=image,
-                          classes=classes, widths=tuple(widths), stem_channels=stem_channels),
+                          classes=classes, widths=tuple(widths), stem_channels=stem_channels,
+                          drop_bn_relu=bool(drop_bn_relu)),
                      units, head, (batch, image, image, 3), (batch,), "labels", classes)
 
 
@@ -181,7 +182,8 @@ def structure(cfg: Dict) -> Structure:
         return resnet_bottleneck_structure(tuple(cfg["stage_blocks"]), cfg["batch"],
                                            cfg.get("image", 224), cfg.get("classes", 1000),
                                            tuple(cfg.get("widths", (64, 128, 256, 512))),
-                                           cfg.get("expansion", 4), cfg.get("stem_channels", 64))
+                                           cfg.get("expansion", 4), cfg.get("stem_channels", 64),
+                                           cfg.get("drop_bn_relu", False))
     if k == "lstm":
         return lstm_structure(cfg["T"], cfg["batch"], cfg["input"], cfg["hidden"], cfg["vocab"])
     raise ValueError(f"unknown workload kind {k!r}")

@@ -261,6 +261,7 @@ def net_of(cfg):
         for t, v in enumerate(sb):
             d.stage_blocks[t] = v
         d.expansion, d.stem_channels = cfg.get("expansion", 4), cfg.get("stem_channels", 64)
+        d.drop_bn_relu = int(bool(cfg.get("drop_bn_relu")))
     h = vp()
     if not ok(LIB.net_create(C.byref(d), C.byref(h)), f"net_create {cfg}"):
         return None
@@ -371,16 +372,22 @@ def dry_runs(quick):
              dict(kind="lstm", T=13, batch=8, input=16, hidden=24, vocab=40, grad_chunk=4,
                   name="lstm small"),
              dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1, 1), widths=(8, 16, 32, 64),
-                  stem_channels=16, image=32, batch=2, classes=10, name="bottleneck small")]
+                  stem_channels=16, image=32, batch=2, classes=10, name="bottleneck small"),
+             dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1, 1), widths=(8, 16, 32, 64),
+                  stem_channels=16, image=32, batch=2, classes=10, drop_bn_relu=1,
+                  name="bottleneck small drop bn-relu")]
     for cfg in small:
         dry_step(cfg, ALL, static=True, graph_step=cfg["kind"] == "mlp", record=True)
     full = [("resnet1000", [(PL.GREEDY, "tenth", 0), (PL.NONE, 0, 0)]),
+            ("resnet1000 drop bn-relu", [(PL.GREEDY, "tenth", 0)]),
             ("cifar110", [(PL.SQRT, 0, 0)]), ("mlp64", [(PL.SQRT, 8, 0)]),
             ("lstm4096", [(PL.SQRT, 64, 0)]), ("mlp1024", [(PL.RECURSIVE, 0, 0)])]
     if quick:
         full = full[:1]
     for name, plans in full:
-        cfg = dict(synth.WORKLOADS[name], name=name)
+        cfg = dict(synth.WORKLOADS[name.split()[0]], name=name)
+        if name.endswith("drop bn-relu"):
+            cfg["drop_bn_relu"] = 1
         dry_step(cfg, plans, static=True)
 
 

@@ -110,7 +110,9 @@ WORKLOADS_CPU = [dict(kind="mlp", depth=64, width=256, batch=64),
                  dict(kind="resnet_bottleneck", stage_blocks=(32, 64, 205, 32), batch=32,
                       image=224, classes=1000),
                  dict(kind="resnet_bottleneck", stage_blocks=(2, 1, 1), widths=(8, 16, 32),
-                      expansion=2, stem_channels=16, image=32, batch=3, classes=10)]
+                      expansion=2, stem_channels=16, image=32, batch=3, classes=10),
+                 dict(kind="resnet_bottleneck", stage_blocks=(32, 64, 205, 32), batch=32,
+                      image=224, classes=1000, drop_bn_relu=1)]
 
 
 @pytest.mark.parametrize("cfg", WORKLOADS_CPU)
@@ -164,7 +166,7 @@ def test_net_create_errors():
     with pytest.raises(K.CkptError) as ei:
         K.net_create(K.NET_MLP, 2, 4, 8, stage_blocks=(1,))
     assert ei.value.code == K.E_INVALID
-    with pytest.raises(K.CkptError) as ei:  # drop bn-relu is a RESNET_BASIC layout
+    with pytest.raises(K.CkptError) as ei:  # drop bn-relu is a layout of the CNNs
         K.net_create(K.NET_MLP, 2, 4, 8, drop_bn_relu=1)
     assert ei.value.code == K.E_INVALID
     B = K.NET_RESNET_BOTTLENECK

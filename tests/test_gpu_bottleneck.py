@@ -99,3 +99,31 @@ def test_bottleneck_plans_chaotic(case):
     print(f"  loss {loss:.6f} vs emulating oracle {le:.6f}: {dl:.1e}", flush=True)
     assert dl <= 2e-2, dl
     assert all(np.all(np.isfinite(v)) for v in g.values())
+
+
+@pytest.mark.parametrize("case", ["p21", "wide"])
+def test_bottleneck_drop_bn_relu_same_bits(case):
+    """The drop bn-relu layout (section 4.2: blocks keep only convolution
+    outputs and form relu(bn(.)) again when needed) gives the standard
+    layout's loss and gradients bit for bit under every plan, with the
+    oracle's (smaller) peak bytes."""
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = dict(WELL_POSED.get(case) or CHAOTIC[case])
+    print(f"[bottleneck drop bn-relu] case={case}", flush=True)
+    d = synth.make(cfg)
+    std = GpuStep(cfg, d["params"], d["input"], d["target"])
+    loss_s, _, bytes_s = _all_plans(std, d["structure"])
+    cfgd = dict(cfg, drop_bn_relu=1)
+    dd = synth.make(cfgd)
+    drop = GpuStep(cfgd, dd["params"], dd["input"], dd["target"])
+    loss_d, _, bytes_d = _all_plans(drop, dd["structure"])
+    assert loss_d == loss_s
+    assert bytes_d == bytes_s, "drop bn-relu gradients differ from the standard layout's"
+    lb, cb = SZ.layer_and_cut_bytes(d["structure"])
+    lbd, cbd = SZ.layer_and_cut_bytes(dd["structure"])
+    p_s = PL.account(PL.plan(d["structure"].n, lb, cb, 0, PL.SQRT), *SZ.tables(d["structure"]),
+                     *SZ.grad_layout(d["structure"])).peak
+    p_d = PL.account(PL.plan(dd["structure"].n, lbd, cbd, 0, PL.SQRT), *SZ.tables(dd["structure"]),
+                     *SZ.grad_layout(dd["structure"])).peak
+    print(f"  sqrt-plan peak {p_s} -> {p_d} bytes", flush=True)
+    assert p_d < p_s

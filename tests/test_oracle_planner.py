@@ -214,6 +214,9 @@ def test_serialize_layout():
                                  dict(kind="resnet_bottleneck", stage_blocks=(2, 1), widths=(8, 16),
                                       expansion=4, stem_channels=8, image=16, batch=2, classes=5,
                                       seed=3),
+                                 dict(kind="resnet_bottleneck", stage_blocks=(2, 1), widths=(8, 16),
+                                      expansion=4, stem_channels=8, image=16, batch=2, classes=5,
+                                      seed=3, drop_bn_relu=1),
                                  dict(kind="lstm", T=3, batch=4, input=8, hidden=16, vocab=24,
                                       seed=4)])
 def test_size_tables_match_kept_tensors(cfg):
@@ -222,13 +225,13 @@ def test_size_tables_match_kept_tensors(cfg):
     bottleneck net's activations and the LSTM's h, fp32 otherwise (batch-norm
     (mean, rstd) pairs as one block).  The bottleneck stem's max-pool window
     choice ("arg") is not kept: the backward finds the window's first maximum
-    again from the pooled output.  The drop bn-relu layout keeps neither the
-    relu(bn1) output."""
+    again from the pooled output.  The drop bn-relu layouts keep no relu(bn(.))
+    output of a block (the basic block's r1, the bottleneck's r1 and r2)."""
     d = synth.make(cfg)
     kind = cfg["kind"]
     chain = nets.Chain(d["structure"], d["params"], U.Prec(np.float32, kind == "resnet_bottleneck"))
     b, a, q = SZ.tables(d["structure"])
-    drop = kind == "resnet_basic" and cfg.get("drop_bn_relu")
+    drop = cfg.get("drop_bn_relu")
 
     def nbytes(name, v, half=False):
         if isinstance(v, tuple):          # BN (mean, rstd) pair: one fp32 block
@@ -249,7 +252,7 @@ def test_size_tables_match_kept_tensors(cfg):
             kept = SZ.align(sum(4 * saved[g].size for g in "ifgo")) + nbytes("dlog", saved["dlog"])
         else:
             for nm, v in saved.items():
-                if nm == "arg" or (drop and nm == "r1"):
+                if nm == "arg" or (drop and nm in ("r1", "r2")):
                     continue
                 kept += nbytes(nm, v, kind == "resnet_bottleneck")
         assert kept == a[i], (i, kept, a[i])

@@ -15,13 +15,17 @@ Every tensor is rounded up to a multiple of 256 bytes.
 
 Unit kinds (fp32 unless stated):
 * residual MLP [B, D]: b = 4BD; a = z (4BD); q = relu-masked gradient (4BD).
-* CIFAR stem (3 -> C, S x S): a = conv output (4NSSC) + BN mean/rstd (8C);
-  q = one [N,S,S,C] tensor.
+* CIFAR stem (3 -> C, S x S): a = conv output (4NSSC); q = one [N,S,S,C]
+  tensor.
 * basic block (Cin -> Cout, output side S): a = conv1 output, relu(bn1)
-  output, conv2 output (3 x 4NSSCout) + two BN mean/rstd pairs (2 x 8Cout);
-  q = two [N,S,S,Cout] tensors.  With the "drop bn-relu" layout (section
-  4.2: keep the convolution outputs, recompute batch norm + ReLU) the relu(bn1)
-  output is not kept: a = 2 x 4NSSCout + 2 x 8Cout.
+  output, conv2 output (3 x 4NSSCout); q = two [N,S,S,Cout] tensors.  With
+  the "drop bn-relu" layout (section 4.2: keep the convolution outputs,
+  recompute batch norm + ReLU) the relu(bn1) output is not kept: a = 2 x
+  4NSSCout.
+* batch-norm statistics of the CNNs (a mean/rstd pair, 8C bytes per BN of C
+  channels): formed by a unit's first forward and read by its re-runs and
+  backward, they are held for the whole step: fixed buffers of the layout
+  (grad_layout's extra), one pair per BN of every unit, not part of a_i.
 * LSTM step (batch B, hidden H, vocabulary V; bf16 GEMM operands): b = h
   (bf16, 2BH) + c (fp32, 4BH); a = activated gates i,f,g,o (fp32, 16BH) +
   the softmax gradient of its head (fp32, 4BV); q = the total hidden-state
@@ -34,12 +38,11 @@ Unit kinds (fp32 unless stated):
 * bottleneck ResNet (bf16 activations; B(m, c) = a bf16 tensor of m pixels x
   c channels, F(m, c) the fp32 one): b_0 = the bf16 image batch.
   - stem (conv7x7/2 output side s, C0 channels, m = N s s): a = conv output
-    and ReLU output (2 x B(m, C0)) + BN mean/rstd (8 C0); q = the max-pool
-    input gradient F(m, C0) + the BN input gradient B(m, C0); the boundary is
-    the pooled output.
+    and ReLU output (2 x B(m, C0)); q = the max-pool input gradient F(m, C0)
+    + the BN input gradient B(m, C0); the boundary is the pooled output.
   - bottleneck (width w, output channels Co, mi / mo input / output pixels):
     a = c1, r1 (B(mi, w) each), c2, r2 (B(mo, w) each), c3 (B(mo, Co)),
-    [cp (B(mo, Co))], BN pairs 8w, 8w, 8Co [, 8Co]; q = max(B(mo, Co),
+    [cp (B(mo, Co))]; q = max(B(mo, Co),
     B(mi, w)) + F(mi, w) + B(mo, w) [+ B(mo, Co)].  With the "drop bn-relu"
     layout (section 4.2) r1 and r2 are not kept but formed again in the
     gradient scratch: a loses B(mi, w) + B(mo, w) and q gains them.
@@ -79,12 +82,11 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
         b.append(align(4 * N * u0.hin * u0.hin * 3))
         for u in structure.units:
             t = align(4 * N * u.hout * u.hout * u.cout)
-            st = align(8 * u.cout)
             if u.kind == "stem3":
-                a.append(t + st)
+                a.append(t)
                 q.append(t)
             else:
-                a.append((2 if cfg.get("drop_bn_relu") else 3) * t + 2 * st)
+                a.append((2 if cfg.get("drop_bn_relu") else 3) * t)
                 q.append(2 * t)
             b.append(t)
         return b, a, q
@@ -103,17 +105,16 @@ def tables(structure) -> Tuple[List[int], List[int], List[int]]:
         for u in structure.units:
             if u.kind == "stem7":
                 m = N * side * side
-                a.append(2 * bf(m, u.cout) + align(8 * u.cout))
+                a.append(2 * bf(m, u.cout))
                 q.append(f32(m, u.cout) + bf(m, u.cout))
             else:
                 mi, mo, w, co = N * u.hin * u.hin, N * u.hout * u.hout, u.width, u.cout
                 relus = bf(mi, w) + bf(mo, w)          # r1, r2
                 drop = cfg.get("drop_bn_relu")
-                aa = bf(mi, w) + bf(mo, w) + bf(mo, co) + 2 * align(8 * w) + align(8 * co) + \
-                    (0 if drop else relus)
+                aa = bf(mi, w) + bf(mo, w) + bf(mo, co) + (0 if drop else relus)
                 qq = max(bf(mo, co), bf(mi, w)) + f32(mi, w) + bf(mo, w) + (relus if drop else 0)
                 if u.proj:
-                    aa += bf(mo, co) + align(8 * co)
+                    aa += bf(mo, co)
                     qq += bf(mo, co)
                 a.append(aa)
                 q.append(qq)
@@ -144,8 +145,25 @@ def grad_layout(structure, grad_chunk=None):
         return slot, extra
     if structure.kind == "resnet_bottleneck":
         N = structure.cfg["batch"]
-        return max(align(4 * N * u.hout * u.hout * u.cout) for u in structure.units), 0
+        slot = max(align(4 * N * u.hout * u.hout * u.cout) for u in structure.units)
+        return slot, bn_stats_bytes(structure)
+    if structure.kind == "resnet_basic":
+        return max(b[1:]), bn_stats_bytes(structure)
     return max(b[1:]), 0
+
+
+def bn_stats_bytes(structure) -> int:
+    """The CNNs' batch-norm statistics held for the whole step: one aligned
+    mean/rstd pair (8 bytes per channel) per batch norm of every unit."""
+    tot = 0
+    for u in structure.units:
+        if u.kind in ("stem3", "stem7"):
+            tot += align(8 * u.cout)
+        elif u.kind == "basic":
+            tot += 2 * align(8 * u.cout)
+        elif u.kind == "bottleneck":
+            tot += 2 * align(8 * u.width) + (2 if u.proj else 1) * align(8 * u.cout)
+    return tot
 
 
 def layer_and_cut_bytes(structure):

@@ -17,20 +17,21 @@
 //
 // Static layout (B(c, s) = one bf16 [N, s, s, c] tensor, F = fp32, SB = a
 // mean/rstd pair, each rounded up to 256 bytes):
-//   stem   a = c | r | st                          q = dr (F) | dc
-//   block  a = c1 | r1 | c2 | r2 | c3 | [cp] | st1 | st2 | st3 | [stp]
+//   stem   a = c | r                               q = dr (F) | dc
+//   block  a = c1 | r1 | c2 | r2 | c3 | [cp]
 //          q = dc3/dc1 | dr2/dr1 (F) | dc2 | [dcp]
+//   fixed  every unit's batch-norm statistics (mean | rstd per BN), held for
+//          the whole step (the gradient region's fixed buffers)
 // With drop_bn_relu (the "drop bn-relu" plan of section 4.2: keep the
 // convolution outputs, form batch norm + ReLU again when needed) a block
-// keeps a = c1 | c2 | c3 | [cp] | st slots and q = r1 | r2 | (the above):
+// keeps a = c1 | c2 | c3 | [cp] and q = r1 | r2 | (the above):
 // its forward forms r1 and r2 in the gradient scratch (which no unit uses
 // outside its backward), and its backward forms them there again from c1,
 // c2 and the statistics with the same kernel, so every value and gradient
 // is the standard layout's bit for bit.
-// The st slots of a are reserved (PEAK counts them) but the statistics live
-// in operator workspace, per BN of every unit: a unit's first forward of the
-// step forms them and its re-runs, which see the same input bits, reuse them
-// instead of finalizing the same sums again.
+// A unit's first forward of the step forms its statistics and its re-runs,
+// which see the same input bits, reuse them instead of finalizing the same
+// sums again.
 // The boundary b_i is the unit's input (b_0 = the bf16 image batch).
 #include <algorithm>
 
@@ -54,8 +55,8 @@ class Bottleneck : public Net {
   std::vector<BUnit> u;
   int hw, hb;
   uint64_t ks_wbf = 0, ks_col = 0, ks_stats = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0,
-           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0, ks_kst = 0;
-  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics within ks_kst
+           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0;
+  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics in the fixed buffers
   uint64_t wpart_floats = 0;
 
   static uint64_t bf(int64_t m, int c) { return align256(uint64_t(m) * c * 2); }
@@ -88,7 +89,7 @@ class Bottleneck : public Net {
       s.b1 = add_param("u0.beta", C0);
       u.push_back(s);
       const int64_t m = int64_t(N) * side * side;
-      a.push_back(2 * bf(m, C0) + align256(8ull * C0));
+      a.push_back(2 * bf(m, C0));
       q.push_back(f32(m, C0) + bf(m, C0));
       b.push_back(bf(int64_t(N) * pooled * pooled, C0));
     }
@@ -117,9 +118,8 @@ class Bottleneck : public Net {
         u.push_back(k);
         const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
         const uint64_t relus = bf(mi, w) + bf(mo, w);  // r1, r2
-        uint64_t av = bf(mi, w) + bf(mo, w) + bf(mo, cout) + 2 * align256(8ull * w) +
-                      align256(8ull * cout) + (drop ? 0 : relus);
-        if (k.proj) av += bf(mo, cout) + align256(8ull * cout);
+        uint64_t av = bf(mi, w) + bf(mo, w) + bf(mo, cout) + (drop ? 0 : relus);
+        if (k.proj) av += bf(mo, cout);
         a.push_back(av);
         q.push_back(std::max(bf(mo, cout), bf(mi, w)) + f32(mi, w) + bf(mo, w) +
                     (k.proj ? bf(mo, cout) : 0) + (drop ? relus : 0));
@@ -182,14 +182,16 @@ class Bottleneck : public Net {
     ks_lossn = take(4ull * N);
     ks_loss = take(4);
     // every unit's batch-norm statistics (st1 | st2 | st3 [| stp], the stem's
-    // st), kept from its first forward of the step for its re-runs
+    // st), formed by its first forward of the step and read by its re-runs
+    // and its backward: held for the whole step, so they are fixed buffers
+    // of the static layout (counted in the peak), not operator workspace
     uint64_t kst = 0;
     for (const BUnit &k : u) {
       kst_off.push_back(kst);
       kst += k.stem ? align256(8ull * C0)
                     : 2 * align256(8ull * k.w) + (k.proj ? 2 : 1) * align256(8ull * k.cout);
     }
-    ks_kst = take(kst);
+    grad_extra = kst;
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
   }
@@ -208,7 +210,7 @@ class Bottleneck : public Net {
                        : which == 1 ? align256(8ull * k.w)
                        : which == 2 ? 2 * align256(8ull * k.w)
                                     : 2 * align256(8ull * k.w) + align256(8ull * k.cout);
-    return reinterpret_cast<float *>(c.ks + ks_kst + kst_off[size_t(i)] + o);
+    return reinterpret_cast<float *>(c.gextra + kst_off[size_t(i)] + o);
   }
   float *ksf(StepCtx &c, uint64_t o) const { return reinterpret_cast<float *>(c.ks + o); }
 

@@ -10,20 +10,21 @@
 //
 // Static layout per unit (T = one [N, Ho, Ho, Cout] f32 tensor, SB = a BN
 // mean/rstd pair of Cout floats each, both rounded up to 256 bytes):
-//   stem   a = c | st            q = dc
-//   block  a = c1 | r1 | c2 | st1 | st2     q = two T buffers
+//   stem   a = c                 q = dc
+//   block  a = c1 | r1 | c2      q = two T buffers
+//   fixed  every unit's SBs, held for the whole step (the gradient region's
+//          fixed buffers, counted in the peak)
 // The second convolution reads c1 and forms r1 = relu(bn1(c1)) as it loads
 // it; when r1 is kept it stores r1 as well (no separate batch-norm pass).
-// With drop_bn_relu the blocks keep only the convolution outputs, a = c1 | c2
-// | st1 | st2, and r1 is formed on the fly from c1 and its statistics
+// With drop_bn_relu the blocks keep only the convolution outputs, a = c1 | c2,
+// and r1 is formed on the fly from c1 and its statistics
 // wherever it is read (the second convolution's input, its data gradient's
 // ReLU mask and its weight gradient's input): the "drop bn-relu" memory plan
 // the paper applies to the conv-BN-activation pipeline (section 4.2), with the
 // same bits as the stored r1.
-// The st slots of a are reserved (PEAK counts them) but the statistics live
-// in operator workspace, one pair per BN of every unit: a unit's first
-// forward of the step forms them and its re-runs, which see the same input
-// bits, reuse them instead of finalizing the same sums again.
+// A unit's first forward of the step forms its statistics and its re-runs,
+// which see the same input bits, reuse them instead of finalizing the same
+// sums again.
 // The boundary b_i is the unit's input tensor (b_0 = the image batch).
 #include <algorithm>
 
@@ -46,8 +47,8 @@ class ResNetBasic : public Net {
   int hw, hb;  // head parameter indices
   // operator workspace offsets (bytes)
   uint64_t ks_loss = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0, ks_pooled = 0, ks_dlog = 0,
-           ks_lossn = 0, ks_kst = 0;
-  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics within ks_kst
+           ks_lossn = 0;
+  std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics in the fixed buffers
 
   explicit ResNetBasic(const ckpt_net_desc &d) {
     desc = d;
@@ -65,7 +66,7 @@ class ResNetBasic : public Net {
       s.g1 = add_param("u0.gamma", C0);
       s.b1 = add_param("u0.beta", C0);
       u.push_back(s);
-      a.push_back(T(S, C0) + align256(8ull * C0));
+      a.push_back(T(S, C0));
       q.push_back(T(S, C0));
       b.push_back(T(S, C0));
     }
@@ -85,7 +86,7 @@ class ResNetBasic : public Net {
         k.b2 = add_param(p + "beta2", cout);
         u.push_back(k);
         const uint64_t t = T(k.hout, cout);
-        a.push_back((drop ? 2 : 3) * t + 2 * align256(8ull * cout));
+        a.push_back((drop ? 2 : 3) * t);
         q.push_back(2 * t);
         b.push_back(t);
         cin = cout;
@@ -131,13 +132,16 @@ class ResNetBasic : public Net {
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
     // every unit's batch-norm statistics (mean | rstd per BN, 256-byte
-    // aligned), kept from its first forward of the step for its re-runs
+    // aligned), formed by its first forward of the step and read by its
+    // re-runs and its backward: held for the whole step, so they are fixed
+    // buffers of the static layout (counted in the peak), not operator
+    // workspace
     uint64_t kst = 0;
     for (const Blk &k : u) {
       kst_off.push_back(kst);
       kst += (k.w2 >= 0 ? 2 : 1) * align256(8ull * k.cout);
     }
-    ks_kst = take(kst);
+    grad_extra = kst;
     ks_bytes = off;
     timed_family = "k_conv3x3< and k_conv3x3s<";
   }
@@ -145,7 +149,7 @@ class ResNetBasic : public Net {
   double *bnpart(StepCtx &c) const { return reinterpret_cast<double *>(c.ks + ks_bnpart); }
   // unit i's statistics: BN 1 (or the stem's), then BN 2 at + align256(8 cout)
   float *kst(const StepCtx &c, int32_t i) const {
-    return reinterpret_cast<float *>(c.ks + ks_kst + kst_off[size_t(i)]);
+    return reinterpret_cast<float *>(c.gextra + kst_off[size_t(i)]);
   }
 
   // a block's saved tensors: c1 | [r1] | c2 (then the reserved statistics slots)

@@ -54,7 +54,7 @@ def _run_pair(cfg, mode, budget):
     g = step.grads_host()
     gbytes = step.grads_bytes()
     op = PL.plan(st.n, lb, cb, budget, mode)
-    assert peak == PL.account(op, b, a, q).peak
+    assert peak == PL.account(op, b, a, q, *SZ.grad_layout(st)).peak
     assert stats["unit_forwards"] == PL.unit_forwards(op)
     step.run(step.plan(K.NONE))
     torch.cuda.synchronize()
@@ -220,7 +220,7 @@ def test_cifar110_drop_bn_relu_full_size_same_bits():
     l0, _, _ = keep.run(keep.plan(PL.SQRT, 0))
     l1, peak, _ = drop.run(drop.plan(PL.SQRT, 0))
     torch.cuda.synchronize()
-    assert peak == PL.account(PL.plan(st.n, lb, cb, 0, PL.SQRT), b, a, q).peak
+    assert peak == PL.account(PL.plan(st.n, lb, cb, 0, PL.SQRT), b, a, q, *SZ.grad_layout(st)).peak
     assert l1 == l0
     assert drop.grads_bytes() == keep.grads_bytes()
 

@@ -66,7 +66,7 @@ def test_resnet_step_parity_all_modes(case):
         loss, peak, stats = step.run(plan)
         torch.cuda.synchronize()
         op = PL.plan(n, lb, cb, budget, mode, user, flags)
-        assert peak == PL.account(op, b, a, q).peak, name
+        assert peak == PL.account(op, b, a, q, *SZ.grad_layout(st)).peak, name
         assert stats["unit_forwards"] == PL.unit_forwards(op), name
         assert abs(loss - loss_o) <= TOL * abs(loss_o), (name, loss, loss_o)
         g = step.grads_host()
@@ -100,6 +100,6 @@ def test_drop_bn_relu_same_bits(case):
         l1, peak, stats = drop.run(drop.plan(mode, budget))
         torch.cuda.synchronize()
         op = PL.plan(n, lb, cb, budget, mode)
-        assert peak == PL.account(op, b, a, q).peak, mode
+        assert peak == PL.account(op, b, a, q, *SZ.grad_layout(st)).peak, mode
         assert l1 == l0, mode
         assert drop.grads_bytes() == keep.grads_bytes(), mode

@@ -223,7 +223,8 @@ def test_size_tables_match_kept_tensors(cfg):
     """a_i and b_{i+1} equal the aligned bytes of what the oracle keeps, each
     tensor counted in the dtype the static layout stores it in: bf16 for the
     bottleneck net's activations and the LSTM's h, fp32 otherwise (batch-norm
-    (mean, rstd) pairs as one block).  The bottleneck stem's max-pool window
+    (mean, rstd) pairs, which the CNNs hold for the whole step, in the
+    layout's fixed buffers instead of a_i).  The bottleneck stem's max-pool window
     choice ("arg") is not kept: the backward finds the window's first maximum
     again from the pooled output.  The drop bn-relu layouts keep no relu(bn(.))
     output of a block (the basic block's r1, the bottleneck's r1 and r2)."""
@@ -234,8 +235,6 @@ def test_size_tables_match_kept_tensors(cfg):
     drop = cfg.get("drop_bn_relu")
 
     def nbytes(name, v, half=False):
-        if isinstance(v, tuple):          # BN (mean, rstd) pair: one fp32 block
-            return SZ.align(sum(4 * t.size for t in v))
         return SZ.align((2 if half else 4) * v.size)
 
     def boundary(x):
@@ -245,6 +244,7 @@ def test_size_tables_match_kept_tensors(cfg):
 
     x = chain.x0(d["input"])
     assert boundary(x) == b[0]
+    stats_kept = 0
     for i in range(chain.n):
         y, saved, _ = chain.units[i].fwd(x, chain.P(i), chain.ext(i, d["input"], d["target"]))
         kept = 0
@@ -254,10 +254,16 @@ def test_size_tables_match_kept_tensors(cfg):
             for nm, v in saved.items():
                 if nm == "arg" or (drop and nm in ("r1", "r2")):
                     continue
+                if isinstance(v, tuple):  # BN (mean, rstd): held step-long, in the fixed buffers
+                    stats_kept += SZ.align(sum(4 * t.size for t in v))
+                    continue
                 kept += nbytes(nm, v, kind == "resnet_bottleneck")
         assert kept == a[i], (i, kept, a[i])
         assert boundary(y) == b[i + 1]
         x = y
+    # the batch-norm statistics of every unit are the layout's fixed buffers
+    assert SZ.grad_layout(d["structure"])[1] == (stats_kept if kind.startswith("resnet") else
+                                                 SZ.grad_layout(d["structure"])[1])
 
 
 # ---- appendix-A search over the budget ----------------------------------

@@ -968,9 +968,36 @@ __global__ __launch_bounds__(256) void k_sum_partials(const float *__restrict__ 
   }
 }
 
+// The same sum when nb is at most 16: k_sum_partials then gives each of the
+// first nb thread slices one partial and adds the slices in order, i.e.
+// ((0 + part[0][e]) + part[1][e]) + ..., which this kernel forms directly,
+// four consecutive e per thread (one 16-byte load per partial).
+__global__ __launch_bounds__(256) void k_sum_partials_seq(const float4 *__restrict__ part, int nb,
+                                                          int E4, float4 *__restrict__ out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= E4) return;
+  float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int b = 0; b < nb; ++b) {
+    const float4 v = part[size_t(b) * E4 + i];
+    t.x += v.x;
+    t.y += v.y;
+    t.z += v.z;
+    t.w += v.w;
+  }
+  out[i] = t;
+}
+
 }  // namespace
 
 void sum_partials(hipStream_t st, const float *part, int nb, int E, float *out) {
+  if (nb <= 16 && E % 4 == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0 &&
+      (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
+    const int E4 = E / 4;
+    hipLaunchKernelGGL(k_sum_partials_seq, dim3((E4 + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<const float4 *>(part), nb, E4, reinterpret_cast<float4 *>(out));
+    return;
+  }
   if (E < 16 * 2048)
     hipLaunchKernelGGL((k_sum_partials<64>), dim3((E + 3) / 4), dim3(256), 0, st, part, nb, E, out);
   else

@@ -24,7 +24,7 @@
 //             k-contiguous bf16 operands side by side along k
 // Out-of-image taps read zero.
 //
-// Block = 256 threads = 4 wavefronts in a WM x WN grid; each wavefront owns a
+// Block = 4 or 8 wavefronts (256 or 512 threads) in a WM x WN grid; each wavefront owns a
 // (BM/WM) x (BN/WN) tile of 16x16 accumulators.  K advances in slices of 32
 // through double-buffered LDS, with the global loads of a slice issued two
 // slices ahead.  A k-contiguous operand is stored [row][k], so every lane
@@ -45,6 +45,7 @@
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
+#include <utility>
 
 #include "kernels.h"
 #include "launch.h"
@@ -290,26 +291,38 @@ __device__ __forceinline__ void load_lds16(const void *src, unsigned char *lds_w
 // of this wavefront are outstanding (the other counters left alone)
 constexpr int vmcnt_le(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
 
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), unrolled
+template <class F, int... I>
+__device__ __forceinline__ void unroll_seq(F &f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void unroll(F &&f) {
+  unroll_seq(f, std::make_integer_sequence<int, N>{});
+}
+
 __device__ __forceinline__ u32x4 gatherB_wdgrad(const Args &p, int k, int n, int kend) {
   const int Co = 1 << p.cshift;
   const int tap = k >> p.cshift, co = k & (Co - 1);
   return masked16(p.B + (size_t(co) * p.R * p.R + tap) * p.N + n, (k < kend) & (n < p.N));
 }
 
-// DEEP (direct loop only): three LDS stages even where two workgroups would
-// then not fit a compute unit (for grids with no more tiles than compute
-// units, where a second workgroup per unit would not exist anyway)
+// STG (direct loop only): the number of LDS stages, 2 to 5; 0 chooses three
+// where two workgroups then still fit a compute unit's LDS, else two
 template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int EPI, int GA, int GB, bool SAFE,
-          bool DEEP = false>
-__global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
+          int STG = 0>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
   constexpr int TM = BM / WM / 16, TN = BN / WN / 16;  // 16x16 tiles per wavefront
-  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1, "wave grid");
+  constexpr int NT = 64 * WM * WN;                      // threads
+  static_assert((WM * WN == 4 || WM * WN == 8) && TM >= 1 && TN >= 1, "wave grid");
   static_assert(GA == G_DENSE || (AK && std::is_same<TA, __bf16>::value), "A gathers are k-contiguous bf16");
   static_assert(GB == G_DENSE || !BK, "B gathers are n-contiguous");
   constexpr int CHA = BM * KS / 8, CHB = BN * KS / 8;  // 8-element chunks per slice
-  constexpr int PA = (CHA + 255) / 256, PB = (CHB + 255) / 256;
+  constexpr int PA = (CHA + NT - 1) / NT, PB = (CHB + NT - 1) / NT;
   constexpr int WC = BN / WN;                           // columns per wavefront
   constexpr bool DIRECT = SAFE && std::is_same<TA, __bf16>::value;
+  static_assert(NT == 256 || (DIRECT && CHA % NT == 0 && CHB % NT == 0),
+                "eight wavefronts: the direct loop, whole chunk rounds");
   // staging row pitch (floats): padded for the register-staged loop; unpadded
   // for the direct loop, whose first stage then holds the staging rows
   constexpr int SP = DIRECT ? WC : WC + 4;
@@ -323,7 +336,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   //   8 elements): chunks are loaded into registers two slices ahead and
   //   written to a double-buffered padded LDS tile.
   // epilogue scratch: staging rows, and the column sums of BF16STATS / BNBWD
-  constexpr int EPI_SCR = cmax(4 * 16 * SP * 4,
+  constexpr int EPI_SCR = cmax(WM * WN * 16 * SP * 4,
                                cmax(EPI == GEMM_EPI_BF16STATS ? WM * 4 * 2 * BN * 8 : 0,
                                     EPI == GEMM_EPI_BNBWD ? WM * (64 / (WC / 4)) * 2 * BN * 8 : 0));
   // ROWSOFTMAX: each wavefront column's (max, sum of exp) per row of the tile
@@ -358,7 +371,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   if constexpr (GA == GA_FWD || GA == GA_DGRAD) {
 #pragma unroll
     for (int c = 0; c < PA; ++c) {
-      const int e = min(tid + c * 256, CHA - 1);
+      const int e = min(tid + c * NT, CHA - 1);
       const int m = m0 + e / (KS / 8);
       rpix[c] = GA == GA_FWD ? row_pixel(p, m, p.Ho, p.Wo) : row_pixel(p, m, p.H, p.W);
     }
@@ -366,7 +379,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
   if constexpr (GB == GB_WGRAD) {
 #pragma unroll
     for (int c = 0; c < PB; ++c) {
-      const int e = min(tid + c * 256, CHB - 1);
+      const int e = min(tid + c * NT, CHB - 1);
       ctap[c] = col_tap(p, n0 + (e % (BN / 8)) * 8);
     }
   }
@@ -391,15 +404,36 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
     //     logical row-group g stored in slot g ^ (2 (k & 3) mod chunks per
     //     row).
     constexpr int SZA1 = BM * KS * 2, SZB1 = BN * KS * 2;
-    // three stages when two workgroups still fit in a compute unit's 160 KB
-    // of LDS with them (or DEEP), else two (latency is then hidden by the
-    // other workgroup)
-    constexpr int NS = (DEEP || direct_three_stages(BM, BN, EPI_SCR)) ? 3 : 2;
-    __shared__ __align__(1024) unsigned char sa0[SZA1], sa1[SZA1], sa2[NS == 3 ? SZA1 : 1];
-    __shared__ __align__(1024) unsigned char sb0[SZB1], sb1[SZB1], sb2[NS == 3 ? SZB1 : 1];
+    // stages: more slices in flight hide more of the load latency, fewer
+    // leave LDS for a second workgroup per compute unit
+    constexpr int NS = STG ? STG : (direct_three_stages(BM, BN, EPI_SCR) ? 3 : 2);
+    static_assert(NS >= 2 && NS <= 5, "two to five stages");
+    static_assert((NS - 2) * (PA + PB) <= 63, "loads in flight fit the vector-memory counter");
+    __shared__ __align__(1024) unsigned char sa0[SZA1], sa1[SZA1], sa2[NS > 2 ? SZA1 : 1],
+        sa3[NS > 3 ? SZA1 : 1], sa4[NS > 4 ? SZA1 : 1];
+    __shared__ __align__(1024) unsigned char sb0[SZB1], sb1[SZB1], sb2[NS > 2 ? SZB1 : 1],
+        sb3[NS > 3 ? SZB1 : 1], sb4[NS > 4 ? SZB1 : 1];
     __shared__ __align__(16) unsigned char sepi[EPI_SCR <= SZA1 ? 1 : EPI_SCR];
     if constexpr (EPI_SCR <= SZA1) scr = sa0;
     else scr = sepi;
+    // stage i's arrays (i a compile-time constant: each stage is its own
+    // object, so the compiler knows which loads an LDS read waits for)
+    auto stage_a = [&](auto I) -> unsigned char * {
+      constexpr int i = decltype(I)::value;
+      if constexpr (i == 0) return sa0;
+      else if constexpr (i == 1) return sa1;
+      else if constexpr (i == 2) return sa2;
+      else if constexpr (i == 3) return sa3;
+      else return sa4;
+    };
+    auto stage_b = [&](auto I) -> unsigned char * {
+      constexpr int i = decltype(I)::value;
+      if constexpr (i == 0) return sb0;
+      else if constexpr (i == 1) return sb1;
+      else if constexpr (i == 2) return sb2;
+      else if constexpr (i == 3) return sb3;
+      else return sb4;
+    };
     // GB_WGRAD: the tap and channel of each chunk's (swizzled) column, fixed
     // for the whole k loop (the swizzle depends on the chunk's row in the
     // slice, not on the slice)
@@ -408,17 +442,17 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
 #pragma unroll
       for (int c = 0; c < PB; ++c) {
         constexpr int RC = BN / 8;
-        const int e = c * 256 + tid, kr = e / RC;
+        const int e = c * NT + tid, kr = e / RC;
         ctapd[c] = col_tap(p, n0 + ((e % RC) ^ ((2 * (kr & 3)) & (RC - 1))) * 8);
       }
     }
 
-    // chunk c*256 + tid of slice s into the stage arrays la, lb
+    // chunk c*NT + tid of slice s into the stage arrays la, lb
     auto issue = [&](int s, unsigned char *la, unsigned char *lb) {
       const int k0 = kslice(s);
 #pragma unroll
       for (int c = 0; c < PA; ++c) {
-        const int e = c * 256 + tid;
+        const int e = c * NT + tid;
         const void *src;
         if (AK) {
           const int mr = e >> 3, kc = ((e & 7) ^ (mr & 7)) * 8;
@@ -440,11 +474,11 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
           const int kk = k0 + kr, m = m0 + mc;
           src = src16(A + size_t(kk) * p.lda + m, (kk < kend) & (m < p.M));
         }
-        load_lds16(src, la + (c * 256 + wave * 64) * 16);
+        load_lds16(src, la + (c * NT + wave * 64) * 16);
       }
 #pragma unroll
       for (int c = 0; c < PB; ++c) {
-        const int e = c * 256 + tid;
+        const int e = c * NT + tid;
         const void *src;
         if (BK) {
           const int nr = e >> 3, kc = ((e & 7) ^ (nr & 7)) * 8;
@@ -462,7 +496,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
             src = src16(p.B + size_t(kk) * p.ldb + n, (kk < kend) & (n < p.N));
           }
         }
-        load_lds16(src, lb + (c * 256 + wave * 64) * 16);
+        load_lds16(src, lb + (c * NT + wave * 64) * 16);
       }
     };
     // one k step of 32 from stage (sa, sb): the MFMA operands, swizzled back
@@ -501,49 +535,26 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(Args p) {
             acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
       }
     };
-    if constexpr (NS == 3) {
-      // Slice kt sits in stage kt % 3.  At step kt each wavefront waits until
-      // only the next slice's loads are outstanding (its own share of slice
-      // kt has landed), then the barrier makes every share visible and tells
-      // that every wavefront is done with slice kt - 1, whose stage then
-      // takes slice kt + 2.  (A bare s_barrier: __syncthreads' fence would
-      // wait for every load in flight.)
-      issue(0, sa0, sb0);
-      issue(1, sa1, sb1);
-      auto step = [&](int kt, const unsigned char *ra, const unsigned char *rb, unsigned char *wa,
-                      unsigned char *wb) {
-        __builtin_amdgcn_s_waitcnt(vmcnt_le(PA + PB));
-        __builtin_amdgcn_s_barrier();
-        issue(kt + 2, wa, wb);
-        compute(ra, rb);
-      };
-      int kt = 0;
-      for (; kt + 3 <= nk; kt += 3) {
-        step(kt, sa0, sb0, sa2, sb2);
-        step(kt + 1, sa1, sb1, sa0, sb0);
-        step(kt + 2, sa2, sb2, sa1, sb1);
-      }
-      if (kt < nk) step(kt, sa0, sb0, sa2, sb2);
-      if (kt + 1 < nk) step(kt + 1, sa1, sb1, sa0, sb0);
-    } else {
-      // two stages: slice kt in stage kt % 2; at step kt every load of slice
-      // kt has landed, and after the barrier the other stage (slice kt - 1)
-      // takes slice kt + 1
-      issue(0, sa0, sb0);
-      auto step = [&](int kt, const unsigned char *ra, const unsigned char *rb, unsigned char *wa,
-                      unsigned char *wb) {
-        __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
-        __builtin_amdgcn_s_barrier();
-        issue(kt + 1, wa, wb);
-        compute(ra, rb);
-      };
-      int kt = 0;
-      for (; kt + 2 <= nk; kt += 2) {
-        step(kt, sa0, sb0, sa1, sb1);
-        step(kt + 1, sa1, sb1, sa0, sb0);
-      }
-      if (kt < nk) step(kt, sa0, sb0, sa1, sb1);
-    }
+    // Slice kt sits in stage kt % NS; NS - 1 slices are in flight ahead of
+    // the one being multiplied.  At step kt each wavefront waits until only
+    // the loads of the next NS - 2 slices are outstanding (its own share of
+    // slice kt has landed), then the barrier makes every share visible and
+    // tells that every wavefront is done with slice kt - 1, whose stage then
+    // takes slice kt + NS - 1.  (A bare s_barrier: __syncthreads' fence
+    // would wait for every load in flight.)
+    unroll<NS - 1>([&](auto J) { issue(decltype(J)::value, stage_a(J), stage_b(J)); });
+    auto step = [&](int kt, auto J) {
+      constexpr int w = (decltype(J)::value + NS - 1) % NS;
+      __builtin_amdgcn_s_waitcnt(vmcnt_le((NS - 2) * (PA + PB)));
+      __builtin_amdgcn_s_barrier();
+      issue(kt + NS - 1, stage_a(std::integral_constant<int, w>{}), stage_b(std::integral_constant<int, w>{}));
+      compute(stage_a(J), stage_b(J));
+    };
+    int kt = 0;
+    for (; kt + NS <= nk; kt += NS) unroll<NS>([&](auto J) { step(kt + decltype(J)::value, J); });
+    unroll<NS - 1>([&](auto J) {
+      if (kt + decltype(J)::value < nk) step(kt + decltype(J)::value, J);
+    });
     // every load (the re-reads past the range included) has landed and every
     // wavefront is done with the stages before the epilogue reuses them
     __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
@@ -953,54 +964,55 @@ inline Tile tile_of(int M, int N) {
   return {64, 32};
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE, bool DEEP>
+template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE, int STG>
 void launch_epi_s(const Args &a, int epi, int splits, hipStream_t s) {
   dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
   if (epi == GEMM_EPI_ADD) {
-    launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+    launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADD, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
     return;
   }
   if constexpr (std::is_same<TA, __bf16>::value) {
     if (epi == GEMM_EPI_ADDMASK) {
-      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ADDMASK, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
       return;
     }
     if (epi == GEMM_EPI_BF16STATS) {
-      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+      launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BF16STATS, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
       return;
     }
     // instantiated for the operand forms the host wrappers accept only
     if constexpr (AK && !BK && SAFE) {
       if (epi == GEMM_EPI_BNBWD) {
-        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_BNBWD, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
         return;
       }
     }
     if constexpr (AK && BK && SAFE && GA == G_DENSE && GB == G_DENSE) {
       if (epi == GEMM_EPI_ROWSOFTMAX) {
-        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+        launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_ROWSOFTMAX, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
         return;
       }
     }
   }
-  launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE, DEEP>), grid, dim3(256), 0, s, a);
+  launch_timed((k_gemm_bf16<BM, BN, WM, WN, AK, BK, TA, GEMM_EPI_STORE, GA, GB, SAFE, STG>), grid, dim3(64 * WM * WN), 0, s, a);
 }
 
-// The direct loop of the two largest tiles runs with three stages (DEEP)
-// when the grid has no more tiles than the device has compute units, else
-// with two, so that two workgroups share a unit.
+// The direct loop of the two largest tiles runs with three stages when the
+// grid has no more tiles than the device has compute units (a second
+// workgroup per unit would not exist anyway), else with two, so that two
+// workgroups share a unit.
 template <int BM, int BN, int WM, int WN, bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
 void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
   constexpr bool direct = SAFE && std::is_same<TA, __bf16>::value;
-  constexpr int scr = cmax(4 * 16 * (BN / WN) * 4, 4 * 2 * BN * 8 * 4);  // a bound on any epilogue's scratch
+  constexpr int scr = cmax(WM * WN * 16 * (BN / WN) * 4, 4 * 2 * BN * 8 * 4);  // a bound on any epilogue's scratch
   if constexpr (direct && !direct_three_stages(BM, BN, scr)) {
     const long tiles = long((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM) * splits;
     if (tiles <= 256) {
-      launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, true>(a, epi, splits, s);
+      launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, 3>(a, epi, splits, s);
       return;
     }
   }
-  launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, false>(a, epi, splits, s);
+  launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, 0>(a, epi, splits, s);
 }
 
 template <bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>

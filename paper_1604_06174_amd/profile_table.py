@@ -1,6 +1,8 @@
 """Per-launch-kind table of the bf16 GEMM family from a rocprofv3 kernel trace.
 
     python -m paper_1604_06174_amd.profile_table <run_kernel_trace.csv> <gemm launch log>
+    python -m paper_1604_06174_amd.profile_table --counters <gemm launch log> <short-step log> \
+        <fetch factor> <write factor> <run_counter_collection.csv> ...
 
 The launch log lists every bf16 GEMM launch of one training step with its
 shape (tests/hostcheck/run.py --gemm-log <workload> <file> writes it from a
@@ -12,6 +14,11 @@ and the result written once, split-K partials not counted), the average
 duration over every traced dispatch of that kind, and the fraction of the
 kind's roofline time max(flops / 2.5 PFLOP/s, bytes / 8 TB/s) that duration
 reaches.  The family line weights every kind by its launches per step.
+
+The --counters form joins rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE,
+SQ_VALU_MFMA_BUSY_CYCLES) of a shorter step -- a bottleneck net with fewer
+blocks per stage, so the same launch kinds -- with that step's launch log in
+dispatch order, and weights each kind by its launches in the full step.
 """
 from __future__ import annotations
 
@@ -126,5 +133,86 @@ def main(trace, log):
           f"({tot_b / tot_t / HBM:.3f} of HBM)")
 
 
+def counters_per_kind(csv_paths, short_log):
+    """Mean counter values per launch kind, from rocprofv3 counter runs of a
+    step whose bf16 GEMM launches short_log lists in order.  The last
+    len(short_log) k_gemm_bf16 dispatches of each run are that step; each is
+    checked against its log line's grid before it is used."""
+    rows = read_log(short_log)
+    acc = defaultdict(lambda: defaultdict(list))
+    for path in csv_paths:
+        per = defaultdict(dict)  # dispatch -> counter -> value (summed over dimensions)
+        meta = {}
+        with open(path) as f:
+            for d in csv.DictReader(f):
+                if "k_gemm_bf16" not in d["Kernel_Name"]:
+                    continue
+                did = int(d["Dispatch_Id"])
+                per[did][d["Counter_Name"]] = per[did].get(d["Counter_Name"], 0.0) + float(d["Counter_Value"])
+                meta[did] = (int(d["Grid_Size"]), int(d["Workgroup_Size"]),
+                             int(d["End_Timestamp"]) - int(d["Start_Timestamp"]))
+        ids = sorted(per)
+        if len(ids) < len(rows):
+            raise SystemExit(f"{path}: {len(ids)} GEMM dispatches, the step has {len(rows)}")
+        for r, did in zip(rows, ids[-len(rows):]):
+            grid, wg, dur = meta[did]
+            gx, gy, gz = r["grid"]
+            if grid != gx * gy * gz * wg:
+                raise SystemExit(f"{path}: dispatch {did} grid {grid} does not match launch {r}")
+            k = (r["name"], r["grid"])
+            for c, v in per[did].items():
+                acc[k][c].append(v)
+            acc[k]["_dur"].append(dur * 1e-9)
+    return {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in acc.items()}
+
+
+def counters_main(log, short_log, csv_paths, fetch_factor, write_factor):
+    """Per launch kind of `log` (the full step), HBM bytes from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch, scaled by the copy calibration) and the MFMA
+    busy fraction, measured on the shorter step of short_log; the family line
+    weights each kind by its launches in `log`."""
+    kinds = counters_per_kind(csv_paths, short_log)
+    full = defaultdict(lambda: dict(n=0))
+    for r in read_log(log):
+        e = full[(r["name"], r["grid"])]
+        e["n"] += 1
+        e["r"] = r
+    n_all = n_cov = 0
+    tr = alg = busy_w = dur_w = 0.0
+    out = []
+    for k, e in full.items():
+        n_all += e["n"]
+        c = kinds.get(k)
+        if not c or "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+            continue
+        n_cov += e["n"]
+        fl, by = work(e["r"])
+        t = c["FETCH_SIZE"] * 1024 * fetch_factor + c["WRITE_SIZE"] * 1024 * write_factor
+        tr += e["n"] * t
+        alg += e["n"] * by
+        mb = c.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        if mb is not None:
+            busy_w += e["n"] * mb
+            dur_w += e["n"] * c["_dur"] * 2.4e9 * 1024
+        out.append((e["n"] * t, e["r"], e["n"], by, t, (mb / (c["_dur"] * 2.4e9 * 1024)) if mb is not None else None))
+    out.sort(key=lambda x: -x[0])
+    print("| launches/step | tile x grid | epilogue | A / B | M x N x K | algorithmic MB | HBM MB (counters) "
+          "| HBM / algorithmic | MFMA busy |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for _, r, n, by, t, mb in out:
+        tile = r["name"].split("ILi")[1].split("E")[0] if "ILi" in r["name"] else "?"
+        print(f"| {n} | {tile} {r['grid'][0]}x{r['grid'][1]}x{r['grid'][2]} | {EPI.get(r['epi'], r['epi'])} | "
+              f"{FORM[r['ga']]} / {FORM[r['gb']]} | {r['M']} x {r['N']} x {r['K']} | {by / 1e6:.1f} | "
+              f"{t / 1e6:.1f} | {t / by:.2f} | {'' if mb is None else f'{mb:.3f}'} |")
+    print(f"\nfamily: {n_all} launches per step, {n_cov} of them of a kind measured; HBM traffic per "
+          f"launch {tr / max(n_cov, 1):.0f} B (algorithmic {alg / max(n_cov, 1):.0f} B, ratio "
+          f"{tr / max(alg, 1):.3f})" + (f"; MFMA busy {busy_w / dur_w:.3f} of the counted kernels' time" if dur_w else ""))
+    return tr / max(n_cov, 1), n_cov, n_all
+
+
 if __name__ == "__main__":
-    main(sys.argv[1], sys.argv[2])
+    if len(sys.argv) > 1 and sys.argv[1] == "--counters":
+        # --counters <full-step log> <short-step log> <fetch factor> <write factor> <csv> [<csv> ...]
+        counters_main(sys.argv[2], sys.argv[3], sys.argv[6:], float(sys.argv[4]), float(sys.argv[5]))
+    else:
+        main(sys.argv[1], sys.argv[2])

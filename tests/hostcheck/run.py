@@ -2,7 +2,7 @@
 preloaded; tests/test_hostcheck.py does that).
 
     LD_PRELOAD=<asan runtime> python tests/hostcheck/run.py [--quick | --plant]
-    LD_PRELOAD=<asan runtime> python tests/hostcheck/run.py --gemm-log resnet1000 <file>
+    LD_PRELOAD=<asan runtime> python tests/hostcheck/run.py --gemm-log resnet1000 <file> [--stage-blocks 3,3,3,3 | --seq-len 512]
 
 1. Planner, budget search and gradient-graph fuzzing through the instrumented
    library, each result compared with the oracle (as the CPU ABI tests do on
@@ -394,12 +394,20 @@ def dry_runs(quick):
 def main():
     quick = "--quick" in sys.argv
     if "--gemm-log" in sys.argv:
-        # --gemm-log <workload> <file>: the workload's step (its default plan)
-        # with every bf16 GEMM launch written to <file>
+        # --gemm-log <workload> <file> [--stage-blocks a,b,c,d]: the
+        # workload's step (its default plan) with every bf16 GEMM launch
+        # written to <file>
         i = sys.argv.index("--gemm-log")
         name, path = sys.argv[i + 1], sys.argv[i + 2]
         os.environ["HC_GEMM_LOG"] = path
         cfg = dict(synth.WORKLOADS[name], name=name)
+        if "--seq-len" in sys.argv:
+            # a shorter LSTM with the same per-step launches
+            cfg["T"] = int(sys.argv[sys.argv.index("--seq-len") + 1])
+        if "--stage-blocks" in sys.argv:
+            # a shorter bottleneck net with the same launch shapes
+            v = sys.argv[sys.argv.index("--stage-blocks") + 1]
+            cfg["stage_blocks"] = tuple(int(t) for t in v.split(","))
         plan = {"greedy": (PL.GREEDY, "tenth", 0), "sqrt": (PL.SQRT, int(cfg.get("stride", 0)), 0),
                 "recursive": (PL.RECURSIVE, 0, 0)}[cfg["plan"]]
         dry_step(cfg, [plan])

@@ -436,7 +436,9 @@ class Bottleneck : public Net {
         gemm_bf16x(c.s, int(mi), k.cin, k.w, qA, false, k.w, true, Wb(c, k.W1), k.cin, false, dx,
                    k.cin, GEMM_EPI_ADDMASK, g, k.cin, nullptr, gx);
       }
-      tend(c, double(mi), k.cin, k.w, 2.0 * (double(mi) * k.w + double(k.w) * k.cin),
+      // ADDMASK also reads g (fp32) and the mask (bf16) once
+      tend(c, double(mi), k.cin, k.w,
+           2.0 * (double(mi) * k.w + double(k.w) * k.cin) + (k.proj ? 0.0 : 6.0 * double(mi) * k.cin),
            4.0 * double(mi) * k.cin);
     }
     if (k.proj) {

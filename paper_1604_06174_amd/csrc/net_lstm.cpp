@@ -122,7 +122,9 @@ class LstmNet : public Net {
             int ldd = 0, const float *bias = nullptr) {
     timer.begin(c.s);
     gemm_bf16(c.s, M, N, Kd, A, a32, lda, ak, Bm, ldb, bk, Cm, ldc, epi, D, ldd, bias);
-    timer.end(c.s, 2.0 * M * N * Kd, 2.0 * (double(M) * Kd + double(Kd) * N) + 4.0 * M * N);
+    // operands and product once; the ADD epilogue also reads D once
+    timer.end(c.s, 2.0 * M * N * Kd,
+              2.0 * (double(M) * Kd + double(Kd) * N) + (epi == GEMM_EPI_ADD ? 8.0 : 4.0) * M * N);
     c.launches += 1;
   }
   // split-K partial products into slices [z0, z0 + splits) of the partial buffer.

@@ -386,6 +386,181 @@ inline int ew_grid(int64_t work) {
   return int(g < 8192 ? (g < 1 ? 1 : g) : 8192);
 }
 
+// ---- operators of the node-level graph (standalone forms of the fused ones) ----
+
+// partial sums (sum x, sum x^2) per channel over this workgroup's pixels,
+// float64, stored channel-major [2][J][nb] as the convolutions' STATS
+// epilogue stores them; the same pixel split and lane tree as the backward
+// partials
+__global__ __launch_bounds__(256) void k_bn_stats_partials(int P, int J, int PB, const float *__restrict__ X,
+                                                           double *__restrict__ part) {
+  __shared__ double red[2][256][4];
+  const int CQ = J / 4, PL = 256 / CQ;
+  const int cq = threadIdx.x % CQ, pl = threadIdx.x / CQ;
+  const int c0 = cq * 4;
+  const int p0 = blockIdx.x * PB, p1 = min(P, p0 + PB);
+  double s1[4] = {0, 0, 0, 0}, s2[4] = {0, 0, 0, 0};
+  if (pl < PL) {
+    for (int p = p0 + pl; p < p1; p += 4 * PL) {
+      float4 x[4];
+      bool ok[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int pp = p + u * PL;
+        ok[u] = pp < p1;
+        x[u] = *reinterpret_cast<const float4 *>(X + size_t(ok[u] ? pp : p) * J + c0);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (!ok[u]) continue;
+        const float xv[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          s1[k] += double(xv[k]);
+          s2[k] += double(xv[k]) * double(xv[k]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    red[0][threadIdx.x][k] = s1[k];
+    red[1][threadIdx.x][k] = s2[k];
+  }
+  __syncthreads();
+  for (int w = PL / 2; w > 0; w >>= 1) {
+    if (pl < w) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        red[0][threadIdx.x][k] += red[0][threadIdx.x + w * CQ][k];
+        red[1][threadIdx.x][k] += red[1][threadIdx.x + w * CQ][k];
+      }
+    }
+    __syncthreads();
+  }
+  if (pl == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      part[size_t(c0 + k) * gridDim.x + blockIdx.x] = red[0][threadIdx.x][k];
+      part[(size_t(J) + c0 + k) * gridDim.x + blockIdx.x] = red[1][threadIdx.x][k];
+    }
+  }
+}
+
+// y = gamma (x - mean) rstd + beta (no activation)
+__global__ __launch_bounds__(256) void k_bn_norm(int64_t P, int J, const float *__restrict__ X,
+                                                 const float *__restrict__ st,
+                                                 const float *__restrict__ gamma,
+                                                 const float *__restrict__ beta, float *__restrict__ Y) {
+  const int CQ = J / 4;
+  const int64_t total = P * CQ;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c0 = int(e % CQ) * 4;
+    const int64_t o = (e / CQ) * J + c0;
+    const float4 x = *reinterpret_cast<const float4 *>(X + o);
+    const float xv[4] = {x.x, x.y, x.z, x.w};
+    float r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      r[k] = __builtin_fmaf(gamma[c0 + k], (xv[k] - st[c0 + k]) * st[J + c0 + k], beta[c0 + k]);
+    *reinterpret_cast<float4 *>(Y + o) = make_float4(r[0], r[1], r[2], r[3]);
+  }
+}
+
+// option-A shortcut: Y[n, h, w, c] = X[n, 2h, 2w, c] for c < Cx, 0 for the
+// appended channels (Y [N, H, W, J], X [N, 2H, 2W, Cx]); backward: DX[n, h,
+// w, c] = DY[n, h/2, w/2, c] at even h and w, 0 elsewhere
+__global__ __launch_bounds__(256) void k_shortcut_a(int64_t P, int H, int W, int J, int Cx,
+                                                    const float *__restrict__ X, float *__restrict__ Y) {
+  const int64_t total = P * J;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c = int(e % J);
+    const int64_t p = e / J;
+    const int64_t w = p % W, h = (p / W) % H, n = p / (int64_t(W) * H);
+    Y[e] = c < Cx ? X[((n * 2 * H + 2 * h) * 2 * W + 2 * w) * Cx + c] : 0.f;
+  }
+}
+__global__ __launch_bounds__(256) void k_shortcut_a_bwd(int64_t P, int H, int W, int J, int Cx,
+                                                        const float *__restrict__ DY,
+                                                        float *__restrict__ DX) {
+  // P = N * 2H * 2W input pixels
+  const int64_t total = P * Cx;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c = int(e % Cx);
+    const int64_t p = e / Cx;
+    const int64_t wi = p % (2 * W), hi = (p / (2 * W)) % (2 * H), n = p / (int64_t(4) * W * H);
+    DX[e] = ((wi | hi) & 1) ? 0.f : DY[((n * H + hi / 2) * W + wi / 2) * J + c];
+  }
+}
+
+// global average pool: Y[n, c] = (sum over p in order of X[n, p, c]) / HW;
+// backward: DX[n, p, c] = DY[n, c] / HW
+__global__ __launch_bounds__(256) void k_avgpool(int N, int HW, int C, const float *__restrict__ X,
+                                                 float *__restrict__ Y) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= N * C) return;
+  const int n = e / C, c = e % C;
+  const float inv = 1.0f / float(HW);
+  float s = 0.f;
+  for (int p = 0; p < HW; ++p) s += X[(size_t(n) * HW + p) * C + c];
+  Y[e] = s * inv;
+}
+__global__ __launch_bounds__(256) void k_avgpool_bwd(int64_t total, int HW, int C,
+                                                     const float *__restrict__ DY, float *__restrict__ DX) {
+  const float inv = 1.0f / float(HW);
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c = int(e % C);
+    const int64_t n = e / (int64_t(HW) * C);
+    DX[e] = DY[n * C + c] * inv;
+  }
+}
+
+// softmax cross-entropy of each row of logits [N, K] with its label: lossn[n]
+// = log(sum exp(l - max)) + max - l[label], G = (softmax - onehot) / N; one
+// workgroup per row (the same arithmetic as the fused head's)
+__global__ __launch_bounds__(256) void k_softmax_ce_rows(int N, int K, const float *__restrict__ L,
+                                                         const int *__restrict__ labels,
+                                                         float *__restrict__ G, float *__restrict__ lossn) {
+  __shared__ float red[256];
+  const int n = blockIdx.x, t = threadIdx.x;
+  const float *lg = L + size_t(n) * K;
+  float mx = -INFINITY;
+  for (int k = t; k < K; k += 256) mx = fmaxf(mx, lg[k]);
+  red[t] = mx;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float se = 0.f;
+  for (int k = t; k < K; k += 256) se += expf(lg[k] - mx);
+  red[t] = se;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] += red[t + w];
+    __syncthreads();
+  }
+  se = red[0];
+  const int lab = labels[n];
+  const bool lab_ok = lab >= 0 && lab < K;
+  if (t == 0) lossn[n] = lab_ok ? (logf(se) + mx) - lg[lab] : NAN;
+  const float invN = 1.0f / float(N);
+  for (int k = t; k < K; k += 256) {
+    const float p = expf(lg[k] - mx) / se;
+    G[size_t(n) * K + k] = (p - (k == lab ? 1.f : 0.f)) * invN;
+  }
+}
+
+// loss = (sum over n in order of lossn[n]) / N
+__global__ void k_loss_mean(int N, const float *__restrict__ lossn, float *__restrict__ loss) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  float s = 0.f;
+  for (int n = 0; n < N; ++n) s += lossn[n];
+  loss[0] = s / float(N);
+}
+
 }  // namespace
 
 int bn_partial_blocks(int64_t P, int J) {
@@ -439,6 +614,42 @@ void bn_apply(hipStream_t s, int res, int64_t P, int J, const float *Cv, const f
     hipLaunchKernelGGL((k_bn_apply<BN_RES_ID>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
   else
     hipLaunchKernelGGL((k_bn_apply<BN_RES_A>), dim3(g), dim3(256), 0, s, P, J, Cv, st, gamma, beta, X, H, W, Cx, Y);
+}
+
+void bn_stats(hipStream_t s, int64_t P, int J, const float *X, double *part, float *st) {
+  const int nb = bn_partial_blocks(P, J);
+  hipLaunchKernelGGL(k_bn_stats_partials, dim3(nb), dim3(256), 0, s, int(P), J, int(bn_pb(P, J)), X, part);
+  bn_finalize_fwd(s, part, nb, J, P, st, true);
+}
+
+void bn_norm(hipStream_t s, int64_t P, int J, const float *X, const float *st, const float *gamma,
+             const float *beta, float *Y) {
+  hipLaunchKernelGGL(k_bn_norm, dim3(ew_grid(P * (J / 4))), dim3(256), 0, s, P, J, X, st, gamma, beta, Y);
+}
+
+void shortcut_a(hipStream_t s, int N, int H, int W, int J, int Cx, const float *X, float *Y) {
+  const int64_t P = int64_t(N) * H * W;
+  hipLaunchKernelGGL(k_shortcut_a, dim3(ew_grid(P * J)), dim3(256), 0, s, P, H, W, J, Cx, X, Y);
+}
+
+void shortcut_a_bwd(hipStream_t s, int N, int H, int W, int J, int Cx, const float *DY, float *DX) {
+  const int64_t P = int64_t(N) * 4 * H * W;
+  hipLaunchKernelGGL(k_shortcut_a_bwd, dim3(ew_grid(P * Cx)), dim3(256), 0, s, P, H, W, J, Cx, DY, DX);
+}
+
+void avgpool(hipStream_t s, int N, int HW, int C, const float *X, float *Y) {
+  hipLaunchKernelGGL(k_avgpool, dim3((N * C + 255) / 256), dim3(256), 0, s, N, HW, C, X, Y);
+}
+
+void avgpool_bwd(hipStream_t s, int N, int HW, int C, const float *DY, float *DX) {
+  const int64_t total = int64_t(N) * HW * C;
+  hipLaunchKernelGGL(k_avgpool_bwd, dim3(ew_grid(total)), dim3(256), 0, s, total, HW, C, DY, DX);
+}
+
+void softmax_ce_rows(hipStream_t s, int N, int K, const float *L, const int *labels, float *G,
+                     float *lossn, float *loss) {
+  hipLaunchKernelGGL(k_softmax_ce_rows, dim3(N), dim3(256), 0, s, N, K, L, labels, G, lossn);
+  hipLaunchKernelGGL(k_loss_mean, dim3(1), dim3(64), 0, s, N, lossn, loss);
 }
 
 void bn_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const float *Ym,

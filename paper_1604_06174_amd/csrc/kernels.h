@@ -115,6 +115,22 @@ void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X,
 void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void *X, const float *Wf,
                           const float *bf, const int *labels, float *pooled, float *dlog,
                           float *lossn, float *G, float *dW, float *db, float *loss);
+// Standalone forms for node-level graphs (NHWC fp32, J a multiple of 4):
+// st = mean | rstd of X [P, J] (part: bn_partial_blocks(P, J) * 2 * J
+// doubles); Y = gamma (X - mean) rstd + beta; the option-A shortcut Y [N, H,
+// W, J] of X [N, 2H, 2W, Cx] and its backward DX [N, 2H, 2W, Cx]; global
+// average pool Y [N, C] of X [N, HW, C] and its backward; softmax
+// cross-entropy rows of logits L [N, K]: G = the mean loss's gradient with
+// respect to L, lossn = each row's loss, loss = their mean.
+void bn_stats(hipStream_t s, int64_t P, int J, const float *X, double *part, float *st);
+void bn_norm(hipStream_t s, int64_t P, int J, const float *X, const float *st, const float *gamma,
+             const float *beta, float *Y);
+void shortcut_a(hipStream_t s, int N, int H, int W, int J, int Cx, const float *X, float *Y);
+void shortcut_a_bwd(hipStream_t s, int N, int H, int W, int J, int Cx, const float *DY, float *DX);
+void avgpool(hipStream_t s, int N, int HW, int C, const float *X, float *Y);
+void avgpool_bwd(hipStream_t s, int N, int HW, int C, const float *DY, float *DX);
+void softmax_ce_rows(hipStream_t s, int N, int K, const float *L, const int *labels, float *G,
+                     float *lossn, float *loss);
 // sums[0..J) = mean(ds), sums[J..2J) = mean(ds xhat), dgamma, dbeta from the
 // backward partials (sum ds, sum ds xhat) of nb workgroups over m values, in
 // either layout (fp32 backward partials: channel-major; bf16: block-major)

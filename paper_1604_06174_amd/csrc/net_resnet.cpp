@@ -47,8 +47,22 @@ class ResNetBasic : public Net {
   int hw, hb;  // head parameter indices
   // operator workspace offsets (bytes)
   uint64_t ks_loss = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0, ks_pooled = 0, ks_dlog = 0,
-           ks_lossn = 0;
+           ks_lossn = 0, ks_nst = 0, ks_fcpart = 0;
   std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics in the fixed buffers
+
+  // ---- the network at operator granularity (node-level graph) ----
+  enum { ND_DATA, ND_CONV, ND_BN, ND_RELU, ND_ADD, ND_SHORT, ND_POOL, ND_FC, ND_LOSS };
+  struct GNode {
+    int op;
+    std::vector<int32_t> in;
+    uint64_t bytes;
+    int h, c;                 // output side and channels (POOL: c features; FC, LOSS: classes)
+    int hin, cin, stride;     // CONV, SHORT, POOL, FC: input side, channels, stride
+    int w = -1, g = -1, bt = -1;  // parameters (CONV: w; BN: g, bt)
+    uint64_t st = 0;          // BN: its statistics' offset in the operator workspace
+  };
+  std::vector<GNode> gn;
+  uint64_t nst_bytes = 0;
 
   explicit ResNetBasic(const ckpt_net_desc &d) {
     desc = d;
@@ -96,6 +110,7 @@ class ResNetBasic : public Net {
     hw = add_param("head.W", uint64_t(cin) * K);
     hb = add_param("head.b", uint64_t(K));
     n = int32_t(u.size());
+    build_nodes();
 
     // operator workspace: the largest partial-sum buffers any unit needs
     uint64_t bnpart = 0, wpart = 0;
@@ -131,6 +146,8 @@ class ResNetBasic : public Net {
     ks_pooled = take(4ull * N * CL);
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
+    ks_nst = take(nst_bytes);                                   // node graph: BN statistics
+    ks_fcpart = take(4ull * mlp_relu_row_blocks(N) * K);         // node graph: FC bias sums
     // every unit's batch-norm statistics (mean | rstd per BN, 256-byte
     // aligned), formed by its first forward of the step and read by its
     // re-runs and its backward: held for the whole step, so they are fixed
@@ -299,6 +316,185 @@ class ResNetBasic : public Net {
 
   const float *loss_ptr(const StepCtx &c) const override {
     return reinterpret_cast<const float *>(c.ks + ks_loss);
+  }
+
+  // Node graph, in topological order: 0 data; the stem conv, BN, ReLU; per
+  // block conv, BN, ReLU, conv, BN, [option-A shortcut of the block input at
+  // stride 2], add (BN output + shortcut), ReLU; then average pool, FC and the
+  // softmax cross-entropy loss, whose output is the loss gradient of the
+  // logits.  Output bytes are the tensors' exact sizes; the flags give what
+  // each operator's backward reads and whether it may run in place (section
+  // 3's minimum dependencies).  Every node runs its own operator (the fused
+  // chain kernels' arithmetic split into standalone conv, batch-norm,
+  // activation, add, pool, FC and loss kernels).
+  void build_nodes() {
+    auto T = [&](int h, int ch) { return uint64_t(N) * h * h * ch * 4; };
+    auto node = [&](GNode d) {
+      gn.push_back(std::move(d));
+      return int32_t(gn.size()) - 1;
+    };
+    auto conv_n = [&](int32_t x, int hin, int cin, int h, int cout, int stride, int w) {
+      GNode d{ND_CONV, {x}, T(h, cout), h, cout, hin, cin, stride};
+      d.w = w;
+      return node(d);
+    };
+    auto bn_n = [&](int32_t x, int h, int ch, int g, int bt) {
+      GNode d{ND_BN, {x}, T(h, ch), h, ch, h, ch, 1};
+      d.g = g;
+      d.bt = bt;
+      d.st = nst_bytes;
+      nst_bytes += align256(8ull * ch);
+      return node(d);
+    };
+    auto relu_n = [&](int32_t x, int h, int ch) { return node(GNode{ND_RELU, {x}, T(h, ch), h, ch, h, ch, 1}); };
+    int32_t x = node(GNode{ND_DATA, {}, T(S, 3), S, 3, S, 3, 1});
+    {
+      const Blk &k = u[0];
+      x = conv_n(x, S, 3, S, C0, 1, k.w1);
+      x = bn_n(x, S, C0, k.g1, k.b1);
+      x = relu_n(x, S, C0);
+    }
+    for (size_t i = 1; i < u.size(); ++i) {
+      const Blk &k = u[i];
+      int32_t y = conv_n(x, k.hin, k.cin, k.hout, k.cout, k.stride, k.w1);
+      y = bn_n(y, k.hout, k.cout, k.g1, k.b1);
+      y = relu_n(y, k.hout, k.cout);
+      y = conv_n(y, k.hout, k.cout, k.hout, k.cout, 1, k.w2);
+      y = bn_n(y, k.hout, k.cout, k.g2, k.b2);
+      int32_t sc = x;
+      if (k.stride != 1)
+        sc = node(GNode{ND_SHORT, {x}, T(k.hout, k.cout), k.hout, k.cout, k.hin, k.cin, k.stride});
+      y = node(GNode{ND_ADD, {y, sc}, T(k.hout, k.cout), k.hout, k.cout, k.hout, k.cout, 1});
+      x = relu_n(y, k.hout, k.cout);
+    }
+    const Blk &l = u.back();
+    const int32_t p = node(GNode{ND_POOL, {x}, uint64_t(N) * l.cout * 4, 1, l.cout, l.hout, l.cout, 1});
+    const int32_t f = node(GNode{ND_FC, {p}, uint64_t(N) * K * 4, 1, K, 1, l.cout, 1});
+    node(GNode{ND_LOSS, {f}, uint64_t(N) * K * 4, 1, K, 1, K, 1});
+  }
+
+  bool node_graph(NodeGraph &g) const override {
+    static const int32_t flag[] = {0,                                          // data
+                                   CKPT_NODE_GRAD_IN,                          // conv
+                                   CKPT_NODE_INPLACE | CKPT_NODE_GRAD_IN,      // bn
+                                   CKPT_NODE_INPLACE | CKPT_NODE_GRAD_OUT,     // relu
+                                   CKPT_NODE_INPLACE,                          // add
+                                   0,                                          // shortcut
+                                   0,                                          // pool
+                                   CKPT_NODE_GRAD_IN,                          // fc
+                                   CKPT_NODE_GRAD_OUT};                        // loss
+    g.ptr.assign(1, 0);
+    g.idx.clear();
+    g.flags.clear();
+    g.bytes.clear();
+    for (const GNode &d : gn) {
+      g.idx.insert(g.idx.end(), d.in.begin(), d.in.end());
+      g.ptr.push_back(int32_t(g.idx.size()));
+      g.flags.push_back(flag[d.op]);
+      g.bytes.push_back(d.bytes);
+    }
+    return true;
+  }
+
+  float *nst(StepCtx &c, const GNode &d) const { return reinterpret_cast<float *>(c.ks + ks_nst + d.st); }
+
+  void node_fwd(int32_t v, const std::vector<const void *> &ins, void *out, StepCtx &c) override {
+    const GNode &d = gn[size_t(v)];
+    float *y = static_cast<float *>(out);
+    const float *x = ins.empty() ? nullptr : static_cast<const float *>(ins[0]);
+    const int64_t np = int64_t(N) * d.h * d.h;
+    switch (d.op) {
+      case ND_DATA:
+        if (hipMemcpyAsync(y, c.input, d.bytes, hipMemcpyDeviceToDevice, c.s) != hipSuccess)
+          fail(CKPT_E_HIP, "train_step_graph: input copy failed");
+        break;
+      case ND_CONV:
+        conv(c, CONV_FWD, d.stride, CONV_EPI_STORE, x, P(c, d.w), y, d.h, d.h, d.hin, d.hin, d.cin, d.c,
+             nullptr, nullptr, 0, 0, 0, d.h, d.cin, d.c);
+        break;
+      case ND_BN:  // statistics (partials + finalize), then the affine map
+        bn_stats(c.s, np, d.c, x, bnpart(c), nst(c, d));
+        bn_norm(c.s, np, d.c, x, nst(c, d), P(c, d.g), P(c, d.bt), y);
+        c.launches += 2;
+        break;
+      case ND_RELU:
+        ew_relu(c.s, np * d.c, x, y);
+        break;
+      case ND_ADD:
+        ew_add(c.s, np * d.c, x, static_cast<const float *>(ins[1]), y);
+        break;
+      case ND_SHORT:
+        shortcut_a(c.s, N, d.h, d.h, d.c, d.cin, x, y);
+        break;
+      case ND_POOL:
+        avgpool(c.s, N, d.hin * d.hin, d.c, x, y);
+        break;
+      case ND_FC:
+        gemm_f32(c.s, N, K, d.cin, x, d.cin, false, P(c, hw), K, false, y, K, GEMM_EPI_BIAS, nullptr, 0,
+                 P(c, hb));
+        break;
+      case ND_LOSS:
+        softmax_ce_rows(c.s, N, K, x, static_cast<const int *>(c.target), y, ksf(c, ks_lossn),
+                        ksf(c, ks_loss));
+        c.launches += 1;
+        break;
+    }
+    c.launches += 1;
+  }
+
+  void node_bwd(int32_t v, const void *dyv, const void *yv, const std::vector<const void *> &ins, void *out,
+                StepCtx &c) override {
+    const GNode &d = gn[size_t(v)];
+    const float *dy = static_cast<const float *>(dyv);
+    float *o = static_cast<float *>(out);
+    const int64_t np = int64_t(N) * d.h * d.h;
+    switch (d.op) {
+      case ND_DATA:
+        return;  // the input has no gradient to form
+      case ND_CONV: {
+        const float *x = static_cast<const float *>(ins[0]);
+        if (d.in[0] != 0) {  // the stem's input is the image: no data gradient
+          conv(c, CONV_DGRAD, d.stride, CONV_EPI_STORE, dy, P(c, d.w), o, d.hin, d.hin, d.h, d.h, d.c,
+               d.cin, nullptr, nullptr, 0, 0, 0, d.h, d.cin, d.c);
+          c.launches += 1;
+        }
+        conv3x3_wgrad(c.s, d.stride, x, dy, ksf(c, ks_wpart), G(c, d.w), N, d.h, d.h, d.hin, d.hin, d.cin,
+                      d.c);
+        c.launches += 2;
+        return;
+      }
+      case ND_BN:
+        bn_backward(c.s, np, d.c, dy, nullptr, static_cast<const float *>(ins[0]), nst(c, d), P(c, d.g),
+                    bnpart(c), ksf(c, ks_sums), G(c, d.g), G(c, d.bt), o);
+        c.launches += 3;
+        return;
+      case ND_RELU:
+        ew_relu_bwd(c.s, np * d.c, dy, static_cast<const float *>(yv), o);
+        break;
+      case ND_ADD:  // both inputs receive dy
+        ew_copy(c.s, np * d.c, dy, o);
+        ew_copy(c.s, np * d.c, dy, o + np * d.c);
+        c.launches += 1;
+        break;
+      case ND_SHORT:
+        shortcut_a_bwd(c.s, N, d.h, d.h, d.c, d.cin, dy, o);
+        break;
+      case ND_POOL:
+        avgpool_bwd(c.s, N, d.hin * d.hin, d.c, dy, o);
+        break;
+      case ND_FC: {  // dx = dy W^T, dW = x^T dy, db = column sums of dy
+        const float *x = static_cast<const float *>(ins[0]);
+        gemm_f32(c.s, N, d.cin, K, dy, K, false, P(c, hw), K, true, o, d.cin, GEMM_EPI_STORE);
+        gemm_f32(c.s, d.cin, K, N, x, d.cin, true, dy, K, false, G(c, hw), K, GEMM_EPI_STORE);
+        mlp_colsum(c.s, N, K, dy, G(c, hb), ksf(c, ks_fcpart));
+        c.launches += 3;
+        break;
+      }
+      case ND_LOSS:  // the loss node's output is dL/d(logits) already
+        ew_copy(c.s, int64_t(N) * K, static_cast<const float *>(yv), o);
+        break;
+    }
+    c.launches += 1;
   }
 };
 

@@ -2,6 +2,7 @@
 
     python -m paper_1604_06174_amd.graph_memory [--workload cifar110]
     python -m paper_1604_06174_amd.graph_memory --workload mlp64 --run [--steps 20]
+    python -m paper_1604_06174_amd.graph_memory --workload cifar110 --run
 
 Builds the workload's forward graph at operator granularity, runs the
 library's graph planner (Alg. 2 gradient-graph construction + section 3's
@@ -11,10 +12,11 @@ segmented sublinear plan (every node mirrored except the outputs of every
 s-th block, s = ceil(sqrt(blocks))) -- and prints one JSON line per strategy
 with the planned bytes, the mirror nodes executed and the planning time.
 With --run (nets whose library object provides the node graph: the residual
-MLP) each plan is also executed on the GPU by train_step_graph -- synthetic
-inputs of the workload, a warm-up step, then --steps timed steps between HIP
-events -- and the line gains ms/step, the workspace bytes and the chain
-executor's no-checkpoint ms/step for comparison.
+MLP and the CIFAR-shaped ResNet) each plan is also executed on the GPU by
+train_step_graph -- synthetic inputs of the workload, a warm-up step, then
+--steps timed steps between HIP events -- and the line gains ms/step, the
+workspace bytes and, for comparison, the chain executor's ms/step and peak
+bytes without checkpoints and under its sqrt plan.
 """
 from __future__ import annotations
 
@@ -74,8 +76,11 @@ def main() -> int:
             torch.cuda.synchronize()
             return e0.elapsed_time(e1) / args.steps
 
-        none = step.plan(K.NONE)
-        chain_ms = timed(lambda: step.run(none, stream=s, want_loss=False))
+        chain = {}
+        for cname, cplan in (("no_ckpt", step.plan(K.NONE)), ("sqrt", step.plan(K.SQRT))):
+            ms = timed(lambda: step.run(cplan, stream=s, want_loss=False))
+            _, peak, _ = step.run(cplan, stream=s, want_loss=False)
+            chain[cname] = (round(ms, 4), round(peak / 1e9, 6))
     for name, mirror, strategy in strategies(g):
         t0 = time.perf_counter()
         plan = K.graph_plan(g["pred"], g["bytes"], g["flags"], mirror, strategy)
@@ -88,7 +93,9 @@ def main() -> int:
             gp = step.graph_plan(mirror, strategy)
             rec["ms_per_step"] = round(timed(lambda: step.run_graph(gp, stream=s, want_loss=False)), 4)
             rec["workspace_gb"] = round(step.net.graph_workspace_bytes(gp) / 1e9, 6)
-            rec["chain_no_ckpt_ms_per_step"] = round(chain_ms, 4)
+            for cname, (ms, gb) in chain.items():
+                rec[f"chain_{cname}_ms_per_step"] = ms
+                rec[f"chain_{cname}_peak_gb"] = gb
         print(json.dumps(rec), flush=True)
     return 0
 

@@ -9,7 +9,7 @@ preloaded; tests/test_hostcheck.py does that).
    the production library).
 2. Dry runs of whole training steps: every net kind at its full workload size
    (the 1000-layer bottleneck ResNet under its greedy plan among them) and at
-   small sizes under every plan mode, train_step_static, the node-graph step
+   small sizes under every plan mode, train_step_static, the node-graph steps
    and a recorded step, on fake device buffers sized exactly as the ABI
    documents.  The stand-in HIP runtime checks every kernel launch's pointers
    against those buffers (the bf16 GEMM's over each operand's whole extent).
@@ -342,7 +342,8 @@ def dry_step(cfg, plans, static=False, graph_step=False, record=False):
         by, fl = (C.c_uint64 * nn.value)(), (C.c_int32 * nn.value)()
         LIB.net_node_graph(net, C.byref(nn), C.byref(ne), ptr, idx, by, fl, nn.value, ne.value)
         for strategy in (0, 1, 2):
-            mirror = arr(C.c_int32, [1 if v % 3 == 2 else 0 for v in range(nn.value)])
+            mirror = arr(C.c_int32, [1 if 0 < v < nn.value - 1 and v % 3 == 2 else 0
+                                     for v in range(nn.value)])
             gp = vp()
             if not ok(LIB.graph_plan(nn.value, ptr, idx, by, fl, mirror, strategy, C.byref(gp)), "graph plan"):
                 continue
@@ -377,7 +378,7 @@ def dry_runs(quick):
                   stem_channels=16, image=32, batch=2, classes=10, drop_bn_relu=1,
                   name="bottleneck small drop bn-relu")]
     for cfg in small:
-        dry_step(cfg, ALL, static=True, graph_step=cfg["kind"] == "mlp", record=True)
+        dry_step(cfg, ALL, static=True, graph_step=cfg["kind"] in ("mlp", "resnet_basic"), record=True)
     full = [("resnet1000", [(PL.GREEDY, "tenth", 0), (PL.NONE, 0, 0)]),
             ("resnet1000 drop bn-relu", [(PL.GREEDY, "tenth", 0)]),
             ("cifar110", [(PL.SQRT, 0, 0)]), ("mlp64", [(PL.SQRT, 8, 0)]),
@@ -388,7 +389,7 @@ def dry_runs(quick):
         cfg = dict(synth.WORKLOADS[name.split()[0]], name=name)
         if name.endswith("drop bn-relu"):
             cfg["drop_bn_relu"] = 1
-        dry_step(cfg, plans, static=True)
+        dry_step(cfg, plans, static=True, graph_step=name == "cifar110")
 
 
 def main():

@@ -351,9 +351,30 @@ def test_mlp_node_graph_is_the_synth_graph(cfg):
     assert need >= p.info()["peak"]
 
 
+@pytest.mark.parametrize("cfg", [
+    dict(kind="resnet_basic", blocks_per_stage=1, base=4, batch=2, image=8, classes=5),
+    dict(kind="resnet_basic", blocks_per_stage=2, base=8, batch=3, image=12, classes=7),
+    dict(kind="resnet_basic", blocks_per_stage=18, base=16, batch=128, image=32, classes=10)])
+def test_resnet_node_graph_is_the_synth_graph(cfg):
+    # the CIFAR-shaped net's operator graph is the one the memory planner
+    # studies (stem, basic blocks with option-A shortcuts, pool, FC, loss)
+    from paper_1604_06174_amd.workload import net_for
+    net = net_for(cfg)
+    g = net.node_graph()
+    sg = SG.resnet_basic(cfg["blocks_per_stage"], cfg["base"], cfg["batch"], cfg["image"], cfg["classes"])
+    assert (g["pred"], g["bytes"], g["flags"]) == (sg["pred"], sg["bytes"], sg["flags"])
+    for mirror in (SG.mirror_none(sg), SG.mirror_bn_relu(sg), SG.mirror_segments(sg, 1)):
+        for strategy in (K.ALLOC_NONE, K.ALLOC_INPLACE, K.ALLOC_SHARE):
+            p = K.graph_plan(g["pred"], g["bytes"], g["flags"], mirror, strategy)
+            op = OG.plan(sg["pred"], sg["bytes"], sg["flags"], mirror, strategy)
+            assert p.info()["peak"] == op.peak
+            assert net.graph_workspace_bytes(p) >= op.peak
+
+
 def test_node_graph_errors():
     from paper_1604_06174_amd.workload import net_for
-    cnn = net_for(dict(kind="resnet_basic", blocks_per_stage=1, base=4, batch=2, image=8, classes=3))
+    cnn = net_for(dict(kind="resnet_bottleneck", stage_blocks=(1,), widths=(8,), stem_channels=8,
+                       image=16, batch=2, classes=3, expansion=4))
     with pytest.raises(K.CkptError) as ei:
         cnn.node_graph()
     assert ei.value.code == K.E_UNSUPPORTED

@@ -1,5 +1,6 @@
-"""GPU: training steps over the residual MLP's operator-level graph, planned by
-Alg. 2 (mirror nodes) and the section-3 allocator.
+"""GPU: training steps over operator-level graphs, planned by Alg. 2 (mirror
+nodes) and the section-3 allocator: the residual MLP's and the CIFAR-shaped
+ResNet's.
 
 For every mirror plan (none; ReLU results dropped; segments of 1 and 3 blocks
 kept; everything mirrored twice) and every allocation strategy (no
@@ -8,11 +9,20 @@ bit-identical to the chain executor's no-checkpoint step (whose parity with the
 oracle the MLP tests establish; the node operators perform the same float
 operations in the same order), the planned bytes equal the oracle planner's,
 and the numbers of forward, mirror and gradient nodes run equal the plan's.
+
+The ResNet's node operators are standalone conv, batch-norm (statistics, then
+the affine map), ReLU, add, option-A shortcut, pool, FC and softmax
+cross-entropy kernels, not the chain's fused ones, so its graph steps are held
+to the float64 oracle at the strict bar (1e-4 per tensor, on shapes first
+checked to be well posed at float32), and every plan and strategy must give the
+same bits as every other.
 """
+import numpy as np
 import pytest
 
 import synth
 from oracle import graph as OG
+from oracle import nets, units as U
 from paper_1604_06174_amd import ckpt as K
 from synth import graphs as SG
 
@@ -60,4 +70,57 @@ def test_graph_steps_match_chain_step(case):
             got = step.grads_host()
             bad = [k for k in ref_t if got[k].tobytes() != ref_t[k].tobytes()]
             assert not bad, f"{tag}: gradients differ from the chain step: {bad[:8]}"
+        print(f"  {mname}: planned {op.peak} B (sharing), {op.n_mirror} mirrors", flush=True)
+
+
+RES_CASES = {
+    "tiny": dict(kind="resnet_basic", blocks_per_stage=1, base=4, batch=2, image=8, classes=5, seed=61),
+    "ragged": dict(kind="resnet_basic", blocks_per_stage=2, base=8, batch=3, image=12, classes=7, seed=62),
+}
+TOL = 1e-4
+
+
+def _err(g, o):
+    g = np.asarray(g, np.float64).reshape(-1)
+    o = np.asarray(o, np.float64).reshape(-1)
+    return float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-30))
+
+
+@pytest.mark.parametrize("case", list(RES_CASES))
+def test_resnet_graph_steps_match_oracle(case):
+    import torch
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = RES_CASES[case]
+    print(f"[resnet graph step] case={case} cfg={cfg}", flush=True)
+    d = synth.make(cfg)
+    full = lambda prec: nets.full_storage_step(nets.Chain(d["structure"], d["params"], prec), d["input"],
+                                               d["target"])
+    loss_o, grads_o = full(U.F64)
+    _, grads_32 = full(U.Prec(np.float32))
+    cond = max(_err(grads_32[k], grads_o[k]) for k in grads_o)
+    assert cond < 2e-5, f"case not well posed at float32 ({cond:.2e})"
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    sg = SG.resnet_basic(cfg["blocks_per_stage"], cfg["base"], cfg["batch"], cfg["image"], cfg["classes"])
+    ref = None
+    for mname, mirror in _mirrors(sg).items():
+        for strategy in (K.ALLOC_NONE, K.ALLOC_INPLACE, K.ALLOC_SHARE):
+            tag = f"{case}/{mname}/{strategy}"
+            plan = step.graph_plan(mirror, strategy)
+            op = OG.plan(sg["pred"], sg["bytes"], sg["flags"], mirror, strategy)
+            step.grads.fill_(float("nan"))
+            loss, peak, stats = step.run_graph(plan)
+            torch.cuda.synchronize()
+            assert peak == op.peak, tag
+            kinds = [op.nodes[w].kind for w in op.order]
+            assert stats["unit_forwards"] == kinds.count(OG.FWD) + kinds.count(OG.MIRROR), tag
+            assert stats["unit_backwards"] == kinds.count(OG.GRAD), tag
+            assert abs(loss - loss_o) <= TOL * abs(loss_o), (tag, loss, loss_o)
+            g = step.grads_host()
+            worst = max((_err(g[k], v), k) for k, v in grads_o.items())
+            assert worst[0] <= TOL, (tag, worst)
+            gb = step.grads_bytes()
+            if ref is None:
+                ref = (loss, gb)
+                print(f"  worst gradient error {worst[0]:.2e} ({worst[1]}), loss {loss:.6f}", flush=True)
+            assert (loss, gb) == ref, f"{tag}: differs from the first plan's step"
         print(f"  {mname}: planned {op.peak} B (sharing), {op.n_mirror} mirrors", flush=True)

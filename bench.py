@@ -275,6 +275,7 @@ def main():
     run(plan, args.steps)
     torch.cuda.synchronize()
     kt = step.net.timing_read()
+    kr = step.net.timing_roofline(PEAK_TFLOPS[cfg.get("dtype", "f32")] * 1e12, HBM_GBS * 1e9)
     step.net.timing_enable(False)
 
     dtype = cfg.get("dtype", "f32")  # "bf16": bf16 GEMM operands, fp32 accumulation
@@ -302,7 +303,10 @@ def main():
             "kernel": kt["kernel"], "launches": kt["launches"],
             "avg_launch_us": round(kt["ms"] * 1e3 / max(kt["launches"], 1), 3),
             "flops_per_launch": kt["flops"] / max(kt["launches"], 1),
-            "tflops_algorithmic": round(tflops, 3), "hbm_gbs_algorithmic": round(gbs, 1)}
+            "tflops_algorithmic": round(tflops, 3), "hbm_gbs_algorithmic": round(gbs, 1),
+            # every launch against its own bound: sum of max(flops / peak, bytes / 8 TB/s)
+            # over the family's launches, over their measured time
+            "frac_of_roofline_time": round(kr["roofline_ms"] / kr["kernel_ms"], 4) if kr["kernel_ms"] > 0 else None}
 
     cpu = None
     sample = args.cpu_sample

@@ -481,6 +481,16 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
 int net_timing_enable(ckpt_net *net, int32_t enable);
 int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops, double *bytes,
                     char *name, int32_t cap);
+/*
+ * The same timed launches against their own rooflines: *roofline_ms = the sum
+ * over the launches of max(flops / peak_flops, bytes / peak_bytes_per_s) (the
+ * time each would take at the bound of its own arithmetic intensity), and
+ * *kernel_ms = their summed measured duration, so a family of launches with
+ * different bounds gets one fraction of its roofline, roofline_ms / kernel_ms.
+ * Peaks in flop/s and byte/s, both > 0 (CKPT_E_INVALID otherwise).
+ */
+int net_timing_roofline(ckpt_net *net, double peak_flops, double peak_bytes_per_s,
+                        double *roofline_ms, double *kernel_ms);
 
 /* ---- operator calls -----------------------------------------------------
  * The single operators the bf16 bottleneck units (section 5.2's deep residual

@@ -104,6 +104,8 @@ _sig("net_param_info", C.c_int, [C.c_void_p, C.c_int32, C.c_char_p, C.c_int32, _
 _sig("plan_accounting", C.c_int, [C.c_void_p, C.c_void_p, _u64p, _u64p, _u64p, _u64p])
 _sig("net_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
 _sig("net_timing_enable", C.c_int, [C.c_void_p, C.c_int32])
+_sig("net_timing_roofline", C.c_int, [C.c_void_p, C.c_double, C.c_double, C.POINTER(C.c_double),
+                                      C.POINTER(C.c_double)])
 _sig("net_timing_read", C.c_int, [C.c_void_p, _u64p, C.POINTER(C.c_double), C.POINTER(C.c_double),
                                   C.POINTER(C.c_double), C.c_char_p, C.c_int32])
 _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
@@ -160,7 +162,7 @@ EXPORTED = ["op_gemm_bf16_blocks", "op_gemm_bf16", "op_sum_partials", "op_conv_b
             "graph_plan_blocks", "graph_plan_free", "net_node_graph", "graph_workspace_bytes",
             "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
-            "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read",
+            "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read", "net_timing_roofline",
             "train_step", "train_step_static", "step_graph_create", "step_graph_launch", "step_graph_free"]
 
 
@@ -400,6 +402,12 @@ class Net:
                                     name, 64))
         return dict(launches=n.value, ms=ms.value, flops=fl.value, bytes=by.value,
                     kernel=name.value.decode())
+
+    def timing_roofline(self, peak_flops: float, peak_bytes_per_s: float) -> Dict:
+        r, k = C.c_double(), C.c_double()
+        _check(_lib.net_timing_roofline(self._h, float(peak_flops), float(peak_bytes_per_s), C.byref(r),
+                                        C.byref(k)))
+        return dict(roofline_ms=r.value, kernel_ms=k.value)
 
     def __del__(self):
         if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:

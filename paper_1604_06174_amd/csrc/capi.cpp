@@ -424,4 +424,17 @@ int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops
   });
 }
 
+int net_timing_roofline(ckpt_net *net, double peak_flops, double peak_bytes_per_s,
+                        double *roofline_ms, double *kernel_ms) {
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_timing_roofline");
+    if (!(peak_flops > 0) || !(peak_bytes_per_s > 0))
+      ckpt::fail(CKPT_E_INVALID, "net_timing_roofline: peaks must be positive");
+    auto &t = net->net->timer;
+    const double r = t.roofline_ms(peak_flops, peak_bytes_per_s);
+    if (roofline_ms) *roofline_ms = r;
+    if (kernel_ms) *kernel_ms = t.ms;
+  });
+}
+
 }  // extern "C"

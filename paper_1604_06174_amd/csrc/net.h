@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <memory>
 #include <string>
 #include <vector>
@@ -19,6 +20,7 @@ struct KernelTimer {
   bool enabled = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;
   std::vector<double> fl, by;
+  std::vector<double> lt, lf, lb;  // every harvested launch: ms, flops, bytes
   size_t used = 0;
   uint64_t launches = 0;
   double ms = 0, flops = 0, bytes = 0;
@@ -59,6 +61,9 @@ struct KernelTimer {
       ms += t;
       flops += fl[k];
       bytes += by[k];
+      lt.push_back(t);
+      lf.push_back(fl[k]);
+      lb.push_back(by[k]);
       ++launches;
     }
     used = 0;
@@ -69,6 +74,16 @@ struct KernelTimer {
     harvest();
     launches = 0;
     ms = flops = bytes = 0;
+    lt.clear();
+    lf.clear();
+    lb.clear();
+  }
+  // summed max(flops / pf, bytes / pb) over the harvested launches, in ms
+  double roofline_ms(double pf, double pb) {
+    harvest();
+    double r = 0;
+    for (size_t k = 0; k < lt.size(); ++k) r += std::max(lf[k] / pf, lb[k] / pb) * 1e3;
+    return r;
   }
   ~KernelTimer() {
     for (auto &e : pool) {

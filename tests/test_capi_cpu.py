@@ -458,3 +458,15 @@ def test_static_step_rejects_workspace_beyond_its_scratch():
     with pytest.raises(K.CkptError) as e:
         K.train_step_static(net, FAKE, FAKE, FAKE, FAKE, small)
     assert e.value.code == K.E_MISMATCH
+
+
+def test_timing_roofline_needs_positive_peaks():
+    # no launch has been timed: both sums are zero; non-positive peaks are refused
+    from paper_1604_06174_amd.workload import net_for
+    net = net_for(dict(kind="mlp", depth=3, width=8, batch=2))
+    r = net.timing_roofline(2.5e15, 8e12)
+    assert r == dict(roofline_ms=0.0, kernel_ms=0.0)
+    for pf, pb in ((0.0, 8e12), (2.5e15, -1.0), (float("nan"), 8e12)):
+        with pytest.raises(K.CkptError) as ei:
+            net.timing_roofline(pf, pb)
+        assert ei.value.code == K.E_INVALID

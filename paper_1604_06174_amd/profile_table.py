@@ -15,6 +15,10 @@ duration over every traced dispatch of that kind, and the fraction of the
 kind's roofline time max(flops / 2.5 PFLOP/s, bytes / 8 TB/s) that duration
 reaches.  The family line weights every kind by its launches per step.
 
+The --others form does the same for every other kernel of the step (batch
+norm, element passes, partial sums), per kernel and grid: counter bytes of a
+shorter step over the durations in the full step's trace.
+
 The --counters form joins rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE,
 SQ_VALU_MFMA_BUSY_CYCLES) of a shorter step -- a bottleneck net with fewer
 blocks per stage, so the same launch kinds -- with that step's launch log in
@@ -23,6 +27,7 @@ dispatch order, and weights each kind by its launches in the full step.
 from __future__ import annotations
 
 import csv
+import re
 import sys
 from collections import defaultdict
 
@@ -210,7 +215,65 @@ def counters_main(log, short_log, csv_paths, fetch_factor, write_factor):
     return tr / max(n_cov, 1), n_cov, n_all
 
 
+def other_kernels_main(trace, fetch_csv, write_csv, fetch_factor, write_factor, steps, skip="k_gemm_bf16"):
+    """HBM bytes per dispatch (calibrated FETCH_SIZE + WRITE_SIZE, means over
+    the counter runs' dispatches of each kernel and total grid size) joined
+    with the mean duration of the same kernel and grid in a kernel trace of
+    the full step: achieved HBM bandwidth per kernel kind, for every kernel
+    but the `skip` family.  `steps` = training steps in the trace."""
+    def short(name):
+        if name.startswith("_Z"):  # a mangled instance: its name and integral template arguments
+            m = re.search(r"(k_[a-z0-9_]+)I((?:L[ib]\d+E)+)E", name)
+            if m:
+                args = re.findall(r"L([ib])(\d+)E", m.group(2))
+                return m.group(1) + "<" + ", ".join(
+                    ("true" if v == "1" else "false") if t == "b" else v for t, v in args) + ">"
+            m = re.search(r"(k_[a-z0-9_]+)", name)
+            return m.group(1) if m else name[:60]
+        n = name.replace("(anonymous namespace)::", "").replace("void ", "").replace("ckpt::", "")
+        return n.split("(")[0][:60]
+    cnt = defaultdict(lambda: defaultdict(list))
+    for path, ctr, fac in ((fetch_csv, "FETCH_SIZE", fetch_factor), (write_csv, "WRITE_SIZE", write_factor)):
+        per = defaultdict(float)
+        key = {}
+        with open(path) as f:
+            for d in csv.DictReader(f):
+                if skip in d["Kernel_Name"] or d["Counter_Name"] != ctr:
+                    continue
+                did = int(d["Dispatch_Id"])
+                per[did] += float(d["Counter_Value"]) * 1024 * fac
+                key[did] = (short(d["Kernel_Name"]), int(d["Grid_Size"]))
+        for did, v in per.items():
+            cnt[key[did]][ctr].append(v)
+    dur = defaultdict(list)
+    with open(trace) as f:
+        for d in csv.DictReader(f):
+            if skip in d["Kernel_Name"]:
+                continue
+            g = int(d["Grid_Size_X"]) * int(d["Grid_Size_Y"]) * int(d["Grid_Size_Z"])
+            dur[(short(d["Kernel_Name"]), g)].append((int(d["End_Timestamp"]) - int(d["Start_Timestamp"])) * 1e-9)
+    rows = []
+    for k, ds in dur.items():
+        c = cnt.get(k)
+        if not c or "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+            continue
+        by = sum(c["FETCH_SIZE"]) / len(c["FETCH_SIZE"]) + sum(c["WRITE_SIZE"]) / len(c["WRITE_SIZE"])
+        t = sum(ds) / len(ds)
+        rows.append((len(ds) / steps * t, k, len(ds) / steps, by, t))
+    rows.sort(key=lambda x: -x[0])
+    print("| kernel | threads | per step | ms per step | HBM MB per dispatch | avg us | HBM TB/s | of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|")
+    for tot, (name, g), n, by, t in rows:
+        print(f"| `{name}` | {g} | {n:.0f} | {tot * 1e3:.2f} | {by / 1e6:.2f} | {t * 1e6:.2f} | "
+              f"{by / t / 1e12:.2f} | {by / t / 8e12:.2f} |")
+
+
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--others":
+        # --others <kernel trace csv> <fetch csv> <write csv> <fetch factor> <write factor> <steps in trace>
+        other_kernels_main(sys.argv[2], sys.argv[3], sys.argv[4], float(sys.argv[5]), float(sys.argv[6]),
+                           float(sys.argv[7]))
+        sys.exit(0)
     if len(sys.argv) > 1 and sys.argv[1] == "--counters":
         # --counters <full-step log> <short-step log> <fetch factor> <write factor> <csv> [<csv> ...]
         counters_main(sys.argv[2], sys.argv[3], sys.argv[6:], float(sys.argv[4]), float(sys.argv[5]))

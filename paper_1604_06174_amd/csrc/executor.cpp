@@ -88,7 +88,8 @@ struct Exec {
   }
 
   // Re-run [lo, hi) from x into the arena's localtemp layout; fills the
-  // per-unit saved/output addresses.
+  // per-unit saved/output addresses, then lets the net finish the segment's
+  // kept forwards together.
   void localtemp(int32_t lo, int32_t hi, const void *x, std::vector<void *> &saved,
                  std::vector<void *> &out) {
     saved.assign(size_t(hi - lo), nullptr);
@@ -108,6 +109,7 @@ struct Exec {
       out[size_t(i - lo)] = y;
       cur_x = y;
     }
+    net.fwd_segment(lo, hi, saved, out, c);
   }
 
   void backward_segment(int32_t lo, int32_t hi, const void *x, const std::vector<void *> &saved,

@@ -61,6 +61,23 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
 #undef CKPT_GB
 }
 
+void gemm_bf16_rowsoftmax_batched(hipStream_t s, int nb, int M, int N, int K, const void *A, int lda,
+                                  int64_t bstrA, const void *B, int ldb, float *C, int64_t bstrC,
+                                  const float *bias, float *rstat, int64_t bstrR) {
+  if (nb <= 0 || M <= 0 || N <= 0) return;
+  if (K % 8 || lda % 8 || ldb % 8 || N % 4 || bstrA % 8 || bstrC % 4 || !bias || !rstat ||
+      bstrR < int64_t(M) * gemm_bf16_col_blocks(M, N) * 2)
+    fail(CKPT_E_INVALID, "gemm_bf16_rowsoftmax_batched: k extents, strides and tile statistics");
+  GemmX x;
+  x.rstat = rstat;
+  Args a = make_args(M, N, K, A, lda, B, ldb, C, N, nullptr, 0, bias, x);
+  a.nbatch = nb;
+  a.bstrA = bstrA;
+  a.bstrC = bstrC;
+  a.bstrR = bstrR;
+  pick_tile<true, true, __bf16, G_DENSE, G_DENSE, true>(a, GEMM_EPI_ROWSOFTMAX, nb, s);
+}
+
 void gemm_bf16(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D, int ldd,
                const float *bias) {

@@ -94,6 +94,11 @@ struct Args {
   const __bf16 *A2;  // GA_CAT: the second operand, from k = K1 on
   int lda2, K1;
   float inv_wo, inv_ho;
+  // batched products (nbatch > 0, one k split): workgroup z computes product
+  // z, whose A, C and row statistics start bstrA, bstrC and bstrR elements
+  // after product z - 1's (B is shared)
+  int nbatch;
+  int64_t bstrA, bstrC, bstrR;
 };
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -359,11 +364,16 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
     tm = (L / gridDim.x) % gridDim.y;
     tz = L / (gridDim.x * gridDim.y);
   }
+  int bz = 0;  // product of a batch
+  if (p.nbatch > 0) {
+    bz = tz;
+    tz = 0;
+  }
   const int m0 = tm * BM, n0 = tn * BN;
   const int kbeg = tz * p.kper;
   const int kend = min(p.K, kbeg + p.kper);
   const int wm = (wave / WN) * (BM / WM), wn = (wave % WN) * (BN / WN);
-  const TA *A = static_cast<const TA *>(p.A);
+  const TA *A = static_cast<const TA *>(p.A) + size_t(bz) * p.bstrA;
 
   // fixed per-chunk gather state
   RowPix rpix[(GA == GA_FWD || GA == GA_DGRAD) ? PA : 1];
@@ -750,7 +760,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
   // tile at a time, then writes whole rows with 16-byte stores (and reads D
   // and the mask the same way).
   float *stage = reinterpret_cast<float *>(scr) + wave * 16 * SP;
-  float *Cz = p.C + size_t(tz) * p.M * p.ldc;
+  float *Cz = p.C + size_t(tz) * p.M * p.ldc + size_t(bz) * p.bstrC;
   constexpr int VEC = EPI == GEMM_EPI_BF16STATS ? 8 : 4;  // output elements per lane
   constexpr int LPR = WC / VEC;                           // lanes per row
   constexpr int RPP = 64 / LPR;                           // rows per pass
@@ -914,7 +924,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
         ls = mx == -INFINITY ? 0.f : ls * expf(lm - mx) + os * expf(om - mx);
         lm = mx;
       }
-      float *r = p.rstat + (size_t(m0 + tid) * gridDim.x + tn) * 2;
+      float *r = p.rstat + size_t(bz) * p.bstrR + (size_t(m0 + tid) * gridDim.x + tn) * 2;
       r[0] = lm;
       r[1] = ls;
     }

@@ -186,6 +186,13 @@ struct GemmX {
 void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                 const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D,
                 int ldd, const float *bias, const GemmX &x);
+// nb products of the ROWSOFTMAX form at once (k-contiguous bf16 A [M, K] and
+// B [N, K], ldc = N): product z reads A + z bstrA and writes C + z bstrC and
+// its row statistics at rstat + z bstrR (at least M * gemm_bf16_col_blocks(M,
+// N) * 2 floats apart); every product's bits are those of its own launch.
+void gemm_bf16_rowsoftmax_batched(hipStream_t s, int nb, int M, int N, int K, const void *A, int lda,
+                                  int64_t bstrA, const void *B, int ldb, float *C, int64_t bstrC,
+                                  const float *bias, float *rstat, int64_t bstrR);
 int gemm_bf16_row_blocks(int M, int N);
 int gemm_bf16_col_blocks(int M, int N);
 int gemm_bf16_tiles(int M, int N);
@@ -251,6 +258,12 @@ void lstm_fwd_point(hipStream_t s, int B, int H, const float *zpart, int ns, con
 // GEMM_EPI_ROWSOFTMAX wrote (nt tiles per row); V % 4 == 0.
 void softmax_ce_tiles(hipStream_t s, int rows, int V, const float *logits, int nt, const float *rstat,
                       const int *labels, float scale, float *dlog, float *loss_rows);
+// the same over nunits units at once, in place (dlog over the logits): unit u's
+// logits at logits + u ul, statistics at rstat + u ur, labels and loss rows at
+// + u rows
+void softmax_ce_tiles_batched(hipStream_t s, int nunits, int rows, int V, float *logits, int64_t ul, int nt,
+                              const float *rstat, int64_t ur, const int *labels, float scale,
+                              float *loss_rows);
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first);
 // dbp receives ceil(B/4) records [4H] of bias-gradient column sums (one per
 // block of 4 batch rows); db_chunk adds a run of such records into db.

@@ -118,14 +118,23 @@ __device__ __forceinline__ void lse_combine(float &m, float &s, float om, float 
 // wavefront combines its row's pairs itself (lane j takes tiles j, j + 64,
 // ... in order, then a butterfly, whose pairwise combinations are symmetric),
 // so all workgroups of a row use the same maximum and sum with no exchange
-// between them.  Workgroup = 1024 columns of one row, four per thread.
-__global__ __launch_bounds__(256) void k_softmax_ce_tiles(int V, const float *__restrict__ logits, int nt,
+// between them.  Workgroup = 1024 columns of one row, four per thread;
+// blockIdx.z = the unit of a batch (its logits, dlog and statistics ul, ul
+// and ur floats after the previous unit's, its labels and loss rows `rows`
+// after).  The row's loss is formed by the thread that holds the label's
+// logit, from its register, so dlog may overwrite the logits in place.
+__global__ __launch_bounds__(256) void k_softmax_ce_tiles(int V, const float *logits, int nt,
                                                           const float *__restrict__ rstat,
                                                           const int *__restrict__ labels, float scale,
-                                                          float *__restrict__ dlog,
-                                                          float *__restrict__ loss_rows) {
+                                                          float *dlog, float *__restrict__ loss_rows,
+                                                          int rows, int64_t ul, int64_t ur) {
   const int row = blockIdx.y, lane = threadIdx.x & 63;
-  const float *rs = rstat + size_t(row) * nt * 2;
+  const int64_t u = blockIdx.z;
+  logits += u * ul;
+  dlog += u * ul;
+  labels += u * rows;
+  loss_rows += u * rows;
+  const float *rs = rstat + u * ur + size_t(row) * nt * 2;
   float m = -INFINITY, se = 0.f;
   for (int j = lane; j < nt; j += 64) lse_combine(m, se, rs[2 * j], rs[2 * j + 1]);
   for (int o = 32; o > 0; o >>= 1) {
@@ -141,13 +150,13 @@ __global__ __launch_bounds__(256) void k_softmax_ce_tiles(int V, const float *__
     const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
     float d[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) d[u] = (expf(xs[u] - m) * inv - (v0 + u == lab ? 1.f : 0.f)) * scale;
+    for (int k = 0; k < 4; ++k) {
+      d[k] = (expf(xs[k] - m) * inv - (v0 + k == lab ? 1.f : 0.f)) * scale;
+      if (v0 + k == lab) loss_rows[row] = (logf(se) + m) - xs[k];
+    }
     *reinterpret_cast<float4 *>(dlog + size_t(row) * V + v0) = make_float4(d[0], d[1], d[2], d[3]);
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    const bool ok = lab >= 0 && lab < V;
-    loss_rows[row] = ok ? (logf(se) + m) - x[lab] : NAN;
-  }
+  if (blockIdx.x == 0 && threadIdx.x == 0 && !(lab >= 0 && lab < V)) loss_rows[row] = NAN;
 }
 
 // Workgroup = 64 columns x 4 row groups (rows b = rg, rg + 4, ...); the
@@ -323,7 +332,17 @@ void softmax_ce_tiles(hipStream_t s, int rows, int V, const float *logits, int n
       reinterpret_cast<uintptr_t>(dlog) % 16 != 0)
     fail(CKPT_E_INVALID, "softmax_ce_tiles: V must be a multiple of 4 and the rows 16-byte aligned");
   hipLaunchKernelGGL(k_softmax_ce_tiles, dim3((V + 1023) / 1024, rows), dim3(256), 0, s, V, logits, nt,
-                     rstat, labels, scale, dlog, loss_rows);
+                     rstat, labels, scale, dlog, loss_rows, rows, int64_t(0), int64_t(0));
+}
+
+void softmax_ce_tiles_batched(hipStream_t s, int nunits, int rows, int V, float *logits, int64_t ul, int nt,
+                              const float *rstat, int64_t ur, const int *labels, float scale,
+                              float *loss_rows) {
+  if (nunits <= 0) return;
+  if (V % 4 != 0 || ul % 4 != 0 || reinterpret_cast<uintptr_t>(logits) % 16 != 0)
+    fail(CKPT_E_INVALID, "softmax_ce_tiles_batched: V and the unit stride multiples of 4, rows 16-byte aligned");
+  hipLaunchKernelGGL(k_softmax_ce_tiles, dim3((V + 1023) / 1024, rows, nunits), dim3(256), 0, s, V, logits,
+                     nt, rstat, labels, scale, logits, loss_rows, rows, ul, ur);
 }
 
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {

@@ -138,13 +138,21 @@ class Net {
   // Unit i forward: x (x_i) -> y (x_{i+1}); saved internals written to `saved`.
   // Every unit runs exactly one forward with c.keep_saved set before its
   // backward; a forward with it clear may leave out work whose only results
-  // are saved internals (and loss terms, which the kept forward then adds).
+  // are saved internals (and loss terms, which the kept forward then adds),
+  // and a kept forward may leave such work to fwd_segment.
   virtual void fwd(int32_t i, const void *x, void *y, void *saved, StepCtx &c) = 0;
   // Unit i backward: g = dL/dx_{i+1} -> dx = dL/dx_i (dx is null for unit 0),
   // reading x, y and saved; q is the unit's gradient scratch.  Writes unit i's
   // parameter gradients.
   virtual void bwd(int32_t i, const void *g, void *dx, const void *x, const void *y,
                    const void *saved, void *q, StepCtx &c) = 0;
+  // Called after a kept forward of units [lo, hi) into the arena (unit lo + k's
+  // saved internals at saved[k], its output at out[k]) and before their
+  // backwards: work of those units that their forwards leave to be done for
+  // all of them at once, in no order across the units (products batched over
+  // the units).
+  virtual void fwd_segment(int32_t, int32_t, const std::vector<void *> &, const std::vector<void *> &,
+                           StepCtx &) {}
   // Called once at the start of every step, before any unit runs, and once at
   // its end, after the last backward.
   virtual void begin_step(StepCtx &) {}

@@ -16,8 +16,11 @@
 // The head of a step (logits, softmax gradient, loss rows) feeds only the
 // unit's saved internals and the loss, so a forward whose saved internals are
 // discarded (a checkpointed step's forward sweeps) runs the recurrence alone;
-// the head runs in the unit's kept forward, once per step in every plan, and
-// the loss rows are reduced after the last backward.
+// the head runs with the unit's kept forward, once per step in every plan,
+// for up to HG steps of a kept segment at once (one batched logits product,
+// each step's product computed exactly as its own launch would, written over
+// the step's saved softmax-gradient buffer, then one batched softmax pass in
+// place), and the loss rows are reduced after the last backward.
 //
 // Static layout: boundary b = h (bf16 [B,H]) | c (fp32 [B,H]); saved a = gates
 // (fp32 [B,4H]) | softmax gradient (fp32 [B,V]); scratch q = total dh (fp32
@@ -36,6 +39,7 @@ namespace {
 
 class LstmNet : public Net {
  public:
+  static constexpr int HG = 64;  // steps per batched head
   int T, B, E, H, V, C;
   int pWx, pWh, pb, pWo, pbo;
   uint64_t hb, cb;  // boundary parts
@@ -108,7 +112,7 @@ class LstmNet : public Net {
     const uint64_t part = std::max({uint64_t(s_x + s_h) * B * 4 * H, uint64_t(B) * V,
                                     uint64_t(std::max(s_dh, s_dm)) * B * H});
     k_part = take(part * 4);
-    k_rstat = take(uint64_t(B) * gemm_bf16_col_blocks(B, V) * 2 * 4);
+    k_rstat = take(uint64_t(HG) * B * gemm_bf16_col_blocks(B, V) * 2 * 4);
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
   }
@@ -154,7 +158,6 @@ class LstmNet : public Net {
     char *y = static_cast<char *>(yv);
     char *sv = static_cast<char *>(saved);
     const void *xt = static_cast<const char *>(c.input) + size_t(i) * B * E * 2;
-    const int *lab = static_cast<const int *>(c.target) + size_t(i) * B;
     // z = x_t W_x + h_{t-1} W_h + b: both products split over k into one
     // slice buffer that the pointwise kernel adds up in order with the bias
     if (i > 0 && zcat) {
@@ -173,24 +176,47 @@ class LstmNet : public Net {
     lstm_fwd_point(c.s, B, H, Kf(c, k_part), s_x + (i > 0 ? s_h : 0), P(c, pb), c_prev, gates, y,
                    reinterpret_cast<float *>(y + hb));
     c.launches += 1;
-    // The head feeds only the saved softmax gradient and the step's loss term:
-    // a forward whose saved internals are discarded leaves it to the unit's
-    // re-run, so it runs once per step as without checkpointing.
-    if (!c.keep_saved) return;
-    // logits = h_t W_o + b_o, with each row's (max, sum of exp) per column
-    // tile formed in the product's epilogue; then the softmax pass
-    {
-      GemmX gx;
-      gx.rstat = Kf(c, k_rstat);
-      timer.begin(c.s);
-      gemm_bf16x(c.s, B, V, H, y, false, H, true, K(c, k_wot), H, true, Kf(c, k_part), V,
-                 GEMM_EPI_ROWSOFTMAX, nullptr, 0, P(c, pbo), gx);
-      timer.end(c.s, 2.0 * B * V * H, 2.0 * (double(B) * H + double(H) * V) + 4.0 * B * V);
-    }
-    softmax_ce_tiles(c.s, B, V, Kf(c, k_part), gemm_bf16_col_blocks(B, V), Kf(c, k_rstat), lab,
-                     1.0f / (float(T) * float(B)), reinterpret_cast<float *>(sv + ga),
-                     Kf(c, k_lossrows) + size_t(i) * B);
+    // the step's head runs after the kept forward of its segment (fwd_segment)
+  }
+
+  // the heads of steps i0 .. i0 + nb - 1: h_t at y0 + k sy (bf16 elements),
+  // logits and then the softmax gradient at dl0 + k sd (floats)
+  void heads(int32_t i0, int nb, const char *y0, int64_t sy, float *dl0, int64_t sd, StepCtx &c) {
+    const int nt = gemm_bf16_col_blocks(B, V);
+    const int64_t ur = int64_t(B) * nt * 2;
+    timer.begin(c.s);
+    gemm_bf16_rowsoftmax_batched(c.s, nb, B, V, H, y0, H, sy, K(c, k_wot), H, dl0, sd, P(c, pbo),
+                                 Kf(c, k_rstat), ur);
+    // each step's h and logits once, the shared W_o once
+    timer.end(c.s, 2.0 * nb * B * V * H, nb * (2.0 * B * H + 4.0 * B * V) + 2.0 * H * V);
+    softmax_ce_tiles_batched(c.s, nb, B, V, dl0, sd, nt, Kf(c, k_rstat), ur,
+                             static_cast<const int *>(c.target) + size_t(i0) * B, 1.0f / (float(T) * float(B)),
+                             Kf(c, k_lossrows) + size_t(i0) * B);
     c.launches += 2;
+  }
+
+  void fwd_segment(int32_t lo, int32_t hi, const std::vector<void *> &saved, const std::vector<void *> &out,
+                   StepCtx &c) override {
+    for (int32_t g0 = lo; g0 < hi; g0 += HG) {
+      const int nb = int(std::min<int32_t>(hi - g0, HG));
+      const char *y0 = static_cast<const char *>(out[size_t(g0 - lo)]);
+      char *s0 = static_cast<char *>(saved[size_t(g0 - lo)]);
+      // the arena places a segment's units at one stride; batch them when it
+      // holds (and the strides are whole elements), else one step at a time
+      const int64_t sy = nb > 1 ? static_cast<const char *>(out[size_t(g0 - lo) + 1]) - y0 : 0;
+      const int64_t ss = nb > 1 ? static_cast<char *>(saved[size_t(g0 - lo) + 1]) - s0 : 0;
+      bool uniform = sy % 16 == 0 && ss % 16 == 0;
+      for (int k = 1; uniform && k < nb; ++k)
+        uniform = static_cast<const char *>(out[size_t(g0 - lo + k)]) - y0 == k * sy &&
+                  static_cast<char *>(saved[size_t(g0 - lo + k)]) - s0 == k * ss;
+      if (uniform) {
+        heads(g0, nb, y0, sy / 2, reinterpret_cast<float *>(s0 + ga), ss / 4, c);
+      } else {
+        for (int k = 0; k < nb; ++k)
+          heads(g0 + k, 1, static_cast<const char *>(out[size_t(g0 - lo + k)]), 0,
+                reinterpret_cast<float *>(static_cast<char *>(saved[size_t(g0 - lo + k)]) + ga), 0, c);
+      }
+    }
   }
 
   void bwd(int32_t i, const void *gv, void *dxv, const void *xv, const void *yv, const void *saved,

@@ -234,11 +234,18 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   if (a.M <= 0 || a.N <= 0 || a.K < 0) error(k.pretty + ": non-positive M or N");
   if (grid.x != (N + BN - 1) / BN || grid.y != (M + BM - 1) / BM)
     error(k.pretty + ": grid does not cover the product's tiles exactly");
-  if (a.kper <= 0 || uint64_t(a.kper) * grid.z < K) error(k.pretty + ": k splits do not cover K");
+  // a batch of products: grid.z = the products, each over the whole k range
+  const uint64_t nb = a.nbatch > 0 ? uint64_t(a.nbatch) : 1;
+  if (a.nbatch > 0 && (grid.z != nb || uint64_t(a.kper) < K))
+    error(k.pretty + ": a batch takes one workgroup layer per product and one k split");
+  if (a.nbatch == 0 && (a.kper <= 0 || uint64_t(a.kper) * grid.z < K))
+    error(k.pretty + ": k splits do not cover K");
+  const uint64_t ba = (nb - 1) * uint64_t(a.bstrA), bc = (nb - 1) * uint64_t(a.bstrC),
+                 br = (nb - 1) * uint64_t(a.bstrR);
   const uint64_t C = a.cshift >= 0 ? uint64_t(1) << a.cshift : 0;
   // A
   if (GA == G_DENSE) {
-    check_extent(k, "A", a.A, (AK ? rows_span(M, a.lda, K) : rows_span(K, a.lda, M)) * ta);
+    check_extent(k, "A", a.A, (ba + (AK ? rows_span(M, a.lda, K) : rows_span(K, a.lda, M))) * ta);
   } else if (GA == GA_FWD) {
     const uint64_t pix = uint64_t(a.Ho) * a.Wo;
     if (M % pix) error(k.pretty + ": forward gather rows are not whole images");
@@ -266,12 +273,12 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
     error(k.pretty + ": unknown B form");
   }
   // result and epilogue operands
-  const uint64_t cz = uint64_t(grid.z);
+  const uint64_t cz = a.nbatch > 0 ? 1 : uint64_t(grid.z);
   if (EPI == ckpt::GEMM_EPI_BF16STATS) {
     check_extent(k, "Cb", a.Cb, rows_span(M, a.ldc, N) * 2);
     check_extent(k, "stats", a.stats, uint64_t(grid.y) * 2 * N * 8);
   } else {
-    check_extent(k, "C", a.C, ((cz - 1) * M * a.ldc + rows_span(M, a.ldc, N)) * 4);
+    check_extent(k, "C", a.C, (bc + (cz - 1) * M * a.ldc + rows_span(M, a.ldc, N)) * 4);
   }
   if (EPI == ckpt::GEMM_EPI_ADD || EPI == ckpt::GEMM_EPI_ADDMASK)
     check_extent(k, "D", a.D, rows_span(M, a.ldd, N) * 4);
@@ -284,7 +291,7 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   }
   if (EPI == ckpt::GEMM_EPI_ROWSOFTMAX) {
     check_extent(k, "bias", a.bias, N * 4);
-    check_extent(k, "row statistics", a.rstat, M * grid.x * 2 * 4);
+    check_extent(k, "row statistics", a.rstat, (br + M * grid.x * 2) * 4);
   } else if (EPI == ckpt::GEMM_EPI_STORE && a.bias) {
     check_extent(k, "bias", a.bias, N * 4);
   }

@@ -37,7 +37,7 @@
 // ADDMASK C = acc + (Ym > 0 ? D : 0) with Ym bf16 shaped like D;
 // BF16STATS Cb = bf16(acc) and, per workgroup row of tiles, float64 sums of
 // the rounded values and their squares per column (batch-norm statistics:
-// stats[m tile][2][N], block-major).  Split-K (gridDim.z > 1): workgroup z reduces the
+// stats[m tile][2][N], block-major; none when stats is null).  Split-K (gridDim.z > 1): workgroup z reduces the
 // k range [z*kper, (z+1)*kper) and stores its partial product to
 // C + z*M*ldc (STORE only); the partials are then added in z order.
 #pragma once
@@ -717,7 +717,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
     }
   }
 
-  if constexpr (EPI == GEMM_EPI_BF16STATS) {
+  // BF16STATS without a statistics buffer (a re-run that reuses its
+  // statistics): the bf16 result alone (the same bits: the stored value is
+  // rounded once either way)
+  if (EPI == GEMM_EPI_BF16STATS && p.stats) {
     // per column: sums of the bf16-rounded values over this wavefront's rows,
     // then over the lane groups and the WM wavefronts sharing the column, in
     // a fixed order

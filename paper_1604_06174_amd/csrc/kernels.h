@@ -224,7 +224,8 @@ struct ConvGeo {
   int N, H, W, Ci, Ho, Wo, Co, R, S, P;
 };
 bool conv_bf16_supported(const ConvGeo &g);
-// Yb = bf16(conv(X, Wt)); stats[row block][2][Co] as for BF16STATS
+// Yb = bf16(conv(X, Wt)); stats[row block][2][Co] as for BF16STATS (none when
+// stats is null)
 // (row blocks: gemm_bf16_row_blocks(N*Ho*Wo, Co)).
 void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *Wt, void *Yb,
                    double *stats);

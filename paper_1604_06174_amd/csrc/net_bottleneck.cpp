@@ -223,12 +223,13 @@ class Bottleneck : public Net {
   }
 
   // forward 1x1 convolution (stride 1) with BN statistics, then the stats
-  // (not on a re-run, which reuses the unit's kept statistics)
+  // (not on a re-run, which reuses the unit's kept statistics and forms no
+  // sums)
   void fwd_1x1(StepCtx &c, int64_t m, int ci, int co, const void *x, int wk, void *out, float *st) {
     tbeg(c);
     GemmX gx;
     gx.Cb = out;
-    gx.stats = statsbuf(c);
+    gx.stats = c.rerun ? nullptr : statsbuf(c);
     gemm_bf16x(c.s, int(m), co, ci, x, false, ci, true, Wb(c, wk), ci, true, nullptr, co,
                GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
     tend(c, double(m), co, ci, 2.0 * (double(m) * ci + double(ci) * co), 2.0 * double(m) * co);
@@ -242,7 +243,7 @@ class Bottleneck : public Net {
     const int64_t m = int64_t(g.N) * g.Ho * g.Wo;
     const double kd = double(g.R) * g.R * g.Ci;
     tbeg(c);
-    conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, statsbuf(c));
+    conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, c.rerun ? nullptr : statsbuf(c));
     tend(c, double(m), g.Co, kd, 2.0 * (double(g.N) * g.H * g.W * g.Ci + kd * g.Co),
          2.0 * double(m) * g.Co);
     if (!c.rerun) {
@@ -293,7 +294,7 @@ class Bottleneck : public Net {
       tbeg(c);
       GemmX gx;
       gx.Cb = cv;
-      gx.stats = statsbuf(c);
+      gx.stats = c.rerun ? nullptr : statsbuf(c);
       gemm_bf16x(c.s, int(m), C0, 147, c.ks + ks_col, false, 147, true, Wb(c, k.W1), 147, true,
                  nullptr, C0, GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
       tend(c, double(m), C0, 147, 2.0 * (double(m) * 147 + 147.0 * C0), 2.0 * double(m) * C0);

@@ -276,7 +276,7 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   const uint64_t cz = a.nbatch > 0 ? 1 : uint64_t(grid.z);
   if (EPI == ckpt::GEMM_EPI_BF16STATS) {
     check_extent(k, "Cb", a.Cb, rows_span(M, a.ldc, N) * 2);
-    check_extent(k, "stats", a.stats, uint64_t(grid.y) * 2 * N * 8);
+    if (a.stats) check_extent(k, "stats", a.stats, uint64_t(grid.y) * 2 * N * 8);
   } else {
     check_extent(k, "C", a.C, (bc + (cz - 1) * M * a.ldc + rows_span(M, a.ldc, N)) * 4);
   }

@@ -81,7 +81,11 @@ __global__ __launch_bounds__(256) void k_bnb_apply(int64_t P, int J, const __bf1
   }
 }
 
-// partial sums for the backward: sum(ds), sum(ds * xhat), ds = [Ym > 0] G
+// partial sums for the backward: sum(ds), sum(ds * xhat), ds = [Ym > 0] G.
+// Workgroup (x, y) = pixels [x PB, (x + 1) PB) of the channel slab
+// [y SL, (y + 1) SL), SL = min(J, 256): SL / 8 threads per pixel (eight
+// channels each), 256 / (SL / 8) pixel lanes; block-major partials
+// part[x][2][J].
 template <bool MASKED>
 __global__ __launch_bounds__(256) void k_bnb_bwd_partials(int P, int J, int PB, const float *__restrict__ G,
                                                           const __bf16 *__restrict__ Ym,
@@ -89,9 +93,10 @@ __global__ __launch_bounds__(256) void k_bnb_bwd_partials(int P, int J, int PB, 
                                                           const float *__restrict__ st,
                                                           double *__restrict__ part) {
   __shared__ double red[2][256][8];
-  const int CQ = J / 8, PL = 256 / CQ;
+  const int SL = J < 256 ? J : 256;
+  const int CQ = SL / 8, PL = 256 / CQ;
   const int cq = threadIdx.x % CQ, pl = threadIdx.x / CQ;
-  const int c0 = cq * 8;
+  const int c0 = blockIdx.y * SL + cq * 8;
   const int p0 = blockIdx.x * PB, p1 = min(P, p0 + PB);
   float mean[8], rstd[8];
 #pragma unroll
@@ -290,9 +295,12 @@ __global__ __launch_bounds__(256) void k_maxpool_bwd(int N, int H, int W, int C,
 
 }  // namespace
 
+// pixel blocks of the backward partial sums: about 512 workgroups over the
+// channel slabs, each block a whole number of pixel-lane rounds
 int bnb_partial_blocks(int64_t P, int J) {
-  const int PL = 256 / (J / 8);
-  int64_t pb = (P + 511) / 512;
+  const int SL = J < 256 ? J : 256, slabs = J / SL, PL = 256 / (SL / 8);
+  const int64_t nbp = (512 + slabs - 1) / slabs;
+  int64_t pb = (P + nbp - 1) / nbp;
   pb = (pb + PL - 1) / PL * PL;
   if (pb < PL) pb = PL;
   return int((P + pb - 1) / pb);
@@ -318,10 +326,11 @@ void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Y
   const int nb = bnb_partial_blocks(P, J);
   const int pb = int((P + nb - 1) / nb);
   const __bf16 *ym = static_cast<const __bf16 *>(Ym), *c = static_cast<const __bf16 *>(Cv);
+  const dim3 grid(nb, J < 256 ? 1 : J / 256);
   if (ym)
-    hipLaunchKernelGGL((k_bnb_bwd_partials<true>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
+    hipLaunchKernelGGL((k_bnb_bwd_partials<true>), grid, dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
   else
-    hipLaunchKernelGGL((k_bnb_bwd_partials<false>), dim3(nb), dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
+    hipLaunchKernelGGL((k_bnb_bwd_partials<false>), grid, dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
   bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta, false);
   bnb_backward_apply(s, P, J, G, Ym, Cv, st, gamma, sums, D);
 }

@@ -468,6 +468,26 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
                      ckpt_step_stats *stats);
 
 /*
+ * net_set_side_stream -- lets (enable = 1, the default) or stops (0) a net run
+ * part of each unit's backward on a second stream of its own.  The
+ * RESNET_BOTTLENECK net uses one for its units' weight gradients (Alg. 1's
+ * backward of a unit: the weight-gradient products do not feed the input
+ * gradient, so they run beside it), ordered with the step's stream by events
+ * so that a unit's backward has ended on both streams before the next one
+ * starts; other nets run everything on the step's stream.  The gradients are
+ * the same bits either way.  The stream and its two events are created by the
+ * first train_step or step_graph_create that can use them (not by a step whose
+ * stream is being captured, and not by train_step_static, which allocates
+ * nothing: those use the second stream only once it exists), on the device
+ * of the step's stream when that device is current; they are released by
+ * net_destroy.  A step on another device than the one they were created on
+ * runs on its own stream alone.
+ * Errors: CKPT_E_INVALID for a null net; CKPT_E_HIP when creating them fails
+ * (reported by the step that tries).
+ */
+int net_set_side_stream(ckpt_net *net, int32_t enable);
+
+/*
  * Kernel timing for benchmarks.  net_timing_enable(net, 1) makes every later
  * train_step bracket each launch of the net's dominant kernel family (the
  * conv3x3 forward / data-gradient kernel of RESNET_BASIC, the GEMM of MLP)

@@ -103,6 +103,7 @@ _sig("net_param_count", C.c_int, [C.c_void_p, _i32p])
 _sig("net_param_info", C.c_int, [C.c_void_p, C.c_int32, C.c_char_p, C.c_int32, _u64p, _u64p])
 _sig("plan_accounting", C.c_int, [C.c_void_p, C.c_void_p, _u64p, _u64p, _u64p, _u64p])
 _sig("net_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
+_sig("net_set_side_stream", C.c_int, [C.c_void_p, C.c_int32])
 _sig("net_timing_enable", C.c_int, [C.c_void_p, C.c_int32])
 _sig("net_timing_roofline", C.c_int, [C.c_void_p, C.c_double, C.c_double, C.POINTER(C.c_double),
                                       C.POINTER(C.c_double)])
@@ -162,7 +163,7 @@ EXPORTED = ["op_gemm_bf16_blocks", "op_gemm_bf16", "op_sum_partials", "op_conv_b
             "graph_plan_blocks", "graph_plan_free", "net_node_graph", "graph_workspace_bytes",
             "train_step_graph", "net_create", "net_destroy", "net_units", "net_unit_sizes",
             "net_layer_sizes", "net_grad_bytes", "net_param_bytes", "net_param_count", "net_param_info",
-            "plan_accounting", "net_workspace_bytes", "net_timing_enable", "net_timing_read", "net_timing_roofline",
+            "plan_accounting", "net_workspace_bytes", "net_set_side_stream", "net_timing_enable", "net_timing_read", "net_timing_roofline",
             "train_step", "train_step_static", "step_graph_create", "step_graph_launch", "step_graph_free"]
 
 
@@ -223,7 +224,7 @@ class Plan:
         return bytes(buf)
 
     def __del__(self):
-        if getattr(self, "_h", None) is not None and self._h.value:
+        if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:
             _lib.plan_free(self._h)
             self._h = None
 
@@ -390,6 +391,11 @@ class Net:
         v = C.c_uint64()
         _check(_lib.graph_workspace_bytes(self._h, plan._h, C.byref(v)))
         return v.value
+
+    def set_side_stream(self, on: bool = True):
+        """Let (True) or stop (False) the net run its units' weight gradients
+        on a second stream beside the input gradients (same bits either way)."""
+        _check(_lib.net_set_side_stream(self._h, 1 if on else 0))
 
     def timing_enable(self, on: bool = True):
         _check(_lib.net_timing_enable(self._h, 1 if on else 0))

@@ -286,6 +286,7 @@ int train_step(ckpt_net *net, const void *params, void *grads, const ckpt_batch 
                float *loss_dev, float *loss_host, uint64_t *peak, ckpt_step_stats *stats) {
   return ckpt::guarded([&] {
     ckpt::check_step_args("train_step", net, params, grads, batch, plan, workspace);
+    ckpt::prepare_side(*net->net, static_cast<hipStream_t>(stream));
     ckpt::run_train_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
                          *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
                          static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
@@ -312,6 +313,7 @@ int step_graph_create(ckpt_net *net, const void *params, void *grads, const ckpt
     if (cs != hipStreamCaptureStatusNone)
       ckpt::fail(CKPT_E_INVALID, "step_graph_create: the stream is already being captured");
     auto g = std::make_unique<ckpt_step_graph>();
+    ckpt::prepare_side(*net->net, s);  // before the capture: it creates a stream and events
     e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
     if (e != hipSuccess)
       ckpt::fail(CKPT_E_HIP, std::string("step_graph_create: ") + hipGetErrorString(e));
@@ -393,6 +395,13 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
     ckpt::run_graph_step(*net->net, static_cast<const float *>(params), static_cast<float *>(grads),
                          *batch, plan->p, static_cast<char *>(workspace), workspace_bytes,
                          static_cast<hipStream_t>(stream), loss_dev, loss_host, peak, stats);
+  });
+}
+
+int net_set_side_stream(ckpt_net *net, int32_t enable) {
+  return ckpt::guarded([&] {
+    ckpt::need(net, "net_set_side_stream");
+    net->net->side.wanted = enable != 0;
   });
 }
 

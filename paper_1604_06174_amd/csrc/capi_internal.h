@@ -36,6 +36,10 @@ uint64_t workspace_bytes(const Net &net, const Accounting &acc);
 void run_train_step(Net &net, const float *params, float *grads, const ckpt_batch &batch,
                     const Plan &p, char *ws, uint64_t ws_bytes, hipStream_t s, float *loss_dev,
                     float *loss_host, uint64_t *peak, ckpt_step_stats *stats);
+// Creates the net's side stream when the net uses one, its owner allows it,
+// none exists yet, s is not being captured and s is on the current device;
+// otherwise does nothing (steps then run on their own stream alone).
+void prepare_side(Net &net, hipStream_t s);
 
 // Runs f; returns CKPT_OK, or the code of the error it threw (message kept for
 // ckpt_last_error).

@@ -232,6 +232,21 @@ struct Exec {
 
 }  // namespace
 
+// device of stream s (the current device for the null stream)
+hipError_t stream_device(hipStream_t s, int *d) { return s ? hipStreamGetDevice(s, d) : hipGetDevice(d); }
+
+void prepare_side(Net &net, hipStream_t s) {
+  if (!net.uses_side || !net.side.wanted || net.side.s) return;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  int d = -1, cur = -1;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone ||
+      stream_device(s, &d) != hipSuccess || hipGetDevice(&cur) != hipSuccess || d != cur) {
+    (void)hipGetLastError();  // no side stream: the step runs on its own stream
+    return;
+  }
+  net.side.create(d);
+}
+
 uint64_t workspace_bytes(const Net &net, const Accounting &acc) {
   return align256(acc.ckpt) + align256(acc.arena) + align256(acc.grad) + align256(net.ks_bytes);
 }
@@ -259,6 +274,16 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
   for (int32_t i = 0; i < net.n; ++i) maxq = std::max(maxq, net.q[size_t(i)]);
   c.gextra = grad + 2 * slot + maxq;
   c.q = grad + 2 * slot;
+
+  if (net.uses_side && net.side.wanted && net.side.s) {
+    int d = -1;
+    if (stream_device(s, &d) == hipSuccess && d == net.side.dev) {
+      c.side = net.side.s;
+      c.ev_side = net.side.to_side;
+      c.ev_main = net.side.to_main;
+      c.ev_mark = net.side.mark;
+    }
+  }
 
   Exec e{net, c, acc, ckpt, arena, {grad, grad + slot}, grad + 2 * slot};
   (void)hipGetLastError();  // clear a stale error left by the caller

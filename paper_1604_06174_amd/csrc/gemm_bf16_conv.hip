@@ -16,6 +16,13 @@ int log2_exact(int c) {
   return (1 << k) == c ? k : -1;
 }
 
+// the tap-uniform gathers apply: the gathered channels and the k range per
+// workgroup are multiples of the k slice (every slice in one tap, no slice
+// past the range), and the tap mask fits 32 bits
+bool tap_uniform(const Args &a) {
+  return a.cshift >= 0 && (1 << a.cshift) % KS == 0 && a.R * a.R <= 32 && a.K % KS == 0 && a.kper % KS == 0;
+}
+
 Args conv_args(const ConvGeo &g, int M, int N, int K, int gathered_c) {
   Args a{};
   a.M = M; a.N = N; a.K = K;
@@ -46,7 +53,10 @@ void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *W
   a.ldc = N;
   a.Cb = static_cast<__bf16 *>(Yb);
   a.stats = stats;
-  pick_tile<true, true, __bf16, GA_FWD, G_DENSE, true>(a, GEMM_EPI_BF16STATS, 1, s);
+  if (tap_uniform(a))
+    pick_tile<true, true, __bf16, GA_FWDT, G_DENSE, true>(a, GEMM_EPI_BF16STATS, 1, s);
+  else
+    pick_tile<true, true, __bf16, GA_FWD, G_DENSE, true>(a, GEMM_EPI_BF16STATS, 1, s);
 }
 
 void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void *Wt, float *DX,
@@ -66,7 +76,10 @@ void conv_bf16_dgrad(hipStream_t s, const ConvGeo &g, const void *DY, const void
   a.Cv = static_cast<const __bf16 *>(Cv);
   a.bst = bst;
   a.stats = stats;
-  pick_tile<true, false, __bf16, GA_DGRAD, GB_WDGRAD, true>(a, epi, 1, s);
+  if (g.S == 1 && tap_uniform(a))
+    pick_tile<true, false, __bf16, GA_DGRADT, GB_WDGRAD, true>(a, epi, 1, s);
+  else
+    pick_tile<true, false, __bf16, GA_DGRAD, GB_WDGRAD, true>(a, epi, 1, s);
 }
 
 void conv_bf16_wgrad(hipStream_t s, const ConvGeo &g, const void *X, const void *DY, float *part,

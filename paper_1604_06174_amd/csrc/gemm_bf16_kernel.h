@@ -22,6 +22,13 @@
 //             forward weights [Co, R, R, Ci] read as the data gradient's B)
 //   GA_CAT    A(m, k) = A[m, k] for k < K1, A2[m, k - K1] after: two
 //             k-contiguous bf16 operands side by side along k
+//   GA_FWDT, GA_DGRADT  GA_FWD and GA_DGRAD (the latter with S = 1) when C
+//             and the k range per workgroup are multiples of the k slice and
+//             R * R <= 32: each slice then lies in one tap, so the tap and its
+//             offset are the same for the whole workgroup, and a chunk's
+//             source is its row's fixed address plus that offset, or zero
+//             when the tap is outside the image (a per-row mask of taps)
+//             (direct loop only)
 // Out-of-image taps read zero.
 //
 // Block = 4 or 8 wavefronts (256 or 512 threads) in a WM x WN grid; each wavefront owns a
@@ -68,7 +75,8 @@ constexpr bool direct_three_stages(int BM, int BN, int epi_scratch) {
 constexpr int KS = 64;      // k per LDS slice: two 32-deep MFMA steps
 constexpr int KP = KS + 8;  // padded row (bf16 elements): 144-byte rows
 
-enum { G_DENSE = 0, GA_FWD = 1, GA_DGRAD = 2, GB_WGRAD = 3, GB_WDGRAD = 4, GA_CAT = 5 };
+enum { G_DENSE = 0, GA_FWD = 1, GA_DGRAD = 2, GB_WGRAD = 3, GB_WDGRAD = 4, GA_CAT = 5, GA_FWDT = 6,
+       GA_DGRADT = 7 };
 
 struct Args {
   int M, N, K;
@@ -393,6 +401,37 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
       ctap[c] = col_tap(p, n0 + (e % (BN / 8)) * 8);
     }
   }
+  // GA_FWDT / GA_DGRADT: per chunk (of the direct loop's layout), the byte
+  // address of its source at tap (0, 0) (an integer: the pixel may lie
+  // outside the image) and the mask of taps inside the image (zero for a
+  // row past M)
+  constexpr bool GAT = GA == GA_FWDT || GA == GA_DGRADT;
+  static_assert(!GAT || DIRECT, "the tap-uniform gathers run in the direct loop");
+  uint64_t tsrc[GAT ? PA : 1];
+  uint32_t tmask[GAT ? PA : 1];
+  if constexpr (GAT) {
+    const int C = 1 << p.cshift;
+#pragma unroll
+    for (int c = 0; c < PA; ++c) {
+      const int e = c * NT + tid, mr = e >> 3, kc = ((e & 7) ^ (mr & 7)) * 8;
+      const RowPix rp = GA == GA_FWDT ? row_pixel(p, m0 + mr, p.Ho, p.Wo) : row_pixel(p, m0 + mr, p.H, p.W);
+      // tap (0, 0)'s source pixel; tap (kh, kw) adds (kh, kw) (forward) or
+      // subtracts it (data gradient)
+      const int oy = GA == GA_FWDT ? rp.y * p.S - p.P : rp.y + p.P;
+      const int ox = GA == GA_FWDT ? rp.x * p.S - p.P : rp.x + p.P;
+      const int sh = GA == GA_FWDT ? p.H : p.Ho, sw = GA == GA_FWDT ? p.W : p.Wo;
+      uint32_t mk = 0;
+      for (int t = 0; t < p.R * p.R; ++t) {
+        int kh, kw;
+        tap_hw(t, p, kh, kw);
+        const int y = GA == GA_FWDT ? oy + kh : oy - kh, x = GA == GA_FWDT ? ox + kw : ox - kw;
+        mk |= uint32_t((y >= 0) & (y < sh) & (x >= 0) & (x < sw)) << t;
+      }
+      tmask[c] = rp.ok ? mk : 0u;
+      const int64_t el = ((int64_t(rp.img) * sh + oy) * sw + ox) * C + kc;
+      tsrc[c] = uint64_t(reinterpret_cast<uintptr_t>(A)) + uint64_t(el * 2);
+    }
+  }
 
   floatx4 acc[TM][TN];
 #pragma unroll
@@ -460,13 +499,28 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
     // chunk c*NT + tid of slice s into the stage arrays la, lb
     auto issue = [&](int s, unsigned char *la, unsigned char *lb) {
       const int k0 = kslice(s);
+      // tap-uniform gathers: the slice's tap, its bit in the masks and the
+      // byte offset of its source from tap (0, 0)'s (workgroup-uniform)
+      uint32_t tbit = 0;
+      int64_t toff = 0;
+      if constexpr (GAT) {
+        const int tap = k0 >> p.cshift, ch0 = k0 & ((1 << p.cshift) - 1);
+        int kh, kw;
+        tap_hw(tap, p, kh, kw);
+        tbit = 1u << tap;
+        const int64_t px = GA == GA_FWDT ? int64_t(kh) * p.W + kw : -(int64_t(kh) * p.Wo + kw);
+        toff = (px * (int64_t(1) << p.cshift) + ch0) * 2;
+      }
 #pragma unroll
       for (int c = 0; c < PA; ++c) {
         const int e = c * NT + tid;
         const void *src;
         if (AK) {
           const int mr = e >> 3, kc = ((e & 7) ^ (mr & 7)) * 8;
-          if constexpr (GA == GA_CAT) {
+          if constexpr (GAT) {
+            (void)mr, (void)kc;  // folded into tsrc
+            src = src16(reinterpret_cast<const void *>(uintptr_t(tsrc[c] + uint64_t(toff))), (tmask[c] & tbit) != 0);
+          } else if constexpr (GA == GA_CAT) {
             const int kk = k0 + kc, m = m0 + mr;
             const bool second = kk >= p.K1;
             const __bf16 *base = second ? p.A2 : reinterpret_cast<const __bf16 *>(A);

@@ -93,9 +93,80 @@ struct KernelTimer {
   }
 };
 
+// A second stream for work that can run beside a unit's chain of data
+// gradients (its weight gradients), ordered with the step's stream by
+// events.  Created, outside any stream capture, by the first step that may use
+// it, on the device of that step's stream; a later step whose stream is on
+// another device runs everything on its own stream.
+struct SideStream {
+  bool wanted = true;  // the net's owner allows it (net_set_side_stream)
+  hipStream_t s = nullptr;
+  hipEvent_t to_side = nullptr, to_main = nullptr, mark = nullptr;
+  int dev = -1;
+  void create(int device) {
+    hipStream_t t = nullptr;
+    hipEvent_t a = nullptr, b = nullptr, m = nullptr;
+    // the events only order the two streams' kernels on this device (each
+    // kernel's own completion already releases its writes to device scope):
+    // no timing, and a device-scope release instead of a system-scope one
+    const unsigned ef = hipEventDisableTiming | hipEventReleaseToDevice;
+    hipError_t e = hipStreamCreateWithFlags(&t, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&a, ef);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&b, ef);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&m, ef);
+    if (e != hipSuccess) {
+      if (m) (void)hipEventDestroy(m);
+      if (b) (void)hipEventDestroy(b);
+      if (a) (void)hipEventDestroy(a);
+      if (t) (void)hipStreamDestroy(t);
+      fail(CKPT_E_HIP, std::string("side stream: ") + hipGetErrorString(e));
+    }
+    s = t, to_side = a, to_main = b, mark = m, dev = device;
+  }
+  ~SideStream() {
+    if (mark) (void)hipEventDestroy(mark);
+    if (to_main) (void)hipEventDestroy(to_main);
+    if (to_side) (void)hipEventDestroy(to_side);
+    if (s) (void)hipStreamDestroy(s);
+  }
+};
+
+// Work enqueued on `after` from here on waits for all work enqueued on
+// `before` so far (an event recorded on one, waited for by the other).
+inline void order_streams(hipStream_t before, hipStream_t after, hipEvent_t e) {
+  hipError_t r = hipEventRecord(e, before);
+  if (r == hipSuccess) r = hipStreamWaitEvent(after, e, 0);
+  if (r != hipSuccess) fail(CKPT_E_HIP, std::string("stream ordering: ") + hipGetErrorString(r));
+}
+
 // Everything a unit launcher needs besides its own tensors.
 struct StepCtx {
   hipStream_t s = nullptr;
+  // the net's side stream for this step (null: everything on s) and its events
+  hipStream_t side = nullptr;
+  hipEvent_t ev_side = nullptr, ev_main = nullptr, ev_mark = nullptr;
+  // stream of weight-gradient work, and the orderings around it: to_side
+  // before side work that reads what s has written; to_main before s writes
+  // what side work still reads (and before a unit's backward ends); mark_side
+  // then main_after_mark to order s behind only the side work enqueued before
+  // the mark
+  hipStream_t ws() const { return side ? side : s; }
+  void to_side() const {
+    if (side) order_streams(s, side, ev_side);
+  }
+  void to_main() const {
+    if (side) order_streams(side, s, ev_main);
+  }
+  void mark_side() const {
+    if (!side) return;
+    const hipError_t r = hipEventRecord(ev_mark, side);
+    if (r != hipSuccess) fail(CKPT_E_HIP, std::string("stream ordering: ") + hipGetErrorString(r));
+  }
+  void main_after_mark() const {
+    if (!side) return;
+    const hipError_t r = hipStreamWaitEvent(s, ev_mark, 0);
+    if (r != hipSuccess) fail(CKPT_E_HIP, std::string("stream ordering: ") + hipGetErrorString(r));
+  }
   const float *params = nullptr;  // device, net.param_bytes
   float *grads = nullptr;         // device, net.param_bytes
   const void *input = nullptr;    // device, batch input
@@ -131,6 +202,8 @@ class Net {
   uint64_t gslot_bytes = 0;       // one gradient slot (0: the largest boundary)
   uint64_t grad_extra = 0;        // fixed gradient buffers (part of the peak)
   KernelTimer timer;              // times `timed_family` launches when enabled
+  bool uses_side = false;         // its backward can run work on a side stream
+  SideStream side;
   std::string timed_family;       // kernel-name prefix of the timed family
 
   virtual ~Net() = default;

@@ -194,6 +194,7 @@ class Bottleneck : public Net {
     grad_extra = kst;
     ks_bytes = off;
     timed_family = "k_gemm_bf16";
+    uses_side = true;
   }
 
   // bf16 mirror of parameter k (same element offset as in the f32 buffer)
@@ -252,27 +253,29 @@ class Bottleneck : public Net {
     }
   }
 
-  // dW [M, Nn] = sum over k of A(m, k) B(k, n), A = dY^T ([Kd, M] bf16), B = X ([Kd, Nn] bf16)
-  void wgrad_1x1(StepCtx &c, int M, int Nn, int64_t Kd, const void *dy, const void *x, float *dW) {
+  // dW [M, Nn] = sum over k of A(m, k) B(k, n), A = dY^T ([Kd, M] bf16), B = X ([Kd, Nn] bf16),
+  // on stream st (with its split-K partials)
+  void wgrad_1x1(StepCtx &c, hipStream_t st, int M, int Nn, int64_t Kd, const void *dy, const void *x,
+                 float *dW) {
     const int s = wsplits(M, Nn, Kd);
     GemmX gx;
     gx.splits = s;
     tbeg(c);
-    gemm_bf16x(c.s, M, Nn, int(Kd), dy, false, M, false, x, Nn, false,
+    gemm_bf16x(st, M, Nn, int(Kd), dy, false, M, false, x, Nn, false,
                s > 1 ? ksf(c, ks_wpart) : dW, Nn, GEMM_EPI_STORE, nullptr, 0, nullptr, gx);
     tend(c, M, Nn, double(Kd), 2.0 * double(Kd) * (M + Nn), 4.0 * M * Nn);
     if (s > 1) {
-      sum_partials(c.s, ksf(c, ks_wpart), s, M * Nn, dW);
+      sum_partials(st, ksf(c, ks_wpart), s, M * Nn, dW);
       c.launches += 1;
     }
   }
 
-  void wgrad_conv(StepCtx &c, const ConvGeo &g, const void *x, const void *dy, float *dW) {
+  void wgrad_conv(StepCtx &c, hipStream_t st, const ConvGeo &g, const void *x, const void *dy, float *dW) {
     const int M = g.Co, Nn = g.R * g.R * g.Ci;
     const int64_t Kd = int64_t(g.N) * g.Ho * g.Wo;
     const int s = wsplits(M, Nn, Kd);
     tbeg(c);
-    conv_bf16_wgrad(c.s, g, x, dy, ksf(c, ks_wpart), s, dW);
+    conv_bf16_wgrad(st, g, x, dy, ksf(c, ks_wpart), s, dW);
     tend(c, M, Nn, double(Kd), 2.0 * (double(g.N) * g.H * g.W * g.Ci + double(Kd) * g.Co),
          4.0 * M * Nn);
     if (s > 1) c.launches += 1;
@@ -355,7 +358,7 @@ class Bottleneck : public Net {
       bnb_backward(c.s, m, C0, dr, r, cv, st, P(c, k.g1), bnpart(c), sums, G(c, k.g1), G(c, k.b1), dc);
       im2col7(c.s, N, S, S, side, side, xv, c.ks + ks_col);
       c.launches += 5;
-      wgrad_1x1(c, C0, 147, m, dc, c.ks + ks_col, G(c, k.W1));
+      wgrad_1x1(c, c.s, C0, 147, m, dc, c.ks + ks_col, G(c, k.W1));
       return;
     }
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;
@@ -377,6 +380,11 @@ class Bottleneck : public Net {
       c1 = sv, r1 = c1 + bf(mi, k.w), c2 = r1 + bf(mi, k.w), r2 = c2 + bf(mo, k.w);
       c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
     }
+    // The weight gradients go to c.ws() (the side stream when there is one),
+    // each after a to_side that orders it behind the writes of the gradient it
+    // reads.  The write of dc1 over dc3 waits for the mark set after conv3's
+    // weight gradient, and the unit's end for all of them (the next unit's
+    // backward reuses the scratch and the split-K partials).
     char *qA = qb;                                         // dc3, then dc1
     float *qB = reinterpret_cast<float *>(qA + std::max(bf(mo, k.cout), bf(mi, k.w)));  // dr2, dr1
     char *qC = reinterpret_cast<char *>(qB) + f32(mi, k.w);  // dc2
@@ -387,8 +395,17 @@ class Bottleneck : public Net {
       bnb_backward(c.s, mo, k.cout, g, yv, cp, stp, P(c, k.gp), bnpart(c), sums, G(c, k.gp),
                    G(c, k.bp), qD);
     c.launches += k.proj ? 6 : 3;
-    // conv3 (1x1): weight and data gradients
-    wgrad_1x1(c, k.cout, k.w, mo, qA, r2, G(c, k.W3));
+    // conv3 (1x1): weight and data gradients (and the projection's weights)
+    c.to_side();
+    if (k.proj) {
+      const ConvGeo gp{N, k.hin, k.hin, k.cin, k.hout, k.hout, k.cout, 1, k.stride, 0};
+      if (k.stride == 1)
+        wgrad_1x1(c, c.ws(), k.cout, k.cin, mo, qD, xv, G(c, k.Wp));
+      else
+        wgrad_conv(c, c.ws(), gp, xv, qD, G(c, k.Wp));
+    }
+    wgrad_1x1(c, c.ws(), k.cout, k.w, mo, qA, r2, G(c, k.W3));
+    c.mark_side();
     // its epilogue masks the product by the second ReLU and adds up the second
     // BN's backward sums (partials per row tile of the GEMM)
     tbeg(c);
@@ -411,7 +428,8 @@ class Bottleneck : public Net {
     c.launches += 2;
     // conv2 (3x3, stride s)
     const ConvGeo g2{N, k.hin, k.hin, k.w, k.hout, k.hout, k.w, 3, k.stride, 1};
-    wgrad_conv(c, g2, r1, qC, G(c, k.W2));
+    c.to_side();
+    wgrad_conv(c, c.ws(), g2, r1, qC, G(c, k.W2));
     // with the first ReLU's mask and the first BN's backward sums in its epilogue
     tbeg(c);
     conv_bf16_dgrad(c.s, g2, qC, Wb(c, k.W2), qB, GEMM_EPI_BNBWD, nullptr, r1, c1, st1, bnpart(c));
@@ -421,10 +439,12 @@ class Bottleneck : public Net {
     // first BN: finalize and element pass
     bn_finalize_bwd(c.s, bnpart(c), gemm_bf16_row_blocks(int(mi), k.w), k.w, mi, sums, G(c, k.g1),
                     G(c, k.b1), false);
+    c.main_after_mark();  // dc1 overwrites dc3
     bnb_backward_apply(c.s, mi, k.w, qB, nullptr, c1, st1, P(c, k.g1), sums, qA);
     c.launches += 2;
     // conv1 (1x1)
-    wgrad_1x1(c, k.w, k.cin, mi, qA, xv, G(c, k.W1));
+    c.to_side();
+    wgrad_1x1(c, c.ws(), k.w, k.cin, mi, qA, xv, G(c, k.W1));
     if (dxv) {
       float *dx = static_cast<float *>(dxv);
       tbeg(c);
@@ -444,10 +464,6 @@ class Bottleneck : public Net {
     }
     if (k.proj) {
       const ConvGeo gp{N, k.hin, k.hin, k.cin, k.hout, k.hout, k.cout, 1, k.stride, 0};
-      if (k.stride == 1)
-        wgrad_1x1(c, k.cout, k.cin, mo, qD, xv, G(c, k.Wp));
-      else
-        wgrad_conv(c, gp, xv, qD, G(c, k.Wp));
       if (dxv) {
         float *dx = static_cast<float *>(dxv);
         tbeg(c);
@@ -460,6 +476,7 @@ class Bottleneck : public Net {
              8.0 * double(mi) * k.cin);
       }
     }
+    c.to_main();
   }
 
   void head(const void *xn, void *g, StepCtx &c) override {

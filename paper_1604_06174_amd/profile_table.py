@@ -34,7 +34,8 @@ from collections import defaultdict
 MFMA_BF16 = 2.5e15
 HBM = 8.0e12
 EPI = {0: "STORE", 1: "ADD", 3: "BF16STATS", 4: "ADDMASK", 6: "BNBWD", 7: "ROWSOFTMAX"}
-FORM = {0: "dense", 1: "fwd-gather", 2: "dgrad-gather", 3: "wgrad-gather", 4: "weights", 5: "cat"}
+FORM = {0: "dense", 1: "fwd-gather", 2: "dgrad-gather", 3: "wgrad-gather", 4: "weights", 5: "cat",
+        6: "fwd-gather", 7: "dgrad-gather"}
 
 
 def read_log(path):
@@ -52,9 +53,9 @@ def read_log(path):
 def work(r):
     """(flops, bytes) of one launch."""
     M, N, K, C = r["M"], r["N"], r["K"], r["C"]
-    if r["ga"] == 1:
+    if r["ga"] in (1, 6):
         a = (M // (r["Ho"] * r["Wo"])) * r["H"] * r["W"] * C * 2
-    elif r["ga"] == 2:
+    elif r["ga"] in (2, 7):
         a = (M // (r["H"] * r["W"])) * r["Ho"] * r["Wo"] * C * 2
     else:
         a = M * K * 2

@@ -246,11 +246,11 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   // A
   if (GA == G_DENSE) {
     check_extent(k, "A", a.A, (ba + (AK ? rows_span(M, a.lda, K) : rows_span(K, a.lda, M))) * ta);
-  } else if (GA == GA_FWD) {
+  } else if (GA == GA_FWD || GA == GA_FWDT) {
     const uint64_t pix = uint64_t(a.Ho) * a.Wo;
     if (M % pix) error(k.pretty + ": forward gather rows are not whole images");
     check_extent(k, "A (gathered input)", a.A, (M / pix) * a.H * a.W * C * 2);
-  } else if (GA == GA_DGRAD) {
+  } else if (GA == GA_DGRAD || GA == GA_DGRADT) {
     const uint64_t pix = uint64_t(a.H) * a.W;
     if (M % pix) error(k.pretty + ": data-gradient gather rows are not whole images");
     check_extent(k, "A (gathered output gradient)", a.A, (M / pix) * a.Ho * a.Wo * C * 2);
@@ -260,6 +260,11 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   } else {
     error(k.pretty + ": unknown A form");
   }
+  // the tap-uniform gathers leave out the per-chunk k bound and keep one bit per tap
+  if ((GA == GA_FWDT || GA == GA_DGRADT) &&
+      (a.cshift < 0 || (1 << a.cshift) % KS || a.K % KS || a.kper % KS || a.R * a.R > 32 || (GA == GA_DGRADT && a.S != 1) ||
+       a.nbatch > 0))
+    error(k.pretty + ": tap-uniform gather outside its conditions");
   // B
   if (GB == G_DENSE) {
     check_extent(k, "B", a.B, (BK ? rows_span(N, a.ldb, K) : rows_span(K, a.ldb, N)) * 2);
@@ -483,6 +488,23 @@ hipError_t hipEventDestroy(hipEvent_t e) {
 hipError_t hipEventSynchronize(hipEvent_t) { return hipSuccess; }
 hipError_t hipEventElapsedTime(float *ms, hipEvent_t, hipEvent_t) {
   *ms = 0.f;
+  return hipSuccess;
+}
+
+// streams and events are tokens; launches run (are checked) in issue order
+hipError_t hipEventCreateWithFlags(hipEvent_t *e, unsigned) { return hipEventCreate(e); }
+hipError_t hipEventRecord(hipEvent_t, hipStream_t) { return hipSuccess; }
+hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned int) { return hipSuccess; }
+hipError_t hipStreamCreateWithFlags(hipStream_t *s, unsigned int) {
+  *s = reinterpret_cast<hipStream_t>(new int(3));
+  return hipSuccess;
+}
+hipError_t hipStreamDestroy(hipStream_t s) {
+  delete reinterpret_cast<int *>(s);
+  return hipSuccess;
+}
+hipError_t hipStreamGetDevice(hipStream_t, hipDevice_t *d) {
+  *d = 0;
   return hipSuccess;
 }
 

@@ -470,3 +470,14 @@ def test_timing_roofline_needs_positive_peaks():
         with pytest.raises(K.CkptError) as ei:
             net.timing_roofline(pf, pb)
         assert ei.value.code == K.E_INVALID
+
+
+def test_set_side_stream_host_only():
+    # toggling allocates and launches nothing (the stream is made by a step);
+    # a null net is refused
+    from paper_1604_06174_amd.workload import net_for
+    net = net_for(dict(kind="resnet_bottleneck", stage_blocks=(1,), widths=(8,), expansion=4,
+                       stem_channels=8, image=16, batch=2, classes=7))
+    net.set_side_stream(False)
+    net.set_side_stream(True)
+    assert K._lib.net_set_side_stream(None, 1) == K.E_INVALID

@@ -127,3 +127,24 @@ def test_bottleneck_drop_bn_relu_same_bits(case):
                      *SZ.grad_layout(dd["structure"])).peak
     print(f"  sqrt-plan peak {p_s} -> {p_d} bytes", flush=True)
     assert p_d < p_s
+
+
+@pytest.mark.parametrize("case", ["p21", "wide"])
+def test_bottleneck_side_stream_same_bits(case):
+    """With the units' weight gradients on the net's second stream (the
+    default), every plan gives the single-stream step's loss and gradients
+    bit for bit (the same kernels reduce in the same order; only their
+    overlap changes).  p21 and wide hold identity, stride-1 and stride-2
+    projection blocks, and wide's weight gradients use split-K partials."""
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = dict(WELL_POSED.get(case) or CHAOTIC[case])
+    print(f"[bottleneck side stream] case={case}", flush=True)
+    d = synth.make(cfg)
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    loss_2, _, bytes_2 = _all_plans(step, d["structure"])
+    step.net.set_side_stream(False)
+    loss_1, _, bytes_1 = _all_plans(step, d["structure"])
+    step.net.set_side_stream(True)
+    loss_3, _, bytes_3 = _all_plans(step, d["structure"])
+    assert loss_1 == loss_2 == loss_3
+    assert bytes_1 == bytes_2 == bytes_3, "second-stream gradients differ from the single-stream step's"

@@ -306,7 +306,15 @@ def main():
             "tflops_algorithmic": round(tflops, 3), "hbm_gbs_algorithmic": round(gbs, 1),
             # every launch against its own bound: sum of max(flops / peak, bytes / 8 TB/s)
             # over the family's launches, over their measured time
-            "frac_of_roofline_time": round(kr["roofline_ms"] / kr["kernel_ms"], 4) if kr["kernel_ms"] > 0 else None}
+            "frac_of_roofline_time": round(kr["roofline_ms"] / kr["kernel_ms"], 4) if kr["kernel_ms"] > 0 else None,
+            # launches of the family on two streams overlap (the bottleneck net's
+            # weight gradients): the time at least one of them ran, per step, and
+            # the family's rate over that time at the same bound
+            "busy_ms_per_step": round(kr["busy_ms"] / args.steps, 3),
+            "summed_ms_per_step": round(kr["kernel_ms"] / args.steps, 3),
+            "frac_over_busy_time": round((kt["flops"] if bound == "mfma" else kt["bytes"]) /
+                                         (kr["busy_ms"] / 1e3) / (peak * (1e12 if bound == "mfma" else 1e9)), 4)
+            if kr["busy_ms"] > 0 else None}
 
     cpu = None
     sample = args.cpu_sample

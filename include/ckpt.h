@@ -507,10 +507,13 @@ int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops
  * time each would take at the bound of its own arithmetic intensity), and
  * *kernel_ms = their summed measured duration, so a family of launches with
  * different bounds gets one fraction of its roofline, roofline_ms / kernel_ms.
- * Peaks in flop/s and byte/s, both > 0 (CKPT_E_INVALID otherwise).
+ * *busy_ms = the time during which at least one of them ran (the union of
+ * their intervals on the device clock): below kernel_ms when launches on the
+ * net's side stream overlap launches on the step's stream.  Any output may be
+ * null.  Peaks in flop/s and byte/s, both > 0 (CKPT_E_INVALID otherwise).
  */
 int net_timing_roofline(ckpt_net *net, double peak_flops, double peak_bytes_per_s,
-                        double *roofline_ms, double *kernel_ms);
+                        double *roofline_ms, double *kernel_ms, double *busy_ms);
 
 /* ---- operator calls -----------------------------------------------------
  * The single operators the bf16 bottleneck units (section 5.2's deep residual

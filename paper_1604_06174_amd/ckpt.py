@@ -106,7 +106,7 @@ _sig("net_workspace_bytes", C.c_int, [C.c_void_p, C.c_void_p, _u64p])
 _sig("net_set_side_stream", C.c_int, [C.c_void_p, C.c_int32])
 _sig("net_timing_enable", C.c_int, [C.c_void_p, C.c_int32])
 _sig("net_timing_roofline", C.c_int, [C.c_void_p, C.c_double, C.c_double, C.POINTER(C.c_double),
-                                      C.POINTER(C.c_double)])
+                                      C.POINTER(C.c_double), C.POINTER(C.c_double)])
 _sig("net_timing_read", C.c_int, [C.c_void_p, _u64p, C.POINTER(C.c_double), C.POINTER(C.c_double),
                                   C.POINTER(C.c_double), C.c_char_p, C.c_int32])
 _sig("train_step", C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Batch), C.c_void_p,
@@ -410,10 +410,10 @@ class Net:
                     kernel=name.value.decode())
 
     def timing_roofline(self, peak_flops: float, peak_bytes_per_s: float) -> Dict:
-        r, k = C.c_double(), C.c_double()
+        r, k, b = C.c_double(), C.c_double(), C.c_double()
         _check(_lib.net_timing_roofline(self._h, float(peak_flops), float(peak_bytes_per_s), C.byref(r),
-                                        C.byref(k)))
-        return dict(roofline_ms=r.value, kernel_ms=k.value)
+                                        C.byref(k), C.byref(b)))
+        return dict(roofline_ms=r.value, kernel_ms=k.value, busy_ms=b.value)
 
     def __del__(self):
         if getattr(self, "_h", None) is not None and self._h.value and _lib is not None:

@@ -434,7 +434,7 @@ int net_timing_read(ckpt_net *net, uint64_t *launches, double *ms, double *flops
 }
 
 int net_timing_roofline(ckpt_net *net, double peak_flops, double peak_bytes_per_s,
-                        double *roofline_ms, double *kernel_ms) {
+                        double *roofline_ms, double *kernel_ms, double *busy_ms) {
   return ckpt::guarded([&] {
     ckpt::need(net, "net_timing_roofline");
     if (!(peak_flops > 0) || !(peak_bytes_per_s > 0))
@@ -443,6 +443,7 @@ int net_timing_roofline(ckpt_net *net, double peak_flops, double peak_bytes_per_
     const double r = t.roofline_ms(peak_flops, peak_bytes_per_s);
     if (roofline_ms) *roofline_ms = r;
     if (kernel_ms) *kernel_ms = t.ms;
+    if (busy_ms) *busy_ms = t.busy;
   });
 }
 

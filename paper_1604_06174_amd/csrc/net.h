@@ -24,6 +24,10 @@ struct KernelTimer {
   size_t used = 0;
   uint64_t launches = 0;
   double ms = 0, flops = 0, bytes = 0;
+  // time during which at least one launch of the family ran (the union of
+  // their intervals; below the summed durations when launches on two streams
+  // overlap)
+  double busy = 0;
 
   // begin arms an event pair for the next launch of the timed family (see
   // launch.h: the launch itself stamps the pair with the kernel's start and
@@ -53,11 +57,15 @@ struct KernelTimer {
     t.armed = t.taken = false;
   }
   void harvest() {
+    std::vector<std::pair<double, double>> iv;  // intervals from the first start (ms)
+    iv.reserve(used);
     for (size_t k = 0; k < used; ++k) {
-      float t = 0.f;
+      float t = 0.f, a = 0.f;
       if (hipEventSynchronize(pool[k].second) != hipSuccess ||
-          hipEventElapsedTime(&t, pool[k].first, pool[k].second) != hipSuccess)
+          hipEventElapsedTime(&t, pool[k].first, pool[k].second) != hipSuccess ||
+          hipEventElapsedTime(&a, pool[0].first, pool[k].first) != hipSuccess)
         fail(CKPT_E_HIP, "kernel timing: event query failed");
+      iv.emplace_back(double(a), double(a) + double(t));
       ms += t;
       flops += fl[k];
       bytes += by[k];
@@ -66,6 +74,17 @@ struct KernelTimer {
       lb.push_back(by[k]);
       ++launches;
     }
+    std::sort(iv.begin(), iv.end());
+    double end = -1e300;
+    for (const auto &v : iv) {
+      if (v.first >= end) {
+        busy += v.second - v.first;
+        end = v.second;
+      } else if (v.second > end) {
+        busy += v.second - end;
+        end = v.second;
+      }
+    }
     used = 0;
     fl.clear();
     by.clear();
@@ -73,7 +92,7 @@ struct KernelTimer {
   void reset() {
     harvest();
     launches = 0;
-    ms = flops = bytes = 0;
+    ms = flops = bytes = busy = 0;
     lt.clear();
     lf.clear();
     lb.clear();

@@ -465,7 +465,7 @@ def test_timing_roofline_needs_positive_peaks():
     from paper_1604_06174_amd.workload import net_for
     net = net_for(dict(kind="mlp", depth=3, width=8, batch=2))
     r = net.timing_roofline(2.5e15, 8e12)
-    assert r == dict(roofline_ms=0.0, kernel_ms=0.0)
+    assert r == dict(roofline_ms=0.0, kernel_ms=0.0, busy_ms=0.0)
     for pf, pb in ((0.0, 8e12), (2.5e15, -1.0), (float("nan"), 8e12)):
         with pytest.raises(K.CkptError) as ei:
             net.timing_roofline(pf, pb)

@@ -148,3 +148,43 @@ def test_bottleneck_side_stream_same_bits(case):
     loss_3, _, bytes_3 = _all_plans(step, d["structure"])
     assert loss_1 == loss_2 == loss_3
     assert bytes_1 == bytes_2 == bytes_3, "second-stream gradients differ from the single-stream step's"
+
+
+def test_kernel_timer_busy_time():
+    """The per-launch timer of the bf16 GEMM family (every launch stamped with
+    its own start and end): one stream, the launches never overlap, so the
+    time at least one ran equals their summed durations; with the weight
+    gradients on the side stream it is positive and at most the sum; both
+    within the steps' wall time."""
+    import torch
+    from paper_1604_06174_amd import ckpt as K
+    from paper_1604_06174_amd.workload import GpuStep
+    cfg = dict(CHAOTIC["wide"])
+    d = synth.make(cfg)
+    step = GpuStep(cfg, d["params"], d["input"], d["target"])
+    plan = step.plan(K.SQRT)
+    step.run(plan)
+    torch.cuda.synchronize()
+    out = {}
+    for side in (False, True):
+        step.net.set_side_stream(side)
+        step.net.timing_enable(True)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(3):
+            step.run(plan, want_loss=False)
+        t1.record()
+        torch.cuda.synchronize()
+        kt = step.net.timing_read()
+        r = step.net.timing_roofline(2.5e15, 8e12)
+        step.net.timing_enable(False)
+        wall = t0.elapsed_time(t1)
+        print(f"  side={side}: {kt['launches']} launches, summed {r['kernel_ms']:.3f} ms, "
+              f"busy {r['busy_ms']:.3f} ms, wall {wall:.3f} ms", flush=True)
+        assert kt["launches"] > 0 and r["kernel_ms"] > 0
+        assert 0 < r["busy_ms"] <= r["kernel_ms"] * (1 + 1e-6) + 1e-6
+        assert r["busy_ms"] <= wall * 1.01 + 0.05
+        out[side] = (kt["launches"], r)
+    assert out[False][0] == out[True][0]
+    assert abs(out[False][1]["busy_ms"] - out[False][1]["kernel_ms"]) <= 1e-3 * out[False][1]["kernel_ms"] + 1e-3
+    step.net.set_side_stream(True)

@@ -355,6 +355,73 @@ __global__ __launch_bounds__(256) void k_head_sample(int N, int HW, int C, int K
   }
 }
 
+// The same head for a wide classifier (the bf16 net: C = 2048 features,
+// K = 1000 classes) in six launches: pool, logits as an fp32 GEMM (bias
+// epilogue), softmax, the pooled gradient as an fp32 GEMM, its broadcast over
+// the pixels, the parameter gradients.
+// pooled[n][c] = (sum over p of X[n][p][c]) / HW
+__global__ __launch_bounds__(256) void k_head_pool_bf16(int N, int HW, int C, const __bf16 *__restrict__ X,
+                                                        float *__restrict__ pooled) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= N * C) return;
+  const int n = e / C, c = e % C;
+  const float inv = 1.0f / float(HW);
+  float s = 0.f;
+#pragma unroll 8
+  for (int p = 0; p < HW; ++p) s += float(X[(size_t(n) * HW + p) * C + c]);
+  pooled[e] = s * inv;
+}
+
+// per sample: max, sum of exp, loss and dlog = (softmax - onehot) / N, in
+// place over the logits (the row is read into LDS first)
+__global__ __launch_bounds__(256) void k_head_softmax(int N, int K, const int *__restrict__ labels,
+                                                      float *__restrict__ dlog, float *__restrict__ lossn) {
+  extern __shared__ float sh[];
+  float *lg = sh;       // [K]
+  float *red = sh + K;  // [256]
+  const int n = blockIdx.x, t = threadIdx.x;
+  for (int k = t; k < K; k += 256) lg[k] = dlog[size_t(n) * K + k];
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int k = t; k < K; k += 256) mx = fmaxf(mx, lg[k]);
+  red[t] = mx;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float se = 0.f;
+  for (int k = t; k < K; k += 256) se += expf(lg[k] - mx);
+  red[t] = se;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] += red[t + w];
+    __syncthreads();
+  }
+  se = red[0];
+  const int lab = labels[n];
+  const bool lab_ok = lab >= 0 && lab < K;
+  if (t == 0) lossn[n] = lab_ok ? (logf(se) + mx) - lg[lab] : NAN;
+  const float invN = 1.0f / float(N);
+  for (int k = t; k < K; k += 256) {
+    const float p = expf(lg[k] - mx) / se;
+    dlog[size_t(n) * K + k] = (p - (k == lab ? 1.f : 0.f)) * invN;
+  }
+}
+
+// G[n][p][c] = dpool[n][c] / HW at every pixel p
+__global__ __launch_bounds__(256) void k_head_bcast(int N, int HW, int C, const float *__restrict__ dpool,
+                                                    float *__restrict__ G) {
+  const int64_t tot = int64_t(N) * HW * C;
+  const float inv = 1.0f / float(HW);
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < tot; e += int64_t(gridDim.x) * 256) {
+    const int64_t n = e / (int64_t(HW) * C);
+    G[e] = dpool[n * C + e % C] * inv;
+  }
+}
+
 // dW[c][k] = sum_n pooled[n][c] dlog[n][k]; db[k] = sum_n dlog[n][k];
 // loss = sum_n lossn[n] / N  (n in order)
 __global__ __launch_bounds__(256) void k_head_params(int N, int C, int K,
@@ -692,10 +759,13 @@ void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X,
 
 void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void *X, const float *Wf,
                           const float *bf, const int *labels, float *pooled, float *dlog,
-                          float *lossn, float *G, float *dW, float *db, float *loss) {
-  const size_t lds = size_t(C + K + 256) * 4;
-  hipLaunchKernelGGL(k_head_sample<__bf16>, dim3(N), dim3(256), lds, s, N, HW, C, K,
-                     static_cast<const __bf16 *>(X), Wf, bf, labels, pooled, dlog, lossn, G);
+                          float *lossn, float *dpool, float *G, float *dW, float *db, float *loss) {
+  hipLaunchKernelGGL(k_head_pool_bf16, dim3((N * C + 255) / 256), dim3(256), 0, s, N, HW, C,
+                     static_cast<const __bf16 *>(X), pooled);
+  gemm_f32(s, N, K, C, pooled, C, false, Wf, K, false, dlog, K, GEMM_EPI_BIAS, nullptr, 0, bf);
+  hipLaunchKernelGGL(k_head_softmax, dim3(N), dim3(256), size_t(K + 256) * 4, s, N, K, labels, dlog, lossn);
+  gemm_f32(s, N, C, K, dlog, K, false, Wf, K, true, dpool, C, GEMM_EPI_STORE);
+  hipLaunchKernelGGL(k_head_bcast, dim3(ew_grid(int64_t(N) * HW * C)), dim3(256), 0, s, N, HW, C, dpool, G);
   const int tot = C * K + K + 1;
   hipLaunchKernelGGL(k_head_params, dim3((tot + 255) / 256), dim3(256), 0, s, N, C, K, pooled,
                      dlog, lossn, dW, db, loss);

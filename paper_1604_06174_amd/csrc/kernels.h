@@ -111,10 +111,11 @@ void bn_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const fl
 void pool_fc_ce_head(hipStream_t s, int N, int HW, int C, int K, const float *X, const float *Wf,
                      const float *bf, const int *labels, float *pooled, float *dlog, float *lossn,
                      float *G, float *dW, float *db, float *loss);
-// the same head over a bf16 X
+// the same head over a bf16 X, for wide classifiers: the two products on the
+// fp32 GEMM; dpool = N x C floats of workspace
 void pool_fc_ce_head_bf16(hipStream_t s, int N, int HW, int C, int K, const void *X, const float *Wf,
                           const float *bf, const int *labels, float *pooled, float *dlog,
-                          float *lossn, float *G, float *dW, float *db, float *loss);
+                          float *lossn, float *dpool, float *G, float *dW, float *db, float *loss);
 // Standalone forms for node-level graphs (NHWC fp32, J a multiple of 4):
 // st = mean | rstd of X [P, J] (part: bn_partial_blocks(P, J) * 2 * J
 // doubles); Y = gamma (X - mean) rstd + beta; the option-A shortcut Y [N, H,

@@ -55,7 +55,7 @@ class Bottleneck : public Net {
   std::vector<BUnit> u;
   int hw, hb;
   uint64_t ks_wbf = 0, ks_col = 0, ks_stats = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0,
-           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0;
+           ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0, ks_dpool = 0;
   std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics in the fixed buffers
   uint64_t wpart_floats = 0;
 
@@ -178,6 +178,7 @@ class Bottleneck : public Net {
     ks_sums = take(8ull * jmax);
     ks_wpart = take(wpart * 4);
     ks_pooled = take(4ull * N * cin);
+    ks_dpool = take(4ull * N * cin);
     ks_dlog = take(4ull * N * K);
     ks_lossn = take(4ull * N);
     ks_loss = take(4);
@@ -483,9 +484,9 @@ class Bottleneck : public Net {
     const BUnit &k = u.back();
     pool_fc_ce_head_bf16(c.s, N, k.hout * k.hout, k.cout, K, xn, P(c, hw), P(c, hb),
                          static_cast<const int *>(c.target), ksf(c, ks_pooled), ksf(c, ks_dlog),
-                         ksf(c, ks_lossn), static_cast<float *>(g), G(c, hw), G(c, hb),
-                         ksf(c, ks_loss));
-    c.launches += 2;
+                         ksf(c, ks_lossn), ksf(c, ks_dpool), static_cast<float *>(g), G(c, hw),
+                         G(c, hb), ksf(c, ks_loss));
+    c.launches += 6;
   }
 
   const float *loss_ptr(const StepCtx &c) const override {

@@ -6,6 +6,7 @@
 // reduced in a fixed order (bit-reproducible); all other arithmetic is fp32.
 #include <hip/hip_runtime.h>
 
+#include "bnb_act.h"
 #include "kernels.h"
 
 namespace ckpt {
@@ -62,7 +63,7 @@ __global__ __launch_bounds__(256) void k_bnb_apply(int64_t P, int J, const __bf1
     float c[8], v[8];
     load8(Cv + o, c);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = gamma[c0 + k] * ((c[k] - st[c0 + k]) * st[J + c0 + k]) + beta[c0 + k];
+    for (int k = 0; k < 8; ++k) v[k] = bnb_affine(c[k], st[c0 + k], st[J + c0 + k], gamma[c0 + k], beta[c0 + k]);
     if (RES == BNB_RES_ID) {
       float x[8];
       load8(X + o, x);
@@ -72,8 +73,7 @@ __global__ __launch_bounds__(256) void k_bnb_apply(int64_t P, int J, const __bf1
       float x[8];
       load8(X + o, x);
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        v[k] += gp[c0 + k] * ((x[k] - stp[c0 + k]) * stp[J + c0 + k]) + bp[c0 + k];
+      for (int k = 0; k < 8; ++k) v[k] += bnb_affine(x[k], stp[c0 + k], stp[J + c0 + k], gp[c0 + k], bp[c0 + k]);
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) v[k] = fmaxf(v[k], 0.f);

@@ -26,6 +26,11 @@ Args make_args(int M, int N, int K, const void *A, int lda, const void *B, int l
   a.Cv = static_cast<const __bf16 *>(x.cv);
   a.bst = x.bst;
   a.rstat = x.rstat;
+  a.Rb = static_cast<__bf16 *>(x.Rb);
+  a.Xr = static_cast<const __bf16 *>(x.Xr);
+  a.ast = x.act_st;
+  a.ag = x.act_g;
+  a.ab = x.act_b;
   a.kper = kper;
   return a;
 }
@@ -43,6 +48,9 @@ void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, 
       (!ak || bk || !safe || splits != 1 || ldc != N || !x.mask || !x.cv || !x.bst || !x.stats))
     fail(CKPT_E_INVALID, "gemm_bf16x: BNBWD takes k-contiguous bf16 A, n-contiguous B, one split, "
                          "ldc == N and the mask, input, statistics and partial buffers");
+  if (x.Rb && (epi != GEMM_EPI_BF16STATS || !x.act_st || !x.act_g || !x.act_b))
+    fail(CKPT_E_INVALID, "gemm_bf16x: the batch-norm apply output goes with BF16STATS and needs the "
+                         "statistics, gamma and beta");
   if (epi == GEMM_EPI_ROWSOFTMAX &&
       (!ak || !bk || !safe || splits != 1 || ldc != N || N % 4 != 0 || !bias || !x.rstat))
     fail(CKPT_E_INVALID, "gemm_bf16x: ROWSOFTMAX takes k-contiguous bf16 A and B, one split, "

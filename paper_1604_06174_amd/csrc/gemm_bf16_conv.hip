@@ -44,7 +44,10 @@ bool conv_bf16_supported(const ConvGeo &g) {
 }
 
 void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *Wt, void *Yb,
-                   double *stats) {
+                   double *stats, const GemmX *act) {
+  if (act && act->Rb && (!act->act_st || !act->act_g || !act->act_b || act->Xr))
+    fail(CKPT_E_INVALID, "conv_bf16_fwd: the batch-norm apply output needs the statistics, gamma and beta "
+                         "(no residual)");
   const int M = g.N * g.Ho * g.Wo, N = g.Co, K = g.R * g.R * g.Ci;
   Args a = conv_args(g, M, N, K, g.Ci);
   a.A = X;
@@ -53,6 +56,12 @@ void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *W
   a.ldc = N;
   a.Cb = static_cast<__bf16 *>(Yb);
   a.stats = stats;
+  if (act && act->Rb) {
+    a.Rb = static_cast<__bf16 *>(act->Rb);
+    a.ast = act->act_st;
+    a.ag = act->act_g;
+    a.ab = act->act_b;
+  }
   if (tap_uniform(a))
     pick_tile<true, true, __bf16, GA_FWDT, G_DENSE, true>(a, GEMM_EPI_BF16STATS, 1, s);
   else

@@ -54,6 +54,7 @@
 #include <type_traits>
 #include <utility>
 
+#include "bnb_act.h"
 #include "kernels.h"
 #include "launch.h"
 
@@ -95,6 +96,11 @@ struct Args {
   const __bf16 *Cv;  // BNBWD: the batch norm's input, [M, N]
   const float *bst;  // BNBWD: its mean [N] and 1/std [N]
   float *rstat;      // ROWSOFTMAX: per row and column tile, (max, sum of exp(x - max))
+  // BF16STATS with Rb: also Rb = bf16(relu(ag ((Cb - ast[n]) ast[N + n]) + ab
+  // [+ Xr])) (the bottleneck units' batch-norm apply, bnb_act.h)
+  __bf16 *Rb;
+  const __bf16 *Xr;
+  const float *ast, *ag, *ab;
   int kper;          // split-K: k per workgroup (multiple of 32)
   // gather geometry
   int H, W, Ho, Wo, R, S, P, cshift;
@@ -838,6 +844,21 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
       bs1[u] = bs2[u] = 0.0;
     }
   }
+  // BF16STATS with Rb: the batch-norm apply's parameters of the lane's VEC
+  // columns, loaded once
+  float amean[EPI == GEMM_EPI_BF16STATS ? VEC : 1], arstd[EPI == GEMM_EPI_BF16STATS ? VEC : 1];
+  float agam[EPI == GEMM_EPI_BF16STATS ? VEC : 1], abet[EPI == GEMM_EPI_BF16STATS ? VEC : 1];
+  if constexpr (EPI == GEMM_EPI_BF16STATS) {
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      const int n = n0 + wn + (lane % LPR) * VEC + u;
+      const bool in = p.Rb && n < p.N;
+      amean[u] = in ? p.ast[n] : 0.f;
+      arstd[u] = in ? p.ast[p.N + n] : 0.f;
+      agam[u] = in ? p.ag[n] : 0.f;
+      abet[u] = in ? p.ab[n] : 0.f;
+    }
+  }
   // ROWSOFTMAX: the bias of the lane's VEC columns (-inf past N), loaded once
   float rbias[EPI == GEMM_EPI_ROWSOFTMAX ? VEC : 1];
   if constexpr (EPI == GEMM_EPI_ROWSOFTMAX) {
@@ -898,14 +919,36 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
       for (int u = 0; u < VEC; ++u) v[u] = stage[rr * SP + cc + u];
       const bool full = vec_ok && n + VEC <= p.N;
       if constexpr (EPI == GEMM_EPI_BF16STATS) {
-        __bf16 *dst = p.Cb + size_t(m) * p.ldc + n;
-        if (full) {
-          bf16x8 h;
+        const size_t o = size_t(m) * p.ldc + n;
+        bf16x8 h;
 #pragma unroll
-          for (int u = 0; u < 8; ++u) h[u] = (__bf16)v[u];
-          *reinterpret_cast<bf16x8 *>(dst) = h;
+        for (int u = 0; u < 8; ++u) h[u] = (__bf16)v[u];
+        if (full) {
+          *reinterpret_cast<bf16x8 *>(p.Cb + o) = h;
         } else {
-          for (int u = 0; u < VEC && n + u < p.N; ++u) dst[u] = (__bf16)v[u];
+          for (int u = 0; u < VEC && n + u < p.N; ++u) p.Cb[o + u] = h[u];
+        }
+        if (p.Rb) {  // the batch-norm apply (+ residual) and ReLU of the rounded values
+          float x[VEC];
+          if (p.Xr && full) {
+            const bf16x8 xh = *reinterpret_cast<const bf16x8 *>(p.Xr + o);
+#pragma unroll
+            for (int u = 0; u < VEC; ++u) x[u] = float(xh[u]);
+          } else {
+#pragma unroll
+            for (int u = 0; u < VEC; ++u) x[u] = p.Xr && n + u < p.N ? float(p.Xr[o + u]) : 0.f;
+          }
+          bf16x8 r;
+#pragma unroll
+          for (int u = 0; u < VEC; ++u) {
+            float y = bnb_affine(float(h[u]), amean[u], arstd[u], agam[u], abet[u]);
+            if (p.Xr) y += x[u];
+            r[u] = (__bf16)fmaxf(y, 0.f);
+          }
+          if (full)
+            *reinterpret_cast<bf16x8 *>(p.Rb + o) = r;
+          else
+            for (int u = 0; u < VEC && n + u < p.N; ++u) p.Rb[o + u] = r[u];
         }
       } else if constexpr (EPI == GEMM_EPI_BNBWD) {
         // ds = [Ym > 0] v, stored; xhat = (Cv - mean) / std

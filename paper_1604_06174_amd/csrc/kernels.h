@@ -183,6 +183,13 @@ struct GemmX {
   const void *cv = nullptr;    // BNBWD: the batch norm's input (bf16, [M, N])
   const float *bst = nullptr;  // BNBWD: its mean [N] and 1/std [N]
   float *rstat = nullptr;      // ROWSOFTMAX: [M][column tiles][2]
+  // BF16STATS with Rb set (a bottleneck unit's re-run, its statistics known):
+  // also Rb = bf16(relu(bn(bf16 product) [+ Xr])), bn = act_g ((c - mean)
+  // rstd) + act_b with act_st = mean [N] | 1/std [N]; Xr a bf16 residual laid
+  // out as Cb, or null (the element pass's bits, see bnb_act.h)
+  void *Rb = nullptr;
+  const void *Xr = nullptr;
+  const float *act_st = nullptr, *act_g = nullptr, *act_b = nullptr;
 };
 void gemm_bf16x(hipStream_t s, int M, int N, int K, const void *A, bool a_fp32, int lda, bool ak,
                 const void *B, int ldb, bool bk, float *C, int ldc, int epi, const float *D,
@@ -228,8 +235,10 @@ bool conv_bf16_supported(const ConvGeo &g);
 // Yb = bf16(conv(X, Wt)); stats[row block][2][Co] as for BF16STATS (none when
 // stats is null)
 // (row blocks: gemm_bf16_row_blocks(N*Ho*Wo, Co)).
+// act (optional): the batch-norm apply output of the BF16STATS epilogue
+// (GemmX::Rb, act_st, act_g, act_b; no residual)
 void conv_bf16_fwd(hipStream_t s, const ConvGeo &g, const void *X, const void *Wt, void *Yb,
-                   double *stats);
+                   double *stats, const GemmX *act = nullptr);
 // DX [N, H, W, Ci] fp32 = data gradient of DY [N, Ho, Wo, Co] (bf16) through
 // Wt; epi STORE, ADD (+ D), ADDMASK (+ D where mask > 0) or BNBWD (mask, Cv,
 // bst and stats as for gemm_bf16x; stats gets gemm_bf16_row_blocks(M, Ci)

@@ -226,10 +226,12 @@ class Bottleneck : public Net {
 
   // forward 1x1 convolution (stride 1) with BN statistics, then the stats
   // (not on a re-run, which reuses the unit's kept statistics and forms no
-  // sums)
-  void fwd_1x1(StepCtx &c, int64_t m, int ci, int co, const void *x, int wk, void *out, float *st) {
+  // sums).  act (a re-run only): the epilogue also writes the BN apply's
+  // output, relu(bn(out) [+ residual]).
+  void fwd_1x1(StepCtx &c, int64_t m, int ci, int co, const void *x, int wk, void *out, float *st,
+               const GemmX *act = nullptr) {
     tbeg(c);
-    GemmX gx;
+    GemmX gx = act ? *act : GemmX{};
     gx.Cb = out;
     gx.stats = c.rerun ? nullptr : statsbuf(c);
     gemm_bf16x(c.s, int(m), co, ci, x, false, ci, true, Wb(c, wk), ci, true, nullptr, co,
@@ -241,11 +243,12 @@ class Bottleneck : public Net {
     }
   }
 
-  void fwd_conv(StepCtx &c, const ConvGeo &g, const void *x, int wk, void *out, float *st) {
+  void fwd_conv(StepCtx &c, const ConvGeo &g, const void *x, int wk, void *out, float *st,
+                const GemmX *act = nullptr) {
     const int64_t m = int64_t(g.N) * g.Ho * g.Wo;
     const double kd = double(g.R) * g.R * g.Ci;
     tbeg(c);
-    conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, c.rerun ? nullptr : statsbuf(c));
+    conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, c.rerun ? nullptr : statsbuf(c), act);
     tend(c, double(m), g.Co, kd, 2.0 * (double(g.N) * g.H * g.W * g.Ci + kd * g.Co),
          2.0 * double(m) * g.Co);
     if (!c.rerun) {
@@ -319,14 +322,35 @@ class Bottleneck : public Net {
       c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
     }
     float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
-    fwd_1x1(c, mi, k.cin, k.w, xv, k.W1, c1, st1);
-    bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
-              nullptr, nullptr, r1);
-    fwd_conv(c, ConvGeo{N, k.hin, k.hin, k.w, k.hout, k.hout, k.w, 3, k.stride, 1}, r1, k.W2, c2, st2);
-    bnb_apply(c.s, BNB_RES_NONE, mo, k.w, c2, st2, P(c, k.g2), P(c, k.b2), nullptr, nullptr,
-              nullptr, nullptr, r2);
-    fwd_1x1(c, mo, k.w, k.cout, r2, k.W3, c3, st3);
-    c.launches += 2;
+    // a re-run knows the unit's statistics: each convolution's epilogue
+    // forms its batch norm + ReLU output itself (the identity block's last
+    // one with the shortcut), so no element pass runs
+    const bool fuse = c.rerun;
+    auto act = [&](void *r, int g, int b, const float *st, const void *res) {
+      GemmX a;
+      a.Rb = r;
+      a.Xr = res;
+      a.act_st = st;
+      a.act_g = P(c, g);
+      a.act_b = P(c, b);
+      return a;
+    };
+    const GemmX a1 = act(r1, k.g1, k.b1, st1, nullptr), a2 = act(r2, k.g2, k.b2, st2, nullptr),
+                a3 = act(yv, k.g3, k.b3, st3, xv);
+    fwd_1x1(c, mi, k.cin, k.w, xv, k.W1, c1, st1, fuse ? &a1 : nullptr);
+    if (!fuse) {
+      bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
+                nullptr, nullptr, r1);
+      c.launches += 1;
+    }
+    fwd_conv(c, ConvGeo{N, k.hin, k.hin, k.w, k.hout, k.hout, k.w, 3, k.stride, 1}, r1, k.W2, c2, st2,
+             fuse ? &a2 : nullptr);
+    if (!fuse) {
+      bnb_apply(c.s, BNB_RES_NONE, mo, k.w, c2, st2, P(c, k.g2), P(c, k.b2), nullptr, nullptr,
+                nullptr, nullptr, r2);
+      c.launches += 1;
+    }
+    fwd_1x1(c, mo, k.w, k.cout, r2, k.W3, c3, st3, fuse && !k.proj ? &a3 : nullptr);
     if (k.proj) {
       if (k.stride == 1)
         fwd_1x1(c, mo, k.cin, k.cout, xv, k.Wp, cp, stp);
@@ -335,11 +359,12 @@ class Bottleneck : public Net {
                  k.Wp, cp, stp);
       bnb_apply(c.s, BNB_RES_BN, mo, k.cout, c3, st3, P(c, k.g3), P(c, k.b3), cp, stp, P(c, k.gp),
                 P(c, k.bp), yv);
-    } else {
+      c.launches += 1;
+    } else if (!fuse) {
       bnb_apply(c.s, BNB_RES_ID, mo, k.cout, c3, st3, P(c, k.g3), P(c, k.b3), xv, nullptr, nullptr,
                 nullptr, yv);
+      c.launches += 1;
     }
-    c.launches += 1;
   }
 
   void bwd(int32_t i, const void *gv, void *dxv, const void *xv, const void *yv, const void *saved,

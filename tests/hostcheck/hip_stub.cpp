@@ -277,11 +277,19 @@ void check_gemm_bf16(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid) {
   } else {
     error(k.pretty + ": unknown B form");
   }
+  if (a.Rb && EPI != ckpt::GEMM_EPI_BF16STATS) error(k.pretty + ": a batch-norm apply output without BF16STATS");
   // result and epilogue operands
   const uint64_t cz = a.nbatch > 0 ? 1 : uint64_t(grid.z);
   if (EPI == ckpt::GEMM_EPI_BF16STATS) {
     check_extent(k, "Cb", a.Cb, rows_span(M, a.ldc, N) * 2);
     if (a.stats) check_extent(k, "stats", a.stats, uint64_t(grid.y) * 2 * N * 8);
+    if (a.Rb) {  // the batch-norm apply output of a re-run
+      check_extent(k, "Rb", a.Rb, rows_span(M, a.ldc, N) * 2);
+      if (a.Xr) check_extent(k, "Xr (residual)", a.Xr, rows_span(M, a.ldc, N) * 2);
+      check_extent(k, "apply statistics", a.ast, 2 * N * 4);
+      check_extent(k, "apply gamma", a.ag, N * 4);
+      check_extent(k, "apply beta", a.ab, N * 4);
+    }
   } else {
     check_extent(k, "C", a.C, (bc + (cz - 1) * M * a.ldc + rows_span(M, a.ldc, N)) * 4);
   }

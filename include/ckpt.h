@@ -636,17 +636,23 @@ int op_bnb_backward_apply(int64_t p, int32_t j, const float *g, const void *ym, 
                           const float *st, const float *gamma, const float *sums, void *d,
                           void *stream);
 
-/* op_im2col7 -- col (bf16, [n ho wo, 147]) = the 7x7 stride-2 pad-3 patches
- * of x (bf16 [n, h, w, 3]) in (kh, kw, c) order, zero outside the image. */
-int op_im2col7(int32_t n, int32_t h, int32_t w, int32_t ho, int32_t wo, const void *x, void *col,
-               void *stream);
+/* op_im2col7 -- col (bf16, [n ho wo, kp]) = the 7x7 stride-2 pad-3 patches
+ * of x (bf16 [n, h, w, 3]) in (kh, kw, c) order in the first 147 columns of
+ * each row, zero outside the image and in the columns past 147; kp = 147 or
+ * a multiple of 8 above it (the network uses 160, rows a GEMM can load in
+ * 16-byte chunks). */
+int op_im2col7(int32_t n, int32_t h, int32_t w, int32_t ho, int32_t wo, int32_t kp, const void *x,
+               void *col, void *stream);
 
 /* op_maxpool -- 3x3 stride-2 pad-1 max pool of r (bf16 [n, h, w, c]):
  * forward (backward = 0) out = y (bf16 [n, ho, wo, c]); backward out = dr
  * (f32 [n, h, w, c]): each window's g (f32 [n, ho, wo, c]) goes to the first
- * maximum of the window in row-major order (y the forward's output). */
+ * maximum of the window in row-major order (y the forward's output).  arg
+ * (backward only, n ho wo c bytes of workspace, or null): two passes (each
+ * window's first-maximum tap, then the sum per input pixel, the network's
+ * form) instead of one; the same result. */
 int op_maxpool(int32_t backward, int32_t n, int32_t h, int32_t w, int32_t c, int32_t ho, int32_t wo,
-               const float *g, const void *r, const void *y, void *out, void *stream);
+               const float *g, const void *r, const void *y, void *out, void *arg, void *stream);
 
 /* ckpt_last_error -- message of the last failed call on this thread ("" if
  * none). */

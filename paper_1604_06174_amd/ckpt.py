@@ -149,8 +149,8 @@ _sig("op_bnb_apply", C.c_int, [C.c_int32, C.c_int64, C.c_int32, _vp, _vp, _vp, _
 _sig("op_bnb_backward", C.c_int, [C.c_int64, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                   _vp, _vp])
 _sig("op_bnb_backward_apply", C.c_int, [C.c_int64, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp])
-_sig("op_im2col7", C.c_int, [C.c_int32] * 5 + [_vp, _vp, _vp])
-_sig("op_maxpool", C.c_int, [C.c_int32] * 7 + [_vp, _vp, _vp, _vp, _vp])
+_sig("op_im2col7", C.c_int, [C.c_int32] * 6 + [_vp, _vp, _vp])
+_sig("op_maxpool", C.c_int, [C.c_int32] * 7 + [_vp, _vp, _vp, _vp, _vp, _vp])
 
 EPI_STORE, EPI_ADD, EPI_BF16STATS, EPI_ADDMASK, EPI_BNBWD = 0, 1, 3, 4, 6
 BNB_RES_NONE, BNB_RES_ID, BNB_RES_BN = 0, 1, 2
@@ -614,10 +614,10 @@ def op_bnb_backward_apply(p, j, g, ym, c, st, gamma, sums, d, stream=None):
                                       _addr(sums), _addr(d), _s(stream)))
 
 
-def op_im2col7(n, h, w, ho, wo, x, col, stream=None):
-    _check(_lib.op_im2col7(n, h, w, ho, wo, _addr(x), _addr(col), _s(stream)))
+def op_im2col7(n, h, w, ho, wo, x, col, kp=147, stream=None):
+    _check(_lib.op_im2col7(n, h, w, ho, wo, kp, _addr(x), _addr(col), _s(stream)))
 
 
-def op_maxpool(backward, n, h, w, c, ho, wo, r, out, g=None, y=None, stream=None):
+def op_maxpool(backward, n, h, w, c, ho, wo, r, out, g=None, y=None, arg=None, stream=None):
     _check(_lib.op_maxpool(int(backward), n, h, w, c, ho, wo, _addr(g), _addr(r), _addr(y), _addr(out),
-                           _s(stream)))
+                           _addr(arg), _s(stream)))

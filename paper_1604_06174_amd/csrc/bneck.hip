@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include "bnb_act.h"
+#include "common.h"
 #include "kernels.h"
 
 namespace ckpt {
@@ -214,6 +215,38 @@ __global__ __launch_bounds__(256) void k_im2col7(int N, int H, int W, int Ho, in
   }
 }
 
+// The same patches in rows of KP >= 147 elements (KP a multiple of 8), the
+// columns past 147 zero: one 16-byte chunk of a row per thread.
+__global__ __launch_bounds__(256) void k_im2col7p(int N, int H, int W, int Ho, int Wo, int KP,
+                                                  const __bf16 *__restrict__ X, __bf16 *__restrict__ col) {
+  const int CH = KP / 8;
+  const int64_t total = int64_t(N) * Ho * Wo * CH;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int j = int(e % CH);
+    const int64_t m = e / CH;
+    const int wo = int(m % Wo), ho = int((m / Wo) % Ho), n = int(m / (int64_t(Wo) * Ho));
+    bf16x8 v;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int k = j * 8 + u;
+      const int ci = k % 3, t = k / 3, kh = t / 7, kw = t % 7;
+      const int hi = 2 * ho + kh - 3, wi = 2 * wo + kw - 3;
+      v[u] = (k < 147 && hi >= 0 && hi < H && wi >= 0 && wi < W) ? X[((int64_t(n) * H + hi) * W + wi) * 3 + ci]
+                                                                : (__bf16)0.f;
+    }
+    *reinterpret_cast<bf16x8 *>(col + m * KP + j * 8) = v;
+  }
+}
+
+// dst [R, KP] bf16 = src [R, C] fp32 rounded, the columns past C zero
+__global__ __launch_bounds__(256) void k_cvt_pad_rows(int R, int C, int KP, const float *__restrict__ src,
+                                                      __bf16 *__restrict__ dst) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= R * KP) return;
+  const int r = e / KP, k = e % KP;
+  dst[e] = k < C ? (__bf16)src[r * C + k] : (__bf16)0.f;
+}
+
 // 3x3 / stride 2 / pad 1 max pool; padding never wins
 __global__ __launch_bounds__(256) void k_maxpool_fwd(int N, int H, int W, int C, int Ho, int Wo,
                                                      const __bf16 *__restrict__ R,
@@ -243,8 +276,82 @@ __global__ __launch_bounds__(256) void k_maxpool_fwd(int N, int H, int W, int C,
   }
 }
 
+// Two passes for the gradient: per window and channel, the tap of its first
+// maximum (row-major order inside the window, taps outside the image
+// skipped; the forward's output Y is the maximum), as a byte ...
+__global__ __launch_bounds__(256) void k_maxpool_arg(int N, int H, int W, int C, int Ho, int Wo,
+                                                     const __bf16 *__restrict__ R, const __bf16 *__restrict__ Y,
+                                                     unsigned char *__restrict__ arg) {
+  const int CQ = C / 8;
+  const int64_t total = int64_t(N) * Ho * Wo * CQ;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c0 = int(e % CQ) * 8;
+    const int64_t m = e / CQ;
+    const int wo = int(m % Wo), ho = int((m / Wo) % Ho), n = int(m / (int64_t(Wo) * Ho));
+    float ymax[8];
+    load8(Y + m * C + c0, ymax);
+    unsigned char a[8];
+    bool found[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      a[k] = 9;
+      found[k] = false;
+    }
+    for (int t = 0; t < 9; ++t) {
+      const int hi = 2 * ho - 1 + t / 3, wi = 2 * wo - 1 + t % 3;
+      if (hi < 0 || hi >= H || wi < 0 || wi >= W) continue;
+      float v[8];
+      load8(R + ((int64_t(n) * H + hi) * W + wi) * C + c0, v);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (!found[k] && v[k] == ymax[k]) {
+          found[k] = true;
+          a[k] = (unsigned char)t;
+        }
+    }
+    *reinterpret_cast<uint2 *>(arg + m * C + c0) =
+        make_uint2(a[0] | a[1] << 8 | a[2] << 16 | uint32_t(a[3]) << 24, a[4] | a[5] << 8 | a[6] << 16 | uint32_t(a[7]) << 24);
+  }
+}
+
+// ... then per input pixel the windows that hold it, in the order the
+// one-pass kernel below visits them: dR[n, h, w, c] = sum of G over the
+// windows whose first maximum is (h, w).
+__global__ __launch_bounds__(256) void k_maxpool_bwd2(int N, int H, int W, int C, int Ho, int Wo,
+                                                      const float *__restrict__ G,
+                                                      const unsigned char *__restrict__ arg,
+                                                      float *__restrict__ dR) {
+  const int CQ = C / 8;
+  const int64_t total = int64_t(N) * H * W * CQ;
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int c0 = int(e % CQ) * 8;
+    const int64_t m = e / CQ;
+    const int w = int(m % W), h = int((m / W) % H), n = int(m / (int64_t(W) * H));
+    float acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+    const int ho_lo = h / 2, ho_hi = min(Ho - 1, (h + 1) / 2);
+    const int wo_lo = w / 2, wo_hi = min(Wo - 1, (w + 1) / 2);
+    for (int ho = ho_lo; ho <= ho_hi; ++ho)
+      for (int wo = wo_lo; wo <= wo_hi; ++wo) {
+        if (2 * ho - 1 > h || 2 * wo - 1 > w) continue;
+        const int64_t oo = ((int64_t(n) * Ho + ho) * Wo + wo) * C + c0;
+        const uint2 ab = *reinterpret_cast<const uint2 *>(arg + oo);
+        float g[8];
+        load8f(G + oo, g);
+        const unsigned my = unsigned((h - (2 * ho - 1)) * 3 + (w - (2 * wo - 1)));
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const unsigned a = ((k < 4 ? ab.x : ab.y) >> (8 * (k & 3))) & 0xFF;
+          if (a == my) acc[k] += g[k];
+        }
+      }
+    store8f(dR + m * C + c0, acc);
+  }
+}
+
 // dR[n, h, w, c] = sum over the pooling windows whose first maximum (row-major
-// order inside the window) is (h, w) of G at that window.
+// order inside the window) is (h, w) of G at that window (one pass).
 __global__ __launch_bounds__(256) void k_maxpool_bwd(int N, int H, int W, int C, int Ho, int Wo,
                                                      const float *__restrict__ G,
                                                      const __bf16 *__restrict__ R,
@@ -347,10 +454,22 @@ void bnb_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const v
     hipLaunchKernelGGL((k_bnb_bwd_apply<false>), dim3(g), dim3(256), 0, s, P, J, G, ym, c, st, gamma, sums, d);
 }
 
-void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, const void *X, void *col) {
-  const int g = ew_grid(int64_t(N) * Ho * Wo * 147);
-  hipLaunchKernelGGL(k_im2col7, dim3(g), dim3(256), 0, s, N, H, W, Ho, Wo,
-                     static_cast<const __bf16 *>(X), static_cast<__bf16 *>(col));
+void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, int KP, const void *X, void *col) {
+  if (KP == 147) {
+    const int g = ew_grid(int64_t(N) * Ho * Wo * 147);
+    hipLaunchKernelGGL(k_im2col7, dim3(g), dim3(256), 0, s, N, H, W, Ho, Wo, static_cast<const __bf16 *>(X),
+                       static_cast<__bf16 *>(col));
+    return;
+  }
+  if (KP < 147 || KP % 8) fail(CKPT_E_INVALID, "im2col7: rows of 147, or of a multiple of 8 above it");
+  const int g = ew_grid(int64_t(N) * Ho * Wo * (KP / 8));
+  hipLaunchKernelGGL(k_im2col7p, dim3(g), dim3(256), 0, s, N, H, W, Ho, Wo, KP, static_cast<const __bf16 *>(X),
+                     static_cast<__bf16 *>(col));
+}
+
+void cvt_pad_rows(hipStream_t s, int R, int C, int KP, const float *src, void *dst) {
+  hipLaunchKernelGGL(k_cvt_pad_rows, dim3((R * KP + 255) / 256), dim3(256), 0, s, R, C, KP, src,
+                     static_cast<__bf16 *>(dst));
 }
 
 void maxpool_fwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const void *R, void *Y) {
@@ -360,10 +479,18 @@ void maxpool_fwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, cons
 }
 
 void maxpool_bwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const float *G,
-                 const void *R, const void *Y, float *dR) {
-  const int g = ew_grid(int64_t(N) * H * W * (C / 8));
-  hipLaunchKernelGGL(k_maxpool_bwd, dim3(g), dim3(256), 0, s, N, H, W, C, Ho, Wo, G,
-                     static_cast<const __bf16 *>(R), static_cast<const __bf16 *>(Y), dR);
+                 const void *R, const void *Y, float *dR, void *arg) {
+  if (!arg) {
+    const int g = ew_grid(int64_t(N) * H * W * (C / 8));
+    hipLaunchKernelGGL(k_maxpool_bwd, dim3(g), dim3(256), 0, s, N, H, W, C, Ho, Wo, G,
+                       static_cast<const __bf16 *>(R), static_cast<const __bf16 *>(Y), dR);
+    return;
+  }
+  const int ga = ew_grid(int64_t(N) * Ho * Wo * (C / 8)), gb = ew_grid(int64_t(N) * H * W * (C / 8));
+  hipLaunchKernelGGL(k_maxpool_arg, dim3(ga), dim3(256), 0, s, N, H, W, C, Ho, Wo, static_cast<const __bf16 *>(R),
+                     static_cast<const __bf16 *>(Y), static_cast<unsigned char *>(arg));
+  hipLaunchKernelGGL(k_maxpool_bwd2, dim3(gb), dim3(256), 0, s, N, H, W, C, Ho, Wo, G,
+                     static_cast<const unsigned char *>(arg), dR);
 }
 
 }  // namespace ckpt

@@ -264,20 +264,22 @@ int op_bnb_backward_apply(int64_t p, int32_t j, const float *g, const void *ym, 
   });
 }
 
-int op_im2col7(int32_t n, int32_t h, int32_t w, int32_t ho, int32_t wo, const void *x, void *col,
-               void *stream) {
+int op_im2col7(int32_t n, int32_t h, int32_t w, int32_t ho, int32_t wo, int32_t kp, const void *x,
+               void *col, void *stream) {
   return guarded_op([&] {
     need(x, "op_im2col7(x)");
     need(col, "op_im2col7(col)");
     if (n < 1 || h < 1 || w < 1 || ho != (h + 6 - 7) / 2 + 1 || wo != (w + 6 - 7) / 2 + 1)
       ckpt::fail(CKPT_E_INVALID, "op_im2col7: positive sizes, ho/wo of a 7x7 stride-2 pad-3 window");
-    ckpt::im2col7(static_cast<hipStream_t>(stream), n, h, w, ho, wo, x, col);
+    if (kp != 147 && (kp < 147 || kp % 8 != 0))
+      ckpt::fail(CKPT_E_INVALID, "op_im2col7: kp = 147 or a multiple of 8 above it");
+    ckpt::im2col7(static_cast<hipStream_t>(stream), n, h, w, ho, wo, kp, x, col);
     launched("op_im2col7");
   });
 }
 
 int op_maxpool(int32_t backward, int32_t n, int32_t h, int32_t w, int32_t c, int32_t ho, int32_t wo,
-               const float *g, const void *r, const void *y, void *out, void *stream) {
+               const float *g, const void *r, const void *y, void *out, void *arg, void *stream) {
   return guarded_op([&] {
     need(r, "op_maxpool(r)");
     need(out, "op_maxpool(out)");
@@ -289,7 +291,7 @@ int op_maxpool(int32_t backward, int32_t n, int32_t h, int32_t w, int32_t c, int
       need(g, "op_maxpool(g)");
       need(y, "op_maxpool(y)");
       ckpt::maxpool_bwd(static_cast<hipStream_t>(stream), n, h, w, c, ho, wo, g, r, y,
-                        static_cast<float *>(out));
+                        static_cast<float *>(out), arg);
     } else {
       ckpt::maxpool_fwd(static_cast<hipStream_t>(stream), n, h, w, c, ho, wo, r, out);
     }

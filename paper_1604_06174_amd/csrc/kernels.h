@@ -156,13 +156,20 @@ void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Y
 void bnb_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const void *Ym,
                         const void *Cv, const float *st, const float *gamma, const float *sums,
                         void *D);
-// col [N*Ho*Wo, 147] bf16 = 7x7 / stride 2 / pad 3 patches of X [N, H, W, 3]
-void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, const void *X, void *col);
+// col [N*Ho*Wo, KP] bf16 = 7x7 / stride 2 / pad 3 patches of X [N, H, W, 3]
+// in the first 147 columns, zero past them (KP = 147, or a multiple of 8
+// above it: 16-byte chunks, and a GEMM row pitch that takes the direct loop)
+void im2col7(hipStream_t s, int N, int H, int W, int Ho, int Wo, int KP, const void *X, void *col);
+// dst [R, KP] bf16 = src [R, C] fp32 rounded, zero past column C
+void cvt_pad_rows(hipStream_t s, int R, int C, int KP, const float *src, void *dst);
 // 3x3 / stride 2 / pad 1 max pool of R [N, H, W, C] into Y [N, Ho, Wo, C] (bf16)
 void maxpool_fwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const void *R, void *Y);
-// dR (fp32) = gradient of the max pool: each window's G goes to its first maximum
+// dR (fp32) = gradient of the max pool: each window's G goes to its first
+// maximum.  arg (N Ho Wo C bytes) or null: two passes (each window's
+// first-maximum tap, then the gather per input pixel) or one (every input
+// pixel scans the windows that hold it); the same bits.
 void maxpool_bwd(hipStream_t s, int N, int H, int W, int C, int Ho, int Wo, const float *G,
-                 const void *R, const void *Y, float *dR);
+                 const void *R, const void *Y, float *dR, void *arg);
 
 // ---- bf16 GEMM (gemm_bf16.hip, gemm_bf16_conv.hip) ----
 // C[M,N] fp32 = op(A) op(B) (+ bias | + D).  A is bf16, or fp32 rounded to

@@ -54,6 +54,10 @@ class Bottleneck : public Net {
   bool drop;  // blocks keep no relu(bn(.)) outputs
   std::vector<BUnit> u;
   int hw, hb;
+  // the stem's patch rows: 147 values padded to 160 (16-byte aligned rows, so
+  // its product takes the direct loop), its weights padded the same way
+  static constexpr int kStemK = 160;
+  uint64_t ks_w7 = 0, ks_parg = 0;
   uint64_t ks_wbf = 0, ks_col = 0, ks_stats = 0, ks_bnpart = 0, ks_sums = 0, ks_wpart = 0,
            ks_pooled = 0, ks_dlog = 0, ks_lossn = 0, ks_loss = 0, ks_dpool = 0;
   std::vector<uint64_t> kst_off;  // each unit's batch-norm statistics in the fixed buffers
@@ -172,7 +176,9 @@ class Bottleneck : public Net {
       return o;
     };
     ks_wbf = take(param_bytes / 2);
-    ks_col = take(uint64_t(N) * side * side * 147 * 2);
+    ks_col = take(uint64_t(N) * side * side * kStemK * 2);
+    ks_w7 = take(uint64_t(C0) * kStemK * 2);
+    ks_parg = take(uint64_t(N) * u[0].hout * u[0].hout * C0);
     ks_stats = take(stats);
     ks_bnpart = take(bnpart);
     ks_sums = take(8ull * jmax);
@@ -259,13 +265,14 @@ class Bottleneck : public Net {
 
   // dW [M, Nn] = sum over k of A(m, k) B(k, n), A = dY^T ([Kd, M] bf16), B = X ([Kd, Nn] bf16),
   // on stream st (with its split-K partials)
+  // (ldx: X's row pitch, Nn when 0)
   void wgrad_1x1(StepCtx &c, hipStream_t st, int M, int Nn, int64_t Kd, const void *dy, const void *x,
-                 float *dW) {
+                 float *dW, int ldx = 0) {
     const int s = wsplits(M, Nn, Kd);
     GemmX gx;
     gx.splits = s;
     tbeg(c);
-    gemm_bf16x(st, M, Nn, int(Kd), dy, false, M, false, x, Nn, false,
+    gemm_bf16x(st, M, Nn, int(Kd), dy, false, M, false, x, ldx ? ldx : Nn, false,
                s > 1 ? ksf(c, ks_wpart) : dW, Nn, GEMM_EPI_STORE, nullptr, 0, nullptr, gx);
     tend(c, M, Nn, double(Kd), 2.0 * double(Kd) * (M + Nn), 4.0 * M * Nn);
     if (s > 1) {
@@ -287,7 +294,8 @@ class Bottleneck : public Net {
 
   void begin_step(StepCtx &c) override {
     cvt_bf16(c.s, int64_t(param_bytes / 4), c.params, c.ks + ks_wbf);
-    c.launches += 1;
+    cvt_pad_rows(c.s, C0, 147, kStemK, P(c, u[0].W1), c.ks + ks_w7);
+    c.launches += 2;
   }
 
   void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
@@ -297,12 +305,12 @@ class Bottleneck : public Net {
       const int64_t m = int64_t(N) * side * side;
       char *cv = sv, *r = sv + bf(m, C0);
       float *st = kst(c, i, 0);
-      im2col7(c.s, N, S, S, side, side, xv, c.ks + ks_col);
+      im2col7(c.s, N, S, S, side, side, kStemK, xv, c.ks + ks_col);
       tbeg(c);
       GemmX gx;
       gx.Cb = cv;
       gx.stats = c.rerun ? nullptr : statsbuf(c);
-      gemm_bf16x(c.s, int(m), C0, 147, c.ks + ks_col, false, 147, true, Wb(c, k.W1), 147, true,
+      gemm_bf16x(c.s, int(m), C0, kStemK, c.ks + ks_col, false, kStemK, true, c.ks + ks_w7, kStemK, true,
                  nullptr, C0, GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
       tend(c, double(m), C0, 147, 2.0 * (double(m) * 147 + 147.0 * C0), 2.0 * double(m) * C0);
       if (!c.rerun) bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), C0), C0, m, st, false);
@@ -380,11 +388,11 @@ class Bottleneck : public Net {
       const float *st = kst(c, i, 0);
       float *dr = reinterpret_cast<float *>(qb);
       char *dc = qb + f32(m, C0);
-      maxpool_bwd(c.s, N, side, side, C0, k.hout, k.hout, g, r, yv, dr);
+      maxpool_bwd(c.s, N, side, side, C0, k.hout, k.hout, g, r, yv, dr, c.ks + ks_parg);
       bnb_backward(c.s, m, C0, dr, r, cv, st, P(c, k.g1), bnpart(c), sums, G(c, k.g1), G(c, k.b1), dc);
-      im2col7(c.s, N, S, S, side, side, xv, c.ks + ks_col);
-      c.launches += 5;
-      wgrad_1x1(c, c.s, C0, 147, m, dc, c.ks + ks_col, G(c, k.W1));
+      im2col7(c.s, N, S, S, side, side, kStemK, xv, c.ks + ks_col);
+      c.launches += 6;
+      wgrad_1x1(c, c.s, C0, 147, m, dc, c.ks + ks_col, G(c, k.W1), kStemK);
       return;
     }
     const int64_t mi = int64_t(N) * k.hin * k.hin, mo = int64_t(N) * k.hout * k.hout;

@@ -427,6 +427,8 @@ FAKE = 1 << 40  # never dereferenced: every call below fails validation first
     (lambda: K.op_maxpool(False, 1, 8, 8, 16, 5, 4, FAKE, FAKE), K.E_INVALID),
     (lambda: K.op_maxpool(True, 1, 8, 8, 16, 4, 4, FAKE, FAKE), K.E_INVALID),  # backward without g
     (lambda: K.op_im2col7(1, 8, 8, 3, 4, FAKE, FAKE), K.E_INVALID),
+    (lambda: K.op_im2col7(1, 8, 8, 4, 4, FAKE, FAKE, kp=150), K.E_INVALID),  # pitch not 147 or 8k
+    (lambda: K.op_im2col7(1, 8, 8, 4, 4, FAKE, FAKE, kp=144), K.E_INVALID),
     (lambda: K.op_bn_finalize(True, FAKE, 1, 8, 10, FAKE), K.E_INVALID),
     (lambda: K.op_sum_partials(FAKE, 0, 8, FAKE), K.E_INVALID),
 ])

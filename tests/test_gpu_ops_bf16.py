@@ -323,6 +323,12 @@ def test_stem_im2col_conv_maxpool():
     m = n * ho * ho
     col = torch.empty((m, 147), dtype=torch.bfloat16, device=DEV)
     K.op_im2col7(n, h, h, ho, ho, dbf(x), col)
+    # the network's form: rows padded to 160 (zero past 147), the product
+    # over K = 160 with the weights padded the same way
+    colp = torch.full((m, 160), float("nan"), dtype=torch.bfloat16, device=DEV)
+    K.op_im2col7(n, h, h, ho, ho, dbf(x), colp, kp=160)
+    assert torch.equal(colp[:, :147], col)
+    assert bool((colp[:, 147:] == 0).all())
     # the patch matrix times the flattened weights is the convolution
     rb, _ = K.op_gemm_bf16_blocks(m, c0)
     cv = torch.empty((m, c0), dtype=torch.bfloat16, device=DEV)
@@ -331,6 +337,12 @@ def test_stem_im2col_conv_maxpool():
                    K.EPI_BF16STATS, cb=cv, stats=stats)
     ref = U.conv2d(x.astype(np.float64), w.astype(np.float64), 2, 3)
     check_bf16("stem conv", host(cv).reshape(ref.shape), ref)
+    wp = np.zeros((c0, 160), np.float32)
+    wp[:, :147] = w.reshape(c0, 147)
+    cvp = torch.empty((m, c0), dtype=torch.bfloat16, device=DEV)
+    K.op_gemm_bf16(m, c0, 160, colp, 160, True, dbf(wp), 160, True, None, c0,
+                   K.EPI_BF16STATS, cb=cvp, stats=stats)
+    check_bf16("stem conv, padded rows", host(cvp).reshape(ref.shape), ref)
     # the pool of a post-ReLU tensor, forward and backward, exact
     r = act(rng, (n, ho, ho, c0))
     pooled = (ho + 2 - 3) // 2 + 1
@@ -343,6 +355,11 @@ def test_stem_im2col_conv_maxpool():
     dr = torch.empty((n, ho, ho, c0), dtype=torch.float32, device=DEV)
     K.op_maxpool(True, n, ho, ho, c0, pooled, pooled, rd, dr, g=df(g), y=y)
     check_f32("max pool gradient", host(dr), U.maxpool_bwd(g.astype(np.float64), arg, r.shape), 1e-6)
+    # the two-pass form (the network's): the same bits
+    dr2 = torch.empty_like(dr)
+    ws = torch.empty(n * pooled * pooled * c0, dtype=torch.uint8, device=DEV)
+    K.op_maxpool(True, n, ho, ho, c0, pooled, pooled, rd, dr2, g=df(g), y=y, arg=ws)
+    assert torch.equal(dr2, dr)
     # the stem's weight gradient: patches^T dc, split over the pixels
     dc = bf(rng.standard_normal((m, c0)) * 0.1)
     part = torch.empty(8 * c0 * 147, dtype=torch.float32, device=DEV)

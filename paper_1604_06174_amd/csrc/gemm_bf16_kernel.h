@@ -1125,9 +1125,46 @@ void launch_epi(const Args &a, int epi, int splits, hipStream_t s) {
   launch_epi_s<BM, BN, WM, WN, AK, BK, TA, GA, GB, SAFE, 0>(a, epi, splits, s);
 }
 
+// Wavefronts per workgroup (the direct loop only; the tile, and so every
+// result bit, is the same either way): with fewer workgroups than compute
+// units, a latency-bound workgroup of four wavefronts issues from one
+// wavefront per SIMD and one of eight from two, which pays once the k loop is
+// long enough to outweigh the eight-wave epilogue's extra passes.  Measured
+// per layer shape of the bottleneck ResNet and the LSTM on gfx950: eight
+// wavefronts for every 256 x 64 tile, and, when the grid has fewer than 256
+// workgroups, for 128 x 128 from 512 k per workgroup and for 64 x 64 from
+// 2048.  The
+// convolution weight gradients (few rows, a long k range per split) take 256-
+// or 128-row tiles of eight wavefronts; their split partials have no
+// row-block layout, so the tile may differ from tile_of's.
 template <bool AK, bool BK, typename TA, int GA, int GB, bool SAFE>
 void pick_tile(const Args &a, int epi, int splits, hipStream_t s) {
   const Tile t = tile_of(a.M, a.N);
+  if constexpr (SAFE && std::is_same<TA, __bf16>::value) {
+    if constexpr (GB == GB_WGRAD) {
+      if (a.M >= 256) {
+        launch_epi<256, 64, 4, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+        return;
+      }
+      if (a.M >= 128) {
+        launch_epi<128, 64, 4, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+        return;
+      }
+    }
+    if (t.BM == 256) {
+      launch_epi<256, 64, 4, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+      return;
+    }
+    const bool few = tiles_for(a.M, a.N, t.BM, t.BN) * splits < 256;
+    if (t.BM == 128 && t.BN == 128 && few && a.kper >= 512) {
+      launch_epi<128, 128, 4, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+      return;
+    }
+    if (t.BM == 64 && t.BN == 64 && few && a.kper >= 2048) {
+      launch_epi<64, 64, 4, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
+      return;
+    }
+  }
   if (t.BM == 256) launch_epi<256, 64, 4, 1, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
   else if (t.BM == 128 && t.BN == 128) launch_epi<128, 128, 2, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);
   else if (t.BM == 128) launch_epi<128, 64, 2, 2, AK, BK, TA, GA, GB, SAFE>(a, epi, splits, s);

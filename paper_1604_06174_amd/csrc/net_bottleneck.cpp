@@ -223,8 +223,13 @@ class Bottleneck : public Net {
   float *ksf(StepCtx &c, uint64_t o) const { return reinterpret_cast<float *>(c.ks + o); }
 
   // timed GEMM-family launches: 2 M N K flops; bytes = operands read once +
-  // result written once
+  // result written once (+ a re-run's batch-norm output, and the shortcut it
+  // reads, when the epilogue forms them)
   void tbeg(StepCtx &c) { timer.begin(c.s); }
+  static double act_bytes(const GemmX *act, double m, double co) {
+    if (!act || !act->Rb) return 0.0;
+    return 2.0 * m * co * (act->Xr ? 2.0 : 1.0);
+  }
   void tend(StepCtx &c, double M, double Nn, double Kd, double in_b, double out_b) {
     timer.end(c.s, 2.0 * M * Nn * Kd, in_b + out_b);
     c.launches += 1;
@@ -242,7 +247,8 @@ class Bottleneck : public Net {
     gx.stats = c.rerun ? nullptr : statsbuf(c);
     gemm_bf16x(c.s, int(m), co, ci, x, false, ci, true, Wb(c, wk), ci, true, nullptr, co,
                GEMM_EPI_BF16STATS, nullptr, 0, nullptr, gx);
-    tend(c, double(m), co, ci, 2.0 * (double(m) * ci + double(ci) * co), 2.0 * double(m) * co);
+    tend(c, double(m), co, ci, 2.0 * (double(m) * ci + double(ci) * co),
+         2.0 * double(m) * co + act_bytes(act, double(m), co));
     if (!c.rerun) {
       bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), co), co, m, st, false);
       c.launches += 1;
@@ -256,7 +262,7 @@ class Bottleneck : public Net {
     tbeg(c);
     conv_bf16_fwd(c.s, g, x, Wb(c, wk), out, c.rerun ? nullptr : statsbuf(c), act);
     tend(c, double(m), g.Co, kd, 2.0 * (double(g.N) * g.H * g.W * g.Ci + kd * g.Co),
-         2.0 * double(m) * g.Co);
+         2.0 * double(m) * g.Co + act_bytes(act, double(m), g.Co));
     if (!c.rerun) {
       bn_finalize_fwd(c.s, statsbuf(c), gemm_bf16_row_blocks(int(m), g.Co), g.Co, m, st, false);
       c.launches += 1;

@@ -44,9 +44,10 @@ def read_log(path):
         for ln in f:
             v = ln.split()
             name = v[0]
-            gx, gy, gz, M, N, K, kper, epi, ga, gb, H, W, Ho, Wo, R, S, cshift, lda = map(int, v[1:])
+            gx, gy, gz, M, N, K, kper, epi, ga, gb, H, W, Ho, Wo, R, S, cshift, lda = map(int, v[1:19])
+            rb, xr = (int(v[19]), int(v[20])) if len(v) > 20 else (0, 0)
             rows.append(dict(name=name, grid=(gx, gy, gz), M=M, N=N, K=K, epi=epi, ga=ga, gb=gb, H=H,
-                             W=W, Ho=Ho, Wo=Wo, R=R, S=S, C=(1 << cshift) if cshift > 0 else 0))
+                             W=W, Ho=Ho, Wo=Wo, R=R, S=S, C=(1 << cshift) if cshift > 0 else 0, rb=rb, xr=xr))
     return rows
 
 
@@ -65,6 +66,9 @@ def work(r):
         b = N * K * 2
     mn = M * N
     out = {3: 2 * mn, 6: 4 * mn + 2 * 2 * mn, 4: 4 * mn + 4 * mn + 2 * mn, 1: 8 * mn}.get(r["epi"], 4 * mn)
+    # a re-run's BF16STATS epilogue also writes the batch-norm output (and
+    # reads the shortcut it adds)
+    out += 2 * mn * (r.get("rb", 0) + r.get("xr", 0))
     return 2.0 * M * N * K, float(a + b + out)
 
 
@@ -102,12 +106,15 @@ def main(trace, log):
         e = kinds[k]
         e["n"] += 1
         e["r"] = r
+        fl, by = work(r)
+        e["fl"] = e.get("fl", 0.0) + fl
+        e["by"] = e.get("by", 0.0) + by
     out = []
     tot_t = tot_roof = tot_f = tot_b = 0.0
     missing = 0
     for k, e in kinds.items():
         r = e["r"]
-        fl, by = work(r)
+        fl, by = e["fl"] / e["n"], e["by"] / e["n"]  # means over the kind's launches
         ds = durs.get(k) or durs.get((prefix(k[0])[0], k[1]))
         if not ds:
             missing += e["n"]
@@ -183,6 +190,7 @@ def counters_main(log, short_log, csv_paths, fetch_factor, write_factor):
         e = full[(r["name"], r["grid"])]
         e["n"] += 1
         e["r"] = r
+        e["by"] = e.get("by", 0.0) + work(r)[1]
     n_all = n_cov = 0
     tr = alg = busy_w = dur_w = 0.0
     out = []
@@ -192,7 +200,7 @@ def counters_main(log, short_log, csv_paths, fetch_factor, write_factor):
         if not c or "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
             continue
         n_cov += e["n"]
-        fl, by = work(e["r"])
+        by = e["by"] / e["n"]  # mean over the kind's launches
         t = c["FETCH_SIZE"] * 1024 * fetch_factor + c["WRITE_SIZE"] * 1024 * write_factor
         tr += e["n"] * t
         alg += e["n"] * by

@@ -65,6 +65,25 @@ __global__ __launch_bounds__(256) void k_cvt_bf16(int64_t n, const float *__rest
     dst[e] = (__bf16)src[e];
 }
 
+// the same conversion, eight elements per thread and iteration (two 16-byte
+// loads, one 16-byte store) for n a multiple of 8 with src 16-byte and dst
+// 16-byte aligned
+__global__ __launch_bounds__(256) void k_cvt_bf16x8(int64_t n8, const float4 *__restrict__ src,
+                                                    uint4 *__restrict__ dst) {
+  for (int64_t e = blockIdx.x * int64_t(256) + threadIdx.x; e < n8; e += int64_t(gridDim.x) * 256) {
+    const float4 a = src[2 * e], b = src[2 * e + 1];
+    const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    unsigned w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const __bf16 lo = (__bf16)f[2 * k], hi = (__bf16)f[2 * k + 1];
+      w[k] = unsigned(__builtin_bit_cast(unsigned short, lo)) |
+             (unsigned(__builtin_bit_cast(unsigned short, hi)) << 16);
+    }
+    dst[e] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 // dst[r * ld + c] = bf16(src[r * C + c]) for src [R][C] fp32
 __global__ __launch_bounds__(256) void k_cvt_bf16_rows(int R, int C, const float *__restrict__ src,
                                                        __bf16 *__restrict__ dst, int ld) {
@@ -317,6 +336,11 @@ void cvt_bf16_rows(hipStream_t s, int R, int C, const float *src, void *dst, int
 }
 
 void cvt_bf16(hipStream_t s, int64_t n, const float *src, void *dst) {
+  if (n % 8 == 0 && uintptr_t(src) % 16 == 0 && uintptr_t(dst) % 16 == 0) {
+    hipLaunchKernelGGL(k_cvt_bf16x8, dim3(grid_for(n / 8)), dim3(256), 0, s, n / 8,
+                       reinterpret_cast<const float4 *>(src), static_cast<uint4 *>(dst));
+    return;
+  }
   hipLaunchKernelGGL(k_cvt_bf16, dim3(grid_for(n)), dim3(256), 0, s, n, src, static_cast<__bf16 *>(dst));
 }
 

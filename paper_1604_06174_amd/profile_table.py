@@ -46,8 +46,10 @@ def read_log(path):
             name = v[0]
             gx, gy, gz, M, N, K, kper, epi, ga, gb, H, W, Ho, Wo, R, S, cshift, lda = map(int, v[1:19])
             rb, xr = (int(v[19]), int(v[20])) if len(v) > 20 else (0, 0)
+            nbatch = int(v[21]) if len(v) > 21 else 0
             rows.append(dict(name=name, grid=(gx, gy, gz), M=M, N=N, K=K, epi=epi, ga=ga, gb=gb, H=H,
-                             W=W, Ho=Ho, Wo=Wo, R=R, S=S, C=(1 << cshift) if cshift > 0 else 0, rb=rb, xr=xr))
+                             W=W, Ho=Ho, Wo=Wo, R=R, S=S, C=(1 << cshift) if cshift > 0 else 0, rb=rb, xr=xr,
+                             nbatch=nbatch))
     return rows
 
 
@@ -69,7 +71,9 @@ def work(r):
     # a re-run's BF16STATS epilogue also writes the batch-norm output (and
     # reads the shortcut it adds)
     out += 2 * mn * (r.get("rb", 0) + r.get("xr", 0))
-    return 2.0 * M * N * K, float(a + b + out)
+    # a batch of products sharing B: A, the result and the flops once per product
+    nb = max(r.get("nbatch", 0), 1)
+    return 2.0 * M * N * K * nb, float(nb * (a + out) + b)
 
 
 def prefix(name):

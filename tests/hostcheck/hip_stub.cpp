@@ -203,18 +203,19 @@ void parse(KernelInfo &k) {
 uint64_t rows_span(uint64_t rows, uint64_t ld, uint64_t cols) { return rows ? (rows - 1) * ld + cols : 0; }
 
 // HC_GEMM_LOG=<file>: one line per bf16 GEMM launch (mangled name, grid,
-// M, N, K, k per split, epilogue, A and B forms, gather geometry, and whether
-// the epilogue also writes the batch-norm output and reads a shortcut), for
-// attaching shapes to a profiler's per-dispatch records
+// M, N, K, k per split, epilogue, A and B forms, gather geometry, whether the
+// epilogue also writes the batch-norm output and reads a shortcut, and the
+// products of a batch), for attaching shapes to a profiler's per-dispatch
+// records
 void log_gemm(const KernelInfo &k, const ckpt::gb::Args &a, dim3 grid, int epi, int ga, int gb) {
   static FILE *f = [] {
     const char *p = std::getenv("HC_GEMM_LOG");
     return p ? std::fopen(p, "w") : nullptr;
   }();
   if (!f) return;
-  std::fprintf(f, "%s %u %u %u %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d\n", k.mangled.c_str(),
+  std::fprintf(f, "%s %u %u %u %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d %d\n", k.mangled.c_str(),
                grid.x, grid.y, grid.z, a.M, a.N, a.K, a.kper, epi, ga, gb, a.H, a.W, a.Ho, a.Wo, a.R, a.S,
-               a.cshift, a.lda, a.Rb != nullptr, a.Xr != nullptr);
+               a.cshift, a.lda, a.Rb != nullptr, a.Xr != nullptr, a.nbatch);
   std::fflush(f);
 }
 

@@ -309,6 +309,8 @@ __device__ __forceinline__ void load_lds16(const void *src, unsigned char *lds_w
 // s_waitcnt immediate that waits until at most n vector-memory operations
 // of this wavefront are outstanding (the other counters left alone)
 constexpr int vmcnt_le(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+// the same, and every LDS read of the wavefront has returned
+constexpr int vmcnt_le_lds0(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70; }
 
 // f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), unrolled
 template <class F, int... I>
@@ -608,14 +610,16 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_bf16(Args p) {
     // Slice kt sits in stage kt % NS; NS - 1 slices are in flight ahead of
     // the one being multiplied.  At step kt each wavefront waits until only
     // the loads of the next NS - 2 slices are outstanding (its own share of
-    // slice kt has landed), then the barrier makes every share visible and
-    // tells that every wavefront is done with slice kt - 1, whose stage then
-    // takes slice kt + NS - 1.  (A bare s_barrier: __syncthreads' fence
-    // would wait for every load in flight.)
+    // slice kt has landed) and its LDS reads of slice kt - 1 have returned
+    // (the compiler may place the MFMAs that consume them, and so its own
+    // wait for them, after the barrier), then the barrier makes every share
+    // visible and tells that every wavefront is done with slice kt - 1, whose
+    // stage then takes slice kt + NS - 1.  (A bare s_barrier: __syncthreads'
+    // fence would wait for every load in flight.)
     unroll<NS - 1>([&](auto J) { issue(decltype(J)::value, stage_a(J), stage_b(J)); });
     auto step = [&](int kt, auto J) {
       constexpr int w = (decltype(J)::value + NS - 1) % NS;
-      __builtin_amdgcn_s_waitcnt(vmcnt_le((NS - 2) * (PA + PB)));
+      __builtin_amdgcn_s_waitcnt(vmcnt_le_lds0((NS - 2) * (PA + PB)));
       __builtin_amdgcn_s_barrier();
       issue(kt + NS - 1, stage_a(std::integral_constant<int, w>{}), stage_b(std::integral_constant<int, w>{}));
       compute(stage_a(J), stage_b(J));

@@ -32,9 +32,10 @@
 // Out-of-image taps read zero.
 //
 // Block = 4 or 8 wavefronts (256 or 512 threads) in a WM x WN grid; each wavefront owns a
-// (BM/WM) x (BN/WN) tile of 16x16 accumulators.  K advances in slices of 32
-// through double-buffered LDS, with the global loads of a slice issued two
-// slices ahead.  A k-contiguous operand is stored [row][k], so every lane
+// (BM/WM) x (BN/WN) tile of 16x16 accumulators.  K advances in slices of 64
+// (two 32-deep MFMA steps): straight from global memory into a ring of two
+// or three LDS stages (the direct loop), or through registers two slices
+// ahead into double-buffered LDS.  A k-contiguous operand is stored [row][k], so every lane
 // reads its MFMA operand (8 consecutive k of one row) as one 16-byte LDS
 // load; a k-major operand stays k-major in LDS and reaches the matrix cores
 // through gfx950's transposing LDS read.  Every output element is reduced
@@ -44,7 +45,11 @@
 // ADDMASK C = acc + (Ym > 0 ? D : 0) with Ym bf16 shaped like D;
 // BF16STATS Cb = bf16(acc) and, per workgroup row of tiles, float64 sums of
 // the rounded values and their squares per column (batch-norm statistics:
-// stats[m tile][2][N], block-major; none when stats is null).  Split-K (gridDim.z > 1): workgroup z reduces the
+// stats[m tile][2][N], block-major; none when stats is null; with Rb also the
+// batch norm + ReLU of the rounded values); BNBWD C = (Ym > 0) acc and the
+// column sums of C and C * (Cv - mean) / std (a batch norm's backward sums);
+// ROWSOFTMAX C = acc + bias and each row's (max, sum of exp) per column tile.
+// Split-K (gridDim.z > 1): workgroup z reduces the
 // k range [z*kper, (z+1)*kper) and stores its partial product to
 // C + z*M*ldc (STORE only); the partials are then added in z order.
 #pragma once

@@ -427,9 +427,8 @@ void bnb_apply(hipStream_t s, int res, int64_t P, int J, const void *Cv, const f
     hipLaunchKernelGGL((k_bnb_apply<BNB_RES_BN>), dim3(g), dim3(256), 0, s, P, J, c, st, gamma, beta, x, stp, gp, bp, y);
 }
 
-void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
-                  const float *st, const float *gamma, double *part, float *sums, float *dgamma,
-                  float *dbeta, void *D) {
+void bnb_backward_sums(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
+                       const float *st, double *part, float *sums, float *dgamma, float *dbeta) {
   const int nb = bnb_partial_blocks(P, J);
   const int pb = int((P + nb - 1) / nb);
   const __bf16 *ym = static_cast<const __bf16 *>(Ym), *c = static_cast<const __bf16 *>(Cv);
@@ -439,6 +438,12 @@ void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Y
   else
     hipLaunchKernelGGL((k_bnb_bwd_partials<false>), grid, dim3(256), 0, s, int(P), J, pb, G, ym, c, st, part);
   bn_finalize_bwd(s, part, nb, J, P, sums, dgamma, dbeta, false);
+}
+
+void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
+                  const float *st, const float *gamma, double *part, float *sums, float *dgamma,
+                  float *dbeta, void *D) {
+  bnb_backward_sums(s, P, J, G, Ym, Cv, st, part, sums, dgamma, dbeta);
   bnb_backward_apply(s, P, J, G, Ym, Cv, st, gamma, sums, D);
 }
 

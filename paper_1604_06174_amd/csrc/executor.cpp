@@ -292,6 +292,7 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
     e.recursive(p, batch.input);
   else
     e.one_level(p, batch.input);
+  c.to_main();  // the weight gradients the last backward left on the side stream
   net.end_step(c);
   if (loss_dev) {
     copy_scalar(s, net.loss_ptr(c), loss_dev);

@@ -151,6 +151,10 @@ int bnb_partial_blocks(int64_t P, int J);
 void bnb_backward(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
                   const float *st, const float *gamma, double *part, float *sums, float *dgamma,
                   float *dbeta, void *D);
+// The partial sums and finalize of bnb_backward alone (sums, dgamma, dbeta),
+// without its element pass.
+void bnb_backward_sums(hipStream_t s, int64_t P, int J, const float *G, const void *Ym, const void *Cv,
+                       const float *st, double *part, float *sums, float *dgamma, float *dbeta);
 // The element pass of bnb_backward alone, given the finalized sums (2J floats:
 // mean of ds, mean of ds * xhat); Ym may be null (G already masked).
 void bnb_backward_apply(hipStream_t s, int64_t P, int J, const float *G, const void *Ym,

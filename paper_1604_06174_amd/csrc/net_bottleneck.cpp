@@ -307,6 +307,9 @@ class Bottleneck : public Net {
   void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
     const BUnit &k = u[size_t(i)];
     char *sv = static_cast<char *>(saved);
+    // a re-run writes the arena, which weight gradients still on the side
+    // stream may read (a unit's backward does not wait for its own)
+    c.to_main();
     if (k.stem) {
       const int64_t m = int64_t(N) * side * side;
       char *cv = sv, *r = sv + bf(m, C0);
@@ -388,7 +391,12 @@ class Bottleneck : public Net {
     const char *sv = static_cast<const char *>(saved);
     char *qb = static_cast<char *>(qv);
     float *sums = ksf(c, ks_sums);
+    // The weight gradients a unit's backward leaves on the side stream read the
+    // gradient scratch and the unit's activations; the next backward waits for
+    // them just before it first writes the scratch (so its first batch norm's
+    // sums run beside them), a re-run forward at its start, the step at its end.
     if (k.stem) {  // no input gradient
+      c.to_main();
       const int64_t m = int64_t(N) * side * side;
       const char *cv = sv, *r = sv + bf(m, C0);
       const float *st = kst(c, i, 0);
@@ -405,9 +413,20 @@ class Bottleneck : public Net {
     const char *c1, *r1, *c2, *r2, *c3, *cp;
     const float *st1 = kst(c, i, 0), *st2 = kst(c, i, 1), *st3 = kst(c, i, 2), *stp = kst(c, i, 3);
     if (drop) {
+      c1 = sv, c2 = c1 + bf(mi, k.w), c3 = c2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+      r1 = r2 = nullptr;
+    } else {
+      c1 = sv, r1 = c1 + bf(mi, k.w), c2 = r1 + bf(mi, k.w), r2 = c2 + bf(mo, k.w);
+      c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
+    }
+    // third BN (input gradient: g masked by the block's final ReLU): its sums
+    // first; everything after writes the gradient scratch, so it waits for the
+    // previous unit's weight gradients
+    bnb_backward_sums(c.s, mo, k.cout, g, yv, c3, st3, bnpart(c), sums, G(c, k.g3), G(c, k.b3));
+    c.to_main();
+    if (drop) {
       // r1, r2 formed again from c1, c2 and their statistics (the forward's
       // kernel on the same bits) at the front of the gradient scratch
-      c1 = sv, c2 = c1 + bf(mi, k.w), c3 = c2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
       char *rr1 = qb, *rr2 = rr1 + bf(mi, k.w);
       bnb_apply(c.s, BNB_RES_NONE, mi, k.w, c1, st1, P(c, k.g1), P(c, k.b1), nullptr, nullptr,
                 nullptr, nullptr, rr1);
@@ -416,21 +435,17 @@ class Bottleneck : public Net {
       c.launches += 2;
       r1 = rr1, r2 = rr2;
       qb = rr2 + bf(mo, k.w);
-    } else {
-      c1 = sv, r1 = c1 + bf(mi, k.w), c2 = r1 + bf(mi, k.w), r2 = c2 + bf(mo, k.w);
-      c3 = r2 + bf(mo, k.w), cp = c3 + bf(mo, k.cout);
     }
     // The weight gradients go to c.ws() (the side stream when there is one),
     // each after a to_side that orders it behind the writes of the gradient it
     // reads.  The write of dc1 over dc3 waits for the mark set after conv3's
-    // weight gradient, and the unit's end for all of them (the next unit's
-    // backward reuses the scratch and the split-K partials).
+    // weight gradient; the next unit's backward waits for all of them before it
+    // writes the scratch (it reuses the scratch and the split-K partials).
     char *qA = qb;                                         // dc3, then dc1
     float *qB = reinterpret_cast<float *>(qA + std::max(bf(mo, k.cout), bf(mi, k.w)));  // dr2, dr1
     char *qC = reinterpret_cast<char *>(qB) + f32(mi, k.w);  // dc2
     char *qD = qC + bf(mo, k.w);                             // dcp
-    // third BN (input gradient: g masked by the block's final ReLU)
-    bnb_backward(c.s, mo, k.cout, g, yv, c3, st3, P(c, k.g3), bnpart(c), sums, G(c, k.g3), G(c, k.b3), qA);
+    bnb_backward_apply(c.s, mo, k.cout, g, yv, c3, st3, P(c, k.g3), sums, qA);
     if (k.proj)
       bnb_backward(c.s, mo, k.cout, g, yv, cp, stp, P(c, k.gp), bnpart(c), sums, G(c, k.gp),
                    G(c, k.bp), qD);
@@ -516,7 +531,6 @@ class Bottleneck : public Net {
              8.0 * double(mi) * k.cin);
       }
     }
-    c.to_main();
   }
 
   void head(const void *xn, void *g, StepCtx &c) override {

@@ -282,9 +282,11 @@ void run_train_step(Net &net, const float *params, float *grads, const ckpt_batc
       c.ev_side = net.side.to_side;
       c.ev_main = net.side.to_main;
       c.ev_mark = net.side.mark;
+      c.ev_mark2 = net.side.mark2;
     }
   }
 
+  c.recursive = p.mode == CKPT_RECURSIVE;
   Exec e{net, c, acc, ckpt, arena, {grad, grad + slot}, grad + 2 * slot};
   (void)hipGetLastError();  // clear a stale error left by the caller
   net.begin_step(c);

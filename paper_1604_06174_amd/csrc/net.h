@@ -120,11 +120,11 @@ struct KernelTimer {
 struct SideStream {
   bool wanted = true;  // the net's owner allows it (net_set_side_stream)
   hipStream_t s = nullptr;
-  hipEvent_t to_side = nullptr, to_main = nullptr, mark = nullptr;
+  hipEvent_t to_side = nullptr, to_main = nullptr, mark = nullptr, mark2 = nullptr;
   int dev = -1;
   void create(int device) {
     hipStream_t t = nullptr;
-    hipEvent_t a = nullptr, b = nullptr, m = nullptr;
+    hipEvent_t a = nullptr, b = nullptr, m = nullptr, m2 = nullptr;
     // the events only order the two streams' kernels on this device (each
     // kernel's own completion already releases its writes to device scope):
     // no timing, and a device-scope release instead of a system-scope one
@@ -133,16 +133,19 @@ struct SideStream {
     if (e == hipSuccess) e = hipEventCreateWithFlags(&a, ef);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&b, ef);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&m, ef);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&m2, ef);
     if (e != hipSuccess) {
+      if (m2) (void)hipEventDestroy(m2);
       if (m) (void)hipEventDestroy(m);
       if (b) (void)hipEventDestroy(b);
       if (a) (void)hipEventDestroy(a);
       if (t) (void)hipStreamDestroy(t);
       fail(CKPT_E_HIP, std::string("side stream: ") + hipGetErrorString(e));
     }
-    s = t, to_side = a, to_main = b, mark = m, dev = device;
+    s = t, to_side = a, to_main = b, mark = m, mark2 = m2, dev = device;
   }
   ~SideStream() {
+    if (mark2) (void)hipEventDestroy(mark2);
     if (mark) (void)hipEventDestroy(mark);
     if (to_main) (void)hipEventDestroy(to_main);
     if (to_side) (void)hipEventDestroy(to_side);
@@ -163,18 +166,36 @@ struct StepCtx {
   hipStream_t s = nullptr;
   // the net's side stream for this step (null: everything on s) and its events
   hipStream_t side = nullptr;
-  hipEvent_t ev_side = nullptr, ev_main = nullptr, ev_mark = nullptr;
+  hipEvent_t ev_side = nullptr, ev_main = nullptr, ev_mark = nullptr, ev_mark2 = nullptr;
+  bool recursive = false;          // the step runs a recursive plan
+  mutable bool side_busy = false;  // side work enqueued since the last to_main
+  mutable bool mark2_set = false;  // mark2_side recorded since the last to_main
   // stream of weight-gradient work, and the orderings around it: to_side
   // before side work that reads what s has written; to_main before s writes
-  // what side work still reads (and before a unit's backward ends); mark_side
-  // then main_after_mark to order s behind only the side work enqueued before
+  // what side work still reads; mark_side (mark2_side) then main_after_mark
+  // (main_after_mark2) to order s behind only the side work enqueued before
   // the mark
   hipStream_t ws() const { return side ? side : s; }
   void to_side() const {
-    if (side) order_streams(s, side, ev_side);
+    if (!side) return;
+    order_streams(s, side, ev_side);
+    side_busy = true;
   }
   void to_main() const {
-    if (side) order_streams(side, s, ev_main);
+    if (!side || !side_busy) return;
+    order_streams(side, s, ev_main);
+    side_busy = mark2_set = false;
+  }
+  void mark2_side() const {
+    if (!side) return;
+    const hipError_t r = hipEventRecord(ev_mark2, side);
+    if (r != hipSuccess) fail(CKPT_E_HIP, std::string("stream ordering: ") + hipGetErrorString(r));
+    mark2_set = true;
+  }
+  void main_after_mark2() const {
+    if (!side || !mark2_set) return;
+    const hipError_t r = hipStreamWaitEvent(s, ev_mark2, 0);
+    if (r != hipSuccess) fail(CKPT_E_HIP, std::string("stream ordering: ") + hipGetErrorString(r));
   }
   void mark_side() const {
     if (!side) return;

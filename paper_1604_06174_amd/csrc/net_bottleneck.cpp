@@ -307,9 +307,15 @@ class Bottleneck : public Net {
   void fwd(int32_t i, const void *xv, void *yv, void *saved, StepCtx &c) override {
     const BUnit &k = u[size_t(i)];
     char *sv = static_cast<char *>(saved);
-    // a re-run writes the arena, which weight gradients still on the side
-    // stream may read (a unit's backward does not wait for its own)
-    c.to_main();
+    // A re-run writes the arena, which the weight gradients a backward left on
+    // the side stream may read (a unit's backward does not wait for its own).
+    // Only the first unit's conv1 weight gradient may then still be running
+    // after the mark set before it: it reads the gradient scratch (which a
+    // forward writes only in the drop bn-relu layout) and the unit's input,
+    // the segment's kept boundary (which only a recursive plan rewrites
+    // during the backward), so otherwise the forward waits for the mark only.
+    if (drop || c.recursive) c.to_main();
+    else c.main_after_mark2();
     if (k.stem) {
       const int64_t m = int64_t(N) * side * side;
       char *cv = sv, *r = sv + bf(m, C0);
@@ -485,6 +491,7 @@ class Bottleneck : public Net {
     const ConvGeo g2{N, k.hin, k.hin, k.w, k.hout, k.hout, k.w, 3, k.stride, 1};
     c.to_side();
     wgrad_conv(c, c.ws(), g2, r1, qC, G(c, k.W2));
+    c.mark2_side();  // all side work but conv1's weight gradient
     // with the first ReLU's mask and the first BN's backward sums in its epilogue
     tbeg(c);
     conv_bf16_dgrad(c.s, g2, qC, Wb(c, k.W2), qB, GEMM_EPI_BNBWD, nullptr, r1, c1, st1, bnpart(c));

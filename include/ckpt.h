@@ -472,10 +472,12 @@ int train_step_graph(ckpt_net *net, const void *params, void *grads, const ckpt_
  * part of each unit's backward on a second stream of its own.  The
  * RESNET_BOTTLENECK net uses one for its units' weight gradients (Alg. 1's
  * backward of a unit: the weight-gradient products do not feed the input
- * gradient, so they run beside it), ordered with the step's stream by events
- * so that a unit's backward has ended on both streams before the next one
- * starts; other nets run everything on the step's stream.  The gradients are
- * the same bits either way.  The stream and its two events are created by the
+ * gradient, so they run beside it), ordered with the step's stream by events:
+ * each waits for the gradient it reads, and the step's stream waits for them
+ * before it next writes what they read (the next unit's gradient scratch, a
+ * re-run's activations) and at the step's end; other nets run everything on
+ * the step's stream.  The gradients are the same bits either way.  The stream
+ * and its events are created by the
  * first train_step or step_graph_create that can use them (not by a step whose
  * stream is being captured, and not by train_step_static, which allocates
  * nothing: those use the second stream only once it exists), on the device

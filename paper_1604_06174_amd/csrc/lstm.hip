@@ -178,30 +178,30 @@ __global__ __launch_bounds__(256) void k_softmax_ce_tiles(int V, const float *lo
   if (blockIdx.x == 0 && threadIdx.x == 0 && !(lab >= 0 && lab < V)) loss_rows[row] = NAN;
 }
 
-// Workgroup = 64 columns x 4 row groups (rows b = rg, rg + 4, ...); the
-// column sums of the groups are combined in order ((s0 + s1) + s2) + s3.
+// Workgroup = 32 columns x 16 row groups, so V = 10000 gives 313 workgroups,
+// more than there are compute units; group rg takes rows b = rg, rg + 16, ...,
+// issuing four row loads before it uses any, and adds them in row order.  The
+// column sums of the groups are combined as a fixed pairwise tree.
 
 // dl_bf[b][v] = bf16(dlog[b][v]);  db_o[v] (+)= sum_b dlog[b][v]
-__global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float *__restrict__ dlog,
+__global__ __launch_bounds__(512) void k_head_bwd_prep(int B, int V, const float *__restrict__ dlog,
                                                        __bf16 *__restrict__ dl_bf,
                                                        float *__restrict__ db_o, int first) {
-  __shared__ float part[4][64];
-  const int cx = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int v = blockIdx.x * 64 + cx;
+  __shared__ float part[16][32];
+  const int cx = threadIdx.x & 31, rg = threadIdx.x >> 5;
+  const int v = blockIdx.x * 32 + cx;
   float s = 0.f;
   if (v < V)
-    // rows rg, rg + 4, ... eight at a time: the eight loads are issued before
-    // any is used; the sum still runs over the rows in order
-    for (int b0 = rg; b0 < B; b0 += 32) {
-      float d[8];
+    for (int b0 = rg; b0 < B; b0 += 64) {
+      float d[4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int b = b0 + 4 * u;
+      for (int u = 0; u < 4; ++u) {
+        const int b = b0 + 16 * u;
         d[u] = b < B ? dlog[size_t(b) * V + v] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int b = b0 + 4 * u;
+      for (int u = 0; u < 4; ++u) {
+        const int b = b0 + 16 * u;
         if (b < B) {
           dl_bf[size_t(b) * V + v] = (__bf16)d[u];
           s += d[u];
@@ -211,7 +211,10 @@ __global__ __launch_bounds__(256) void k_head_bwd_prep(int B, int V, const float
   part[rg][cx] = s;
   __syncthreads();
   if (rg == 0 && v < V) {
-    const float t = ((part[0][cx] + part[1][cx]) + part[2][cx]) + part[3][cx];
+    float q[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) q[i] = part[2 * i][cx] + part[2 * i + 1][cx];
+    const float t = (((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7])));
     db_o[v] = first ? t : db_o[v] + t;
   }
 }
@@ -370,7 +373,7 @@ void softmax_ce_tiles_batched(hipStream_t s, int nunits, int rows, int V, float 
 }
 
 void head_bwd_prep(hipStream_t s, int B, int V, const float *dlog, void *dl_bf, float *db_o, bool first) {
-  hipLaunchKernelGGL(k_head_bwd_prep, dim3((V + 63) / 64), dim3(256), 0, s, B, V, dlog,
+  hipLaunchKernelGGL(k_head_bwd_prep, dim3((V + 31) / 32), dim3(512), 0, s, B, V, dlog,
                      static_cast<__bf16 *>(dl_bf), db_o, first ? 1 : 0);
 }
 
